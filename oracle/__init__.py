@@ -1,0 +1,102 @@
+"""fp64 CPU oracle for row softmax -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The HIP library never imports, links or
+calls it, and it never imports the HIP library: the two share no code.
+
+Contents
+  * ``softmax_f64``   -- the oracle proper, a plain C loop (``softmax_f64.c``)
+                         over fp64 rows: max, exp(x - max), sequential sum,
+                         divide.  That is the textbook stable softmax over the
+                         last dimension, which is what PyTorch's reference
+                         computes (the paper judges every operator against a
+                         PyTorch reference: Evaluation, Experimental Setup).
+  * ``widen_f32`` / ``widen_bf16_bits`` -- exact widening of the stored input
+                         bit patterns to fp64 (bf16 -> bits << 16 -> fp32 ->
+                         fp64), so the oracle sees exactly the values the GPU
+                         reads.
+  * ``build``         -- compiles ``softmax_f64.c`` with gcc.
+
+The oracle is pinned by tests/test_oracle.py (high-precision brute force with a
+different formula, closed forms, invariants, library routines) and
+tests/test_oracle_mutants.py (planted mistakes must fail those pins).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "softmax_f64.c")
+_LIB = os.path.join(_HERE, "liboracle_softmax.so")
+
+_lib = None
+
+
+def gcc_command(src: str, out: str) -> list:
+    """The gcc line that builds the oracle (IEEE semantics: no fast-math, no
+    contraction of a*b+c into fma)."""
+    return ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math",
+            "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror", "-o", out, src,
+            "-lm", "-lpthread"]
+
+
+def build(src: str = _SRC, out: str = _LIB) -> str:
+    """Compile the oracle's C source into a shared library; returns its path."""
+    tmp = out + ".tmp"
+    subprocess.run(gcc_command(src, tmp), check=True)
+    os.replace(tmp, out)
+    return out
+
+
+def load(path: str | None = None):
+    """Load (building first if absent) the oracle library; returns the
+    ctypes handle with ``oracle_softmax_f64`` typed."""
+    global _lib
+    if path is None:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB):
+            build()
+        path = _LIB
+    lib = ctypes.CDLL(path)
+    fn = lib.oracle_softmax_f64
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_int64, ctypes.c_int]
+    if path == _LIB:
+        _lib = lib
+    return lib
+
+
+def softmax_f64(x: np.ndarray, threads: int = 1, lib=None) -> np.ndarray:
+    """y = softmax(x, axis=-1) in fp64 for a 2-D array (any leading shape is
+    flattened to rows).  ``threads`` splits rows across host threads; the
+    result does not depend on it."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    if x.ndim == 1:
+        x = x[None, :]
+    shape = x.shape
+    x2 = x.reshape(int(np.prod(shape[:-1])), shape[-1])
+    y = np.full_like(x2, np.nan)  # rows the C code never writes stay NaN
+    lib = lib if lib is not None else load()
+    rc = lib.oracle_softmax_f64(x2.ctypes.data, y.ctypes.data, x2.shape[0],
+                                x2.shape[1], int(threads))
+    if rc != 0:
+        raise RuntimeError(f"oracle_softmax_f64 failed with status {rc}")
+    return y.reshape(shape)
+
+
+def widen_f32(x: np.ndarray) -> np.ndarray:
+    """fp32 values -> fp64, exact."""
+    return np.asarray(x, dtype=np.float32).astype(np.float64)
+
+
+def widen_bf16_bits(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16/int16) -> fp64, exact: the 16 bits are the
+    high half of an fp32 word."""
+    u = np.asarray(bits).view(np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)

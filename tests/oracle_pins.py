@@ -1,0 +1,206 @@
+"""Pins for the fp64 softmax oracle: facts fixed by mathematics, not by the
+oracle's own code.
+
+``run_pins(sm)`` applies every pin to a candidate implementation
+``sm(x, threads=1) -> y`` (fp64 2-D arrays, softmax over the last axis) and
+returns the list of failures.  The real oracle must return none
+(tests/test_oracle.py); every planted mistake must trip at least one
+(tests/test_oracle_mutants.py).
+
+Pins
+  brute_force   y_i = 1 / sum_j exp(x_j - x_i) in 50-digit mpmath: a different
+                formula (no max subtraction, no division of a sum) evaluated
+                far above fp64 precision, on tiny seeded inputs including ties,
+                bf16-representable values, large spreads and -inf entries.
+  closed_forms  hand-derived values (tests/golden/closed_forms.json).
+  invariants    rows sum to 1; exact shift invariance on a coarse grid; a
+                constant row gives exactly 1/C; a dominant entry gives exactly
+                one-hot; -inf gives exactly 0; 0 <= y <= 1; order preserved;
+                permutation equivariance; C == 1 gives 1; independence of
+                the thread count; special rows (NaN, +inf, all -inf) are NaN.
+  libraries     scipy.special.softmax and torch.softmax in fp64, both
+                independent implementations of the same definition.
+  orientation   a non-square matrix is normalised along rows, not columns.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "closed_forms.json")
+
+
+def _num(v):
+    return float(v) if not isinstance(v, str) else float(v)
+
+
+def brute_force_rows(x: np.ndarray) -> np.ndarray:
+    """softmax by y_i = 1 / sum_j exp(x_j - x_i) at 50 decimal digits."""
+    import mpmath
+    mpmath.mp.dps = 50
+    x = np.asarray(x, dtype=np.float64)
+    out = np.empty_like(x)
+    for r in range(x.shape[0]):
+        row = [mpmath.mpf(float(v)) for v in x[r]]
+        for i, xi in enumerate(row):
+            if mpmath.isinf(xi) and xi < 0:
+                out[r, i] = 0.0
+                continue
+            tot = mpmath.mpf(0)
+            for xj in row:
+                if mpmath.isinf(xj) and xj < 0:
+                    continue
+                tot += mpmath.exp(xj - xi)
+            out[r, i] = float(1 / tot)
+    return out
+
+
+def brute_force_inputs() -> list:
+    """Tiny seeded inputs: several widths and spreads, ties, values on the
+    bf16 grid, and -inf entries in rows that keep a finite maximum."""
+    rng = np.random.default_rng(20260726)
+    cases = []
+    for cols in (1, 2, 3, 7, 8, 16, 33):
+        for sigma in (1.0, 8.0, 100.0):
+            x = rng.normal(0.0, sigma, size=(4, cols))
+            if cols >= 3:
+                x[1, cols // 2] = x[1, 0]                   # tie at an interior value
+                x[2, :] = np.round(x[2, :], 0)              # many ties
+                x[3, -1] = -np.inf                          # masked entry
+            cases.append(x)
+    # values representable in bf16 (8 significant bits)
+    b = rng.normal(0.0, 4.0, size=(6, 16))
+    m, e = np.frexp(b)
+    cases.append(np.ldexp(np.round(m * 256.0) / 256.0, e))
+    return cases
+
+
+def _close(a, b, rel, abs_=0.0):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    if a.shape != b.shape:
+        return False
+    na, nb = np.isnan(a), np.isnan(b)
+    if not np.array_equal(na, nb):
+        return False
+    f = ~na
+    return bool(np.all(np.abs(a[f] - b[f]) <= rel * np.abs(b[f]) + abs_))
+
+
+def run_pins(sm) -> list:
+    fails = []
+
+    def fail(name, msg):
+        fails.append(f"{name}: {msg}")
+
+    # --- brute force -----------------------------------------------------
+    for x in brute_force_inputs():
+        try:
+            y = sm(x)
+        except Exception as e:  # a crashing candidate fails the pin
+            fail("brute_force", f"raised {e!r}")
+            break
+        v = brute_force_rows(x)
+        # fp64 error bound of exp(x - m) / s: the exponent's rounding is
+        # amplified by |x - m| (conditioning of exp), each of the C terms of
+        # the sum adds at most one rounding, and exp, the subtraction and the
+        # division add a few more.
+        with np.errstate(invalid="ignore"):
+            gap = np.abs(x - np.max(np.where(np.isneginf(x), np.nan, x), axis=1,
+                                    keepdims=True, initial=-np.inf, where=~np.isneginf(x)))
+        gap = np.where(np.isfinite(gap), gap, 0.0)
+        rel = (8.0 + 2.0 * gap + x.shape[1]) * 2.0 ** -53
+        y = np.asarray(y, dtype=np.float64)
+        ok = y.shape == v.shape and np.array_equal(np.isnan(y), np.isnan(v))
+        if ok:
+            ok = bool(np.all(np.abs(y - v) <= rel * np.abs(v) + 2.0 ** -1070))
+        if not ok:
+            d = np.abs(y - v) if y.shape == v.shape else np.array([np.nan])
+            err = float(np.max(d[np.isfinite(d)])) if np.isfinite(d).any() else float("nan")
+            fail("brute_force", f"shape {x.shape}: max abs diff {err:.3e}")
+
+    # --- closed forms ----------------------------------------------------
+    with open(GOLDEN) as f:
+        gold = json.load(f)
+    for case in gold["cases"]:
+        x = np.array([[_num(v) for v in case["x"]]])
+        want = np.array([[_num(v) for v in case["y"]]])
+        y = sm(x)
+        tol = float(case["rel_tol"])
+        ok = _close(y, want, tol) if tol > 0 else (
+            np.array_equal(np.isnan(y), np.isnan(want))
+            and np.array_equal(y[~np.isnan(y)], want[~np.isnan(want)]))
+        if not ok:
+            fail("closed_forms", f"{case['name']}: got {y.ravel().tolist()}")
+
+    rng = np.random.default_rng(7)
+    # --- invariants ------------------------------------------------------
+    x = rng.normal(0.0, 3.0, size=(16, 129))
+    y = sm(x)
+    if not np.all(np.abs(y.sum(axis=1) - 1.0) <= x.shape[1] * 2.0 ** -52):
+        fail("sum_to_one", f"max |sum-1| {np.max(np.abs(y.sum(axis=1) - 1.0)):.3e}")
+    if not (np.all(y >= 0.0) and np.all(y <= 1.0)):
+        fail("range", "y outside [0, 1]")
+    order_x = np.argsort(x, axis=1, kind="stable")
+    ys = np.take_along_axis(y, order_x, axis=1)
+    if not np.all(np.diff(ys, axis=1) >= 0.0):
+        fail("monotone", "larger x gave smaller y")
+    perm = rng.permutation(x.shape[1])
+    if not _close(sm(x[:, perm]), y[:, perm], 1e-15, 1e-300):
+        fail("permutation", "column permutation changed the result")
+    # exact shift invariance on a grid where x + c and x - max are exact
+    xq = np.round(rng.normal(0.0, 5.0, size=(8, 64)) * 2.0 ** 16) / 2.0 ** 16
+    yq = sm(xq)
+    for c in (-3.0, 0.5, 1024.0):
+        if not np.array_equal(sm(xq + c), yq):
+            fail("shift", f"x + {c} changed the result")
+    for cols in (1, 5, 64, 1000):
+        yc = sm(np.full((2, cols), -2.75))
+        if not np.all(yc == 1.0 / cols):
+            fail("constant_row", f"cols={cols}")
+    xd = np.full((3, 40), -1000.0)
+    xd[np.arange(3), [0, 17, 39]] = 0.0
+    yd = sm(xd)
+    want = np.zeros_like(xd)
+    want[np.arange(3), [0, 17, 39]] = 1.0
+    if not np.array_equal(yd, want):
+        fail("one_hot", "dominant entry is not exactly one-hot")
+    xm = rng.normal(0.0, 1.0, size=(4, 32))
+    xm[:, 5::3] = -np.inf
+    ym = sm(xm)
+    if not np.all(ym[:, 5::3] == 0.0) or not np.all(ym[:, :5] > 0.0):
+        fail("masked", "-inf entries are not exactly 0")
+    if not np.all(sm(rng.normal(0.0, 50.0, size=(5, 1))) == 1.0):
+        fail("one_column", "C == 1 did not give 1")
+    xs = np.array([[np.nan, 1.0, 2.0], [np.inf, 1.0, 2.0], [-np.inf] * 3, [0.0, 1.0, 2.0]])
+    ys_ = sm(xs)
+    if not (np.all(np.isnan(ys_[:3])) and not np.any(np.isnan(ys_[3]))):
+        fail("special_rows", f"got {ys_.tolist()}")
+    xt = rng.normal(0.0, 2.0, size=(37, 50))
+    y1 = sm(xt, threads=1)
+    for th in (2, 3, 8):
+        if not np.array_equal(sm(xt, threads=th), y1):
+            fail("threads", f"threads={th} differs from threads=1")
+
+    # --- independent library implementations ----------------------------
+    import scipy.special
+    import torch
+    xl = rng.normal(0.0, 4.0, size=(32, 300))
+    yl = sm(xl)
+    # The libraries sum in other orders and use other exp kernels: agreement
+    # to 1e-14 relative (about 45 fp64 ulps) is what rounding allows here.
+    if not _close(yl, scipy.special.softmax(xl, axis=-1), 1e-14):
+        fail("scipy", "differs from scipy.special.softmax by > 1e-14 relative")
+    yt = torch.softmax(torch.from_numpy(xl), dim=-1).numpy()
+    if not _close(yl, yt, 1e-14):
+        fail("torch", "differs from torch.softmax(float64) by > 1e-14 relative")
+
+    # --- orientation -------------------------------------------------------
+    xo = rng.normal(0.0, 1.0, size=(3, 11))
+    yo = sm(xo)
+    if not np.allclose(yo.sum(axis=1), 1.0, rtol=0, atol=1e-14):
+        fail("orientation", "rows of a 3 x 11 input do not sum to 1")
+    return fails
