@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Row-softmax benchmark on one MI355X.
+
+One step is one pass of the whole hot path over one batch of each row-length
+regime, in this order (inputs resident in HBM before timing starts):
+
+  small_262144x64    bf16 -> bf16   small-row kernel
+  causal_32768x4096  bf16 -> bf16   medium-row kernel
+  large_1024x262144  f32  -> f32    large-row kernel
+  vocab_4096x151936  bf16 -> f32    launcher's choice for 151936-wide rows
+
+Between two visits of the same input the other three move more than 3 GB, far
+more than the 256 MB memory-side cache plus L2, so every launch reads x from
+HBM.  Each launch is bracketed by HIP events recorded on the stream it runs
+on; ``value`` is the step's algorithmic bytes (x read once + y written once,
+summed over the regimes) divided by the measured step time.
+
+Prints ONE JSON line (rank 0).  ``--gpus`` above 1 is refused: this path runs
+on one GPU (rows shard across GPUs without communication).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "row-softmax achieved HBM GB/s and % of MI355X peak, per row-length regime"
+PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_SOURCES = ["rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
+                  "rowsm.hip"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_23089_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(regime: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    try:
+        with open(PROFILE_COUNTERS) as f:
+            prof = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if prof.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    ent = prof.get("regimes", {}).get(regime)
+    return None if ent is None else ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
+    """Time the fp64 oracle on the host cores over every row of the step (row
+    chunks bounded in memory), repeating passes until ``min_seconds`` of
+    oracle time has accumulated, and check evenly spaced GPU rows against it
+    on the way."""
+    import numpy as np
+
+    import oracle
+    from oracle.compare import compare, widen_output
+    from paper_2607_23089_amd import workloads as W
+
+    threads = len(os.sched_getaffinity(0))
+    oracle.load()
+    chunk_elems = 1 << 25
+    tot_bytes, tot_time, passes = 0, 0.0, 0
+    parity = {}
+    widened = {}  # host fp64 copies of the inputs, kept for repeated passes
+    while passes == 0 or tot_time < min_seconds:
+        for name in regimes:
+            w = W.WORKLOADS[name]
+            step_rows = max(1, chunk_elems // w.cols)
+            for r0 in range(0, w.rows, step_rows):
+                v = widened.get((name, r0))
+                if v is None:
+                    xs = W.to_bits_numpy(inputs[name][r0:r0 + step_rows])
+                    v = (oracle.widen_bf16_bits(xs) if w.in_dtype == "bf16"
+                         else oracle.widen_f32(xs))
+                    widened[(name, r0)] = v
+                t = time.perf_counter()
+                ref = oracle.softmax_f64(v, threads=threads)
+                tot_time += time.perf_counter() - t
+                tot_bytes += v.size * (w.in_bytes + w.out_bytes)
+                if passes == 0:
+                    # parity on every 16th row of the chunk
+                    got = widen_output(W.to_bits_numpy(outputs[name][r0:r0 + step_rows:16]),
+                                       w.out_dtype)
+                    res = compare(got, ref[::16], w.out_dtype)
+                    p = parity.setdefault(name, {"rows_checked": 0, "parity_ok": True,
+                                                 "max_abs": 0.0, "max_tol_ratio": 0.0})
+                    p["rows_checked"] += int(got.shape[0])
+                    p["parity_ok"] &= bool(res["ok"])
+                    p["max_abs"] = max(p["max_abs"], res["max_abs"])
+                    p["max_tol_ratio"] = max(p["max_tol_ratio"], res["max_tol_ratio"])
+        passes += 1
+    return {
+        "value": tot_bytes / tot_time / 1e9,
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"every row of the step ({', '.join(regimes)}), {passes} pass(es), "
+                   f"{tot_time:.1f} s of oracle time; widening and copies not timed"),
+        "seconds": tot_time,
+        "parity_on_sample": parity,
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--regimes", default=None,
+                    help="comma-separated subset of the regimes (default: all four)")
+    ap.add_argument("--cpu-budget", type=float, default=10.0,
+                    help="minimum seconds of oracle time for the CPU baseline (0 = skip)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this row-softmax path runs on one GPU; rows shard across "
+              "GPUs with no communication, so no multi-GPU run is made (use --gpus 1).",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    R.lib()  # fails loudly when the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    regimes = list(W.REGIMES if not args.regimes else args.regimes.split(","))
+
+    inputs, outputs, calls = {}, {}, []
+    stream = torch.cuda.current_stream(dev)
+    for name in regimes:
+        w = W.WORKLOADS[name]
+        x = W.make_input(w, device=dev)
+        y = torch.empty(w.rows, w.cols, dtype=W.TORCH_DTYPES[w.out_dtype], device=dev)
+        inputs[name], outputs[name] = x, y
+        calls.append((name, w, x.data_ptr(), y.data_ptr(), R.dtype_code(x.dtype),
+                      R.dtype_code(y.dtype)))
+    torch.cuda.synchronize()
+    sh = stream.cuda_stream
+
+    def step(events=None):
+        for i, (name, w, xp, yp, di, do) in enumerate(calls):
+            if events is not None:
+                events[i][0].record(stream)
+            st = R.rowsm_forward(xp, yp, w.rows, w.cols, di, do, sh)
+            if st != R.OK:
+                raise R.RowsmError(f"{name}: status {st} {R.rowsm_status_string(st)}")
+            if events is not None:
+                events[i][1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in calls]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    step_bytes = sum(W.WORKLOADS[n].algorithmic_bytes for n in regimes)
+    ms_per_step = wall / args.steps * 1e3
+    per = {}
+    for i, (name, w, *_r) in enumerate(calls):
+        ms = [evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(args.steps)]
+        ms.sort()
+        avg = sum(ms) / len(ms)
+        gbs = w.algorithmic_bytes / (avg * 1e-3) / 1e9
+        st, desc = R.rowsm_describe(w.rows, w.cols, R.dtype_code(W.TORCH_DTYPES[w.in_dtype]),
+                                    R.dtype_code(W.TORCH_DTYPES[w.out_dtype]))
+        per[name] = {
+            "kernel": desc.split(" ")[0], "launch": desc,
+            "algorithmic_bytes": w.algorithmic_bytes,
+            "avg_us": avg * 1e3, "median_us": ms[len(ms) // 2] * 1e3,
+            "min_us": ms[0] * 1e3,
+            "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
+            "hbm_bytes_per_launch": measured_traffic(name),
+        }
+    dom = max(per, key=lambda n: per[n]["avg_us"])
+    d = per[dom]
+    value = step_bytes / (wall / args.steps) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded, generated on the GPU)",
+        "config": {
+            "workload": "row softmax over the row-length regimes, one launch each per step: "
+                        + ", ".join(f"{n} {W.WORKLOADS[n].in_dtype}->{W.WORKLOADS[n].out_dtype}"
+                                    for n in regimes),
+            "algorithmic_bytes_per_step": step_bytes,
+            "regimes": {n: {"GBps": round(v["GBps"], 1),
+                            "frac_of_peak": round(v["frac_of_peak"], 4),
+                            "avg_us": round(v["avg_us"], 2), "kernel": v["kernel"]}
+                        for n, v in per.items()},
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": f"{d['kernel']} ({dom})",
+            "achieved": d["GBps"],
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": d["GBps"] / PEAK_HBM_GBS,
+            "traffic": d["hbm_bytes_per_launch"],
+            "algorithmic_bytes_per_launch": d["algorithmic_bytes"],
+            "avg_launch_us": d["avg_us"],
+        },
+        "regimes_detail": per,
+    }
+    if args.cpu_budget > 0:
+        result["cpu_baseline"] = cpu_baseline(inputs, outputs, regimes, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,148 @@
+/*
+ * rowsm.h -- C ABI of the MI355X (gfx950) row-softmax library.
+ *
+ * The operation is the numerically stable softmax over the last dimension of a
+ * row-major matrix:
+ *
+ *     y[r, j] = exp(x[r, j] - m_r) / sum_k exp(x[r, k] - m_r),  m_r = max_k x[r, k]
+ *
+ * The paper names this hot path only through its running-example listing
+ * style, which declares a row-length-specialised reduction with small-, medium-
+ * and large-row kernels, a row-count launcher and a BLOCK_ROWS tile parameter
+ * (preamble listing style for the running example); its benchmark operators
+ * are all checked against a PyTorch reference (Evaluation, Experimental
+ * Setup), whose softmax over dim -1 is the formula above.  The kernels and the
+ * dispatcher behind this header are this library's own gfx950 design.
+ *
+ * Conventions shared by every entry point
+ *   - x and y are DEVICE pointers owned by the caller; the library never frees
+ *     or retains them.  Layout: row-major, contiguous, row stride == cols
+ *     elements.  x is only read.  y may equal x (in place) when in_dtype ==
+ *     out_dtype; any other overlap of the two ranges is rejected.
+ *   - dtypes: ROWSM_F32 (IEEE binary32) or ROWSM_BF16 (bfloat16, stored as
+ *     its 16-bit pattern).  Every pair {f32, bf16} x {f32, bf16} is supported.
+ *     Arithmetic is fp32: bf16 inputs widen exactly, bf16 outputs are rounded
+ *     to nearest even.
+ *   - stream is a hipStream_t (NULL = the legacy default stream).  The call
+ *     only enqueues work; results are visible once the caller synchronises the
+ *     stream.  Nothing is allocated per call.
+ *   - Errors are reported through the return value only (a rowsm_status);
+ *     the library never aborts, prints or throws.  Argument errors are found
+ *     on the host before any HIP call.  A failed launch maps to ROWSM_EHIP.
+ *   - Special values follow IEEE arithmetic of the formula: a row holding a
+ *     NaN or +inf, or only -inf, is all NaN; a -inf entry in a row with a
+ *     finite maximum gives exactly +0.
+ *   - Limits: rows * cols < 2^62 and cols < 2^30 (every byte offset inside a
+ *     row fits 32 bits); larger sizes return ROWSM_EINVAL.
+ */
+#ifndef ROWSM_H
+#define ROWSM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { ROWSM_F32 = 0, ROWSM_BF16 = 1 } rowsm_dtype;
+
+typedef enum {
+    ROWSM_OK = 0,
+    ROWSM_EINVAL = -1, /* bad size, NULL pointer, bad overlap, bad variant  */
+    ROWSM_EDTYPE = -2, /* dtype code outside rowsm_dtype                    */
+    ROWSM_EHIP = -3    /* the HIP runtime reported an error for the launch  */
+} rowsm_status;
+
+/* Kernel families.  SMALL packs several rows into one 64-lane wavefront;
+ * MEDIUM gives each row one workgroup (or one wavefront) and keeps the row in
+ * registers; LARGE streams a row through tiles twice (statistics pass with an
+ * online max/sum merge, then a normalize pass). */
+typedef enum {
+    ROWSM_AUTO = 0,
+    ROWSM_SMALL = 1,
+    ROWSM_MEDIUM = 2,
+    ROWSM_LARGE = 3
+} rowsm_variant;
+
+/*
+ * rowsm_forward: y = softmax(x, dim=-1) for a rows x cols matrix.
+ *   x         device pointer, rows*cols elements of in_dtype
+ *   y         device pointer, rows*cols elements of out_dtype
+ *   rows      >= 0; rows == 0 or cols == 0 is a no-op returning ROWSM_OK
+ *   cols      >= 0
+ *   in_dtype  rowsm_dtype of x;  out_dtype rowsm_dtype of y
+ *   stream    hipStream_t the kernel is enqueued on
+ * Returns ROWSM_OK or a negative rowsm_status.  The kernel family is chosen
+ * by rowsm_select.
+ */
+int rowsm_forward(const void *x, void *y, int64_t rows, int64_t cols,
+                  int in_dtype, int out_dtype, void *stream);
+
+/*
+ * rowsm_select: the kernel family rowsm_forward uses for this shape and dtype
+ * pair (the row-count and row-length launcher).  Pure host function, no HIP
+ * call.  Returns a rowsm_variant > 0, or a negative rowsm_status for invalid
+ * arguments.
+ */
+int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dtype);
+
+/*
+ * rowsm_forward_variant: rowsm_forward with the kernel family forced
+ * (ROWSM_AUTO behaves like rowsm_forward).  Used by tests and benchmarks to
+ * check every family on every shape it supports.  A family that cannot run
+ * this shape (SMALL or MEDIUM with a row too long for registers) returns
+ * ROWSM_EINVAL without launching.
+ */
+int rowsm_forward_variant(const void *x, void *y, int64_t rows, int64_t cols,
+                          int in_dtype, int out_dtype, void *stream,
+                          int variant);
+
+/*
+ * rowsm_config: launch overrides for rowsm_forward_config.  Every field left
+ * at 0 (packed: -1) takes the launcher's default for the chosen family.
+ */
+typedef struct rowsm_config {
+    int32_t variant;        /* rowsm_variant; ROWSM_AUTO = launcher's choice      */
+    int32_t vw;             /* elements per vector access: power of two that
+                               divides cols, <= 16 bytes of input, with x and y
+                               aligned to it                                      */
+    int32_t lanes_per_row;  /* SMALL: lanes holding one row, power of two <= 32   */
+    int32_t rows_per_lane;  /* SMALL: rows each lane handles per pass: 1,2,4,8    */
+    int32_t waves_per_row;  /* MEDIUM: wavefronts holding one row: 1,2,4,8,16     */
+    int32_t rows_per_block; /* MEDIUM: rows per block (rows*waves_per_row <= 16)  */
+    int32_t packed;         /* MEDIUM: 1 keep raw bf16 and recompute exp,
+                               0 keep fp32 exp values, -1 launcher's choice       */
+    int32_t block;          /* LARGE: threads per block, multiple of 64, <= 1024  */
+    int32_t tile_vectors;   /* LARGE: vectors per thread per tile: 2, 4, 8        */
+    int32_t blocks_per_cu;  /* grid cap = blocks_per_cu * compute units           */
+} rowsm_config;
+
+/*
+ * rowsm_forward_config: rowsm_forward with explicit launch overrides (kernel
+ * family, vector width, lane/wave grouping, tile size, grid cap), for tuning
+ * sweeps and tests.  cfg == NULL behaves like rowsm_forward.  An override the
+ * family cannot honour returns ROWSM_EINVAL without launching.  Results are
+ * the same softmax for every accepted configuration.
+ */
+int rowsm_forward_config(const void *x, void *y, int64_t rows, int64_t cols,
+                         int in_dtype, int out_dtype, void *stream,
+                         const rowsm_config *cfg);
+
+/*
+ * rowsm_describe: writes into buf (capacity len, always NUL-terminated when
+ * len > 0) a one-line description of the launch rowsm_forward_variant would
+ * make: kernel family, template configuration, grid and block sizes.  Pure
+ * host function.  Returns the status rowsm_forward_variant would return for
+ * these arguments with valid pointers.
+ */
+int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
+                   int variant, char *buf, int64_t len);
+
+/* rowsm_status_string: static, human-readable text for a rowsm_status. */
+const char *rowsm_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROWSM_H */

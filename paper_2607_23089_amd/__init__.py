@@ -1,0 +1,163 @@
+"""MI355X (gfx950) row softmax: Python binding of the C ABI in include/rowsm.h.
+
+Every function here only marshals arguments to the shared library
+``librowsm.so`` (built by ``paper_2607_23089_amd.build``); every step of the
+softmax runs in the library's HIP kernels.  There is no fallback: when the
+library is missing or fails to load, the calls raise ``RowsmError``.
+
+Raw entry points (same names and arguments as the C ABI; pointers are ints,
+``stream`` a hipStream_t handle as an int, 0 = default stream):
+
+    rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream) -> status
+    rowsm_forward_variant(x, y, rows, cols, in_dtype, out_dtype, stream, variant)
+    rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, cfg)
+    rowsm_select(rows, cols, in_dtype, out_dtype) -> variant or status
+    rowsm_describe(rows, cols, in_dtype, out_dtype, variant) -> (status, text)
+    rowsm_status_string(status) -> str
+
+Tensor helper: ``softmax(x, out_dtype=None, out=None, ...)`` for torch tensors
+on a GPU (marshalling only: pointers, sizes, dtype codes and the current
+stream).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+F32, BF16 = 0, 1
+AUTO, SMALL, MEDIUM, LARGE = 0, 1, 2, 3
+OK, EINVAL, EDTYPE, EHIP = 0, -1, -2, -3
+VARIANT_NAMES = {SMALL: "small", MEDIUM: "medium", LARGE: "large"}
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librowsm.so")
+
+# Symbols declared in include/rowsm.h.
+EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
+           "rowsm_forward_config", "rowsm_describe", "rowsm_status_string")
+
+
+class RowsmError(RuntimeError):
+    pass
+
+
+class RowsmConfig(ctypes.Structure):
+    """Mirror of ``rowsm_config`` (launch overrides; 0 / packed=-1 = default)."""
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "variant", "vw", "lanes_per_row", "rows_per_lane", "waves_per_row",
+        "rows_per_block", "packed", "block", "tile_vectors", "blocks_per_cu")]
+
+    def __init__(self, **kw):
+        super().__init__()
+        self.packed = -1
+        for k, v in kw.items():
+            if k not in dict(self._fields_):
+                raise TypeError(f"unknown rowsm_config field {k!r}")
+            setattr(self, k, int(v))
+
+
+_lib = None
+
+
+def lib(path: str | None = None) -> ctypes.CDLL:
+    """Load librowsm.so (once) and type its entry points."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RowsmError(f"{p} is missing: build it with "
+                         "`python -m paper_2607_23089_amd.build`")
+    try:
+        h = ctypes.CDLL(p)
+    except OSError as e:
+        raise RowsmError(f"cannot load {p}: {e}") from e
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    fwd = [vp, vp, i64, i64, i32, i32, vp]
+    h.rowsm_forward.argtypes = fwd
+    h.rowsm_forward.restype = i32
+    h.rowsm_forward_variant.argtypes = fwd + [i32]
+    h.rowsm_forward_variant.restype = i32
+    h.rowsm_forward_config.argtypes = fwd + [ctypes.POINTER(RowsmConfig)]
+    h.rowsm_forward_config.restype = i32
+    h.rowsm_select.argtypes = [i64, i64, i32, i32]
+    h.rowsm_select.restype = i32
+    h.rowsm_describe.argtypes = [i64, i64, i32, i32, i32, ctypes.c_char_p, i64]
+    h.rowsm_describe.restype = i32
+    h.rowsm_status_string.argtypes = [i32]
+    h.rowsm_status_string.restype = ctypes.c_char_p
+    if path is None:
+        _lib = h
+    return h
+
+
+def rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream=0) -> int:
+    return lib().rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream)
+
+
+def rowsm_forward_variant(x, y, rows, cols, in_dtype, out_dtype, stream, variant) -> int:
+    return lib().rowsm_forward_variant(x, y, rows, cols, in_dtype, out_dtype, stream,
+                                       variant)
+
+
+def rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, cfg) -> int:
+    if cfg is not None and not isinstance(cfg, RowsmConfig):
+        cfg = RowsmConfig(**cfg)
+    ref = ctypes.byref(cfg) if cfg is not None else None
+    return lib().rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, ref)
+
+
+def rowsm_select(rows, cols, in_dtype, out_dtype) -> int:
+    return lib().rowsm_select(rows, cols, in_dtype, out_dtype)
+
+
+def rowsm_describe(rows, cols, in_dtype, out_dtype, variant=AUTO):
+    buf = ctypes.create_string_buffer(256)
+    st = lib().rowsm_describe(rows, cols, in_dtype, out_dtype, variant, buf, len(buf))
+    return st, buf.value.decode()
+
+
+def rowsm_status_string(status) -> str:
+    return lib().rowsm_status_string(status).decode()
+
+
+def check(status: int) -> None:
+    if status != OK:
+        raise RowsmError(f"rowsm status {status}: {rowsm_status_string(status)}")
+
+
+def dtype_code(dtype) -> int:
+    import torch
+    if dtype == torch.float32:
+        return F32
+    if dtype == torch.bfloat16:
+        return BF16
+    raise RowsmError(f"unsupported dtype {dtype}")
+
+
+def softmax(x, out_dtype=None, out=None, variant: int = AUTO, config=None, stream=None):
+    """softmax(x, dim=-1) of a contiguous fp32/bf16 GPU tensor through the
+    library.  Returns ``out`` (allocated with ``out_dtype``, default x.dtype,
+    when not given).  Runs on torch's current stream unless ``stream`` (a
+    torch.cuda.Stream) is given."""
+    import torch
+    if not x.is_cuda:
+        raise RowsmError("rowsm.softmax needs a GPU tensor")
+    if not x.is_contiguous():
+        raise RowsmError("rowsm.softmax needs a contiguous tensor")
+    if out is None:
+        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
+        raise RowsmError("out must be a contiguous tensor of x's shape on x's device")
+    cols = x.shape[-1] if x.dim() else 1
+    rows = x.numel() // cols if cols else 0
+    st = (stream or torch.cuda.current_stream(x.device)).cuda_stream
+    args = (x.data_ptr(), out.data_ptr(), rows, cols, dtype_code(x.dtype),
+            dtype_code(out.dtype), st)
+    if config is not None:
+        check(rowsm_forward_config(*args, config))
+    elif variant != AUTO:
+        check(rowsm_forward_variant(*args, variant))
+    else:
+        check(rowsm_forward(*args))
+    return out

@@ -1,0 +1,151 @@
+// Medium-row softmax kernel: one row per group of WPR wavefronts, the whole row
+// held in registers, so x is read once and y written once.
+//
+// A block holds RPB = waves / WPR row groups.  Thread t of a row group
+// (t = 64 * wave_in_group + lane, T = 64 * WPR threads) owns the vectors
+// t, t + T, ..., t + (NV-1) T of the row, with NV = ceil(nvec / T) fixed at
+// compile time so that only the last slot can be partial, and every load
+// instruction of a wave reads 64 consecutive vectors.  The row
+// maximum and the row sum are reduced inside each wave with DPP and
+// permlane swaps, then across the WPR waves through LDS (one barrier each;
+// WPR == 1 needs neither LDS nor barriers).
+//
+// PACKED == false widens the row to fp32 once and keeps exp(x - m) in
+// registers for the normalise step.  PACKED == true keeps the row in its raw
+// input form (bf16 pairs take half the registers) and evaluates exp(x - m) a
+// second time when normalising; it lets one 1024-thread block hold a longer
+// bf16 row in registers.
+//
+// Blocks loop over rows with a grid stride; the trip count depends only on
+// blockIdx, so every wave of a block reaches every barrier.  Rows past the end
+// hold -inf, load and store nothing, and take part in the barriers.
+//
+// This is the medium-row member of the row-length-specialised family the
+// paper names for its running example (preamble listing style); the layout and
+// reductions are this library's gfx950 design.
+#pragma once
+
+#include "rowsm_device.hpp"
+
+namespace rowsm {
+
+// Reduce v over the row group of the calling wave: within the wave, then,
+// when the row spans wpr > 1 waves, across them through red[] (one barrier).
+// Partial results are combined in wave order, so the result is deterministic.
+template <typename Op>
+__device__ __forceinline__ float block_row_reduce(float v, int wpr, int wave, int g, int lane,
+                                                  float* red) {
+  v = group_reduce<kWave, Op>(v);
+  if (wpr > 1) {
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    v = red[g * wpr];
+    for (int w = 1; w < wpr; ++w) v = Op::apply(v, red[g * wpr + w]);
+  }
+  return v;
+}
+
+template <typename In, typename Out, int VW, int NV, bool PACKED>
+__global__ __launch_bounds__(1024) void medium_row_kernel(
+    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
+    int64_t rows, int cols, int wpr) {
+  __shared__ float red_m[16];
+  __shared__ float red_s[16];
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int rpb = (blockDim.x / kWave) / wpr;
+  const int g = wave / wpr;
+  const int T = wpr * kWave;
+  const int t = (wave - g * wpr) * kWave + lane;
+  const int nvec = cols / VW;
+  const uint32_t vin = (uint32_t)t * (VW * In::bytes);
+  const uint32_t vout = (uint32_t)t * (VW * Out::bytes);
+  const uint32_t sin = (uint32_t)T * (VW * In::bytes);    // byte stride between slots
+  const uint32_t sout = (uint32_t)T * (VW * Out::bytes);
+  // Slots 0 .. NV-2 lie wholly inside the row (the launcher picks
+  // NV = ceil(nvec / T)); only slot NV-1 needs a per-lane bound.
+  const bool last_ok = (NV - 1) * T + t < nvec;
+
+  for (int64_t base = (int64_t)blockIdx.x * rpb; base < rows;
+       base += (int64_t)gridDim.x * rpb) {
+    const int64_t row = base + g;
+    const bool row_ok = row < rows;
+    const int64_t rr = row_ok ? row : 0;
+    const rsrc_t rx = make_rsrc(x + rr * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t ry = make_rsrc(y + rr * cols, (uint64_t)cols * Out::bytes);
+
+    if constexpr (PACKED) {
+      InVec<In, VW> v[NV];
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        if (row_ok && (s < NV - 1 || last_ok)) v[s].load(rx, vin, s * sin);
+        else v[s].set_neg_inf();
+      }
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int s = 0; s < NV; ++s)
+#pragma unroll
+        for (int i = 0; i < VW; ++i) mx = fmax_nn(mx, v[s].get(i));
+      mx = block_row_reduce<MaxOp>(mx, wpr, wave, g, lane, red_m);
+      const float nml = -mx * kLog2e;
+#pragma unroll
+      for (int s = 0; s < NV; ++s) v[s].opaque();
+      float sum = 0.0f;
+#pragma unroll
+      for (int s = 0; s < NV; ++s)
+#pragma unroll
+        for (int i = 0; i < VW; ++i)
+          sum += exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml));
+      sum = block_row_reduce<SumOp>(sum, wpr, wave, g, lane, red_s);
+#pragma unroll
+      for (int s = 0; s < NV; ++s) v[s].opaque();
+      const float inv = __builtin_amdgcn_rcpf(sum);  // v_rcp_f32, 1 ulp
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        float o[VW];
+#pragma unroll
+        for (int i = 0; i < VW; ++i)
+          o[i] = exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml)) * inv;
+        if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(ry, vout + s * sout, o);
+      }
+    } else {
+      float f[NV][VW];
+      {
+        InVec<In, VW> v[NV];
+#pragma unroll
+        for (int s = 0; s < NV; ++s) {
+          if (row_ok && (s < NV - 1 || last_ok)) v[s].load(rx, vin, s * sin);
+          else v[s].set_neg_inf();
+        }
+#pragma unroll
+        for (int s = 0; s < NV; ++s) v[s].to_float(f[s]);
+      }
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int s = 0; s < NV; ++s)
+#pragma unroll
+        for (int i = 0; i < VW; ++i) mx = fmax_nn(mx, f[s][i]);
+      mx = block_row_reduce<MaxOp>(mx, wpr, wave, g, lane, red_m);
+      const float nml = -mx * kLog2e;
+      float sum = 0.0f;
+#pragma unroll
+      for (int s = 0; s < NV; ++s)
+#pragma unroll
+        for (int i = 0; i < VW; ++i) {
+          f[s][i] = exp2_fast(__builtin_fmaf(f[s][i], kLog2e, nml));
+          sum += f[s][i];
+        }
+      sum = block_row_reduce<SumOp>(sum, wpr, wave, g, lane, red_s);
+      const float inv = __builtin_amdgcn_rcpf(sum);  // v_rcp_f32, 1 ulp
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+#pragma unroll
+        for (int i = 0; i < VW; ++i) f[s][i] *= inv;
+        if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(ry, vout + s * sout, f[s]);
+      }
+    }
+  }
+}
+
+}  // namespace rowsm

@@ -1,0 +1,439 @@
+// Host side of the row-softmax library: argument validation, the row-length
+// and row-count launcher that picks a kernel family and its launch shape, the
+// template dispatch, and the C ABI declared in include/rowsm.h.
+//
+// The launcher mirrors the structure the paper names for its running example
+// (small-, medium- and large-row kernels selected by a row launcher, preamble
+// listing style).  Its thresholds are this library's, stated in plan_for():
+//   SMALL   a row is at most 32 vectors (one vector per lane, >= 2 rows per wave)
+//   MEDIUM  the row fits the registers of at most 16 waves
+//           (<= 64 fp32 values per lane, or <= 24 raw 16-byte bf16 vectors
+//           per lane in the packed form)
+//   LARGE   anything longer: two streaming passes over tiles.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdio>
+#include <cstring>
+#include <type_traits>
+#include <utility>
+
+#include "large_row.hpp"
+#include "medium_row.hpp"
+#include "rowsm.h"
+#include "small_row.hpp"
+
+namespace rowsm {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+
+// Compute-unit count of the current device (cached per device).  Falls back
+// to 256, the MI355X count, when no device can be queried.
+int cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int n = g_cu_count[dev].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0)
+    n = 256;
+  g_cu_count[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+int dtype_bytes(int dt) { return dt == ROWSM_F32 ? 4 : 2; }
+bool dtype_ok(int dt) { return dt == ROWSM_F32 || dt == ROWSM_BF16; }
+int next_pow2(int v) {
+  int p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+struct Plan {
+  int variant = 0;
+  int vw = 1;       // elements per vector
+  int nvec = 0;     // vectors per row
+  // SMALL
+  int lpr = 1, rpl = 4;
+  // MEDIUM
+  int wpr = 1, vpl = 1, nv = 1;
+  bool packed = false;
+  // LARGE
+  int u = 4;
+  // launch
+  int block = 256;
+  int64_t grid = 1;
+};
+
+// Vector widths (elements) with compiled kernels: 16-byte and 8-byte input
+// vectors, and single elements for rows that are not 8-byte aligned.
+bool vw_supported(int vw, int ib) { return vw == 1 || vw * ib == 16 || vw * ib == 8; }
+
+// Largest supported vector width that divides cols and keeps both the x and
+// the y accesses naturally aligned (16-byte loads at most).
+int choose_vw(int64_t cols, int ib, int ob, uintptr_t xa, uintptr_t ya) {
+  for (int vw = 16 / ib; vw > 1; vw >>= 1) {
+    if (!vw_supported(vw, ib)) continue;
+    const int xal = vw * ib;
+    const int yal = vw * ob < 16 ? vw * ob : 16;
+    if (cols % vw == 0 && xa % xal == 0 && ya % yal == 0) return vw;
+  }
+  return 1;
+}
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
+
+// Fill p for the given family (AUTO resolves first) and config overrides.
+// Returns ROWSM_OK or ROWSM_EINVAL when the family cannot take this shape.
+int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
+             const rowsm_config* cfg, int cus, Plan* p) {
+  const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
+  int vw = choose_vw(cols, ib, ob, xa, ya);
+  if (cfg && cfg->vw > 0) {
+    const int want = cfg->vw;
+    if (want > 16 / ib || (want & (want - 1)) || !vw_supported(want, ib) || cols % want ||
+        xa % (want * ib) || ya % (want * ob < 16 ? want * ob : 16))
+      return ROWSM_EINVAL;
+    vw = want;
+  }
+  const int nvec = (int)(cols / vw);
+  p->vw = vw;
+  p->nvec = nvec;
+
+  int variant = cfg ? cfg->variant : ROWSM_AUTO;
+  if (variant == ROWSM_AUTO) {
+    if (nvec <= 32) {
+      variant = ROWSM_SMALL;
+    } else if (nvec <= 16 * kWave * (64 / vw < 16 ? 64 / vw : 16) ||
+               (in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24)) {
+      variant = ROWSM_MEDIUM;
+    } else {
+      variant = ROWSM_LARGE;
+    }
+  }
+  p->variant = variant;
+
+  const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
+  if (variant == ROWSM_SMALL) {
+    if (nvec > 32) return ROWSM_EINVAL;
+    p->lpr = next_pow2(nvec);
+    if (cfg && cfg->lanes_per_row > 0) {
+      const int l = cfg->lanes_per_row;
+      if ((l & (l - 1)) || l > 32 || l < p->lpr) return ROWSM_EINVAL;
+      p->lpr = l;
+    }
+    p->rpl = 4;
+    if (cfg && cfg->rows_per_lane > 0) {
+      const int r = cfg->rows_per_lane;
+      if (r != 1 && r != 2 && r != 4 && r != 8) return ROWSM_EINVAL;
+      p->rpl = r;
+    }
+    p->block = 256;
+    const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 8);
+    p->grid = cdiv(rows, rows_per_block);
+    if (p->grid > cap) p->grid = cap;
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_MEDIUM) {
+    int wpr = 0, vpl = 0;
+    bool packed = false;
+    const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
+    const int want_packed = cfg ? cfg->packed : -1;
+    if (want_wpr && (want_wpr & (want_wpr - 1) || want_wpr > 16)) return ROWSM_EINVAL;
+    // Unpacked: the smallest group whose lanes hold <= 32 fp32 values each
+    // (<= 64 when the row is longer), unless a group size is forced.
+    if (want_packed != 1) {
+      for (int cap_vals : {32, 64}) {
+        for (int w = 1; w <= 16; w <<= 1) {
+          if (want_wpr && w != want_wpr) continue;
+          const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+          if (v * vw <= cap_vals && medium_unpacked_cap(vw, v)) {
+            wpr = w;
+            vpl = v;
+            break;
+          }
+        }
+        if (wpr) break;
+      }
+    }
+    if (!wpr && want_packed != 0 && in_dt == ROWSM_BF16 && vw == 8) {
+      for (int w = 1; w <= 16; w <<= 1) {
+        if (want_wpr && w != want_wpr) continue;
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v <= 24 && (w == 16 || want_wpr)) {
+          wpr = w;
+          vpl = v;
+          packed = true;
+          break;
+        }
+      }
+    }
+    if (!wpr) return ROWSM_EINVAL;
+    // Slot counts are exact (only the last slot may be partial); packed
+    // kernels exist for 9..24 slots.
+    if (packed && (vpl < 9 || vpl > 24)) return ROWSM_EINVAL;
+    p->wpr = wpr;
+    p->vpl = vpl;
+    p->packed = packed;
+    p->nv = vpl;
+    int rpb = wpr >= 4 ? 1 : 4 / wpr;
+    if (cfg && cfg->rows_per_block > 0) {
+      rpb = cfg->rows_per_block;
+      if (rpb * wpr > 16) return ROWSM_EINVAL;
+    }
+    p->block = rpb * wpr * kWave;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 8);
+    p->grid = cdiv(rows, rpb);
+    if (p->grid > cap) p->grid = cap;
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_LARGE) {
+    p->u = 4;
+    if (cfg && cfg->tile_vectors > 0) {
+      const int u = cfg->tile_vectors;
+      if (u != 2 && u != 4 && u != 8) return ROWSM_EINVAL;
+      p->u = u;
+    }
+    p->block = 512;
+    if (cfg && cfg->block > 0) {
+      const int b = cfg->block;
+      if (b % kWave || b > 1024) return ROWSM_EINVAL;
+      p->block = b;
+    }
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 2);
+    p->grid = rows < cap ? rows : cap;
+    return ROWSM_OK;
+  }
+  return ROWSM_EINVAL;
+}
+
+// ---- template dispatch ------------------------------------------------------
+
+template <typename In, typename Out, int VW>
+bool launch_small(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                  hipStream_t st) {
+  auto xp = static_cast<const typename In::storage*>(x);
+  auto yp = static_cast<typename Out::storage*>(y);
+#define ROWSM_SMALL_CASE(L, R)                                                           \
+  if (p.lpr == L && p.rpl == R) {                                                        \
+    small_row_kernel<In, Out, VW, L, R><<<dim3((unsigned)p.grid), dim3(p.block), 0, st>>>( \
+        xp, yp, rows, cols);                                                             \
+    return true;                                                                         \
+  }
+#define ROWSM_SMALL_L(L) \
+  ROWSM_SMALL_CASE(L, 1) ROWSM_SMALL_CASE(L, 2) ROWSM_SMALL_CASE(L, 4) ROWSM_SMALL_CASE(L, 8)
+  ROWSM_SMALL_L(1) ROWSM_SMALL_L(2) ROWSM_SMALL_L(4) ROWSM_SMALL_L(8) ROWSM_SMALL_L(16)
+  ROWSM_SMALL_L(32)
+#undef ROWSM_SMALL_L
+#undef ROWSM_SMALL_CASE
+  return false;
+}
+
+template <typename In, typename Out, int VW, int NV, bool PACKED>
+bool try_medium(const Plan& p, const void* x, void* y, int64_t rows, int cols, hipStream_t st) {
+  constexpr bool compiled =
+      PACKED ? (std::is_same<In, BF16>::value && VW == 8 && NV >= 9 && NV <= 24)
+             : (NV * VW <= 64 && NV <= 16);
+  if constexpr (compiled) {
+    if (p.nv == NV && p.packed == PACKED) {
+      medium_row_kernel<In, Out, VW, NV, PACKED>
+          <<<dim3((unsigned)p.grid), dim3(p.block), 0, st>>>(
+              static_cast<const typename In::storage*>(x),
+              static_cast<typename Out::storage*>(y), rows, cols, p.wpr);
+      return true;
+    }
+  }
+  return false;
+}
+
+template <typename In, typename Out, int VW, bool PACKED, int... NVs>
+bool launch_medium_nv(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                      hipStream_t st, std::integer_sequence<int, NVs...>) {
+  return (try_medium<In, Out, VW, NVs + 1, PACKED>(p, x, y, rows, cols, st) || ...);
+}
+
+template <typename In, typename Out, int VW>
+bool launch_medium(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                   hipStream_t st) {
+  if (p.packed)
+    return launch_medium_nv<In, Out, VW, true>(p, x, y, rows, cols, st,
+                                               std::make_integer_sequence<int, 24>{});
+  return launch_medium_nv<In, Out, VW, false>(p, x, y, rows, cols, st,
+                                              std::make_integer_sequence<int, 16>{});
+}
+
+template <typename In, typename Out, int VW>
+bool launch_large(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                  hipStream_t st) {
+  auto xp = static_cast<const typename In::storage*>(x);
+  auto yp = static_cast<typename Out::storage*>(y);
+  const dim3 g((unsigned)p.grid), b(p.block);
+  if (p.u == 2) large_row_kernel<In, Out, VW, 2><<<g, b, 0, st>>>(xp, yp, rows, cols);
+  else if (p.u == 4) large_row_kernel<In, Out, VW, 4><<<g, b, 0, st>>>(xp, yp, rows, cols);
+  else if (p.u == 8) large_row_kernel<In, Out, VW, 8><<<g, b, 0, st>>>(xp, yp, rows, cols);
+  else return false;
+  return true;
+}
+
+template <typename In, typename Out, int VW>
+bool launch_vw(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+               hipStream_t st) {
+  if (p.variant == ROWSM_SMALL) return launch_small<In, Out, VW>(p, x, y, rows, cols, st);
+  if (p.variant == ROWSM_MEDIUM) return launch_medium<In, Out, VW>(p, x, y, rows, cols, st);
+  if (p.variant == ROWSM_LARGE) return launch_large<In, Out, VW>(p, x, y, rows, cols, st);
+  return false;
+}
+
+// Compiled vector widths: 16- and 8-byte input vectors and single elements.
+template <typename In, typename Out>
+bool launch_io(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+               hipStream_t st) {
+  constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
+  if (p.vw == 1) return launch_vw<In, Out, 1>(p, x, y, rows, cols, st);
+  if (p.vw == V8) return launch_vw<In, Out, V8>(p, x, y, rows, cols, st);
+  if (p.vw == V16) return launch_vw<In, Out, V16>(p, x, y, rows, cols, st);
+  return false;
+}
+
+// Returns false when no compiled kernel matches the plan (no launch made).
+bool launch(const Plan& p, int in_dt, int out_dt, const void* x, void* y, int64_t rows,
+            int cols, hipStream_t st) {
+  if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32)
+    return launch_io<F32, F32>(p, x, y, rows, cols, st);
+  if (in_dt == ROWSM_F32) return launch_io<F32, BF16>(p, x, y, rows, cols, st);
+  if (out_dt == ROWSM_F32) return launch_io<BF16, F32>(p, x, y, rows, cols, st);
+  return launch_io<BF16, BF16>(p, x, y, rows, cols, st);
+}
+
+// ---- validation -------------------------------------------------------------
+
+// Host-only argument checks shared by every entry point.  *noop is set when
+// the call is valid and has nothing to do.
+int validate(const void* x, const void* y, int64_t rows, int64_t cols, int in_dt,
+             int out_dt, bool check_ptrs, bool* noop) {
+  *noop = false;
+  if (!dtype_ok(in_dt) || !dtype_ok(out_dt)) return ROWSM_EDTYPE;
+  if (rows < 0 || cols < 0) return ROWSM_EINVAL;
+  if (rows == 0 || cols == 0) {
+    *noop = true;
+    return ROWSM_OK;
+  }
+  if (cols >= ((int64_t)1 << 30)) return ROWSM_EINVAL;  // row bytes fit 32-bit offsets
+  if (rows > ((int64_t)1 << 62) / cols) return ROWSM_EINVAL;
+  if (!check_ptrs) return ROWSM_OK;
+  if (!x || !y) return ROWSM_EINVAL;
+  const uintptr_t xa = (uintptr_t)x, ya = (uintptr_t)y;
+  const uint64_t n = (uint64_t)rows * (uint64_t)cols;
+  const uint64_t xb = n * (uint64_t)dtype_bytes(in_dt), yb = n * (uint64_t)dtype_bytes(out_dt);
+  const bool overlap = xa < ya + yb && ya < xa + xb;
+  if (overlap && !(xa == ya && in_dt == out_dt)) return ROWSM_EINVAL;
+  return ROWSM_OK;
+}
+
+int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, int out_dt,
+                 void* stream, const rowsm_config* cfg) {
+  bool noop = false;
+  int st = validate(x, y, rows, cols, in_dt, out_dt, true, &noop);
+  if (st != ROWSM_OK || noop) return st;
+  if (cfg && (cfg->variant < ROWSM_AUTO || cfg->variant > ROWSM_LARGE)) return ROWSM_EINVAL;
+  Plan p;
+  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, cu_count(), &p);
+  if (st != ROWSM_OK) return st;
+  (void)hipGetLastError();  // do not report an earlier, unrelated error
+  if (!launch(p, in_dt, out_dt, x, y, rows, (int)cols, static_cast<hipStream_t>(stream)))
+    return ROWSM_EINVAL;  // no compiled kernel for this plan: nothing was enqueued
+  return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+}
+
+const char* variant_name(int v) {
+  switch (v) {
+    case ROWSM_SMALL: return "small";
+    case ROWSM_MEDIUM: return "medium";
+    case ROWSM_LARGE: return "large";
+    default: return "?";
+  }
+}
+
+}  // namespace
+}  // namespace rowsm
+
+using namespace rowsm;
+
+extern "C" int rowsm_forward(const void* x, void* y, int64_t rows, int64_t cols, int in_dtype,
+                             int out_dtype, void* stream) {
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr);
+}
+
+extern "C" int rowsm_forward_variant(const void* x, void* y, int64_t rows, int64_t cols,
+                                     int in_dtype, int out_dtype, void* stream, int variant) {
+  if (variant < ROWSM_AUTO || variant > ROWSM_LARGE) {
+    bool noop = false;
+    const int st = validate(x, y, rows, cols, in_dtype, out_dtype, true, &noop);
+    return st != ROWSM_OK ? st : ROWSM_EINVAL;
+  }
+  rowsm_config cfg;
+  std::memset(&cfg, 0, sizeof(cfg));
+  cfg.variant = variant;
+  cfg.packed = -1;
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, &cfg);
+}
+
+extern "C" int rowsm_forward_config(const void* x, void* y, int64_t rows, int64_t cols,
+                                    int in_dtype, int out_dtype, void* stream,
+                                    const rowsm_config* cfg) {
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg);
+}
+
+extern "C" int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dtype) {
+  bool noop = false;
+  const int st = validate(nullptr, nullptr, rows, cols, in_dtype, out_dtype, false, &noop);
+  if (st != ROWSM_OK) return st;
+  if (noop) return ROWSM_SMALL;  // nothing is launched; report the smallest family
+  Plan p;
+  const int r = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, &p);
+  return r == ROWSM_OK ? p.variant : r;
+}
+
+extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
+                              int variant, char* buf, int64_t len) {
+  bool noop = false;
+  int st = validate(nullptr, nullptr, rows, cols, in_dtype, out_dtype, false, &noop);
+  if (st == ROWSM_OK && (variant < ROWSM_AUTO || variant > ROWSM_LARGE)) st = ROWSM_EINVAL;
+  Plan p;
+  if (st == ROWSM_OK && !noop) {
+    rowsm_config cfg;
+    std::memset(&cfg, 0, sizeof(cfg));
+    cfg.variant = variant;
+    cfg.packed = -1;
+    st = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, &cfg, 256, &p);
+  }
+  if (buf && len > 0) {
+    if (st != ROWSM_OK) {
+      std::snprintf(buf, (size_t)len, "error %d", st);
+    } else if (noop) {
+      std::snprintf(buf, (size_t)len, "empty: no launch");
+    } else {
+      std::snprintf(buf, (size_t)len,
+                    "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
+                    "block=%d grid=%lld (grid assumes 256 CUs)",
+                    variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
+                    (int)p.packed, p.u, p.block, (long long)p.grid);
+    }
+  }
+  return st;
+}
+
+extern "C" const char* rowsm_status_string(int status) {
+  switch (status) {
+    case ROWSM_OK: return "ok";
+    case ROWSM_EINVAL: return "invalid argument";
+    case ROWSM_EDTYPE: return "unsupported dtype";
+    case ROWSM_EHIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}

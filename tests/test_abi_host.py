@@ -1,0 +1,139 @@
+"""C ABI on the host (no GPU): the library loads, exports every declared
+symbol, validates arguments before any HIP call, and the launcher's family
+choice follows its stated thresholds."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_23089_amd as R
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "rowsm.h")
+MiB = 1 << 20
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(R.LIB_PATH):
+        from paper_2607_23089_amd.build import build_library
+        build_library()
+    return R.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rowsm_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(R.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_config_struct_matches_header():
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct rowsm_config \{(.*?)\} rowsm_config;", text, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"int32_t\s+(\w+);", body)
+    assert fields == [f for f, _ in R.RowsmConfig._fields_]
+
+
+def test_status_strings(lib):
+    assert R.rowsm_status_string(R.OK) == "ok"
+    assert "invalid" in R.rowsm_status_string(R.EINVAL)
+    assert "dtype" in R.rowsm_status_string(R.EDTYPE)
+    assert "HIP" in R.rowsm_status_string(R.EHIP)
+    assert R.rowsm_status_string(12345) == "unknown status"
+
+
+# Fake, never-dereferenced addresses: every call below must be rejected (or be
+# a no-op) before the library makes any HIP call.
+X, Y = 0x7f0000000000, 0x7f8000000000
+
+
+@pytest.mark.parametrize("args,want", [
+    ((X, Y, 4, 8, 7, R.F32), R.EDTYPE),
+    ((X, Y, 4, 8, R.F32, -1), R.EDTYPE),
+    ((X, Y, -1, 8, R.F32, R.F32), R.EINVAL),
+    ((X, Y, 4, -8, R.F32, R.F32), R.EINVAL),
+    ((0, Y, 4, 8, R.F32, R.F32), R.EINVAL),
+    ((X, 0, 4, 8, R.F32, R.F32), R.EINVAL),
+    ((X, X + 4, 4, 8, R.F32, R.F32), R.EINVAL),          # partial overlap
+    ((X, X, 4, 8, R.BF16, R.F32), R.EINVAL),             # in place, dtype change
+    ((X, Y, 1, 1 << 30, R.F32, R.F32), R.EINVAL),        # row too long
+    ((X, Y, 1 << 40, 1 << 23, R.F32, R.F32), R.EINVAL),  # rows*cols >= 2^62
+    ((0, 0, 0, 8, R.F32, R.F32), R.OK),                  # empty: no launch
+    ((0, 0, 8, 0, R.BF16, R.BF16), R.OK),
+])
+def test_argument_errors(lib, args, want):
+    assert R.rowsm_forward(*args, 0) == want
+    assert R.rowsm_forward_variant(*args, 0, R.AUTO) == want
+
+
+def test_bad_variant_and_config(lib):
+    assert R.rowsm_forward_variant(X, Y, 4, 8, R.F32, R.F32, 0, 9) == R.EINVAL
+    assert R.rowsm_forward_variant(X, Y, 4, 8, R.F32, R.F32, 0, -2) == R.EINVAL
+    # a family that cannot take the shape
+    assert R.rowsm_forward_variant(X, Y, 4, 4096, R.F32, R.F32, 0, R.SMALL) == R.EINVAL
+    assert R.rowsm_forward_variant(X, Y, 4, 1 << 20, R.F32, R.F32, 0, R.MEDIUM) == R.EINVAL
+    bad = [dict(variant=R.SMALL, lanes_per_row=3), dict(variant=R.SMALL, lanes_per_row=64),
+           dict(variant=R.SMALL, rows_per_lane=3), dict(variant=R.MEDIUM, waves_per_row=3),
+           dict(variant=R.MEDIUM, waves_per_row=4, rows_per_block=8),
+           dict(variant=R.LARGE, block=100), dict(variant=R.LARGE, tile_vectors=3),
+           dict(variant=R.AUTO, vw=3), dict(variant=R.AUTO, vw=2),
+           dict(variant=R.MEDIUM, packed=1, waves_per_row=16)]
+    for cfg in bad:
+        st = R.rowsm_forward_config(X, Y, 64, 64, R.BF16, R.BF16, 0, R.RowsmConfig(**cfg))
+        assert st == R.EINVAL, cfg
+
+
+def test_select_regimes(lib):
+    s = R.rowsm_select
+    # row of <= 32 vectors -> SMALL
+    assert s(262144, 64, R.BF16, R.BF16) == R.SMALL
+    assert s(10, 256, R.BF16, R.BF16) == R.SMALL      # 32 bf16 vectors of 8
+    assert s(10, 257, R.BF16, R.BF16) == R.MEDIUM     # odd: 257 single elements
+    assert s(10, 264, R.BF16, R.BF16) == R.MEDIUM     # 33 vectors
+    assert s(10, 128, R.F32, R.F32) == R.SMALL
+    assert s(10, 132, R.F32, R.F32) == R.MEDIUM
+    assert s(10, 32, R.F32, R.F32) == R.SMALL
+    assert s(10, 33, R.F32, R.F32) == R.MEDIUM        # 33 single elements
+    # medium: up to 16 waves x 64 lanes x 64 fp32 values
+    assert s(64, 1000, R.F32, R.F32) == R.MEDIUM
+    assert s(32768, 4096, R.BF16, R.BF16) == R.MEDIUM
+    assert s(10, 65536, R.F32, R.F32) == R.MEDIUM
+    assert s(10, 65540, R.F32, R.F32) == R.LARGE
+    assert s(10, 65536, R.BF16, R.BF16) == R.MEDIUM
+    # packed bf16 rows up to 16 x 64 x 24 vectors of 8
+    assert s(4096, 151936, R.BF16, R.F32) == R.MEDIUM
+    assert s(10, 196608, R.BF16, R.BF16) == R.MEDIUM
+    assert s(10, 196616, R.BF16, R.BF16) == R.LARGE
+    assert s(1024, 262144, R.F32, R.F32) == R.LARGE
+    assert s(0, 5, R.F32, R.F32) > 0
+    assert s(5, 5, 3, R.F32) == R.EDTYPE
+    assert s(-5, 5, R.F32, R.F32) == R.EINVAL
+
+
+def test_describe(lib):
+    st, text = R.rowsm_describe(262144, 64, R.BF16, R.BF16)
+    assert st == R.OK and text.startswith("small") and "lpr=8" in text and "vw=8" in text
+    st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
+    assert st == R.OK and text.startswith("medium")
+    st, text = R.rowsm_describe(4096, 151936, R.BF16, R.F32)
+    assert st == R.OK and "packed=1" in text and "vpl=19" in text and "wpr=16" in text
+    st, text = R.rowsm_describe(1024, 262144, R.F32, R.F32, R.LARGE)
+    assert st == R.OK and text.startswith("large")
+    st, text = R.rowsm_describe(4, 4096, R.F32, R.F32, R.SMALL)
+    assert st == R.EINVAL and text.startswith("error")
+    st, text = R.rowsm_describe(0, 4096, R.F32, R.F32)
+    assert st == R.OK and "no launch" in text
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(R.RowsmError):
+        R.lib(str(tmp_path / "missing.so"))

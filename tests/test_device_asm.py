@@ -1,0 +1,81 @@
+"""Checks on the gfx950 assembly of the library's own kernels (no GPU).
+
+The device code is compiled to assembly (hipcc -S, device pass only) and
+scanned for properties the kernels rely on:
+  * no store through a buffer descriptor uses a register soffset: the
+    compiler then treats the store's data registers as free for the next
+    VALU write, which corrupted outputs on gfx950; with a constant soffset it
+    inserts the wait states;
+  * no store of more than 64 bits is followed directly by a VALU write of its
+    data registers;
+  * the kernels the launcher picks for the benchmark workloads spill nothing
+    to scratch;
+  * the reductions use DPP and the gfx950 permlane swaps, the exponentials
+    v_exp_f32, and bf16 outputs v_cvt_pk_bf16_f32.
+"""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2607_23089_amd import build as B
+
+
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    out = tmp_path_factory.mktemp("asm") / "rowsm.s"
+    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-I", B.INCLUDE, "-I", B.CSRC, "-o", str(out)] + B.SOURCES
+    subprocess.run(cmd, check=True, capture_output=True)
+    return out.read_text()
+
+
+def kernels(asm):
+    return {m.group(1): m.group(2) for m in
+            re.finditer(r"\.amdhsa_kernel (\S+)(.*?)\.end_amdhsa_kernel", asm, re.S)}
+
+
+def test_buffer_stores_use_constant_soffset(asm):
+    soffs = re.findall(r"buffer_store_\S+ \S+, \S+, s\[\d+:\d+\], (\S+)", asm)
+    assert soffs, "no buffer stores found"
+    assert set(soffs) == {"0"}
+
+
+def test_no_immediate_overwrite_of_store_data(asm):
+    lines = asm.splitlines()
+    for i, line in enumerate(lines):
+        m = re.match(r"\s*(?:buffer|global)_store_dwordx(?:3|4) v\[(\d+):(\d+)\]", line)
+        if not m:
+            m2 = re.match(r"\s*global_store_dwordx(?:3|4) \S+, v\[(\d+):(\d+)\]", line)
+            if not m2:
+                continue
+            m = m2
+        lo, hi = int(m.group(1)), int(m.group(2))
+        nxt = lines[i + 1].strip()
+        d = re.match(r"v_\S+\s+v(\d+)", nxt)
+        assert not (d and lo <= int(d.group(1)) <= hi), f"{line.strip()} | {nxt}"
+
+
+@pytest.mark.parametrize("pattern", [
+    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4E",        # small_262144x64
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi4ELb0E",       # causal_32768x4096
+    r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0E",        # fp32_64x1000
+    r"medium_row_kernelINS_4BF16ENS_3F32ELi8ELi19ELb1E",  # vocab_4096x151936
+    r"large_row_kernelINS_3F32ES1_Li4ELi4E",             # large_1024x262144
+])
+def test_workload_kernels_do_not_spill(asm, pattern):
+    ks = {k: v for k, v in kernels(asm).items() if re.search(pattern, k)}
+    assert len(ks) == 1, pattern
+    body = next(iter(ks.values()))
+    assert int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", body).group(1)) == 0
+
+
+def test_expected_instructions(asm):
+    for ins in ("row_half_mirror", "row_mirror", "quad_perm:[1,0,3,2]",
+                "v_permlane16_swap_b32", "v_permlane32_swap_b32", "v_exp_f32",
+                "v_cvt_pk_bf16_f32", "buffer_load_dwordx4", "buffer_store_dwordx4"):
+        assert ins in asm, ins
+    # no packed-fp32 arithmetic anywhere
+    assert not re.search(r"v_pk_(add|mul|fma)_f32", asm)

@@ -1,0 +1,188 @@
+"""GPU parity: every kernel family through the C ABI against the fp64 oracle.
+
+Element-by-element comparison on seeded inputs that span several tiles and a
+ragged tail, for every family the launcher can choose and every dtype pair,
+plus the edge cases (empty, one column, odd widths and misaligned rows,
+special values, in place).  Tolerances (oracle/compare.py): fp32 output
+within 2e-6 absolute; bf16 output within one bf16 ulp of the oracle value;
+NaN positions and exact zeros identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_23089_amd as R
+from oracle.compare import compare, widen_output
+from paper_2607_23089_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+DT = {"f32": torch.float32, "bf16": torch.bfloat16}
+PAIRS = [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32"), ("f32", "bf16")]
+
+
+def oracle_of(x_cpu: torch.Tensor) -> np.ndarray:
+    b = W.to_bits_numpy(x_cpu)
+    v = oracle.widen_bf16_bits(b) if x_cpu.dtype == torch.bfloat16 else oracle.widen_f32(b)
+    return oracle.softmax_f64(v.reshape(-1, x_cpu.shape[-1]), threads=4)
+
+
+def run(x_dev, dout, variant=R.AUTO, config=None, out=None):
+    y = R.softmax(x_dev, out_dtype=DT[dout], out=out, variant=variant, config=config)
+    torch.cuda.synchronize()
+    return y
+
+
+def assert_parity(x_cpu, y_dev, dout, what=""):
+    v = oracle_of(x_cpu)
+    y = widen_output(W.to_bits_numpy(y_dev), dout).reshape(v.shape)
+    res = compare(y, v, dout)
+    assert res["ok"], f"{what}: {res}"
+    return res
+
+
+def family_accepts(rows, cols, din, dout, fam):
+    st, _ = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]), fam)
+    return st == R.OK
+
+
+GRID_COLS = {
+    R.SMALL: [1, 2, 3, 7, 8, 9, 16, 31, 32, 33, 63, 64, 65, 127, 128, 255, 256],
+    R.MEDIUM: [1, 7, 33, 64, 200, 1000, 1023, 1024, 4095, 4096, 4097, 8200, 16385,
+               65536, 151936],
+    R.LARGE: [1, 7, 1000, 4097, 65536, 65540, 100003, 262144],
+}
+
+
+def grid_cases():
+    for fam, cols_list in GRID_COLS.items():
+        for din, dout in PAIRS:
+            for cols in cols_list:
+                for rows in (1, 3, 67):
+                    if rows * cols > 3_000_000:
+                        continue
+                    yield fam, din, dout, rows, cols
+
+
+@pytest.mark.parametrize("fam,din,dout,rows,cols", list(grid_cases()))
+def test_family_grid(fam, din, dout, rows, cols):
+    if not family_accepts(rows, cols, din, dout, fam):
+        pytest.skip("family does not take this shape (checked by test_family_limits)")
+    x = W.random_matrix(rows, cols, din, sigma=6.0, seed=rows * 7919 + cols)
+    y = run(x.to(DEV), dout, variant=fam)
+    assert_parity(x, y, dout, f"{R.VARIANT_NAMES[fam]} {rows}x{cols} {din}->{dout}")
+
+
+def test_family_limits():
+    # SMALL takes rows of at most 32 vectors, MEDIUM at most the registers of
+    # 16 waves; anything else is refused without a launch.
+    x = torch.zeros(4, 4096, device=DEV)
+    y = torch.empty_like(x)
+    st = R.rowsm_forward_variant(x.data_ptr(), y.data_ptr(), 4, 4096, R.F32, R.F32, 0, R.SMALL)
+    assert st == R.EINVAL
+    x = torch.zeros(2, 70000, device=DEV)
+    y = torch.empty_like(x)
+    st = R.rowsm_forward_variant(x.data_ptr(), y.data_ptr(), 2, 70000, R.F32, R.F32, 0, R.MEDIUM)
+    assert st == R.EINVAL
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("fam", [R.SMALL, R.MEDIUM, R.LARGE])
+def test_special_values(fam, din, dout):
+    cols = {R.SMALL: 48, R.MEDIUM: 1000, R.LARGE: 70000}[fam]
+    x = W.random_matrix(8, cols, "f32", sigma=3.0, seed=11)
+    x[0, 5] = float("nan")
+    x[1, 0] = float("inf")
+    x[2, :] = float("-inf")
+    x[3, ::3] = float("-inf")           # masked entries with a finite max
+    x[4, :] = 2.5                       # constant row
+    x[5, :] = -1000.0
+    x[5, cols // 2] = 0.0               # dominant entry
+    x[6, :-1] = float("-inf")           # single finite entry, at the end
+    x = x.to(DT[din])
+    y = run(x.to(DEV), dout, variant=fam)
+    assert_parity(x, y, dout, f"special {R.VARIANT_NAMES[fam]} {din}->{dout}")
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+def test_misaligned_rows_fall_back_to_narrow_vectors(din, dout):
+    # A view starting one element into its storage breaks 8/16-byte alignment;
+    # the launcher must pick single-element accesses and stay exact.
+    for fam, cols in ((R.SMALL, 24), (R.MEDIUM, 1024), (R.LARGE, 65600)):
+        base = W.random_matrix(1, 5 * cols + 1, din, sigma=2.0, seed=cols).to(DEV)
+        x = base.view(-1)[1:].view(5, cols)
+        assert x.data_ptr() % 8 != 0
+        y = run(x, dout, variant=fam)
+        assert_parity(x.cpu(), y, dout, f"misaligned {R.VARIANT_NAMES[fam]} {din}->{dout}")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("fam,cols", [(R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 80000)])
+def test_in_place(fam, cols, dt):
+    x = W.random_matrix(9, cols, dt, sigma=5.0, seed=3)
+    xd = x.to(DEV)
+    run(xd, dt, variant=fam, out=xd)
+    assert_parity(x, xd, dt, f"in place {R.VARIANT_NAMES[fam]}")
+
+
+def test_empty_and_degenerate():
+    for rows, cols in ((0, 16), (16, 0), (0, 0)):
+        x = torch.empty(rows, cols, device=DEV)
+        y = torch.full((rows, cols), 7.0, device=DEV)
+        assert R.rowsm_forward(x.data_ptr(), y.data_ptr(), rows, cols, R.F32, R.F32, 0) == R.OK
+    x = W.random_matrix(300, 1, "f32", sigma=50.0, seed=1)
+    y = run(x.to(DEV), "f32")
+    assert_parity(x, y, "f32", "one column")
+
+
+@pytest.mark.parametrize("cfg", [
+    dict(variant=R.SMALL, lanes_per_row=16, rows_per_lane=1),
+    dict(variant=R.SMALL, lanes_per_row=32, rows_per_lane=8, blocks_per_cu=1),
+    dict(variant=R.SMALL, rows_per_lane=2, blocks_per_cu=1),
+    dict(variant=R.MEDIUM, waves_per_row=1, rows_per_block=8, blocks_per_cu=1),
+    dict(variant=R.MEDIUM, waves_per_row=2, blocks_per_cu=1),
+    dict(variant=R.MEDIUM, waves_per_row=16),
+    dict(variant=R.MEDIUM, waves_per_row=4, rows_per_block=3, blocks_per_cu=1),
+    dict(variant=R.LARGE, block=256, tile_vectors=8, blocks_per_cu=1),
+    dict(variant=R.LARGE, block=1024, tile_vectors=2),
+    dict(variant=R.LARGE, block=64, tile_vectors=4, blocks_per_cu=1),
+])
+def test_launch_overrides(cfg):
+    # Overrides change the launch shape, never the result; blocks_per_cu=1
+    # makes every block loop over several rows or row groups.
+    cols = {R.SMALL: 64, R.MEDIUM: 3000, R.LARGE: 20000}[cfg["variant"]]
+    for din, dout in (("bf16", "bf16"), ("f32", "f32")):
+        rows = 2500 if cfg["variant"] != R.LARGE else 600
+        x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols)
+        y = run(x.to(DEV), dout, config=R.RowsmConfig(**cfg))
+        assert_parity(x, y, dout, f"override {cfg} {din}->{dout}")
+
+
+def test_deterministic_and_bounded_writes():
+    # Same input twice -> bitwise-identical output; nothing written outside y;
+    # x untouched.
+    for fam, cols in ((R.SMALL, 64), (R.MEDIUM, 4096), (R.MEDIUM, 151936), (R.LARGE, 262144)):
+        rows = max(2, 2_000_000 // cols)
+        x = W.random_matrix(rows, cols, "bf16", sigma=8.0, seed=5).to(DEV)
+        x_before = x.clone()
+        guard = 4096
+        n = rows * cols
+        buf = torch.full((n + 2 * guard,), -123.0, device=DEV)
+        y1 = buf[guard:guard + n].view(rows, cols)
+        run(x, "f32", variant=fam, out=y1)
+        y2 = run(x, "f32", variant=fam)
+        assert torch.equal(y1, y2), R.VARIANT_NAMES[fam]
+        assert torch.all(buf[:guard] == -123.0) and torch.all(buf[guard + n:] == -123.0)
+        assert torch.equal(x, x_before)
+
+
+def test_streams():
+    # The kernel runs on the stream it is given.
+    s = torch.cuda.Stream()
+    x = W.random_matrix(512, 1000, "f32", seed=9).to(DEV)
+    with torch.cuda.stream(s):
+        y = R.softmax(x, stream=s)
+    s.synchronize()
+    assert_parity(x.cpu(), y, "f32", "side stream")
