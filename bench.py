@@ -34,7 +34,7 @@ METRIC = "row-softmax achieved HBM GB/s and % of MI355X peak, per row-length reg
 PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = ["rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
-                  "rowsm.hip"]
+                  "split_row.hpp", "rowsm.hip"]
 
 
 def kernel_source_hash() -> str:

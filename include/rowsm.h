@@ -25,7 +25,13 @@
  *     to nearest even.
  *   - stream is a hipStream_t (NULL = the legacy default stream).  The call
  *     only enqueues work; results are visible once the caller synchronises the
- *     stream.  Nothing is allocated per call.
+ *     stream.  Nothing is allocated per call.  The single-read LARGE form
+ *     uses a 2 MiB device workspace that the first such call on a device
+ *     allocates and clears (synchronously) and that lives until the process
+ *     ends; make that first call outside stream capture.  Such launches on
+ *     one device are ordered one after another whatever their streams (each
+ *     waits for the previous one through an event), so the workspace is never
+ *     shared by two running launches.
  *   - Errors are reported through the return value only (a rowsm_status);
  *     the library never aborts, prints or throws.  Argument errors are found
  *     on the host before any HIP call.  A failed launch maps to ROWSM_EHIP.
@@ -55,8 +61,10 @@ typedef enum {
 
 /* Kernel families.  SMALL packs several rows into one 64-lane wavefront;
  * MEDIUM gives each row one workgroup (or one wavefront) and keeps the row in
- * registers; LARGE streams a row through tiles twice (statistics pass with an
- * online max/sum merge, then a normalize pass). */
+ * registers; LARGE spreads a row over several co-resident workgroups that
+ * keep their shares in registers and exchange (max, sum) pairs through a
+ * small device workspace (single read), or, for rows too long for that,
+ * streams the row through tiles twice (online max/sum pass, then normalize). */
 typedef enum {
     ROWSM_AUTO = 0,
     ROWSM_SMALL = 1,
@@ -115,6 +123,9 @@ typedef struct rowsm_config {
     int32_t block;          /* LARGE: threads per block, multiple of 64, <= 1024  */
     int32_t tile_vectors;   /* LARGE: vectors per thread per tile: 2, 4, 8        */
     int32_t blocks_per_cu;  /* grid cap = blocks_per_cu * compute units           */
+    int32_t split_blocks;   /* LARGE: blocks sharing one row in the single-read
+                               form (1..64), 0 launcher's choice, -1 the
+                               two-pass streaming form                            */
 } rowsm_config;
 
 /*

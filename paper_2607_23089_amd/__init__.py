@@ -45,7 +45,8 @@ class RowsmConfig(ctypes.Structure):
     """Mirror of ``rowsm_config`` (launch overrides; 0 / packed=-1 = default)."""
     _fields_ = [(name, ctypes.c_int32) for name in (
         "variant", "vw", "lanes_per_row", "rows_per_lane", "waves_per_row",
-        "rows_per_block", "packed", "block", "tile_vectors", "blocks_per_cu")]
+        "rows_per_block", "packed", "block", "tile_vectors", "blocks_per_cu",
+        "split_blocks")]
 
     def __init__(self, **kw):
         super().__init__()

@@ -16,7 +16,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librowsm.so")
 SOURCES = [os.path.join(CSRC, "rowsm.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in
-           ("rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp")]
+           ("rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
+            "split_row.hpp")]
 
 
 def hipcc_command(out: str) -> list:

@@ -9,12 +9,15 @@
 //   MEDIUM  the row fits the registers of at most 16 waves
 //           (<= 64 fp32 values per lane, or <= 24 raw 16-byte bf16 vectors
 //           per lane in the packed form)
-//   LARGE   anything longer: two streaming passes over tiles.
+//   LARGE   anything longer: the row split over S <= 64 co-resident blocks
+//           that each hold their share in registers (single read), or, for
+//           rows too long even for that, two streaming passes over tiles.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <type_traits>
 #include <utility>
 
@@ -22,6 +25,7 @@
 #include "medium_row.hpp"
 #include "rowsm.h"
 #include "small_row.hpp"
+#include "split_row.hpp"
 
 namespace rowsm {
 namespace {
@@ -62,6 +66,7 @@ struct Plan {
   bool packed = false;
   // LARGE
   int u = 4;
+  int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
   // launch
   int block = 256;
   int64_t grid = 1;
@@ -72,9 +77,11 @@ struct Plan {
 bool vw_supported(int vw, int ib) { return vw == 1 || vw * ib == 16 || vw * ib == 8; }
 
 // Largest supported vector width that divides cols and keeps both the x and
-// the y accesses naturally aligned (16-byte loads at most).
+// the y accesses naturally aligned, with at most 16 bytes on either side: a
+// lane's output vector then never exceeds one 16-byte store, so each store
+// instruction of a wave writes one contiguous stretch of whole cache lines.
 int choose_vw(int64_t cols, int ib, int ob, uintptr_t xa, uintptr_t ya) {
-  for (int vw = 16 / ib; vw > 1; vw >>= 1) {
+  for (int vw = 16 / (ib > ob ? ib : ob); vw > 1; vw >>= 1) {
     if (!vw_supported(vw, ib)) continue;
     const int xal = vw * ib;
     const int yal = vw * ob < 16 ? vw * ob : 16;
@@ -89,13 +96,33 @@ bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; 
 
 // Fill p for the given family (AUTO resolves first) and config overrides.
 // Returns ROWSM_OK or ROWSM_EINVAL when the family cannot take this shape.
+bool pow2_upto(int v, int hi) { return v >= 1 && v <= hi && (v & (v - 1)) == 0; }
+
+// Every override must lie in its documented domain, whichever family or form
+// ends up being used.
+bool config_in_domain(const rowsm_config* c) {
+  if (!c) return true;
+  return c->variant >= ROWSM_AUTO && c->variant <= ROWSM_LARGE && c->vw >= 0 &&
+         (c->lanes_per_row == 0 || pow2_upto(c->lanes_per_row, 32)) &&
+         (c->rows_per_lane == 0 || pow2_upto(c->rows_per_lane, 8)) &&
+         (c->waves_per_row == 0 || pow2_upto(c->waves_per_row, 16)) &&
+         c->rows_per_block >= 0 && c->rows_per_block <= 16 &&
+         c->packed >= -1 && c->packed <= 1 &&
+         c->block >= 0 && c->block <= 1024 && c->block % kWave == 0 &&
+         (c->tile_vectors == 0 || c->tile_vectors == 2 || c->tile_vectors == 4 ||
+          c->tile_vectors == 8) &&
+         c->blocks_per_cu >= 0 && c->split_blocks >= -1 && c->split_blocks <= 64;
+}
+
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
              const rowsm_config* cfg, int cus, Plan* p) {
+  if (!config_in_domain(cfg)) return ROWSM_EINVAL;
   const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
   int vw = choose_vw(cols, ib, ob, xa, ya);
   if (cfg && cfg->vw > 0) {
     const int want = cfg->vw;
-    if (want > 16 / ib || (want & (want - 1)) || !vw_supported(want, ib) || cols % want ||
+    if (want > 16 / (ib > ob ? ib : ob) || (want & (want - 1)) || !vw_supported(want, ib) ||
+        cols % want ||
         xa % (want * ib) || ya % (want * ob < 16 ? want * ob : 16))
       return ROWSM_EINVAL;
     vw = want;
@@ -110,6 +137,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       variant = ROWSM_SMALL;
     } else if (nvec <= 16 * kWave * (64 / vw < 16 ? 64 / vw : 16) ||
                (in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24)) {
+      // whole row in the registers of one block
       variant = ROWSM_MEDIUM;
     } else {
       variant = ROWSM_LARGE;
@@ -193,23 +221,159 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     return ROWSM_OK;
   }
   if (variant == ROWSM_LARGE) {
+    const int want_split = cfg ? cfg->split_blocks : 0;
+    if (cfg && cfg->block > 0) {
+      const int b = cfg->block;
+      if (b % kWave || b > 1024) return ROWSM_EINVAL;
+    }
+    if (want_split >= 0) {
+      // Single-read form: T threads per block, at most 64 fp32 values per
+      // lane, S blocks per row (S <= 64: one wave polls the S peers).
+      const int T = (cfg && cfg->block > 0) ? cfg->block : 256;
+      const int nv_cap = 64 / vw < 16 ? 64 / vw : 16;
+      int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
+      if (S < 1) S = 1;
+      const int nv = (int)cdiv(nvec, (int64_t)S * T);
+      if (S <= 64 && nv <= nv_cap && nv * vw <= 64) {
+        p->split = S;
+        p->nv = nv;
+        p->vpl = nv;
+        p->block = T;
+        p->grid = 0;  // sized at launch from occupancy (cooperative launch)
+        if (bpc) p->grid = -(int64_t)bpc;  // negative: blocks-per-CU cap
+        return ROWSM_OK;
+      }
+      if (want_split > 0) return ROWSM_EINVAL;
+    }
+    p->split = 0;
     p->u = 4;
     if (cfg && cfg->tile_vectors > 0) {
       const int u = cfg->tile_vectors;
       if (u != 2 && u != 4 && u != 8) return ROWSM_EINVAL;
       p->u = u;
     }
-    p->block = 512;
-    if (cfg && cfg->block > 0) {
-      const int b = cfg->block;
-      if (b % kWave || b > 1024) return ROWSM_EINVAL;
-      p->block = b;
-    }
-    const int64_t cap = (int64_t)cus * (bpc ? bpc : 2);
+    p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
     p->grid = rows < cap ? rows : cap;
     return ROWSM_OK;
   }
   return ROWSM_EINVAL;
+}
+
+// ---- single-read split form: per-device workspace and launch ---------------
+
+constexpr int kSplitMaxBlocks = 1 << 16;  // workspace capacity in blocks
+
+// Per-device state of the split form.  The workspace (two 64-bit words per
+// block and row parity, an error count; 2 MiB) is allocated and cleared on
+// the first split launch on a device and kept until the process ends.  Split
+// launches on one device are ordered through `last` (each waits for the
+// previous one, whatever its stream), so two launches never use the
+// workspace at the same time.  Tags are handed out from `next_tag`: a launch
+// whose blocks process at most n rows each uses tags tag0 .. tag0 + n - 1,
+// so a tag is never reused while the workspace may still hold it; when the
+// 32-bit tag space runs out the workspace is cleared again and tags restart
+// at 1.
+struct SplitState {
+  std::mutex mu;
+  void* base = nullptr;
+  hipEvent_t last = nullptr;
+  bool have_last = false;
+  uint32_t next_tag = 1;
+};
+SplitState g_split[kMaxDevices];
+
+constexpr size_t kSplitWorkspaceBytes = (size_t)kSplitMaxBlocks * 32 + 256;
+
+int split_clear(void* p) {
+  if (hipMemset(p, 0, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
+  return hipDeviceSynchronize() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+}
+
+int split_workspace(int dev, SplitWorkspace* ws) {
+  SplitState& st = g_split[dev];
+  if (!st.base) {
+    void* p = nullptr;
+    if (hipMalloc(&p, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
+    if (split_clear(p) != ROWSM_OK ||
+        hipEventCreateWithFlags(&st.last, hipEventDisableTiming) != hipSuccess) {
+      (void)hipFree(p);
+      return ROWSM_EHIP;
+    }
+    st.base = p;
+    st.next_tag = 1;
+  }
+  char* b = static_cast<char*>(st.base);
+  ws->wm = reinterpret_cast<uint64_t*>(b);
+  ws->ws = reinterpret_cast<uint64_t*>(b + (size_t)kSplitMaxBlocks * 16);
+  ws->error = reinterpret_cast<uint32_t*>(b + (size_t)kSplitMaxBlocks * 32);
+  return ROWSM_OK;
+}
+
+// Reserve n consecutive tags (n >= 1); clears the workspace when the tag
+// space would wrap.
+int split_tags(SplitState& st, uint64_t n, uint32_t* tag0) {
+  if (n >= 0x80000000ull) return ROWSM_EINVAL;
+  if ((uint64_t)st.next_tag + n > 0xffffffffull) {
+    if (st.have_last && hipEventSynchronize(st.last) != hipSuccess) return ROWSM_EHIP;
+    if (split_clear(st.base) != ROWSM_OK) return ROWSM_EHIP;
+    st.next_tag = 1;
+  }
+  *tag0 = st.next_tag;
+  st.next_tag += (uint32_t)n;
+  return ROWSM_OK;
+}
+
+template <typename In, typename Out, int VW, int NV>
+int launch_split_nv(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                    hipStream_t stream, int cus) {
+  auto kern = split_row_kernel<In, Out, VW, NV>;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
+                                                   p.block, 0) != hipSuccess)
+    return ROWSM_EHIP;
+  if (p.grid < 0 && per_cu > -p.grid) per_cu = (int)-p.grid;
+  const int64_t resident = (int64_t)per_cu * cus;
+  int64_t slots = resident / p.split;
+  if (slots > rows) slots = rows;
+  if (slots > kSplitMaxBlocks / p.split) slots = kSplitMaxBlocks / p.split;
+  if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
+  const unsigned grid = (unsigned)(slots * p.split);
+
+  SplitState& st = g_split[dev];
+  std::lock_guard<std::mutex> lock(st.mu);
+  SplitWorkspace ws;
+  int r = split_workspace(dev, &ws);
+  if (r != ROWSM_OK) return r;
+  uint32_t tag0 = 0;
+  r = split_tags(st, (uint64_t)((rows + slots - 1) / slots), &tag0);
+  if (r != ROWSM_OK) return r;
+  if (st.have_last && hipStreamWaitEvent(stream, st.last, 0) != hipSuccess) return ROWSM_EHIP;
+  auto xp = static_cast<const typename In::storage*>(x);
+  auto yp = static_cast<typename Out::storage*>(y);
+  int S = p.split;
+  void* args[] = {&xp, &yp, &rows, &cols, &S, &ws, &tag0};
+  if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(grid),
+                                 dim3(p.block), args, 0, stream) != hipSuccess)
+    return ROWSM_EHIP;
+  if (hipEventRecord(st.last, stream) != hipSuccess) return ROWSM_EHIP;
+  st.have_last = true;
+  return ROWSM_OK;
+}
+
+template <typename In, typename Out, int VW, int... NVs>
+int launch_split_seq(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                     hipStream_t st, int cus, std::integer_sequence<int, NVs...>) {
+  int r = ROWSM_EINVAL;
+  (void)((p.nv == NVs + 1 && NVs + 1 <= 16 && (NVs + 1) * VW <= 64
+              ? (r = launch_split_nv < In, Out, VW,
+                 ((NVs + 1) * VW <= 64 ? NVs + 1 : 1) > (p, x, y, rows, cols, st, cus),
+                 true)
+              : false) ||
+         ...);
+  return r;
 }
 
 // ---- template dispatch ------------------------------------------------------
@@ -300,6 +464,26 @@ bool launch_io(const Plan& p, const void* x, void* y, int64_t rows, int cols,
   return false;
 }
 
+template <typename In, typename Out>
+int launch_split_io(const Plan& p, const void* x, void* y, int64_t rows, int cols,
+                    hipStream_t st, int cus) {
+  constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
+  auto seq = std::make_integer_sequence<int, 16>{};
+  if (p.vw == 1) return launch_split_seq<In, Out, 1>(p, x, y, rows, cols, st, cus, seq);
+  if (p.vw == V8) return launch_split_seq<In, Out, V8>(p, x, y, rows, cols, st, cus, seq);
+  if (p.vw == V16) return launch_split_seq<In, Out, V16>(p, x, y, rows, cols, st, cus, seq);
+  return ROWSM_EINVAL;
+}
+
+int launch_split(const Plan& p, int in_dt, int out_dt, const void* x, void* y, int64_t rows,
+                 int cols, hipStream_t st, int cus) {
+  if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32)
+    return launch_split_io<F32, F32>(p, x, y, rows, cols, st, cus);
+  if (in_dt == ROWSM_F32) return launch_split_io<F32, BF16>(p, x, y, rows, cols, st, cus);
+  if (out_dt == ROWSM_F32) return launch_split_io<BF16, F32>(p, x, y, rows, cols, st, cus);
+  return launch_split_io<BF16, BF16>(p, x, y, rows, cols, st, cus);
+}
+
 // Returns false when no compiled kernel matches the plan (no launch made).
 bool launch(const Plan& p, int in_dt, int out_dt, const void* x, void* y, int64_t rows,
             int cols, hipStream_t st) {
@@ -340,11 +524,14 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   bool noop = false;
   int st = validate(x, y, rows, cols, in_dt, out_dt, true, &noop);
   if (st != ROWSM_OK || noop) return st;
-  if (cfg && (cfg->variant < ROWSM_AUTO || cfg->variant > ROWSM_LARGE)) return ROWSM_EINVAL;
   Plan p;
-  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, cu_count(), &p);
+  const int cus = cu_count();
+  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, cus, &p);
   if (st != ROWSM_OK) return st;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
+  if (p.variant == ROWSM_LARGE && p.split > 0)
+    return launch_split(p, in_dt, out_dt, x, y, rows, (int)cols,
+                        static_cast<hipStream_t>(stream), cus);
   if (!launch(p, in_dt, out_dt, x, y, rows, (int)cols, static_cast<hipStream_t>(stream)))
     return ROWSM_EINVAL;  // no compiled kernel for this plan: nothing was enqueued
   return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
@@ -420,9 +607,11 @@ extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_
     } else {
       std::snprintf(buf, (size_t)len,
                     "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
-                    "block=%d grid=%lld (grid assumes 256 CUs)",
+                    "split=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
-                    (int)p.packed, p.u, p.block, (long long)p.grid);
+                    (int)p.packed, p.u, p.split, p.block, (long long)(p.split ? 0 : p.grid),
+                    p.split ? "cooperative grid sized from occupancy at launch"
+                            : "grid assumes 256 CUs");
     }
   }
   return st;

@@ -1,0 +1,177 @@
+// Split-row softmax kernel: one row spread over S co-resident blocks, each
+// holding its share in registers, so x is read once even when a row is far
+// larger than one compute unit's registers.
+//
+// Layout.  The S blocks of a row act as one group of S*T threads (T threads
+// per block): global thread g = c*T + t of block c owns the vectors
+// g, g + S*T, ..., g + (NV-1) S*T of the row, NV = ceil(nvec / (S*T)) fixed at
+// compile time, so only the last slot can be partial and every load
+// instruction of a wave reads 64 consecutive vectors.
+//
+// Statistics.  Each block reduces its share to a pair (m_b, s_b): m_b the
+// block's maximum and s_b = sum exp(x - m_b) over its entries (a block that
+// holds only -inf reports (-inf, 0)).  The pairs are exchanged through global
+// memory and merged, in block order, with the online identity
+//     M = max_b m_b,  S = sum_b s_b * exp(m_b - M),
+// and the block writes y = exp(x - m_b) * exp(m_b - M) / S from the values it
+// still holds.  One exchange per row.
+//
+// Exchange protocol (per device workspace, reused across launches).  Each
+// block publishes its pair as two self-validating 64-bit words
+//     wm[b][k & 1] = (tag << 32) | bits(m_b),   ws[b][k & 1] = (tag << 32) | bits(s_b)
+// with relaxed agent-scope atomic stores, where k counts the rows this block
+// has processed in this launch and tag = tag0 + k is unique to (launch, k)
+// (the host hands out tags; tag 0 never occurs, and fresh memory is zero).
+// A peer polls both words with relaxed agent-scope atomic loads until their
+// tags match: a 64-bit atomic access is indivisible, so a word with the
+// expected tag carries the right value and no ordering between the two
+// stores, and no cache write-back or invalidation, is needed.  Two slots per
+// block (k & 1) suffice: a block can only rewrite slot k & 1 at row k + 2,
+// after every block of the group has published row k + 1, i.e. after all of
+// them have read row k's words.
+//
+// Co-residency.  The launch is cooperative: every block of the grid is
+// resident at once, so a block only ever waits for peers that are running
+// and publish before they wait.  The wait is still bounded; a block that
+// gives up records the failure in the workspace and carries on, so the grid
+// always drains.
+#pragma once
+
+#include "rowsm_device.hpp"
+
+namespace rowsm {
+
+// Workspace layout (device memory, zeroed when it is created).
+struct SplitWorkspace {
+  uint64_t* wm;     // [max_blocks][2]: (tag << 32) | bits(block max)
+  uint64_t* ws;     // [max_blocks][2]: (tag << 32) | bits(block sum)
+  uint32_t* error;  // [1]: number of waits that gave up
+};
+
+// Polls before a wait gives up (about a second at the load latency of an
+// agent-scope poll).  A lane that gave up once never waits again in this
+// launch, so even a broken exchange lets the whole grid drain quickly.
+constexpr uint32_t kSplitSpinLimit = 1u << 20;
+
+template <typename In, typename Out, int VW, int NV>
+__global__ __launch_bounds__(1024) void split_row_kernel(
+    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
+    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0) {
+  __shared__ float red_m[16];
+  __shared__ float red_s[16];
+  __shared__ float bcast[2];
+
+  const int T = blockDim.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int nwaves = T / kWave;
+  const int c = blockIdx.x % S;                 // chunk of the row
+  const int q = blockIdx.x / S;                 // row slot
+  const int64_t slots = gridDim.x / S;
+  const int RT = S * T;
+  const int g = c * T + threadIdx.x;
+  const int nvec = cols / VW;
+  const bool last_ok = (NV - 1) * RT + g < nvec;
+  const uint32_t vin = (uint32_t)g * (VW * In::bytes);
+  const uint32_t vout = (uint32_t)g * (VW * Out::bytes);
+  const uint32_t sin = (uint32_t)RT * (VW * In::bytes);
+  const uint32_t sout = (uint32_t)RT * (VW * Out::bytes);
+  const float ninf = -__builtin_inff();
+
+  bool gave_up = false;  // per lane of the first wave
+  uint32_t k = 0;
+  for (int64_t row = q; row < rows; row += slots, ++k) {
+    const rsrc_t rx = make_rsrc(x + row * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * Out::bytes);
+
+    float f[NV][VW];
+    {
+      InVec<In, VW> v[NV];
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        if (s < NV - 1 || last_ok) v[s].load(rx, vin, s * sin);
+        else v[s].set_neg_inf();
+      }
+#pragma unroll
+      for (int s = 0; s < NV; ++s) v[s].to_float(f[s]);
+    }
+
+    // Block maximum.
+    float mb = ninf;
+#pragma unroll
+    for (int s = 0; s < NV; ++s)
+#pragma unroll
+      for (int i = 0; i < VW; ++i) mb = fmax_nn(mb, f[s][i]);
+    mb = group_reduce<kWave, MaxOp>(mb);
+    if (lane == 0) red_m[wave] = mb;
+    __syncthreads();
+    mb = red_m[0];
+    for (int w = 1; w < nwaves; ++w) mb = fmax_nn(mb, red_m[w]);
+
+    // Block sum relative to the block maximum.
+    const float nml = (mb == ninf) ? 0.0f : -mb * kLog2e;
+    float sb = 0.0f;
+#pragma unroll
+    for (int s = 0; s < NV; ++s)
+#pragma unroll
+      for (int i = 0; i < VW; ++i) {
+        f[s][i] = exp2_fast(__builtin_fmaf(f[s][i], kLog2e, nml));
+        sb += f[s][i];
+      }
+    sb = group_reduce<kWave, SumOp>(sb);
+    if (lane == 0) red_s[wave] = sb;
+    __syncthreads();
+    sb = red_s[0];
+    for (int w = 1; w < nwaves; ++w) sb += red_s[w];
+
+    // Exchange with the other blocks of the row (first wave only).
+    if (wave == 0) {
+      const uint32_t b0 = (uint32_t)q * S;
+      const uint64_t tag = (uint64_t)(tag0 + k) << 32;
+      const uint32_t slot = k & 1;
+      if (lane == 0) {
+        __hip_atomic_store(&w.wm[2 * (b0 + c) + slot], tag | __float_as_uint(mb),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(sb),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      MaxSum p = {ninf, 0.0f};
+      if (lane < S) {
+        const uint32_t i = 2 * (b0 + lane) + slot;
+        uint64_t vm = 0, vs = 0;
+        uint32_t spins = 0;
+        while (!gave_up) {
+          vm = __hip_atomic_load(&w.wm[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          vs = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if ((vm & ~0xffffffffull) == tag && (vs & ~0xffffffffull) == tag) break;
+          __builtin_amdgcn_s_sleep(1);
+          if (++spins == kSplitSpinLimit) {
+            __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            gave_up = true;
+          }
+        }
+        p = {__uint_as_float((uint32_t)vm), __uint_as_float((uint32_t)vs)};
+      }
+      p = group_merge<kWave>(p);  // fixed lane order: deterministic
+      if (lane == 0) {
+        // y = exp(x - m_b) * exp(m_b - M) / S
+        bcast[0] = exp2_fast((mb - p.m) * kLog2e) * __builtin_amdgcn_rcpf(p.s);
+      }
+    }
+    __syncthreads();
+    const float scale = bcast[0];
+
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+#pragma unroll
+      for (int i = 0; i < VW; ++i) f[s][i] *= scale;
+      if (s < NV - 1 || last_ok) store_out<Out, VW>(ry, vout + s * sout, f[s]);
+    }
+    // LDS reuse across rows: red_m is rewritten after this row's last barrier,
+    // which every wave passes only after reading red_m (before the second
+    // barrier); red_s and bcast are rewritten after the next row's first and
+    // second barriers, which every wave reaches only after reading them here.
+  }
+}
+
+}  // namespace rowsm

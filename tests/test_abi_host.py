@@ -52,7 +52,8 @@ def test_status_strings(lib):
 
 
 # Fake, never-dereferenced addresses: every call below must be rejected (or be
-# a no-op) before the library makes any HIP call.
+# a no-op) before the library makes any HIP call.  A case that would pass
+# validation must never be added here: it would launch on these addresses.
 X, Y = 0x7f0000000000, 0x7f8000000000
 
 
@@ -85,7 +86,11 @@ def test_bad_variant_and_config(lib):
            dict(variant=R.SMALL, rows_per_lane=3), dict(variant=R.MEDIUM, waves_per_row=3),
            dict(variant=R.MEDIUM, waves_per_row=4, rows_per_block=8),
            dict(variant=R.LARGE, block=100), dict(variant=R.LARGE, tile_vectors=3),
+           dict(variant=R.LARGE, block=2048), dict(variant=R.SMALL, rows_per_block=17),
+           dict(variant=R.LARGE, split_blocks=-2), dict(variant=R.MEDIUM, packed=2),
+           dict(variant=R.SMALL, blocks_per_cu=-1), dict(variant=7),
            dict(variant=R.AUTO, vw=3), dict(variant=R.AUTO, vw=2),
+           dict(variant=R.LARGE, split_blocks=65),
            dict(variant=R.MEDIUM, packed=1, waves_per_row=16)]
     for cfg in bad:
         st = R.rowsm_forward_config(X, Y, 64, 64, R.BF16, R.BF16, 0, R.RowsmConfig(**cfg))
@@ -109,8 +114,10 @@ def test_select_regimes(lib):
     assert s(10, 65536, R.F32, R.F32) == R.MEDIUM
     assert s(10, 65540, R.F32, R.F32) == R.LARGE
     assert s(10, 65536, R.BF16, R.BF16) == R.MEDIUM
-    # packed bf16 rows up to 16 x 64 x 24 vectors of 8
-    assert s(4096, 151936, R.BF16, R.F32) == R.MEDIUM
+    # packed bf16 rows up to 16 x 64 x 24 vectors of 8 (bf16 -> bf16 only:
+    # bf16 -> f32 uses 4-element vectors so that each store is 16 bytes)
+    assert s(10, 151936, R.BF16, R.BF16) == R.MEDIUM
+    assert s(4096, 151936, R.BF16, R.F32) == R.LARGE
     assert s(10, 196608, R.BF16, R.BF16) == R.MEDIUM
     assert s(10, 196616, R.BF16, R.BF16) == R.LARGE
     assert s(1024, 262144, R.F32, R.F32) == R.LARGE
@@ -124,10 +131,16 @@ def test_describe(lib):
     assert st == R.OK and text.startswith("small") and "lpr=8" in text and "vw=8" in text
     st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("medium")
-    st, text = R.rowsm_describe(4096, 151936, R.BF16, R.F32)
+    st, text = R.rowsm_describe(64, 151936, R.BF16, R.BF16)
     assert st == R.OK and "packed=1" in text and "vpl=19" in text and "wpr=16" in text
+    st, text = R.rowsm_describe(4096, 151936, R.BF16, R.F32)
+    assert st == R.OK and text.startswith("large") and "vw=4" in text and "split=10" in text
+    assert "nv=15" in text
     st, text = R.rowsm_describe(1024, 262144, R.F32, R.F32, R.LARGE)
-    assert st == R.OK and text.startswith("large")
+    assert st == R.OK and text.startswith("large") and "split=16" in text and "nv=16" in text
+    cfg_two_pass = R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
+    st = R.rowsm_forward_config(X, Y, 4, 8, 7, R.F32, 0, cfg_two_pass)
+    assert st == R.EDTYPE
     st, text = R.rowsm_describe(4, 4096, R.F32, R.F32, R.SMALL)
     assert st == R.EINVAL and text.startswith("error")
     st, text = R.rowsm_describe(0, 4096, R.F32, R.F32)

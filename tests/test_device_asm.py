@@ -62,14 +62,27 @@ def test_no_immediate_overwrite_of_store_data(asm):
     r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4E",        # small_262144x64
     r"medium_row_kernelINS_4BF16ES1_Li8ELi4ELb0E",       # causal_32768x4096
     r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0E",        # fp32_64x1000
-    r"medium_row_kernelINS_4BF16ENS_3F32ELi8ELi19ELb1E",  # vocab_4096x151936
-    r"large_row_kernelINS_3F32ES1_Li4ELi4E",             # large_1024x262144
+    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi15E",      # vocab_4096x151936
+    r"split_row_kernelINS_3F32ES1_Li4ELi16E",            # large_1024x262144
+    r"large_row_kernelINS_3F32ES1_Li4ELi4E",             # two-pass form
 ])
 def test_workload_kernels_do_not_spill(asm, pattern):
     ks = {k: v for k, v in kernels(asm).items() if re.search(pattern, k)}
     assert len(ks) == 1, pattern
     body = next(iter(ks.values()))
     assert int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", body).group(1)) == 0
+
+
+def test_split_exchange_has_no_cache_maintenance(asm):
+    # The exchange words are self-validating 64-bit atomics: no L2 write-back
+    # or invalidation may appear in the split kernel (each one serialises the
+    # whole device), and the polls and stores are device-coherent (sc1).
+    body = asm[asm.index("split_row_kernelINS_3F32ES1_Li4ELi16E"):]
+    body = body[:body.index("s_endpgm")]
+    assert "buffer_wbl2" not in body and "buffer_inv" not in body
+    assert "s_sleep" in body
+    assert re.search(r"global_store_dwordx2 .* sc1", body)
+    assert re.search(r"global_load_dwordx2 .* sc1", body)
 
 
 def test_expected_instructions(asm):

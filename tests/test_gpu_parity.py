@@ -145,14 +145,21 @@ def test_empty_and_degenerate():
     dict(variant=R.MEDIUM, waves_per_row=2, blocks_per_cu=1),
     dict(variant=R.MEDIUM, waves_per_row=16),
     dict(variant=R.MEDIUM, waves_per_row=4, rows_per_block=3, blocks_per_cu=1),
-    dict(variant=R.LARGE, block=256, tile_vectors=8, blocks_per_cu=1),
-    dict(variant=R.LARGE, block=1024, tile_vectors=2),
-    dict(variant=R.LARGE, block=64, tile_vectors=4, blocks_per_cu=1),
+    dict(variant=R.LARGE, split_blocks=-1, block=256, tile_vectors=8, blocks_per_cu=1),
+    dict(variant=R.LARGE, split_blocks=-1, block=1024, tile_vectors=2),
+    dict(variant=R.LARGE, split_blocks=-1, block=64, tile_vectors=4, blocks_per_cu=1),
+    dict(variant=R.LARGE, split_blocks=1, block=1024),
+    dict(variant=R.LARGE, split_blocks=2, block=1024),
+    dict(variant=R.LARGE, split_blocks=7, block=128, blocks_per_cu=1),
+    dict(variant=R.LARGE, split_blocks=64, block=64),
+    dict(variant=R.LARGE, blocks_per_cu=1),
 ])
 def test_launch_overrides(cfg):
     # Overrides change the launch shape, never the result; blocks_per_cu=1
     # makes every block loop over several rows or row groups.
     cols = {R.SMALL: 64, R.MEDIUM: 3000, R.LARGE: 20000}[cfg["variant"]]
+    if cfg.get("split_blocks", 0) >= 1:
+        cols = 40000
     for din, dout in (("bf16", "bf16"), ("f32", "f32")):
         rows = 2500 if cfg["variant"] != R.LARGE else 600
         x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols)
@@ -163,7 +170,7 @@ def test_launch_overrides(cfg):
 def test_deterministic_and_bounded_writes():
     # Same input twice -> bitwise-identical output; nothing written outside y;
     # x untouched.
-    for fam, cols in ((R.SMALL, 64), (R.MEDIUM, 4096), (R.MEDIUM, 151936), (R.LARGE, 262144)):
+    for fam, cols in ((R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 151936), (R.LARGE, 262144)):
         rows = max(2, 2_000_000 // cols)
         x = W.random_matrix(rows, cols, "bf16", sigma=8.0, seed=5).to(DEV)
         x_before = x.clone()
@@ -176,6 +183,39 @@ def test_deterministic_and_bounded_writes():
         assert torch.equal(y1, y2), R.VARIANT_NAMES[fam]
         assert torch.all(buf[:guard] == -123.0) and torch.all(buf[guard + n:] == -123.0)
         assert torch.equal(x, x_before)
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+def test_two_pass_large_form(din, dout):
+    # The streaming two-pass form is the fallback for rows too long for the
+    # split form; check it on its own over widths with ragged tiles.
+    for cols in (5, 4097, 70001, 262144):
+        rows = 3 if cols > 100000 else 9
+        x = W.random_matrix(rows, cols, din, sigma=5.0, seed=cols + 1)
+        cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
+        y = run(x.to(DEV), dout, config=cfg)
+        assert_parity(x, y, dout, f"two-pass {rows}x{cols} {din}->{dout}")
+
+
+def test_split_many_launches_and_streams():
+    # Consecutive split launches (new epoch each) on alternating streams reuse
+    # the device workspace; each result must be exact, and repeated launches
+    # on the same data bitwise equal.
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    xs = [W.random_matrix(37, 33000 + 8 * i, "bf16", sigma=4.0, seed=i).to(DEV)
+          for i in range(4)]
+    ys = []
+    for it in range(12):
+        s = s1 if it % 2 == 0 else s2
+        x = xs[it % 4]
+        with torch.cuda.stream(s):
+            ys.append(R.softmax(x, out_dtype=torch.float32, variant=R.LARGE, stream=s))
+    torch.cuda.synchronize()
+    for it, y in enumerate(ys):
+        if it < 4:
+            assert_parity(xs[it].cpu(), y, "f32", f"split launch {it}")
+        else:
+            assert torch.equal(y, ys[it % 4])
 
 
 def test_streams():
