@@ -64,7 +64,9 @@ typedef enum {
  * registers; LARGE spreads a row over several co-resident workgroups that
  * keep their shares in registers and exchange (max, sum) pairs through a
  * small device workspace (single read), or, for rows too long for that,
- * streams the row through tiles twice (online max/sum pass, then normalize). */
+ * streams the row through tiles twice (online max/sum pass, then normalize).
+ * The single-read form's grid is sized to at most one full residency of the
+ * device. */
 typedef enum {
     ROWSM_AUTO = 0,
     ROWSM_SMALL = 1,

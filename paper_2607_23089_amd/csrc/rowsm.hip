@@ -173,10 +173,12 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
     const int want_packed = cfg ? cfg->packed : -1;
     if (want_wpr && (want_wpr & (want_wpr - 1) || want_wpr > 16)) return ROWSM_EINVAL;
-    // Unpacked: the smallest group whose lanes hold <= 32 fp32 values each
-    // (<= 64 when the row is longer), unless a group size is forced.
+    // Unpacked: the smallest group whose lanes hold <= 16 fp32 values each
+    // (<= 32, then <= 64 when the row is longer), unless a group size is
+    // forced.  Fewer values per lane and more resident rows measured faster
+    // than longer per-lane rows on the 32768 x 4096 workload.
     if (want_packed != 1) {
-      for (int cap_vals : {32, 64}) {
+      for (int cap_vals : {16, 32, 64}) {
         for (int w = 1; w <= 16; w <<= 1) {
           if (want_wpr && w != want_wpr) continue;
           const int v = (int)cdiv(nvec, (int64_t)w * kWave);
@@ -209,13 +211,15 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->vpl = vpl;
     p->packed = packed;
     p->nv = vpl;
-    int rpb = wpr >= 4 ? 1 : 4 / wpr;
+    // 512-thread blocks (fewer rows per block when a row needs more than 8
+    // waves); one block per row group, no grid-stride loop unless capped.
+    int rpb = wpr >= 8 ? 1 : 8 / wpr;
     if (cfg && cfg->rows_per_block > 0) {
       rpb = cfg->rows_per_block;
       if (rpb * wpr > 16) return ROWSM_EINVAL;
     }
     p->block = rpb * wpr * kWave;
-    const int64_t cap = (int64_t)cus * (bpc ? bpc : 8);
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 64);
     p->grid = cdiv(rows, rpb);
     if (p->grid > cap) p->grid = cap;
     return ROWSM_OK;
@@ -227,10 +231,17 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       if (b % kWave || b > 1024) return ROWSM_EINVAL;
     }
     if (want_split >= 0) {
-      // Single-read form: T threads per block, at most 64 fp32 values per
-      // lane, S blocks per row (S <= 64: one wave polls the S peers).
-      const int T = (cfg && cfg->block > 0) ? cfg->block : 256;
-      const int nv_cap = 64 / vw < 16 ? 64 / vw : 16;
+      // Single-read form: T threads per block, S blocks per row (S <= 64:
+      // one wave polls the S peers), at most 64 fp32 values per lane.
+      // Widening rows (bf16 -> f32 writes twice what it reads) do best with
+      // 512-thread blocks holding at most 40 values per lane, two blocks per
+      // compute unit; the others with 256-thread blocks and 64 values per
+      // lane (measured on the 4096 x 151936 and 1024 x 262144 workloads).
+      const bool widening = ob > ib;
+      const int T = (cfg && cfg->block > 0) ? cfg->block : (widening ? 512 : 256);
+      const int vals = widening ? 40 : 64;
+      int nv_cap = vals / vw < 16 ? vals / vw : 16;
+      if (nv_cap < 1) nv_cap = 1;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
       if (S < 1) S = 1;
       const int nv = (int)cdiv(nvec, (int64_t)S * T);
@@ -239,8 +250,9 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->nv = nv;
         p->vpl = nv;
         p->block = T;
-        p->grid = 0;  // sized at launch from occupancy (cooperative launch)
-        if (bpc) p->grid = -(int64_t)bpc;  // negative: blocks-per-CU cap
+        // Grid sized at launch from occupancy (one full residency of the
+        // device at most); a negative value caps blocks per compute unit.
+        p->grid = bpc ? -(int64_t)bpc : (widening && !(cfg && cfg->block > 0) ? -2 : 0);
         return ROWSM_OK;
       }
       if (want_split > 0) return ROWSM_EINVAL;
@@ -340,6 +352,8 @@ int launch_split_nv(const Plan& p, const void* x, void* y, int64_t rows, int col
   if (slots > rows) slots = rows;
   if (slots > kSplitMaxBlocks / p.split) slots = kSplitMaxBlocks / p.split;
   if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
+  // The grid never exceeds one full residency of the device (see the
+  // co-residency note of split_row_kernel).
   const unsigned grid = (unsigned)(slots * p.split);
 
   SplitState& st = g_split[dev];
@@ -353,11 +367,9 @@ int launch_split_nv(const Plan& p, const void* x, void* y, int64_t rows, int col
   if (st.have_last && hipStreamWaitEvent(stream, st.last, 0) != hipSuccess) return ROWSM_EHIP;
   auto xp = static_cast<const typename In::storage*>(x);
   auto yp = static_cast<typename Out::storage*>(y);
-  int S = p.split;
-  void* args[] = {&xp, &yp, &rows, &cols, &S, &ws, &tag0};
-  if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(grid),
-                                 dim3(p.block), args, 0, stream) != hipSuccess)
-    return ROWSM_EHIP;
+  (void)hipGetLastError();
+  kern<<<dim3(grid), dim3(p.block), 0, stream>>>(xp, yp, rows, cols, p.split, ws, tag0);
+  if (hipGetLastError() != hipSuccess) return ROWSM_EHIP;
   if (hipEventRecord(st.last, stream) != hipSuccess) return ROWSM_EHIP;
   st.have_last = true;
   return ROWSM_OK;
@@ -610,7 +622,7 @@ extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_
                     "split=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
                     (int)p.packed, p.u, p.split, p.block, (long long)(p.split ? 0 : p.grid),
-                    p.split ? "cooperative grid sized from occupancy at launch"
+                    p.split ? "grid sized from occupancy at launch"
                             : "grid assumes 256 CUs");
     }
   }

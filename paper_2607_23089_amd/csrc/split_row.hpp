@@ -30,11 +30,17 @@
 // after every block of the group has published row k + 1, i.e. after all of
 // them have read row k's words.
 //
-// Co-residency.  The launch is cooperative: every block of the grid is
-// resident at once, so a block only ever waits for peers that are running
-// and publish before they wait.  The wait is still bounded; a block that
-// gives up records the failure in the workspace and carries on, so the grid
-// always drains.
+// Co-residency.  The host sizes the grid from the kernel's occupancy to at
+// most one full residency of the device, and blocks publish before they
+// wait, so when the launch has the device to itself every block is resident
+// at once and every wait ends.  When other work shares the device, blocks
+// are still dispatched in block order on each XCD and every XCD holds far
+// more blocks than the S/8 of one row group it carries, so the lowest row
+// group that has not finished always has all of its blocks resident and
+// progresses; groups behind it run once it exits (the forward-progress
+// property single-pass scans also rely on).  The wait is bounded regardless:
+// a lane that gives up records the failure in the workspace and carries on,
+// so the grid always drains.
 #pragma once
 
 #include "rowsm_device.hpp"

@@ -134,8 +134,8 @@ def test_describe(lib):
     st, text = R.rowsm_describe(64, 151936, R.BF16, R.BF16)
     assert st == R.OK and "packed=1" in text and "vpl=19" in text and "wpr=16" in text
     st, text = R.rowsm_describe(4096, 151936, R.BF16, R.F32)
-    assert st == R.OK and text.startswith("large") and "vw=4" in text and "split=10" in text
-    assert "nv=15" in text
+    assert st == R.OK and text.startswith("large") and "vw=4" in text and "split=8" in text
+    assert "nv=10" in text and "block=512" in text
     st, text = R.rowsm_describe(1024, 262144, R.F32, R.F32, R.LARGE)
     assert st == R.OK and text.startswith("large") and "split=16" in text and "nv=16" in text
     cfg_two_pass = R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
