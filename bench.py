@@ -33,8 +33,9 @@ sys.path.insert(0, ROOT)
 METRIC = "row-softmax achieved HBM GB/s and % of MI355X peak, per row-length regime"
 PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+# Device code of the kernels; a profile also records each launch's shape.
 KERNEL_SOURCES = ["rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
-                  "split_row.hpp", "rowsm.hip"]
+                  "split_row.hpp"]
 
 
 def kernel_source_hash() -> str:
@@ -45,9 +46,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(regime: str):
+def measured_traffic(regime: str, launch: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when there is none or the kernels changed since it was taken."""
+    None when there is none, or the kernels' device code or this launch's
+    shape changed since it was taken."""
     try:
         with open(PROFILE_COUNTERS) as f:
             prof = json.load(f)
@@ -56,7 +58,9 @@ def measured_traffic(regime: str):
     if prof.get("kernel_source_hash") != kernel_source_hash():
         return None
     ent = prof.get("regimes", {}).get(regime)
-    return None if ent is None else ent.get("hbm_bytes_per_launch")
+    if ent is None or ent.get("launch") != launch:
+        return None
+    return ent.get("hbm_bytes_per_launch")
 
 
 def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
@@ -194,8 +198,11 @@ def main() -> int:
             "avg_us": avg * 1e3, "median_us": ms[len(ms) // 2] * 1e3,
             "min_us": ms[0] * 1e3,
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
-            "hbm_bytes_per_launch": measured_traffic(name),
+            "hbm_bytes_per_launch": measured_traffic(name, desc),
         }
+    failures = R.rowsm_split_wait_failures()
+    if failures != 0:
+        raise R.RowsmError(f"{failures} split-row exchange waits gave up: results invalid")
     dom = max(per, key=lambda n: per[n]["avg_us"])
     d = per[dom]
     value = step_bytes / (wall / args.steps) / 1e9

@@ -151,6 +151,15 @@ int rowsm_forward_config(const void *x, void *y, int64_t rows, int64_t cols,
 int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
                    int variant, char *buf, int64_t len);
 
+/*
+ * rowsm_split_wait_failures: diagnostics of the single-read LARGE form on
+ * the current device.  Waits for the last such launch to finish, then returns
+ * how many exchange waits have given up since the workspace was created (0
+ * when every row's blocks met; a non-zero count means some rows of some
+ * launch are wrong), 0 when no such launch has run, or ROWSM_EHIP.
+ */
+int64_t rowsm_split_wait_failures(void);
+
 /* rowsm_status_string: static, human-readable text for a rowsm_status. */
 const char *rowsm_status_string(int status);
 

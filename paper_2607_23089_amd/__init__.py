@@ -13,6 +13,7 @@ Raw entry points (same names and arguments as the C ABI; pointers are ints,
     rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, cfg)
     rowsm_select(rows, cols, in_dtype, out_dtype) -> variant or status
     rowsm_describe(rows, cols, in_dtype, out_dtype, variant) -> (status, text)
+    rowsm_split_wait_failures() -> count (diagnostics of the split LARGE form)
     rowsm_status_string(status) -> str
 
 Tensor helper: ``softmax(x, out_dtype=None, out=None, ...)`` for torch tensors
@@ -34,7 +35,8 @@ LIB_PATH = os.path.join(_PKG, "librowsm.so")
 
 # Symbols declared in include/rowsm.h.
 EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
-           "rowsm_forward_config", "rowsm_describe", "rowsm_status_string")
+           "rowsm_forward_config", "rowsm_describe", "rowsm_split_wait_failures",
+           "rowsm_status_string")
 
 
 class RowsmError(RuntimeError):
@@ -85,6 +87,8 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     h.rowsm_select.restype = i32
     h.rowsm_describe.argtypes = [i64, i64, i32, i32, i32, ctypes.c_char_p, i64]
     h.rowsm_describe.restype = i32
+    h.rowsm_split_wait_failures.argtypes = []
+    h.rowsm_split_wait_failures.restype = i64
     h.rowsm_status_string.argtypes = [i32]
     h.rowsm_status_string.restype = ctypes.c_char_p
     if path is None:
@@ -116,6 +120,10 @@ def rowsm_describe(rows, cols, in_dtype, out_dtype, variant=AUTO):
     buf = ctypes.create_string_buffer(256)
     st = lib().rowsm_describe(rows, cols, in_dtype, out_dtype, variant, buf, len(buf))
     return st, buf.value.decode()
+
+
+def rowsm_split_wait_failures() -> int:
+    return lib().rowsm_split_wait_failures()
 
 
 def rowsm_status_string(status) -> str:

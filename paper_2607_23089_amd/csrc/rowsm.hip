@@ -629,6 +629,21 @@ extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_
   return st;
 }
 
+extern "C" int64_t rowsm_split_wait_failures(void) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
+  SplitState& st = g_split[dev];
+  std::lock_guard<std::mutex> lock(st.mu);
+  if (!st.base) return 0;  // no split launch on this device yet
+  if (st.have_last && hipEventSynchronize(st.last) != hipSuccess) return ROWSM_EHIP;
+  uint32_t n = 0;
+  const char* b = static_cast<const char*>(st.base);
+  if (hipMemcpy(&n, b + (size_t)kSplitMaxBlocks * 32, sizeof(n), hipMemcpyDeviceToHost) !=
+      hipSuccess)
+    return ROWSM_EHIP;
+  return (int64_t)n;
+}
+
 extern "C" const char* rowsm_status_string(int status) {
   switch (status) {
     case ROWSM_OK: return "ok";

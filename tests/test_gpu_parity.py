@@ -216,6 +216,7 @@ def test_split_many_launches_and_streams():
             assert_parity(xs[it].cpu(), y, "f32", f"split launch {it}")
         else:
             assert torch.equal(y, ys[it % 4])
+    assert R.rowsm_split_wait_failures() == 0
 
 
 def test_streams():
