@@ -11,6 +11,9 @@ Contents
                          last dimension, which is what PyTorch's reference
                          computes (the paper judges every operator against a
                          PyTorch reference: Evaluation, Experimental Setup).
+  * ``softmax_scaled_causal_f64`` -- the same definition applied to
+                         scale * x with a causal mask from the indices
+                         (scaled attention scores).
   * ``widen_f32`` / ``widen_bf16_bits`` -- exact widening of the stored input
                          bit patterns to fp64 (bf16 -> bits << 16 -> fp32 ->
                          fp64), so the oracle sees exactly the values the GPU
@@ -67,6 +70,11 @@ def load(path: str | None = None):
     fn.restype = ctypes.c_int
     fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                    ctypes.c_int64, ctypes.c_int]
+    fn = lib.oracle_softmax_scaled_causal_f64
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_int64, ctypes.c_double, ctypes.c_int64,
+                   ctypes.c_int64, ctypes.c_int]
     if path == _LIB:
         _lib = lib
     return lib
@@ -88,6 +96,33 @@ def softmax_f64(x: np.ndarray, threads: int = 1, lib=None) -> np.ndarray:
     if rc != 0:
         raise RuntimeError(f"oracle_softmax_f64 failed with status {rc}")
     return y.reshape(shape)
+
+
+def softmax_scaled_causal_f64(x: np.ndarray, scale: float, period: int, offset: int,
+                              threads: int = 1, lib=None, row0: int = 0) -> np.ndarray:
+    """y = softmax(scale * x + mask) per row, mask(r, c) = -inf where
+    period > 0 and c > ((row0 + r) mod period) + offset (row0: index of the
+    first given row in the full matrix, so that samples keep their mask)."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    if x.ndim == 1:
+        x = x[None, :]
+    rows, cols = x.shape
+    y = np.full_like(x, np.nan)
+    lib = lib if lib is not None else load()
+    if row0 == 0:
+        rc = lib.oracle_softmax_scaled_causal_f64(x.ctypes.data, y.ctypes.data, rows, cols,
+                                                  float(scale), int(period), int(offset),
+                                                  int(threads))
+    else:  # shift the offset so row r sees its row0 + r query
+        rc = 0
+        for r in range(rows):
+            q = (row0 + r) % period if period > 0 else 0
+            rc |= lib.oracle_softmax_scaled_causal_f64(
+                x[r].ctypes.data, y[r].ctypes.data, 1, cols, float(scale), 1 if period > 0 else 0,
+                q + int(offset) if period > 0 else 0, 1)
+    if rc != 0:
+        raise RuntimeError(f"oracle_softmax_scaled_causal_f64 failed with status {rc}")
+    return y
 
 
 def widen_f32(x: np.ndarray) -> np.ndarray:

@@ -56,18 +56,90 @@ static void oracle_row(const double *x, double *y, int64_t cols)
         y[j] = y[j] / s;
 }
 
+/*
+ * Scaled, causally masked rows (attention scores): row r is treated as query
+ * q = r mod period, and column c survives when c <= q + offset; the others
+ * are -inf.  The row is t_j = scale * x_j for surviving columns, -inf
+ * otherwise, and the result is the plain definition above applied to t.
+ * period == 0 means no mask.  Written out element by element into a scratch
+ * row so that the definition above is applied unchanged.
+ */
+static void oracle_row_scaled_causal(const double *x, double *y, double *t, int64_t r,
+                                     int64_t cols, double scale, int64_t period,
+                                     int64_t offset)
+{
+    for (int64_t j = 0; j < cols; ++j) {
+        int masked = period > 0 && j > (r % period) + offset;
+        t[j] = masked ? -INFINITY : scale * x[j];
+    }
+    oracle_row(t, y, cols);
+}
+
 struct oracle_job {
     const double *x;
     double *y;
     int64_t row_begin, row_end, cols;
+    int fused;
+    double scale;
+    int64_t period, offset;
 };
 
 static void *oracle_worker(void *arg)
 {
     const struct oracle_job *job = (const struct oracle_job *)arg;
-    for (int64_t r = job->row_begin; r < job->row_end; ++r)
-        oracle_row(job->x + r * job->cols, job->y + r * job->cols, job->cols);
+    double *t = NULL;
+    if (job->fused) {
+        t = (double *)malloc((size_t)job->cols * sizeof(double));
+        if (!t)
+            return NULL; /* rows stay unwritten; the wrapper fills NaN first */
+    }
+    for (int64_t r = job->row_begin; r < job->row_end; ++r) {
+        if (job->fused)
+            oracle_row_scaled_causal(job->x + r * job->cols, job->y + r * job->cols, t, r,
+                                     job->cols, job->scale, job->period, job->offset);
+        else
+            oracle_row(job->x + r * job->cols, job->y + r * job->cols, job->cols);
+    }
+    free(t);
     return NULL;
+}
+
+/* Row-parallel driver shared by both entry points. */
+static int oracle_run(struct oracle_job proto, int64_t rows, int threads)
+{
+    if (threads <= 1 || rows == 1) {
+        proto.row_begin = 0;
+        proto.row_end = rows;
+        oracle_worker(&proto);
+        return 0;
+    }
+    if (threads > rows)
+        threads = (int)rows;
+
+    pthread_t *tid = (pthread_t *)calloc((size_t)threads, sizeof(pthread_t));
+    struct oracle_job *jobs =
+        (struct oracle_job *)calloc((size_t)threads, sizeof(struct oracle_job));
+    if (!tid || !jobs) {
+        free(tid);
+        free(jobs);
+        return -2;
+    }
+    for (int t = 0; t < threads; ++t) {
+        jobs[t] = proto;
+        jobs[t].row_begin = rows * t / threads;
+        jobs[t].row_end = rows * (t + 1) / threads;
+    }
+    int started = 0;
+    while (started < threads &&
+           pthread_create(&tid[started], NULL, oracle_worker, &jobs[started]) == 0)
+        ++started;
+    for (int t = started; t < threads; ++t) /* rows whose thread never started */
+        oracle_worker(&jobs[t]);
+    for (int t = 0; t < started; ++t)
+        pthread_join(tid[t], NULL);
+    free(tid);
+    free(jobs);
+    return 0;
 }
 
 /*
@@ -87,38 +159,26 @@ int oracle_softmax_f64(const double *x, double *y, int64_t rows, int64_t cols,
         return 0;
     if (!x || !y)
         return -1;
-    if (threads <= 1 || rows == 1) {
-        struct oracle_job job = {x, y, 0, rows, cols};
-        oracle_worker(&job);
-        return 0;
-    }
-    if (threads > rows)
-        threads = (int)rows;
+    struct oracle_job proto = {x, y, 0, 0, cols, 0, 1.0, 0, 0};
+    return oracle_run(proto, rows, threads);
+}
 
-    pthread_t *tid = (pthread_t *)calloc((size_t)threads, sizeof(pthread_t));
-    struct oracle_job *jobs =
-        (struct oracle_job *)calloc((size_t)threads, sizeof(struct oracle_job));
-    if (!tid || !jobs) {
-        free(tid);
-        free(jobs);
-        return -2;
-    }
-    for (int t = 0; t < threads; ++t) {
-        jobs[t].x = x;
-        jobs[t].y = y;
-        jobs[t].cols = cols;
-        jobs[t].row_begin = rows * t / threads;
-        jobs[t].row_end = rows * (t + 1) / threads;
-    }
-    int started = 0;
-    while (started < threads &&
-           pthread_create(&tid[started], NULL, oracle_worker, &jobs[started]) == 0)
-        ++started;
-    for (int t = started; t < threads; ++t) /* rows whose thread never started */
-        oracle_worker(&jobs[t]);
-    for (int t = 0; t < started; ++t)
-        pthread_join(tid[t], NULL);
-    free(tid);
-    free(jobs);
-    return 0;
+/*
+ * oracle_softmax_scaled_causal_f64: y = softmax(scale * x + mask, dim=-1),
+ * mask(r, c) = -inf when period > 0 and c > (r mod period) + offset, else 0
+ * (see oracle_row_scaled_causal).  Same arguments and return codes as
+ * oracle_softmax_f64, plus scale, period (>= 0) and offset.
+ */
+int oracle_softmax_scaled_causal_f64(const double *x, double *y, int64_t rows,
+                                     int64_t cols, double scale, int64_t period,
+                                     int64_t offset, int threads)
+{
+    if (rows < 0 || cols < 0 || period < 0)
+        return -1;
+    if (rows == 0 || cols == 0)
+        return 0;
+    if (!x || !y)
+        return -1;
+    struct oracle_job proto = {x, y, 0, 0, cols, 1, scale, period, offset};
+    return oracle_run(proto, rows, threads);
 }

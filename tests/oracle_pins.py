@@ -204,3 +204,88 @@ def run_pins(sm) -> list:
     if not np.allclose(yo.sum(axis=1), 1.0, rtol=0, atol=1e-14):
         fail("orientation", "rows of a 3 x 11 input do not sum to 1")
     return fails
+
+
+# ---------------------------------------------------------------------------
+# Scaled, causally masked rows: y = softmax(scale * x + mask), mask(r, c) =
+# -inf where period > 0 and c > (r mod period) + offset.
+
+def brute_force_scaled_causal(x, scale, period, offset):
+    """50-digit brute force of the masked, scaled definition, written from the
+    definition: kept columns K(r) = {c : period == 0 or c <= r mod period +
+    offset}; y_i = 1 / sum_{j in K} exp(scale (x_j - x_i)) for i in K, 0
+    otherwise; NaN for a row with no kept column."""
+    import mpmath
+    mpmath.mp.dps = 50
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    for r in range(x.shape[0]):
+        kept = [c for c in range(x.shape[1])
+                if period == 0 or c <= (r % period) + offset]
+        if not kept:
+            out[r, :] = np.nan
+            continue
+        for i in kept:
+            tot = mpmath.mpf(0)
+            for j in kept:
+                tot += mpmath.exp(mpmath.mpf(scale) * (mpmath.mpf(float(x[r, j])) -
+                                                       mpmath.mpf(float(x[r, i]))))
+            out[r, i] = float(1 / tot)
+    return out
+
+
+def run_fused_pins(smf, sm_plain) -> list:
+    """smf(x, scale, period, offset, threads=1) -> y; sm_plain = the pinned
+    plain oracle, used only for the masked-data identity."""
+    fails = []
+
+    def fail(name, msg):
+        fails.append(f"{name}: {msg}")
+
+    rng = np.random.default_rng(99)
+    for scale in (0.125, 1.0, -0.5, 3.0):
+        for period, offset in ((0, 0), (1, 0), (3, 0), (5, 2), (4, -1), (7, 3)):
+            x = rng.normal(0.0, 4.0, size=(9, 11))
+            y = np.asarray(smf(x, scale, period, offset))
+            v = brute_force_scaled_causal(x, scale, period, offset)
+            gap = np.abs(scale) * np.abs(x - np.nanmax(x, axis=1, keepdims=True))
+            rel = (16.0 + 4.0 * gap + x.shape[1]) * 2.0 ** -53
+            ok = y.shape == v.shape and np.array_equal(np.isnan(y), np.isnan(v))
+            if ok:
+                f = ~np.isnan(v)
+                ok = bool(np.all(np.abs(y[f] - v[f]) <= rel[f] * np.abs(v[f]) + 2.0 ** -1070))
+            if not ok:
+                fail("fused_brute_force", f"scale={scale} period={period} offset={offset}")
+
+    # identity: scale 1 and the mask written into the data as -inf equal the
+    # plain definition, bit for bit (same arithmetic)
+    x = rng.normal(0.0, 2.0, size=(12, 17))
+    for period, offset in ((4, 0), (12, 5), (3, -1)):
+        xm = x.copy()
+        for r in range(x.shape[0]):
+            xm[r, (r % period) + offset + 1:] = -np.inf
+            if (r % period) + offset < 0:
+                xm[r, :] = -np.inf
+        if not np.array_equal(np.asarray(smf(x, 1.0, period, offset)), np.asarray(sm_plain(xm)),
+                              equal_nan=True):
+            fail("masked_data_identity", f"period={period} offset={offset}")
+
+    # power-of-two scale: scale * x is exact, so scale=4 on x equals scale=1 on 4x
+    xq = np.round(rng.normal(0.0, 3.0, size=(6, 20)) * 256.0) / 256.0
+    if not np.array_equal(np.asarray(smf(xq, 4.0, 6, 0)), np.asarray(smf(4.0 * xq, 1.0, 6, 0)),
+                          equal_nan=True):
+        fail("pow2_scale", "scale 4 differs from pre-scaled data")
+
+    # causal structure: query 0 with offset 0 keeps column 0 only -> one-hot;
+    # masked entries are exactly 0; a row with nothing kept is NaN
+    x = rng.normal(0.0, 1.0, size=(8, 8))
+    y = np.asarray(smf(x, 0.7, 4, 0))
+    if not (y[0, 0] == 1.0 and np.all(y[0, 1:] == 0.0) and y[4, 0] == 1.0):
+        fail("one_hot_query0", f"row 0 {y[0].tolist()}")
+    for r in range(8):
+        if not np.all(y[r, (r % 4) + 1:] == 0.0):
+            fail("masked_zero", f"row {r}")
+    yn = np.asarray(smf(x, 1.0, 4, -1))
+    if not (np.all(np.isnan(yn[0])) and np.all(np.isnan(yn[4])) and not np.isnan(yn[1, 0])):
+        fail("empty_row_nan", "query 0 with offset -1 should keep nothing")
+    return fails
