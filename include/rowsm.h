@@ -142,6 +142,28 @@ int rowsm_forward_config(const void *x, void *y, int64_t rows, int64_t cols,
                          const rowsm_config *cfg);
 
 /*
+ * rowsm_forward_scaled_causal: y = softmax(scale * x + mask, dim=-1), the
+ * scaled and causally masked attention-score form of the operation:
+ *     mask(r, c) = -inf   when causal_period > 0 and
+ *                         c > (r mod causal_period) + causal_offset,
+ *                  0      otherwise.
+ * Row r is query r mod causal_period of its group; causal_offset shifts the
+ * diagonal (0: query q sees keys 0..q; cols - causal_period: keys aligned to
+ * the end).  causal_period == 0 disables the mask (scale only); < 0 returns
+ * ROWSM_EINVAL.  Masked columns are never read and are written as exact
+ * zeros; a row whose every column is masked is all NaN, as the plain
+ * operation gives for an all -inf row.  scale * x is formed in fp32 (any
+ * scale; IEEE semantics for zero, infinite or NaN products).  Other
+ * arguments, layout and errors as rowsm_forward; cfg (NULL = launcher's
+ * choice) as rowsm_forward_config, except that the packed medium form and
+ * rows_per_lane other than 4 are not available here.
+ */
+int rowsm_forward_scaled_causal(const void *x, void *y, int64_t rows, int64_t cols,
+                                int in_dtype, int out_dtype, float scale,
+                                int64_t causal_period, int64_t causal_offset,
+                                void *stream, const rowsm_config *cfg);
+
+/*
  * rowsm_describe: writes into buf (capacity len, always NUL-terminated when
  * len > 0) a one-line description of the launch rowsm_forward_variant would
  * make: kernel family, template configuration, grid and block sizes.  Pure

@@ -11,6 +11,8 @@ Raw entry points (same names and arguments as the C ABI; pointers are ints,
     rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream) -> status
     rowsm_forward_variant(x, y, rows, cols, in_dtype, out_dtype, stream, variant)
     rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, cfg)
+    rowsm_forward_scaled_causal(x, y, rows, cols, in_dtype, out_dtype, scale,
+                                causal_period, causal_offset, stream, cfg)
     rowsm_select(rows, cols, in_dtype, out_dtype) -> variant or status
     rowsm_describe(rows, cols, in_dtype, out_dtype, variant) -> (status, text)
     rowsm_split_wait_failures() -> count (diagnostics of the split LARGE form)
@@ -35,8 +37,8 @@ LIB_PATH = os.path.join(_PKG, "librowsm.so")
 
 # Symbols declared in include/rowsm.h.
 EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
-           "rowsm_forward_config", "rowsm_describe", "rowsm_split_wait_failures",
-           "rowsm_status_string")
+           "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_describe",
+           "rowsm_split_wait_failures", "rowsm_status_string")
 
 
 class RowsmError(RuntimeError):
@@ -83,6 +85,9 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     h.rowsm_forward_variant.restype = i32
     h.rowsm_forward_config.argtypes = fwd + [ctypes.POINTER(RowsmConfig)]
     h.rowsm_forward_config.restype = i32
+    h.rowsm_forward_scaled_causal.argtypes = [vp, vp, i64, i64, i32, i32, ctypes.c_float,
+                                              i64, i64, vp, ctypes.POINTER(RowsmConfig)]
+    h.rowsm_forward_scaled_causal.restype = i32
     h.rowsm_select.argtypes = [i64, i64, i32, i32]
     h.rowsm_select.restype = i32
     h.rowsm_describe.argtypes = [i64, i64, i32, i32, i32, ctypes.c_char_p, i64]
@@ -110,6 +115,15 @@ def rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, cfg) -> 
         cfg = RowsmConfig(**cfg)
     ref = ctypes.byref(cfg) if cfg is not None else None
     return lib().rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, ref)
+
+
+def rowsm_forward_scaled_causal(x, y, rows, cols, in_dtype, out_dtype, scale, causal_period,
+                                causal_offset, stream=0, cfg=None) -> int:
+    if cfg is not None and not isinstance(cfg, RowsmConfig):
+        cfg = RowsmConfig(**cfg)
+    ref = ctypes.byref(cfg) if cfg is not None else None
+    return lib().rowsm_forward_scaled_causal(x, y, rows, cols, in_dtype, out_dtype, scale,
+                                             causal_period, causal_offset, stream, ref)
 
 
 def rowsm_select(rows, cols, in_dtype, out_dtype) -> int:
@@ -142,6 +156,26 @@ def dtype_code(dtype) -> int:
     if dtype == torch.bfloat16:
         return BF16
     raise RowsmError(f"unsupported dtype {dtype}")
+
+
+def scaled_causal_softmax(x, scale: float, causal_period: int, causal_offset: int = 0,
+                          out_dtype=None, out=None, config=None, stream=None):
+    """softmax(scale * x + causal mask, dim=-1) of a contiguous fp32/bf16 GPU
+    tensor (see rowsm_forward_scaled_causal).  Marshalling only."""
+    import torch
+    if not x.is_cuda or not x.is_contiguous():
+        raise RowsmError("scaled_causal_softmax needs a contiguous GPU tensor")
+    if out is None:
+        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
+        raise RowsmError("out must be a contiguous tensor of x's shape on x's device")
+    cols = x.shape[-1] if x.dim() else 1
+    rows = x.numel() // cols if cols else 0
+    st = (stream or torch.cuda.current_stream(x.device)).cuda_stream
+    check(rowsm_forward_scaled_causal(x.data_ptr(), out.data_ptr(), rows, cols,
+                                      dtype_code(x.dtype), dtype_code(out.dtype), float(scale),
+                                      int(causal_period), int(causal_offset), st, config))
+    return out
 
 
 def softmax(x, out_dtype=None, out=None, variant: int = AUTO, config=None, stream=None):

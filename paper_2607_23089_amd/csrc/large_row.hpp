@@ -10,6 +10,9 @@
 // first so that the most recently fetched tiles are re-read while they are
 // most likely still cached, and writes exp(x - m) / sum.
 //
+// FUSED computes softmax(scale * x + causal mask) (see Fused): columns past
+// the row's limit are not loaded and come out as exact zeros.
+//
 // A thread that has seen only -inf so far uses 0 in place of -m*log2e, so a
 // fully masked tile adds exp(-inf) = 0 instead of exp(-inf + inf) = NaN; a row
 // whose maximum is -inf, +inf or that holds a NaN still ends as all NaN.
@@ -23,10 +26,10 @@
 
 namespace rowsm {
 
-template <typename In, typename Out, int VW, int U>
+template <typename In, typename Out, int VW, int U, bool FUSED>
 __global__ __launch_bounds__(1024) void large_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
-    int64_t rows, int cols) {
+    int64_t rows, int cols, Fused fz) {
   __shared__ float red_m[16];
   __shared__ float red_s[16];
 
@@ -45,25 +48,34 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const rsrc_t rx = make_rsrc(x + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * Out::bytes);
+    const int lim = FUSED ? fused_limit(fz, row, cols) : cols - 1;
 
     // Pass 1: running (max, sum).
     float m = ninf, s = 0.0f;
     for (int tt = 0; tt < ntiles; ++tt) {
-      InVec<In, VW> v[U];
-      const bool full = tt < ntiles - 1;  // every tile but the last is whole
+      float f[U][VW];
+      {
+        InVec<In, VW> v[U];
+        const bool full = tt < ntiles - 1;  // every tile but the last is whole
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int idx = tt * tile + u * T + tid;
-        if (full || idx < nvec)
-          v[u].load(rx, vin, (uint32_t)(tt * tile + u * T) * (VW * In::bytes));
-        else
-          v[u].set_neg_inf();
+        for (int u = 0; u < U; ++u) {
+          const int idx = tt * tile + u * T + tid;
+          if ((full || idx < nvec) && (!FUSED || idx * VW <= lim))
+            v[u].load(rx, vin, (uint32_t)(tt * tile + u * T) * (VW * In::bytes));
+          else
+            v[u].set_neg_inf();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          v[u].to_float(f[u]);
+          if constexpr (FUSED) fused_apply(f[u], (tt * tile + u * T + tid) * VW, lim, fz.scale);
+        }
       }
       float tm = ninf;
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int i = 0; i < VW; ++i) tm = fmax_nn(tm, v[u].get(i));
+        for (int i = 0; i < VW; ++i) tm = fmax_nn(tm, f[u][i]);
       const float M = fmax_nn(m, tm);
       const float nml = (M == ninf) ? 0.0f : -M * kLog2e;
       float acc = rescale(s, m, M);
@@ -71,7 +83,7 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
       for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int i = 0; i < VW; ++i)
-          acc += exp2_fast(__builtin_fmaf(v[u].get(i), kLog2e, nml));
+          acc += exp2_fast(__builtin_fmaf(f[u][i], kLog2e, nml));
       m = M;
       s = acc;
     }
@@ -96,7 +108,7 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int idx = tt * tile + u * T + tid;
-        if (full || idx < nvec)
+        if ((full || idx < nvec) && (!FUSED || idx * VW <= lim))
           v[u].load(rx, vin, (uint32_t)(tt * tile + u * T) * (VW * In::bytes));
         else
           v[u].set_neg_inf();
@@ -105,9 +117,11 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
       for (int u = 0; u < U; ++u) {
         const int idx = tt * tile + u * T + tid;
         float o[VW];
+        v[u].to_float(o);
+        if constexpr (FUSED) fused_apply(o, idx * VW, lim, fz.scale);
 #pragma unroll
         for (int i = 0; i < VW; ++i)
-          o[i] = exp2_fast(__builtin_fmaf(v[u].get(i), kLog2e, nml)) * inv;
+          o[i] = exp2_fast(__builtin_fmaf(o[i], kLog2e, nml)) * inv;
         if (full || idx < nvec)
           store_out<Out, VW>(ry, vout + (uint32_t)(tt * tile + u * T) * (VW * Out::bytes), o);
       }

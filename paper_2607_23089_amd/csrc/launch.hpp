@@ -1,0 +1,83 @@
+// Launch plans and the per-family launchers.  Each family's kernels are
+// instantiated in translation units of their own (plain and fused apart), so
+// the library builds in parallel; rowsm.hip holds the launcher logic and the
+// C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rowsm.h"
+#include "rowsm_device.hpp"
+
+namespace rowsm {
+
+constexpr int kMaxDevices = 64;
+
+// The launch the row launcher chose (fields unused by a family stay default).
+struct Plan {
+  int variant = 0;
+  int vw = 1;       // elements per vector
+  int nvec = 0;     // vectors per row
+  // SMALL
+  int lpr = 1, rpl = 4;
+  // MEDIUM
+  int wpr = 1, vpl = 1, nv = 1;
+  bool packed = false;
+  // LARGE
+  int u = 4;
+  int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
+  // launch
+  int block = 256;
+  int64_t grid = 1;  // split form: 0 = occupancy, < 0 = minus the blocks-per-CU cap
+};
+
+// One launch request: the plan plus its operands.  fz == nullptr selects the
+// plain kernels, otherwise the FUSED instantiations with *fz.
+struct Call {
+  Plan p;
+  const void* x;
+  void* y;
+  int64_t rows;
+  int cols;
+  hipStream_t st;
+  int cus;
+  const Fused* fz;
+};
+
+inline Fused fused_or_identity(const Call& c) { return c.fz ? *c.fz : Fused{1.0f, 0, 0}; }
+
+// Calls L<In, Out, VW, FUSED>::run(c) for the call's dtype pair and vector
+// width (16-byte, 8-byte or single-element vectors).  Returns a rowsm_status:
+// ROWSM_EINVAL when nothing matches (nothing enqueued).
+template <template <typename, typename, int, bool> class L, bool FUSED>
+int dispatch(const Call& c, int in_dt, int out_dt) {
+  auto io = [&](auto in_tag, auto out_tag) -> int {
+    using In = decltype(in_tag);
+    using Out = decltype(out_tag);
+    constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
+    if (c.p.vw == 1) return L<In, Out, 1, FUSED>::run(c);
+    if (c.p.vw == V8) return L<In, Out, V8, FUSED>::run(c);
+    if (c.p.vw == V16) return L<In, Out, V16, FUSED>::run(c);
+    return ROWSM_EINVAL;
+  };
+  if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32) return io(F32{}, F32{});
+  if (in_dt == ROWSM_F32) return io(F32{}, BF16{});
+  if (out_dt == ROWSM_F32) return io(BF16{}, F32{});
+  return io(BF16{}, BF16{});
+}
+
+// Per-family launchers (launch_<family>_<plain|fused>.hip).
+int launch_small_plain(const Call& c, int in_dt, int out_dt);
+int launch_small_fused(const Call& c, int in_dt, int out_dt);
+int launch_medium_plain(const Call& c, int in_dt, int out_dt);
+int launch_medium_fused(const Call& c, int in_dt, int out_dt);
+int launch_large_plain(const Call& c, int in_dt, int out_dt);
+int launch_large_fused(const Call& c, int in_dt, int out_dt);
+int launch_split_plain(const Call& c, int in_dt, int out_dt);
+int launch_split_fused(const Call& c, int in_dt, int out_dt);
+
+// Split-form diagnostics (launch_split_common.hip).
+int64_t split_wait_failures_current_device();
+
+}  // namespace rowsm

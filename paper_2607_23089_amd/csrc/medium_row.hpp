@@ -10,6 +10,9 @@
 // permlane swaps, then across the WPR waves through LDS (one barrier each;
 // WPR == 1 needs neither LDS nor barriers).
 //
+// FUSED computes softmax(scale * x + causal mask) (see Fused): columns past
+// the row's limit are not loaded and come out as exact zeros.
+//
 // PACKED == false widens the row to fp32 once and keeps exp(x - m) in
 // registers for the normalise step.  PACKED == true keeps the row in its raw
 // input form (bf16 pairs take half the registers) and evaluates exp(x - m) a
@@ -45,10 +48,11 @@ __device__ __forceinline__ float block_row_reduce(float v, int wpr, int wave, in
   return v;
 }
 
-template <typename In, typename Out, int VW, int NV, bool PACKED>
+template <typename In, typename Out, int VW, int NV, bool PACKED, bool FUSED>
 __global__ __launch_bounds__(1024) void medium_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
-    int64_t rows, int cols, int wpr) {
+    int64_t rows, int cols, int wpr, Fused fz) {
+  static_assert(!(PACKED && FUSED), "the fused variants keep the row in fp32");
   __shared__ float red_m[16];
   __shared__ float red_s[16];
 
@@ -74,6 +78,7 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
     const int64_t rr = row_ok ? row : 0;
     const rsrc_t rx = make_rsrc(x + rr * cols, (uint64_t)cols * In::bytes);
     const rsrc_t ry = make_rsrc(y + rr * cols, (uint64_t)cols * Out::bytes);
+    const int lim = FUSED ? fused_limit(fz, rr, cols) : cols - 1;
 
     if constexpr (PACKED) {
       InVec<In, VW> v[NV];
@@ -115,11 +120,16 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
         InVec<In, VW> v[NV];
 #pragma unroll
         for (int s = 0; s < NV; ++s) {
-          if (row_ok && (s < NV - 1 || last_ok)) v[s].load(rx, vin, s * sin);
-          else v[s].set_neg_inf();
+          if (row_ok && (s < NV - 1 || last_ok) && (!FUSED || (s * T + t) * VW <= lim))
+            v[s].load(rx, vin, s * sin);
+          else
+            v[s].set_neg_inf();
         }
 #pragma unroll
-        for (int s = 0; s < NV; ++s) v[s].to_float(f[s]);
+        for (int s = 0; s < NV; ++s) {
+          v[s].to_float(f[s]);
+          if constexpr (FUSED) fused_apply(f[s], (s * T + t) * VW, lim, fz.scale);
+        }
       }
       float mx = -__builtin_inff();
 #pragma unroll

@@ -17,20 +17,14 @@
 #include <atomic>
 #include <cstdio>
 #include <cstring>
-#include <mutex>
 #include <type_traits>
 #include <utility>
 
-#include "large_row.hpp"
-#include "medium_row.hpp"
-#include "rowsm.h"
-#include "small_row.hpp"
-#include "split_row.hpp"
+#include "launch.hpp"
 
 namespace rowsm {
 namespace {
 
-constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
 
 // Compute-unit count of the current device (cached per device).  Falls back
@@ -55,22 +49,6 @@ int next_pow2(int v) {
   return p;
 }
 
-struct Plan {
-  int variant = 0;
-  int vw = 1;       // elements per vector
-  int nvec = 0;     // vectors per row
-  // SMALL
-  int lpr = 1, rpl = 4;
-  // MEDIUM
-  int wpr = 1, vpl = 1, nv = 1;
-  bool packed = false;
-  // LARGE
-  int u = 4;
-  int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
-  // launch
-  int block = 256;
-  int64_t grid = 1;
-};
 
 // Vector widths (elements) with compiled kernels: 16-byte and 8-byte input
 // vectors, and single elements for rows that are not 8-byte aligned.
@@ -115,7 +93,7 @@ bool config_in_domain(const rowsm_config* c) {
 }
 
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
-             const rowsm_config* cfg, int cus, Plan* p) {
+             const rowsm_config* cfg, int cus, bool fused, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
   const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
   int vw = choose_vw(cols, ib, ob, xa, ya);
@@ -135,8 +113,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   if (variant == ROWSM_AUTO) {
     if (nvec <= 32) {
       variant = ROWSM_SMALL;
-    } else if (nvec <= 16 * kWave * (64 / vw < 16 ? 64 / vw : 16) ||
-               (in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24)) {
+    } else if (nvec <= 16 * kWave * ((fused ? 32 : 64) / vw < 16 ? (fused ? 32 : 64) / vw : 16) ||
+               (!fused && in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24)) {
       // whole row in the registers of one block
       variant = ROWSM_MEDIUM;
     } else {
@@ -158,6 +136,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     if (cfg && cfg->rows_per_lane > 0) {
       const int r = cfg->rows_per_lane;
       if (r != 1 && r != 2 && r != 4 && r != 8) return ROWSM_EINVAL;
+      if (fused && r != 4) return ROWSM_EINVAL;  // fused kernels: 4 rows per lane
       p->rpl = r;
     }
     p->block = 256;
@@ -171,14 +150,17 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     int wpr = 0, vpl = 0;
     bool packed = false;
     const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
-    const int want_packed = cfg ? cfg->packed : -1;
+    const int want_packed = fused ? 0 : (cfg ? cfg->packed : -1);
+    if (fused && cfg && cfg->packed == 1) return ROWSM_EINVAL;
     if (want_wpr && (want_wpr & (want_wpr - 1) || want_wpr > 16)) return ROWSM_EINVAL;
     // Unpacked: the smallest group whose lanes hold <= 16 fp32 values each
     // (<= 32, then <= 64 when the row is longer), unless a group size is
     // forced.  Fewer values per lane and more resident rows measured faster
     // than longer per-lane rows on the 32768 x 4096 workload.
     if (want_packed != 1) {
+      // Fused rows keep column indices live as well: at most 32 values.
       for (int cap_vals : {16, 32, 64}) {
+        if (fused && cap_vals > 32) break;
         for (int w = 1; w <= 16; w <<= 1) {
           if (want_wpr && w != want_wpr) continue;
           const int v = (int)cdiv(nvec, (int64_t)w * kWave);
@@ -239,7 +221,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       // lane (measured on the 4096 x 151936 and 1024 x 262144 workloads).
       const bool widening = ob > ib;
       const int T = (cfg && cfg->block > 0) ? cfg->block : (widening ? 512 : 256);
-      const int vals = widening ? 40 : 64;
+      const int vals = fused ? 32 : (widening ? 40 : 64);
       int nv_cap = vals / vw < 16 ? vals / vw : 16;
       if (nv_cap < 1) nv_cap = 1;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
@@ -272,238 +254,22 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   return ROWSM_EINVAL;
 }
 
-// ---- single-read split form: per-device workspace and launch ---------------
+// ---- family dispatch ------------------------------------------------------------
 
-constexpr int kSplitMaxBlocks = 1 << 16;  // workspace capacity in blocks
-
-// Per-device state of the split form.  The workspace (two 64-bit words per
-// block and row parity, an error count; 2 MiB) is allocated and cleared on
-// the first split launch on a device and kept until the process ends.  Split
-// launches on one device are ordered through `last` (each waits for the
-// previous one, whatever its stream), so two launches never use the
-// workspace at the same time.  Tags are handed out from `next_tag`: a launch
-// whose blocks process at most n rows each uses tags tag0 .. tag0 + n - 1,
-// so a tag is never reused while the workspace may still hold it; when the
-// 32-bit tag space runs out the workspace is cleared again and tags restart
-// at 1.
-struct SplitState {
-  std::mutex mu;
-  void* base = nullptr;
-  hipEvent_t last = nullptr;
-  bool have_last = false;
-  uint32_t next_tag = 1;
-};
-SplitState g_split[kMaxDevices];
-
-constexpr size_t kSplitWorkspaceBytes = (size_t)kSplitMaxBlocks * 32 + 256;
-
-int split_clear(void* p) {
-  if (hipMemset(p, 0, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
-  return hipDeviceSynchronize() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
-}
-
-int split_workspace(int dev, SplitWorkspace* ws) {
-  SplitState& st = g_split[dev];
-  if (!st.base) {
-    void* p = nullptr;
-    if (hipMalloc(&p, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
-    if (split_clear(p) != ROWSM_OK ||
-        hipEventCreateWithFlags(&st.last, hipEventDisableTiming) != hipSuccess) {
-      (void)hipFree(p);
-      return ROWSM_EHIP;
-    }
-    st.base = p;
-    st.next_tag = 1;
+int launch(const Call& c, int in_dt, int out_dt) {
+  const bool f = c.fz != nullptr;
+  switch (c.p.variant) {
+    case ROWSM_SMALL:
+      return f ? launch_small_fused(c, in_dt, out_dt) : launch_small_plain(c, in_dt, out_dt);
+    case ROWSM_MEDIUM:
+      return f ? launch_medium_fused(c, in_dt, out_dt) : launch_medium_plain(c, in_dt, out_dt);
+    case ROWSM_LARGE:
+      if (c.p.split > 0)
+        return f ? launch_split_fused(c, in_dt, out_dt) : launch_split_plain(c, in_dt, out_dt);
+      return f ? launch_large_fused(c, in_dt, out_dt) : launch_large_plain(c, in_dt, out_dt);
+    default:
+      return ROWSM_EINVAL;
   }
-  char* b = static_cast<char*>(st.base);
-  ws->wm = reinterpret_cast<uint64_t*>(b);
-  ws->ws = reinterpret_cast<uint64_t*>(b + (size_t)kSplitMaxBlocks * 16);
-  ws->error = reinterpret_cast<uint32_t*>(b + (size_t)kSplitMaxBlocks * 32);
-  return ROWSM_OK;
-}
-
-// Reserve n consecutive tags (n >= 1); clears the workspace when the tag
-// space would wrap.
-int split_tags(SplitState& st, uint64_t n, uint32_t* tag0) {
-  if (n >= 0x80000000ull) return ROWSM_EINVAL;
-  if ((uint64_t)st.next_tag + n > 0xffffffffull) {
-    if (st.have_last && hipEventSynchronize(st.last) != hipSuccess) return ROWSM_EHIP;
-    if (split_clear(st.base) != ROWSM_OK) return ROWSM_EHIP;
-    st.next_tag = 1;
-  }
-  *tag0 = st.next_tag;
-  st.next_tag += (uint32_t)n;
-  return ROWSM_OK;
-}
-
-template <typename In, typename Out, int VW, int NV>
-int launch_split_nv(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                    hipStream_t stream, int cus) {
-  auto kern = split_row_kernel<In, Out, VW, NV>;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
-                                                   p.block, 0) != hipSuccess)
-    return ROWSM_EHIP;
-  if (p.grid < 0 && per_cu > -p.grid) per_cu = (int)-p.grid;
-  const int64_t resident = (int64_t)per_cu * cus;
-  int64_t slots = resident / p.split;
-  if (slots > rows) slots = rows;
-  if (slots > kSplitMaxBlocks / p.split) slots = kSplitMaxBlocks / p.split;
-  if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
-  // The grid never exceeds one full residency of the device (see the
-  // co-residency note of split_row_kernel).
-  const unsigned grid = (unsigned)(slots * p.split);
-
-  SplitState& st = g_split[dev];
-  std::lock_guard<std::mutex> lock(st.mu);
-  SplitWorkspace ws;
-  int r = split_workspace(dev, &ws);
-  if (r != ROWSM_OK) return r;
-  uint32_t tag0 = 0;
-  r = split_tags(st, (uint64_t)((rows + slots - 1) / slots), &tag0);
-  if (r != ROWSM_OK) return r;
-  if (st.have_last && hipStreamWaitEvent(stream, st.last, 0) != hipSuccess) return ROWSM_EHIP;
-  auto xp = static_cast<const typename In::storage*>(x);
-  auto yp = static_cast<typename Out::storage*>(y);
-  (void)hipGetLastError();
-  kern<<<dim3(grid), dim3(p.block), 0, stream>>>(xp, yp, rows, cols, p.split, ws, tag0);
-  if (hipGetLastError() != hipSuccess) return ROWSM_EHIP;
-  if (hipEventRecord(st.last, stream) != hipSuccess) return ROWSM_EHIP;
-  st.have_last = true;
-  return ROWSM_OK;
-}
-
-template <typename In, typename Out, int VW, int... NVs>
-int launch_split_seq(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                     hipStream_t st, int cus, std::integer_sequence<int, NVs...>) {
-  int r = ROWSM_EINVAL;
-  (void)((p.nv == NVs + 1 && NVs + 1 <= 16 && (NVs + 1) * VW <= 64
-              ? (r = launch_split_nv < In, Out, VW,
-                 ((NVs + 1) * VW <= 64 ? NVs + 1 : 1) > (p, x, y, rows, cols, st, cus),
-                 true)
-              : false) ||
-         ...);
-  return r;
-}
-
-// ---- template dispatch ------------------------------------------------------
-
-template <typename In, typename Out, int VW>
-bool launch_small(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                  hipStream_t st) {
-  auto xp = static_cast<const typename In::storage*>(x);
-  auto yp = static_cast<typename Out::storage*>(y);
-#define ROWSM_SMALL_CASE(L, R)                                                           \
-  if (p.lpr == L && p.rpl == R) {                                                        \
-    small_row_kernel<In, Out, VW, L, R><<<dim3((unsigned)p.grid), dim3(p.block), 0, st>>>( \
-        xp, yp, rows, cols);                                                             \
-    return true;                                                                         \
-  }
-#define ROWSM_SMALL_L(L) \
-  ROWSM_SMALL_CASE(L, 1) ROWSM_SMALL_CASE(L, 2) ROWSM_SMALL_CASE(L, 4) ROWSM_SMALL_CASE(L, 8)
-  ROWSM_SMALL_L(1) ROWSM_SMALL_L(2) ROWSM_SMALL_L(4) ROWSM_SMALL_L(8) ROWSM_SMALL_L(16)
-  ROWSM_SMALL_L(32)
-#undef ROWSM_SMALL_L
-#undef ROWSM_SMALL_CASE
-  return false;
-}
-
-template <typename In, typename Out, int VW, int NV, bool PACKED>
-bool try_medium(const Plan& p, const void* x, void* y, int64_t rows, int cols, hipStream_t st) {
-  constexpr bool compiled =
-      PACKED ? (std::is_same<In, BF16>::value && VW == 8 && NV >= 9 && NV <= 24)
-             : (NV * VW <= 64 && NV <= 16);
-  if constexpr (compiled) {
-    if (p.nv == NV && p.packed == PACKED) {
-      medium_row_kernel<In, Out, VW, NV, PACKED>
-          <<<dim3((unsigned)p.grid), dim3(p.block), 0, st>>>(
-              static_cast<const typename In::storage*>(x),
-              static_cast<typename Out::storage*>(y), rows, cols, p.wpr);
-      return true;
-    }
-  }
-  return false;
-}
-
-template <typename In, typename Out, int VW, bool PACKED, int... NVs>
-bool launch_medium_nv(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                      hipStream_t st, std::integer_sequence<int, NVs...>) {
-  return (try_medium<In, Out, VW, NVs + 1, PACKED>(p, x, y, rows, cols, st) || ...);
-}
-
-template <typename In, typename Out, int VW>
-bool launch_medium(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                   hipStream_t st) {
-  if (p.packed)
-    return launch_medium_nv<In, Out, VW, true>(p, x, y, rows, cols, st,
-                                               std::make_integer_sequence<int, 24>{});
-  return launch_medium_nv<In, Out, VW, false>(p, x, y, rows, cols, st,
-                                              std::make_integer_sequence<int, 16>{});
-}
-
-template <typename In, typename Out, int VW>
-bool launch_large(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                  hipStream_t st) {
-  auto xp = static_cast<const typename In::storage*>(x);
-  auto yp = static_cast<typename Out::storage*>(y);
-  const dim3 g((unsigned)p.grid), b(p.block);
-  if (p.u == 2) large_row_kernel<In, Out, VW, 2><<<g, b, 0, st>>>(xp, yp, rows, cols);
-  else if (p.u == 4) large_row_kernel<In, Out, VW, 4><<<g, b, 0, st>>>(xp, yp, rows, cols);
-  else if (p.u == 8) large_row_kernel<In, Out, VW, 8><<<g, b, 0, st>>>(xp, yp, rows, cols);
-  else return false;
-  return true;
-}
-
-template <typename In, typename Out, int VW>
-bool launch_vw(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-               hipStream_t st) {
-  if (p.variant == ROWSM_SMALL) return launch_small<In, Out, VW>(p, x, y, rows, cols, st);
-  if (p.variant == ROWSM_MEDIUM) return launch_medium<In, Out, VW>(p, x, y, rows, cols, st);
-  if (p.variant == ROWSM_LARGE) return launch_large<In, Out, VW>(p, x, y, rows, cols, st);
-  return false;
-}
-
-// Compiled vector widths: 16- and 8-byte input vectors and single elements.
-template <typename In, typename Out>
-bool launch_io(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-               hipStream_t st) {
-  constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
-  if (p.vw == 1) return launch_vw<In, Out, 1>(p, x, y, rows, cols, st);
-  if (p.vw == V8) return launch_vw<In, Out, V8>(p, x, y, rows, cols, st);
-  if (p.vw == V16) return launch_vw<In, Out, V16>(p, x, y, rows, cols, st);
-  return false;
-}
-
-template <typename In, typename Out>
-int launch_split_io(const Plan& p, const void* x, void* y, int64_t rows, int cols,
-                    hipStream_t st, int cus) {
-  constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
-  auto seq = std::make_integer_sequence<int, 16>{};
-  if (p.vw == 1) return launch_split_seq<In, Out, 1>(p, x, y, rows, cols, st, cus, seq);
-  if (p.vw == V8) return launch_split_seq<In, Out, V8>(p, x, y, rows, cols, st, cus, seq);
-  if (p.vw == V16) return launch_split_seq<In, Out, V16>(p, x, y, rows, cols, st, cus, seq);
-  return ROWSM_EINVAL;
-}
-
-int launch_split(const Plan& p, int in_dt, int out_dt, const void* x, void* y, int64_t rows,
-                 int cols, hipStream_t st, int cus) {
-  if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32)
-    return launch_split_io<F32, F32>(p, x, y, rows, cols, st, cus);
-  if (in_dt == ROWSM_F32) return launch_split_io<F32, BF16>(p, x, y, rows, cols, st, cus);
-  if (out_dt == ROWSM_F32) return launch_split_io<BF16, F32>(p, x, y, rows, cols, st, cus);
-  return launch_split_io<BF16, BF16>(p, x, y, rows, cols, st, cus);
-}
-
-// Returns false when no compiled kernel matches the plan (no launch made).
-bool launch(const Plan& p, int in_dt, int out_dt, const void* x, void* y, int64_t rows,
-            int cols, hipStream_t st) {
-  if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32)
-    return launch_io<F32, F32>(p, x, y, rows, cols, st);
-  if (in_dt == ROWSM_F32) return launch_io<F32, BF16>(p, x, y, rows, cols, st);
-  if (out_dt == ROWSM_F32) return launch_io<BF16, F32>(p, x, y, rows, cols, st);
-  return launch_io<BF16, BF16>(p, x, y, rows, cols, st);
 }
 
 // ---- validation -------------------------------------------------------------
@@ -532,21 +298,23 @@ int validate(const void* x, const void* y, int64_t rows, int64_t cols, int in_dt
 }
 
 int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, int out_dt,
-                 void* stream, const rowsm_config* cfg) {
+                 void* stream, const rowsm_config* cfg, const Fused* fz) {
   bool noop = false;
   int st = validate(x, y, rows, cols, in_dt, out_dt, true, &noop);
   if (st != ROWSM_OK || noop) return st;
-  Plan p;
-  const int cus = cu_count();
-  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, cus, &p);
+  Call c;
+  c.cus = cu_count();
+  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus,
+                fz != nullptr, &c.p);
   if (st != ROWSM_OK) return st;
+  c.x = x;
+  c.y = y;
+  c.rows = rows;
+  c.cols = (int)cols;
+  c.st = static_cast<hipStream_t>(stream);
+  c.fz = fz;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
-  if (p.variant == ROWSM_LARGE && p.split > 0)
-    return launch_split(p, in_dt, out_dt, x, y, rows, (int)cols,
-                        static_cast<hipStream_t>(stream), cus);
-  if (!launch(p, in_dt, out_dt, x, y, rows, (int)cols, static_cast<hipStream_t>(stream)))
-    return ROWSM_EINVAL;  // no compiled kernel for this plan: nothing was enqueued
-  return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+  return launch(c, in_dt, out_dt);
 }
 
 const char* variant_name(int v) {
@@ -565,7 +333,7 @@ using namespace rowsm;
 
 extern "C" int rowsm_forward(const void* x, void* y, int64_t rows, int64_t cols, int in_dtype,
                              int out_dtype, void* stream) {
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr, nullptr);
 }
 
 extern "C" int rowsm_forward_variant(const void* x, void* y, int64_t rows, int64_t cols,
@@ -579,13 +347,26 @@ extern "C" int rowsm_forward_variant(const void* x, void* y, int64_t rows, int64
   std::memset(&cfg, 0, sizeof(cfg));
   cfg.variant = variant;
   cfg.packed = -1;
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, &cfg);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, &cfg, nullptr);
 }
 
 extern "C" int rowsm_forward_config(const void* x, void* y, int64_t rows, int64_t cols,
                                     int in_dtype, int out_dtype, void* stream,
                                     const rowsm_config* cfg) {
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, nullptr);
+}
+
+extern "C" int rowsm_forward_scaled_causal(const void* x, void* y, int64_t rows, int64_t cols,
+                                           int in_dtype, int out_dtype, float scale,
+                                           int64_t causal_period, int64_t causal_offset,
+                                           void* stream, const rowsm_config* cfg) {
+  if (causal_period < 0) {
+    bool noop = false;
+    const int st = validate(x, y, rows, cols, in_dtype, out_dtype, true, &noop);
+    return st != ROWSM_OK ? st : ROWSM_EINVAL;
+  }
+  const Fused fz{scale, causal_period, causal_offset};
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, &fz);
 }
 
 extern "C" int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dtype) {
@@ -594,7 +375,7 @@ extern "C" int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dt
   if (st != ROWSM_OK) return st;
   if (noop) return ROWSM_SMALL;  // nothing is launched; report the smallest family
   Plan p;
-  const int r = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, &p);
+  const int r = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, false, &p);
   return r == ROWSM_OK ? p.variant : r;
 }
 
@@ -609,7 +390,7 @@ extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_
     std::memset(&cfg, 0, sizeof(cfg));
     cfg.variant = variant;
     cfg.packed = -1;
-    st = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, &cfg, 256, &p);
+    st = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, &cfg, 256, false, &p);
   }
   if (buf && len > 0) {
     if (st != ROWSM_OK) {
@@ -630,18 +411,7 @@ extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_
 }
 
 extern "C" int64_t rowsm_split_wait_failures(void) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
-  SplitState& st = g_split[dev];
-  std::lock_guard<std::mutex> lock(st.mu);
-  if (!st.base) return 0;  // no split launch on this device yet
-  if (st.have_last && hipEventSynchronize(st.last) != hipSuccess) return ROWSM_EHIP;
-  uint32_t n = 0;
-  const char* b = static_cast<const char*>(st.base);
-  if (hipMemcpy(&n, b + (size_t)kSplitMaxBlocks * 32, sizeof(n), hipMemcpyDeviceToHost) !=
-      hipSuccess)
-    return ROWSM_EHIP;
-  return (int64_t)n;
+  return split_wait_failures_current_device();
 }
 
 extern "C" const char* rowsm_status_string(int status) {

@@ -248,6 +248,35 @@ __device__ __forceinline__ float group_reduce(float v) {
   return v;
 }
 
+// ---- fused scale and causal mask ---------------------------------------------
+//
+// The fused variants compute softmax(scale * x + mask) with mask(r, c) = -inf
+// for c > (r mod period) + offset (period == 0: no mask).  Columns past a
+// row's limit are never loaded: they count as -inf, so they add nothing to
+// the sum and their outputs are exactly 0.  The product scale * x is formed
+// in fp32.
+
+struct Fused {
+  float scale;
+  int64_t period;
+  int64_t offset;
+};
+
+// Last kept column of `row` (inclusive), clamped to [-1, cols - 1].
+__device__ __forceinline__ int fused_limit(const Fused& f, int64_t row, int cols) {
+  if (f.period <= 0) return cols - 1;
+  const int64_t lim = row % f.period + f.offset;
+  return lim < -1 ? -1 : (lim > cols - 1 ? cols - 1 : (int)lim);
+}
+
+// Columns col0 .. col0 + VW - 1 of one vector: scale the kept ones, -inf the
+// rest (their loads were skipped or are beyond the limit).
+template <int VW>
+__device__ __forceinline__ void fused_apply(float (&v)[VW], int col0, int lim, float scale) {
+#pragma unroll
+  for (int i = 0; i < VW; ++i) v[i] = (col0 + i <= lim) ? v[i] * scale : -__builtin_inff();
+}
+
 // ---- online (max, sum) ------------------------------------------------------
 
 // Rescale factor of a partial sum taken relative to max m when the reference

@@ -20,10 +20,10 @@
 
 namespace rowsm {
 
-template <typename In, typename Out, int VW, int LPR, int RPL>
+template <typename In, typename Out, int VW, int LPR, int RPL, bool FUSED>
 __global__ __launch_bounds__(256) void small_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
-    int64_t rows, int cols) {
+    int64_t rows, int cols, Fused fz) {
   constexpr int RPW = kWave / LPR;     // rows per wave per load instruction
   constexpr int RPT = RPW * RPL;       // rows per wave per task
   const int lane = threadIdx.x & (kWave - 1);
@@ -46,10 +46,15 @@ __global__ __launch_bounds__(256) void small_row_kernel(
     const rsrc_t rx = make_rsrc(x + row0 * cols, (uint64_t)(nrows * cols) * In::bytes);
     const rsrc_t ry = make_rsrc(y + row0 * cols, (uint64_t)(nrows * cols) * Out::bytes);
 
+    int lim[RPL];
+#pragma unroll
+    for (int k = 0; k < RPL; ++k)
+      lim[k] = FUSED ? fused_limit(fz, row0 + k * RPW + grp, cols) : cols - 1;
+
     InVec<In, VW> v[RPL];
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
-      const bool ok = col_ok && (k * RPW + grp < nrows);
+      const bool ok = col_ok && (k * RPW + grp < nrows) && (!FUSED || sub * VW <= lim[k]);
       if (ok) v[k].load(rx, vin, k * group_elts * In::bytes);
       else v[k].set_neg_inf();
     }
@@ -59,6 +64,7 @@ __global__ __launch_bounds__(256) void small_row_kernel(
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
       v[k].to_float(f[k]);
+      if constexpr (FUSED) fused_apply(f[k], sub * VW, lim[k], fz.scale);
       float t = f[k][0];
 #pragma unroll
       for (int i = 1; i < VW; ++i) t = fmax_nn(t, f[k][i]);

@@ -1,0 +1,54 @@
+// Launch of the single-read split-row kernels: grid sizing from occupancy,
+// and the per-device exchange workspace (launch_split_common.hip).
+#pragma once
+
+#include "launch.hpp"
+#include "split_row.hpp"
+
+namespace rowsm {
+
+constexpr int kSplitMaxBlocks = 1 << 16;  // workspace capacity in blocks
+
+// A split launch in progress: split_begin takes the device's split lock,
+// orders the launch after the previous split launch on the device (whatever
+// its stream), reserves ntags row tags and hands out the workspace;
+// split_end records the launch for the next one and releases the lock.
+struct SplitTicket {
+  int dev = -1;
+  SplitWorkspace ws{};
+  uint32_t tag0 = 0;
+};
+int split_begin(hipStream_t st, uint64_t ntags, SplitTicket* t);
+int split_end(SplitTicket* t, hipStream_t st, bool launched);
+
+template <typename In, typename Out, int VW, int NV, bool FUSED>
+int launch_split_nv(const Call& c) {
+  const Plan& p = c.p;
+  auto kern = split_row_kernel<In, Out, VW, NV, FUSED>;
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
+                                                   p.block, 0) != hipSuccess)
+    return ROWSM_EHIP;
+  if (p.grid < 0 && per_cu > -p.grid) per_cu = (int)-p.grid;
+  const int64_t resident = (int64_t)per_cu * c.cus;
+  int64_t slots = resident / p.split;
+  if (slots > c.rows) slots = c.rows;
+  if (slots > kSplitMaxBlocks / p.split) slots = kSplitMaxBlocks / p.split;
+  if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
+  // The grid never exceeds one full residency of the device (see the
+  // co-residency note of split_row_kernel).
+  const unsigned grid = (unsigned)(slots * p.split);
+
+  SplitTicket t;
+  int r = split_begin(c.st, (uint64_t)((c.rows + slots - 1) / slots), &t);
+  if (r != ROWSM_OK) return r;
+  (void)hipGetLastError();
+  kern<<<dim3(grid), dim3(p.block), 0, c.st>>>(
+      static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
+      c.rows, c.cols, p.split, t.ws, t.tag0, fused_or_identity(c));
+  const bool launched = hipGetLastError() == hipSuccess;
+  r = split_end(&t, c.st, launched);
+  return launched ? r : ROWSM_EHIP;
+}
+
+}  // namespace rowsm

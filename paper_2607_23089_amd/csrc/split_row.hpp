@@ -8,6 +8,9 @@
 // compile time, so only the last slot can be partial and every load
 // instruction of a wave reads 64 consecutive vectors.
 //
+// FUSED computes softmax(scale * x + causal mask) (see Fused): columns past
+// the row's limit are not loaded and come out as exact zeros.
+//
 // Statistics.  Each block reduces its share to a pair (m_b, s_b): m_b the
 // block's maximum and s_b = sum exp(x - m_b) over its entries (a block that
 // holds only -inf reports (-inf, 0)).  The pairs are exchanged through global
@@ -59,10 +62,10 @@ struct SplitWorkspace {
 // launch, so even a broken exchange lets the whole grid drain quickly.
 constexpr uint32_t kSplitSpinLimit = 1u << 20;
 
-template <typename In, typename Out, int VW, int NV>
+template <typename In, typename Out, int VW, int NV, bool FUSED>
 __global__ __launch_bounds__(1024) void split_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
-    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0) {
+    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0, Fused fz) {
   __shared__ float red_m[16];
   __shared__ float red_s[16];
   __shared__ float bcast[2];
@@ -90,16 +93,22 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
     const rsrc_t rx = make_rsrc(x + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * Out::bytes);
 
+    const int lim = FUSED ? fused_limit(fz, row, cols) : cols - 1;
     float f[NV][VW];
     {
       InVec<In, VW> v[NV];
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
-        if (s < NV - 1 || last_ok) v[s].load(rx, vin, s * sin);
-        else v[s].set_neg_inf();
+        if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim))
+          v[s].load(rx, vin, s * sin);
+        else
+          v[s].set_neg_inf();
       }
 #pragma unroll
-      for (int s = 0; s < NV; ++s) v[s].to_float(f[s]);
+      for (int s = 0; s < NV; ++s) {
+        v[s].to_float(f[s]);
+        if constexpr (FUSED) fused_apply(f[s], (s * RT + g) * VW, lim, fz.scale);
+      }
     }
 
     // Block maximum.

@@ -97,6 +97,18 @@ def test_bad_variant_and_config(lib):
         assert st == R.EINVAL, cfg
 
 
+def test_scaled_causal_argument_errors(lib):
+    f = R.rowsm_forward_scaled_causal
+    assert f(X, Y, 4, 8, R.F32, R.F32, 0.5, -1, 0, 0) == R.EINVAL       # negative period
+    assert f(X, Y, 4, 8, 9, R.F32, 0.5, 4, 0, 0) == R.EDTYPE
+    assert f(X, Y, -4, 8, R.F32, R.F32, 0.5, 4, 0, 0) == R.EINVAL
+    assert f(0, 0, 0, 8, R.F32, R.F32, 0.5, 4, 0, 0) == R.OK             # empty
+    assert f(X, X + 4, 4, 8, R.F32, R.F32, 0.5, 4, 0, 0) == R.EINVAL     # overlap
+    for cfg in (dict(variant=R.MEDIUM, packed=1), dict(variant=R.SMALL, rows_per_lane=2),
+                dict(variant=R.SMALL, lanes_per_row=3)):
+        assert f(X, Y, 64, 64, R.BF16, R.BF16, 0.5, 4, 0, 0, R.RowsmConfig(**cfg)) == R.EINVAL
+
+
 def test_select_regimes(lib):
     s = R.rowsm_select
     # row of <= 32 vectors -> SMALL

@@ -24,12 +24,19 @@ from paper_2607_23089_amd import build as B
 
 @pytest.fixture(scope="module")
 def asm(tmp_path_factory):
-    out = tmp_path_factory.mktemp("asm") / "rowsm.s"
-    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I", B.INCLUDE, "-I", B.CSRC, "-o", str(out)] + B.SOURCES
-    subprocess.run(cmd, check=True, capture_output=True)
-    return out.read_text()
+    from concurrent.futures import ThreadPoolExecutor
+    d = tmp_path_factory.mktemp("asm")
+
+    def one(src):
+        out = d / (os.path.basename(src) + ".s")
+        cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only",
+               "-S", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-I", B.INCLUDE, "-I", B.CSRC, "-o", str(out), src]
+        subprocess.run(cmd, check=True, capture_output=True)
+        return out.read_text()
+
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as pool:
+        return "\n".join(pool.map(one, B.SOURCES))
 
 
 def kernels(asm):
@@ -59,12 +66,15 @@ def test_no_immediate_overwrite_of_store_data(asm):
 
 
 @pytest.mark.parametrize("pattern", [
-    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4E",        # small_262144x64
-    r"medium_row_kernelINS_4BF16ES1_Li8ELi4ELb0E",       # causal_32768x4096
-    r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0E",        # fp32_64x1000
-    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi15E",      # vocab_4096x151936
-    r"split_row_kernelINS_3F32ES1_Li4ELi16E",            # large_1024x262144
-    r"large_row_kernelINS_3F32ES1_Li4ELi4E",             # two-pass form
+    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELb0E",      # small_262144x64
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELb0E",     # causal_32768x4096
+    r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0ELb0E",      # fp32_64x1000
+    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELb0E",    # vocab_4096x151936
+    r"split_row_kernelINS_3F32ES1_Li4ELi16ELb0E",          # large_1024x262144
+    r"large_row_kernelINS_3F32ES1_Li4ELi4ELb0E",           # two-pass form
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELb1E",     # fused causal 32768x4096
+    r"split_row_kernelINS_3F32ES1_Li4ELi8ELb1E",           # fused f32 long rows
+    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELb1E",      # fused small rows
 ])
 def test_workload_kernels_do_not_spill(asm, pattern):
     ks = {k: v for k, v in kernels(asm).items() if re.search(pattern, k)}
@@ -77,7 +87,7 @@ def test_split_exchange_has_no_cache_maintenance(asm):
     # The exchange words are self-validating 64-bit atomics: no L2 write-back
     # or invalidation may appear in the split kernel (each one serialises the
     # whole device), and the polls and stores are device-coherent (sc1).
-    body = asm[asm.index("split_row_kernelINS_3F32ES1_Li4ELi16E"):]
+    body = asm[asm.index("split_row_kernelINS_3F32ES1_Li4ELi16ELb0E"):]
     body = body[:body.index("s_endpgm")]
     assert "buffer_wbl2" not in body and "buffer_inv" not in body
     assert "s_sleep" in body
