@@ -131,6 +131,17 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
           if constexpr (FUSED) fused_apply(f[s], (s * T + t) * VW, lim, fz.scale);
         }
       }
+      if constexpr (FUSED) {
+        // Vectors wholly past the limit are zeros whatever the row's max and
+        // sum: store them now, overlapping the loads and the reductions.
+        float z[VW];
+#pragma unroll
+        for (int i = 0; i < VW; ++i) z[i] = 0.0f;
+#pragma unroll
+        for (int s = 0; s < NV; ++s)
+          if (row_ok && (s < NV - 1 || last_ok) && (s * T + t) * VW > lim)
+            store_out<Out, VW>(ry, vout + s * sout, z);
+      }
       float mx = -__builtin_inff();
 #pragma unroll
       for (int s = 0; s < NV; ++s)
@@ -141,18 +152,19 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
       float sum = 0.0f;
 #pragma unroll
       for (int s = 0; s < NV; ++s)
-#pragma unroll
-        for (int i = 0; i < VW; ++i) {
-          f[s][i] = exp2_fast(__builtin_fmaf(f[s][i], kLog2e, nml));
-          sum += f[s][i];
-        }
+        exp_accumulate<FUSED>(f[s], nml, (s * T + t) * VW <= lim, &sum);
       sum = block_row_reduce<SumOp>(sum, wpr, wave, g, lane, red_s);
       const float inv = __builtin_amdgcn_rcpf(sum);  // v_rcp_f32, 1 ulp
+      // A row whose sum is not >= 1 (nothing kept, or a NaN/+inf among the
+      // kept values) is all NaN, masked columns included: rewrite those too.
+      const bool redo_masked = FUSED && !(sum > 0.5f);
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
 #pragma unroll
         for (int i = 0; i < VW; ++i) f[s][i] *= inv;
-        if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(ry, vout + s * sout, f[s]);
+        if (row_ok && (s < NV - 1 || last_ok) &&
+            (!FUSED || (s * T + t) * VW <= lim || redo_masked))
+          store_out<Out, VW>(ry, vout + s * sout, f[s]);
       }
     }
   }

@@ -158,9 +158,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // forced.  Fewer values per lane and more resident rows measured faster
     // than longer per-lane rows on the 32768 x 4096 workload.
     if (want_packed != 1) {
-      // Fused rows keep column indices live as well: at most 32 values.
+      // Fused rows keep column indices live as well: at most 32 values, and
+      // 32 (fewer waves per row) measured fastest on the causal workload.
       for (int cap_vals : {16, 32, 64}) {
-        if (fused && cap_vals > 32) break;
+        if (fused && cap_vals != 32) continue;
         for (int w = 1; w <= 16; w <<= 1) {
           if (want_wpr && w != want_wpr) continue;
           const int v = (int)cdiv(nvec, (int64_t)w * kWave);
@@ -193,9 +194,11 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->vpl = vpl;
     p->packed = packed;
     p->nv = vpl;
-    // 512-thread blocks (fewer rows per block when a row needs more than 8
-    // waves); one block per row group, no grid-stride loop unless capped.
-    int rpb = wpr >= 8 ? 1 : 8 / wpr;
+    // 512-thread blocks (256 for the fused form, fewer rows per block when a
+    // row needs more waves); one block per row group, no grid-stride loop
+    // unless capped.
+    const int waves_per_block = fused ? 4 : 8;
+    int rpb = wpr >= waves_per_block ? 1 : waves_per_block / wpr;
     if (cfg && cfg->rows_per_block > 0) {
       rpb = cfg->rows_per_block;
       if (rpb * wpr > 16) return ROWSM_EINVAL;

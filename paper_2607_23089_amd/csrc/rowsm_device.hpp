@@ -273,8 +273,30 @@ __device__ __forceinline__ int fused_limit(const Fused& f, int64_t row, int cols
 // rest (their loads were skipped or are beyond the limit).
 template <int VW>
 __device__ __forceinline__ void fused_apply(float (&v)[VW], int col0, int lim, float scale) {
+  if (col0 + VW - 1 <= lim) {  // whole vector kept: the common case
 #pragma unroll
-  for (int i = 0; i < VW; ++i) v[i] = (col0 + i <= lim) ? v[i] * scale : -__builtin_inff();
+    for (int i = 0; i < VW; ++i) v[i] *= scale;
+  } else {
+#pragma unroll
+    for (int i = 0; i < VW; ++i) v[i] = (col0 + i <= lim) ? v[i] * scale : -__builtin_inff();
+  }
+}
+
+// exp(v - m) for the VW values of one vector, added to *sum.  A fused
+// vector wholly past the row's limit holds only -inf: its exponentials are
+// exactly 0 and are not evaluated.
+template <bool FUSED, int VW>
+__device__ __forceinline__ void exp_accumulate(float (&v)[VW], float nml, bool live, float* sum) {
+  if (!FUSED || live) {
+#pragma unroll
+    for (int i = 0; i < VW; ++i) {
+      v[i] = exp2_fast(__builtin_fmaf(v[i], kLog2e, nml));
+      *sum += v[i];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VW; ++i) v[i] = 0.0f;
+  }
 }
 
 // ---- online (max, sum) ------------------------------------------------------

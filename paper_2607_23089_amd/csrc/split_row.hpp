@@ -110,6 +110,17 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
         if constexpr (FUSED) fused_apply(f[s], (s * RT + g) * VW, lim, fz.scale);
       }
     }
+    if constexpr (FUSED) {
+      // Vectors wholly past the limit are zeros whatever the row's max and
+      // sum: store them now, overlapping the loads and the exchange.
+      float z[VW];
+#pragma unroll
+      for (int i = 0; i < VW; ++i) z[i] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < NV; ++s)
+        if ((s < NV - 1 || last_ok) && (s * RT + g) * VW > lim)
+          store_out<Out, VW>(ry, vout + s * sout, z);
+    }
 
     // Block maximum.
     float mb = ninf;
@@ -128,11 +139,7 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
     float sb = 0.0f;
 #pragma unroll
     for (int s = 0; s < NV; ++s)
-#pragma unroll
-      for (int i = 0; i < VW; ++i) {
-        f[s][i] = exp2_fast(__builtin_fmaf(f[s][i], kLog2e, nml));
-        sb += f[s][i];
-      }
+      exp_accumulate<FUSED>(f[s], nml, (s * RT + g) * VW <= lim, &sb);
     sb = group_reduce<kWave, SumOp>(sb);
     if (lane == 0) red_s[wave] = sb;
     __syncthreads();
@@ -171,16 +178,19 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
       if (lane == 0) {
         // y = exp(x - m_b) * exp(m_b - M) / S
         bcast[0] = exp2_fast((mb - p.m) * kLog2e) * __builtin_amdgcn_rcpf(p.s);
+        bcast[1] = (p.s > 0.5f) ? 0.0f : 1.0f;  // row without a normal sum: all NaN
       }
     }
     __syncthreads();
     const float scale = bcast[0];
+    const bool redo_masked = FUSED && bcast[1] != 0.0f;
 
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
 #pragma unroll
       for (int i = 0; i < VW; ++i) f[s][i] *= scale;
-      if (s < NV - 1 || last_ok) store_out<Out, VW>(ry, vout + s * sout, f[s]);
+      if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim || redo_masked))
+        store_out<Out, VW>(ry, vout + s * sout, f[s]);
     }
     // LDS reuse across rows: red_m is rewritten after this row's last barrier,
     // which every wave passes only after reading red_m (before the second

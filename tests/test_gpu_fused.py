@@ -77,18 +77,39 @@ def test_fully_masked_rows_are_nan_and_masked_entries_zero():
         assert torch.all(y[r, q:] == 0) and torch.all(y[r, :q] > 0)
 
 
+@pytest.mark.parametrize("fam,cols", [(R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 40000),
+                                      (R.LARGE, 70001)])
+def test_fused_special_rows(fam, cols):
+    # NaN or +inf among the kept columns makes the whole row NaN, masked
+    # columns included (0 / NaN); -inf among the kept ones is an ordinary 0.
+    x = W.random_matrix(8, cols, "f32", sigma=2.0, seed=2)
+    x[1, 0] = float("nan")
+    x[2, 1] = float("inf")
+    x[3, 0] = float("-inf")
+    x[5, 0] = float("nan")     # kept for query 5 % 4 = 1 (columns 0..1)
+    cfg = R.RowsmConfig(variant=fam) if cols != 70001 else R.RowsmConfig(variant=fam,
+                                                                          split_blocks=-1)
+    for din, dout in PAIRS:
+        xx = x.to(DT[din])
+        y = run_fused(xx.to(DEV), dout, 1.5, 4, 0, config=cfg)
+        assert_fused_parity(xx, y, dout, 1.5, 4, 0, f"special {fam} {cols} {din}->{dout}")
+
+
 def test_causal_workload_in_kernel_mask_matches_stored_mask():
     # The causal workload at full size: softmax with the mask computed in the
     # kernel from the indices (x holds no -inf) must equal, bit for bit, the
-    # plain kernel on the same scores with the mask stored as -inf (same
-    # launch shape, same arithmetic: scale 1 multiplies exactly).
+    # plain kernel on the same scores with the mask stored as -inf (in the
+    # same launch shape, same arithmetic: scale 1 multiplies exactly).
     w = W.WORKLOADS["causal_32768x4096"]
     xm = W.make_input(w, device=DEV)                       # mask stored as -inf
     g = torch.Generator(device=DEV).manual_seed(0)
     x = (torch.randn(w.rows, w.cols, generator=g, device=DEV) * w.sigma).to(torch.bfloat16)
     assert torch.equal(torch.where(torch.isinf(xm), xm, x), xm)
-    y_plain = R.softmax(xm)
     y_fused = R.scaled_causal_softmax(x, 1.0, w.period, 0)
+    # the plain form forced to the fused form's launch shape (2 waves per row,
+    # 2 rows per block) sums in the same order
+    same_shape = R.RowsmConfig(variant=R.MEDIUM, waves_per_row=2, rows_per_block=2)
+    y_plain = R.softmax(xm, config=same_shape)
     torch.cuda.synchronize()
     assert torch.equal(y_plain, y_fused)
     for r in (0, 1, 4095, 4096, 20000, 32767):
