@@ -14,6 +14,9 @@ Contents
   * ``softmax_scaled_causal_f64`` -- the same definition applied to
                          scale * x with a causal mask from the indices
                          (scaled attention scores).
+  * ``log_softmax_f64``  -- x - max - log(sum exp(x - max)) per row.
+  * ``softmax_backward_f64`` -- dx = y * (dy - sum(y * dy)) per row, the
+                         softmax Jacobian applied to dy.
   * ``widen_f32`` / ``widen_bf16_bits`` -- exact widening of the stored input
                          bit patterns to fp64 (bf16 -> bits << 16 -> fp32 ->
                          fp64), so the oracle sees exactly the values the GPU
@@ -70,6 +73,14 @@ def load(path: str | None = None):
     fn.restype = ctypes.c_int
     fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                    ctypes.c_int64, ctypes.c_int]
+    fn = lib.oracle_log_softmax_f64
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_int64, ctypes.c_int]
+    fn = lib.oracle_softmax_backward_f64
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_int64, ctypes.c_int]
     fn = lib.oracle_softmax_scaled_causal_f64
     fn.restype = ctypes.c_int
     fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
@@ -96,6 +107,38 @@ def softmax_f64(x: np.ndarray, threads: int = 1, lib=None) -> np.ndarray:
     if rc != 0:
         raise RuntimeError(f"oracle_softmax_f64 failed with status {rc}")
     return y.reshape(shape)
+
+
+def log_softmax_f64(x: np.ndarray, threads: int = 1, lib=None) -> np.ndarray:
+    """y = log_softmax(x, axis=-1) in fp64 (2-D, rows x cols)."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    if x.ndim == 1:
+        x = x[None, :]
+    y = np.full_like(x, np.nan)
+    lib = lib if lib is not None else load()
+    rc = lib.oracle_log_softmax_f64(x.ctypes.data, y.ctypes.data, x.shape[0], x.shape[1],
+                                    int(threads))
+    if rc != 0:
+        raise RuntimeError(f"oracle_log_softmax_f64 failed with status {rc}")
+    return y
+
+
+def softmax_backward_f64(y: np.ndarray, dy: np.ndarray, threads: int = 1,
+                         lib=None) -> np.ndarray:
+    """dx = y * (dy - rowsum(y * dy)) in fp64 (2-D, rows x cols)."""
+    y = np.ascontiguousarray(np.asarray(y, dtype=np.float64))
+    dy = np.ascontiguousarray(np.asarray(dy, dtype=np.float64))
+    if y.ndim == 1:
+        y, dy = y[None, :], dy[None, :]
+    if y.shape != dy.shape:
+        raise ValueError("y and dy must have the same shape")
+    dx = np.full_like(y, np.nan)
+    lib = lib if lib is not None else load()
+    rc = lib.oracle_softmax_backward_f64(y.ctypes.data, dy.ctypes.data, dx.ctypes.data,
+                                         y.shape[0], y.shape[1], int(threads))
+    if rc != 0:
+        raise RuntimeError(f"oracle_softmax_backward_f64 failed with status {rc}")
+    return dx
 
 
 def softmax_scaled_causal_f64(x: np.ndarray, scale: float, period: int, offset: int,

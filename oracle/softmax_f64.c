@@ -57,6 +57,41 @@ static void oracle_row(const double *x, double *y, int64_t cols)
 }
 
 /*
+ * Log-softmax of one row: y_j = x_j - m - log(sum_k exp(x_k - m)), i.e. the
+ * logarithm of the softmax above written without forming the quotient (its
+ * tiny entries would underflow).  Same special values: a NaN or +inf entry,
+ * or a row of only -inf, gives an all-NaN row; a -inf entry in a row with a
+ * finite maximum gives -inf.
+ */
+static void oracle_row_log(const double *x, double *y, int64_t cols)
+{
+    double m = -INFINITY;
+    for (int64_t j = 0; j < cols; ++j)
+        m = fmax(m, x[j]); /* fmax skips a NaN operand, as the comparison above */
+    double sum_e = 0.0;
+    for (int64_t j = 0; j < cols; ++j)
+        sum_e += exp(x[j] - m);
+    double lse = m + log(sum_e);
+    for (int64_t j = 0; j < cols; ++j)
+        y[j] = x[j] - lse;
+}
+
+/*
+ * Softmax backward of one row: given y = softmax(x) and the gradient dy of a
+ * loss with respect to y, dx_j = y_j * (dy_j - sum_k y_k dy_k).  This is the
+ * product of the softmax Jacobian (diag(y) - y y^T, symmetric) with dy,
+ * written out.
+ */
+static void oracle_row_backward(const double *yv, const double *dy, double *dx, int64_t cols)
+{
+    double dot = 0.0;
+    for (int64_t k = 0; k < cols; ++k)
+        dot += yv[k] * dy[k];
+    for (int64_t j = 0; j < cols; ++j)
+        dx[j] = yv[j] * (dy[j] - dot);
+}
+
+/*
  * Scaled, causally masked rows (attention scores): row r is treated as query
  * q = r mod period, and column c survives when c <= q + offset; the others
  * are -inf.  The row is t_j = scale * x_j for surviving columns, -inf
@@ -75,28 +110,36 @@ static void oracle_row_scaled_causal(const double *x, double *y, double *t, int6
     oracle_row(t, y, cols);
 }
 
+enum { ORACLE_SOFTMAX = 0, ORACLE_FUSED = 1, ORACLE_LOG = 2, ORACLE_BACKWARD = 3 };
+
 struct oracle_job {
-    const double *x;
-    double *y;
+    const double *x;   /* backward: y */
+    double *y;         /* backward: dx */
     int64_t row_begin, row_end, cols;
-    int fused;
+    int kind;
     double scale;
     int64_t period, offset;
+    const double *dy;  /* backward only */
 };
 
 static void *oracle_worker(void *arg)
 {
     const struct oracle_job *job = (const struct oracle_job *)arg;
     double *t = NULL;
-    if (job->fused) {
+    if (job->kind == ORACLE_FUSED) {
         t = (double *)malloc((size_t)job->cols * sizeof(double));
         if (!t)
             return NULL; /* rows stay unwritten; the wrapper fills NaN first */
     }
     for (int64_t r = job->row_begin; r < job->row_end; ++r) {
-        if (job->fused)
-            oracle_row_scaled_causal(job->x + r * job->cols, job->y + r * job->cols, t, r,
-                                     job->cols, job->scale, job->period, job->offset);
+        const int64_t o = r * job->cols;
+        if (job->kind == ORACLE_FUSED)
+            oracle_row_scaled_causal(job->x + o, job->y + o, t, r, job->cols, job->scale,
+                                     job->period, job->offset);
+        else if (job->kind == ORACLE_LOG)
+            oracle_row_log(job->x + o, job->y + o, job->cols);
+        else if (job->kind == ORACLE_BACKWARD)
+            oracle_row_backward(job->x + o, job->dy + o, job->y + o, job->cols);
         else
             oracle_row(job->x + r * job->cols, job->y + r * job->cols, job->cols);
     }
@@ -159,7 +202,7 @@ int oracle_softmax_f64(const double *x, double *y, int64_t rows, int64_t cols,
         return 0;
     if (!x || !y)
         return -1;
-    struct oracle_job proto = {x, y, 0, 0, cols, 0, 1.0, 0, 0};
+    struct oracle_job proto = {x, y, 0, 0, cols, ORACLE_SOFTMAX, 1.0, 0, 0, NULL};
     return oracle_run(proto, rows, threads);
 }
 
@@ -179,6 +222,40 @@ int oracle_softmax_scaled_causal_f64(const double *x, double *y, int64_t rows,
         return 0;
     if (!x || !y)
         return -1;
-    struct oracle_job proto = {x, y, 0, 0, cols, 1, scale, period, offset};
+    struct oracle_job proto = {x, y, 0, 0, cols, ORACLE_FUSED, scale, period, offset, NULL};
+    return oracle_run(proto, rows, threads);
+}
+
+/*
+ * oracle_log_softmax_f64: y = log_softmax(x, dim=-1) (oracle_row_log).  Same
+ * arguments and return codes as oracle_softmax_f64.
+ */
+int oracle_log_softmax_f64(const double *x, double *y, int64_t rows, int64_t cols,
+                           int threads)
+{
+    if (rows < 0 || cols < 0)
+        return -1;
+    if (rows == 0 || cols == 0)
+        return 0;
+    if (!x || !y)
+        return -1;
+    struct oracle_job proto = {x, y, 0, 0, cols, ORACLE_LOG, 1.0, 0, 0, NULL};
+    return oracle_run(proto, rows, threads);
+}
+
+/*
+ * oracle_softmax_backward_f64: dx = y * (dy - rowsum(y * dy)) for rows x cols
+ * fp64 matrices y, dy, dx (oracle_row_backward).  Return codes as above.
+ */
+int oracle_softmax_backward_f64(const double *y, const double *dy, double *dx, int64_t rows,
+                                int64_t cols, int threads)
+{
+    if (rows < 0 || cols < 0)
+        return -1;
+    if (rows == 0 || cols == 0)
+        return 0;
+    if (!y || !dy || !dx)
+        return -1;
+    struct oracle_job proto = {y, dx, 0, 0, cols, ORACLE_BACKWARD, 1.0, 0, 0, dy};
     return oracle_run(proto, rows, threads);
 }

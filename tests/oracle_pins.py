@@ -289,3 +289,136 @@ def run_fused_pins(smf, sm_plain) -> list:
     if not (np.all(np.isnan(yn[0])) and np.all(np.isnan(yn[4])) and not np.isnan(yn[1, 0])):
         fail("empty_row_nan", "query 0 with offset -1 should keep nothing")
     return fails
+
+
+# ---------------------------------------------------------------------------
+# Log-softmax: y_j = x_j - log(sum_k exp(x_k)).
+
+def brute_force_log_softmax(x):
+    """50-digit y_i = -log(sum_j exp(x_j - x_i)): a different formula (no max,
+    no separate log of a sum of shifted terms)."""
+    import mpmath
+    mpmath.mp.dps = 50
+    x = np.asarray(x, dtype=np.float64)
+    out = np.empty_like(x)
+    for r in range(x.shape[0]):
+        row = [mpmath.mpf(float(v)) for v in x[r]]
+        for i, xi in enumerate(row):
+            if mpmath.isinf(xi) and xi < 0:
+                out[r, i] = -np.inf
+                continue
+            tot = mpmath.mpf(0)
+            for xj in row:
+                if not (mpmath.isinf(xj) and xj < 0):
+                    tot += mpmath.exp(xj - xi)
+            out[r, i] = float(-mpmath.log(tot))
+    return out
+
+
+def run_log_pins(lsm) -> list:
+    fails = []
+
+    def fail(name, msg):
+        fails.append(f"{name}: {msg}")
+
+    for x in brute_force_inputs():
+        y = np.asarray(lsm(x))
+        v = brute_force_log_softmax(x)
+        fin = np.isfinite(v)
+        m = np.max(np.where(np.isneginf(x), -np.inf, x), axis=1, keepdims=True)
+        tol = (8.0 + x.shape[1]) * 2.0 ** -52 * (1.0 + np.abs(x) + np.abs(m) + np.abs(v))
+        ok = y.shape == v.shape and np.array_equal(np.isneginf(y), np.isneginf(v)) and \
+            np.array_equal(np.isnan(y), np.isnan(v))
+        if ok:
+            ok = bool(np.all(np.abs(y[fin] - v[fin]) <= tol[fin]))
+        if not ok:
+            fail("log_brute_force", f"shape {x.shape}")
+    rng = np.random.default_rng(11)
+    x = rng.normal(0.0, 3.0, size=(10, 57))
+    y = np.asarray(lsm(x))
+    if not np.all(np.abs(np.exp(y).sum(axis=1) - 1.0) <= 64 * 2.0 ** -52):
+        fail("log_normalised", "sum exp(y) != 1")
+    d_y = y[:, :, None] - y[:, None, :]
+    d_x = x[:, :, None] - x[:, None, :]
+    if not np.all(np.abs(d_y - d_x) <= 8 * 2.0 ** -52 * (np.abs(y).max() + np.abs(x).max())):
+        fail("log_differences", "y_i - y_j != x_i - x_j")
+    for cols in (1, 7, 1000):
+        yc = np.asarray(lsm(np.zeros((2, cols))))
+        if not np.all(yc == -np.log(float(cols))):
+            fail("log_constant_row", f"cols={cols}")
+    xd = np.full((2, 9), -1000.0)
+    xd[:, 4] = 0.0
+    yd = np.asarray(lsm(xd))
+    if not (np.all(yd[:, 4] == 0.0) and np.all(yd[:, :4] == -1000.0)):
+        fail("log_dominant", f"{yd[0].tolist()}")
+    xs = np.array([[np.nan, 1.0], [np.inf, 1.0], [-np.inf, -np.inf], [-np.inf, 2.0]])
+    ys = np.asarray(lsm(xs))
+    if not (np.all(np.isnan(ys[:3])) and ys[3, 0] == -np.inf and ys[3, 1] == 0.0):
+        fail("log_special_rows", f"{ys.tolist()}")
+    return fails
+
+
+# ---------------------------------------------------------------------------
+# Softmax backward: dx = y * (dy - sum(y * dy)).
+
+def brute_force_backward(y, dy):
+    """50-digit product of the softmax Jacobian J = diag(y) - y y^T with dy,
+    formed as a full matrix (the oracle uses a dot product instead)."""
+    import mpmath
+    mpmath.mp.dps = 50
+    out = np.empty_like(np.asarray(y, dtype=np.float64))
+    for r in range(y.shape[0]):
+        yr = [mpmath.mpf(float(v)) for v in y[r]]
+        dr = [mpmath.mpf(float(v)) for v in dy[r]]
+        n = len(yr)
+        for i in range(n):
+            acc = mpmath.mpf(0)
+            for j in range(n):
+                jac = yr[i] * ((1 if i == j else 0) - yr[j])
+                acc += jac * dr[j]
+            out[r, i] = float(acc)
+    return out
+
+
+def run_backward_pins(bwd, sm) -> list:
+    """bwd(y, dy) -> dx; sm = the pinned softmax oracle (for finite
+    differences and for probability rows)."""
+    fails = []
+
+    def fail(name, msg):
+        fails.append(f"{name}: {msg}")
+
+    rng = np.random.default_rng(5)
+    for cols in (1, 2, 5, 16, 33):
+        y = np.asarray(sm(rng.normal(0.0, 2.0, size=(4, cols))))
+        dy = rng.normal(0.0, 1.0, size=(4, cols))
+        dx = np.asarray(bwd(y, dy))
+        v = brute_force_backward(y, dy)
+        tol = (16.0 + cols) * 2.0 ** -52 * (np.abs(y) * (np.abs(dy) + np.sum(np.abs(y * dy), axis=1,
+                                                                            keepdims=True)) + 1e-300)
+        if not (dx.shape == v.shape and np.all(np.abs(dx - v) <= tol)):
+            fail("backward_brute_force", f"cols={cols}")
+    # the gradient of L(x) = sum(dy * softmax(x)) by central differences
+    x = rng.normal(0.0, 1.5, size=(3, 12))
+    dy = rng.normal(0.0, 1.0, size=(3, 12))
+    y = np.asarray(sm(x))
+    dx = np.asarray(bwd(y, dy))
+    h = 1e-6
+    fd = np.empty_like(x)
+    for j in range(x.shape[1]):
+        xp, xm = x.copy(), x.copy()
+        xp[:, j] += h
+        xm[:, j] -= h
+        fd[:, j] = ((np.asarray(sm(xp)) * dy).sum(1) - (np.asarray(sm(xm)) * dy).sum(1)) / (2 * h)
+    if not np.all(np.abs(fd - dx) <= 1e-8):
+        fail("backward_finite_difference", f"max {np.max(np.abs(fd - dx)):.2e}")
+    # rows of a probability vector: sum(dx) = dot * (1 - sum(y)) = 0; adding a
+    # constant to dy changes nothing
+    y = np.asarray(sm(rng.normal(0.0, 3.0, size=(6, 50))))
+    dy = rng.normal(0.0, 1.0, size=(6, 50))
+    dx = np.asarray(bwd(y, dy))
+    if not np.all(np.abs(dx.sum(1)) <= 1e-14):
+        fail("backward_sum_zero", f"{np.abs(dx.sum(1)).max():.2e}")
+    if not np.allclose(np.asarray(bwd(y, dy + 3.0)), dx, rtol=0, atol=1e-14):
+        fail("backward_shift", "dy + c changed dx")
+    return fails
