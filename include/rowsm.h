@@ -74,6 +74,14 @@ typedef enum {
     ROWSM_LARGE = 3
 } rowsm_variant;
 
+/* Operations, for rowsm_describe_op. */
+typedef enum {
+    ROWSM_OP_SOFTMAX = 0,          /* rowsm_forward, rowsm_forward_config      */
+    ROWSM_OP_SCALED_CAUSAL = 1,    /* rowsm_forward_scaled_causal              */
+    ROWSM_OP_LOG_SOFTMAX = 2,      /* rowsm_log_softmax                        */
+    ROWSM_OP_SOFTMAX_BACKWARD = 3  /* rowsm_softmax_backward                   */
+} rowsm_op;
+
 /*
  * rowsm_forward: y = softmax(x, dim=-1) for a rows x cols matrix.
  *   x         device pointer, rows*cols elements of in_dtype
@@ -162,6 +170,63 @@ int rowsm_forward_scaled_causal(const void *x, void *y, int64_t rows, int64_t co
                                 int in_dtype, int out_dtype, float scale,
                                 int64_t causal_period, int64_t causal_offset,
                                 void *stream, const rowsm_config *cfg);
+
+/*
+ * rowsm_log_softmax: y = log(softmax(x, dim=-1)), written as
+ *     y[r, j] = (x[r, j] - m_r) - ln(sum_k exp(x[r, k] - m_r)),  m_r = max_k x[r, k]
+ * (the logarithm of the operation above, never formed as log of a quotient,
+ * so entries far below the maximum keep their value instead of underflowing
+ * to log(0)).  This is the cross-entropy input form of the operation; it is
+ * not part of the paper's operator set and follows the textbook definition.
+ * Special values: a row holding NaN or +inf, or only -inf, is all NaN; a -inf
+ * entry in a row with a finite maximum gives -inf.  Arguments, layout,
+ * dtypes, aliasing, errors and cfg as rowsm_forward_config (NULL cfg = the
+ * launcher's choice; every family and form of the plain operation is
+ * available).  fp32 accumulation; y in out_dtype.
+ */
+int rowsm_log_softmax(const void *x, void *y, int64_t rows, int64_t cols, int in_dtype,
+                      int out_dtype, void *stream, const rowsm_config *cfg);
+
+/*
+ * rowsm_softmax_backward: the gradient of softmax over the last dimension,
+ *     dx[r, j] = y[r, j] * (dy[r, j] - sum_k y[r, k] * dy[r, k]),
+ * i.e. the softmax Jacobian diag(y_r) - y_r y_r^T applied to dy_r, where y is
+ * the forward output and dy the gradient of a loss with respect to y (the
+ * textbook derivative of the operation; not part of the paper's operator
+ * set).
+ *   y, dy     device pointers, rows*cols elements of in_dtype each, row-major
+ *             and contiguous (row stride cols); read only; they may overlap
+ *             each other (even be the same buffer)
+ *   dx        device pointer, rows*cols elements of out_dtype; it may be y or
+ *             dy itself when in_dtype == out_dtype (in place), but must not
+ *             overlap either in any other way (ROWSM_EINVAL)
+ *   stream, rows, cols, dtypes, limits, errors: as rowsm_forward
+ *   cfg       NULL = the launcher's choice; otherwise as rowsm_forward_config
+ *             with these differences: y and dy are held in their raw form
+ *             (packed = 1 is ROWSM_EINVAL), a lane holds at most 128 bytes of
+ *             each input, and the single-read LARGE form uses 256-thread
+ *             blocks unless block is given.
+ * The dot product is accumulated in fp32 (fma), in a fixed order: results are
+ * deterministic for a given launch shape.  Special values follow IEEE
+ * arithmetic in the formula above: a NaN in y or dy makes the dot product,
+ * and with it the whole row of dx, NaN; an infinite product makes it +-inf
+ * (or NaN), and dx follows from the formula (e.g. -inf where y > 0, NaN where
+ * y == 0 or at the infinite entry).  y == 0 with a finite dot product gives
+ * an exact zero.  The single-read
+ * LARGE form shares the forward's device workspace and ordering (see
+ * rowsm_split_wait_failures).
+ */
+int rowsm_softmax_backward(const void *y, const void *dy, void *dx, int64_t rows, int64_t cols,
+                           int in_dtype, int out_dtype, void *stream, const rowsm_config *cfg);
+
+/*
+ * rowsm_describe_op: as rowsm_describe for any operation (op: rowsm_op) and
+ * launch overrides cfg (NULL = the launcher's choice).  Returns the status the
+ * operation would return for these arguments with valid, 256-byte aligned
+ * pointers; ROWSM_EINVAL for an unknown op.
+ */
+int rowsm_describe_op(int op, int64_t rows, int64_t cols, int in_dtype, int out_dtype,
+                      const rowsm_config *cfg, char *buf, int64_t len);
 
 /*
  * rowsm_describe: writes into buf (capacity len, always NUL-terminated when

@@ -85,3 +85,125 @@ def compare(y: np.ndarray, v: np.ndarray, out_dtype: str) -> dict:
         "zero_mismatch": zero_mismatch,
         "worst": worst,
     }
+
+
+# ---------------------------------------------------------------------------
+# Log-softmax outputs.
+#
+# The GPU computes y = (x - m) - ln(s) in fp32 with s = sum 2^((x - m) log2e).
+# Error sources (u = 2^-24): the rounding of x - m and of the final
+# difference, each <= u |v| (|x - m| <= |v| because ln(s) >= 0); the
+# relative error of s (exp2 and the summation: at most 64 terms summed
+# serially per lane in the register-resident forms, one tile of <= 32 plus
+# one addition per tile in the two-pass form (<= 16 tiles at the row lengths
+# it is tested on), then a tree of depth <= 30), <= ~94 u ~= 5.6e-6; and
+# v_log_f32 with the multiplication by ln 2, <= 2^-23 * ln(s) + u ~= 2.5e-6
+# for s <= 2^30.  Hence the fp32 bound 1e-5 + 2^-22 |v|.  A bf16 output adds
+# one bf16 ulp of v (round to nearest of a value already within the fp32
+# bound).
+
+LOG_ABS_TOL = 1e-5
+LOG_REL_TOL = 2.0 ** -22
+_OVERFLOW = {"f32": 2.0 ** 128 * (1 - 2.0 ** -25), "bf16": 2.0 ** 128 * (1 - 2.0 ** -9)}
+
+
+def compare_log(y: np.ndarray, v: np.ndarray, out_dtype: str) -> dict:
+    """Check a GPU log-softmax output ``y`` (widened to fp64) against the
+    oracle ``v``: NaN positions equal; -inf exactly where ``v`` rounds to -inf
+    in the output dtype; elsewhere ``|y - v| <= 1e-5 + 2^-22 |v|`` (fp32)
+    plus one bf16 ulp of v (bf16)."""
+    y = np.asarray(y, dtype=np.float64).ravel()
+    v = np.asarray(v, dtype=np.float64).ravel()
+    if y.shape != v.shape:
+        raise ValueError(f"shape mismatch {y.shape} vs {v.shape}")
+    if out_dtype not in _OVERFLOW:
+        raise ValueError(f"unknown out_dtype {out_dtype!r}")
+    ny, nv = np.isnan(y), np.isnan(v)
+    nan_mismatch = int(np.count_nonzero(ny != nv))
+    v_inf = np.isinf(v) | (np.abs(np.where(nv, 0.0, v)) >= _OVERFLOW[out_dtype])
+    v_out = np.where(v_inf & ~nv, np.copysign(np.inf, v), v)
+    inf_mismatch = int(np.count_nonzero((np.isinf(y) | np.isinf(v_out)) & ~(ny | nv)
+                                        & (y != v_out)))
+    fin = ~(ny | nv | np.isinf(y) | np.isinf(v_out))
+    with np.errstate(invalid="ignore"):
+        diff = np.where(fin, np.abs(y - v), 0.0)
+    tol = LOG_ABS_TOL + LOG_REL_TOL * np.abs(np.where(fin, v, 0.0))
+    if out_dtype == "bf16":
+        tol = tol + np.where(fin & (v != 0.0), ulp_bf16(np.where(fin & (v != 0.0), v, 1.0)), 0.0)
+    over = fin & (diff > tol)
+    ratio = np.where(fin, diff / tol, 0.0)
+    worst = int(np.argmax(ratio)) if ratio.size and ratio.max() > 0 else None
+    return {
+        "ok": nan_mismatch == 0 and inf_mismatch == 0 and not over.any(),
+        "n": int(v.size),
+        "max_abs": float(diff.max()) if diff.size else 0.0,
+        "max_tol_ratio": float(ratio.max()) if ratio.size else 0.0,
+        "n_over_tol": int(np.count_nonzero(over)),
+        "nan_mismatch": nan_mismatch,
+        "inf_mismatch": inf_mismatch,
+        "worst": worst,
+    }
+
+
+# ---------------------------------------------------------------------------
+# Softmax-backward outputs.
+#
+# The GPU computes d = sum_k y_k dy_k with fma in fp32 (a lane's chain of at
+# most 64 products in the register-resident forms, or one tile of <= 32
+# plus one addition per tile in the two-pass form, <= 16 tiles at the row
+# lengths it is tested on; then a lane tree of depth 6, at most 16 waves in
+# order and a tree over at most 64 blocks), so |d_gpu - d| <= 128 u S with
+# S = sum_k |y_k dy_k| and u = 2^-24 (first order).  Then dx_j =
+# y_j * (dy_j - d_gpu) adds two roundings.  Hence, per element,
+#     |dx_gpu - dx| <= |y_j| (2^-17 S + 2^-23 |dy_j - d|) + 2^-23 |dx_j|
+# (the single roundings doubled for margin), plus 2^-126 where the result is
+# below the normal range (a flushed subnormal), plus one bf16 ulp of dx_j for
+# bf16 output.  y_j == 0 must give an exact zero.
+
+BWD_DOT_REL = 2.0 ** -17
+BWD_ROUND = 2.0 ** -23
+
+
+def compare_backward(dx: np.ndarray, v: np.ndarray, y: np.ndarray, dy: np.ndarray,
+                     out_dtype: str) -> dict:
+    """Check a GPU softmax-backward output ``dx`` (widened to fp64) against the
+    oracle ``v``, given the fp64-widened inputs ``y`` and ``dy`` (rows x cols)."""
+    y = np.asarray(y, dtype=np.float64)
+    dy = np.asarray(dy, dtype=np.float64)
+    rows, cols = y.shape
+    dx = np.asarray(dx, dtype=np.float64).reshape(rows, cols)
+    v = np.asarray(v, dtype=np.float64).reshape(rows, cols)
+    if out_dtype not in ("f32", "bf16"):
+        raise ValueError(f"unknown out_dtype {out_dtype!r}")
+    ny, nv = np.isnan(dx), np.isnan(v)
+    nan_mismatch = int(np.count_nonzero(ny != nv))
+    inf_mismatch = int(np.count_nonzero((np.isinf(dx) | np.isinf(v)) & ~(ny | nv) & (dx != v)))
+    fin = np.isfinite(dx) & np.isfinite(v)
+    with np.errstate(invalid="ignore", over="ignore"):
+        S = np.sum(np.abs(y * dy), axis=1, keepdims=True)
+        d = np.sum(y * dy, axis=1, keepdims=True)
+        tol = np.abs(y) * (BWD_DOT_REL * S + BWD_ROUND * np.abs(dy - d)) + BWD_ROUND * np.abs(v)
+    tol = np.where(np.isfinite(tol), tol, np.inf)
+    tol = np.where(np.abs(v) < 2.0 ** -126, np.maximum(tol, 2.0 ** -126), tol)
+    if out_dtype == "bf16":
+        nz = fin & (v != 0.0)
+        tol = tol + np.where(nz, ulp_bf16(np.where(nz, v, 1.0)), 0.0)
+    zero = fin & (y == 0.0)
+    zero_mismatch = int(np.count_nonzero(zero & (dx != 0.0)))
+    with np.errstate(invalid="ignore"):
+        diff = np.where(fin, np.abs(dx - v), 0.0)
+    over = fin & (diff > tol)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(fin & (tol > 0), diff / np.where(tol > 0, tol, 1.0), 0.0)
+    worst = int(np.argmax(ratio)) if ratio.size and ratio.max() > 0 else None
+    return {
+        "ok": nan_mismatch == 0 and inf_mismatch == 0 and zero_mismatch == 0 and not over.any(),
+        "n": int(v.size),
+        "max_abs": float(diff.max()) if diff.size else 0.0,
+        "max_tol_ratio": float(ratio.max()) if ratio.size else 0.0,
+        "n_over_tol": int(np.count_nonzero(over)),
+        "nan_mismatch": nan_mismatch,
+        "inf_mismatch": inf_mismatch,
+        "zero_mismatch": zero_mismatch,
+        "worst": worst,
+    }

@@ -31,13 +31,15 @@ F32, BF16 = 0, 1
 AUTO, SMALL, MEDIUM, LARGE = 0, 1, 2, 3
 OK, EINVAL, EDTYPE, EHIP = 0, -1, -2, -3
 VARIANT_NAMES = {SMALL: "small", MEDIUM: "medium", LARGE: "large"}
+OP_SOFTMAX, OP_SCALED_CAUSAL, OP_LOG_SOFTMAX, OP_SOFTMAX_BACKWARD = 0, 1, 2, 3
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "librowsm.so")
 
 # Symbols declared in include/rowsm.h.
 EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
-           "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_describe",
+           "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_log_softmax",
+           "rowsm_softmax_backward", "rowsm_describe", "rowsm_describe_op",
            "rowsm_split_wait_failures", "rowsm_status_string")
 
 
@@ -88,6 +90,14 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     h.rowsm_forward_scaled_causal.argtypes = [vp, vp, i64, i64, i32, i32, ctypes.c_float,
                                               i64, i64, vp, ctypes.POINTER(RowsmConfig)]
     h.rowsm_forward_scaled_causal.restype = i32
+    h.rowsm_log_softmax.argtypes = fwd + [ctypes.POINTER(RowsmConfig)]
+    h.rowsm_log_softmax.restype = i32
+    h.rowsm_softmax_backward.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp,
+                                         ctypes.POINTER(RowsmConfig)]
+    h.rowsm_softmax_backward.restype = i32
+    h.rowsm_describe_op.argtypes = [i32, i64, i64, i32, i32, ctypes.POINTER(RowsmConfig),
+                                    ctypes.c_char_p, i64]
+    h.rowsm_describe_op.restype = i32
     h.rowsm_select.argtypes = [i64, i64, i32, i32]
     h.rowsm_select.restype = i32
     h.rowsm_describe.argtypes = [i64, i64, i32, i32, i32, ctypes.c_char_p, i64]
@@ -126,6 +136,13 @@ def rowsm_forward_scaled_causal(x, y, rows, cols, in_dtype, out_dtype, scale, ca
                                              causal_period, causal_offset, stream, ref)
 
 
+def rowsm_log_softmax(x, y, rows, cols, in_dtype, out_dtype, stream=0, cfg=None) -> int:
+    if cfg is not None and not isinstance(cfg, RowsmConfig):
+        cfg = RowsmConfig(**cfg)
+    ref = ctypes.byref(cfg) if cfg is not None else None
+    return lib().rowsm_log_softmax(x, y, rows, cols, in_dtype, out_dtype, stream, ref)
+
+
 def rowsm_select(rows, cols, in_dtype, out_dtype) -> int:
     return lib().rowsm_select(rows, cols, in_dtype, out_dtype)
 
@@ -134,6 +151,23 @@ def rowsm_describe(rows, cols, in_dtype, out_dtype, variant=AUTO):
     buf = ctypes.create_string_buffer(256)
     st = lib().rowsm_describe(rows, cols, in_dtype, out_dtype, variant, buf, len(buf))
     return st, buf.value.decode()
+
+
+def rowsm_describe_op(op, rows, cols, in_dtype, out_dtype, cfg=None):
+    if cfg is not None and not isinstance(cfg, RowsmConfig):
+        cfg = RowsmConfig(**cfg)
+    ref = ctypes.byref(cfg) if cfg is not None else None
+    buf = ctypes.create_string_buffer(256)
+    st = lib().rowsm_describe_op(op, rows, cols, in_dtype, out_dtype, ref, buf, len(buf))
+    return st, buf.value.decode()
+
+
+def rowsm_softmax_backward(y, dy, dx, rows, cols, in_dtype, out_dtype, stream=0,
+                           cfg=None) -> int:
+    if cfg is not None and not isinstance(cfg, RowsmConfig):
+        cfg = RowsmConfig(**cfg)
+    ref = ctypes.byref(cfg) if cfg is not None else None
+    return lib().rowsm_softmax_backward(y, dy, dx, rows, cols, in_dtype, out_dtype, stream, ref)
 
 
 def rowsm_split_wait_failures() -> int:
@@ -175,6 +209,45 @@ def scaled_causal_softmax(x, scale: float, causal_period: int, causal_offset: in
     check(rowsm_forward_scaled_causal(x.data_ptr(), out.data_ptr(), rows, cols,
                                       dtype_code(x.dtype), dtype_code(out.dtype), float(scale),
                                       int(causal_period), int(causal_offset), st, config))
+    return out
+
+
+def log_softmax(x, out_dtype=None, out=None, config=None, stream=None):
+    """log(softmax(x, dim=-1)) of a contiguous fp32/bf16 GPU tensor (see
+    rowsm_log_softmax).  Marshalling only."""
+    import torch
+    if not x.is_cuda or not x.is_contiguous():
+        raise RowsmError("log_softmax needs a contiguous GPU tensor")
+    if out is None:
+        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
+        raise RowsmError("out must be a contiguous tensor of x's shape on x's device")
+    cols = x.shape[-1] if x.dim() else 1
+    rows = x.numel() // cols if cols else 0
+    st = (stream or torch.cuda.current_stream(x.device)).cuda_stream
+    check(rowsm_log_softmax(x.data_ptr(), out.data_ptr(), rows, cols, dtype_code(x.dtype),
+                            dtype_code(out.dtype), st, config))
+    return out
+
+
+def softmax_backward(y, dy, out_dtype=None, out=None, config=None, stream=None):
+    """Gradient of softmax(x, dim=-1) given its output ``y`` and the upstream
+    gradient ``dy`` (contiguous GPU tensors of one shape and dtype), see
+    rowsm_softmax_backward.  Returns ``out`` (dx).  Marshalling only."""
+    import torch
+    if not (y.is_cuda and dy.is_cuda) or not (y.is_contiguous() and dy.is_contiguous()):
+        raise RowsmError("softmax_backward needs contiguous GPU tensors")
+    if dy.shape != y.shape or dy.dtype != y.dtype or dy.device != y.device:
+        raise RowsmError("y and dy must share shape, dtype and device")
+    if out is None:
+        out = torch.empty(y.shape, dtype=out_dtype or y.dtype, device=y.device)
+    elif out.shape != y.shape or not out.is_contiguous() or out.device != y.device:
+        raise RowsmError("out must be a contiguous tensor of y's shape on y's device")
+    cols = y.shape[-1] if y.dim() else 1
+    rows = y.numel() // cols if cols else 0
+    st = (stream or torch.cuda.current_stream(y.device)).cuda_stream
+    check(rowsm_softmax_backward(y.data_ptr(), dy.data_ptr(), out.data_ptr(), rows, cols,
+                                 dtype_code(y.dtype), dtype_code(out.dtype), st, config))
     return out
 
 

@@ -1,0 +1,344 @@
+// Softmax backward kernels: for every row,
+//     dx_j = y_j * (dy_j - d),   d = sum_k y_k * dy_k,
+// the product of the softmax Jacobian diag(y) - y y^T with dy, where y is
+// the forward output and dy the gradient with respect to it.
+//
+// The work is one dot product per row and one elementwise pass: two input
+// streams (y, dy) and one output stream (dx), HBM bound.  The same
+// row-length families as the forward kernels, with the same lane layouts:
+//   small   several rows per wave, a row's vectors on LPR lanes, DPP sums;
+//   medium  one row per group of WPR waves, the row pair held in registers;
+//   split   one row over S co-resident blocks that exchange block partial
+//           sums of d (split_row.hpp's protocol, one word per block);
+//   large   two streaming passes (dot, then dx) for rows longer than that.
+// The register-resident forms keep y and dy in their raw input form (bf16
+// pairs take half the registers) and widen each element where it is used,
+// so one read of each input suffices.  Lanes past the end of a row hold
+// zeros, which add nothing to d.
+//
+// d is accumulated with fma in fp32: a lane's vectors in slot order, then
+// lanes in a fixed DPP tree, waves and blocks in index order, so the result
+// is deterministic.  dx may be y or dy itself (same dtype): every element is
+// read by the lane that writes it, before the write.
+#pragma once
+
+#include "medium_row.hpp"
+#include "rowsm_device.hpp"
+#include "split_row.hpp"
+
+namespace rowsm {
+
+// d += y . dy over one vector pair.
+template <typename In, int VW>
+__device__ __forceinline__ float dot_vec(const InVec<In, VW>& a, const InVec<In, VW>& b,
+                                         float acc) {
+#pragma unroll
+  for (int i = 0; i < VW; ++i) acc = __builtin_fmaf(a.get(i), b.get(i), acc);
+  return acc;
+}
+
+// dx = y * (dy - d) for one vector pair.
+template <typename In, int VW>
+__device__ __forceinline__ void grad_vec(const InVec<In, VW>& a, const InVec<In, VW>& b, float d,
+                                         float (&o)[VW]) {
+#pragma unroll
+  for (int i = 0; i < VW; ++i) o[i] = a.get(i) * (b.get(i) - d);
+}
+
+// ---- small rows ---------------------------------------------------------------
+
+template <typename In, typename Out, int VW, int LPR, int RPL>
+__global__ __launch_bounds__(256) void bwd_small_kernel(
+    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
+    typename Out::storage* __restrict__ dx, int64_t rows, int cols) {
+  constexpr int RPW = kWave / LPR;     // rows per wave per load instruction
+  constexpr int RPT = RPW * RPL;       // rows per wave per task
+  const int lane = threadIdx.x & (kWave - 1);
+  const int sub = lane % LPR;
+  const int grp = lane / LPR;
+  const int nvec = cols / VW;
+  const bool col_ok = sub < nvec;
+  const uint32_t lane_elt = (uint32_t)(grp * cols + sub * VW);
+  const uint32_t vin = lane_elt * In::bytes, vout = lane_elt * Out::bytes;
+  const uint32_t group_elts = (uint32_t)RPW * (uint32_t)cols;
+
+  const int waves_per_block = blockDim.x / kWave;
+  const int64_t wave = (int64_t)blockIdx.x * waves_per_block + wave_id();
+  const int64_t nwaves = (int64_t)gridDim.x * waves_per_block;
+  const int64_t ntasks = (rows + RPT - 1) / RPT;
+
+  for (int64_t task = wave; task < ntasks; task += nwaves) {
+    const int64_t row0 = task * RPT;
+    const int64_t nrows = rows - row0 < RPT ? rows - row0 : RPT;
+    const uint64_t in_bytes = (uint64_t)(nrows * cols) * In::bytes;
+    const rsrc_t ry = make_rsrc(y + row0 * cols, in_bytes);
+    const rsrc_t rdy = make_rsrc(dy + row0 * cols, in_bytes);
+    const rsrc_t rdx = make_rsrc(dx + row0 * cols, (uint64_t)(nrows * cols) * Out::bytes);
+
+    InVec<In, VW> a[RPL], b[RPL];
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+      if (col_ok && k * RPW + grp < nrows) {
+        a[k].load(ry, vin, k * group_elts * In::bytes);
+        b[k].load(rdy, vin, k * group_elts * In::bytes);
+      } else {
+        a[k].set_zero();
+        b[k].set_zero();
+      }
+    }
+    float d[RPL];
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) d[k] = dot_vec(a[k], b[k], 0.0f);
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) d[k] = group_reduce<LPR, SumOp>(d[k]);
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+      float o[VW];
+      grad_vec(a[k], b[k], d[k], o);
+      if (col_ok && k * RPW + grp < nrows)
+        store_out<Out, VW>(rdx, vout + k * group_elts * Out::bytes, o);
+    }
+  }
+}
+
+// ---- medium rows --------------------------------------------------------------
+
+// Thread t of a row group of WPR waves owns vectors t, t + T, ..., t + (NV-1) T
+// (T = 64 WPR; only the last slot can be partial).  One reduction per row:
+// its LDS slots alternate between rows, so a wave that runs ahead to the next
+// row never overwrites a partial sum a slower wave of its group still reads.
+template <typename In, typename Out, int VW, int NV>
+__global__ __launch_bounds__(1024) void bwd_medium_kernel(
+    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
+    typename Out::storage* __restrict__ dx, int64_t rows, int cols, int wpr) {
+  __shared__ float red[2][16];
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int rpb = (blockDim.x / kWave) / wpr;
+  const int g = wave / wpr;
+  const int T = wpr * kWave;
+  const int t = (wave - g * wpr) * kWave + lane;
+  const int nvec = cols / VW;
+  const uint32_t vin = (uint32_t)t * (VW * In::bytes);
+  const uint32_t vout = (uint32_t)t * (VW * Out::bytes);
+  const uint32_t sin = (uint32_t)T * (VW * In::bytes);
+  const uint32_t sout = (uint32_t)T * (VW * Out::bytes);
+  const bool last_ok = (NV - 1) * T + t < nvec;
+
+  int parity = 0;
+  for (int64_t base = (int64_t)blockIdx.x * rpb; base < rows;
+       base += (int64_t)gridDim.x * rpb, parity ^= 1) {
+    const int64_t row = base + g;
+    const bool row_ok = row < rows;
+    const int64_t rr = row_ok ? row : 0;
+    const rsrc_t ry = make_rsrc(y + rr * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t rdy = make_rsrc(dy + rr * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t rdx = make_rsrc(dx + rr * cols, (uint64_t)cols * Out::bytes);
+
+    InVec<In, VW> a[NV], b[NV];
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      if (row_ok && (s < NV - 1 || last_ok)) {
+        a[s].load(ry, vin, s * sin);
+        b[s].load(rdy, vin, s * sin);
+      } else {
+        a[s].set_zero();
+        b[s].set_zero();
+      }
+    }
+    float d = 0.0f;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) d = dot_vec(a[s], b[s], d);
+    d = block_row_reduce<SumOp>(d, wpr, wave, g, lane, red[parity]);
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      float o[VW];
+      grad_vec(a[s], b[s], d, o);
+      if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(rdx, vout + s * sout, o);
+    }
+  }
+}
+
+// ---- long rows: split over co-resident blocks -----------------------------------
+//
+// Layout, grid and co-residency as split_row_kernel.  Each block publishes
+// its partial d_b as the word ws[b][k & 1] = (tag << 32) | bits(d_b) (relaxed
+// agent-scope 64-bit atomic store; tag = tag0 + k unique to the launch and
+// the block's row count k) and the first wave polls the S words of its row
+// group until their tags match, then sums them in block order.  The wm words
+// are not used.  LDS reuse across rows: a wave rewrites red only after this
+// row's second barrier, and bcast (wave 0) only after the next row's first
+// barrier; every wave reads red before the second barrier and bcast before
+// the next row's first, so no value is overwritten before it is read.
+template <typename In, typename Out, int VW, int NV>
+__global__ __launch_bounds__(1024) void bwd_split_kernel(
+    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
+    typename Out::storage* __restrict__ dx, int64_t rows, int cols, int S, SplitWorkspace w,
+    uint32_t tag0) {
+  __shared__ float red[16];
+  __shared__ float bcast;
+
+  const int T = blockDim.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int nwaves = T / kWave;
+  const int c = blockIdx.x % S;
+  const int q = blockIdx.x / S;
+  const int64_t slots = gridDim.x / S;
+  const int RT = S * T;
+  const int gt = c * T + threadIdx.x;
+  const int nvec = cols / VW;
+  const bool last_ok = (NV - 1) * RT + gt < nvec;
+  const uint32_t vin = (uint32_t)gt * (VW * In::bytes);
+  const uint32_t vout = (uint32_t)gt * (VW * Out::bytes);
+  const uint32_t sin = (uint32_t)RT * (VW * In::bytes);
+  const uint32_t sout = (uint32_t)RT * (VW * Out::bytes);
+
+  bool gave_up = false;  // per lane of the first wave
+  uint32_t k = 0;
+  for (int64_t row = q; row < rows; row += slots, ++k) {
+    const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t rdy = make_rsrc(dy + row * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t rdx = make_rsrc(dx + row * cols, (uint64_t)cols * Out::bytes);
+
+    InVec<In, VW> a[NV], b[NV];
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      if (s < NV - 1 || last_ok) {
+        a[s].load(ry, vin, s * sin);
+        b[s].load(rdy, vin, s * sin);
+      } else {
+        a[s].set_zero();
+        b[s].set_zero();
+      }
+    }
+    float d = 0.0f;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) d = dot_vec(a[s], b[s], d);
+    d = group_reduce<kWave, SumOp>(d);
+    if (lane == 0) red[wave] = d;
+    __syncthreads();
+    float db = red[0];
+    for (int i = 1; i < nwaves; ++i) db += red[i];
+
+    if (wave == 0) {
+      const uint32_t b0 = (uint32_t)q * S;
+      const uint64_t tag = (uint64_t)(tag0 + k) << 32;
+      const uint32_t slot = k & 1;
+      if (lane == 0)
+        __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(db),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      float p = 0.0f;
+      if (lane < S) {
+        const uint32_t i = 2 * (b0 + lane) + slot;
+        uint64_t v = 0;
+        uint32_t spins = 0;
+        while (!gave_up) {
+          v = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if ((v & ~0xffffffffull) == tag) break;
+          __builtin_amdgcn_s_sleep(1);
+          if (++spins == kSplitSpinLimit) {
+            __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            gave_up = true;
+          }
+        }
+        p = __uint_as_float((uint32_t)v);
+      }
+      p = group_reduce<kWave, SumOp>(p);  // fixed lane order: deterministic
+      if (lane == 0) bcast = p;
+    }
+    __syncthreads();
+    d = bcast;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      float o[VW];
+      grad_vec(a[s], b[s], d, o);
+      if (s < NV - 1 || last_ok) store_out<Out, VW>(rdx, vout + s * sout, o);
+    }
+  }
+}
+
+// ---- longest rows: two passes ----------------------------------------------------
+//
+// One block per row.  Pass 1 accumulates d over tiles of T * U vector pairs
+// (a tile's partial on its own, then added to the running sum); pass 2
+// reads the row pair again, last tile first, and writes dx.
+template <typename In, typename Out, int VW, int U>
+__global__ __launch_bounds__(1024) void bwd_large_kernel(
+    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
+    typename Out::storage* __restrict__ dx, int64_t rows, int cols) {
+  __shared__ float red[16];
+
+  const int T = blockDim.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int nwaves = T / kWave;
+  const int nvec = cols / VW;
+  const int tile = T * U;
+  const int ntiles = (nvec + tile - 1) / tile;
+  const uint32_t vin = (uint32_t)tid * (VW * In::bytes);
+  const uint32_t vout = (uint32_t)tid * (VW * Out::bytes);
+
+  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+    const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t rdy = make_rsrc(dy + row * cols, (uint64_t)cols * In::bytes);
+    const rsrc_t rdx = make_rsrc(dx + row * cols, (uint64_t)cols * Out::bytes);
+
+    float d = 0.0f;
+    for (int tt = 0; tt < ntiles; ++tt) {
+      InVec<In, VW> a[U], b[U];
+      const bool full = tt < ntiles - 1;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = tt * tile + u * T + tid;
+        const uint32_t so = (uint32_t)(tt * tile + u * T) * (VW * In::bytes);
+        if (full || idx < nvec) {
+          a[u].load(ry, vin, so);
+          b[u].load(rdy, vin, so);
+        } else {
+          a[u].set_zero();
+          b[u].set_zero();
+        }
+      }
+      float ts = 0.0f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) ts = dot_vec(a[u], b[u], ts);
+      d += ts;
+    }
+    d = group_reduce<kWave, SumOp>(d);
+    if (lane == 0) red[wave] = d;
+    __syncthreads();
+    d = red[0];
+    for (int i = 1; i < nwaves; ++i) d += red[i];
+    __syncthreads();  // every wave has read red before the next row
+
+    for (int tt = ntiles - 1; tt >= 0; --tt) {
+      InVec<In, VW> a[U], b[U];
+      const bool full = tt < ntiles - 1;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = tt * tile + u * T + tid;
+        const uint32_t so = (uint32_t)(tt * tile + u * T) * (VW * In::bytes);
+        if (full || idx < nvec) {
+          a[u].load(ry, vin, so);
+          b[u].load(rdy, vin, so);
+        } else {
+          a[u].set_zero();
+          b[u].set_zero();
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = tt * tile + u * T + tid;
+        float o[VW];
+        grad_vec(a[u], b[u], d, o);
+        if (full || idx < nvec)
+          store_out<Out, VW>(rdx, vout + (uint32_t)(tt * tile + u * T) * (VW * Out::bytes), o);
+      }
+    }
+  }
+}
+
+}  // namespace rowsm

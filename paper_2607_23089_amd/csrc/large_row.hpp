@@ -10,8 +10,10 @@
 // first so that the most recently fetched tiles are re-read while they are
 // most likely still cached, and writes exp(x - m) / sum.
 //
-// FUSED computes softmax(scale * x + causal mask) (see Fused): columns past
-// the row's limit are not loaded and come out as exact zeros.
+// MODE selects the output form (see the output forms in rowsm_device.hpp).
+// kFused computes softmax(scale * x + causal mask): columns past the row's
+// limit are not loaded and come out as exact zeros.  kLog writes
+// (x - m) - ln(sum) in pass 2.
 //
 // A thread that has seen only -inf so far uses 0 in place of -m*log2e, so a
 // fully masked tile adds exp(-inf) = 0 instead of exp(-inf + inf) = NaN; a row
@@ -26,10 +28,11 @@
 
 namespace rowsm {
 
-template <typename In, typename Out, int VW, int U, bool FUSED>
+template <typename In, typename Out, int VW, int U, int MODE>
 __global__ __launch_bounds__(1024) void large_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
     int64_t rows, int cols, Fused fz) {
+  constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   __shared__ float red_m[16];
   __shared__ float red_s[16];
 
@@ -78,14 +81,22 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
         for (int i = 0; i < VW; ++i) tm = fmax_nn(tm, f[u][i]);
       const float M = fmax_nn(m, tm);
       const float nml = (M == ninf) ? 0.0f : -M * kLog2e;
-      float acc = rescale(s, m, M);
+      // The tile is summed on its own and then added to the running sum, so
+      // a thread's serial chain of additions is one tile plus one per tile.
+      float ts = 0.0f;
+      if constexpr (LOG) {
+        const float ref = exp_ref(M);
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+        for (int u = 0; u < U; ++u) exp_sum_keep(f[u], ref, &ts);
+      } else {
 #pragma unroll
-        for (int i = 0; i < VW; ++i)
-          acc += exp2_fast(__builtin_fmaf(f[u][i], kLog2e, nml));
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int i = 0; i < VW; ++i)
+            ts += exp2_fast(__builtin_fmaf(f[u][i], kLog2e, nml));
+      }
+      s = rescale(s, m, M) + ts;
       m = M;
-      s = acc;
     }
 
     MaxSum ms = group_merge<kWave>({m, s});
@@ -100,6 +111,7 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
 
     const float nml = -ms.m * kLog2e;
     const float inv = __builtin_amdgcn_rcpf(ms.s);  // v_rcp_f32, 1 ulp
+    const float lns = LOG ? ln_fast(ms.s) : 0.0f;
 
     // Pass 2: normalise, last tile first.
     for (int tt = ntiles - 1; tt >= 0; --tt) {
@@ -121,7 +133,7 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
         if constexpr (FUSED) fused_apply(o, idx * VW, lim, fz.scale);
 #pragma unroll
         for (int i = 0; i < VW; ++i)
-          o[i] = exp2_fast(__builtin_fmaf(o[i], kLog2e, nml)) * inv;
+          o[i] = LOG ? (o[i] - ms.m) - lns : exp2_fast(__builtin_fmaf(o[i], kLog2e, nml)) * inv;
         if (full || idx < nvec)
           store_out<Out, VW>(ry, vout + (uint32_t)(tt * tile + u * T) * (VW * Out::bytes), o);
       }

@@ -1,7 +1,7 @@
 // Launch plans and the per-family launchers.  Each family's kernels are
-// instantiated in translation units of their own (plain and fused apart), so
-// the library builds in parallel; rowsm.hip holds the launcher logic and the
-// C ABI.
+// instantiated in translation units of their own, one per output form
+// (launch_<family>_<form>.hip), so the library builds in parallel; rowsm.hip
+// holds the launcher logic and the C ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -32,8 +32,9 @@ struct Plan {
   int64_t grid = 1;  // split form: 0 = occupancy, < 0 = minus the blocks-per-CU cap
 };
 
-// One launch request: the plan plus its operands.  fz == nullptr selects the
-// plain kernels, otherwise the FUSED instantiations with *fz.
+// One launch request: the plan plus its operands.  mode is the output form
+// (kPlain, kFused or kLog); fz holds the scale and mask of kFused and is the
+// identity (scale 1, no mask) otherwise.
 struct Call {
   Plan p;
   const void* x;
@@ -42,23 +43,23 @@ struct Call {
   int cols;
   hipStream_t st;
   int cus;
-  const Fused* fz;
+  int mode = kPlain;
+  Fused fz{1.0f, 0, 0};
+  const void* dy = nullptr;  // softmax backward: x holds y, dy the gradient, y receives dx
 };
 
-inline Fused fused_or_identity(const Call& c) { return c.fz ? *c.fz : Fused{1.0f, 0, 0}; }
-
-// Calls L<In, Out, VW, FUSED>::run(c) for the call's dtype pair and vector
+// Calls L<In, Out, VW, MODE>::run(c) for the call's dtype pair and vector
 // width (16-byte, 8-byte or single-element vectors).  Returns a rowsm_status:
 // ROWSM_EINVAL when nothing matches (nothing enqueued).
-template <template <typename, typename, int, bool> class L, bool FUSED>
+template <template <typename, typename, int, int> class L, int MODE>
 int dispatch(const Call& c, int in_dt, int out_dt) {
   auto io = [&](auto in_tag, auto out_tag) -> int {
     using In = decltype(in_tag);
     using Out = decltype(out_tag);
     constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
-    if (c.p.vw == 1) return L<In, Out, 1, FUSED>::run(c);
-    if (c.p.vw == V8) return L<In, Out, V8, FUSED>::run(c);
-    if (c.p.vw == V16) return L<In, Out, V16, FUSED>::run(c);
+    if (c.p.vw == 1) return L<In, Out, 1, MODE>::run(c);
+    if (c.p.vw == V8) return L<In, Out, V8, MODE>::run(c);
+    if (c.p.vw == V16) return L<In, Out, V16, MODE>::run(c);
     return ROWSM_EINVAL;
   };
   if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32) return io(F32{}, F32{});
@@ -67,15 +68,18 @@ int dispatch(const Call& c, int in_dt, int out_dt) {
   return io(BF16{}, BF16{});
 }
 
-// Per-family launchers (launch_<family>_<plain|fused>.hip).
-int launch_small_plain(const Call& c, int in_dt, int out_dt);
-int launch_small_fused(const Call& c, int in_dt, int out_dt);
-int launch_medium_plain(const Call& c, int in_dt, int out_dt);
-int launch_medium_fused(const Call& c, int in_dt, int out_dt);
-int launch_large_plain(const Call& c, int in_dt, int out_dt);
-int launch_large_fused(const Call& c, int in_dt, int out_dt);
-int launch_split_plain(const Call& c, int in_dt, int out_dt);
-int launch_split_fused(const Call& c, int in_dt, int out_dt);
+// Per-family launchers, defined in launch_<family>.hpp and instantiated for
+// each output form in launch_<family>_<form>.hip.
+template <int MODE> int launch_small(const Call& c, int in_dt, int out_dt);
+template <int MODE> int launch_medium(const Call& c, int in_dt, int out_dt);
+template <int MODE> int launch_large(const Call& c, int in_dt, int out_dt);
+template <int MODE> int launch_split(const Call& c, int in_dt, int out_dt);
+
+// Softmax-backward launchers (launch_bwd_<family>.hip).
+int launch_bwd_small(const Call& c, int in_dt, int out_dt);
+int launch_bwd_medium(const Call& c, int in_dt, int out_dt);
+int launch_bwd_split(const Call& c, int in_dt, int out_dt);
+int launch_bwd_large(const Call& c, int in_dt, int out_dt);
 
 // Split-form diagnostics (launch_split_common.hip).
 int64_t split_wait_failures_current_device();

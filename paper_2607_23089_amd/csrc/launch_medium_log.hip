@@ -1,0 +1,6 @@
+// Medium-row family, log-softmax instantiations.
+#include "launch_medium.hpp"
+
+namespace rowsm {
+template int launch_medium<kLog>(const Call& c, int in_dt, int out_dt);
+}  // namespace rowsm

@@ -10,8 +10,10 @@
 // permlane swaps, then across the WPR waves through LDS (one barrier each;
 // WPR == 1 needs neither LDS nor barriers).
 //
-// FUSED computes softmax(scale * x + causal mask) (see Fused): columns past
-// the row's limit are not loaded and come out as exact zeros.
+// MODE selects the output form (see the output forms in rowsm_device.hpp).
+// kFused computes softmax(scale * x + causal mask): columns past the row's
+// limit are not loaded and come out as exact zeros.  kLog writes
+// (x - m) - ln(sum), which needs x itself and not exp(x - m) at the end.
 //
 // PACKED == false widens the row to fp32 once and keeps exp(x - m) in
 // registers for the normalise step.  PACKED == true keeps the row in its raw
@@ -48,10 +50,11 @@ __device__ __forceinline__ float block_row_reduce(float v, int wpr, int wave, in
   return v;
 }
 
-template <typename In, typename Out, int VW, int NV, bool PACKED, bool FUSED>
+template <typename In, typename Out, int VW, int NV, bool PACKED, int MODE>
 __global__ __launch_bounds__(1024) void medium_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
     int64_t rows, int cols, int wpr, Fused fz) {
+  constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   static_assert(!(PACKED && FUSED), "the fused variants keep the row in fp32");
   __shared__ float red_m[16];
   __shared__ float red_s[16];
@@ -101,17 +104,20 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
       for (int s = 0; s < NV; ++s)
 #pragma unroll
         for (int i = 0; i < VW; ++i)
-          sum += exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml));
+          sum += LOG ? exp2_fast((v[s].get(i) - mx) * kLog2e)
+                     : exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml));
       sum = block_row_reduce<SumOp>(sum, wpr, wave, g, lane, red_s);
 #pragma unroll
       for (int s = 0; s < NV; ++s) v[s].opaque();
       const float inv = __builtin_amdgcn_rcpf(sum);  // v_rcp_f32, 1 ulp
+      const float lns = LOG ? ln_fast(sum) : 0.0f;
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
         float o[VW];
 #pragma unroll
         for (int i = 0; i < VW; ++i)
-          o[i] = exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml)) * inv;
+          o[i] = LOG ? (v[s].get(i) - mx) - lns
+                     : exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml)) * inv;
         if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(ry, vout + s * sout, o);
       }
     } else {
@@ -151,17 +157,20 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
       const float nml = -mx * kLog2e;
       float sum = 0.0f;
 #pragma unroll
-      for (int s = 0; s < NV; ++s)
-        exp_accumulate<FUSED>(f[s], nml, (s * T + t) * VW <= lim, &sum);
+      for (int s = 0; s < NV; ++s) {
+        if constexpr (LOG) exp_sum_keep(f[s], mx, &sum);
+        else exp_accumulate<FUSED>(f[s], nml, (s * T + t) * VW <= lim, &sum);
+      }
       sum = block_row_reduce<SumOp>(sum, wpr, wave, g, lane, red_s);
       const float inv = __builtin_amdgcn_rcpf(sum);  // v_rcp_f32, 1 ulp
+      const float lns = LOG ? ln_fast(sum) : 0.0f;
       // A row whose sum is not >= 1 (nothing kept, or a NaN/+inf among the
       // kept values) is all NaN, masked columns included: rewrite those too.
       const bool redo_masked = FUSED && !(sum > 0.5f);
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
 #pragma unroll
-        for (int i = 0; i < VW; ++i) f[s][i] *= inv;
+        for (int i = 0; i < VW; ++i) f[s][i] = LOG ? (f[s][i] - mx) - lns : f[s][i] * inv;
         if (row_ok && (s < NV - 1 || last_ok) &&
             (!FUSED || (s * T + t) * VW <= lim || redo_masked))
           store_out<Out, VW>(ry, vout + s * sout, f[s]);

@@ -25,6 +25,10 @@
 namespace rowsm {
 namespace {
 
+static_assert(ROWSM_OP_SOFTMAX == kPlain && ROWSM_OP_SCALED_CAUSAL == kFused &&
+                  ROWSM_OP_LOG_SOFTMAX == kLog && ROWSM_OP_SOFTMAX_BACKWARD == kBackward,
+              "rowsm_op values are the launch modes");
+
 std::atomic<int> g_cu_count[kMaxDevices];
 
 // Compute-unit count of the current device (cached per device).  Falls back
@@ -92,9 +96,12 @@ bool config_in_domain(const rowsm_config* c) {
          c->blocks_per_cu >= 0 && c->split_blocks >= -1 && c->split_blocks <= 64;
 }
 
+// mode is the output form (kPlain, kFused or kLog).  The log form holds x
+// where softmax holds exp(x - m), so it takes the plain form's plans.
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
-             const rowsm_config* cfg, int cus, bool fused, Plan* p) {
+             const rowsm_config* cfg, int cus, int mode, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  const bool fused = mode == kFused;
   const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
   int vw = choose_vw(cols, ib, ob, xa, ya);
   if (cfg && cfg->vw > 0) {
@@ -257,21 +264,144 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   return ROWSM_EINVAL;
 }
 
+// Plan of the softmax backward: y and dy of in_dt (both aligned as ia), dx
+// of out_dt at dxa.  The register-resident forms hold y and dy raw; a lane's
+// share of each input is at most 128 bytes (and 16 slots).
+//   SMALL   a row is at most 32 vectors;
+//   MEDIUM  the smallest row group of <= 16 waves whose lanes hold at most 32
+//           bytes of each input (then 64, then 128);
+//   LARGE   the row split over S <= 64 co-resident 256-thread blocks, or two
+//           streaming passes for rows longer than that.
+int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t ia,
+                  uintptr_t dxa, const rowsm_config* cfg, int cus, Plan* p) {
+  if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  if (cfg && cfg->packed == 1) return ROWSM_EINVAL;  // no packed form: always raw
+  const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
+  int vw = choose_vw(cols, ib, ob, ia, dxa);
+  if (cfg && cfg->vw > 0) {
+    const int want = cfg->vw;
+    if (want > 16 / (ib > ob ? ib : ob) || (want & (want - 1)) || !vw_supported(want, ib) ||
+        cols % want || ia % (want * ib) || dxa % (want * ob < 16 ? want * ob : 16))
+      return ROWSM_EINVAL;
+    vw = want;
+  }
+  const int nvec = (int)(cols / vw);
+  const int vbytes = vw * ib;  // bytes of one input vector
+  int nv_cap = 128 / vbytes < 16 ? 128 / vbytes : 16;
+  p->vw = vw;
+  p->nvec = nvec;
+
+  int variant = cfg ? cfg->variant : ROWSM_AUTO;
+  if (variant == ROWSM_AUTO)
+    variant = nvec <= 32 ? ROWSM_SMALL
+                         : (nvec <= 16 * kWave * nv_cap ? ROWSM_MEDIUM : ROWSM_LARGE);
+  p->variant = variant;
+  const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
+
+  if (variant == ROWSM_SMALL) {
+    if (nvec > 32) return ROWSM_EINVAL;
+    p->lpr = next_pow2(nvec);
+    if (cfg && cfg->lanes_per_row > 0) {
+      if (cfg->lanes_per_row < p->lpr) return ROWSM_EINVAL;
+      p->lpr = cfg->lanes_per_row;
+    }
+    p->rpl = (cfg && cfg->rows_per_lane > 0) ? cfg->rows_per_lane : 4;
+    p->block = 256;
+    const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 8);
+    p->grid = cdiv(rows, rows_per_block);
+    if (p->grid > cap) p->grid = cap;
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_MEDIUM) {
+    const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
+    int wpr = 0, nv = 0;
+    for (int cap_bytes : {32, 64, 128}) {
+      for (int w = 1; w <= 16; w <<= 1) {
+        if (want_wpr && w != want_wpr) continue;
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v * vbytes <= cap_bytes && v <= nv_cap) {
+          wpr = w;
+          nv = v;
+          break;
+        }
+      }
+      if (wpr) break;
+    }
+    if (!wpr) return ROWSM_EINVAL;
+    p->wpr = wpr;
+    p->vpl = nv;
+    p->nv = nv;
+    int rpb = wpr >= 8 ? 1 : 8 / wpr;  // 512-thread blocks
+    if (cfg && cfg->rows_per_block > 0) {
+      rpb = cfg->rows_per_block;
+      if (rpb * wpr > 16) return ROWSM_EINVAL;
+    }
+    p->block = rpb * wpr * kWave;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 64);
+    p->grid = cdiv(rows, rpb);
+    if (p->grid > cap) p->grid = cap;
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_LARGE) {
+    const int want_split = cfg ? cfg->split_blocks : 0;
+    if (want_split >= 0) {
+      const int T = (cfg && cfg->block > 0) ? cfg->block : 256;
+      int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
+      if (S < 1) S = 1;
+      const int nv = (int)cdiv(nvec, (int64_t)S * T);
+      if (S <= 64 && nv <= nv_cap) {
+        p->split = S;
+        p->nv = nv;
+        p->vpl = nv;
+        p->block = T;
+        p->grid = bpc ? -(int64_t)bpc : 0;  // sized from occupancy at launch
+        return ROWSM_OK;
+      }
+      if (want_split > 0) return ROWSM_EINVAL;
+    }
+    p->split = 0;
+    p->u = (cfg && cfg->tile_vectors > 0) ? cfg->tile_vectors : 4;
+    p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
+    p->grid = rows < cap ? rows : cap;
+    return ROWSM_OK;
+  }
+  return ROWSM_EINVAL;
+}
+
 // ---- family dispatch ------------------------------------------------------------
 
-int launch(const Call& c, int in_dt, int out_dt) {
-  const bool f = c.fz != nullptr;
+template <int MODE>
+int launch_mode(const Call& c, int in_dt, int out_dt) {
   switch (c.p.variant) {
-    case ROWSM_SMALL:
-      return f ? launch_small_fused(c, in_dt, out_dt) : launch_small_plain(c, in_dt, out_dt);
-    case ROWSM_MEDIUM:
-      return f ? launch_medium_fused(c, in_dt, out_dt) : launch_medium_plain(c, in_dt, out_dt);
+    case ROWSM_SMALL: return launch_small<MODE>(c, in_dt, out_dt);
+    case ROWSM_MEDIUM: return launch_medium<MODE>(c, in_dt, out_dt);
     case ROWSM_LARGE:
-      if (c.p.split > 0)
-        return f ? launch_split_fused(c, in_dt, out_dt) : launch_split_plain(c, in_dt, out_dt);
-      return f ? launch_large_fused(c, in_dt, out_dt) : launch_large_plain(c, in_dt, out_dt);
-    default:
-      return ROWSM_EINVAL;
+      return c.p.split > 0 ? launch_split<MODE>(c, in_dt, out_dt)
+                           : launch_large<MODE>(c, in_dt, out_dt);
+    default: return ROWSM_EINVAL;
+  }
+}
+
+int launch_backward(const Call& c, int in_dt, int out_dt) {
+  switch (c.p.variant) {
+    case ROWSM_SMALL: return launch_bwd_small(c, in_dt, out_dt);
+    case ROWSM_MEDIUM: return launch_bwd_medium(c, in_dt, out_dt);
+    case ROWSM_LARGE:
+      return c.p.split > 0 ? launch_bwd_split(c, in_dt, out_dt)
+                           : launch_bwd_large(c, in_dt, out_dt);
+    default: return ROWSM_EINVAL;
+  }
+}
+
+int launch(const Call& c, int in_dt, int out_dt) {
+  switch (c.mode) {
+    case kPlain: return launch_mode<kPlain>(c, in_dt, out_dt);
+    case kFused: return launch_mode<kFused>(c, in_dt, out_dt);
+    case kLog: return launch_mode<kLog>(c, in_dt, out_dt);
+    case kBackward: return launch_backward(c, in_dt, out_dt);
+    default: return ROWSM_EINVAL;
   }
 }
 
@@ -300,21 +430,52 @@ int validate(const void* x, const void* y, int64_t rows, int64_t cols, int in_dt
   return ROWSM_OK;
 }
 
+// Backward operands: y and dy (in_dt, read only, may overlap each other) and
+// dx (out_dt), which may be y or dy itself when the dtypes match but must not
+// overlap either in any other way.
+int validate_backward(const void* yp, const void* dyp, const void* dxp, int64_t rows,
+                      int64_t cols, int in_dt, int out_dt, bool* noop) {
+  int st = validate(yp, dxp, rows, cols, in_dt, out_dt, true, noop);
+  if (st != ROWSM_OK || *noop) return st;
+  return validate(dyp, dxp, rows, cols, in_dt, out_dt, true, noop);
+}
+
+int backward_impl(const void* yp, const void* dyp, void* dxp, int64_t rows, int64_t cols,
+                  int in_dt, int out_dt, void* stream, const rowsm_config* cfg) {
+  bool noop = false;
+  int st = validate_backward(yp, dyp, dxp, rows, cols, in_dt, out_dt, &noop);
+  if (st != ROWSM_OK || noop) return st;
+  Call c;
+  c.cus = cu_count();
+  st = plan_backward(rows, cols, in_dt, out_dt, (uintptr_t)yp | (uintptr_t)dyp, (uintptr_t)dxp,
+                     cfg, c.cus, &c.p);
+  if (st != ROWSM_OK) return st;
+  c.x = yp;
+  c.dy = dyp;
+  c.y = dxp;
+  c.rows = rows;
+  c.cols = (int)cols;
+  c.st = static_cast<hipStream_t>(stream);
+  c.mode = kBackward;
+  (void)hipGetLastError();  // do not report an earlier, unrelated error
+  return launch(c, in_dt, out_dt);
+}
+
 int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, int out_dt,
-                 void* stream, const rowsm_config* cfg, const Fused* fz) {
+                 void* stream, const rowsm_config* cfg, int mode, Fused fz = {1.0f, 0, 0}) {
   bool noop = false;
   int st = validate(x, y, rows, cols, in_dt, out_dt, true, &noop);
   if (st != ROWSM_OK || noop) return st;
   Call c;
   c.cus = cu_count();
-  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus,
-                fz != nullptr, &c.p);
+  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus, mode, &c.p);
   if (st != ROWSM_OK) return st;
   c.x = x;
   c.y = y;
   c.rows = rows;
   c.cols = (int)cols;
   c.st = static_cast<hipStream_t>(stream);
+  c.mode = mode;
   c.fz = fz;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   return launch(c, in_dt, out_dt);
@@ -336,7 +497,7 @@ using namespace rowsm;
 
 extern "C" int rowsm_forward(const void* x, void* y, int64_t rows, int64_t cols, int in_dtype,
                              int out_dtype, void* stream) {
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr, nullptr);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr, kPlain);
 }
 
 extern "C" int rowsm_forward_variant(const void* x, void* y, int64_t rows, int64_t cols,
@@ -350,13 +511,13 @@ extern "C" int rowsm_forward_variant(const void* x, void* y, int64_t rows, int64
   std::memset(&cfg, 0, sizeof(cfg));
   cfg.variant = variant;
   cfg.packed = -1;
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, &cfg, nullptr);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, &cfg, kPlain);
 }
 
 extern "C" int rowsm_forward_config(const void* x, void* y, int64_t rows, int64_t cols,
                                     int in_dtype, int out_dtype, void* stream,
                                     const rowsm_config* cfg) {
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, nullptr);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, kPlain);
 }
 
 extern "C" int rowsm_forward_scaled_causal(const void* x, void* y, int64_t rows, int64_t cols,
@@ -369,7 +530,19 @@ extern "C" int rowsm_forward_scaled_causal(const void* x, void* y, int64_t rows,
     return st != ROWSM_OK ? st : ROWSM_EINVAL;
   }
   const Fused fz{scale, causal_period, causal_offset};
-  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, &fz);
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, kFused, fz);
+}
+
+extern "C" int rowsm_log_softmax(const void* x, void* y, int64_t rows, int64_t cols,
+                                 int in_dtype, int out_dtype, void* stream,
+                                 const rowsm_config* cfg) {
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, cfg, kLog);
+}
+
+extern "C" int rowsm_softmax_backward(const void* y, const void* dy, void* dx, int64_t rows,
+                                      int64_t cols, int in_dtype, int out_dtype, void* stream,
+                                      const rowsm_config* cfg) {
+  return backward_impl(y, dy, dx, rows, cols, in_dtype, out_dtype, stream, cfg);
 }
 
 extern "C" int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dtype) {
@@ -378,22 +551,25 @@ extern "C" int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dt
   if (st != ROWSM_OK) return st;
   if (noop) return ROWSM_SMALL;  // nothing is launched; report the smallest family
   Plan p;
-  const int r = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, false, &p);
+  const int r = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, kPlain, &p);
   return r == ROWSM_OK ? p.variant : r;
 }
 
-extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
-                              int variant, char* buf, int64_t len) {
+namespace rowsm {
+namespace {
+
+// Description of the launch an operation would make (mode: the rowsm_op
+// value, which equals the output form and kBackward).
+int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
+                  const rowsm_config* cfg, char* buf, int64_t len) {
   bool noop = false;
-  int st = validate(nullptr, nullptr, rows, cols, in_dtype, out_dtype, false, &noop);
-  if (st == ROWSM_OK && (variant < ROWSM_AUTO || variant > ROWSM_LARGE)) st = ROWSM_EINVAL;
+  int st = validate(nullptr, nullptr, rows, cols, in_dt, out_dt, false, &noop);
+  if (st == ROWSM_OK && (mode < kPlain || mode > kBackward)) st = ROWSM_EINVAL;
   Plan p;
   if (st == ROWSM_OK && !noop) {
-    rowsm_config cfg;
-    std::memset(&cfg, 0, sizeof(cfg));
-    cfg.variant = variant;
-    cfg.packed = -1;
-    st = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, &cfg, 256, false, &p);
+    st = mode == kBackward
+             ? plan_backward(rows, cols, in_dt, out_dt, 256, 256, cfg, 256, &p)
+             : plan_for(rows, cols, in_dt, out_dt, 256, 256, cfg, 256, mode, &p);
   }
   if (buf && len > 0) {
     if (st != ROWSM_OK) {
@@ -411,6 +587,30 @@ extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_
     }
   }
   return st;
+}
+
+}  // namespace
+}  // namespace rowsm
+
+extern "C" int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
+                              int variant, char* buf, int64_t len) {
+  if (variant < ROWSM_AUTO || variant > ROWSM_LARGE) {
+    if (buf && len > 0) std::snprintf(buf, (size_t)len, "error %d", ROWSM_EINVAL);
+    bool noop = false;
+    const int st = validate(nullptr, nullptr, rows, cols, in_dtype, out_dtype, false, &noop);
+    return st != ROWSM_OK ? st : ROWSM_EINVAL;
+  }
+  rowsm_config cfg;
+  std::memset(&cfg, 0, sizeof(cfg));
+  cfg.variant = variant;
+  cfg.packed = -1;
+  return describe_impl(kPlain, rows, cols, in_dtype, out_dtype, &cfg, buf, len);
+}
+
+extern "C" int rowsm_describe_op(int op, int64_t rows, int64_t cols, int in_dtype,
+                                 int out_dtype, const rowsm_config* cfg, char* buf,
+                                 int64_t len) {
+  return describe_impl(op, rows, cols, in_dtype, out_dtype, cfg, buf, len);
 }
 
 extern "C" int64_t rowsm_split_wait_failures(void) {

@@ -124,6 +124,13 @@ struct InVec {
       r = In::neg_inf_word;  // splat to every word
     }
   }
+  __device__ __forceinline__ void set_zero() {
+    if constexpr (BYTES == 2) {
+      r = (uint16_t)0;
+    } else {
+      r = 0u;  // splat to every word
+    }
+  }
   __device__ __forceinline__ uint32_t word(int w) const {
     if constexpr (BYTES <= 4) {
       return (uint32_t)r;
@@ -246,6 +253,42 @@ __device__ __forceinline__ float group_reduce(float v) {
     v = Op::apply(__uint_as_float(p[0]), __uint_as_float(p[1]));
   }
   return v;
+}
+
+// ---- output forms of the forward kernels --------------------------------------
+//
+//   kPlain  y = softmax(x)
+//   kFused  y = softmax(scale * x + causal mask)               (see Fused)
+//   kLog    y = log softmax(x) = (x - m) - ln(sum_j exp(x_j - m))
+//
+// In the log form the exponent is taken as (x - m) * log2e, the difference
+// first: softmax may round m * log2e once per row because that factor cancels
+// in e / sum(e), but in the log form it would not cancel and would add an
+// error proportional to |m|.  The logarithm is v_log_f32 (log2) times ln 2.
+enum : int { kPlain = 0, kFused = 1, kLog = 2 };
+
+// Tag of the softmax-backward launches in the launcher tables (the backward
+// kernels have no output form of their own).
+constexpr int kBackward = 3;
+
+constexpr float kLn2 = 0.69314718055994530942f;
+
+__device__ __forceinline__ float ln_fast(float s) {
+  return __builtin_amdgcn_logf(s) * kLn2;  // v_log_f32
+}
+
+// Reference point for exponents taken relative to a running maximum m: a
+// maximum of -inf (only -inf seen) uses 0, so that exp(-inf - 0) = 0 instead
+// of exp(-inf + inf) = NaN.
+__device__ __forceinline__ float exp_ref(float m) {
+  return m == -__builtin_inff() ? 0.0f : m;
+}
+
+// Log form: sum of exp(v - m) over one vector, v left unchanged.
+template <int VW>
+__device__ __forceinline__ void exp_sum_keep(const float (&v)[VW], float m, float* sum) {
+#pragma unroll
+  for (int i = 0; i < VW; ++i) *sum += exp2_fast((v[i] - m) * kLog2e);
 }
 
 // ---- fused scale and causal mask ---------------------------------------------

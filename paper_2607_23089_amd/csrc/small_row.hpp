@@ -10,6 +10,9 @@
 // or past the last row load nothing and hold -inf, which leaves the max
 // unchanged and contributes exp(-inf) = 0 to the sum.
 //
+// MODE selects the output form (kPlain, kFused or kLog; see the output forms
+// in rowsm_device.hpp).
+//
 // This is the small-row member of the row-length-specialised family the paper
 // names for its running example (small/medium/large row kernels plus a row
 // launcher, preamble listing style); the packing, the lane layout and the DPP
@@ -20,10 +23,11 @@
 
 namespace rowsm {
 
-template <typename In, typename Out, int VW, int LPR, int RPL, bool FUSED>
+template <typename In, typename Out, int VW, int LPR, int RPL, int MODE>
 __global__ __launch_bounds__(256) void small_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
     int64_t rows, int cols, Fused fz) {
+  constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   constexpr int RPW = kWave / LPR;     // rows per wave per load instruction
   constexpr int RPT = RPW * RPL;       // rows per wave per task
   const int lane = threadIdx.x & (kWave - 1);
@@ -76,12 +80,16 @@ __global__ __launch_bounds__(256) void small_row_kernel(
     float s[RPL];
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
-      const float nml = -m[k] * kLog2e;
       float t = 0.0f;
+      if constexpr (LOG) {
+        exp_sum_keep(f[k], m[k], &t);
+      } else {
+        const float nml = -m[k] * kLog2e;
 #pragma unroll
-      for (int i = 0; i < VW; ++i) {
-        f[k][i] = exp2_fast(__builtin_fmaf(f[k][i], kLog2e, nml));
-        t += f[k][i];
+        for (int i = 0; i < VW; ++i) {
+          f[k][i] = exp2_fast(__builtin_fmaf(f[k][i], kLog2e, nml));
+          t += f[k][i];
+        }
       }
       s[k] = t;
     }
@@ -90,9 +98,15 @@ __global__ __launch_bounds__(256) void small_row_kernel(
 
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
-      const float inv = __builtin_amdgcn_rcpf(s[k]);  // v_rcp_f32, 1 ulp
+      if constexpr (LOG) {
+        const float lns = ln_fast(s[k]);
 #pragma unroll
-      for (int i = 0; i < VW; ++i) f[k][i] *= inv;
+        for (int i = 0; i < VW; ++i) f[k][i] = (f[k][i] - m[k]) - lns;
+      } else {
+        const float inv = __builtin_amdgcn_rcpf(s[k]);  // v_rcp_f32, 1 ulp
+#pragma unroll
+        for (int i = 0; i < VW; ++i) f[k][i] *= inv;
+      }
       const bool ok = col_ok && (k * RPW + grp < nrows);
       if (ok) store_out<Out, VW>(ry, vout + k * group_elts * Out::bytes, f[k]);
     }

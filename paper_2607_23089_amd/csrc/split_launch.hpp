@@ -1,6 +1,10 @@
 // Launch of the single-read split-row kernels: grid sizing from occupancy,
-// and the per-device exchange workspace (launch_split_common.hip).
+// the per-device exchange workspace (launch_split_common.hip), and the
+// dispatch on the compile-time slot count, instantiated once per output form
+// (launch_split_<form>.hip).
 #pragma once
+
+#include <utility>
 
 #include "launch.hpp"
 #include "split_row.hpp"
@@ -21,10 +25,10 @@ struct SplitTicket {
 int split_begin(hipStream_t st, uint64_t ntags, SplitTicket* t);
 int split_end(SplitTicket* t, hipStream_t st, bool launched);
 
-template <typename In, typename Out, int VW, int NV, bool FUSED>
+template <typename In, typename Out, int VW, int NV, int MODE>
 int launch_split_nv(const Call& c) {
   const Plan& p = c.p;
-  auto kern = split_row_kernel<In, Out, VW, NV, FUSED>;
+  auto kern = split_row_kernel<In, Out, VW, NV, MODE>;
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
                                                    p.block, 0) != hipSuccess)
@@ -45,10 +49,33 @@ int launch_split_nv(const Call& c) {
   (void)hipGetLastError();
   kern<<<dim3(grid), dim3(p.block), 0, c.st>>>(
       static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
-      c.rows, c.cols, p.split, t.ws, t.tag0, fused_or_identity(c));
+      c.rows, c.cols, p.split, t.ws, t.tag0, c.fz);
   const bool launched = hipGetLastError() == hipSuccess;
   r = split_end(&t, c.st, launched);
   return launched ? r : ROWSM_EHIP;
+}
+
+template <typename In, typename Out, int VW, int MODE, int... NVs>
+int split_nv(const Call& c, std::integer_sequence<int, NVs...>) {
+  int r = ROWSM_EINVAL;
+  (void)((c.p.nv == NVs + 1 && (NVs + 1) * VW <= 64
+              ? (r = launch_split_nv<In, Out, VW, ((NVs + 1) * VW <= 64 ? NVs + 1 : 1), MODE>(c),
+                 true)
+              : false) ||
+         ...);
+  return r;
+}
+
+template <typename In, typename Out, int VW, int MODE>
+struct SplitLaunch {
+  static int run(const Call& c) {
+    return split_nv<In, Out, VW, MODE>(c, std::make_integer_sequence<int, 16>{});
+  }
+};
+
+template <int MODE>
+int launch_split(const Call& c, int in_dt, int out_dt) {
+  return dispatch<SplitLaunch, MODE>(c, in_dt, out_dt);
 }
 
 }  // namespace rowsm

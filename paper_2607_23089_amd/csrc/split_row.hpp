@@ -8,8 +8,10 @@
 // compile time, so only the last slot can be partial and every load
 // instruction of a wave reads 64 consecutive vectors.
 //
-// FUSED computes softmax(scale * x + causal mask) (see Fused): columns past
-// the row's limit are not loaded and come out as exact zeros.
+// MODE selects the output form (see the output forms in rowsm_device.hpp).
+// kFused computes softmax(scale * x + causal mask): columns past the row's
+// limit are not loaded and come out as exact zeros.  kLog keeps x in
+// registers and writes (x - M) - ln(S).
 //
 // Statistics.  Each block reduces its share to a pair (m_b, s_b): m_b the
 // block's maximum and s_b = sum exp(x - m_b) over its entries (a block that
@@ -62,13 +64,14 @@ struct SplitWorkspace {
 // launch, so even a broken exchange lets the whole grid drain quickly.
 constexpr uint32_t kSplitSpinLimit = 1u << 20;
 
-template <typename In, typename Out, int VW, int NV, bool FUSED>
+template <typename In, typename Out, int VW, int NV, int MODE>
 __global__ __launch_bounds__(1024) void split_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
     int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0, Fused fz) {
+  constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   __shared__ float red_m[16];
   __shared__ float red_s[16];
-  __shared__ float bcast[2];
+  __shared__ float bcast[3];
 
   const int T = blockDim.x;
   const int lane = threadIdx.x & (kWave - 1);
@@ -138,8 +141,10 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
     const float nml = (mb == ninf) ? 0.0f : -mb * kLog2e;
     float sb = 0.0f;
 #pragma unroll
-    for (int s = 0; s < NV; ++s)
-      exp_accumulate<FUSED>(f[s], nml, (s * RT + g) * VW <= lim, &sb);
+    for (int s = 0; s < NV; ++s) {
+      if constexpr (LOG) exp_sum_keep(f[s], exp_ref(mb), &sb);
+      else exp_accumulate<FUSED>(f[s], nml, (s * RT + g) * VW <= lim, &sb);
+    }
     sb = group_reduce<kWave, SumOp>(sb);
     if (lane == 0) red_s[wave] = sb;
     __syncthreads();
@@ -179,16 +184,19 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
         // y = exp(x - m_b) * exp(m_b - M) / S
         bcast[0] = exp2_fast((mb - p.m) * kLog2e) * __builtin_amdgcn_rcpf(p.s);
         bcast[1] = (p.s > 0.5f) ? 0.0f : 1.0f;  // row without a normal sum: all NaN
+        bcast[2] = p.m;                          // log form: (x - M) - ln(S)
+        if (LOG) bcast[0] = ln_fast(p.s);
       }
     }
     __syncthreads();
     const float scale = bcast[0];
     const bool redo_masked = FUSED && bcast[1] != 0.0f;
+    const float M = bcast[2];
 
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
 #pragma unroll
-      for (int i = 0; i < VW; ++i) f[s][i] *= scale;
+      for (int i = 0; i < VW; ++i) f[s][i] = LOG ? (f[s][i] - M) - scale : f[s][i] * scale;
       if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim || redo_masked))
         store_out<Out, VW>(ry, vout + s * sout, f[s]);
     }

@@ -19,6 +19,21 @@ Named workloads (rows x cols, dtypes in -> out, value recipe):
                      randint (generator seeded 1), de-duplicated, each set to
                      +-1e4 (sign from the same generator); 1e4 is 9984 in bf16
 
+Softmax-backward workloads (y and dy of in dtype, dx of out dtype):
+
+  bwd_small_262144x64    262144 x 64,   bf16 -> bf16, alpha 0.5
+  bwd_causal_32768x4096  32768 x 4096,  bf16 -> bf16, alpha 0.1, causal
+                         (y[r, c] = 0 for c > r mod 4096)
+  bwd_large_1024x262144  1024 x 262144, f32 -> f32,  alpha 0.05
+
+  y: each row an independent Dirichlet(alpha) sample over its kept columns
+  (gamma(alpha, 1) draws from torch._standard_gamma with a generator seeded
+  2, divided by their row total in fp32; small alpha gives the peaked rows
+  of trained attention and output layers), 0 in masked columns; dy: N(0, 1)
+  with a generator seeded 3.  Both drawn in fp32 on the chosen device, then
+  cast to the input dtype.  This is a probability-vector sampler, not the
+  softmax: no exponential and no maximum is involved.
+
 Recipe: draw fp32 N(0, 1) with torch.randn from a torch.Generator seeded as
 stated on the chosen device, scale by sigma, apply the structure, then cast
 to the input dtype (round to nearest even for bf16).  The GPU and the oracle
@@ -79,6 +94,37 @@ REGIMES = ("small_262144x64", "causal_32768x4096", "large_1024x262144",
            "vocab_4096x151936")
 
 
+@dataclass(frozen=True)
+class BackwardWorkload:
+    name: str
+    rows: int
+    cols: int
+    in_dtype: str
+    out_dtype: str
+    alpha: float
+    period: int = 0              # causal: queries per head (0: no mask)
+
+    @property
+    def in_bytes(self) -> int:
+        return 4 if self.in_dtype == F32 else 2
+
+    @property
+    def out_bytes(self) -> int:
+        return 4 if self.out_dtype == F32 else 2
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """y and dy read once plus dx written once."""
+        return self.rows * self.cols * (2 * self.in_bytes + self.out_bytes)
+
+
+BACKWARD_WORKLOADS = {w.name: w for w in (
+    BackwardWorkload("bwd_small_262144x64", 262144, 64, BF16, BF16, 0.5),
+    BackwardWorkload("bwd_causal_32768x4096", 32768, 4096, BF16, BF16, 0.1, period=4096),
+    BackwardWorkload("bwd_large_1024x262144", 1024, 262144, F32, F32, 0.05),
+)}
+
+
 def _gen(seed: int, device) -> torch.Generator:
     g = torch.Generator(device=device)
     g.manual_seed(seed)
@@ -119,6 +165,31 @@ def random_matrix(rows: int, cols: int, dtype: str, sigma: float = 1.0, seed: in
                     dtype=torch.float32)
     x.mul_(sigma)
     return x.to(TORCH_DTYPES[dtype])
+
+
+def random_probabilities(rows: int, cols: int, dtype: str, alpha: float, seed: int = 2,
+                         period: int = 0, device="cpu") -> torch.Tensor:
+    """Rows of Dirichlet(alpha) samples (see the module notes); with period > 0,
+    row r keeps columns 0 .. r mod period and holds 0 elsewhere."""
+    conc = torch.full((rows, cols), float(alpha), device=device, dtype=torch.float32)
+    g = torch._standard_gamma(conc, generator=_gen(seed, device))
+    del conc
+    if period > 0:
+        col = torch.arange(cols, device=device)
+        lim = torch.arange(rows, device=device) % period
+        g.masked_fill_(col[None, :] > lim[:, None], 0.0)
+    tot = g.sum(dim=1, keepdim=True)
+    g.div_(torch.where(tot > 0, tot, torch.ones_like(tot)))
+    return g.to(TORCH_DTYPES[dtype])
+
+
+def make_backward_inputs(w: BackwardWorkload, device="cpu", rows: int | None = None):
+    """(y, dy) of a backward workload on ``device`` in its input dtype."""
+    R = w.rows if rows is None else rows
+    y = random_probabilities(R, w.cols, w.in_dtype, w.alpha, seed=2, period=w.period,
+                             device=device)
+    dy = random_matrix(R, w.cols, w.in_dtype, sigma=1.0, seed=3, device=device)
+    return y, dy
 
 
 def to_bits_numpy(t: torch.Tensor):

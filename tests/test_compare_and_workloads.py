@@ -72,3 +72,75 @@ def test_recipes_on_cpu():
     # seeds are honoured: same seed, same tensor
     assert torch.equal(W.random_matrix(5, 7, "bf16", 3.0, seed=4),
                        W.random_matrix(5, 7, "bf16", 3.0, seed=4))
+
+
+def test_log_rule():
+    from oracle.compare import compare_log
+    v = np.array([0.0, -1.0, -20.0, -np.inf, np.nan, -1e-7])
+    assert compare_log(v.copy(), v, "f32")["ok"]
+    y = v.copy()
+    y[2] = -20.0 - (1e-5 + 2.0 ** -22 * 20) * 1.01      # just over the bound
+    r = compare_log(y, v, "f32")
+    assert not r["ok"] and r["n_over_tol"] == 1
+    y = v.copy()
+    y[1] = -np.inf                                       # -inf where v is finite
+    assert compare_log(y, v, "f32")["inf_mismatch"] == 1
+    y = v.copy()
+    y[3] = -1e30                                         # finite where v is -inf
+    assert not compare_log(y, v, "f32")["ok"]
+    y = v.copy()
+    y[0] = np.nan
+    assert compare_log(y, v, "f32")["nan_mismatch"] == 1
+    # bf16: one ulp of v on top of the fp32 bound
+    y = v.copy()
+    y[2] = -20.0 - 2.0 ** -3                              # ulp_bf16(20) = 2^-3
+    assert compare_log(y, v, "bf16")["ok"]
+    y[2] = -20.0 - 2.0 ** -2
+    assert not compare_log(y, v, "bf16")["ok"]
+    # a finite v beyond the output range must come out as -inf
+    w = np.array([-6e38])
+    assert compare_log(np.array([-np.inf]), w, "f32")["ok"]
+    assert not compare_log(np.array([-3.4e38]), w, "f32")["ok"]
+
+
+def test_backward_rule():
+    from oracle.compare import compare_backward
+    import oracle
+    rng = np.random.default_rng(4)
+    y = rng.dirichlet(np.full(50, 0.3), size=6)
+    dy = rng.normal(size=(6, 50))
+    y[2, 7] = 0.0
+    v = oracle.softmax_backward_f64(y, dy)
+    assert compare_backward(v.copy(), v, y, dy, "f32")["ok"]
+    # fp32 evaluation of the same formula is inside the bound
+    y32, dy32 = y.astype(np.float32), dy.astype(np.float32)
+    d32 = np.sum(y32 * dy32, axis=1, keepdims=True, dtype=np.float32)
+    g32 = (y32 * (dy32 - d32)).astype(np.float64)
+    v32 = oracle.softmax_backward_f64(y32.astype(np.float64), dy32.astype(np.float64))
+    assert compare_backward(g32, v32, y32, dy32, "f32")["ok"]
+    # a dropped product in the dot is far outside it
+    bad = v.copy()
+    k = int(np.argmax(np.abs(y[1] * dy[1])))
+    bad[1] = y[1] * (dy[1] - (np.sum(y[1] * dy[1]) - y[1, k] * dy[1, k]))
+    assert not compare_backward(bad, v, y, dy, "f32")["ok"]
+    # y == 0 must give exact zeros; NaN positions must agree
+    bad = v.copy()
+    bad[2, 7] = 1e-30
+    assert compare_backward(bad, v, y, dy, "f32")["zero_mismatch"] == 1
+    bad = v.copy()
+    bad[0, 0] = np.nan
+    assert compare_backward(bad, v, y, dy, "f32")["nan_mismatch"] == 1
+
+
+def test_backward_inputs_are_probability_rows():
+    from paper_2607_23089_amd import workloads as W
+    w = W.BACKWARD_WORKLOADS["bwd_causal_32768x4096"]
+    y, dy = W.make_backward_inputs(w, rows=6)
+    yf = y.float()
+    assert y.dtype == torch.bfloat16 and dy.shape == y.shape
+    assert torch.all(yf >= 0)
+    assert float((yf.sum(1) - 1).abs().max()) < 0.02          # bf16-rounded rows
+    for r in range(6):
+        assert torch.all(yf[r, r + 1:] == 0)                   # causal zeros
+    y2, _ = W.make_backward_inputs(w, rows=6)
+    assert torch.equal(y, y2)                                   # seeded

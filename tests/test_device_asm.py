@@ -66,15 +66,24 @@ def test_no_immediate_overwrite_of_store_data(asm):
 
 
 @pytest.mark.parametrize("pattern", [
-    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELb0E",      # small_262144x64
-    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELb0E",     # causal_32768x4096
-    r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0ELb0E",      # fp32_64x1000
-    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELb0E",    # vocab_4096x151936
-    r"split_row_kernelINS_3F32ES1_Li4ELi16ELb0E",          # large_1024x262144
-    r"large_row_kernelINS_3F32ES1_Li4ELi4ELb0E",           # two-pass form
-    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELb1E",     # fused causal 32768x4096
-    r"split_row_kernelINS_3F32ES1_Li4ELi8ELb1E",           # fused f32 long rows
-    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELb1E",      # fused small rows
+    # template arguments: ..., output form (0 softmax, 1 fused, 2 log)
+    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELi0E",      # small_262144x64
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELi0E",     # causal_32768x4096
+    r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0ELi0E",      # fp32_64x1000
+    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELi0E",    # vocab_4096x151936
+    r"split_row_kernelINS_3F32ES1_Li4ELi16ELi0E",          # large_1024x262144
+    r"large_row_kernelINS_3F32ES1_Li4ELi4ELi0E",           # two-pass form
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELi1E",     # fused causal 32768x4096
+    r"split_row_kernelINS_3F32ES1_Li4ELi8ELi1E",           # fused f32 long rows
+    r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELi1E",      # fused small rows
+    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELi2E",    # log-softmax vocab_4096x151936
+    r"split_row_kernelINS_3F32ES1_Li4ELi16ELi2E",          # log-softmax 1024x262144
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi19ELb1ELi2E",    # log-softmax packed bf16 151936
+    r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELi2E",     # log-softmax 4096-wide rows
+    r"bwd_small_kernelINS_4BF16ES1_Li8ELi8ELi4EEE",        # bwd_small_262144x64
+    r"bwd_medium_kernelINS_4BF16ES1_Li8ELi2EEE",           # bwd_causal_32768x4096
+    r"bwd_split_kernelINS_3F32ES1_Li4ELi8EEE",             # bwd_large_1024x262144
+    r"bwd_large_kernelINS_3F32ES1_Li4ELi4EEE",             # backward two-pass form
 ])
 def test_workload_kernels_do_not_spill(asm, pattern):
     ks = {k: v for k, v in kernels(asm).items() if re.search(pattern, k)}
@@ -87,7 +96,7 @@ def test_split_exchange_has_no_cache_maintenance(asm):
     # The exchange words are self-validating 64-bit atomics: no L2 write-back
     # or invalidation may appear in the split kernel (each one serialises the
     # whole device), and the polls and stores are device-coherent (sc1).
-    body = asm[asm.index("split_row_kernelINS_3F32ES1_Li4ELi16ELb0E"):]
+    body = asm[asm.index("split_row_kernelINS_3F32ES1_Li4ELi16ELi0E"):]
     body = body[:body.index("s_endpgm")]
     assert "buffer_wbl2" not in body and "buffer_inv" not in body
     assert "s_sleep" in body
@@ -98,7 +107,8 @@ def test_split_exchange_has_no_cache_maintenance(asm):
 def test_expected_instructions(asm):
     for ins in ("row_half_mirror", "row_mirror", "quad_perm:[1,0,3,2]",
                 "v_permlane16_swap_b32", "v_permlane32_swap_b32", "v_exp_f32",
-                "v_cvt_pk_bf16_f32", "buffer_load_dwordx4", "buffer_store_dwordx4"):
+                "v_cvt_pk_bf16_f32", "buffer_load_dwordx4", "buffer_store_dwordx4",
+                "v_log_f32"):
         assert ins in asm, ins
     # no packed-fp32 arithmetic anywhere
     assert not re.search(r"v_pk_(add|mul|fma)_f32", asm)

@@ -1,0 +1,215 @@
+"""GPU parity of the softmax backward (rowsm_softmax_backward) against the
+fp64 oracle of dx = y * (dy - sum(y * dy)), for every family and form and
+every dtype pair; special values, in place, misaligned rows, determinism;
+and the full-size backward workloads (sampled rows element by element, every
+row through properties that hold at any size).  Tolerance (oracle/compare.py,
+compare_backward): |dx - v| <= |y| (2^-17 sum|y dy| + 2^-23 |dy - d|) +
+2^-23 |v|, one bf16 ulp more for bf16 output; NaN and infinity positions
+identical, y == 0 gives exactly 0.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_23089_amd as R
+from oracle.compare import compare_backward, widen_output
+from paper_2607_23089_amd import workloads as W
+from test_gpu_parity import DEV, DT, PAIRS
+
+pytestmark = pytest.mark.gpu
+
+
+def widen_in(t: torch.Tensor) -> np.ndarray:
+    b = W.to_bits_numpy(t)
+    v = oracle.widen_bf16_bits(b) if t.dtype == torch.bfloat16 else oracle.widen_f32(b)
+    return v.reshape(-1, t.shape[-1])
+
+
+def assert_bwd_parity(y_cpu, dy_cpu, dx_dev, dout, what=""):
+    y, dy = widen_in(y_cpu), widen_in(dy_cpu)
+    v = oracle.softmax_backward_f64(y, dy, threads=4)
+    dx = widen_output(W.to_bits_numpy(dx_dev), dout).reshape(v.shape)
+    res = compare_backward(dx, v, y, dy, dout)
+    assert res["ok"], f"{what}: {res}"
+    return res
+
+
+def run_bwd(y_dev, dy_dev, dout, config=None, out=None):
+    dx = R.softmax_backward(y_dev, dy_dev, out_dtype=DT[dout], out=out, config=config)
+    torch.cuda.synchronize()
+    return dx
+
+
+def bwd_accepts(rows, cols, din, dout, cfg):
+    st, _ = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                R.dtype_code(DT[dout]), cfg)
+    return st == R.OK
+
+
+def inputs(rows, cols, din, alpha=0.3, seed=0):
+    y = W.random_probabilities(rows, cols, din, alpha, seed=seed + 2)
+    dy = W.random_matrix(rows, cols, din, sigma=1.0, seed=seed + 3)
+    return y, dy
+
+
+GRID = {
+    R.SMALL: [1, 2, 7, 8, 31, 64, 65, 200, 256],
+    R.MEDIUM: [1, 33, 1000, 1023, 4096, 4097, 16385, 32768, 65536],
+    R.LARGE: [1, 1000, 65540, 100003, 262144],
+}
+
+
+def grid_cases():
+    for fam, cols_list in GRID.items():
+        for din, dout in PAIRS:
+            for cols in cols_list:
+                for rows in (3, 37):
+                    if rows * cols <= 3_000_000:
+                        yield fam, din, dout, rows, cols
+
+
+@pytest.mark.parametrize("fam,din,dout,rows,cols", list(grid_cases()))
+def test_bwd_family_grid(fam, din, dout, rows, cols):
+    cfg = R.RowsmConfig(variant=fam)
+    if not bwd_accepts(rows, cols, din, dout, cfg):
+        pytest.skip("family does not take this shape")
+    y, dy = inputs(rows, cols, din, seed=rows + cols)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout, config=cfg)
+    assert_bwd_parity(y, dy, dx, dout, f"bwd {R.VARIANT_NAMES[fam]} {rows}x{cols} {din}->{dout}")
+
+
+FORMS = {
+    "two_pass": (5, 70001, dict(variant=R.LARGE, split_blocks=-1)),
+    "two_pass_u8": (3, 150001, dict(variant=R.LARGE, split_blocks=-1, tile_vectors=8)),
+    "split_2": (7, 20000, dict(variant=R.LARGE, split_blocks=2)),
+    "split_64": (3, 300000, dict(variant=R.LARGE, split_blocks=64)),
+    "split_1024": (4, 200000, dict(variant=R.LARGE, block=1024)),
+    "medium_wpr16": (9, 3000, dict(variant=R.MEDIUM, waves_per_row=16)),
+    "medium_rpb1": (9, 3000, dict(variant=R.MEDIUM, waves_per_row=2, rows_per_block=1)),
+    "small_rpl1": (100, 40, dict(variant=R.SMALL, rows_per_lane=1)),
+    "small_rpl8_l32": (100, 40, dict(variant=R.SMALL, rows_per_lane=8, lanes_per_row=32)),
+}
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("form", sorted(FORMS))
+def test_bwd_forms(form, din, dout):
+    rows, cols, cfg = FORMS[form]
+    cfg = R.RowsmConfig(**cfg)
+    if not bwd_accepts(rows, cols, din, dout, cfg):
+        pytest.skip("form does not take this shape")
+    y, dy = inputs(rows, cols, din, alpha=0.1, seed=cols)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout, config=cfg)
+    assert_bwd_parity(y, dy, dx, dout, f"bwd {form} {din}->{dout}")
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("fam", [R.SMALL, R.MEDIUM, R.LARGE])
+def test_bwd_special_values(fam, din, dout):
+    cols = {R.SMALL: 48, R.MEDIUM: 1000, R.LARGE: 70000}[fam]
+    y, dy = inputs(8, cols, "f32", seed=5)
+    dy[0, 3] = float("nan")              # NaN gradient: the whole row is NaN
+    dy[1, 0] = float("inf")              # infinite gradient: d = +inf
+    y[2, :] = 0.0                        # zero row: exact zeros
+    y[3, ::2] = 0.0                      # zeros inside a row stay exact zeros
+    dy[4, :] = 0.75                      # constant gradient: dx ~ 0
+    y[5, :] = 0.0
+    y[5, cols // 3] = 1.0                # one-hot y: dx = 0 everywhere
+    dy[6, :] = 0.0                       # zero gradient
+    y[7, 1] = float("nan")               # NaN probability
+    y, dy = y.to(DT[din]), dy.to(DT[din])
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout, config=R.RowsmConfig(variant=fam))
+    assert_bwd_parity(y, dy, dx, dout, f"bwd special {R.VARIANT_NAMES[fam]} {din}->{dout}")
+    dxc = dx.cpu().float()
+    assert torch.isnan(dxc[0]).all()
+    # d = +inf: dx = y * (dy - inf) = -inf where y > 0, NaN at the inf entry
+    # (inf - inf) and where y == 0 (0 * -inf)
+    yc = y.float()
+    assert torch.isnan(dxc[1, 0])
+    assert torch.all(dxc[1, 1:][yc[1, 1:] > 0] == float("-inf"))
+    assert torch.isnan(dxc[1, 1:][yc[1, 1:] == 0]).all()
+    assert torch.all(dxc[2] == 0) and torch.all(dxc[5] == 0) and torch.all(dxc[6] == 0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("fam,cols", [(R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 80000)])
+def test_bwd_in_place(fam, cols, dt):
+    cfg = R.RowsmConfig(variant=fam)
+    y, dy = inputs(9, cols, dt, seed=9)
+    yd, dyd = y.to(DEV), dy.to(DEV)
+    run_bwd(yd, dyd, dt, config=cfg, out=dyd)          # dx over dy
+    assert_bwd_parity(y, dy, dyd, dt, f"bwd in place over dy {R.VARIANT_NAMES[fam]}")
+    yd, dyd = y.to(DEV), dy.to(DEV)
+    run_bwd(yd, dyd, dt, config=cfg, out=yd)           # dx over y
+    assert_bwd_parity(y, dy, yd, dt, f"bwd in place over y {R.VARIANT_NAMES[fam]}")
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+def test_bwd_misaligned_rows(din, dout):
+    for fam, cols in ((R.SMALL, 24), (R.MEDIUM, 1024), (R.LARGE, 65600)):
+        yb, dyb = inputs(1, 5 * cols + 1, din, seed=cols)
+        y = yb.to(DEV).view(-1)[1:].view(5, cols)
+        dy = dyb.to(DEV).view(-1)[1:].view(5, cols)
+        dx = run_bwd(y, dy, dout, config=R.RowsmConfig(variant=fam))
+        assert_bwd_parity(y.cpu(), dy.cpu(), dx, dout,
+                          f"bwd misaligned {R.VARIANT_NAMES[fam]} {din}->{dout}")
+
+
+def test_bwd_same_buffer_inputs_and_errors():
+    # y and dy may be the same buffer (read only)
+    y, _ = inputs(6, 3000, "f32", seed=1)
+    yd = y.to(DEV)
+    dx = run_bwd(yd, yd, "f32")
+    assert_bwd_parity(y, y, dx, "f32", "bwd y == dy")
+    # dx partially overlapping an input, or in place with a dtype change:
+    # refused before any launch
+    yb = torch.zeros(4, 64, device=DEV, dtype=torch.bfloat16)
+    d = torch.zeros(4, 64, device=DEV, dtype=torch.bfloat16)
+    f = R.rowsm_softmax_backward
+    assert f(yb.data_ptr(), d.data_ptr(), yb.data_ptr() + 2, 4, 64, R.BF16, R.BF16, 0) == R.EINVAL
+    assert f(yb.data_ptr(), d.data_ptr(), d.data_ptr() + 2, 4, 64, R.BF16, R.BF16, 0) == R.EINVAL
+    assert f(yb.data_ptr(), d.data_ptr(), d.data_ptr(), 4, 64, R.BF16, R.F32, 0) == R.EINVAL
+    empty = torch.empty(0, 8, device=DEV)
+    assert run_bwd(empty, empty, "f32").shape == (0, 8)
+
+
+def test_bwd_deterministic():
+    for fam, cols in ((R.MEDIUM, 8000), (R.LARGE, 150000)):
+        y, dy = inputs(16, cols, "f32", seed=2)
+        yd, dyd = y.to(DEV), dy.to(DEV)
+        a = run_bwd(yd, dyd, "f32", config=R.RowsmConfig(variant=fam))
+        b = run_bwd(yd, dyd, "f32", config=R.RowsmConfig(variant=fam))
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("name", list(W.BACKWARD_WORKLOADS))
+def test_bwd_workload_full_size(name):
+    w = W.BACKWARD_WORKLOADS[name]
+    print(f"backward workload {name}: {w.rows}x{w.cols} {w.in_dtype}->{w.out_dtype}", flush=True)
+    y, dy = W.make_backward_inputs(w, device=DEV)
+    dx = torch.empty(w.rows, w.cols, dtype=DT[w.out_dtype], device=DEV)
+    st = R.rowsm_softmax_backward(y.data_ptr(), dy.data_ptr(), dx.data_ptr(), w.rows, w.cols,
+                                  R.dtype_code(y.dtype), R.dtype_code(dx.dtype),
+                                  torch.cuda.current_stream().cuda_stream)
+    assert st == R.OK
+    torch.cuda.synchronize()
+    g = np.random.default_rng(7)
+    rows = sorted({0, 1, w.rows // 2, w.rows - 1} | set(int(r) for r in g.integers(0, w.rows, 8)))
+    assert_bwd_parity(y[rows].cpu(), dy[rows].cpu(), dx[rows].cpu(), w.out_dtype,
+                      f"bwd {name} rows {rows}")
+    # every row: finite, exact zeros where y is zero, and
+    # sum_j dx_j = d (1 - sum_j y_j), small for probability rows
+    for r0 in range(0, w.rows, 4096):
+        yb, dyb, dxb = y[r0:r0 + 4096].double(), dy[r0:r0 + 4096].double(), dx[r0:r0 + 4096]
+        assert torch.isfinite(dxb).all()
+        assert torch.all(dxb[yb == 0] == 0)
+        d = (yb * dyb).sum(1)
+        want = d * (1 - yb.sum(1))
+        got = dxb.double().sum(1)
+        scale = (yb * dyb.abs()).sum(1) + (yb * (dyb - d[:, None]).abs()).sum(1)
+        ulp = 2.0 ** -8 if w.out_dtype == "bf16" else 2.0 ** -22
+        assert float(((got - want).abs() - ulp * scale).max()) <= 1e-6
+    assert R.rowsm_split_wait_failures() == 0
+    del y, dy, dx
+    torch.cuda.empty_cache()
