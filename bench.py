@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 # Device code of the kernels; a profile also records each launch's shape.
 KERNEL_SOURCES = ["rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
-                  "split_row.hpp"]
+                  "split_row.hpp", "backward_row.hpp"]
 
 
 def kernel_source_hash() -> str:
@@ -119,6 +119,107 @@ def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
     }
 
 
+# Read-only and write-only rates of plain streaming kernels measured on this
+# GPU; a kernel moving read fraction r and write fraction 1 - r of its bytes
+# is bounded by 1 / (r / READ + (1 - r) / WRITE).
+MEASURED_READ_GBS = 6870.0
+MEASURED_WRITE_GBS = 5950.0
+
+
+def mix_bound_gbs(read_bytes: float, write_bytes: float) -> float:
+    tot = read_bytes + write_bytes
+    return tot / (read_bytes / MEASURED_READ_GBS + write_bytes / MEASURED_WRITE_GBS)
+
+
+def timed_alone(fn, reps: int, flush, stream) -> float:
+    """Average microseconds of fn() over reps launches (after 2 untimed),
+    each preceded by a 1 GiB write that evicts the memory-side cache."""
+    import torch
+    ts = []
+    for i in range(reps + 2):
+        flush.zero_()
+        e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if i >= 2:
+            ts.append(e0.elapsed_time(e1))
+    return sum(ts) / len(ts) * 1e3
+
+
+def log_softmax_leg(reps: int):
+    """Log-softmax on the long-row workloads (its cross-entropy use), each
+    launch timed alone, next to softmax on the same input under the same
+    protocol.  Algorithmic bytes: x read once plus y written once."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    out = {}
+    for name in ("vocab_4096x151936", "large_1024x262144"):
+        w = W.WORKLOADS[name]
+        x = W.make_input(w, device=dev)
+        y = torch.empty(w.rows, w.cols, dtype=W.TORCH_DTYPES[w.out_dtype], device=dev)
+        di, do = R.dtype_code(x.dtype), R.dtype_code(y.dtype)
+        log_us = timed_alone(lambda: R.check(R.rowsm_log_softmax(
+            x.data_ptr(), y.data_ptr(), w.rows, w.cols, di, do, sh, None)), reps, flush, stream)
+        sm_us = timed_alone(lambda: R.check(R.rowsm_forward(
+            x.data_ptr(), y.data_ptr(), w.rows, w.cols, di, do, sh)), reps, flush, stream)
+        gbs = w.algorithmic_bytes / (log_us * 1e-6) / 1e9
+        bound = mix_bound_gbs(w.rows * w.cols * w.in_bytes, w.rows * w.cols * w.out_bytes)
+        _, desc = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, w.rows, w.cols, di, do)
+        out[name] = {
+            "launch": desc, "hbm_bytes_per_launch": measured_traffic(f"log_softmax/{name}", desc),
+            "algorithmic_bytes": w.algorithmic_bytes, "avg_us": log_us,
+            "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
+            "frac_of_measured_mix_bound": gbs / bound,
+            "softmax_same_protocol_us": sm_us,
+        }
+        del x, y
+    return out
+
+
+def backward_leg(reps: int):
+    """Softmax backward on the backward workloads, each launch timed alone.
+    Algorithmic bytes: y and dy read once plus dx written once."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    out = {}
+    for name, w in W.BACKWARD_WORKLOADS.items():
+        y, dy = W.make_backward_inputs(w, device=dev)
+        dx = torch.empty(w.rows, w.cols, dtype=W.TORCH_DTYPES[w.out_dtype], device=dev)
+        di, do = R.dtype_code(y.dtype), R.dtype_code(dx.dtype)
+        us = timed_alone(lambda: R.check(R.rowsm_softmax_backward(
+            y.data_ptr(), dy.data_ptr(), dx.data_ptr(), w.rows, w.cols, di, do, sh)),
+            reps, flush, stream)
+        gbs = w.algorithmic_bytes / (us * 1e-6) / 1e9
+        bound = mix_bound_gbs(2 * w.rows * w.cols * w.in_bytes, w.rows * w.cols * w.out_bytes)
+        _, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, w.rows, w.cols, di, do)
+        out[name] = {
+            "launch": desc, "hbm_bytes_per_launch": measured_traffic(f"softmax_backward/{name}", desc),
+            "algorithmic_bytes": w.algorithmic_bytes, "avg_us": us,
+            "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
+            "frac_of_measured_mix_bound": gbs / bound,
+        }
+        del y, dy, dx
+    if R.rowsm_split_wait_failures() != 0:
+        raise R.RowsmError("split-row exchange waits gave up: results invalid")
+    return out
+
+
 def fused_causal_leg(reps: int):
     """The fused form (scale and causal mask computed in the kernel) on the
     causal workload's shape, next to the plain form on the same scores with
@@ -141,17 +242,7 @@ def fused_causal_leg(reps: int):
     scale = 0.125  # 1/sqrt(64), a head dimension of 64
 
     def timed(fn):
-        ts = []
-        for i in range(reps + 2):
-            flush.zero_()
-            e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
-            e0.record(stream)
-            fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            if i >= 2:
-                ts.append(e0.elapsed_time(e1))
-        return sum(ts) / len(ts) * 1e3
+        return timed_alone(fn, reps, flush, stream)
 
     sh = stream.cuda_stream
     fused_us = timed(lambda: R.check(R.rowsm_forward_scaled_causal(
@@ -181,7 +272,8 @@ def main() -> int:
     ap.add_argument("--regimes", default=None,
                     help="comma-separated subset of the regimes (default: all four)")
     ap.add_argument("--no-next", action="store_true",
-                    help="skip the extra measurement of the fused scale+causal form")
+                    help="skip the measurements of the fused scale+causal form, "
+                         "log-softmax and the softmax backward")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="minimum seconds of oracle time for the CPU baseline (0 = skip)")
     args = ap.parse_args()
@@ -299,7 +391,9 @@ def main() -> int:
         "regimes_detail": per,
     }
     if not args.no_next:
-        result["next_rows"] = {"fused_scale_causal": fused_causal_leg(reps=10)}
+        result["next_rows"] = {"fused_scale_causal": fused_causal_leg(reps=10),
+                               "log_softmax": log_softmax_leg(reps=10),
+                               "softmax_backward": backward_leg(reps=10)}
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(inputs, outputs, regimes, args.cpu_budget)
     print(json.dumps(result), flush=True)
