@@ -162,3 +162,62 @@ def test_describe(lib):
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(R.RowsmError):
         R.lib(str(tmp_path / "missing.so"))
+
+
+def test_log_softmax_argument_errors(lib):
+    f = R.rowsm_log_softmax
+    assert f(X, Y, 4, 8, 7, R.F32, 0) == R.EDTYPE
+    assert f(X, Y, -4, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(0, Y, 4, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, X + 4, 4, 8, R.F32, R.F32, 0) == R.EINVAL        # partial overlap
+    assert f(X, X, 4, 8, R.BF16, R.F32, 0) == R.EINVAL           # in place, dtype change
+    assert f(0, 0, 0, 8, R.F32, R.F32, 0) == R.OK                # empty
+    assert f(X, Y, 64, 64, R.F32, R.F32, 0, R.RowsmConfig(variant=R.SMALL,
+                                                         lanes_per_row=3)) == R.EINVAL
+    # log-softmax takes the softmax plans
+    for rows, cols, i, o in ((262144, 64, R.BF16, R.BF16), (64, 151936, R.BF16, R.BF16),
+                             (4096, 151936, R.BF16, R.F32), (1024, 262144, R.F32, R.F32)):
+        a = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, rows, cols, i, o)
+        b = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, i, o)
+        assert a == b and a[0] == R.OK
+
+
+def test_backward_argument_errors(lib):
+    f = R.rowsm_softmax_backward
+    D = 0x7f4000000000                                             # a third fake buffer
+    assert f(X, Y, D, 4, 8, 7, R.F32, 0) == R.EDTYPE
+    assert f(X, Y, D, 4, 8, R.F32, 5, 0) == R.EDTYPE
+    assert f(X, Y, D, -1, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(0, Y, D, 4, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, 0, D, 4, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, Y, 0, 4, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, Y, X + 4, 4, 8, R.F32, R.F32, 0) == R.EINVAL       # dx partially over y
+    assert f(X, Y, Y + 4, 4, 8, R.F32, R.F32, 0) == R.EINVAL       # dx partially over dy
+    assert f(X, Y, Y, 4, 8, R.BF16, R.F32, 0) == R.EINVAL          # in place, dtype change
+    assert f(X, Y, D, 1, 1 << 30, R.F32, R.F32, 0) == R.EINVAL     # row too long
+    assert f(0, 0, 0, 0, 8, R.F32, R.F32, 0) == R.OK               # empty: no launch
+    assert f(X, Y, D, 64, 64, R.F32, R.F32, 0, R.RowsmConfig(packed=1)) == R.EINVAL
+    assert f(X, Y, D, 64, 4096, R.F32, R.F32, 0, R.RowsmConfig(variant=R.SMALL)) == R.EINVAL
+    assert f(X, Y, D, 64, 64, R.F32, R.F32, 0, R.RowsmConfig(variant=R.LARGE,
+                                                             split_blocks=65)) == R.EINVAL
+
+
+def test_backward_plans(lib):
+    d = lambda rows, cols, i, o, **cfg: R.rowsm_describe_op(
+        R.OP_SOFTMAX_BACKWARD, rows, cols, i, o, R.RowsmConfig(**cfg) if cfg else None)
+    st, t = d(262144, 64, R.BF16, R.BF16)
+    assert st == R.OK and t.startswith("small") and "lpr=8" in t and "rpl=4" in t
+    st, t = d(32768, 4096, R.BF16, R.BF16)
+    assert st == R.OK and t.startswith("medium") and "wpr=4" in t and "nv=2" in t
+    # medium holds at most 128 bytes of each input per lane: 16 x 64 x 8 vectors
+    assert d(4, 65536, R.BF16, R.BF16)[1].startswith("medium")
+    assert d(4, 65544, R.BF16, R.BF16)[1].startswith("large")
+    assert d(4, 32768, R.F32, R.F32)[1].startswith("medium")
+    st, t = d(1024, 262144, R.F32, R.F32)
+    assert st == R.OK and "split=32" in t and "nv=8" in t and "block=256" in t
+    # past 64 blocks x 256 threads x 8 vectors: the two-pass form
+    st, t = d(4, 64 * 256 * 8 * 4 + 4, R.F32, R.F32)
+    assert st == R.OK and "split=0" in t and "block=1024" in t
+    assert d(4, 100, R.F32, R.F32, variant=R.MEDIUM, waves_per_row=16)[0] == R.OK
+    assert d(4, 8, 9, R.F32)[0] == R.EDTYPE
+    assert R.rowsm_describe_op(9, 4, 8, R.F32, R.F32)[0] == R.EINVAL
