@@ -17,11 +17,16 @@ Contents
   * ``log_softmax_f64``  -- x - max - log(sum exp(x - max)) per row.
   * ``softmax_backward_f64`` -- dx = y * (dy - sum(y * dy)) per row, the
                          softmax Jacobian applied to dy.
+  * ``moe_group_top2_f64`` -- the paper's running example (``moe_group_f64.c``):
+                         per group of G consecutive expert scores, the sum of
+                         its two largest values (a tied maximum counts twice),
+                         an fp32 sum rounded to the output dtype.
   * ``widen_f32`` / ``widen_bf16_bits`` -- exact widening of the stored input
                          bit patterns to fp64 (bf16 -> bits << 16 -> fp32 ->
                          fp64), so the oracle sees exactly the values the GPU
                          reads.
-  * ``build``         -- compiles ``softmax_f64.c`` with gcc.
+  * ``build``         -- compiles ``softmax_f64.c`` with gcc (``build_moe``:
+                         ``moe_group_f64.c``).
 
 The oracle is pinned by tests/test_oracle.py (high-precision brute force with a
 different formula, closed forms, invariants, library routines) and
@@ -39,7 +44,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "softmax_f64.c")
 _LIB = os.path.join(_HERE, "liboracle_softmax.so")
 
+_MOE_SRC = os.path.join(_HERE, "moe_group_f64.c")
+_MOE_LIB = os.path.join(_HERE, "liboracle_moe.so")
+
 _lib = None
+_moe_lib = None
 
 
 def gcc_command(src: str, out: str) -> list:
@@ -89,6 +98,50 @@ def load(path: str | None = None):
     if path == _LIB:
         _lib = lib
     return lib
+
+
+def build_moe(src: str = _MOE_SRC, out: str = _MOE_LIB) -> str:
+    """Compile the MoE group-score oracle; returns the library path."""
+    return build(src, out)
+
+
+def load_moe(path: str | None = None):
+    """Load (building first if absent) the MoE group-score oracle library."""
+    global _moe_lib
+    if path is None:
+        if _moe_lib is not None:
+            return _moe_lib
+        if not os.path.exists(_MOE_LIB):
+            build_moe()
+        path = _MOE_LIB
+    lib = ctypes.CDLL(path)
+    fn = lib.oracle_moe_group_top2_f64
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                   ctypes.c_int64, ctypes.c_int]
+    if path == _MOE_LIB:
+        _moe_lib = lib
+    return lib
+
+
+def moe_group_top2_f64(scores: np.ndarray, group: int, out_dtype: str = "f32",
+                       lib=None) -> np.ndarray:
+    """tokens x experts scores (fp64 values of the stored scores) ->
+    tokens x (experts / group) group scores, each the fp32 sum of the group's
+    two largest values rounded to ``out_dtype`` ('f32' or 'bf16'), as fp64."""
+    s = np.ascontiguousarray(np.asarray(scores, dtype=np.float64))
+    if s.ndim == 1:
+        s = s[None, :]
+    tokens, experts = s.shape
+    if group < 2 or experts % group:
+        raise ValueError("group must be >= 2 and divide the expert count")
+    out = np.full((tokens, experts // group), np.nan)
+    lib = lib if lib is not None else load_moe()
+    rc = lib.oracle_moe_group_top2_f64(s.ctypes.data, out.ctypes.data, tokens, experts,
+                                       int(group), 1 if out_dtype == "bf16" else 0)
+    if rc != 0:
+        raise RuntimeError(f"oracle_moe_group_top2_f64 failed with status {rc}")
+    return out
 
 
 def softmax_f64(x: np.ndarray, threads: int = 1, lib=None) -> np.ndarray:

@@ -422,3 +422,104 @@ def run_backward_pins(bwd, sm) -> list:
     if not np.allclose(np.asarray(bwd(y, dy + 3.0)), dx, rtol=0, atol=1e-14):
         fail("backward_shift", "dy + c changed dx")
     return fails
+
+
+# ---------------------------------------------------------------------------
+# MoE group score: per group of G scores, the sum of the two largest values.
+
+def _f32(x):
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def _bf16_rne(x32):
+    """fp32 values -> nearest bf16 (ties to even), as fp64; NaN kept."""
+    a = np.asarray(x32, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000).astype(np.uint32)
+    out = r.view(np.float32).astype(np.float64)
+    return np.where(np.isnan(a), np.nan, out)
+
+
+def brute_force_group_pairs(scores, group, out_dtype="f32"):
+    """The paper's identity written out: max over i != j of v_i + v_j (every
+    ordered pair, the diagonal excluded), the exact double sum of two stored
+    values rounded once to float, then to bf16 if asked.  NaN in a group -> NaN."""
+    s = np.asarray(scores, dtype=np.float64)
+    t, e = s.shape
+    v = s.reshape(t, e // group, group)
+    with np.errstate(invalid="ignore"):
+        pair = v[..., :, None] + v[..., None, :]
+    eye = np.eye(group, dtype=bool)
+    pair = np.where(eye, -np.inf, pair)
+    has_nan = np.isnan(v).any(axis=-1)
+    with np.errstate(invalid="ignore"):
+        best = np.where(np.isnan(pair), -np.inf, pair).max(axis=(-1, -2))
+    # a pair sum that is NaN without a NaN input is +inf + -inf: keep it only
+    # when no larger pair exists
+    inf_nan = np.isnan(pair).any(axis=(-1, -2)) & ~has_nan & (best == -np.inf)
+    best = np.where(has_nan | inf_nan, np.nan, best)
+    r = _f32(best)
+    return _bf16_rne(r) if out_dtype == "bf16" else r
+
+
+def _same(a, b):
+    a, b = np.asarray(a, dtype=np.float64), np.asarray(b, dtype=np.float64)
+    return a.shape == b.shape and np.array_equal(np.isnan(a), np.isnan(b)) and \
+        bool(np.all((a == b) | np.isnan(a)))
+
+
+def run_moe_pins(fn) -> list:
+    """fn(scores, group, out_dtype) -> group scores (fp64 array)."""
+    import torch
+    fails = []
+
+    def fail(name, msg):
+        fails.append(f"{name}: {msg}")
+
+    rng = np.random.default_rng(21)
+    for group in (2, 4, 8, 32, 64):
+        # bf16-valued scores: ties are frequent, as with low-precision routing scores
+        x = rng.normal(size=(40, 4 * group))
+        xb = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+        for dt in ("f32", "bf16"):
+            if not _same(fn(xb, group, dt), brute_force_group_pairs(xb, group, dt)):
+                fail("pairwise_identity", f"group={group} {dt}")
+        tk = torch.topk(torch.tensor(xb).view(40, 4, group), 2, dim=-1).values.sum(-1)
+        if not _same(fn(xb, group, "f32"), _f32(tk.view(40, 4).numpy())):
+            fail("torch_topk", f"group={group}")
+    # sums that are not floats: rounded once to float
+    x = np.array([[1.0, 2.0 ** -30, -5.0, 0.0]])
+    if not _same(fn(x, 4, "f32"), [[1.0]]):
+        fail("float_rounding", f"{fn(x, 4, 'f32')}")
+    x = np.array([[1.0, 1.0 + 2.0 ** -23, -1.0, 3.0 * 2.0 ** -25]])
+    if not _same(fn(x, 4, "f32"), _f32([[2.0 + 2.0 ** -23]])):
+        fail("float_rounding_2", f"{fn(x, 4, 'f32')}")
+    # ties: a maximum that occurs twice counts twice (value masking would
+    # give 5 + 1)
+    x = np.array([[5.0, 1.0, 5.0, -2.0, 0.5, 1.0, 1.0, 0.0]])
+    if not _same(fn(x, 8, "f32"), [[10.0]]):
+        fail("tied_max", f"{fn(x, 8, 'f32')}")
+    if not _same(fn(np.full((1, 32), -0.75), 32, "f32"), [[-1.5]]):
+        fail("constant_group", "")
+    x = np.array([[3.0, 1.0, 2.0, 2.0, -9.0, 7.0, 7.0, 7.0]])
+    if not _same(fn(x, 4, "f32"), [[5.0, 14.0]]):
+        fail("two_groups", f"{fn(x, 4, 'f32')}")
+    # special values
+    x = np.array([[np.nan, 1.0, 2.0, 3.0], [1.0, 2.0, np.nan, 3.0],
+                  [np.inf, -np.inf, -np.inf, -np.inf],
+                  [np.inf, np.inf, 0.0, 1.0], [-np.inf, -np.inf, -np.inf, -np.inf],
+                  [-np.inf, 4.0, -np.inf, -np.inf], [np.inf, 1.0, -np.inf, 2.0]])
+    want = [[np.nan], [np.nan], [np.nan], [np.inf], [-np.inf], [-np.inf], [np.inf]]
+    if not _same(fn(x, 4, "f32"), want):
+        fail("special_values", f"{fn(x, 4, 'f32').ravel().tolist()}")
+    # bf16 output rounds the float sum to nearest, ties to even
+    x = np.array([[1.0, 2.0 ** -8, 0.0, -1.0], [1.0, 3.0 * 2.0 ** -8, 0.0, -1.0],
+                  [1.0, 2.0 ** -9, 0.0, -1.0]])
+    if not _same(fn(x, 4, "bf16"), [[1.0], [1.0 + 2.0 ** -6], [1.0]]):
+        fail("bf16_ties_to_even", f"{fn(x, 4, 'bf16').ravel().tolist()}")
+    # order inside a group does not matter
+    x = rng.normal(size=(16, 32))
+    p = rng.permutation(32)
+    if not _same(fn(x, 32, "f32"), fn(x[:, p], 32, "f32")):
+        fail("permutation", "")
+    return fails
