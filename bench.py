@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 # Device code of the kernels; a profile also records each launch's shape.
 KERNEL_SOURCES = ["rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
-                  "split_row.hpp", "backward_row.hpp"]
+                  "split_row.hpp", "backward_row.hpp", "group_top2.hpp"]
 
 
 def kernel_source_hash() -> str:
@@ -220,6 +220,42 @@ def backward_leg(reps: int):
     return out
 
 
+def moe_leg(reps: int):
+    """MoE group score (sum of the two largest of each group of 32 expert
+    scores) on the MoE workloads, each launch timed alone.  Algorithmic
+    bytes: scores read once plus group scores written once."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    out = {}
+    for name, w in W.MOE_WORKLOADS.items():
+        x = W.make_moe_scores(w, device=dev)
+        o = torch.empty(w.tokens, w.experts // w.group, dtype=W.TORCH_DTYPES[w.out_dtype],
+                        device=dev)
+        di, do = R.dtype_code(x.dtype), R.dtype_code(o.dtype)
+        us = timed_alone(lambda: R.check(R.rowsm_moe_group_top2(
+            x.data_ptr(), o.data_ptr(), w.tokens, w.experts, w.group, di, do, sh)),
+            reps, flush, stream)
+        gbs = w.algorithmic_bytes / (us * 1e-6) / 1e9
+        n = w.tokens * w.experts
+        bound = mix_bound_gbs(n * w.in_bytes, n // w.group * w.out_bytes)
+        _, desc = R.rowsm_describe_op(R.OP_MOE_GROUP_TOP2, n // w.group, w.group, di, do)
+        out[name] = {
+            "launch": desc, "hbm_bytes_per_launch": measured_traffic(f"moe_group_top2/{name}", desc),
+            "algorithmic_bytes": w.algorithmic_bytes, "avg_us": us,
+            "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
+            "frac_of_measured_mix_bound": gbs / bound,
+        }
+        del x, o
+    return out
+
+
 def fused_causal_leg(reps: int):
     """The fused form (scale and causal mask computed in the kernel) on the
     causal workload's shape, next to the plain form on the same scores with
@@ -273,7 +309,7 @@ def main() -> int:
                     help="comma-separated subset of the regimes (default: all four)")
     ap.add_argument("--no-next", action="store_true",
                     help="skip the measurements of the fused scale+causal form, "
-                         "log-softmax and the softmax backward")
+                         "log-softmax, the softmax backward and the MoE group score")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="minimum seconds of oracle time for the CPU baseline (0 = skip)")
     args = ap.parse_args()
@@ -393,7 +429,8 @@ def main() -> int:
     if not args.no_next:
         result["next_rows"] = {"fused_scale_causal": fused_causal_leg(reps=10),
                                "log_softmax": log_softmax_leg(reps=10),
-                               "softmax_backward": backward_leg(reps=10)}
+                               "softmax_backward": backward_leg(reps=10),
+                               "moe_group_top2": moe_leg(reps=10)}
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(inputs, outputs, regimes, args.cpu_budget)
     print(json.dumps(result), flush=True)

@@ -79,7 +79,9 @@ typedef enum {
     ROWSM_OP_SOFTMAX = 0,          /* rowsm_forward, rowsm_forward_config      */
     ROWSM_OP_SCALED_CAUSAL = 1,    /* rowsm_forward_scaled_causal              */
     ROWSM_OP_LOG_SOFTMAX = 2,      /* rowsm_log_softmax                        */
-    ROWSM_OP_SOFTMAX_BACKWARD = 3  /* rowsm_softmax_backward                   */
+    ROWSM_OP_SOFTMAX_BACKWARD = 3, /* rowsm_softmax_backward                   */
+    ROWSM_OP_MOE_GROUP_TOP2 = 4    /* rowsm_moe_group_top2: rows = number of
+                                      groups, cols = group size               */
 } rowsm_op;
 
 /*
@@ -218,6 +220,34 @@ int rowsm_log_softmax(const void *x, void *y, int64_t rows, int64_t cols, int in
  */
 int rowsm_softmax_backward(const void *y, const void *dy, void *dx, int64_t rows, int64_t cols,
                            int in_dtype, int out_dtype, void *stream, const rowsm_config *cfg);
+
+/*
+ * rowsm_moe_group_top2: the MoE group score of the paper's running example
+ * (Motivation section and the figure of its source rewrite).  The experts
+ * scores of each token are cut into consecutive groups of group_size; the
+ * score of a group is the sum of its two largest values counted with
+ * multiplicity (a maximum that occurs twice counts twice), which the paper
+ * shows equals max over i != j of v_i + v_j:
+ *     group_scores[t, g] = top1 + top2 of scores[t, g*G .. g*G + G - 1]
+ *   scores        device pointer, tokens x experts of in_dtype, row-major and
+ *                 contiguous; read only
+ *   group_scores  device pointer, tokens x (experts / group_size) of
+ *                 out_dtype, aligned to its element size; must not overlap
+ *                 scores (ROWSM_EINVAL)
+ *   group_size    a power of two from 2 to 64 that divides experts, else
+ *                 ROWSM_EINVAL (the paper's operator uses 32)
+ *   stream, dtypes, errors: as rowsm_forward; tokens * experts < 2^62
+ *   cfg           NULL = the launcher's choice; only variant (AUTO or SMALL),
+ *                 vw, rows_per_lane (groups per lane: 1, 2, 4, 8) and
+ *                 blocks_per_cu are used
+ * The sum is one fp32 addition of the two stored values, rounded to
+ * out_dtype (nearest, ties to even, for bf16).  A NaN anywhere in a group
+ * makes its score NaN; infinities follow IEEE addition (+inf + -inf = NaN).
+ * Results do not depend on the launch shape.
+ */
+int rowsm_moe_group_top2(const void *scores, void *group_scores, int64_t tokens,
+                         int64_t experts, int64_t group_size, int in_dtype, int out_dtype,
+                         void *stream, const rowsm_config *cfg);
 
 /*
  * rowsm_describe_op: as rowsm_describe for any operation (op: rowsm_op) and

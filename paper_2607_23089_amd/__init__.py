@@ -32,6 +32,7 @@ AUTO, SMALL, MEDIUM, LARGE = 0, 1, 2, 3
 OK, EINVAL, EDTYPE, EHIP = 0, -1, -2, -3
 VARIANT_NAMES = {SMALL: "small", MEDIUM: "medium", LARGE: "large"}
 OP_SOFTMAX, OP_SCALED_CAUSAL, OP_LOG_SOFTMAX, OP_SOFTMAX_BACKWARD = 0, 1, 2, 3
+OP_MOE_GROUP_TOP2 = 4
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "librowsm.so")
@@ -39,7 +40,8 @@ LIB_PATH = os.path.join(_PKG, "librowsm.so")
 # Symbols declared in include/rowsm.h.
 EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
            "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_log_softmax",
-           "rowsm_softmax_backward", "rowsm_describe", "rowsm_describe_op",
+           "rowsm_softmax_backward", "rowsm_moe_group_top2", "rowsm_describe",
+           "rowsm_describe_op",
            "rowsm_split_wait_failures", "rowsm_status_string")
 
 
@@ -95,6 +97,9 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     h.rowsm_softmax_backward.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp,
                                          ctypes.POINTER(RowsmConfig)]
     h.rowsm_softmax_backward.restype = i32
+    h.rowsm_moe_group_top2.argtypes = [vp, vp, i64, i64, i64, i32, i32, vp,
+                                       ctypes.POINTER(RowsmConfig)]
+    h.rowsm_moe_group_top2.restype = i32
     h.rowsm_describe_op.argtypes = [i32, i64, i64, i32, i32, ctypes.POINTER(RowsmConfig),
                                     ctypes.c_char_p, i64]
     h.rowsm_describe_op.restype = i32
@@ -168,6 +173,15 @@ def rowsm_softmax_backward(y, dy, dx, rows, cols, in_dtype, out_dtype, stream=0,
         cfg = RowsmConfig(**cfg)
     ref = ctypes.byref(cfg) if cfg is not None else None
     return lib().rowsm_softmax_backward(y, dy, dx, rows, cols, in_dtype, out_dtype, stream, ref)
+
+
+def rowsm_moe_group_top2(scores, out, tokens, experts, group_size, in_dtype, out_dtype,
+                         stream=0, cfg=None) -> int:
+    if cfg is not None and not isinstance(cfg, RowsmConfig):
+        cfg = RowsmConfig(**cfg)
+    ref = ctypes.byref(cfg) if cfg is not None else None
+    return lib().rowsm_moe_group_top2(scores, out, tokens, experts, group_size, in_dtype,
+                                      out_dtype, stream, ref)
 
 
 def rowsm_split_wait_failures() -> int:
@@ -248,6 +262,30 @@ def softmax_backward(y, dy, out_dtype=None, out=None, config=None, stream=None):
     st = (stream or torch.cuda.current_stream(y.device)).cuda_stream
     check(rowsm_softmax_backward(y.data_ptr(), dy.data_ptr(), out.data_ptr(), rows, cols,
                                  dtype_code(y.dtype), dtype_code(out.dtype), st, config))
+    return out
+
+
+def moe_group_top2(scores, group_size: int = 32, out_dtype=None, out=None, config=None,
+                   stream=None):
+    """MoE group scores of a contiguous tokens x experts fp32/bf16 GPU tensor:
+    the sum of the two largest scores of every group of ``group_size``
+    consecutive experts (see rowsm_moe_group_top2).  Returns ``out``
+    (tokens x experts / group_size, ``out_dtype``, default fp32).
+    Marshalling only."""
+    import torch
+    if not scores.is_cuda or not scores.is_contiguous():
+        raise RowsmError("moe_group_top2 needs a contiguous GPU tensor")
+    experts = scores.shape[-1] if scores.dim() else 1
+    tokens = scores.numel() // experts if experts else 0
+    shape = tuple(scores.shape[:-1]) + (experts // group_size if group_size else 0,)
+    if out is None:
+        out = torch.empty(shape, dtype=out_dtype or torch.float32, device=scores.device)
+    elif tuple(out.shape) != shape or not out.is_contiguous() or out.device != scores.device:
+        raise RowsmError("out must be a contiguous tokens x (experts / group_size) tensor")
+    st = (stream or torch.cuda.current_stream(scores.device)).cuda_stream
+    check(rowsm_moe_group_top2(scores.data_ptr(), out.data_ptr(), tokens, experts,
+                               int(group_size), dtype_code(scores.dtype), dtype_code(out.dtype),
+                               st, config))
     return out
 
 

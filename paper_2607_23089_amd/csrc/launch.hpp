@@ -81,6 +81,10 @@ int launch_bwd_medium(const Call& c, int in_dt, int out_dt);
 int launch_bwd_split(const Call& c, int in_dt, int out_dt);
 int launch_bwd_large(const Call& c, int in_dt, int out_dt);
 
+// MoE group-score launchers (launch_moe_<dtype>.hip).
+int launch_moe_f32(const Call& c, int out_dt);
+int launch_moe_bf16(const Call& c, int out_dt);
+
 // Split-form diagnostics (launch_split_common.hip).
 int64_t split_wait_failures_current_device();
 

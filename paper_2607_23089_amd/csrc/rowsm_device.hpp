@@ -270,6 +270,8 @@ enum : int { kPlain = 0, kFused = 1, kLog = 2 };
 // Tag of the softmax-backward launches in the launcher tables (the backward
 // kernels have no output form of their own).
 constexpr int kBackward = 3;
+// Tag of the MoE group-score launches.
+constexpr int kMoe = 4;
 
 constexpr float kLn2 = 0.69314718055994530942f;
 

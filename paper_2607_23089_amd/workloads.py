@@ -34,6 +34,19 @@ Softmax-backward workloads (y and dy of in dtype, dx of out dtype):
   cast to the input dtype.  This is a probability-vector sampler, not the
   softmax: no exponential and no maximum is involved.
 
+MoE group-score workloads (scores tokens x experts of in dtype; group
+scores tokens x experts / 32 written):
+
+  moe_65536x256_f32      65536 x 256, f32 -> f32, groups of 32
+  moe_65536x256_bf16     65536 x 256, bf16 -> f32, groups of 32
+  moe_1048576x256_f32    1048576 x 256, f32 -> f32, groups of 32
+
+  256 routed experts in 8 groups of 32 is the routing shape the paper's
+  operator serves; 65536 tokens is a large prefill batch, 1048576 tokens a
+  bandwidth-scale batch.  Scores: N(0, 1) in fp32 from a generator seeded 4,
+  cast to the input dtype; in bf16 about one group in a hundred holds a
+  tied maximum, the case the paper's rewrite must keep.
+
 Recipe: draw fp32 N(0, 1) with torch.randn from a torch.Generator seeded as
 stated on the chosen device, scale by sigma, apply the structure, then cast
 to the input dtype (round to nearest even for bf16).  The GPU and the oracle
@@ -123,6 +136,43 @@ BACKWARD_WORKLOADS = {w.name: w for w in (
     BackwardWorkload("bwd_causal_32768x4096", 32768, 4096, BF16, BF16, 0.1, period=4096),
     BackwardWorkload("bwd_large_1024x262144", 1024, 262144, F32, F32, 0.05),
 )}
+
+
+@dataclass(frozen=True)
+class MoeWorkload:
+    name: str
+    tokens: int
+    experts: int
+    group: int
+    in_dtype: str
+    out_dtype: str
+
+    @property
+    def in_bytes(self) -> int:
+        return 4 if self.in_dtype == F32 else 2
+
+    @property
+    def out_bytes(self) -> int:
+        return 4 if self.out_dtype == F32 else 2
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """Scores read once plus group scores written once."""
+        return self.tokens * self.experts * self.in_bytes + \
+            self.tokens * (self.experts // self.group) * self.out_bytes
+
+
+MOE_WORKLOADS = {w.name: w for w in (
+    MoeWorkload("moe_65536x256_f32", 65536, 256, 32, F32, F32),
+    MoeWorkload("moe_65536x256_bf16", 65536, 256, 32, BF16, F32),
+    MoeWorkload("moe_1048576x256_f32", 1048576, 256, 32, F32, F32),
+)}
+
+
+def make_moe_scores(w: MoeWorkload, device="cpu", tokens: int | None = None) -> torch.Tensor:
+    """Expert scores of a MoE workload on ``device`` in its input dtype."""
+    return random_matrix(w.tokens if tokens is None else tokens, w.experts, w.in_dtype,
+                         sigma=1.0, seed=4, device=device)
 
 
 def _gen(seed: int, device) -> torch.Generator:

@@ -25,7 +25,7 @@ def lib():
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(rowsm_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(rowsm_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -221,3 +221,32 @@ def test_backward_plans(lib):
     assert d(4, 100, R.F32, R.F32, variant=R.MEDIUM, waves_per_row=16)[0] == R.OK
     assert d(4, 8, 9, R.F32)[0] == R.EDTYPE
     assert R.rowsm_describe_op(9, 4, 8, R.F32, R.F32)[0] == R.EINVAL
+
+
+def test_moe_argument_errors_and_plans(lib):
+    f = R.rowsm_moe_group_top2
+    O = 0x7f4000000000
+    assert f(X, O, 4, 64, 32, 7, R.F32, 0) == R.EDTYPE
+    assert f(X, O, 4, 64, 32, R.F32, 3, 0) == R.EDTYPE
+    for g in (0, 1, 3, 24, 128):
+        assert f(X, O, 4, 64 * 3, g, R.F32, R.F32, 0) == R.EINVAL, g
+    assert f(X, O, 4, 60, 32, R.F32, R.F32, 0) == R.EINVAL          # 32 does not divide 60
+    assert f(X, O, -1, 64, 32, R.F32, R.F32, 0) == R.EINVAL
+    assert f(0, O, 4, 64, 32, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, 0, 4, 64, 32, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, X + 256, 4, 64, 32, R.F32, R.F32, 0) == R.EINVAL    # output inside scores
+    assert f(X, O + 2, 4, 64, 32, R.F32, R.F32, 0) == R.EINVAL      # misaligned f32 output
+    assert f(X + 2, O, 4, 64, 32, R.F32, R.F32, 0) == R.EINVAL      # misaligned f32 scores
+    assert f(0, 0, 0, 64, 32, R.F32, R.F32, 0) == R.OK              # empty: no launch
+    assert f(X, O, 4, 64, 32, R.F32, R.F32, 0, R.RowsmConfig(variant=R.MEDIUM)) == R.EINVAL
+    assert f(X, O, 4, 64, 32, R.F32, R.F32, 0, R.RowsmConfig(vw=8)) == R.EINVAL  # 32-byte vector
+    d = lambda groups, g, i, **cfg: R.rowsm_describe_op(
+        R.OP_MOE_GROUP_TOP2, groups, g, i, R.F32, R.RowsmConfig(**cfg) if cfg else None)
+    st, t = d(1048576 * 8, 32, R.F32)
+    assert st == R.OK and "vw=4" in t and "lpr=8" in t and "rpl=4" in t and "grid=65536" in t
+    st, t = d(65536 * 8, 32, R.BF16)
+    assert st == R.OK and "vw=8" in t and "lpr=4" in t
+    st, t = d(1000, 2, R.F32)
+    assert st == R.OK and "vw=2" in t and "lpr=1" in t
+    st, t = d(100000 * 8, 32, R.F32, blocks_per_cu=1)
+    assert st == R.OK and "grid=256" in t

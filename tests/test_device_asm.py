@@ -84,6 +84,8 @@ def test_no_immediate_overwrite_of_store_data(asm):
     r"bwd_medium_kernelINS_4BF16ES1_Li8ELi2EEE",           # bwd_causal_32768x4096
     r"bwd_split_kernelINS_3F32ES1_Li4ELi8EEE",             # bwd_large_1024x262144
     r"bwd_large_kernelINS_3F32ES1_Li4ELi4EEE",             # backward two-pass form
+    r"group_top2_kernelINS_3F32ES1_Li4ELi8ELi4EEE",        # moe_*x256_f32, groups of 32
+    r"group_top2_kernelINS_4BF16ENS_3F32ELi8ELi4ELi4EEE",  # moe_65536x256_bf16
 ])
 def test_workload_kernels_do_not_spill(asm, pattern):
     ks = {k: v for k, v in kernels(asm).items() if re.search(pattern, k)}
@@ -108,7 +110,7 @@ def test_expected_instructions(asm):
     for ins in ("row_half_mirror", "row_mirror", "quad_perm:[1,0,3,2]",
                 "v_permlane16_swap_b32", "v_permlane32_swap_b32", "v_exp_f32",
                 "v_cvt_pk_bf16_f32", "buffer_load_dwordx4", "buffer_store_dwordx4",
-                "v_log_f32"):
+                "v_log_f32", "v_maximum3_f32", "v_minimum3_f32"):
         assert ins in asm, ins
     # no packed-fp32 arithmetic anywhere
     assert not re.search(r"v_pk_(add|mul|fma)_f32", asm)
