@@ -66,7 +66,15 @@ typedef enum {
  * small device workspace (single read), or, for rows too long for that,
  * streams the row through tiles twice (online max/sum pass, then normalize).
  * The single-read form's grid is sized to at most one full residency of the
- * device. */
+ * device.
+ *
+ * HIP graphs: every entry point may be called on a stream that is being
+ * captured.  The single-read LARGE form keeps per-launch state on the host
+ * (exchange tags), so under capture a LARGE plan uses the two-pass form
+ * instead (same results to the stated tolerances, one extra read of each
+ * input); a single-read form forced through cfg->split_blocks > 0 returns
+ * ROWSM_EINVAL there.  No entry point records a memset or an allocation
+ * into a capture. */
 typedef enum {
     ROWSM_AUTO = 0,
     ROWSM_SMALL = 1,
@@ -273,7 +281,9 @@ int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
  * the current device.  Waits for the last such launch to finish, then returns
  * how many exchange waits have given up since the workspace was created (0
  * when every row's blocks met; a non-zero count means some rows of some
- * launch are wrong), 0 when no such launch has run, or ROWSM_EHIP.
+ * launch are wrong), 0 when no such launch has run, or ROWSM_EHIP.  It
+ * synchronises with the device: not to be called while a stream capture is
+ * in progress.
  */
 int64_t rowsm_split_wait_failures(void);
 

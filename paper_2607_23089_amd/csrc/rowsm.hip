@@ -448,6 +448,37 @@ int launch(const Call& c, int in_dt, int out_dt) {
   }
 }
 
+// ---- stream capture -------------------------------------------------------------
+//
+// The single-read split form takes exchange tags from the host for every
+// launch; a captured graph would replay one launch's tags, and a replay could
+// then accept words left by the previous replay as its own.  While the launch
+// stream is being captured, long rows therefore take the two-pass form,
+// which keeps no state between launches.  A failed query counts as capture.
+bool stream_capturing(hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess) return true;
+  return cs != hipStreamCaptureStatusNone;
+}
+
+// Re-plan a split-form plan as the two-pass form under capture; a split form
+// forced by the caller is refused there.
+template <typename Replan>
+int avoid_split_under_capture(const rowsm_config* cfg, hipStream_t st, Plan* p, Replan replan) {
+  if (p->variant != ROWSM_LARGE || p->split <= 0 || !stream_capturing(st)) return ROWSM_OK;
+  if (cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
+  rowsm_config two_pass;
+  if (cfg) {
+    two_pass = *cfg;
+  } else {
+    std::memset(&two_pass, 0, sizeof(two_pass));
+    two_pass.packed = -1;
+  }
+  two_pass.variant = ROWSM_LARGE;
+  two_pass.split_blocks = -1;
+  return replan(&two_pass);
+}
+
 // ---- validation -------------------------------------------------------------
 
 // Host-only argument checks shared by every entry point.  *noop is set when
@@ -490,8 +521,14 @@ int backward_impl(const void* yp, const void* dyp, void* dxp, int64_t rows, int6
   if (st != ROWSM_OK || noop) return st;
   Call c;
   c.cus = cu_count();
-  st = plan_backward(rows, cols, in_dt, out_dt, (uintptr_t)yp | (uintptr_t)dyp, (uintptr_t)dxp,
-                     cfg, c.cus, &c.p);
+  const uintptr_t ia = (uintptr_t)yp | (uintptr_t)dyp;
+  st = plan_backward(rows, cols, in_dt, out_dt, ia, (uintptr_t)dxp, cfg, c.cus, &c.p);
+  if (st != ROWSM_OK) return st;
+  st = avoid_split_under_capture(cfg, static_cast<hipStream_t>(stream), &c.p,
+                                 [&](const rowsm_config* tp) {
+                                   return plan_backward(rows, cols, in_dt, out_dt, ia,
+                                                        (uintptr_t)dxp, tp, c.cus, &c.p);
+                                 });
   if (st != ROWSM_OK) return st;
   c.x = yp;
   c.dy = dyp;
@@ -557,6 +594,12 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   Call c;
   c.cus = cu_count();
   st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus, mode, &c.p);
+  if (st != ROWSM_OK) return st;
+  st = avoid_split_under_capture(cfg, static_cast<hipStream_t>(stream), &c.p,
+                                 [&](const rowsm_config* tp) {
+                                   return plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x,
+                                                   (uintptr_t)y, tp, c.cus, mode, &c.p);
+                                 });
   if (st != ROWSM_OK) return st;
   c.x = x;
   c.y = y;

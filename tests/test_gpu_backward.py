@@ -213,3 +213,38 @@ def test_bwd_workload_full_size(name):
     assert R.rowsm_split_wait_failures() == 0
     del y, dy, dx
     torch.cuda.empty_cache()
+
+
+def test_bwd_and_forward_split_launches_interleaved_on_streams():
+    # Forward and backward single-read launches share the device's exchange
+    # workspace; interleaved on two streams they must be ordered and exact,
+    # and repeats on the same data bitwise equal.
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    cases = [inputs(9, 70000 + 64 * i, "f32", seed=i) for i in range(3)]
+    xs = [W.random_matrix(11, 90000 + 8 * i, "bf16", sigma=3.0, seed=i).to(DEV) for i in range(3)]
+    dev_cases = [(y.to(DEV), dy.to(DEV)) for y, dy in cases]
+    outs = []
+    for it in range(12):
+        s = s1 if it % 2 == 0 else s2
+        k = it % 3
+        with torch.cuda.stream(s):
+            if (it // 3) % 2 == 0:
+                yd, dyd = dev_cases[k]
+                outs.append(("bwd", k, R.softmax_backward(yd, dyd, stream=s,
+                                                          config=R.RowsmConfig(variant=R.LARGE))))
+            else:
+                outs.append(("fwd", k, R.softmax(xs[k], out_dtype=torch.float32, variant=R.LARGE,
+                                                 stream=s)))
+    torch.cuda.synchronize()
+    first = {}
+    for kind, k, o in outs:
+        if (kind, k) not in first:
+            first[(kind, k)] = o
+            if kind == "bwd":
+                assert_bwd_parity(cases[k][0], cases[k][1], o, "f32", f"interleaved bwd {k}")
+            else:
+                from test_gpu_parity import assert_parity
+                assert_parity(xs[k].cpu(), o, "f32", f"interleaved fwd {k}")
+        else:
+            assert torch.equal(o, first[(kind, k)])
+    assert R.rowsm_split_wait_failures() == 0
