@@ -63,6 +63,38 @@ def measured_traffic(regime: str, launch: str):
     return ent.get("hbm_bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def copy_ceiling(reps: int = 10):
+    """Same-run context: torch's device copy (the runtime's copy kernel) and
+    fill of 1 GiB, timed like the next-row legs."""
+    import torch
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    a = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    copy_us = timed_alone(lambda: b.copy_(a), reps, flush, stream)
+    fill_us = timed_alone(lambda: b.zero_(), reps, flush, stream)
+    nbytes = a.numel() * 4
+    props = torch.cuda.get_device_properties(dev)
+    return {"torch_copy_1GiB_GBps": 2 * nbytes / (copy_us * 1e3),
+            "torch_fill_1GiB_GBps": nbytes / (fill_us * 1e3),
+            "measured_read_GBps_probe": MEASURED_READ_GBS,
+            "measured_write_GBps_probe": MEASURED_WRITE_GBS,
+            "device": props.name, "gcn_arch": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count}
+
+
 def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
     """Time the fp64 oracle on the host cores over every row of the step (row
     chunks bounded in memory), repeating passes until ``min_seconds`` of
@@ -107,6 +139,13 @@ def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
                     p["max_abs"] = max(p["max_abs"], res["max_abs"])
                     p["max_tol_ratio"] = max(p["max_tol_ratio"], res["max_tol_ratio"])
         passes += 1
+    # one thread on one chunk of the longest-row regime, for scale
+    name = max(regimes, key=lambda n: W.WORKLOADS[n].cols)
+    v1 = widened[(name, 0)]
+    t = time.perf_counter()
+    oracle.softmax_f64(v1, threads=1)
+    t1 = time.perf_counter() - t
+    w1 = W.WORKLOADS[name]
     return {
         "value": tot_bytes / tot_time / 1e9,
         "unit": "GB/s",
@@ -115,6 +154,9 @@ def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
         "sample": (f"every row of the step ({', '.join(regimes)}), {passes} pass(es), "
                    f"{tot_time:.1f} s of oracle time; widening and copies not timed"),
         "seconds": tot_time,
+        "single_thread_GBps": v1.size * (w1.in_bytes + w1.out_bytes) / t1 / 1e9,
+        "single_thread_sample": f"{v1.shape[0]} rows of {name}",
+        "cpu_model": cpu_model(),
         "parity_on_sample": parity,
     }
 
@@ -379,7 +421,8 @@ def main() -> int:
             "kernel": desc.split(" ")[0], "launch": desc,
             "algorithmic_bytes": w.algorithmic_bytes,
             "avg_us": avg * 1e3, "median_us": ms[len(ms) // 2] * 1e3,
-            "min_us": ms[0] * 1e3,
+            "min_us": ms[0] * 1e3, "p10_us": ms[len(ms) // 10] * 1e3,
+            "p90_us": ms[(9 * len(ms)) // 10] * 1e3,
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
             "hbm_bytes_per_launch": measured_traffic(name, desc),
         }
@@ -427,6 +470,7 @@ def main() -> int:
         "regimes_detail": per,
     }
     if not args.no_next:
+        result["context"] = copy_ceiling()
         result["next_rows"] = {"fused_scale_causal": fused_causal_leg(reps=10),
                                "log_softmax": log_softmax_leg(reps=10),
                                "softmax_backward": backward_leg(reps=10),

@@ -22,8 +22,10 @@
 // and RPL such load groups per task, so every lane has RPL independent loads
 // in flight before the first reduction.  The pair is reduced across the LPG
 // lanes with DPP and permlane steps.  Scores past the last group load nothing
-// and hold -inf.  Stores: for load group k, the lanes with sub-index k mod LPG
-// write the 64 / LPG consecutive scores of that load group.
+// and hold -inf.  Stores: the task's GPT results are gathered with
+// ds_bpermute so that lane q holds the result of the task's group q, and each
+// store instruction writes 64 consecutive results (one instruction per task
+// when GPT <= 64): whole cache lines instead of one short run per load group.
 #pragma once
 
 #include "rowsm_device.hpp"
@@ -119,11 +121,31 @@ __global__ __launch_bounds__(256) void group_top2_kernel(
     }
 #pragma unroll
     for (int k = 0; k < RPL; ++k) p[k] = group_top2_reduce<LPG>(p[k]);
+    float r[RPL];
 #pragma unroll
-    for (int k = 0; k < RPL; ++k) {
-      if ((k % LPG) == sub && k * GPW + grp < n) {
-        const float r[1] = {p[k].t1 + p[k].t2};
-        store_out<Out, 1>(ro, (uint32_t)(k * GPW + grp) * Out::bytes, r);
+    for (int k = 0; k < RPL; ++k) r[k] = p[k].t1 + p[k].t2;
+    // Group q of the task is load group q / GPW, held by lanes
+    // (q % GPW) * LPG ... + LPG - 1 after the all-reduce.
+    constexpr int NSTORE = (GPT + kWave - 1) / kWave;
+#pragma unroll
+    for (int j = 0; j < NSTORE; ++j) {
+      const int q = j * kWave + lane;
+      float val;
+      if constexpr (LPG == 1) {
+        val = r[j];  // GPW == 64: lane q already holds group q of load group j
+      } else {
+        const int src = (q % GPW) * LPG;
+        const int kq = q / GPW;
+        val = 0.0f;
+#pragma unroll
+        for (int k = 0; k < RPL; ++k) {
+          const float b = __int_as_float(__builtin_amdgcn_ds_bpermute(src * 4, __float_as_int(r[k])));
+          if (kq == k) val = b;
+        }
+      }
+      if (q < n) {
+        const float o1[1] = {val};
+        store_out<Out, 1>(ro, (uint32_t)q * Out::bytes, o1);
       }
     }
   }
