@@ -33,32 +33,47 @@ sys.path.insert(0, ROOT)
 METRIC = "row-softmax achieved HBM GB/s and % of MI355X peak, per row-length regime"
 PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-# Device code of the kernels; a profile also records each launch's shape.
-KERNEL_SOURCES = ["rowsm_device.hpp", "small_row.hpp", "medium_row.hpp", "large_row.hpp",
-                  "split_row.hpp", "backward_row.hpp", "group_top2.hpp"]
+# Device code each kernel family is compiled from; a profile entry records the
+# hash of its family's sources and the launch's shape.
+KERNEL_SOURCES = {
+    "small_row": ["rowsm_device.hpp", "small_row.hpp"],
+    "medium_row": ["rowsm_device.hpp", "medium_row.hpp"],
+    "split_row": ["rowsm_device.hpp", "split_row.hpp"],
+    "large_row": ["rowsm_device.hpp", "large_row.hpp"],
+    "bwd": ["rowsm_device.hpp", "medium_row.hpp", "split_row.hpp", "backward_row.hpp"],
+    "group_top2": ["rowsm_device.hpp", "group_top2.hpp"],
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_family(kernel: str) -> str:
+    """Family of a kernel name (e.g. 'split_row_kernel<...>' -> 'split_row')."""
+    if kernel.startswith("bwd_"):
+        return "bwd"
+    return kernel.split("_kernel")[0]
+
+
+def kernel_source_hash(family: str) -> str:
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[family]:
         with open(os.path.join(ROOT, "paper_2607_23089_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(regime: str, launch: str):
+def measured_traffic(key: str, launch: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when there is none, or the kernels' device code or this launch's
-    shape changed since it was taken."""
+    None when there is none, or the device code of that launch's kernel
+    family or the launch's shape changed since it was taken."""
     try:
         with open(PROFILE_COUNTERS) as f:
             prof = json.load(f)
     except (OSError, ValueError):
         return None
-    if prof.get("kernel_source_hash") != kernel_source_hash():
-        return None
-    ent = prof.get("regimes", {}).get(regime)
+    ent = prof.get("launches", {}).get(key)
     if ent is None or ent.get("launch") != launch:
+        return None
+    fam = kernel_family(ent.get("kernel", ""))
+    if fam not in KERNEL_SOURCES or ent.get("source_hash") != kernel_source_hash(fam):
         return None
     return ent.get("hbm_bytes_per_launch")
 
