@@ -13,7 +13,10 @@
 //   large   two streaming passes (dot, then dx) for rows longer than that.
 // The register-resident forms keep y and dy in their raw input form (bf16
 // pairs take half the registers) and widen each element where it is used,
-// so one read of each input suffices.  Lanes past the end of a row hold
+// so one read of each input suffices.  The raw words are hidden from the
+// optimiser between the dot product and the gradient (InVec::opaque()):
+// otherwise it keeps the widened fp32 copies of the first phase alive for the
+// second, twice the registers, and the widest bf16 forms spilled.  Lanes past the end of a row hold
 // zeros, which add nothing to d.
 //
 // d is accumulated with fma in fp32: a lane's vectors in slot order, then
@@ -90,6 +93,11 @@ __global__ __launch_bounds__(256) void bwd_small_kernel(
 #pragma unroll
     for (int k = 0; k < RPL; ++k) d[k] = dot_vec(a[k], b[k], 0.0f);
 #pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+      a[k].opaque();
+      b[k].opaque();
+    }
+#pragma unroll
     for (int k = 0; k < RPL; ++k) d[k] = group_reduce<LPR, SumOp>(d[k]);
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
@@ -150,6 +158,11 @@ __global__ __launch_bounds__(1024) void bwd_medium_kernel(
     float d = 0.0f;
 #pragma unroll
     for (int s = 0; s < NV; ++s) d = dot_vec(a[s], b[s], d);
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      a[s].opaque();
+      b[s].opaque();
+    }
     d = block_row_reduce<SumOp>(d, wpr, wave, g, lane, red[parity]);
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
@@ -216,6 +229,11 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
     float d = 0.0f;
 #pragma unroll
     for (int s = 0; s < NV; ++s) d = dot_vec(a[s], b[s], d);
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      a[s].opaque();
+      b[s].opaque();
+    }
     d = group_reduce<kWave, SumOp>(d);
     if (lane == 0) red[wave] = d;
     __syncthreads();

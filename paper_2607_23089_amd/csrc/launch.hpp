@@ -49,8 +49,10 @@ struct Call {
 };
 
 // Calls L<In, Out, VW, MODE>::run(c) for the call's dtype pair and vector
-// width (16-byte, 8-byte or single-element vectors).  Returns a rowsm_status:
-// ROWSM_EINVAL when nothing matches (nothing enqueued).
+// width (16-byte, 8-byte or single-element input vectors).  Widths whose
+// output vector would exceed 16 bytes are never planned (the width rule of
+// choose_vw) and are not compiled.  Returns a rowsm_status: ROWSM_EINVAL when
+// nothing matches (nothing enqueued).
 template <template <typename, typename, int, int> class L, int MODE>
 int dispatch(const Call& c, int in_dt, int out_dt) {
   auto io = [&](auto in_tag, auto out_tag) -> int {
@@ -58,8 +60,12 @@ int dispatch(const Call& c, int in_dt, int out_dt) {
     using Out = decltype(out_tag);
     constexpr int V16 = 16 / In::bytes, V8 = 8 / In::bytes;
     if (c.p.vw == 1) return L<In, Out, 1, MODE>::run(c);
-    if (c.p.vw == V8) return L<In, Out, V8, MODE>::run(c);
-    if (c.p.vw == V16) return L<In, Out, V16, MODE>::run(c);
+    if (c.p.vw == V8) {
+      if constexpr (V8 * Out::bytes <= 16) return L<In, Out, V8, MODE>::run(c);
+    }
+    if (c.p.vw == V16) {
+      if constexpr (V16 * Out::bytes <= 16) return L<In, Out, V16, MODE>::run(c);
+    }
     return ROWSM_EINVAL;
   };
   if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32) return io(F32{}, F32{});

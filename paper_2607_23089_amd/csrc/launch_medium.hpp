@@ -13,10 +13,12 @@ namespace rowsm {
 
 template <typename In, typename Out, int VW, int NV, bool PACKED, int MODE>
 bool try_medium(const Call& c, int* status) {
+  // Slot counts the planner can choose: fused rows hold at most 32 values
+  // per lane (the column indices are live too), the others 64.
   constexpr bool compiled =
       PACKED ? (MODE != kFused && std::is_same<In, BF16>::value && VW == 8 && NV >= 9 &&
                 NV <= 24)
-             : (NV * VW <= 64 && NV <= 16);
+             : (NV * VW <= (MODE == kFused ? 32 : 64) && NV <= 16);
   if constexpr (compiled) {
     if (c.p.nv == NV && c.p.packed == PACKED) {
       medium_row_kernel<In, Out, VW, NV, PACKED, MODE>

@@ -12,6 +12,10 @@
 //   LARGE   anything longer: the row split over S <= 64 co-resident blocks
 //           that each hold their share in registers (single read), or, for
 //           rows too long even for that, two streaming passes over tiles.
+// Row count: a launch of few rows must still fill the device, so fewer than
+// cus/4 rows of >= 384 KiB each (at most cus/4 rows for the packed form) take
+// the split form rather than one block per row, and the split form gives
+// each of fewer than cus rows up to cus/rows blocks (few_rows_split()).
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -99,6 +103,40 @@ bool config_in_domain(const rowsm_config* c) {
 
 // mode is the output form (kPlain, kFused or kLog).  The log form holds x
 // where softmax holds exp(x - m), so it takes the plain form's plans.
+// Row-count rules, from a sweep of 1-128 rows x 4096-262144 columns in every
+// dtype pair (cold caches): below ~384 KiB of traffic per row every form sits
+// at the launch floor; above it, a block per row on fewer than a quarter of
+// the compute units loses up to 17% to the split form (the packed bf16 form
+// up to 1.8x, still 1.4x at a quarter), and the split form is fastest with
+// about one block per compute unit over the launch.
+// The backward moves three streams per element and gains from splitting from
+// 512 KiB of traffic per row on.
+constexpr int64_t kFewRowsMinBytes = 384 * 1024;
+constexpr int64_t kFewRowsMinBytesBackward = 512 * 1024;
+bool few_long_rows(int64_t rows, int64_t row_bytes, bool packed, int cus,
+                   int64_t min_bytes = kFewRowsMinBytes) {
+  return row_bytes >= min_bytes && (packed ? rows <= cus / 4 : rows < cus / 4);
+}
+
+// Blocks per row for a split launch of fewer than cus rows with T-thread
+// blocks holding at most nv_cap vectors per thread: about one block per
+// compute unit over the launch (the largest power of two with rows * S <=
+// cus), at least 8, and at most what gives every thread two vectors (smaller
+// blocks measured slower); raised to the power of two that the register cap
+// needs.  0 when rows >= cus, or when the result exceeds 64 blocks per row or
+// 4 blocks per compute unit over the launch (a register-limited plan with
+// fewer, larger blocks then measured faster).
+int few_rows_split(int64_t rows, int64_t nvec, int T, int nv_cap, int cus) {
+  if (rows >= cus) return 0;
+  int sf = 1;
+  while (sf < 64 && rows * (sf * 2) <= cus) sf *= 2;
+  if (sf < 8) sf = 8;
+  while (sf > 1 && (int64_t)sf * T * 2 > nvec) sf >>= 1;
+  while ((int64_t)sf * T * nv_cap < nvec) sf *= 2;  // register cap
+  if (sf > 64 || rows * sf > 4 * (int64_t)cus) return 0;
+  return sf;
+}
+
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
              const rowsm_config* cfg, int cus, int mode, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
@@ -121,10 +159,12 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   if (variant == ROWSM_AUTO) {
     if (nvec <= 32) {
       variant = ROWSM_SMALL;
-    } else if (nvec <= 16 * kWave * ((fused ? 32 : 64) / vw < 16 ? (fused ? 32 : 64) / vw : 16) ||
-               (!fused && in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24)) {
-      // whole row in the registers of one block
-      variant = ROWSM_MEDIUM;
+    } else if (nvec <= 16 * kWave * ((fused ? 32 : 64) / vw < 16 ? (fused ? 32 : 64) / vw : 16)) {
+      // whole row in the registers of one block, unless few long rows would
+      // then leave most of the device idle
+      variant = few_long_rows(rows, cols * (ib + ob), false, cus) ? ROWSM_LARGE : ROWSM_MEDIUM;
+    } else if (!fused && in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24) {
+      variant = few_long_rows(rows, cols * (ib + ob), true, cus) ? ROWSM_LARGE : ROWSM_MEDIUM;
     } else {
       variant = ROWSM_LARGE;
     }
@@ -231,21 +271,34 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       // compute unit; the others with 256-thread blocks and 64 values per
       // lane (measured on the 4096 x 151936 and 1024 x 262144 workloads).
       const bool widening = ob > ib;
-      const int T = (cfg && cfg->block > 0) ? cfg->block : (widening ? 512 : 256);
+      const bool forced_block = cfg && cfg->block > 0;
+      int T = forced_block ? cfg->block : (widening ? 512 : 256);
       const int vals = fused ? 32 : (widening ? 40 : 64);
       int nv_cap = vals / vw < 16 ? vals / vw : 16;
       if (nv_cap < 1) nv_cap = 1;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
       if (S < 1) S = 1;
+      // Grid sized at launch from occupancy (one full residency of the
+      // device at most); a negative value caps blocks per compute unit.
+      int64_t grid = bpc ? -(int64_t)bpc : (widening && !forced_block ? -2 : 0);
+      if (want_split == 0) {
+        // Few rows: more, smaller blocks per row so that the launch fills
+        // the device (256-thread blocks unless a block size is given).
+        const int Tf = forced_block ? T : 256;
+        const int sf = few_rows_split(rows, nvec, Tf, nv_cap, cus);
+        if (sf > 0 && (int64_t)sf * Tf > (int64_t)S * T) {
+          S = sf;
+          T = Tf;
+          grid = bpc ? -(int64_t)bpc : 0;
+        }
+      }
       const int nv = (int)cdiv(nvec, (int64_t)S * T);
       if (S <= 64 && nv <= nv_cap && nv * vw <= 64) {
         p->split = S;
         p->nv = nv;
         p->vpl = nv;
         p->block = T;
-        // Grid sized at launch from occupancy (one full residency of the
-        // device at most); a negative value caps blocks per compute unit.
-        p->grid = bpc ? -(int64_t)bpc : (widening && !(cfg && cfg->block > 0) ? -2 : 0);
+        p->grid = grid;
         return ROWSM_OK;
       }
       if (want_split > 0) return ROWSM_EINVAL;
@@ -270,9 +323,11 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
 // share of each input is at most 128 bytes (and 16 slots).
 //   SMALL   a row is at most 32 vectors;
 //   MEDIUM  the smallest row group of <= 16 waves whose lanes hold at most 32
-//           bytes of each input (then 64, then 128);
-//   LARGE   the row split over S <= 64 co-resident 256-thread blocks, or two
-//           streaming passes for rows longer than that.
+//           bytes of each input (then 64, then 128), unless the rows are few
+//           and long (the forward's row-count rule, on the backward's bytes);
+//   LARGE   the row split over S <= 64 co-resident 256-thread blocks (more
+//           blocks per row for few rows, as the forward), or two streaming
+//           passes for rows longer than that.
 int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t ia,
                   uintptr_t dxa, const rowsm_config* cfg, int cus, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
@@ -293,9 +348,15 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
   p->nvec = nvec;
 
   int variant = cfg ? cfg->variant : ROWSM_AUTO;
-  if (variant == ROWSM_AUTO)
-    variant = nvec <= 32 ? ROWSM_SMALL
-                         : (nvec <= 16 * kWave * nv_cap ? ROWSM_MEDIUM : ROWSM_LARGE);
+  if (variant == ROWSM_AUTO) {
+    if (nvec <= 32)
+      variant = ROWSM_SMALL;
+    else if (nvec <= 16 * kWave * nv_cap &&
+             !few_long_rows(rows, cols * (2 * ib + ob), false, cus, kFewRowsMinBytesBackward))
+      variant = ROWSM_MEDIUM;
+    else
+      variant = ROWSM_LARGE;
+  }
   p->variant = variant;
   const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
 
@@ -350,6 +411,10 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       const int T = (cfg && cfg->block > 0) ? cfg->block : 256;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
       if (S < 1) S = 1;
+      if (want_split == 0) {  // few rows: fill the device (as the forward plan)
+        const int sf = few_rows_split(rows, nvec, T, nv_cap, cus);
+        if (sf > S) S = sf;
+      }
       const int nv = (int)cdiv(nvec, (int64_t)S * T);
       if (S <= 64 && nv <= nv_cap) {
         p->split = S;

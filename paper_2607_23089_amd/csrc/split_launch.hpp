@@ -55,11 +55,18 @@ int launch_split_nv(const Call& c) {
   return launched ? r : ROWSM_EHIP;
 }
 
+// Values per lane the planner can choose: 32 for fused rows, 64 otherwise.
+template <int MODE>
+constexpr int split_max_values() {
+  return MODE == kFused ? 32 : 64;
+}
+
 template <typename In, typename Out, int VW, int MODE, int... NVs>
 int split_nv(const Call& c, std::integer_sequence<int, NVs...>) {
+  constexpr int MAXV = split_max_values<MODE>();
   int r = ROWSM_EINVAL;
-  (void)((c.p.nv == NVs + 1 && (NVs + 1) * VW <= 64
-              ? (r = launch_split_nv<In, Out, VW, ((NVs + 1) * VW <= 64 ? NVs + 1 : 1), MODE>(c),
+  (void)((c.p.nv == NVs + 1 && (NVs + 1) * VW <= MAXV
+              ? (r = launch_split_nv<In, Out, VW, ((NVs + 1) * VW <= MAXV ? NVs + 1 : 1), MODE>(c),
                  true)
               : false) ||
          ...);

@@ -123,15 +123,22 @@ def test_select_regimes(lib):
     # medium: up to 16 waves x 64 lanes x 64 fp32 values
     assert s(64, 1000, R.F32, R.F32) == R.MEDIUM
     assert s(32768, 4096, R.BF16, R.BF16) == R.MEDIUM
-    assert s(10, 65536, R.F32, R.F32) == R.MEDIUM
-    assert s(10, 65540, R.F32, R.F32) == R.LARGE
-    assert s(10, 65536, R.BF16, R.BF16) == R.MEDIUM
+    assert s(100, 65536, R.F32, R.F32) == R.MEDIUM
+    assert s(100, 65540, R.F32, R.F32) == R.LARGE
+    assert s(10, 65536, R.BF16, R.BF16) == R.MEDIUM      # 256 KiB rows: launch bound
     # packed bf16 rows up to 16 x 64 x 24 vectors of 8 (bf16 -> bf16 only:
     # bf16 -> f32 uses 4-element vectors so that each store is 16 bytes)
-    assert s(10, 151936, R.BF16, R.BF16) == R.MEDIUM
+    assert s(100, 151936, R.BF16, R.BF16) == R.MEDIUM
     assert s(4096, 151936, R.BF16, R.F32) == R.LARGE
-    assert s(10, 196608, R.BF16, R.BF16) == R.MEDIUM
-    assert s(10, 196616, R.BF16, R.BF16) == R.LARGE
+    assert s(100, 196608, R.BF16, R.BF16) == R.MEDIUM
+    assert s(100, 196616, R.BF16, R.BF16) == R.LARGE
+    # few long rows (>= 384 KiB of traffic): the split form fills the device
+    # (the select assumes 256 compute units)
+    assert s(63, 65536, R.F32, R.F32) == R.LARGE
+    assert s(64, 65536, R.F32, R.F32) == R.MEDIUM
+    assert s(64, 151936, R.BF16, R.BF16) == R.LARGE       # packed form: <= cus / 4
+    assert s(65, 151936, R.BF16, R.BF16) == R.MEDIUM
+    assert s(8, 32768, R.F32, R.F32) == R.MEDIUM          # 256 KiB rows
     assert s(1024, 262144, R.F32, R.F32) == R.LARGE
     assert s(0, 5, R.F32, R.F32) > 0
     assert s(5, 5, 3, R.F32) == R.EDTYPE
@@ -143,7 +150,7 @@ def test_describe(lib):
     assert st == R.OK and text.startswith("small") and "lpr=8" in text and "vw=8" in text
     st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("medium")
-    st, text = R.rowsm_describe(64, 151936, R.BF16, R.BF16)
+    st, text = R.rowsm_describe(128, 151936, R.BF16, R.BF16)
     assert st == R.OK and "packed=1" in text and "vpl=19" in text and "wpr=16" in text
     st, text = R.rowsm_describe(4096, 151936, R.BF16, R.F32)
     assert st == R.OK and text.startswith("large") and "vw=4" in text and "split=8" in text
@@ -210,9 +217,16 @@ def test_backward_plans(lib):
     st, t = d(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and t.startswith("medium") and "wpr=4" in t and "nv=2" in t
     # medium holds at most 128 bytes of each input per lane: 16 x 64 x 8 vectors
-    assert d(4, 65536, R.BF16, R.BF16)[1].startswith("medium")
-    assert d(4, 65544, R.BF16, R.BF16)[1].startswith("large")
-    assert d(4, 32768, R.F32, R.F32)[1].startswith("medium")
+    assert d(100, 65536, R.BF16, R.BF16)[1].startswith("medium")
+    assert d(100, 65544, R.BF16, R.BF16)[1].startswith("large")
+    assert d(100, 32768, R.F32, R.F32)[1].startswith("medium")
+    # few long rows (>= 512 KiB of y, dy and dx per row): the split form,
+    # about one block per compute unit
+    st, t = d(8, 65536, R.F32, R.F32)
+    assert st == R.OK and t.startswith("large") and "split=32" in t
+    assert d(4, 65536, R.BF16, R.BF16)[1].startswith("medium")    # 384 KiB rows
+    st, t = d(32, 151936, R.BF16, R.BF16)                          # register cap: 16
+    assert st == R.OK and "split=16" in t and "nv=5" in t
     st, t = d(1024, 262144, R.F32, R.F32)
     assert st == R.OK and "split=32" in t and "nv=8" in t and "block=256" in t
     # past 64 blocks x 256 threads x 8 vectors: the two-pass form
@@ -250,3 +264,24 @@ def test_moe_argument_errors_and_plans(lib):
     assert st == R.OK and "vw=2" in t and "lpr=1" in t
     st, t = d(100000 * 8, 32, R.F32, blocks_per_cu=1)
     assert st == R.OK and "grid=256" in t
+
+
+def test_few_rows_split_counts(lib):
+    # about one block per compute unit, at least 8 and at most 64 blocks per
+    # row, at least two vectors per thread; never below the register minimum
+    d = lambda rows, cols, i, o: R.rowsm_describe(rows, cols, i, o)[1]
+    assert "split=32" in d(1, 65536, R.F32, R.F32) and "block=256" in d(1, 65536, R.F32, R.F32)
+    assert "split=16" in d(16, 65536, R.F32, R.F32)
+    assert "split=8" in d(32, 65536, R.F32, R.F32) and "split=8" in d(63, 65536, R.F32, R.F32)
+    assert "split=64" in d(1, 262144, R.F32, R.F32)
+    assert "split=32" in d(8, 262144, R.F32, R.F32)
+    assert "split=16" in d(1024, 262144, R.F32, R.F32)              # many rows: registers
+    assert "split=32" in d(8, 151936, R.BF16, R.F32) and "block=256" in d(8, 151936, R.BF16, R.F32)
+    t = d(4096, 151936, R.BF16, R.F32)
+    assert "split=8" in t and "block=512" in t                       # the vocab workload
+    t = d(16, 262144, R.BF16, R.F32)
+    assert "split=32" in t and "block=256" in t                      # raised to the register cap
+    t = d(48, 262144, R.BF16, R.F32)
+    assert "split=13" in t and "block=512" in t                      # 48 x 32 > 4 x 256 blocks
+    t = d(128, 151936, R.F32, R.F32)
+    assert "split=10" in t                                           # register plan

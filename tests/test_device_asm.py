@@ -8,8 +8,8 @@ scanned for properties the kernels rely on:
     inserts the wait states;
   * no store of more than 64 bits is followed directly by a VALU write of its
     data registers;
-  * the kernels the launcher picks for the benchmark workloads spill nothing
-    to scratch;
+  * no kernel spills to scratch (and the benchmark workloads' kernels are
+    checked by name);
   * the reductions use DPP and the gfx950 permlane swaps, the exponentials
     v_exp_f32, and bf16 outputs v_cvt_pk_bf16_f32.
 """
@@ -92,6 +92,15 @@ def test_workload_kernels_do_not_spill(asm, pattern):
     assert len(ks) == 1, pattern
     body = next(iter(ks.values()))
     assert int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", body).group(1)) == 0
+
+
+def test_no_kernel_spills(asm):
+    # every instantiation the launchers can choose keeps its data in registers
+    spills = {k: int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", v).group(1))
+              for k, v in kernels(asm).items()}
+    assert spills, "no kernels found"
+    bad = {k: v for k, v in spills.items() if v}
+    assert not bad, f"{len(bad)} kernels spill, e.g. {sorted(bad.items())[:3]}"
 
 
 def test_split_exchange_has_no_cache_maintenance(asm):
