@@ -248,3 +248,16 @@ def test_bwd_and_forward_split_launches_interleaved_on_streams():
         else:
             assert torch.equal(o, first[(kind, k)])
     assert R.rowsm_split_wait_failures() == 0
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("rows,cols", [(1, 65536), (8, 65536), (32, 151936), (3, 262144),
+                                       (16, 262144)])
+def test_bwd_few_rows_launcher_choice(rows, cols, din, dout):
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK
+    y, dy = inputs(rows, cols, din, alpha=0.2, seed=rows + cols)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
+    assert_bwd_parity(y, dy, dx, dout, f"bwd few rows {rows}x{cols} {din}->{dout} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0

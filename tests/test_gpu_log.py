@@ -159,3 +159,11 @@ def test_log_workload_full_size(name):
     assert R.rowsm_split_wait_failures() == 0
     del x, y
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("rows,cols", [(2, 65536), (24, 151936), (5, 262144)])
+def test_log_few_rows_launcher_choice(rows, cols, din, dout):
+    x = W.random_matrix(rows, cols, din, sigma=5.0, seed=rows + 7 * cols)
+    y = run_log(x.to(DEV), dout)
+    assert_log_parity(x, y, dout, f"log few rows {rows}x{cols} {din}->{dout}")

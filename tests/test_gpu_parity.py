@@ -227,3 +227,17 @@ def test_streams():
         y = R.softmax(x, stream=s)
     s.synchronize()
     assert_parity(x.cpu(), y, "f32", "side stream")
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("rows,cols", [(1, 65536), (5, 65536), (40, 65536), (1, 151936),
+                                       (17, 151936), (64, 151936), (3, 262144), (48, 262144)])
+def test_few_rows_launcher_choice(rows, cols, din, dout):
+    # few long rows: the launcher spreads each row over more blocks
+    # (the row-count rules); parity in the launch it picks by itself
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK
+    x = W.random_matrix(rows, cols, din, sigma=5.0, seed=rows * 13 + cols)
+    y = run(x.to(DEV), dout)
+    assert_parity(x, y, dout, f"few rows {rows}x{cols} {din}->{dout} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0
