@@ -81,8 +81,6 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
 
-// Fill p for the given family (AUTO resolves first) and config overrides.
-// Returns ROWSM_OK or ROWSM_EINVAL when the family cannot take this shape.
 bool pow2_upto(int v, int hi) { return v >= 1 && v <= hi && (v & (v - 1)) == 0; }
 
 // Every override must lie in its documented domain, whichever family or form
@@ -101,8 +99,6 @@ bool config_in_domain(const rowsm_config* c) {
          c->blocks_per_cu >= 0 && c->split_blocks >= -1 && c->split_blocks <= 64;
 }
 
-// mode is the output form (kPlain, kFused or kLog).  The log form holds x
-// where softmax holds exp(x - m), so it takes the plain form's plans.
 // Row-count rules, from a sweep of 1-128 rows x 4096-262144 columns in every
 // dtype pair (cold caches): below ~384 KiB of traffic per row every form sits
 // at the launch floor; above it, a block per row on fewer than a quarter of
@@ -137,6 +133,11 @@ int few_rows_split(int64_t rows, int64_t nvec, int T, int nv_cap, int cus) {
   return sf;
 }
 
+// Forward plan: fills p for the family cfg asks for (AUTO resolves first)
+// and the config overrides; returns ROWSM_OK, or ROWSM_EINVAL when the family
+// cannot take this shape.  mode is the output form (kPlain, kFused or kLog);
+// the log form holds x where softmax holds exp(x - m), so it takes the plain
+// plans.
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
              const rowsm_config* cfg, int cus, int mode, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
