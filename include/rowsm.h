@@ -146,6 +146,10 @@ typedef struct rowsm_config {
     int32_t split_blocks;   /* LARGE: blocks sharing one row in the single-read
                                form (1..64), 0 launcher's choice, -1 the
                                two-pass streaming form                            */
+    int32_t prefetch;       /* LARGE single-read form: 1 load a block's next row
+                               while the current one is exchanged and written
+                               (software pipelining), -1 never, 0 launcher's
+                               choice                                             */
 } rowsm_config;
 
 /*

@@ -54,7 +54,7 @@ class RowsmConfig(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "variant", "vw", "lanes_per_row", "rows_per_lane", "waves_per_row",
         "rows_per_block", "packed", "block", "tile_vectors", "blocks_per_cu",
-        "split_blocks")]
+        "split_blocks", "prefetch")]
 
     def __init__(self, **kw):
         super().__init__()

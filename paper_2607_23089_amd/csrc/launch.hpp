@@ -27,6 +27,7 @@ struct Plan {
   // LARGE
   int u = 4;
   int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
+  bool prefetch = false;  // single-read form: load the next row during the exchange
   // launch
   int block = 256;
   int64_t grid = 1;  // split form: 0 = occupancy, < 0 = minus the blocks-per-CU cap

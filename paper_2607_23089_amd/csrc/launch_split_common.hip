@@ -4,7 +4,9 @@
 // 2 MiB) is allocated and cleared on the first split launch on a device and
 // kept until the process ends.  Split launches on one device are ordered
 // through `last` (each waits for the previous one, whatever its stream), so
-// two launches never use the workspace at the same time.  Tags are handed
+// two launches never use the workspace at the same time.  `last` only orders
+// device work against device work, so it is recorded without a system-scope
+// fence (and without timing).  Tags are handed
 // out from `next_tag`: a launch whose blocks process at most n rows each uses
 // tags tag0 .. tag0 + n - 1, so a tag is never reused while the workspace may
 // still hold it; when the 32-bit tag space runs out the workspace is cleared
@@ -38,7 +40,8 @@ int split_workspace(SplitState& st, SplitWorkspace* ws) {
     void* p = nullptr;
     if (hipMalloc(&p, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
     if (split_clear(p) != ROWSM_OK ||
-        hipEventCreateWithFlags(&st.last, hipEventDisableTiming) != hipSuccess) {
+        hipEventCreateWithFlags(&st.last, hipEventDisableTiming | hipEventDisableSystemFence) !=
+            hipSuccess) {
       (void)hipFree(p);
       return ROWSM_EHIP;
     }

@@ -96,7 +96,8 @@ bool config_in_domain(const rowsm_config* c) {
          c->block >= 0 && c->block <= 1024 && c->block % kWave == 0 &&
          (c->tile_vectors == 0 || c->tile_vectors == 2 || c->tile_vectors == 4 ||
           c->tile_vectors == 8) &&
-         c->blocks_per_cu >= 0 && c->split_blocks >= -1 && c->split_blocks <= 64;
+         c->blocks_per_cu >= 0 && c->split_blocks >= -1 && c->split_blocks <= 64 &&
+         c->prefetch >= -1 && c->prefetch <= 1;
 }
 
 // Row-count rules, from a sweep of 1-128 rows x 4096-262144 columns in every
@@ -300,6 +301,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->vpl = nv;
         p->block = T;
         p->grid = grid;
+        p->prefetch = cfg && cfg->prefetch == 1;
+        // registers: at most 48 values per lane, plain and log forms only
+        // (split_launch.hpp)
+        if (p->prefetch && (fused || nv * vw > 48)) return ROWSM_EINVAL;
         return ROWSM_OK;
       }
       if (want_split > 0) return ROWSM_EINVAL;
@@ -788,9 +793,10 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
     } else {
       std::snprintf(buf, (size_t)len,
                     "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
-                    "split=%d block=%d grid=%lld (%s)",
+                    "split=%d prefetch=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
-                    (int)p.packed, p.u, p.split, p.block, (long long)(p.split ? 0 : p.grid),
+                    (int)p.packed, p.u, p.split, (int)p.prefetch, p.block,
+                    (long long)(p.split ? 0 : p.grid),
                     p.split ? "grid sized from occupancy at launch"
                             : "grid assumes 256 CUs");
     }

@@ -25,10 +25,10 @@ struct SplitTicket {
 int split_begin(hipStream_t st, uint64_t ntags, SplitTicket* t);
 int split_end(SplitTicket* t, hipStream_t st, bool launched);
 
-template <typename In, typename Out, int VW, int NV, int MODE>
+template <typename In, typename Out, int VW, int NV, int MODE, bool PIPE>
 int launch_split_nv(const Call& c) {
   const Plan& p = c.p;
-  auto kern = split_row_kernel<In, Out, VW, NV, MODE>;
+  auto kern = split_row_kernel<In, Out, VW, NV, MODE, PIPE>;
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
                                                    p.block, 0) != hipSuccess)
@@ -55,6 +55,10 @@ int launch_split_nv(const Call& c) {
   return launched ? r : ROWSM_EHIP;
 }
 
+// Values per lane the prefetching form holds at most: the next row's raw
+// share comes on top of the current one (more spilled on gfx950).
+constexpr int kSplitPrefetchMaxValues = 48;
+
 // Values per lane the planner can choose: 32 for fused rows, 64 otherwise.
 template <int MODE>
 constexpr int split_max_values() {
@@ -64,9 +68,19 @@ constexpr int split_max_values() {
 template <typename In, typename Out, int VW, int MODE, int... NVs>
 int split_nv(const Call& c, std::integer_sequence<int, NVs...>) {
   constexpr int MAXV = split_max_values<MODE>();
+  // prefetching: plain and log forms only (the fused form keeps column
+  // indices live as well)
+  constexpr int PMAXV = MODE == kFused ? 0 : kSplitPrefetchMaxValues;
   int r = ROWSM_EINVAL;
   (void)((c.p.nv == NVs + 1 && (NVs + 1) * VW <= MAXV
-              ? (r = launch_split_nv<In, Out, VW, ((NVs + 1) * VW <= MAXV ? NVs + 1 : 1), MODE>(c),
+              ? (r = c.p.prefetch
+                         ? ((NVs + 1) * VW <= PMAXV
+                                ? launch_split_nv<In, Out, VW,
+                                                  ((NVs + 1) * VW <= PMAXV ? NVs + 1 : 1), MODE,
+                                                  true>(c)
+                                : ROWSM_EINVAL)
+                         : launch_split_nv<In, Out, VW, ((NVs + 1) * VW <= MAXV ? NVs + 1 : 1),
+                                           MODE, false>(c),
                  true)
               : false) ||
          ...);

@@ -64,7 +64,25 @@ struct SplitWorkspace {
 // launch, so even a broken exchange lets the whole grid drain quickly.
 constexpr uint32_t kSplitSpinLimit = 1u << 20;
 
-template <typename In, typename Out, int VW, int NV, int MODE>
+// Loads a block's share of one row (raw), masked as the row's form needs.
+template <typename In, int VW, int NV, bool FUSED>
+__device__ __forceinline__ void split_load_share(InVec<In, VW> (&v)[NV], rsrc_t rx, uint32_t vin,
+                                                 uint32_t sin, int RT, int g, bool last_ok,
+                                                 int lim) {
+#pragma unroll
+  for (int s = 0; s < NV; ++s) {
+    if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim))
+      v[s].load(rx, vin, s * sin);
+    else
+      v[s].set_neg_inf();
+  }
+}
+
+// PIPE (software pipelining): while a block reduces, exchanges and writes
+// row k, the loads of its next row are already in flight, so memory keeps
+// streaming through the exchange wait and the write burst (one more raw
+// share per lane in registers).
+template <typename In, typename Out, int VW, int NV, int MODE, bool PIPE>
 __global__ __launch_bounds__(1024) void split_row_kernel(
     const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
     int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0, Fused fz) {
@@ -90,28 +108,40 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
   const uint32_t sout = (uint32_t)RT * (VW * Out::bytes);
   const float ninf = -__builtin_inff();
 
+  auto row_rsrc = [&](int64_t r) { return make_rsrc(x + r * cols, (uint64_t)cols * In::bytes); };
+  auto row_limit = [&](int64_t r) { return FUSED ? fused_limit(fz, r, cols) : cols - 1; };
+
   bool gave_up = false;  // per lane of the first wave
+  InVec<In, VW> nxt[NV];  // PIPE: the next row's share, in flight
+  if constexpr (PIPE) {
+    if (q < rows) split_load_share<In, VW, NV, FUSED>(nxt, row_rsrc(q), vin, sin, RT, g, last_ok,
+                                                      row_limit(q));
+  }
   uint32_t k = 0;
   for (int64_t row = q; row < rows; row += slots, ++k) {
-    const rsrc_t rx = make_rsrc(x + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * Out::bytes);
 
-    const int lim = FUSED ? fused_limit(fz, row, cols) : cols - 1;
+    const int lim = row_limit(row);
     float f[NV][VW];
     {
       InVec<In, VW> v[NV];
+      if constexpr (PIPE) {
 #pragma unroll
-      for (int s = 0; s < NV; ++s) {
-        if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim))
-          v[s].load(rx, vin, s * sin);
-        else
-          v[s].set_neg_inf();
+        for (int s = 0; s < NV; ++s) v[s] = nxt[s];
+      } else {
+        split_load_share<In, VW, NV, FUSED>(v, row_rsrc(row), vin, sin, RT, g, last_ok, lim);
       }
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
         v[s].to_float(f[s]);
         if constexpr (FUSED) fused_apply(f[s], (s * RT + g) * VW, lim, fz.scale);
       }
+    }
+    if constexpr (PIPE) {
+      const int64_t next = row + slots;
+      if (next < rows)
+        split_load_share<In, VW, NV, FUSED>(nxt, row_rsrc(next), vin, sin, RT, g, last_ok,
+                                            row_limit(next));
     }
     if constexpr (FUSED) {
       // Vectors wholly past the limit are zeros whatever the row's max and

@@ -285,3 +285,16 @@ def test_few_rows_split_counts(lib):
     assert "split=13" in t and "block=512" in t                      # 48 x 32 > 4 x 256 blocks
     t = d(128, 151936, R.F32, R.F32)
     assert "split=10" in t                                           # register plan
+
+
+def test_prefetch_config(lib):
+    d = lambda rows, cols, i, o, **cfg: R.rowsm_describe_op(
+        R.OP_SOFTMAX, rows, cols, i, o, R.RowsmConfig(**cfg))
+    st, t = d(4096, 151936, R.BF16, R.F32, prefetch=1)
+    assert st == R.OK and "prefetch=1" in t and "nv=10" in t
+    assert d(1024, 262144, R.F32, R.F32, prefetch=1)[0] == R.EINVAL      # 64 values per lane
+    assert d(1024, 262144, R.F32, R.F32, prefetch=1, split_blocks=32)[0] == R.OK
+    assert d(8, 4096, R.F32, R.F32, prefetch=2)[0] == R.EINVAL            # outside its domain
+    st, t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 64, 262144, R.F32, R.F32,
+                                R.RowsmConfig(prefetch=1, split_blocks=32))
+    assert st == R.EINVAL                                                # fused: no prefetching

@@ -70,14 +70,14 @@ def test_no_immediate_overwrite_of_store_data(asm):
     r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELi0E",      # small_262144x64
     r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELi0E",     # causal_32768x4096
     r"medium_row_kernelINS_3F32ES1_Li4ELi4ELb0ELi0E",      # fp32_64x1000
-    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELi0E",    # vocab_4096x151936
-    r"split_row_kernelINS_3F32ES1_Li4ELi16ELi0E",          # large_1024x262144
+    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELi0ELb0E",    # vocab_4096x151936
+    r"split_row_kernelINS_3F32ES1_Li4ELi16ELi0ELb0E",          # large_1024x262144
     r"large_row_kernelINS_3F32ES1_Li4ELi4ELi0E",           # two-pass form
     r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELi1E",     # fused causal 32768x4096
-    r"split_row_kernelINS_3F32ES1_Li4ELi8ELi1E",           # fused f32 long rows
+    r"split_row_kernelINS_3F32ES1_Li4ELi8ELi1ELb0E",           # fused f32 long rows
     r"small_row_kernelINS_4BF16ES1_Li8ELi8ELi4ELi1E",      # fused small rows
-    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELi2E",    # log-softmax vocab_4096x151936
-    r"split_row_kernelINS_3F32ES1_Li4ELi16ELi2E",          # log-softmax 1024x262144
+    r"split_row_kernelINS_4BF16ENS_3F32ELi4ELi10ELi2ELb0E",    # log-softmax vocab_4096x151936
+    r"split_row_kernelINS_3F32ES1_Li4ELi16ELi2ELb0E",          # log-softmax 1024x262144
     r"medium_row_kernelINS_4BF16ES1_Li8ELi19ELb1ELi2E",    # log-softmax packed bf16 151936
     r"medium_row_kernelINS_4BF16ES1_Li8ELi2ELb0ELi2E",     # log-softmax 4096-wide rows
     r"bwd_small_kernelINS_4BF16ES1_Li8ELi8ELi4EEE",        # bwd_small_262144x64

@@ -167,3 +167,11 @@ def test_log_few_rows_launcher_choice(rows, cols, din, dout):
     x = W.random_matrix(rows, cols, din, sigma=5.0, seed=rows + 7 * cols)
     y = run_log(x.to(DEV), dout)
     assert_log_parity(x, y, dout, f"log few rows {rows}x{cols} {din}->{dout}")
+
+
+@pytest.mark.parametrize("din,dout", [("bf16", "f32"), ("f32", "f32")])
+def test_log_split_prefetch_form(din, dout):
+    cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=16, blocks_per_cu=1, prefetch=1)
+    x = W.random_matrix(200, 151936, din, sigma=4.0, seed=3)
+    y = run_log(x.to(DEV), dout, config=cfg)
+    assert_log_parity(x, y, dout, f"log prefetch {din}->{dout}")

@@ -241,3 +241,23 @@ def test_few_rows_launcher_choice(rows, cols, din, dout):
     y = run(x.to(DEV), dout)
     assert_parity(x, y, dout, f"few rows {rows}x{cols} {din}->{dout} [{desc}]")
     assert R.rowsm_split_wait_failures() == 0
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("cols,S,bpc", [(65536, 8, 1), (151936, 8, 2), (262144, 32, 1),
+                                        (100003, 16, 1), (40000, 2, 1)])
+def test_split_prefetch_form(cols, S, bpc, din, dout):
+    # the software-pipelined single-read form: each block loads its next row
+    # during the current row's exchange; few blocks per compute unit so that
+    # every block walks many rows
+    rows = 300 if cols < 200000 else 120
+    cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=S, blocks_per_cu=bpc, prefetch=1)
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]), cfg)
+    if st != R.OK:
+        pytest.skip("more than 48 values per lane: no prefetching form")
+    assert "prefetch=1" in desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols + S)
+    y = run(x.to(DEV), dout, config=cfg)
+    assert_parity(x, y, dout, f"prefetch {rows}x{cols} S={S} {din}->{dout}")
+    assert R.rowsm_split_wait_failures() == 0
