@@ -261,3 +261,19 @@ def test_bwd_few_rows_launcher_choice(rows, cols, din, dout):
     dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
     assert_bwd_parity(y, dy, dx, dout, f"bwd few rows {rows}x{cols} {din}->{dout} [{desc}]")
     assert R.rowsm_split_wait_failures() == 0
+
+
+def test_bwd_bounded_writes_and_inputs_untouched():
+    # nothing written outside dx; y and dy unchanged
+    for fam, cols in ((R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 151936)):
+        rows = max(2, 1_000_000 // cols)
+        y, dy = inputs(rows, cols, "bf16", seed=cols)
+        yd, dyd = y.to(DEV), dy.to(DEV)
+        y0, dy0 = yd.clone(), dyd.clone()
+        guard, n = 4096, rows * cols
+        buf = torch.full((n + 2 * guard,), -123.0, device=DEV)
+        dx = buf[guard:guard + n].view(rows, cols)
+        run_bwd(yd, dyd, "f32", config=R.RowsmConfig(variant=fam), out=dx)
+        assert torch.all(buf[:guard] == -123.0) and torch.all(buf[guard + n:] == -123.0)
+        assert torch.equal(yd, y0) and torch.equal(dyd, dy0)
+        assert_bwd_parity(y, dy, dx, "f32", f"bounded {R.VARIANT_NAMES[fam]}")

@@ -175,3 +175,18 @@ def test_log_split_prefetch_form(din, dout):
     x = W.random_matrix(200, 151936, din, sigma=4.0, seed=3)
     y = run_log(x.to(DEV), dout, config=cfg)
     assert_log_parity(x, y, dout, f"log prefetch {din}->{dout}")
+
+
+def test_log_bounded_writes_and_deterministic():
+    for fam, cols in ((R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 151936)):
+        rows = max(2, 1_000_000 // cols)
+        x = W.random_matrix(rows, cols, "bf16", sigma=6.0, seed=cols).to(DEV)
+        x0 = x.clone()
+        guard, n = 4096, rows * cols
+        buf = torch.full((n + 2 * guard,), -123.0, device=DEV)
+        y = buf[guard:guard + n].view(rows, cols)
+        run_log(x, "f32", config=R.RowsmConfig(variant=fam), out=y)
+        y2 = run_log(x, "f32", config=R.RowsmConfig(variant=fam))
+        assert torch.equal(y, y2)
+        assert torch.all(buf[:guard] == -123.0) and torch.all(buf[guard + n:] == -123.0)
+        assert torch.equal(x, x0)

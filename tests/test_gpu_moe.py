@@ -144,3 +144,17 @@ def test_moe_workload_full_size(name):
         assert torch.equal(o[t0:t0 + (1 << 16)].float(), want)
     del x, o
     torch.cuda.empty_cache()
+
+
+def test_moe_bounded_writes_and_scores_untouched():
+    x = W.random_matrix(3333, 256, "bf16", seed=8).to(DEV)
+    x0 = x.clone()
+    guard, n = 1024, 3333 * 8
+    buf = torch.full((n + 2 * guard,), -123.0, device=DEV)
+    o = buf[guard:guard + n].view(3333, 8)
+    run_moe(x, 32, "f32", out=o)
+    assert torch.all(buf[:guard] == -123.0) and torch.all(buf[guard + n:] == -123.0)
+    assert torch.equal(x, x0)
+    o2 = run_moe(x, 32, "f32")
+    assert torch.equal(o, o2)
+    assert_moe_exact(x.cpu(), o, 32, "f32", "bounded")

@@ -261,3 +261,24 @@ def test_split_prefetch_form(cols, S, bpc, din, dout):
     y = run(x.to(DEV), dout, config=cfg)
     assert_parity(x, y, dout, f"prefetch {rows}x{cols} S={S} {din}->{dout}")
     assert R.rowsm_split_wait_failures() == 0
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("rows", [63, 64, 65, 255, 256, 257])
+@pytest.mark.parametrize("cols", [65536, 151936, 262144])
+def test_row_count_boundaries(rows, cols, dt):
+    # the row-count rules switch at cus / 4 and cus rows (256 compute units):
+    # parity on every row at and around both thresholds, launcher's choice
+    x = W.random_matrix(rows, cols, dt, sigma=3.0, seed=rows + cols)
+    y = run(x.to(DEV), dt)
+    assert_parity(x, y, dt, f"rows {rows} x {cols} {dt}")
+    assert R.rowsm_split_wait_failures() == 0
+
+
+@pytest.mark.parametrize("rows,cols", [(4099, 64), (4099, 1000), (4099, 4097)])
+def test_many_rows_grid_stride(rows, cols):
+    # more rows than one grid covers in the small and medium families
+    x = W.random_matrix(rows, cols, "bf16", sigma=4.0, seed=rows + cols)
+    for cfg in (None, R.RowsmConfig(blocks_per_cu=1)):
+        y = run(x.to(DEV), "bf16", config=cfg)
+        assert_parity(x, y, "bf16", f"{rows}x{cols} cfg={cfg is not None}")
