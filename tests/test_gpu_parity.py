@@ -282,3 +282,39 @@ def test_many_rows_grid_stride(rows, cols):
     for cfg in (None, R.RowsmConfig(blocks_per_cu=1)):
         y = run(x.to(DEV), "bf16", config=cfg)
         assert_parity(x, y, "bf16", f"{rows}x{cols} cfg={cfg is not None}")
+
+
+def test_split_launches_from_host_threads():
+    # four host threads, each with its own stream, launch single-read split
+    # softmax and backward concurrently (the C calls run without the GIL):
+    # the per-device workspace lock, tag reservation and cross-stream
+    # ordering must keep every result exact
+    import threading
+    shapes = [(9, 70000 + 16 * i) for i in range(4)]
+    xs = [W.random_matrix(r, c, "f32", sigma=3.0, seed=c).to(DEV) for r, c in shapes]
+    refs = [run(x, "f32", variant=R.LARGE) for x in xs]
+    errors = []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for _ in range(6):
+                    y = R.softmax(xs[i], variant=R.LARGE, stream=s)
+                    s.synchronize()
+                    if not torch.equal(y, refs[i]):
+                        errors.append(f"thread {i}: result differs")
+                        return
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append(f"thread {i}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=60)
+    assert not any(t.is_alive() for t in threads), "a launching thread did not finish"
+    assert not errors, errors
+    assert R.rowsm_split_wait_failures() == 0
+    for i, x in enumerate(xs):
+        assert_parity(x.cpu(), refs[i], "f32", f"threaded shape {i}")
