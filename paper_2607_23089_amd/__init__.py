@@ -206,41 +206,62 @@ def dtype_code(dtype) -> int:
     raise RowsmError(f"unsupported dtype {dtype}")
 
 
+def _row_operands(name, x, out, out_dtype):
+    """Shared marshalling of the row operations: x must be a contiguous GPU
+    tensor; out (allocated when None) a contiguous tensor of x's shape on x's
+    device.  Returns (out, rows, cols)."""
+    import torch
+    if not x.is_cuda or not x.is_contiguous():
+        raise RowsmError(f"{name} needs a contiguous GPU tensor")
+    if out is None:
+        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
+        raise RowsmError("out must be a contiguous tensor of the input's shape on its device")
+    cols = x.shape[-1] if x.dim() else 1
+    rows = x.numel() // cols if cols else 0
+    return out, rows, cols
+
+
+def _stream_handle(stream, device) -> int:
+    import torch
+    return (stream or torch.cuda.current_stream(device)).cuda_stream
+
+
+def softmax(x, out_dtype=None, out=None, variant: int = AUTO, config=None, stream=None):
+    """softmax(x, dim=-1) of a contiguous fp32/bf16 GPU tensor through the
+    library.  Returns ``out`` (allocated with ``out_dtype``, default x.dtype,
+    when not given).  Runs on torch's current stream unless ``stream`` (a
+    torch.cuda.Stream) is given."""
+    out, rows, cols = _row_operands("softmax", x, out, out_dtype)
+    args = (x.data_ptr(), out.data_ptr(), rows, cols, dtype_code(x.dtype),
+            dtype_code(out.dtype), _stream_handle(stream, x.device))
+    if config is not None:
+        check(rowsm_forward_config(*args, config))
+    elif variant != AUTO:
+        check(rowsm_forward_variant(*args, variant))
+    else:
+        check(rowsm_forward(*args))
+    return out
+
+
 def scaled_causal_softmax(x, scale: float, causal_period: int, causal_offset: int = 0,
                           out_dtype=None, out=None, config=None, stream=None):
     """softmax(scale * x + causal mask, dim=-1) of a contiguous fp32/bf16 GPU
     tensor (see rowsm_forward_scaled_causal).  Marshalling only."""
-    import torch
-    if not x.is_cuda or not x.is_contiguous():
-        raise RowsmError("scaled_causal_softmax needs a contiguous GPU tensor")
-    if out is None:
-        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
-    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
-        raise RowsmError("out must be a contiguous tensor of x's shape on x's device")
-    cols = x.shape[-1] if x.dim() else 1
-    rows = x.numel() // cols if cols else 0
-    st = (stream or torch.cuda.current_stream(x.device)).cuda_stream
+    out, rows, cols = _row_operands("scaled_causal_softmax", x, out, out_dtype)
     check(rowsm_forward_scaled_causal(x.data_ptr(), out.data_ptr(), rows, cols,
                                       dtype_code(x.dtype), dtype_code(out.dtype), float(scale),
-                                      int(causal_period), int(causal_offset), st, config))
+                                      int(causal_period), int(causal_offset),
+                                      _stream_handle(stream, x.device), config))
     return out
 
 
 def log_softmax(x, out_dtype=None, out=None, config=None, stream=None):
     """log(softmax(x, dim=-1)) of a contiguous fp32/bf16 GPU tensor (see
     rowsm_log_softmax).  Marshalling only."""
-    import torch
-    if not x.is_cuda or not x.is_contiguous():
-        raise RowsmError("log_softmax needs a contiguous GPU tensor")
-    if out is None:
-        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
-    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
-        raise RowsmError("out must be a contiguous tensor of x's shape on x's device")
-    cols = x.shape[-1] if x.dim() else 1
-    rows = x.numel() // cols if cols else 0
-    st = (stream or torch.cuda.current_stream(x.device)).cuda_stream
+    out, rows, cols = _row_operands("log_softmax", x, out, out_dtype)
     check(rowsm_log_softmax(x.data_ptr(), out.data_ptr(), rows, cols, dtype_code(x.dtype),
-                            dtype_code(out.dtype), st, config))
+                            dtype_code(out.dtype), _stream_handle(stream, x.device), config))
     return out
 
 
@@ -248,20 +269,14 @@ def softmax_backward(y, dy, out_dtype=None, out=None, config=None, stream=None):
     """Gradient of softmax(x, dim=-1) given its output ``y`` and the upstream
     gradient ``dy`` (contiguous GPU tensors of one shape and dtype), see
     rowsm_softmax_backward.  Returns ``out`` (dx).  Marshalling only."""
-    import torch
-    if not (y.is_cuda and dy.is_cuda) or not (y.is_contiguous() and dy.is_contiguous()):
+    if not dy.is_cuda or not dy.is_contiguous():
         raise RowsmError("softmax_backward needs contiguous GPU tensors")
     if dy.shape != y.shape or dy.dtype != y.dtype or dy.device != y.device:
         raise RowsmError("y and dy must share shape, dtype and device")
-    if out is None:
-        out = torch.empty(y.shape, dtype=out_dtype or y.dtype, device=y.device)
-    elif out.shape != y.shape or not out.is_contiguous() or out.device != y.device:
-        raise RowsmError("out must be a contiguous tensor of y's shape on y's device")
-    cols = y.shape[-1] if y.dim() else 1
-    rows = y.numel() // cols if cols else 0
-    st = (stream or torch.cuda.current_stream(y.device)).cuda_stream
+    out, rows, cols = _row_operands("softmax_backward", y, out, out_dtype)
     check(rowsm_softmax_backward(y.data_ptr(), dy.data_ptr(), out.data_ptr(), rows, cols,
-                                 dtype_code(y.dtype), dtype_code(out.dtype), st, config))
+                                 dtype_code(y.dtype), dtype_code(out.dtype),
+                                 _stream_handle(stream, y.device), config))
     return out
 
 
@@ -282,36 +297,7 @@ def moe_group_top2(scores, group_size: int = 32, out_dtype=None, out=None, confi
         out = torch.empty(shape, dtype=out_dtype or torch.float32, device=scores.device)
     elif tuple(out.shape) != shape or not out.is_contiguous() or out.device != scores.device:
         raise RowsmError("out must be a contiguous tokens x (experts / group_size) tensor")
-    st = (stream or torch.cuda.current_stream(scores.device)).cuda_stream
     check(rowsm_moe_group_top2(scores.data_ptr(), out.data_ptr(), tokens, experts,
                                int(group_size), dtype_code(scores.dtype), dtype_code(out.dtype),
-                               st, config))
-    return out
-
-
-def softmax(x, out_dtype=None, out=None, variant: int = AUTO, config=None, stream=None):
-    """softmax(x, dim=-1) of a contiguous fp32/bf16 GPU tensor through the
-    library.  Returns ``out`` (allocated with ``out_dtype``, default x.dtype,
-    when not given).  Runs on torch's current stream unless ``stream`` (a
-    torch.cuda.Stream) is given."""
-    import torch
-    if not x.is_cuda:
-        raise RowsmError("rowsm.softmax needs a GPU tensor")
-    if not x.is_contiguous():
-        raise RowsmError("rowsm.softmax needs a contiguous tensor")
-    if out is None:
-        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
-    elif out.shape != x.shape or not out.is_contiguous() or out.device != x.device:
-        raise RowsmError("out must be a contiguous tensor of x's shape on x's device")
-    cols = x.shape[-1] if x.dim() else 1
-    rows = x.numel() // cols if cols else 0
-    st = (stream or torch.cuda.current_stream(x.device)).cuda_stream
-    args = (x.data_ptr(), out.data_ptr(), rows, cols, dtype_code(x.dtype),
-            dtype_code(out.dtype), st)
-    if config is not None:
-        check(rowsm_forward_config(*args, config))
-    elif variant != AUTO:
-        check(rowsm_forward_variant(*args, variant))
-    else:
-        check(rowsm_forward(*args))
+                               _stream_handle(stream, scores.device), config))
     return out
