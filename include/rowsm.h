@@ -26,7 +26,7 @@
  *   - stream is a hipStream_t (NULL = the legacy default stream).  The call
  *     only enqueues work; results are visible once the caller synchronises the
  *     stream.  Nothing is allocated per call.  The single-read LARGE form
- *     uses a 2 MiB device workspace that the first such call on a device
+ *     uses a 32 MiB device workspace that the first such call on a device
  *     allocates and clears (synchronously) and that lives until the process
  *     ends; make that first call outside stream capture.  Such launches on
  *     one device are ordered one after another whatever their streams (each
@@ -65,8 +65,9 @@ typedef enum {
  * keep their shares in registers and exchange (max, sum) pairs through a
  * small device workspace (single read), or, for rows too long for that,
  * streams the row through tiles twice (online max/sum pass, then normalize).
- * The single-read form's grid is sized to at most one full residency of the
- * device.
+ * The single-read form launches one group of blocks per row; with
+ * cfg->blocks_per_cu given, one residency of the device whose groups loop
+ * over the rows.
  *
  * HIP graphs: every entry point may be called on a stream that is being
  * captured.  The single-read LARGE form keeps per-launch state on the host

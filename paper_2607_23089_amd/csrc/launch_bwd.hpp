@@ -88,13 +88,9 @@ int launch_bwd_split_nv(const Call& c) {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
                                                    p.block, 0) != hipSuccess)
     return ROWSM_EHIP;
-  if (p.grid < 0 && per_cu > -p.grid) per_cu = (int)-p.grid;
-  const int64_t resident = (int64_t)per_cu * c.cus;
-  int64_t slots = resident / p.split;
-  if (slots > c.rows) slots = c.rows;
-  if (slots > kSplitMaxBlocks / p.split) slots = kSplitMaxBlocks / p.split;
+  const int64_t slots = split_slots(p, c.rows, per_cu, c.cus);
   if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
-  const unsigned grid = (unsigned)(slots * p.split);  // at most one full residency
+  const unsigned grid = (unsigned)(slots * p.split);
 
   SplitTicket t;
   int r = split_begin(c.st, (uint64_t)((c.rows + slots - 1) / slots), &t);

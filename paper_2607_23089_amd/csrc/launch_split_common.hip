@@ -1,7 +1,7 @@
 // Per-device state of the single-read split-row form.
 //
 // The workspace (two 64-bit words per block and row parity, an error count;
-// 2 MiB) is allocated and cleared on the first split launch on a device and
+// 32 MiB) is allocated and cleared on the first split launch on a device and
 // kept until the process ends.  Split launches on one device are ordered
 // through `last` (each waits for the previous one, whatever its stream), so
 // two launches never use the workspace at the same time.  `last` only orders

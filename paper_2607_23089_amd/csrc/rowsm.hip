@@ -267,22 +267,27 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     }
     if (want_split >= 0) {
       // Single-read form: T threads per block, S blocks per row (S <= 64:
-      // one wave polls the S peers), at most 64 fp32 values per lane.
-      // Widening rows (bf16 -> f32 writes twice what it reads) do best with
-      // 512-thread blocks holding at most 40 values per lane, two blocks per
-      // compute unit; the others with 256-thread blocks and 64 values per
-      // lane (measured on the 4096 x 151936 and 1024 x 262144 workloads).
+      // one wave polls the S peers), at most 64 fp32 values per lane (40
+      // for widening rows, bf16 -> f32, which write twice what they read).
+      // 512-thread blocks, except 256 where 512 would leave fewer than 8
+      // blocks to a row that does not widen (a sweep of 1024-4096 rows x
+      // 98304-1048576 columns in every dtype pair, one group per row: 512
+      // gains up to 15% on the longest rows; 256 is 8% faster on
+      // 1024 x 131072 f32).
       const bool widening = ob > ib;
       const bool forced_block = cfg && cfg->block > 0;
-      int T = forced_block ? cfg->block : (widening ? 512 : 256);
       const int vals = fused ? 32 : (widening ? 40 : 64);
       int nv_cap = vals / vw < 16 ? vals / vw : 16;
       if (nv_cap < 1) nv_cap = 1;
+      int T = 512;
+      if (forced_block) T = cfg->block;
+      else if (!widening && cdiv(nvec, (int64_t)nv_cap * 512) < 8) T = 256;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
       if (S < 1) S = 1;
-      // Grid sized at launch from occupancy (one full residency of the
-      // device at most); a negative value caps blocks per compute unit.
-      int64_t grid = bpc ? -(int64_t)bpc : (widening && !forced_block ? -2 : 0);
+      // Grid: one group of S blocks per row (0), or with blocks_per_cu
+      // given, one residency of at most that many blocks per compute unit
+      // whose groups loop over the rows (negative; split_slots()).
+      int64_t grid = bpc ? -(int64_t)bpc : 0;
       if (want_split == 0) {
         // Few rows: more, smaller blocks per row so that the launch fills
         // the device (256-thread blocks unless a block size is given).
@@ -291,7 +296,6 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         if (sf > 0 && (int64_t)sf * Tf > (int64_t)S * T) {
           S = sf;
           T = Tf;
-          grid = bpc ? -(int64_t)bpc : 0;
         }
       }
       const int nv = (int)cdiv(nvec, (int64_t)S * T);
@@ -331,9 +335,9 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
 //   MEDIUM  the smallest row group of <= 16 waves whose lanes hold at most 32
 //           bytes of each input (then 64, then 128), unless the rows are few
 //           and long (the forward's row-count rule, on the backward's bytes);
-//   LARGE   the row split over S <= 64 co-resident 256-thread blocks (more
-//           blocks per row for few rows, as the forward), or two streaming
-//           passes for rows longer than that.
+//   LARGE   the row split over S <= 64 co-resident 512-thread blocks (more,
+//           256-thread blocks per row for few rows, as the forward), or two
+//           streaming passes for rows longer than that.
 int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t ia,
                   uintptr_t dxa, const rowsm_config* cfg, int cus, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
@@ -414,12 +418,20 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
   if (variant == ROWSM_LARGE) {
     const int want_split = cfg ? cfg->split_blocks : 0;
     if (want_split >= 0) {
-      const int T = (cfg && cfg->block > 0) ? cfg->block : 256;
+      // 512-thread blocks (measured 0-4% faster than 256 on long rows of
+      // every dtype pair with one group per row); few rows as the forward
+      // plan, with 256-thread blocks unless a block size is given.
+      const bool forced_block = cfg && cfg->block > 0;
+      int T = forced_block ? cfg->block : 512;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
       if (S < 1) S = 1;
-      if (want_split == 0) {  // few rows: fill the device (as the forward plan)
-        const int sf = few_rows_split(rows, nvec, T, nv_cap, cus);
-        if (sf > S) S = sf;
+      if (want_split == 0) {
+        const int Tf = forced_block ? T : 256;
+        const int sf = few_rows_split(rows, nvec, Tf, nv_cap, cus);
+        if (sf > 0 && (int64_t)sf * Tf > (int64_t)S * T) {
+          S = sf;
+          T = Tf;
+        }
       }
       const int nv = (int)cdiv(nvec, (int64_t)S * T);
       if (S <= 64 && nv <= nv_cap) {
@@ -427,7 +439,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
         p->nv = nv;
         p->vpl = nv;
         p->block = T;
-        p->grid = bpc ? -(int64_t)bpc : 0;  // sized from occupancy at launch
+        p->grid = bpc ? -(int64_t)bpc : 0;  // as the forward plan
         return ROWSM_OK;
       }
       if (want_split > 0) return ROWSM_EINVAL;
@@ -796,8 +808,9 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
                     "split=%d prefetch=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
                     (int)p.packed, p.u, p.split, (int)p.prefetch, p.block,
-                    (long long)(p.split ? 0 : p.grid),
-                    p.split ? "grid sized from occupancy at launch"
+                    (long long)(p.split ? (p.grid < 0 ? 0 : rows * p.split) : p.grid),
+                    p.split ? (p.grid < 0 ? "one residency sized from occupancy at launch"
+                                          : "one group of blocks per row")
                             : "grid assumes 256 CUs");
     }
   }

@@ -35,17 +35,19 @@
 // after every block of the group has published row k + 1, i.e. after all of
 // them have read row k's words.
 //
-// Co-residency.  The host sizes the grid from the kernel's occupancy to at
-// most one full residency of the device, and blocks publish before they
-// wait, so when the launch has the device to itself every block is resident
-// at once and every wait ends.  When other work shares the device, blocks
-// are still dispatched in block order on each XCD and every XCD holds far
-// more blocks than the S/8 of one row group it carries, so the lowest row
-// group that has not finished always has all of its blocks resident and
-// progresses; groups behind it run once it exits (the forward-progress
-// property single-pass scans also rely on).  The wait is bounded regardless:
-// a lane that gives up records the failure in the workspace and carries on,
-// so the grid always drains.
+// Forward progress.  A block waits only for the other blocks of its own row
+// group, never for a later group, and the S blocks of a group fit on the
+// device at once (the host checks the occupancy).  Workgroups are dispatched
+// in block order on each XCD, so on every XCD the blocks of the lowest row
+// group that has not finished are dispatched before any block of a later
+// group: if one of them were not yet dispatched, that XCD would hold no block
+// of this launch at all and would dispatch it next.  That group therefore
+// has all of its blocks resident, completes, and exits, and so on by
+// induction, whether the grid is one full residency of the device whose
+// groups loop over the rows or one group per row far larger than the device
+// (the host's default), and whether or not other work shares the device.
+// The wait is bounded regardless: a lane that gives up records the failure
+// in the workspace and carries on, so the grid always drains.
 #pragma once
 
 #include "rowsm_device.hpp"

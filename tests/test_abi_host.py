@@ -156,7 +156,15 @@ def test_describe(lib):
     assert st == R.OK and text.startswith("large") and "vw=4" in text and "split=8" in text
     assert "nv=10" in text and "block=512" in text
     st, text = R.rowsm_describe(1024, 262144, R.F32, R.F32, R.LARGE)
-    assert st == R.OK and text.startswith("large") and "split=16" in text and "nv=16" in text
+    assert st == R.OK and text.startswith("large") and "split=8" in text and "nv=16" in text
+    assert "block=512" in text and "grid=8192" in text and "one group of blocks per row" in text
+    # a grid cap gives one residency whose groups loop over the rows
+    st, text = R.rowsm_describe_op(R.OP_SOFTMAX, 1024, 262144, R.F32, R.F32,
+                                   R.RowsmConfig(blocks_per_cu=2))
+    assert st == R.OK and "split=8" in text and "one residency" in text
+    # 512 threads would leave fewer than 8 blocks to the row: 256
+    st, text = R.rowsm_describe(1024, 131072, R.F32, R.F32)
+    assert st == R.OK and "split=8" in text and "block=256" in text
     cfg_two_pass = R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
     st = R.rowsm_forward_config(X, Y, 4, 8, 7, R.F32, 0, cfg_two_pass)
     assert st == R.EDTYPE
@@ -228,9 +236,11 @@ def test_backward_plans(lib):
     st, t = d(32, 151936, R.BF16, R.BF16)                          # register cap: 16
     assert st == R.OK and "split=16" in t and "nv=5" in t
     st, t = d(1024, 262144, R.F32, R.F32)
-    assert st == R.OK and "split=32" in t and "nv=8" in t and "block=256" in t
-    # past 64 blocks x 256 threads x 8 vectors: the two-pass form
-    st, t = d(4, 64 * 256 * 8 * 4 + 4, R.F32, R.F32)
+    assert st == R.OK and "split=16" in t and "nv=8" in t and "block=512" in t
+    st, t = d(4, 64 * 256 * 8 * 4 + 4, R.F32, R.F32)                # 512-thread blocks
+    assert st == R.OK and "split=33" in t and "block=512" in t
+    # past 64 blocks x 512 threads x 8 vectors: the two-pass form
+    st, t = d(4, 64 * 512 * 8 * 4 + 4, R.F32, R.F32)
     assert st == R.OK and "split=0" in t and "block=1024" in t
     assert d(4, 100, R.F32, R.F32, variant=R.MEDIUM, waves_per_row=16)[0] == R.OK
     assert d(4, 8, 9, R.F32)[0] == R.EDTYPE
@@ -275,7 +285,7 @@ def test_few_rows_split_counts(lib):
     assert "split=8" in d(32, 65536, R.F32, R.F32) and "split=8" in d(63, 65536, R.F32, R.F32)
     assert "split=64" in d(1, 262144, R.F32, R.F32)
     assert "split=32" in d(8, 262144, R.F32, R.F32)
-    assert "split=16" in d(1024, 262144, R.F32, R.F32)              # many rows: registers
+    assert "split=8" in d(1024, 262144, R.F32, R.F32)               # many rows: registers
     assert "split=32" in d(8, 151936, R.BF16, R.F32) and "block=256" in d(8, 151936, R.BF16, R.F32)
     t = d(4096, 151936, R.BF16, R.F32)
     assert "split=8" in t and "block=512" in t                       # the vocab workload
