@@ -12,8 +12,14 @@ regime, in this order (inputs resident in HBM before timing starts):
 Between two visits of the same input the other three move more than 3 GB, far
 more than the 256 MB memory-side cache plus L2, so every launch reads x from
 HBM.  Each launch is bracketed by HIP timing events (created without a
-system-scope fence) recorded on the stream it runs on; ``value`` is the step's algorithmic bytes (x read once + y written once,
-summed over the regimes) divided by the measured step time.
+system-scope fence) recorded on the stream it runs on; ``value`` is the
+step's algorithmic bytes (x read once + y written once, summed over the
+regimes) divided by the measured step time.
+
+Before the timed steps the same protocol times the library's streaming copy
+(rowsm_stream_copy) of each regime's bytes, same dtype pair and buffers: a
+plain copy moving the same bytes in the same run, reported per launch as
+``ratio_to_copy`` (kernel rate / copy rate).
 
 Prints ONE JSON line (rank 0).  ``--gpus`` above 1 is refused: this path runs
 on one GPU (rows shard across GPUs without communication).
@@ -449,9 +455,32 @@ def main() -> int:
             if events is not None:
                 events[i][1].record(stream)
 
+    def copy_step(events=None):
+        # The library's streaming copy of each regime's bytes (same dtype
+        # pair, same buffers): what a plain copy of the same bytes takes.
+        for i, (name, w, xp, yp, di, do) in enumerate(calls):
+            if events is not None:
+                events[i][0].record(stream)
+            st = R.rowsm_stream_copy(xp, yp, w.rows * w.cols, di, do, sh)
+            if st != R.OK:
+                raise R.RowsmError(f"copy {name}: status {st} {R.rowsm_status_string(st)}")
+            if events is not None:
+                events[i][1].record(stream)
+
     for _ in range(args.warmup):
         step()
+        copy_step()
     torch.cuda.synchronize()
+
+    # Copies first, so that the timed softmax steps leave their
+    # outputs in y for the CPU baseline's parity check.
+    cevs = [[[HipEvent() for _ in range(2)] for _ in calls] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        copy_step(cevs[k])
+    torch.cuda.synchronize()
+    copy_wall = time.perf_counter() - t0
 
     evs = [[[HipEvent() for _ in range(2)] for _ in calls]
            for _ in range(args.steps)]
@@ -472,6 +501,9 @@ def main() -> int:
         gbs = w.algorithmic_bytes / (avg * 1e-3) / 1e9
         st, desc = R.rowsm_describe(w.rows, w.cols, R.dtype_code(W.TORCH_DTYPES[w.in_dtype]),
                                     R.dtype_code(W.TORCH_DTYPES[w.out_dtype]))
+        cavg = sum(cevs[k][i][0].elapsed_time(cevs[k][i][1]) for k in range(args.steps)) \
+            / args.steps
+        cgbs = w.algorithmic_bytes / (cavg * 1e-3) / 1e9
         per[name] = {
             "kernel": desc.split(" ")[0], "launch": desc,
             "algorithmic_bytes": w.algorithmic_bytes,
@@ -480,6 +512,7 @@ def main() -> int:
             "p90_us": ms[(9 * len(ms)) // 10] * 1e3,
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
             "hbm_bytes_per_launch": measured_traffic(name, desc),
+            "copy_us": cavg * 1e3, "copy_GBps": cgbs, "ratio_to_copy": gbs / cgbs,
         }
     failures = R.rowsm_split_wait_failures()
     if failures != 0:
@@ -508,7 +541,8 @@ def main() -> int:
             "algorithmic_bytes_per_step": step_bytes,
             "regimes": {n: {"GBps": round(v["GBps"], 1),
                             "frac_of_peak": round(v["frac_of_peak"], 4),
-                            "avg_us": round(v["avg_us"], 2), "kernel": v["kernel"]}
+                            "avg_us": round(v["avg_us"], 2), "kernel": v["kernel"],
+                            "ratio_to_copy": round(v["ratio_to_copy"], 4)}
                         for n, v in per.items()},
         },
         "roofline": {
@@ -521,6 +555,14 @@ def main() -> int:
             "traffic": d["hbm_bytes_per_launch"],
             "algorithmic_bytes_per_launch": d["algorithmic_bytes"],
             "avg_launch_us": d["avg_us"],
+            "copy_GBps": d["copy_GBps"],
+            "ratio_to_copy": d["ratio_to_copy"],
+        },
+        "copy_step": {
+            "what": "the library's streaming copy (rowsm_stream_copy) of each regime's bytes, "
+                    "same dtype pairs and buffers, back to back in the same protocol",
+            "GBps": step_bytes / (copy_wall / args.steps) / 1e9,
+            "ms_per_step": copy_wall / args.steps * 1e3,
         },
         "regimes_detail": per,
     }

@@ -219,8 +219,8 @@ int rowsm_log_softmax(const void *x, void *y, int64_t rows, int64_t cols, int in
  *   cfg       NULL = the launcher's choice; otherwise as rowsm_forward_config
  *             with these differences: y and dy are held in their raw form
  *             (packed = 1 is ROWSM_EINVAL), a lane holds at most 128 bytes of
- *             each input, and the single-read LARGE form uses 256-thread
- *             blocks unless block is given.
+ *             each input, and the single-read LARGE form uses 512-thread
+ *             blocks (256 for few rows) unless block is given.
  * The dot product is accumulated in fp32 (fma), in a fixed order: results are
  * deterministic for a given launch shape.  Special values follow IEEE
  * arithmetic in the formula above: a NaN in y or dy makes the dot product,
@@ -291,6 +291,26 @@ int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
  * in progress.
  */
 int64_t rowsm_split_wait_failures(void);
+
+/*
+ * rowsm_stream_copy: y[i] = x[i] converted from in_dtype to out_dtype, for
+ * i < n.  Not an operation of the method: a measurement aid.  It moves the
+ * bytes a row operation of the same dtype pair moves (every input byte read
+ * once, every output byte written once) in the access pattern that streams
+ * fastest on this device (one vector of at most 16 bytes per thread, each
+ * workgroup one contiguous chunk, non-temporal accesses), and benchmarks time
+ * it beside each row kernel as that workload's practical HBM ceiling.
+ *   x, y      device pointers to n elements of in_dtype / out_dtype, aligned
+ *             to their element size; y may equal x when the dtypes are equal,
+ *             any other overlap is rejected
+ *   n         >= 0 (n == 0: no launch), at most 2^60
+ *   stream    hipStream_t the kernel is enqueued on
+ * Conversion: bf16 -> f32 exact; f32 -> bf16 round to nearest even.
+ * Returns ROWSM_OK, ROWSM_EDTYPE, ROWSM_EINVAL (checked before any HIP call)
+ * or ROWSM_EHIP.
+ */
+int rowsm_stream_copy(const void *x, void *y, int64_t n, int in_dtype, int out_dtype,
+                      void *stream);
 
 /* rowsm_status_string: static, human-readable text for a rowsm_status. */
 const char *rowsm_status_string(int status);

@@ -42,7 +42,7 @@ EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
            "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_log_softmax",
            "rowsm_softmax_backward", "rowsm_moe_group_top2", "rowsm_describe",
            "rowsm_describe_op",
-           "rowsm_split_wait_failures", "rowsm_status_string")
+           "rowsm_split_wait_failures", "rowsm_stream_copy", "rowsm_status_string")
 
 
 class RowsmError(RuntimeError):
@@ -107,6 +107,8 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     h.rowsm_select.restype = i32
     h.rowsm_describe.argtypes = [i64, i64, i32, i32, i32, ctypes.c_char_p, i64]
     h.rowsm_describe.restype = i32
+    h.rowsm_stream_copy.argtypes = [vp, vp, i64, i32, i32, vp]
+    h.rowsm_stream_copy.restype = i32
     h.rowsm_split_wait_failures.argtypes = []
     h.rowsm_split_wait_failures.restype = i64
     h.rowsm_status_string.argtypes = [i32]
@@ -182,6 +184,10 @@ def rowsm_moe_group_top2(scores, out, tokens, experts, group_size, in_dtype, out
     ref = ctypes.byref(cfg) if cfg is not None else None
     return lib().rowsm_moe_group_top2(scores, out, tokens, experts, group_size, in_dtype,
                                       out_dtype, stream, ref)
+
+
+def rowsm_stream_copy(x, y, n, in_dtype, out_dtype, stream=0) -> int:
+    return lib().rowsm_stream_copy(x, y, n, in_dtype, out_dtype, stream)
 
 
 def rowsm_split_wait_failures() -> int:
@@ -300,4 +306,14 @@ def moe_group_top2(scores, group_size: int = 32, out_dtype=None, out=None, confi
     check(rowsm_moe_group_top2(scores.data_ptr(), out.data_ptr(), tokens, experts,
                                int(group_size), dtype_code(scores.dtype), dtype_code(out.dtype),
                                _stream_handle(stream, scores.device), config))
+    return out
+
+
+def stream_copy(x, out_dtype=None, out=None, stream=None):
+    """x converted to ``out_dtype`` (default x.dtype) by the library's
+    streaming copy (see rowsm_stream_copy), the measurement ceiling of the
+    row kernels.  Marshalling only."""
+    out, rows, cols = _row_operands("stream_copy", x, out, out_dtype)
+    check(rowsm_stream_copy(x.data_ptr(), out.data_ptr(), rows * cols, dtype_code(x.dtype),
+                            dtype_code(out.dtype), _stream_handle(stream, x.device)))
     return out

@@ -30,7 +30,7 @@ struct Plan {
   bool prefetch = false;  // single-read form: load the next row during the exchange
   // launch
   int block = 256;
-  int64_t grid = 1;  // split form: 0 = occupancy, < 0 = minus the blocks-per-CU cap
+  int64_t grid = 1;  // split form: 0 = one group per row, < 0 = minus the blocks-per-CU cap
 };
 
 // One launch request: the plan plus its operands.  mode is the output form

@@ -297,6 +297,22 @@ def test_few_rows_split_counts(lib):
     assert "split=10" in t                                           # register plan
 
 
+def test_stream_copy_argument_errors(lib):
+    f = R.rowsm_stream_copy
+    assert f(X, Y, 8, 7, R.F32, 0) == R.EDTYPE
+    assert f(X, Y, 8, R.F32, 2, 0) == R.EDTYPE
+    assert f(X, Y, -1, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, Y, (1 << 60) + 1, R.F32, R.F32, 0) == R.EINVAL
+    assert f(0, Y, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X, 0, 8, R.F32, R.F32, 0) == R.EINVAL
+    assert f(X + 2, Y, 8, R.F32, R.F32, 0) == R.EINVAL              # misaligned f32
+    assert f(X, Y + 1, 8, R.F32, R.BF16, 0) == R.EINVAL             # misaligned bf16
+    assert f(X, X + 16, 8, R.F32, R.F32, 0) == R.EINVAL             # partial overlap
+    assert f(X, X, 8, R.BF16, R.F32, 0) == R.EINVAL                 # in place, widening
+    assert f(X, X + 8, 8, R.BF16, R.F32, 0) == R.EINVAL             # output over the input
+    assert f(0, 0, 0, R.F32, R.F32, 0) == R.OK                      # empty: no launch
+
+
 def test_prefetch_config(lib):
     d = lambda rows, cols, i, o, **cfg: R.rowsm_describe_op(
         R.OP_SOFTMAX, rows, cols, i, o, R.RowsmConfig(**cfg))
