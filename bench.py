@@ -11,10 +11,12 @@ regime, in this order (inputs resident in HBM before timing starts):
 
 Between two visits of the same input the other three move more than 3 GB, far
 more than the 256 MB memory-side cache plus L2, so every launch reads x from
-HBM.  Each launch is bracketed by HIP timing events (created without a
-system-scope fence) recorded on the stream it runs on; ``value`` is the
-step's algorithmic bytes (x read once + y written once, summed over the
-regimes) divided by the measured step time.
+HBM.  ``value`` is the step's algorithmic bytes (x read once + y written
+once, summed over the regimes) divided by the step time: the host clock over
+K back-to-back steps between two device synchronisations.  Per-launch times
+come from a separate pass of K steps in which each launch is bracketed by
+HIP timing events (created without a system-scope fence) recorded on the
+stream it runs on.
 
 Before the timed steps the same protocol times the library's streaming copy
 (rowsm_stream_copy) of each regime's bytes, same dtype pair and buffers: a
@@ -476,18 +478,29 @@ def main() -> int:
     # outputs in y for the CPU baseline's parity check.
     cevs = [[[HipEvent() for _ in range(2)] for _ in calls] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for k in range(args.steps):
         copy_step(cevs[k])
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        copy_step()
+    torch.cuda.synchronize()
     copy_wall = time.perf_counter() - t0
 
+    # Per-launch times: the steps with a HIP event pair around each launch.
     evs = [[[HipEvent() for _ in range(2)] for _ in calls]
            for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for k in range(args.steps):
         step(evs[k])
+    torch.cuda.synchronize()
+    # Whole-step throughput: the same steps again, without the per-launch
+    # events (their markers sit between the kernels), timed by the host
+    # clock between two device synchronisations.
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 

@@ -13,6 +13,7 @@
 namespace rowsm {
 
 constexpr int kMaxDevices = 64;
+constexpr int kSplitMaxBlocks = 1 << 20;  // split-form workspace capacity in blocks
 
 // The launch the row launcher chose (fields unused by a family stay default).
 struct Plan {

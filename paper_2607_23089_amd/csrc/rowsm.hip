@@ -803,15 +803,21 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
     } else if (noop) {
       std::snprintf(buf, (size_t)len, "empty: no launch");
     } else {
+      // The split form's grid: one group of S blocks per row up to the
+      // workspace capacity (split_slots()), or a residency sized at launch.
+      int64_t grid = p.grid;
+      const char* how = "grid assumes 256 CUs";
+      if (p.split) {
+        const int64_t groups = kSplitMaxBlocks / p.split;
+        grid = p.grid < 0 ? 0 : (rows < groups ? rows : groups) * p.split;
+        how = p.grid < 0 ? "one residency sized from occupancy at launch"
+                         : "one group of blocks per row";
+      }
       std::snprintf(buf, (size_t)len,
                     "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
                     "split=%d prefetch=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
-                    (int)p.packed, p.u, p.split, (int)p.prefetch, p.block,
-                    (long long)(p.split ? (p.grid < 0 ? 0 : rows * p.split) : p.grid),
-                    p.split ? (p.grid < 0 ? "one residency sized from occupancy at launch"
-                                          : "one group of blocks per row")
-                            : "grid assumes 256 CUs");
+                    (int)p.packed, p.u, p.split, (int)p.prefetch, p.block, (long long)grid, how);
     }
   }
   return st;

@@ -11,8 +11,6 @@
 
 namespace rowsm {
 
-constexpr int kSplitMaxBlocks = 1 << 20;  // workspace capacity in blocks
-
 // Row groups of S blocks in a split launch with occupancy per_cu blocks per
 // compute unit, or 0 when the S blocks of one row cannot be resident at once.
 //   p.grid == 0  one group per row (up to the workspace capacity, beyond

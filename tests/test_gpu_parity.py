@@ -275,6 +275,23 @@ def test_row_count_boundaries(rows, cols, dt):
     assert R.rowsm_split_wait_failures() == 0
 
 
+@pytest.mark.parametrize("din,dout", [("f32", "f32"), ("bf16", "f32")])
+@pytest.mark.parametrize("rows,cols,S", [(20000, 4096, 4), (300000, 256, 4)])
+def test_split_grid_beyond_residency(rows, cols, S, din, dout):
+    # The single-read form launches one group of S blocks per row: with
+    # 64-thread blocks the grid holds far more blocks than the device does at
+    # once (80000 groups' blocks), and past the workspace's 2^20 blocks the
+    # groups loop over the rows (300000 rows x 4 blocks)
+    cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=S, block=64)
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]), cfg)
+    assert st == R.OK and f"split={S}" in desc and f"grid={min(rows, (1 << 20) // S) * S}" in desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + S)
+    y = run(x.to(DEV), dout, config=cfg)
+    assert_parity(x, y, dout, f"split grid {rows}x{cols} S={S} {din}->{dout}")
+    assert R.rowsm_split_wait_failures() == 0
+
+
 @pytest.mark.parametrize("rows,cols", [(4099, 64), (4099, 1000), (4099, 4097)])
 def test_many_rows_grid_stride(rows, cols):
     # more rows than one grid covers in the small and medium families
