@@ -26,9 +26,10 @@
  *   - stream is a hipStream_t (NULL = the legacy default stream).  The call
  *     only enqueues work; results are visible once the caller synchronises the
  *     stream.  Nothing is allocated per call.  The single-read LARGE form
- *     uses a 32 MiB device workspace that the first such call on a device
+ *     uses a 32 MiB device workspace (and a 64 MiB region for captured
+ *     launches, see HIP graphs below) that the first such call on a device
  *     allocates and clears (synchronously) and that lives until the process
- *     ends; make that first call outside stream capture.  Such launches on
+ *     ends; make that first call outside stream capture.  Eager launches on
  *     one device are ordered one after another whatever their streams (each
  *     waits for the previous one through an event), so the workspace is never
  *     shared by two running launches.
@@ -70,12 +71,19 @@ typedef enum {
  * over the rows.
  *
  * HIP graphs: every entry point may be called on a stream that is being
- * captured.  The single-read LARGE form keeps per-launch state on the host
- * (exchange tags), so under capture a LARGE plan uses the two-pass form
- * instead (same results to the stated tolerances, one extra read of each
- * input); a single-read form forced through cfg->split_blocks > 0 returns
- * ROWSM_EINVAL there.  No entry point records a memset or an allocation
- * into a capture. */
+ * captured.  An eager single-read LARGE launch takes its exchange tags from
+ * the host, which a replayed graph cannot do; a captured one instead records
+ * a small epoch kernel before it that advances the tags on the device at
+ * every replay, in a private slice of a per-device 64 MiB capture region (at
+ * most 2^15 blocks per launch; larger launches loop over their rows).  Graph
+ * executables that contain the same captured launch (e.g. two
+ * instantiations of one graph) must not run at the same time.  When no slice
+ * is left, or the region does not exist yet (it is created with the shared
+ * workspace by the first single-read launch outside capture on the device),
+ * a captured LARGE plan uses the two-pass form instead (same results to the
+ * stated tolerances, one extra read of each input), and a single-read form
+ * forced through cfg->split_blocks > 0 returns ROWSM_EINVAL.  No entry point
+ * records a memset or an allocation into a capture. */
 typedef enum {
     ROWSM_AUTO = 0,
     ROWSM_SMALL = 1,
@@ -283,7 +291,8 @@ int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
 
 /*
  * rowsm_split_wait_failures: diagnostics of the single-read LARGE form on
- * the current device.  Waits for the last such launch to finish, then returns
+ * the current device.  Waits for the last eager such launch to finish
+ * (synchronise the streams of graph replays first), then returns
  * how many exchange waits have given up since the workspace was created (0
  * when every row's blocks met; a non-zero count means some rows of some
  * launch are wrong), 0 when no such launch has run, or ROWSM_EHIP.  It

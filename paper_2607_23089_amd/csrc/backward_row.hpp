@@ -208,6 +208,7 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
   const uint32_t sin = (uint32_t)RT * (VW * In::bytes);
   const uint32_t sout = (uint32_t)RT * (VW * Out::bytes);
 
+  tag0 = split_tag0(w, tag0);
   bool gave_up = false;  // per lane of the first wave
   uint32_t k = 0;
   for (int64_t row = q; row < rows; row += slots, ++k) {

@@ -14,6 +14,9 @@ namespace rowsm {
 
 constexpr int kMaxDevices = 64;
 constexpr int kSplitMaxBlocks = 1 << 20;  // split-form workspace capacity in blocks
+// Blocks of one single-read launch recorded under stream capture (the size
+// of its private workspace slice; split_capture_reserve()).
+constexpr int kCaptureMaxBlocks = 1 << 15;
 
 // The launch the row launcher chose (fields unused by a family stay default).
 struct Plan {
@@ -48,6 +51,10 @@ struct Call {
   int mode = kPlain;
   Fused fz{1.0f, 0, 0};
   const void* dy = nullptr;  // softmax backward: x holds y, dy the gradient, y receives dx
+  // Single-read LARGE form on a capturing stream: the launch's private
+  // workspace slice and its capacity in blocks (null when not captured).
+  char* cap_slice = nullptr;
+  int64_t cap_blocks = 0;
 };
 
 // Calls L<In, Out, VW, MODE>::run(c) for the call's dtype pair and vector
@@ -95,5 +102,9 @@ int launch_moe_bf16(const Call& c, int out_dt);
 
 // Split-form diagnostics (launch_split_common.hip).
 int64_t split_wait_failures_current_device();
+// Reserves a private workspace slice for a single-read launch of at most
+// `blocks` blocks recorded under stream capture (launch_split_common.hip).
+// ROWSM_EINVAL when there is no room or no capture region on this device.
+int split_capture_reserve(int64_t blocks, char** slice);
 
 }  // namespace rowsm

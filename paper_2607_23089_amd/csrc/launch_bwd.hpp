@@ -88,12 +88,12 @@ int launch_bwd_split_nv(const Call& c) {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
                                                    p.block, 0) != hipSuccess)
     return ROWSM_EHIP;
-  const int64_t slots = split_slots(p, c.rows, per_cu, c.cus);
+  const int64_t slots = split_slots(c, per_cu);
   if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
   const unsigned grid = (unsigned)(slots * p.split);
 
   SplitTicket t;
-  int r = split_begin(c.st, (uint64_t)((c.rows + slots - 1) / slots), &t);
+  int r = split_begin(c, (uint64_t)((c.rows + slots - 1) / slots), &t);
   if (r != ROWSM_OK) return r;
   (void)hipGetLastError();
   const BwdPtrs<In> in = bwd_inputs<In>(c);

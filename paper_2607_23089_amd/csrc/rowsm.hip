@@ -534,21 +534,32 @@ int launch(const Call& c, int in_dt, int out_dt) {
 // ---- stream capture -------------------------------------------------------------
 //
 // The single-read split form takes exchange tags from the host for every
-// launch; a captured graph would replay one launch's tags, and a replay could
-// then accept words left by the previous replay as its own.  While the launch
-// stream is being captured, long rows therefore take the two-pass form,
-// which keeps no state between launches.  A failed query counts as capture.
+// eager launch; a captured graph would replay one launch's tags, and a replay
+// could then accept words left by the previous replay as its own.  While the
+// launch stream is being captured, a single-read launch therefore gets a
+// private workspace slice whose tags a small epoch kernel, recorded before
+// it, advances on the device at every replay (launch_split_common.hip).
+// Without a slice (the capture region is full, or was never created because
+// no single-read launch has run outside capture on this device) long rows
+// take the two-pass form, which keeps no state between launches, and a
+// single-read form forced by the caller is refused.  A failed query counts
+// as capture.
 bool stream_capturing(hipStream_t s) {
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(s, &cs) != hipSuccess) return true;
   return cs != hipStreamCaptureStatusNone;
 }
 
-// Re-plan a split-form plan as the two-pass form under capture; a split form
-// forced by the caller is refused there.
 template <typename Replan>
-int avoid_split_under_capture(const rowsm_config* cfg, hipStream_t st, Plan* p, Replan replan) {
-  if (p->variant != ROWSM_LARGE || p->split <= 0 || !stream_capturing(st)) return ROWSM_OK;
+int prepare_capture(const rowsm_config* cfg, Call* c, Replan replan) {
+  Plan* p = &c->p;
+  if (p->variant != ROWSM_LARGE || p->split <= 0 || !stream_capturing(c->st)) return ROWSM_OK;
+  const int64_t groups = kCaptureMaxBlocks / p->split;
+  const int64_t blocks = (c->rows < groups ? c->rows : groups) * p->split;
+  if (split_capture_reserve(blocks, &c->cap_slice) == ROWSM_OK) {
+    c->cap_blocks = blocks;
+    return ROWSM_OK;
+  }
   if (cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
   rowsm_config two_pass;
   if (cfg) {
@@ -607,12 +618,6 @@ int backward_impl(const void* yp, const void* dyp, void* dxp, int64_t rows, int6
   const uintptr_t ia = (uintptr_t)yp | (uintptr_t)dyp;
   st = plan_backward(rows, cols, in_dt, out_dt, ia, (uintptr_t)dxp, cfg, c.cus, &c.p);
   if (st != ROWSM_OK) return st;
-  st = avoid_split_under_capture(cfg, static_cast<hipStream_t>(stream), &c.p,
-                                 [&](const rowsm_config* tp) {
-                                   return plan_backward(rows, cols, in_dt, out_dt, ia,
-                                                        (uintptr_t)dxp, tp, c.cus, &c.p);
-                                 });
-  if (st != ROWSM_OK) return st;
   c.x = yp;
   c.dy = dyp;
   c.y = dxp;
@@ -620,6 +625,10 @@ int backward_impl(const void* yp, const void* dyp, void* dxp, int64_t rows, int6
   c.cols = (int)cols;
   c.st = static_cast<hipStream_t>(stream);
   c.mode = kBackward;
+  st = prepare_capture(cfg, &c, [&](const rowsm_config* tp) {
+    return plan_backward(rows, cols, in_dt, out_dt, ia, (uintptr_t)dxp, tp, c.cus, &c.p);
+  });
+  if (st != ROWSM_OK) return st;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   return launch(c, in_dt, out_dt);
 }
@@ -678,12 +687,6 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   c.cus = cu_count();
   st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus, mode, &c.p);
   if (st != ROWSM_OK) return st;
-  st = avoid_split_under_capture(cfg, static_cast<hipStream_t>(stream), &c.p,
-                                 [&](const rowsm_config* tp) {
-                                   return plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x,
-                                                   (uintptr_t)y, tp, c.cus, mode, &c.p);
-                                 });
-  if (st != ROWSM_OK) return st;
   c.x = x;
   c.y = y;
   c.rows = rows;
@@ -691,6 +694,10 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   c.st = static_cast<hipStream_t>(stream);
   c.mode = mode;
   c.fz = fz;
+  st = prepare_capture(cfg, &c, [&](const rowsm_config* tp) {
+    return plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, tp, c.cus, mode, &c.p);
+  });
+  if (st != ROWSM_OK) return st;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   return launch(c, in_dt, out_dt);
 }

@@ -22,28 +22,37 @@ namespace rowsm {
 //                rows than groups that exit.
 //   p.grid < 0   at most -p.grid blocks per compute unit and one full
 //                residency of the device: each group loops over rows.
-inline int64_t split_slots(const Plan& p, int64_t rows, int per_cu, int cus) {
-  if ((int64_t)per_cu * cus < p.split) return 0;
-  int64_t slots = rows;
+//   The grid holds at most the workspace's blocks: kSplitMaxBlocks, or a
+//   captured launch's slice (c.cap_blocks).
+inline int64_t split_slots(const Call& c, int per_cu) {
+  const Plan& p = c.p;
+  if ((int64_t)per_cu * c.cus < p.split) return 0;
+  int64_t slots = c.rows;
   if (p.grid < 0) {
     const int64_t cap = per_cu > -p.grid ? -p.grid : per_cu;
-    slots = cap * cus / p.split;
+    slots = cap * c.cus / p.split;
   }
-  if (slots > rows) slots = rows;
-  if (slots > kSplitMaxBlocks / p.split) slots = kSplitMaxBlocks / p.split;
+  const int64_t max_blocks = c.cap_slice ? c.cap_blocks : kSplitMaxBlocks;
+  if (slots > c.rows) slots = c.rows;
+  if (slots > max_blocks / p.split) slots = max_blocks / p.split;
   return slots;
 }
 
-// A split launch in progress: split_begin takes the device's split lock,
-// orders the launch after the previous split launch on the device (whatever
-// its stream), reserves ntags row tags and hands out the workspace;
-// split_end records the launch for the next one and releases the lock.
+// A split launch in progress.  Eager launches: split_begin takes the
+// device's split lock, orders the launch after the previous split launch on
+// the device (whatever its stream), reserves ntags row tags and hands out the
+// shared workspace; split_end records the launch for the next one and
+// releases the lock.  A launch recorded under capture (c.cap_slice set):
+// split_begin enqueues the slice's epoch kernel, which advances the slice's
+// tags by ntags on every replay, and hands out the slice, whose tag base the
+// kernel reads on the device; split_end has nothing to do.
 struct SplitTicket {
   int dev = -1;
+  bool captured = false;
   SplitWorkspace ws{};
   uint32_t tag0 = 0;
 };
-int split_begin(hipStream_t st, uint64_t ntags, SplitTicket* t);
+int split_begin(const Call& c, uint64_t ntags, SplitTicket* t);
 int split_end(SplitTicket* t, hipStream_t st, bool launched);
 
 template <typename In, typename Out, int VW, int NV, int MODE, bool PIPE>
@@ -54,12 +63,12 @@ int launch_split_nv(const Call& c) {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
                                                    p.block, 0) != hipSuccess)
     return ROWSM_EHIP;
-  const int64_t slots = split_slots(p, c.rows, per_cu, c.cus);
+  const int64_t slots = split_slots(c, per_cu);
   if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
   const unsigned grid = (unsigned)(slots * p.split);
 
   SplitTicket t;
-  int r = split_begin(c.st, (uint64_t)((c.rows + slots - 1) / slots), &t);
+  int r = split_begin(c, (uint64_t)((c.rows + slots - 1) / slots), &t);
   if (r != ROWSM_OK) return r;
   (void)hipGetLastError();
   kern<<<dim3(grid), dim3(p.block), 0, c.st>>>(

@@ -59,7 +59,18 @@ struct SplitWorkspace {
   uint64_t* wm;     // [max_blocks][2]: (tag << 32) | bits(block max)
   uint64_t* ws;     // [max_blocks][2]: (tag << 32) | bits(block sum)
   uint32_t* error;  // [1]: number of waits that gave up
+  // Launches recorded under stream capture: the tag base, written by the
+  // launch's epoch kernel just before it on every replay (the tag0 argument
+  // is then unused); null for eager launches.
+  const uint32_t* dtag;
 };
+
+// Tag base of a launch: the host's, or a captured launch's from its slice.
+__device__ __forceinline__ uint32_t split_tag0(const SplitWorkspace& w, uint32_t tag0) {
+  if (w.dtag == nullptr) return tag0;
+  return __builtin_amdgcn_readfirstlane(
+      __hip_atomic_load(w.dtag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
 
 // Polls before a wait gives up (about a second at the load latency of an
 // agent-scope poll).  A lane that gave up once never waits again in this
@@ -113,6 +124,7 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
   auto row_rsrc = [&](int64_t r) { return make_rsrc(x + r * cols, (uint64_t)cols * In::bytes); };
   auto row_limit = [&](int64_t r) { return FUSED ? fused_limit(fz, r, cols) : cols - 1; };
 
+  tag0 = split_tag0(w, tag0);
   bool gave_up = false;  // per lane of the first wave
   InVec<In, VW> nxt[NV];  // PIPE: the next row's share, in flight
   if constexpr (PIPE) {

@@ -1,9 +1,13 @@
 """Every entry point captured into a HIP graph (torch.cuda.graph) and
 replayed several times, with new inputs written eagerly and the device
 synchronised between replays; every replay is checked against the fp64
-oracle with the operation's tolerance.  Long rows take the two-pass form
-under capture (the single-read form keeps per-launch host state); forcing the
-single-read form there is refused."""
+oracle with the operation's tolerance.  Long rows keep the single-read split
+form under capture (a private workspace slice whose tags an epoch kernel
+recorded before each launch advances at every replay): captured replays are
+bitwise equal to eager launches of the same plan, also with eager split
+launches and other graphs' replays in between.  When the capture region is
+full, long rows take the two-pass form and a forced split form is refused.
+"""
 import numpy as np
 import pytest
 import torch
@@ -129,9 +133,112 @@ def test_moe_graph_replays():
     replay_and_check(g, lambda i: s.copy_(src[i].to(DEV)), check)
 
 
-def test_forced_split_form_refused_under_capture():
+def eager_split_launch():
+    # the first single-read launch outside capture creates the workspaces
+    x = torch.zeros(2, 262144, device=DEV)
+    R.softmax(x, variant=R.LARGE)
+    torch.cuda.synchronize()
+
+
+SPLIT_CASES = [  # (op, rows, cols, din, dout)
+    ("softmax", 300, 65540, "f32", "f32"),
+    ("softmax", 64, 151936, "bf16", "f32"),
+    ("log_softmax", 24, 262144, "f32", "bf16"),
+    ("backward", 64, 262144, "f32", "f32"),
+    ("backward", 40, 151936, "bf16", "bf16"),
+]
+
+
+def split_case(op, rows, cols, din, dout, seed):
+    """Buffers, a launch closure and a refill for one single-read case."""
+    x = torch.empty(rows, cols, dtype=DT[din], device=DEV)
+    dy = torch.empty_like(x)
+    y = torch.empty(rows, cols, dtype=DT[dout], device=DEV)
+
+    def run(out=y, stream=None):
+        if op == "softmax":
+            R.softmax(x, out=out, stream=stream)
+        elif op == "log_softmax":
+            R.log_softmax(x, out=out, stream=stream)
+        else:
+            R.softmax_backward(x, dy, out=out, stream=stream)
+
+    def refill(i):
+        if op == "backward":
+            x.copy_(W.random_probabilities(rows, cols, din, 0.1, seed=seed + i).to(DEV))
+            dy.copy_(W.random_matrix(rows, cols, din, seed=seed + 50 + i).to(DEV))
+        else:
+            x.copy_(W.random_matrix(rows, cols, din, sigma=4.0, seed=seed + i).to(DEV))
+
+    return x, dy, y, run, refill
+
+
+@pytest.mark.parametrize("op,rows,cols,din,dout", SPLIT_CASES)
+def test_captured_split_form_matches_eager(op, rows, cols, din, dout):
+    eager_split_launch()
+    code = {"softmax": R.OP_SOFTMAX, "log_softmax": R.OP_LOG_SOFTMAX,
+            "backward": R.OP_SOFTMAX_BACKWARD}[op]
+    st, desc = R.rowsm_describe_op(code, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and "split=" in desc and "split=0" not in desc, desc
+    x, dy, y, run, refill = split_case(op, rows, cols, din, dout, seed=rows + cols)
+    refill(0)
+    g = capture(run)
+    side = torch.cuda.Stream()
+    y_eager = torch.empty_like(y)
+    for i in range(4):
+        refill(i)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):          # eager split launch, shared workspace
+            run(out=y_eager, stream=side)
+        side.synchronize()
+        assert torch.equal(y.view(torch.int16 if dout == "bf16" else torch.int32),
+                           y_eager.view(torch.int16 if dout == "bf16" else torch.int32)), \
+            f"{op} {rows}x{cols} replay {i}: captured single-read launch differs from eager"
+    # and the last replay against the oracle
+    xw = widen(x.cpu())
+    if op == "softmax":
+        res = compare(out_np(y, dout), oracle.softmax_f64(xw, threads=4), dout)
+    elif op == "log_softmax":
+        res = compare_log(out_np(y, dout), oracle.log_softmax_f64(xw, threads=4), dout)
+    else:
+        dyw = widen(dy.cpu())
+        res = compare_backward(out_np(y, dout), oracle.softmax_backward_f64(xw, dyw, threads=4),
+                               xw, dyw, dout)
+    assert res["ok"], f"{op} {rows}x{cols}: {res}"
+    assert R.rowsm_split_wait_failures() == 0
+
+
+def test_two_graphs_with_split_launches_alternate():
+    eager_split_launch()
+    a = split_case("softmax", 64, 151936, "bf16", "f32", seed=7)
+    b = split_case("backward", 64, 262144, "f32", "f32", seed=9)
+    ga, gb = None, None
+    a[4](0)
+    b[4](0)
+    ga, gb = capture(a[3]), capture(b[3])
+    for i in range(6):
+        a[4](i)
+        b[4](i)
+        torch.cuda.synchronize()
+        (ga if i % 2 == 0 else gb).replay()
+        (gb if i % 2 == 0 else ga).replay()
+        torch.cuda.synchronize()
+        for x, dy, y, run, _ in (a, b):
+            ref = torch.empty_like(y)
+            run(out=ref)
+            torch.cuda.synchronize()
+            assert torch.equal(y, ref), f"alternating graphs, round {i}"
+    assert R.rowsm_split_wait_failures() == 0
+
+
+def test_forced_split_form_under_capture():
+    eager_split_launch()
     x = torch.zeros(4, 262144, device=DEV)
     y = torch.empty_like(x)
+    y2 = torch.empty_like(x)
     statuses = []
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
@@ -139,9 +246,52 @@ def test_forced_split_form_refused_under_capture():
         cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=8)
         statuses.append(R.rowsm_forward_config(x.data_ptr(), y.data_ptr(), 4, 262144,
                                                R.F32, R.F32, sh, cfg))
-        statuses.append(R.rowsm_forward(x.data_ptr(), y.data_ptr(), 4, 262144,
+        statuses.append(R.rowsm_forward(x.data_ptr(), y2.data_ptr(), 4, 262144,
                                         R.F32, R.F32, sh))
-    assert statuses == [R.EINVAL, R.OK]
-    g.replay()
-    torch.cuda.synchronize()
-    assert torch.allclose(y, torch.full_like(y, 1.0 / 262144))
+    assert statuses == [R.OK, R.OK]
+    for _ in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.allclose(y, torch.full_like(y, 1.0 / 262144))
+        assert torch.allclose(y2, torch.full_like(y2, 1.0 / 262144))
+    assert R.rowsm_split_wait_failures() == 0
+
+
+def test_zz_capture_region_exhausted_falls_back():
+    # Runs last in this file: it fills the per-device capture region (64 MiB,
+    # 1 MiB per captured 2^15-block launch).  A forced single-read launch is
+    # then refused under capture and the launcher's own plan takes the
+    # two-pass form, whose replays stay exact.
+    eager_split_launch()
+    rows, cols = 4096, 4096
+    x = torch.zeros(rows, cols, device=DEV)
+    y = torch.empty_like(x)
+    cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=8, block=64)
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.F32, R.F32, cfg)
+    assert st == R.OK and "grid=32768" in desc
+    refused_at = None
+    for k in range(80):
+        status = []
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            status.append(R.rowsm_forward_config(x.data_ptr(), y.data_ptr(), rows, cols, R.F32,
+                                                 R.F32, torch.cuda.current_stream().cuda_stream,
+                                                 cfg))
+        if status[0] == R.EINVAL:
+            refused_at = k
+            break
+        assert status[0] == R.OK
+        del g
+    assert refused_at is not None and refused_at <= 64, refused_at
+    # the launcher's own plan for long rows still captures (two-pass form)
+    xs = [W.random_matrix(8, 262144, "f32", sigma=4.0, seed=60 + i) for i in range(3)]
+    xl = torch.empty(8, 262144, device=DEV)
+    yl = torch.empty_like(xl)
+    xl.copy_(xs[0].to(DEV))
+    g = capture(lambda: R.softmax(xl, out=yl))
+
+    def check(i):
+        res = compare(out_np(yl, "f32"), oracle.softmax_f64(widen(xs[i]), threads=4), "f32")
+        assert res["ok"], f"two-pass fallback replay {i}: {res}"
+
+    replay_and_check(g, lambda i: xl.copy_(xs[i].to(DEV)), check)
