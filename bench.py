@@ -18,6 +18,9 @@ come from a separate pass of K steps in which each launch is bracketed by
 HIP timing events (created without a system-scope fence) recorded on the
 stream it runs on.
 
+The same four launches are also captured into one HIP graph and replayed
+(``graph_step``).
+
 Before the timed steps the same protocol times the library's streaming copy
 (rowsm_stream_copy) of each regime's bytes, same dtype pair and buffers: a
 plain copy moving the same bytes in the same run, reported per launch as
@@ -579,6 +582,37 @@ def main() -> int:
         },
         "regimes_detail": per,
     }
+    # The same step captured into a HIP graph and replayed (the single-read
+    # form keeps its one-read plan under capture).
+    graph_leg = None
+    if not args.no_next:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            sh_cap = side.cuda_stream
+            for name, w, xp, yp, di, do in calls:
+                st = R.rowsm_forward(xp, yp, w.rows, w.cols, di, do, sh_cap)
+                if st != R.OK:
+                    raise R.RowsmError(f"capture {name}: status {st}")
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        gwall = time.perf_counter() - t0
+        graph_leg = {"what": "the step's four launches captured into one HIP graph, "
+                             "replayed back to back",
+                     "GBps": step_bytes / (gwall / args.steps) / 1e9,
+                     "ms_per_step": gwall / args.steps * 1e3}
+        del g
+        if R.rowsm_split_wait_failures() != 0:
+            raise R.RowsmError("split-row exchange waits gave up under graph replay")
+    if graph_leg is not None:
+        result["graph_step"] = graph_leg
     if not args.no_next:
         result["context"] = copy_ceiling()
         result["next_rows"] = {"fused_scale_causal": fused_causal_leg(reps=10),
