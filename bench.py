@@ -43,6 +43,10 @@ sys.path.insert(0, ROOT)
 
 METRIC = "row-softmax achieved HBM GB/s and % of MI355X peak, per row-length regime"
 PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
+# Bandwidth targets per regime, as fractions of the HBM peak: at least 60%
+# for the small-row regime, 80% for medium and long rows.
+TARGET_FRAC = {"small_262144x64": 0.60, "causal_32768x4096": 0.80,
+               "large_1024x262144": 0.80, "vocab_4096x151936": 0.80}
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 # Device code each kernel family is compiled from; a profile entry records the
 # hash of its family's sources and the launch's shape.
@@ -529,6 +533,9 @@ def main() -> int:
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
             "hbm_bytes_per_launch": measured_traffic(name, desc),
             "copy_us": cavg * 1e3, "copy_GBps": cgbs, "ratio_to_copy": gbs / cgbs,
+            "target_frac_of_peak": TARGET_FRAC.get(name),
+            "meets_target": (gbs / PEAK_HBM_GBS >= TARGET_FRAC[name]) if name in TARGET_FRAC
+            else None,
         }
     failures = R.rowsm_split_wait_failures()
     if failures != 0:
@@ -558,7 +565,9 @@ def main() -> int:
             "regimes": {n: {"GBps": round(v["GBps"], 1),
                             "frac_of_peak": round(v["frac_of_peak"], 4),
                             "avg_us": round(v["avg_us"], 2), "kernel": v["kernel"],
-                            "ratio_to_copy": round(v["ratio_to_copy"], 4)}
+                            "ratio_to_copy": round(v["ratio_to_copy"], 4),
+                            "target_frac_of_peak": v["target_frac_of_peak"],
+                            "meets_target": v["meets_target"]}
                         for n, v in per.items()},
         },
         "roofline": {
