@@ -281,8 +281,12 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
 // ---- longest rows: two passes ----------------------------------------------------
 //
 // One block per row.  Pass 1 accumulates d over tiles of T * U vector pairs
-// (a tile's partial on its own, then added to the running sum); pass 2
-// reads the row pair again, last tile first, and writes dx.
+// (a tile's partial on its own, then added to the running sum with a Kahan
+// compensation term, as the forward two-pass form does: up to 2^16 tile
+// partials per thread on the longest rows); pass 2 reads the row pair again,
+// last tile first, and writes dx.  An infinite running sum drops the
+// compensation, so d keeps IEEE semantics (+-inf, or NaN from inf - inf or a
+// NaN term).
 template <typename In, typename Out, int VW, int U>
 __global__ __launch_bounds__(1024) void bwd_large_kernel(
     const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
@@ -305,7 +309,7 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
     const rsrc_t rdy = make_rsrc(dy + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t rdx = make_rsrc(dx + row * cols, (uint64_t)cols * Out::bytes);
 
-    float d = 0.0f;
+    float d = 0.0f, cd = 0.0f;  // running sum and its compensation
     for (int tt = 0; tt < ntiles; ++tt) {
       InVec<In, VW> a[U], b[U];
       const bool full = tt < ntiles - 1;
@@ -324,8 +328,12 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
       float ts = 0.0f;
 #pragma unroll
       for (int u = 0; u < U; ++u) ts = dot_vec(a[u], b[u], ts);
-      d += ts;
+      const float yk = ts - cd;
+      const float t = d + yk;
+      cd = __builtin_isfinite(t) ? (t - d) - yk : 0.0f;
+      d = t;
     }
+    d -= cd;
     d = group_reduce<kWave, SumOp>(d);
     if (lane == 0) red[wave] = d;
     __syncthreads();

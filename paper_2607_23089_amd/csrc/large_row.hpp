@@ -5,8 +5,11 @@
 // wave reads 64 consecutive vectors).  Pass 1 keeps a running (max, sum) per
 // thread: for each tile it takes the tile maximum M' = max(m, tile max),
 // rescales the running sum by exp(m - M') and adds exp(x - M') for the tile's
-// entries.  The per-thread pairs are merged across the wave with DPP/permlane
-// steps and across waves through LDS.  Pass 2 reads the row again, last tile
+// entries.  The running sum carries a compensation term (Kahan summation):
+// a thread adds one tile sum per tile, up to 2^16 of them on the longest rows,
+// and near-equal addends would otherwise round the same way at every step, an
+// error that grows with their count.  The per-thread pairs are merged across
+// the wave with DPP/permlane steps and across waves through LDS.  Pass 2 reads the row again, last tile
 // first so that the most recently fetched tiles are re-read while they are
 // most likely still cached, and writes exp(x - m) / sum.
 //
@@ -53,8 +56,9 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
     const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * Out::bytes);
     const int lim = FUSED ? fused_limit(fz, row, cols) : cols - 1;
 
-    // Pass 1: running (max, sum).
-    float m = ninf, s = 0.0f;
+    // Pass 1: running (max, sum); c is the compensation of s (the sum is
+    // s - c).
+    float m = ninf, s = 0.0f, c = 0.0f;
     for (int tt = 0; tt < ntiles; ++tt) {
       float f[U][VW];
       {
@@ -95,11 +99,18 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
           for (int i = 0; i < VW; ++i)
             ts += exp2_fast(__builtin_fmaf(f[u][i], kLog2e, nml));
       }
-      s = rescale(s, m, M) + ts;
+      if (M != m) {
+        s = rescale(s, m, M);
+        c = rescale(c, m, M);
+      }
+      const float yk = ts - c;
+      const float t = s + yk;
+      c = (t - s) - yk;
+      s = t;
       m = M;
     }
 
-    MaxSum ms = group_merge<kWave>({m, s});
+    MaxSum ms = group_merge<kWave>({m, s - c});
     if (lane == 0) {
       red_m[wave] = ms.m;
       red_s[wave] = ms.s;

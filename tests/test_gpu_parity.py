@@ -292,6 +292,62 @@ def test_split_grid_beyond_residency(rows, cols, S, din, dout):
     assert R.rowsm_split_wait_failures() == 0
 
 
+@pytest.mark.parametrize("rows,din,dout", [(1, "f32", "f32"), (3, "bf16", "bf16"),
+                                           (2, "bf16", "f32")])
+def test_maximum_row_length(rows, din, dout):
+    # cols = 2^30 - 1, the longest row the ABI accepts (offsets inside a row
+    # are 32-bit byte offsets; a 4 GiB - 4 byte fp32 row); with several rows
+    # the row bases lie past 4 GiB.  Closed form: zeros with one 1.0 per row
+    # at a seeded column, so y = e^-1 / s at the zeros and 1 / s at the one,
+    # s = (cols - 1) e^-1 + 1 (the rows' fp32 sums run over 2^30 terms).
+    import math
+    cols = (1 << 30) - 1
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("large"), desc
+    assert R.rowsm_forward(0, 0, 1, 1 << 30, R.F32, R.F32, 0) == R.EINVAL  # one past the limit
+    x = torch.zeros(rows, cols, dtype=DT[din], device=DEV)
+    pos = [(r * 2654435761 + 12345) % cols for r in range(rows)]
+    for r, p in enumerate(pos):
+        x[r, p] = 1.0
+    y = torch.empty(rows, cols, dtype=DT[dout], device=DEV)
+    R.softmax(x, out=y)
+    torch.cuda.synchronize()
+    ssum = (cols - 1) * math.exp(-1.0) + 1.0
+    v0, v1 = math.exp(-1.0) / ssum, 1.0 / ssum
+    got, want = [], []
+    for r, p in enumerate(pos):
+        row = y[r]
+        got.append(row[p].double().item())
+        want.append(v1)
+        for part in (row[:p], row[p + 1:]):
+            if part.numel():
+                got += [part.min().double().item(), part.max().double().item()]
+                want += [v0, v0]
+    del x, y
+    torch.cuda.empty_cache()
+    res = compare(np.array(got), np.array(want), dout)
+    assert res["ok"], f"max row length {rows}x{cols} {din}->{dout} [{desc}]: {res} {got}"
+
+
+@pytest.mark.parametrize("rows,din,dout,cols,want", [
+    (2, "f32", "f32", 1 << 21, "split=64"),            # 64 blocks x 512 x 64 values
+    (2, "f32", "f32", (1 << 21) + 4, "split=0"),        # one vector more: two passes
+    (2, "bf16", "bf16", 1 << 21, "split=64"),
+    (2, "bf16", "f32", 64 * 512 * 40, "split=64"),      # widening: 40 values per lane
+    (2, "bf16", "f32", 64 * 512 * 40 + 4, "split=0"),
+    (65, "bf16", "bf16", 196608, "packed=1"),           # packed medium: 24 slots x 1024
+    (65, "bf16", "bf16", 196616, "large"),
+])
+def test_form_capacity_limits(rows, din, dout, cols, want):
+    # the largest rows each register-resident form holds, and one vector more
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and want in desc, desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols)
+    y = run(x.to(DEV), dout)
+    assert_parity(x, y, dout, f"capacity {rows}x{cols} {din}->{dout} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0
+
+
 @pytest.mark.parametrize("rows,cols", [(4099, 64), (4099, 1000), (4099, 4097)])
 def test_many_rows_grid_stride(rows, cols):
     # more rows than one grid covers in the small and medium families
