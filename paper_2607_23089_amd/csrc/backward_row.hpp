@@ -10,7 +10,8 @@
 //   medium  one row per group of WPR waves, the row pair held in registers;
 //   split   one row over S co-resident blocks that exchange block partial
 //           sums of d (split_row.hpp's protocol, one word per block);
-//   large   two streaming passes (dot, then dx) for rows longer than that.
+//   large   two streaming passes (dot, then dx) for rows longer than that,
+//           over S >= 1 blocks per row.
 // The register-resident forms keep y and dy in their raw input form (bf16
 // pairs take half the registers) and widen each element where it is used,
 // so one read of each input suffices.  The raw words are hidden from the
@@ -249,21 +250,7 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
         __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(db),
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       float p = 0.0f;
-      if (lane < S) {
-        const uint32_t i = 2 * (b0 + lane) + slot;
-        uint64_t v = 0;
-        uint32_t spins = 0;
-        while (!gave_up) {
-          v = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if ((v & ~0xffffffffull) == tag) break;
-          __builtin_amdgcn_s_sleep(1);
-          if (++spins == kSplitSpinLimit) {
-            __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            gave_up = true;
-          }
-        }
-        p = __uint_as_float((uint32_t)v);
-      }
+      if (lane < S) p = split_poll_word(w, b0 + lane, slot, tag, &gave_up);
       p = group_reduce<kWave, SumOp>(p);  // fixed lane order: deterministic
       if (lane == 0) bcast = p;
     }
@@ -280,31 +267,44 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
 
 // ---- longest rows: two passes ----------------------------------------------------
 //
-// One block per row.  Pass 1 accumulates d over tiles of T * U vector pairs
+// The two-pass form of the forward (large_row.hpp) for the gradient: S >= 1
+// blocks per row with the same layout (global thread g = c * T + t reads the
+// vector pairs g + j * S * T, U per tile).  Pass 1 accumulates d over tiles
 // (a tile's partial on its own, then added to the running sum with a Kahan
-// compensation term, as the forward two-pass form does: up to 2^16 tile
-// partials per thread on the longest rows); pass 2 reads the row pair again,
-// last tile first, and writes dx.  An infinite running sum drops the
-// compensation, so d keeps IEEE semantics (+-inf, or NaN from inf - inf or a
-// NaN term).
+// compensation term: up to 2^16 tile partials per thread on the longest
+// rows); with S > 1 the blocks exchange their partial d once (one tagged
+// word each, as bwd_split_kernel) and sum them in block order.  Pass 2 reads
+// the block's share again, last tile first, and writes dx.  An infinite
+// running sum drops the compensation, so d keeps IEEE semantics (+-inf, or
+// NaN from inf - inf or a NaN term).
 template <typename In, typename Out, int VW, int U>
 __global__ __launch_bounds__(1024) void bwd_large_kernel(
     const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
-    typename Out::storage* __restrict__ dx, int64_t rows, int cols) {
+    typename Out::storage* __restrict__ dx, int64_t rows, int cols, int S, SplitWorkspace w,
+    uint32_t tag0) {
   __shared__ float red[16];
+  __shared__ float bcast;
 
   const int T = blockDim.x;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
+  const int wave = wave_id();
   const int nwaves = T / kWave;
+  const int c = blockIdx.x % S;
+  const int q = blockIdx.x / S;
+  const int64_t slots = gridDim.x / S;
+  const int RT = S * T;
+  const int g = c * T + tid;
   const int nvec = cols / VW;
-  const int tile = T * U;
-  const int ntiles = (nvec + tile - 1) / tile;
-  const uint32_t vin = (uint32_t)tid * (VW * In::bytes);
-  const uint32_t vout = (uint32_t)tid * (VW * Out::bytes);
+  const int per_thread = (nvec + RT - 1) / RT;
+  const int ntiles = (per_thread + U - 1) / U;
+  const uint32_t vin = (uint32_t)g * (VW * In::bytes);
+  const uint32_t vout = (uint32_t)g * (VW * Out::bytes);
+  if (S > 1) tag0 = split_tag0(w, tag0);
+  bool gave_up = false;  // per lane of the first wave
 
-  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+  uint32_t k = 0;
+  for (int64_t row = q; row < rows; row += slots, ++k) {
     const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t rdy = make_rsrc(dy + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t rdx = make_rsrc(dx + row * cols, (uint64_t)cols * Out::bytes);
@@ -312,12 +312,11 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
     float d = 0.0f, cd = 0.0f;  // running sum and its compensation
     for (int tt = 0; tt < ntiles; ++tt) {
       InVec<In, VW> a[U], b[U];
-      const bool full = tt < ntiles - 1;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int idx = tt * tile + u * T + tid;
-        const uint32_t so = (uint32_t)(tt * tile + u * T) * (VW * In::bytes);
-        if (full || idx < nvec) {
+        const int j = (tt * U + u) * RT;
+        const uint32_t so = (uint32_t)j * (VW * In::bytes);
+        if (j + g < nvec) {
           a[u].load(ry, vin, so);
           b[u].load(rdy, vin, so);
         } else {
@@ -339,16 +338,32 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
     __syncthreads();
     d = red[0];
     for (int i = 1; i < nwaves; ++i) d += red[i];
-    __syncthreads();  // every wave has read red before the next row
+
+    if (S > 1) {
+      if (wave == 0) {
+        const uint32_t b0 = (uint32_t)q * S;
+        const uint64_t tag = (uint64_t)(tag0 + k) << 32;
+        const uint32_t slot = k & 1;
+        if (lane == 0)
+          __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(d),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        float p = 0.0f;
+        for (int bb = lane; bb < S; bb += kWave) p += split_poll_word(w, b0 + bb, slot, tag,
+                                                                      &gave_up);
+        p = group_reduce<kWave, SumOp>(p);  // fixed lane order: deterministic
+        if (lane == 0) bcast = p;
+      }
+      __syncthreads();
+      d = bcast;
+    }
 
     for (int tt = ntiles - 1; tt >= 0; --tt) {
       InVec<In, VW> a[U], b[U];
-      const bool full = tt < ntiles - 1;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int idx = tt * tile + u * T + tid;
-        const uint32_t so = (uint32_t)(tt * tile + u * T) * (VW * In::bytes);
-        if (full || idx < nvec) {
+        const int j = (tt * U + u) * RT;
+        const uint32_t so = (uint32_t)j * (VW * In::bytes);
+        if (j + g < nvec) {
           a[u].load(ry, vin, so);
           b[u].load(rdy, vin, so);
         } else {
@@ -358,13 +373,15 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int idx = tt * tile + u * T + tid;
+        const int j = (tt * U + u) * RT;
         float o[VW];
         grad_vec(a[u], b[u], d, o);
-        if (full || idx < nvec)
-          store_out<Out, VW>(rdx, vout + (uint32_t)(tt * tile + u * T) * (VW * Out::bytes), o);
+        if (j + g < nvec)
+          store_out<Out, VW>(rdx, vout + (uint32_t)j * (VW * Out::bytes), o);
       }
     }
+    // Every wave has read red and bcast before the next row rewrites them.
+    __syncthreads();
   }
 }
 

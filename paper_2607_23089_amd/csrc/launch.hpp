@@ -17,6 +17,11 @@ constexpr int kSplitMaxBlocks = 1 << 20;  // split-form workspace capacity in bl
 // Blocks of one single-read launch recorded under stream capture (the size
 // of its private workspace slice; split_capture_reserve()).
 constexpr int kCaptureMaxBlocks = 1 << 15;
+// Blocks per row of the two-pass LARGE form at most (and at most the compute
+// units: all of a row's blocks must be resident at once, and a 1024-thread
+// block of it may take a whole compute unit's registers).  Wave 0 of a
+// block polls up to 4 peers per lane in its exchange.
+constexpr int kStreamMaxSplit = 256;
 
 // The launch the row launcher chose (fields unused by a family stay default).
 struct Plan {
@@ -31,6 +36,7 @@ struct Plan {
   // LARGE
   int u = 4;
   int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
+  int stream = 1;   // two-pass form: blocks per row (1: one block per row)
   bool prefetch = false;  // single-read form: load the next row during the exchange
   // launch
   int block = 256;
@@ -51,7 +57,8 @@ struct Call {
   int mode = kPlain;
   Fused fz{1.0f, 0, 0};
   const void* dy = nullptr;  // softmax backward: x holds y, dy the gradient, y receives dx
-  // Single-read LARGE form on a capturing stream: the launch's private
+  // LARGE forms that exchange between blocks (single-read, or two-pass with
+  // more than one block per row) on a capturing stream: the launch's private
   // workspace slice and its capacity in blocks (null when not captured).
   char* cap_slice = nullptr;
   int64_t cap_blocks = 0;

@@ -82,27 +82,13 @@ struct BwdMediumLaunch {
 
 template <typename In, typename Out, int VW, int NV>
 int launch_bwd_split_nv(const Call& c) {
-  const Plan& p = c.p;
   auto kern = bwd_split_kernel<In, Out, VW, NV>;
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
-                                                   p.block, 0) != hipSuccess)
-    return ROWSM_EHIP;
-  const int64_t slots = split_slots(c, per_cu);
-  if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
-  const unsigned grid = (unsigned)(slots * p.split);
-
-  SplitTicket t;
-  int r = split_begin(c, (uint64_t)((c.rows + slots - 1) / slots), &t);
-  if (r != ROWSM_OK) return r;
-  (void)hipGetLastError();
   const BwdPtrs<In> in = bwd_inputs<In>(c);
-  kern<<<dim3(grid), dim3(p.block), 0, c.st>>>(in.y, in.dy,
-                                               static_cast<typename Out::storage*>(c.y), c.rows,
-                                               c.cols, p.split, t.ws, t.tag0);
-  const bool launched = hipGetLastError() == hipSuccess;
-  r = split_end(&t, c.st, launched);
-  return launched ? r : ROWSM_EHIP;
+  return launch_exchanging(c, kern, c.p.split, [&](unsigned grid, SplitWorkspace ws, uint32_t tag0) {
+    kern<<<dim3(grid), dim3(c.p.block), 0, c.st>>>(in.y, in.dy,
+                                                  static_cast<typename Out::storage*>(c.y),
+                                                  c.rows, c.cols, c.p.split, ws, tag0);
+  });
 }
 
 template <typename In, typename Out, int VW, int... NVs>
@@ -124,21 +110,33 @@ struct BwdSplitLaunch {
   }
 };
 
+// Two-pass backward: one block per row (p.stream == 1, grid p.grid), or
+// p.stream blocks per row that exchange their partial dot products.
+template <typename In, typename Out, int VW, int U>
+int launch_bwd_large_u(const Call& c) {
+  auto kern = bwd_large_kernel<In, Out, VW, U>;
+  const BwdPtrs<In> in = bwd_inputs<In>(c);
+  auto dxp = static_cast<typename Out::storage*>(c.y);
+  if (c.p.stream <= 1) {
+    (void)hipGetLastError();
+    kern<<<dim3((unsigned)c.p.grid), dim3(c.p.block), 0, c.st>>>(in.y, in.dy, dxp, c.rows,
+                                                                  c.cols, 1, SplitWorkspace{}, 0);
+    return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+  }
+  return launch_exchanging(c, kern, c.p.stream, [&](unsigned grid, SplitWorkspace ws,
+                                                    uint32_t tag0) {
+    kern<<<dim3(grid), dim3(c.p.block), 0, c.st>>>(in.y, in.dy, dxp, c.rows, c.cols, c.p.stream,
+                                                  ws, tag0);
+  });
+}
+
 template <typename In, typename Out, int VW, int MODE>
 struct BwdLargeLaunch {
   static int run(const Call& c) {
-    const BwdPtrs<In> in = bwd_inputs<In>(c);
-    auto dxp = static_cast<typename Out::storage*>(c.y);
-    const dim3 g((unsigned)c.p.grid), b(c.p.block);
-    if (c.p.u == 2)
-      bwd_large_kernel<In, Out, VW, 2><<<g, b, 0, c.st>>>(in.y, in.dy, dxp, c.rows, c.cols);
-    else if (c.p.u == 4)
-      bwd_large_kernel<In, Out, VW, 4><<<g, b, 0, c.st>>>(in.y, in.dy, dxp, c.rows, c.cols);
-    else if (c.p.u == 8)
-      bwd_large_kernel<In, Out, VW, 8><<<g, b, 0, c.st>>>(in.y, in.dy, dxp, c.rows, c.cols);
-    else
-      return ROWSM_EINVAL;
-    return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+    if (c.p.u == 2) return launch_bwd_large_u<In, Out, VW, 2>(c);
+    if (c.p.u == 4) return launch_bwd_large_u<In, Out, VW, 4>(c);
+    if (c.p.u == 8) return launch_bwd_large_u<In, Out, VW, 8>(c);
+    return ROWSM_EINVAL;
   }
 };
 

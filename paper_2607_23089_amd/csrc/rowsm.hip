@@ -134,6 +134,20 @@ int few_rows_split(int64_t rows, int64_t nvec, int T, int nv_cap, int cus) {
   return sf;
 }
 
+// Blocks per row of the two-pass LARGE form: 1 for launches of at least
+// 2 * cus rows, or with a grid capped per compute unit (bpc); otherwise the
+// power of two that gives the launch about two blocks per compute unit, at
+// most kStreamMaxSplit and the compute units, and at most what leaves every
+// thread U vectors of the row.  One block per row would leave a launch of
+// few such rows on a few compute units.
+int stream_blocks(int64_t rows, int64_t nvec, int T, int U, int bpc, int cus) {
+  if (bpc || rows >= 2 * (int64_t)cus) return 1;
+  int S = 1;
+  while (S * 2 <= kStreamMaxSplit && S * 2 <= cus && rows * S < 2 * (int64_t)cus) S *= 2;
+  while (S > 1 && (int64_t)S * T * U > nvec) S >>= 1;
+  return S;
+}
+
 // Forward plan: fills p for the family cfg asks for (AUTO resolves first)
 // and the config overrides; returns ROWSM_OK, or ROWSM_EINVAL when the family
 // cannot take this shape.  mode is the output form (kPlain, kFused or kLog);
@@ -323,6 +337,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
     const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
     p->grid = rows < cap ? rows : cap;
+    p->stream = stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
     return ROWSM_OK;
   }
   return ROWSM_EINVAL;
@@ -449,6 +464,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
     const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
     p->grid = rows < cap ? rows : cap;
+    p->stream = stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
     return ROWSM_OK;
   }
   return ROWSM_EINVAL;
@@ -553,14 +569,17 @@ bool stream_capturing(hipStream_t s) {
 template <typename Replan>
 int prepare_capture(const rowsm_config* cfg, Call* c, Replan replan) {
   Plan* p = &c->p;
-  if (p->variant != ROWSM_LARGE || p->split <= 0 || !stream_capturing(c->st)) return ROWSM_OK;
-  const int64_t groups = kCaptureMaxBlocks / p->split;
-  const int64_t blocks = (c->rows < groups ? c->rows : groups) * p->split;
+  const int S = p->split > 0 ? p->split : p->stream;
+  if (p->variant != ROWSM_LARGE || S <= 1 || !stream_capturing(c->st)) return ROWSM_OK;
+  const int64_t groups = kCaptureMaxBlocks / S;
+  const int64_t blocks = (c->rows < groups ? c->rows : groups) * S;
   if (split_capture_reserve(blocks, &c->cap_slice) == ROWSM_OK) {
     c->cap_blocks = blocks;
     return ROWSM_OK;
   }
   if (cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
+  // The two-pass form with one block per row keeps no state between
+  // launches (a grid cap of one block per compute unit, unless given).
   rowsm_config two_pass;
   if (cfg) {
     two_pass = *cfg;
@@ -570,6 +589,7 @@ int prepare_capture(const rowsm_config* cfg, Call* c, Replan replan) {
   }
   two_pass.variant = ROWSM_LARGE;
   two_pass.split_blocks = -1;
+  if (two_pass.blocks_per_cu <= 0) two_pass.blocks_per_cu = 1;
   return replan(&two_pass);
 }
 
@@ -814,17 +834,19 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
       // workspace capacity (split_slots()), or a residency sized at launch.
       int64_t grid = p.grid;
       const char* how = "grid assumes 256 CUs";
-      if (p.split) {
-        const int64_t groups = kSplitMaxBlocks / p.split;
-        grid = p.grid < 0 ? 0 : (rows < groups ? rows : groups) * p.split;
+      const int S = p.split > 0 ? p.split : (p.variant == ROWSM_LARGE ? p.stream : 1);
+      if (S > 1 || p.split > 0) {
+        const int64_t groups = kSplitMaxBlocks / S;
+        grid = p.grid < 0 ? 0 : (rows < groups ? rows : groups) * S;
         how = p.grid < 0 ? "one residency sized from occupancy at launch"
                          : "one group of blocks per row";
       }
       std::snprintf(buf, (size_t)len,
                     "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
-                    "split=%d prefetch=%d block=%d grid=%lld (%s)",
+                    "split=%d stream=%d prefetch=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
-                    (int)p.packed, p.u, p.split, (int)p.prefetch, p.block, (long long)grid, how);
+                    (int)p.packed, p.u, p.split, p.variant == ROWSM_LARGE && !p.split ? p.stream : 0,
+                    (int)p.prefetch, p.block, (long long)grid, how);
     }
   }
   return st;

@@ -24,17 +24,19 @@ namespace rowsm {
 //                residency of the device: each group loops over rows.
 //   The grid holds at most the workspace's blocks: kSplitMaxBlocks, or a
 //   captured launch's slice (c.cap_blocks).
-inline int64_t split_slots(const Call& c, int per_cu) {
+//   S is the launch's blocks per row (p.split, or p.stream for the two-pass
+//   form, whose grid is always one group per row).
+inline int64_t split_slots(const Call& c, int per_cu, int S) {
   const Plan& p = c.p;
-  if ((int64_t)per_cu * c.cus < p.split) return 0;
+  if ((int64_t)per_cu * c.cus < S) return 0;
   int64_t slots = c.rows;
   if (p.grid < 0) {
     const int64_t cap = per_cu > -p.grid ? -p.grid : per_cu;
-    slots = cap * c.cus / p.split;
+    slots = cap * c.cus / S;
   }
   const int64_t max_blocks = c.cap_slice ? c.cap_blocks : kSplitMaxBlocks;
   if (slots > c.rows) slots = c.rows;
-  if (slots > max_blocks / p.split) slots = max_blocks / p.split;
+  if (slots > max_blocks / S) slots = max_blocks / S;
   return slots;
 }
 
@@ -55,28 +57,38 @@ struct SplitTicket {
 int split_begin(const Call& c, uint64_t ntags, SplitTicket* t);
 int split_end(SplitTicket* t, hipStream_t st, bool launched);
 
-template <typename In, typename Out, int VW, int NV, int MODE, bool PIPE>
-int launch_split_nv(const Call& c) {
-  const Plan& p = c.p;
-  auto kern = split_row_kernel<In, Out, VW, NV, MODE, PIPE>;
+// Launch of a kernel whose S > 1 blocks per row exchange through the
+// workspace (the single-read forms, and the two-pass forms with more than
+// one block per row): occupancy check, grid, tags and workspace, eager or
+// captured.  go(grid, workspace, tag0) enqueues the kernel itself.
+template <typename Kern, typename Go>
+int launch_exchanging(const Call& c, Kern kern, int S, Go go) {
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
-                                                   p.block, 0) != hipSuccess)
+                                                   c.p.block, 0) != hipSuccess)
     return ROWSM_EHIP;
-  const int64_t slots = split_slots(c, per_cu);
+  const int64_t slots = split_slots(c, per_cu, S);
   if (slots < 1) return ROWSM_EINVAL;  // the S blocks of one row cannot be co-resident
-  const unsigned grid = (unsigned)(slots * p.split);
+  const unsigned grid = (unsigned)(slots * S);
 
   SplitTicket t;
   int r = split_begin(c, (uint64_t)((c.rows + slots - 1) / slots), &t);
   if (r != ROWSM_OK) return r;
   (void)hipGetLastError();
-  kern<<<dim3(grid), dim3(p.block), 0, c.st>>>(
-      static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
-      c.rows, c.cols, p.split, t.ws, t.tag0, c.fz);
+  go(grid, t.ws, t.tag0);
   const bool launched = hipGetLastError() == hipSuccess;
   r = split_end(&t, c.st, launched);
   return launched ? r : ROWSM_EHIP;
+}
+
+template <typename In, typename Out, int VW, int NV, int MODE, bool PIPE>
+int launch_split_nv(const Call& c) {
+  auto kern = split_row_kernel<In, Out, VW, NV, MODE, PIPE>;
+  return launch_exchanging(c, kern, c.p.split, [&](unsigned grid, SplitWorkspace ws, uint32_t tag0) {
+    kern<<<dim3(grid), dim3(c.p.block), 0, c.st>>>(
+        static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
+        c.rows, c.cols, c.p.split, ws, tag0, c.fz);
+  });
 }
 
 // Values per lane the prefetching form holds at most: the next row's raw

@@ -77,6 +77,46 @@ __device__ __forceinline__ uint32_t split_tag0(const SplitWorkspace& w, uint32_t
 // launch, so even a broken exchange lets the whole grid drain quickly.
 constexpr uint32_t kSplitSpinLimit = 1u << 20;
 
+// Polls block b's (max, sum) words of the current row (parity slot) until
+// both carry the expected tag, and returns the pair.  A lane that gives up
+// records it once in the workspace and never waits again in this launch.
+__device__ __forceinline__ MaxSum split_poll_pair(const SplitWorkspace& w, uint32_t b,
+                                                  uint32_t slot, uint64_t tag, bool* gave_up) {
+  const uint32_t i = 2 * b + slot;
+  uint64_t vm = 0, vs = 0;
+  uint32_t spins = 0;
+  while (!*gave_up) {
+    vm = __hip_atomic_load(&w.wm[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    vs = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((vm & ~0xffffffffull) == tag && (vs & ~0xffffffffull) == tag) break;
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins == kSplitSpinLimit) {
+      __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *gave_up = true;
+    }
+  }
+  return {__uint_as_float((uint32_t)vm), __uint_as_float((uint32_t)vs)};
+}
+
+// The same for a single word per block (the ws words; the softmax backward's
+// partial dot products).
+__device__ __forceinline__ float split_poll_word(const SplitWorkspace& w, uint32_t b,
+                                                 uint32_t slot, uint64_t tag, bool* gave_up) {
+  const uint32_t i = 2 * b + slot;
+  uint64_t v = 0;
+  uint32_t spins = 0;
+  while (!*gave_up) {
+    v = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((v & ~0xffffffffull) == tag) break;
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins == kSplitSpinLimit) {
+      __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *gave_up = true;
+    }
+  }
+  return __uint_as_float((uint32_t)v);
+}
+
 // Loads a block's share of one row (raw), masked as the row's form needs.
 template <typename In, int VW, int NV, bool FUSED>
 __device__ __forceinline__ void split_load_share(InVec<In, VW> (&v)[NV], rsrc_t rx, uint32_t vin,
@@ -207,22 +247,7 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       MaxSum p = {ninf, 0.0f};
-      if (lane < S) {
-        const uint32_t i = 2 * (b0 + lane) + slot;
-        uint64_t vm = 0, vs = 0;
-        uint32_t spins = 0;
-        while (!gave_up) {
-          vm = __hip_atomic_load(&w.wm[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          vs = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if ((vm & ~0xffffffffull) == tag && (vs & ~0xffffffffull) == tag) break;
-          __builtin_amdgcn_s_sleep(1);
-          if (++spins == kSplitSpinLimit) {
-            __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            gave_up = true;
-          }
-        }
-        p = {__uint_as_float((uint32_t)vm), __uint_as_float((uint32_t)vs)};
-      }
+      if (lane < S) p = split_poll_pair(w, b0 + lane, slot, tag, &gave_up);
       p = group_merge<kWave>(p);  // fixed lane order: deterministic
       if (lane == 0) {
         // y = exp(x - m_b) * exp(m_b - M) / S

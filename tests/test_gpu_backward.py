@@ -80,7 +80,9 @@ def test_bwd_family_grid(fam, din, dout, rows, cols):
 
 
 FORMS = {
-    "two_pass": (5, 70001, dict(variant=R.LARGE, split_blocks=-1)),
+    "two_pass": (5, 70001, dict(variant=R.LARGE, split_blocks=-1)),      # 16 blocks per row
+    "two_pass_1block": (5, 70001, dict(variant=R.LARGE, split_blocks=-1, blocks_per_cu=1)),
+    "two_pass_long": (2, (1 << 21) + 5, dict(variant=R.LARGE)),         # past the split form
     "two_pass_u8": (3, 150001, dict(variant=R.LARGE, split_blocks=-1, tile_vectors=8)),
     "split_2": (7, 20000, dict(variant=R.LARGE, split_blocks=2)),
     "split_64": (3, 300000, dict(variant=R.LARGE, split_blocks=64)),
@@ -104,10 +106,22 @@ def test_bwd_forms(form, din, dout):
     assert_bwd_parity(y, dy, dx, dout, f"bwd {form} {din}->{dout}")
 
 
+TWO_PASS = -1    # the two-pass LARGE form, several blocks per row
+TWO_PASS_1 = -2  # the two-pass LARGE form, one block per row
+
+
+def special_config(fam):
+    if fam == TWO_PASS:
+        return R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
+    if fam == TWO_PASS_1:
+        return R.RowsmConfig(variant=R.LARGE, split_blocks=-1, blocks_per_cu=1)
+    return R.RowsmConfig(variant=fam)
+
+
 @pytest.mark.parametrize("din,dout", PAIRS)
-@pytest.mark.parametrize("fam", [R.SMALL, R.MEDIUM, R.LARGE])
+@pytest.mark.parametrize("fam", [R.SMALL, R.MEDIUM, R.LARGE, TWO_PASS, TWO_PASS_1])
 def test_bwd_special_values(fam, din, dout):
-    cols = {R.SMALL: 48, R.MEDIUM: 1000, R.LARGE: 70000}[fam]
+    cols = {R.SMALL: 48, R.MEDIUM: 1000}.get(fam, 70000)
     y, dy = inputs(8, cols, "f32", seed=5)
     dy[0, 3] = float("nan")              # NaN gradient: the whole row is NaN
     dy[1, 0] = float("inf")              # infinite gradient: d = +inf
@@ -119,8 +133,8 @@ def test_bwd_special_values(fam, din, dout):
     dy[6, :] = 0.0                       # zero gradient
     y[7, 1] = float("nan")               # NaN probability
     y, dy = y.to(DT[din]), dy.to(DT[din])
-    dx = run_bwd(y.to(DEV), dy.to(DEV), dout, config=R.RowsmConfig(variant=fam))
-    assert_bwd_parity(y, dy, dx, dout, f"bwd special {R.VARIANT_NAMES[fam]} {din}->{dout}")
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout, config=special_config(fam))
+    assert_bwd_parity(y, dy, dx, dout, f"bwd special {fam} {din}->{dout}")
     dxc = dx.cpu().float()
     assert torch.isnan(dxc[0]).all()
     # d = +inf: dx = y * (dy - inf) = -inf where y > 0, NaN at the inf entry

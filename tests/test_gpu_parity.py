@@ -89,9 +89,9 @@ def test_family_limits():
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
-@pytest.mark.parametrize("fam", [R.SMALL, R.MEDIUM, R.LARGE])
+@pytest.mark.parametrize("fam", [R.SMALL, R.MEDIUM, R.LARGE, "two_pass", "two_pass_1block"])
 def test_special_values(fam, din, dout):
-    cols = {R.SMALL: 48, R.MEDIUM: 1000, R.LARGE: 70000}[fam]
+    cols = {R.SMALL: 48, R.MEDIUM: 1000}.get(fam, 70000)
     x = W.random_matrix(8, cols, "f32", sigma=3.0, seed=11)
     x[0, 5] = float("nan")
     x[1, 0] = float("inf")
@@ -102,8 +102,14 @@ def test_special_values(fam, din, dout):
     x[5, cols // 2] = 0.0               # dominant entry
     x[6, :-1] = float("-inf")           # single finite entry, at the end
     x = x.to(DT[din])
-    y = run(x.to(DEV), dout, variant=fam)
-    assert_parity(x, y, dout, f"special {R.VARIANT_NAMES[fam]} {din}->{dout}")
+    if fam == "two_pass":
+        y = run(x.to(DEV), dout, config=R.RowsmConfig(variant=R.LARGE, split_blocks=-1))
+    elif fam == "two_pass_1block":
+        y = run(x.to(DEV), dout, config=R.RowsmConfig(variant=R.LARGE, split_blocks=-1,
+                                                      blocks_per_cu=1))
+    else:
+        y = run(x.to(DEV), dout, variant=fam)
+    assert_parity(x, y, dout, f"special {fam} {din}->{dout}")
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
@@ -189,12 +195,21 @@ def test_deterministic_and_bounded_writes():
 def test_two_pass_large_form(din, dout):
     # The streaming two-pass form is the fallback for rows too long for the
     # split form; check it on its own over widths with ragged tiles.
+    # several blocks per row for few rows (8-16 at 9 x 70001 and 3 x 262144),
+    # one block per row with a grid cap
     for cols in (5, 4097, 70001, 262144):
         rows = 3 if cols > 100000 else 9
         x = W.random_matrix(rows, cols, din, sigma=5.0, seed=cols + 1)
-        cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
-        y = run(x.to(DEV), dout, config=cfg)
-        assert_parity(x, y, dout, f"two-pass {rows}x{cols} {din}->{dout}")
+        for bpc in (0, 1):
+            cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=-1, blocks_per_cu=bpc)
+            st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.dtype_code(DT[din]),
+                                           R.dtype_code(DT[dout]), cfg)
+            assert st == R.OK and "split=0" in desc
+            stream = int(desc.split("stream=")[1].split()[0])
+            assert stream == 1 if bpc else (stream >= 8 or cols <= 5000), desc
+            y = run(x.to(DEV), dout, config=cfg)
+            assert_parity(x, y, dout, f"two-pass {rows}x{cols} {din}->{dout} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0
 
 
 def test_split_many_launches_and_streams():
