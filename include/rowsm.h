@@ -65,10 +65,12 @@ typedef enum {
  * registers; LARGE spreads a row over several co-resident workgroups that
  * keep their shares in registers and exchange (max, sum) pairs through a
  * small device workspace (single read), or, for rows too long for that,
- * streams the row through tiles twice (online max/sum pass, then normalize).
- * The single-read form launches one group of blocks per row; with
- * cfg->blocks_per_cu given, one residency of the device whose groups loop
- * over the rows.
+ * streams the row through tiles twice (online max/sum pass, then normalize),
+ * over one block per row for many rows and over up to 256 blocks per row,
+ * which exchange their pairs the same way, for few.  Both launch one group
+ * of blocks per row; with cfg->blocks_per_cu given, the single-read form
+ * launches one residency of the device whose groups loop over the rows, and
+ * the two-pass form one block per row.
  *
  * HIP graphs: every entry point may be called on a stream that is being
  * captured.  An eager single-read LARGE launch takes its exchange tags from
@@ -80,7 +82,8 @@ typedef enum {
  * instantiations of one graph) must not run at the same time.  When no slice
  * is left, or the region does not exist yet (it is created with the shared
  * workspace by the first single-read launch outside capture on the device),
- * a captured LARGE plan uses the two-pass form instead (same results to the
+ * a captured LARGE plan uses the two-pass form with one block per row
+ * instead (same results to the
  * stated tolerances, one extra read of each input), and a single-read form
  * forced through cfg->split_blocks > 0 returns ROWSM_EINVAL.  No entry point
  * records a memset or an allocation into a capture. */

@@ -11,7 +11,8 @@
 //           per lane in the packed form)
 //   LARGE   anything longer: the row split over S <= 64 co-resident blocks
 //           that each hold their share in registers (single read), or, for
-//           rows too long even for that, two streaming passes over tiles.
+//           rows too long even for that, two streaming passes over tiles
+//           (several blocks per row for few rows, stream_blocks()).
 // Row count: a launch of few rows must still fill the device, so fewer than
 // cus/4 rows of >= 384 KiB each (at most cus/4 rows for the packed form) take
 // the split form rather than one block per row, and the split form gives
