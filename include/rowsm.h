@@ -32,7 +32,13 @@
  *     ends; make that first call outside stream capture.  Eager launches on
  *     one device are ordered one after another whatever their streams (each
  *     waits for the previous one through an event), so the workspace is never
- *     shared by two running launches.
+ *     shared by two running launches.  The blocks of one row wait for each
+ *     other; a launch's progress needs only that workgroups are dispatched
+ *     in order, whatever else runs.  Work that itself waits on the device
+ *     for blocks that are not yet resident (such a launch from another
+ *     process on the same GPU) can hold blocks out in the worst case: a wait
+ *     then gives up after about a second, the row's result is wrong, and
+ *     rowsm_split_wait_failures() counts it.
  *   - Errors are reported through the return value only (a rowsm_status);
  *     the library never aborts, prints or throws.  Argument errors are found
  *     on the host before any HIP call.  A failed launch maps to ROWSM_EHIP.
