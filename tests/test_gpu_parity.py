@@ -113,6 +113,28 @@ def test_special_values(fam, din, dout):
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("fam,cols", [(R.SMALL, 64), (R.MEDIUM, 4096), (R.LARGE, 70000),
+                                      ("two_pass", 70000)])
+def test_subnormal_exponent_range(fam, cols, din, dout):
+    # entries spread evenly over x - max in [-110, 0]: exp(x - max) passes
+    # through the fp32 subnormal range (x - max in [-103.3, -87.3]) and
+    # underflows to zero below it; the comparator accepts flush to zero only
+    # where the fp64 value is itself below 2^-126
+    rows = 6
+    g = torch.Generator().manual_seed(cols)
+    base = torch.linspace(-110.0, 0.0, cols).repeat(rows, 1)
+    x = base[:, torch.randperm(cols, generator=g)] + torch.arange(rows).view(-1, 1) * 7.5
+    x = x.to(DT[din])
+    if fam == "two_pass":
+        y = run(x.to(DEV), dout, config=R.RowsmConfig(variant=R.LARGE, split_blocks=-1))
+    else:
+        y = run(x.to(DEV), dout, variant=fam)
+    res = assert_parity(x, y, dout, f"subnormal range {fam} {cols} {din}->{dout}")
+    v = oracle_of(x)
+    assert (v[(v > 0) & (v < 2.0 ** -126)]).size > 0     # the row does reach it
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
 def test_misaligned_rows_fall_back_to_narrow_vectors(din, dout):
     # A view starting one element into its storage breaks 8/16-byte alignment;
     # the launcher must pick single-element accesses and stay exact.
