@@ -163,10 +163,14 @@ def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
                                        w.out_dtype)
                     res = compare(got, ref[::16], w.out_dtype)
                     p = parity.setdefault(name, {"rows_checked": 0, "parity_ok": True,
-                                                 "max_abs": 0.0, "max_tol_ratio": 0.0})
+                                                 "max_abs": 0.0, "max_rel": 0.0,
+                                                 "max_tol_ratio": 0.0})
                     p["rows_checked"] += int(got.shape[0])
                     p["parity_ok"] &= bool(res["ok"])
                     p["max_abs"] = max(p["max_abs"], res["max_abs"])
+                    # relative error over entries of magnitude >= 1e-30 (reported,
+                    # not gated: the fp32 bound is absolute)
+                    p["max_rel"] = max(p["max_rel"], res["max_rel"])
                     p["max_tol_ratio"] = max(p["max_tol_ratio"], res["max_tol_ratio"])
         passes += 1
     # one thread on one chunk of the longest-row regime, for scale
