@@ -61,11 +61,12 @@ def test_fused_grid(fam, cols, din, dout):
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
-def test_fused_two_pass_form(din, dout):
+@pytest.mark.parametrize("bpc", [0, 1])   # 16 blocks per row, or one
+def test_fused_two_pass_form(din, dout, bpc):
     x = W.random_matrix(5, 70001, din, sigma=3.0, seed=7)
-    cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=-1)
+    cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=-1, blocks_per_cu=bpc)
     y = run_fused(x.to(DEV), dout, 0.3, 5, 40000, config=cfg)
-    assert_fused_parity(x, y, dout, 0.3, 5, 40000, f"two-pass fused {din}->{dout}")
+    assert_fused_parity(x, y, dout, 0.3, 5, 40000, f"two-pass fused bpc={bpc} {din}->{dout}")
 
 
 def test_fully_masked_rows_are_nan_and_masked_entries_zero():

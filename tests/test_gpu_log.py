@@ -65,10 +65,12 @@ def test_log_family_grid(fam, din, dout, rows, cols):
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
-@pytest.mark.parametrize("form", ["two_pass", "packed", "split_2"])
+@pytest.mark.parametrize("form", ["two_pass", "two_pass_1block", "packed", "split_2"])
 def test_log_forms(form, din, dout):
-    if form == "two_pass":
+    if form == "two_pass":                 # 16 blocks per row
         rows, cols, cfg = 5, 70001, dict(variant=R.LARGE, split_blocks=-1)
+    elif form == "two_pass_1block":
+        rows, cols, cfg = 5, 70001, dict(variant=R.LARGE, split_blocks=-1, blocks_per_cu=1)
     elif form == "packed":
         if din != "bf16" or dout != "bf16":
             pytest.skip("the packed form holds bf16 -> bf16 rows")
