@@ -125,7 +125,7 @@ def copy_ceiling(reps: int = 10):
             "compute_units": props.multi_processor_count}
 
 
-def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
+def cpu_baseline(inputs, outputs, regimes, min_seconds: float, threads: int = 0):
     """Time the fp64 oracle on the host cores over every row of the step (row
     chunks bounded in memory), repeating passes until ``min_seconds`` of
     oracle time has accumulated, and check evenly spaced GPU rows against it
@@ -136,7 +136,7 @@ def cpu_baseline(inputs, outputs, regimes, min_seconds: float):
     from oracle.compare import compare, widen_output
     from paper_2607_23089_amd import workloads as W
 
-    threads = len(os.sched_getaffinity(0))
+    threads = threads or len(os.sched_getaffinity(0))
     oracle.load()
     chunk_elems = 1 << 25
     tot_bytes, tot_time, passes = 0, 0.0, 0
@@ -372,6 +372,50 @@ def moe_leg(reps: int):
     return out
 
 
+def launch_bound_leg(reps: int):
+    """The 64 x 1000 fp32 workload, 256 KB: launch bound, so timed two ways,
+    each launch alone between events, and many launches back to back between
+    one event pair (the per-launch cost of a stream of such launches)."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    w = W.WORKLOADS["fp32_64x1000"]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    x = W.make_input(w, device=dev)
+    y = torch.empty_like(x)
+
+    def launch():
+        R.check(R.rowsm_forward(x.data_ptr(), y.data_ptr(), w.rows, w.cols, R.F32, R.F32, sh))
+
+    for _ in range(10):
+        launch()
+    torch.cuda.synchronize()
+    alone = []
+    for _ in range(reps):
+        e0, e1 = HipEvent(), HipEvent()
+        e0.record(stream)
+        launch()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        alone.append(e0.elapsed_time(e1) * 1e3)
+    alone.sort()
+    n = 200
+    e0, e1 = HipEvent(), HipEvent()
+    e0.record(stream)
+    for _ in range(n):
+        launch()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    _, desc = R.rowsm_describe(w.rows, w.cols, R.F32, R.F32)
+    return {"workload": "fp32_64x1000 f32->f32 (parity workload; 256 KB, launch bound)",
+            "launch": desc, "median_us_alone": alone[len(alone) // 2],
+            "us_per_launch_back_to_back": e0.elapsed_time(e1) * 1e3 / n}
+
+
 def fused_causal_leg(reps: int):
     """The fused form (scale and causal mask computed in the kernel) on the
     causal workload's shape, next to the plain form on the same scores with
@@ -426,6 +470,8 @@ def main() -> int:
     ap.add_argument("--no-next", action="store_true",
                     help="skip the measurements of the fused scale+causal form, "
                          "log-softmax, the softmax backward and the MoE group score")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="host threads of the CPU baseline (0 = every core this process may use)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="minimum seconds of oracle time for the CPU baseline (0 = skip)")
     args = ap.parse_args()
@@ -630,12 +676,14 @@ def main() -> int:
         result["graph_step"] = graph_leg
     if not args.no_next:
         result["context"] = copy_ceiling()
+        result["launch_bound"] = launch_bound_leg(reps=20)
         result["next_rows"] = {"fused_scale_causal": fused_causal_leg(reps=10),
                                "log_softmax": log_softmax_leg(reps=10),
                                "softmax_backward": backward_leg(reps=10),
                                "moe_group_top2": moe_leg(reps=10)}
     if args.cpu_budget > 0:
-        result["cpu_baseline"] = cpu_baseline(inputs, outputs, regimes, args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(inputs, outputs, regimes, args.cpu_budget,
+                                              args.cpu_threads)
     print(json.dumps(result), flush=True)
     return 0
 
