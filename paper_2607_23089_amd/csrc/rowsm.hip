@@ -173,6 +173,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   p->nvec = nvec;
 
   int variant = cfg ? cfg->variant : ROWSM_AUTO;
+  const bool auto_variant = variant == ROWSM_AUTO;
+  bool wide_row = false;  // a MEDIUM row redirected to the split form
   if (variant == ROWSM_AUTO) {
     if (nvec <= 32) {
       variant = ROWSM_SMALL;
@@ -258,7 +260,29 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->wpr = wpr;
     p->vpl = vpl;
     p->packed = packed;
-    p->nv = vpl;
+    // A row that needs all 16 waves of a 1024-thread block goes to the
+    // single-read split form of 256-thread blocks once the launch has many
+    // rows: from 8 * cus rows, or from cus / 4 when a lane would hold 64 or
+    // more values (or the packed form); rows of at least 64 KiB of input,
+    // the range measured.  A sweep of 256-8192 rows x
+    // 16384-151936 columns in every dtype pair (launches timed alone after
+    // a cache-evicting write) measured the split form 5-31% faster there
+    // (and within 2% of the medium form below these row counts): the
+    // 16-wave blocks synchronise a whole compute unit's worth of waves at
+    // each reduction and leave at most two blocks per compute unit.
+    if (auto_variant && !fused && wpr == 16 && cols * ib >= 65536 &&
+        (rows >= 8 * (int64_t)cus ||
+         ((vpl * vw >= 64 || packed) && rows >= cus / 4))) {
+      wide_row = true;
+      variant = ROWSM_LARGE;
+      p->variant = variant;
+      p->wpr = 1;
+      p->packed = false;
+    }
+  }
+  if (variant == ROWSM_MEDIUM) {
+    const int wpr = p->wpr;
+    p->nv = p->vpl;
     // 512-thread blocks (256 for the fused form, fewer rows per block when a
     // row needs more waves); one block per row group, no grid-stride loop
     // unless capped.
@@ -298,6 +322,21 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       if (forced_block) T = cfg->block;
       else if (!widening && cdiv(nvec, (int64_t)nv_cap * 512) < 8) T = 256;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
+      if (wide_row && want_split == 0 && !forced_block) {
+        // Rows redirected from the 16-wave medium form: the power of two of
+        // threads per row that gives each lane 64-128 bytes of the input,
+        // in 256-thread blocks up to 2048 threads per row and 512-thread
+        // blocks beyond, and a power of two of blocks at least as large as
+        // the register cap needs (whole slots: 7 blocks of a 65536-wide
+        // bf16 -> f32 row measured 10-13% slower than 8).  Fastest or
+        // within 3% at 16384-151936 columns and 256-8192 rows.
+        int64_t thr = 1;
+        while (thr * 128 < cols * ib) thr <<= 1;
+        T = thr <= 2048 ? 256 : 512;
+        S = thr / T > 1 ? (int)(thr / T) : 1;
+        const int64_t s_cap = cdiv(nvec, (int64_t)nv_cap * T);
+        while (S < s_cap) S <<= 1;
+      }
       if (S < 1) S = 1;
       // Grid: one group of S blocks per row (0), or with blocks_per_cu
       // given, one residency of at most that many blocks per compute unit
@@ -305,10 +344,12 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       int64_t grid = bpc ? -(int64_t)bpc : 0;
       if (want_split == 0) {
         // Few rows: more, smaller blocks per row so that the launch fills
-        // the device (256-thread blocks unless a block size is given).
+        // the device (256-thread blocks unless a block size is given; also
+        // when the row then has as many threads as in the plan above, which
+        // measured up to 9% faster at 16-64 rows of 151936-262144 columns).
         const int Tf = forced_block ? T : 256;
         const int sf = few_rows_split(rows, nvec, Tf, nv_cap, cus);
-        if (sf > 0 && (int64_t)sf * Tf > (int64_t)S * T) {
+        if (sf > 0 && (int64_t)sf * Tf >= (int64_t)S * T) {
           S = sf;
           T = Tf;
         }
@@ -374,6 +415,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
   p->nvec = nvec;
 
   int variant = cfg ? cfg->variant : ROWSM_AUTO;
+  const bool auto_variant = variant == ROWSM_AUTO;
   if (variant == ROWSM_AUTO) {
     if (nvec <= 32)
       variant = ROWSM_SMALL;
@@ -417,19 +459,29 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       if (wpr) break;
     }
     if (!wpr) return ROWSM_EINVAL;
-    p->wpr = wpr;
-    p->vpl = nv;
-    p->nv = nv;
-    int rpb = wpr >= 8 ? 1 : 8 / wpr;  // 512-thread blocks
-    if (cfg && cfg->rows_per_block > 0) {
-      rpb = cfg->rows_per_block;
-      if (rpb * wpr > 16) return ROWSM_EINVAL;
+    // A row that needs all 16 waves of a 1024-thread block goes to the
+    // split form from 4 * cus rows when it holds at least 64 KiB of each
+    // input (measured 4-20% faster there at 16384-65536 columns in every
+    // dtype pair, and within 1% of the medium form at 256-512 rows; the
+    // forward's reason).
+    if (auto_variant && wpr == 16 && cols * ib >= 65536 && rows >= 4 * (int64_t)cus) {
+      variant = ROWSM_LARGE;
+      p->variant = variant;
+    } else {
+      p->wpr = wpr;
+      p->vpl = nv;
+      p->nv = nv;
+      int rpb = wpr >= 8 ? 1 : 8 / wpr;  // 512-thread blocks
+      if (cfg && cfg->rows_per_block > 0) {
+        rpb = cfg->rows_per_block;
+        if (rpb * wpr > 16) return ROWSM_EINVAL;
+      }
+      p->block = rpb * wpr * kWave;
+      const int64_t cap = (int64_t)cus * (bpc ? bpc : 64);
+      p->grid = cdiv(rows, rpb);
+      if (p->grid > cap) p->grid = cap;
+      return ROWSM_OK;
     }
-    p->block = rpb * wpr * kWave;
-    const int64_t cap = (int64_t)cus * (bpc ? bpc : 64);
-    p->grid = cdiv(rows, rpb);
-    if (p->grid > cap) p->grid = cap;
-    return ROWSM_OK;
   }
   if (variant == ROWSM_LARGE) {
     const int want_split = cfg ? cfg->split_blocks : 0;
@@ -440,11 +492,25 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       const bool forced_block = cfg && cfg->block > 0;
       int T = forced_block ? cfg->block : 512;
       int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
+      if (want_split == 0 && !forced_block && rows >= cus && cols * ib <= 4096 * 128) {
+        // Rows of at most 512 KiB per input in launches of at least cus
+        // rows: 2048 threads per row, 4096 beyond 128 KiB per input, about
+        // 32-64 bytes of each input per lane, in 256- and 512-thread blocks
+        // (within 3% of the fastest form at 16384-151936 columns and
+        // 256-4096 rows; the register-cap plan above was up to 8% slower);
+        // a power of two of blocks at least as large as the cap needs.
+        const int64_t thr = cols * ib > 2048 * 64 ? 4096 : 2048;
+        T = thr <= 2048 ? 256 : 512;
+        S = (int)(thr / T);
+        const int64_t s_cap = cdiv(nvec, (int64_t)nv_cap * T);
+        while (S < s_cap) S <<= 1;
+      }
       if (S < 1) S = 1;
       if (want_split == 0) {
+        // (ties go to the few-rows plan, as in the forward)
         const int Tf = forced_block ? T : 256;
         const int sf = few_rows_split(rows, nvec, Tf, nv_cap, cus);
-        if (sf > 0 && (int64_t)sf * Tf > (int64_t)S * T) {
+        if (sf > 0 && (int64_t)sf * Tf >= (int64_t)S * T) {
           S = sf;
           T = Tf;
         }

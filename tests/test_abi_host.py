@@ -120,24 +120,40 @@ def test_select_regimes(lib):
     assert s(10, 132, R.F32, R.F32) == R.MEDIUM
     assert s(10, 32, R.F32, R.F32) == R.SMALL
     assert s(10, 33, R.F32, R.F32) == R.MEDIUM        # 33 single elements
-    # medium: up to 16 waves x 64 lanes x 64 fp32 values
+    # medium holds up to 16 waves x 64 lanes x 64 fp32 values (forced)
+    d = lambda rows, cols, i, o, v=R.AUTO: R.rowsm_describe(rows, cols, i, o, v)
     assert s(64, 1000, R.F32, R.F32) == R.MEDIUM
     assert s(32768, 4096, R.BF16, R.BF16) == R.MEDIUM
-    assert s(100, 65536, R.F32, R.F32) == R.MEDIUM
+    assert d(100, 65536, R.F32, R.F32, R.MEDIUM)[0] == R.OK
+    assert d(100, 65540, R.F32, R.F32, R.MEDIUM)[0] == R.EINVAL
     assert s(100, 65540, R.F32, R.F32) == R.LARGE
-    assert s(10, 65536, R.BF16, R.BF16) == R.MEDIUM      # 256 KiB rows: launch bound
     # packed bf16 rows up to 16 x 64 x 24 vectors of 8 (bf16 -> bf16 only:
     # bf16 -> f32 uses 4-element vectors so that each store is 16 bytes)
-    assert s(100, 151936, R.BF16, R.BF16) == R.MEDIUM
-    assert s(4096, 151936, R.BF16, R.F32) == R.LARGE
-    assert s(100, 196608, R.BF16, R.BF16) == R.MEDIUM
+    assert "packed=1" in d(100, 196608, R.BF16, R.BF16, R.MEDIUM)[1]
+    assert d(100, 196616, R.BF16, R.BF16, R.MEDIUM)[0] == R.EINVAL
     assert s(100, 196616, R.BF16, R.BF16) == R.LARGE
+    assert s(4096, 151936, R.BF16, R.F32) == R.LARGE
+    # rows that need all 16 waves of a block: the split form from 8 cus rows,
+    # from cus / 4 rows at 64 values per lane or packed (256 compute units)
+    assert s(2047, 32768, R.F32, R.F32) == R.MEDIUM       # 32 values per lane
+    assert s(2048, 32768, R.F32, R.F32) == R.LARGE
+    assert "split=4 " in d(2048, 32768, R.F32, R.F32)[1]     # ~128 bytes per lane
+    assert s(63, 65536, R.BF16, R.BF16) == R.MEDIUM       # 64 values per lane
+    assert s(64, 65536, R.BF16, R.BF16) == R.LARGE
+    assert s(100, 151936, R.BF16, R.BF16) == R.LARGE      # packed
+    assert s(100000, 8192, R.F32, R.F32) == R.MEDIUM      # 8 waves: unchanged
+    assert s(100000, 4096, R.BF16, R.F32) == R.MEDIUM
+    assert s(100000, 16384, R.BF16, R.BF16) == R.MEDIUM   # 16 waves, 32 KiB rows
+    bd = lambda rows, cols, i, o: R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, i, o)[1]
+    assert bd(1023, 16384, R.F32, R.F32).startswith("medium")  # backward: from 4 cus rows
+    assert bd(1024, 16384, R.F32, R.F32).startswith("large")
+    assert "split=8 " in bd(1024, 16384, R.F32, R.F32) and "block=256" in bd(1024, 16384, R.F32, R.F32)
+    assert bd(4096, 8192, R.F32, R.F32).startswith("medium")   # 32 KiB rows: unchanged
     # few long rows (>= 384 KiB of traffic): the split form fills the device
     # (the select assumes 256 compute units)
     assert s(63, 65536, R.F32, R.F32) == R.LARGE
-    assert s(64, 65536, R.F32, R.F32) == R.MEDIUM
-    assert s(64, 151936, R.BF16, R.BF16) == R.LARGE       # packed form: <= cus / 4
-    assert s(65, 151936, R.BF16, R.BF16) == R.MEDIUM
+    assert s(64, 65536, R.F32, R.F32) == R.LARGE          # and 64 values per lane
+    assert s(64, 151936, R.BF16, R.BF16) == R.LARGE
     assert s(8, 32768, R.F32, R.F32) == R.MEDIUM          # 256 KiB rows
     assert s(1024, 262144, R.F32, R.F32) == R.LARGE
     assert s(0, 5, R.F32, R.F32) > 0
@@ -150,7 +166,7 @@ def test_describe(lib):
     assert st == R.OK and text.startswith("small") and "lpr=8" in text and "vw=8" in text
     st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("medium")
-    st, text = R.rowsm_describe(128, 151936, R.BF16, R.BF16)
+    st, text = R.rowsm_describe(128, 151936, R.BF16, R.BF16, R.MEDIUM)
     assert st == R.OK and "packed=1" in text and "vpl=19" in text and "wpr=16" in text
     st, text = R.rowsm_describe(4096, 151936, R.BF16, R.F32)
     assert st == R.OK and text.startswith("large") and "vw=4" in text and "split=8" in text

@@ -94,6 +94,21 @@ FORMS = {
 }
 
 
+@pytest.mark.parametrize("rows,cols,din,dout", [
+    (1024, 16384, "f32", "f32"), (1024, 32768, "bf16", "f32"), (1024, 32768, "bf16", "bf16"),
+    (300, 65536, "f32", "f32")])
+def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
+    # rows that would need all 16 waves of one block, many rows: the split
+    # form with 2048-4096 threads per row (the launcher's own choice)
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("large") and "split=0" not in desc, desc
+    y, dy = inputs(rows, cols, din, alpha=0.1, seed=rows + cols)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
+    assert_bwd_parity(y, dy, dx, dout, f"bwd wide rows {rows}x{cols} {din}->{dout} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0
+
+
 @pytest.mark.parametrize("din,dout", PAIRS)
 @pytest.mark.parametrize("form", sorted(FORMS))
 def test_bwd_forms(form, din, dout):

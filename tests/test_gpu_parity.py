@@ -366,22 +366,37 @@ def test_maximum_row_length(rows, din, dout):
     assert res["ok"], f"max row length {rows}x{cols} {din}->{dout} [{desc}]: {res} {got}"
 
 
-@pytest.mark.parametrize("rows,din,dout,cols,want", [
-    (2, "f32", "f32", 1 << 21, "split=64"),            # 64 blocks x 512 x 64 values
-    (2, "f32", "f32", (1 << 21) + 4, "split=0"),        # one vector more: two passes
-    (2, "bf16", "bf16", 1 << 21, "split=64"),
-    (2, "bf16", "f32", 64 * 512 * 40, "split=64"),      # widening: 40 values per lane
-    (2, "bf16", "f32", 64 * 512 * 40 + 4, "split=0"),
-    (65, "bf16", "bf16", 196608, "packed=1"),           # packed medium: 24 slots x 1024
-    (65, "bf16", "bf16", 196616, "large"),
+@pytest.mark.parametrize("rows,din,dout,cols,want,fam", [
+    (2, "f32", "f32", 1 << 21, "split=64", R.AUTO),     # 64 blocks x 512 x 64 values
+    (2, "f32", "f32", (1 << 21) + 4, "split=0", R.AUTO),  # one vector more: two passes
+    (2, "bf16", "bf16", 1 << 21, "split=64", R.AUTO),
+    (2, "bf16", "f32", 64 * 512 * 40, "split=64", R.AUTO),  # widening: 40 values per lane
+    (2, "bf16", "f32", 64 * 512 * 40 + 4, "split=0", R.AUTO),
+    (65, "bf16", "bf16", 196608, "packed=1", R.MEDIUM),  # packed medium: 24 slots x 1024
+    (65, "bf16", "bf16", 196616, "large", R.AUTO),
+    (3, "f32", "f32", 65536, "wpr=16", R.MEDIUM),       # 16 waves x 64 values
 ])
-def test_form_capacity_limits(rows, din, dout, cols, want):
+def test_form_capacity_limits(rows, din, dout, cols, want, fam):
     # the largest rows each register-resident form holds, and one vector more
-    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]), fam)
     assert st == R.OK and want in desc, desc
     x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols)
-    y = run(x.to(DEV), dout)
+    y = run(x.to(DEV), dout, variant=fam)
     assert_parity(x, y, dout, f"capacity {rows}x{cols} {din}->{dout} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0
+
+
+@pytest.mark.parametrize("rows,cols,din,dout", [
+    (2048, 32768, "f32", "f32"), (64, 65536, "bf16", "bf16"), (100, 151936, "bf16", "bf16"),
+    (512, 65536, "bf16", "f32"), (300, 65536, "f32", "bf16")])
+def test_wide_rows_take_split_form(rows, cols, din, dout):
+    # rows that would need all 16 waves of one block: the launcher's own
+    # choice at these row counts is the split form (about 128 bytes per lane)
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("large") and "split=0" not in desc, desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + cols)
+    y = run(x.to(DEV), dout)
+    assert_parity(x, y, dout, f"wide rows {rows}x{cols} {din}->{dout} [{desc}]")
     assert R.rowsm_split_wait_failures() == 0
 
 
