@@ -119,8 +119,8 @@ def copy_ceiling(reps: int = 10):
     props = torch.cuda.get_device_properties(dev)
     return {"torch_copy_1GiB_GBps": 2 * nbytes / (copy_us * 1e3),
             "torch_fill_1GiB_GBps": nbytes / (fill_us * 1e3),
-            "measured_read_GBps_probe": MEASURED_READ_GBS,
-            "measured_write_GBps_probe": MEASURED_WRITE_GBS,
+            "read_write_model_read_GBps": MEASURED_READ_GBS,
+            "read_write_model_write_GBps": MEASURED_WRITE_GBS,
             "device": props.name, "gcn_arch": getattr(props, "gcnArchName", None),
             "compute_units": props.multi_processor_count}
 
@@ -235,9 +235,11 @@ class HipEvent:
             HipEvent._hip.hipEventDestroy(self.ev)
 
 
-# Read-only and write-only rates of plain streaming kernels measured on this
-# GPU; a kernel moving read fraction r and write fraction 1 - r of its bytes
-# is bounded by 1 / (r / READ + (1 - r) / WRITE).
+# Read-only and write-only rates of streaming probes with 8 vectors per
+# thread, an early model of a read/write mix: 1 / (r / READ + (1 - r) / WRITE)
+# for read fraction r.  It is a model, not a bound (streams with one vector
+# per thread, the long-row kernels among them, exceed it); the same-run copy
+# of the same byte mix (ratio_to_copy) is the reference where one exists.
 MEASURED_READ_GBS = 6870.0
 MEASURED_WRITE_GBS = 5950.0
 
@@ -267,7 +269,8 @@ def timed_alone(fn, reps: int, flush, stream) -> float:
 def log_softmax_leg(reps: int):
     """Log-softmax on the long-row workloads (its cross-entropy use), each
     launch timed alone, next to softmax on the same input under the same
-    protocol.  Algorithmic bytes: x read once plus y written once."""
+    protocol, and the library's streaming copy of the same bytes (same dtype
+    pair and buffers).  Algorithmic bytes: x read once plus y written once."""
     import torch
 
     import paper_2607_23089_amd as R
@@ -287,15 +290,19 @@ def log_softmax_leg(reps: int):
             x.data_ptr(), y.data_ptr(), w.rows, w.cols, di, do, sh, None)), reps, flush, stream)
         sm_us = timed_alone(lambda: R.check(R.rowsm_forward(
             x.data_ptr(), y.data_ptr(), w.rows, w.cols, di, do, sh)), reps, flush, stream)
+        copy_us = timed_alone(lambda: R.check(R.rowsm_stream_copy(
+            x.data_ptr(), y.data_ptr(), w.rows * w.cols, di, do, sh)), reps, flush, stream)
         gbs = w.algorithmic_bytes / (log_us * 1e-6) / 1e9
+        copy_gbs = w.algorithmic_bytes / (copy_us * 1e-6) / 1e9
         bound = mix_bound_gbs(w.rows * w.cols * w.in_bytes, w.rows * w.cols * w.out_bytes)
         _, desc = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, w.rows, w.cols, di, do)
         out[name] = {
             "launch": desc, "hbm_bytes_per_launch": measured_traffic(f"log_softmax/{name}", desc),
             "algorithmic_bytes": w.algorithmic_bytes, "avg_us": log_us,
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
-            "frac_of_measured_mix_bound": gbs / bound,
+            "frac_of_read_write_model": gbs / bound,
             "softmax_same_protocol_us": sm_us,
+            "copy_us": copy_us, "copy_GBps": copy_gbs, "ratio_to_copy": gbs / copy_gbs,
         }
         del x, y
     return out
@@ -328,7 +335,7 @@ def backward_leg(reps: int):
             "launch": desc, "hbm_bytes_per_launch": measured_traffic(f"softmax_backward/{name}", desc),
             "algorithmic_bytes": w.algorithmic_bytes, "avg_us": us,
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
-            "frac_of_measured_mix_bound": gbs / bound,
+            "frac_of_read_write_model": gbs / bound,
         }
         del y, dy, dx
     if R.rowsm_split_wait_failures() != 0:
@@ -366,7 +373,7 @@ def moe_leg(reps: int):
             "launch": desc, "hbm_bytes_per_launch": measured_traffic(f"moe_group_top2/{name}", desc),
             "algorithmic_bytes": w.algorithmic_bytes, "avg_us": us,
             "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
-            "frac_of_measured_mix_bound": gbs / bound,
+            "frac_of_read_write_model": gbs / bound,
         }
         del x, o
     return out
@@ -421,7 +428,8 @@ def fused_causal_leg(reps: int):
     causal workload's shape, next to the plain form on the same scores with
     the mask stored as -inf.  Each launch is timed alone after a 1 GiB write
     that evicts the memory-side cache.  Algorithmic bytes of the fused form:
-    the kept entries of x read once plus all of y written once."""
+    the kept entries of x read once plus all of y written once.  A widening
+    streaming copy with the same read:write mix is timed beside it."""
     import torch
 
     import paper_2607_23089_amd as R
@@ -449,6 +457,13 @@ def fused_causal_leg(reps: int):
     kept = (w.rows // q) * (q * (q + 1) // 2)
     alg = kept * w.in_bytes + w.rows * w.cols * w.out_bytes
     gbs = alg / (fused_us * 1e-6) / 1e9
+    # The same 1:2 read:write mix as a plain stream: a bf16 -> fp32 widening
+    # copy of `kept` elements reads the kept bytes and writes twice as many.
+    wide = torch.empty(kept, dtype=torch.float32, device=dev)
+    copy_us = timed(lambda: R.check(R.rowsm_stream_copy(
+        x.data_ptr(), wide.data_ptr(), kept, R.BF16, R.F32, sh)))
+    copy_gbs = kept * 6 / (copy_us * 1e-6) / 1e9
+    del wide
     st, desc = R.rowsm_describe(w.rows, w.cols, R.BF16, R.BF16)
     return {
         "workload": "causal_32768x4096 scores without stored mask, scale 0.125, "
@@ -456,6 +471,7 @@ def fused_causal_leg(reps: int):
         "algorithmic_bytes": alg, "kept_fraction": kept / (w.rows * w.cols),
         "avg_us": fused_us, "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
         "stored_mask_same_protocol_us": plain_us, "speedup_vs_stored_mask": plain_us / fused_us,
+        "copy_1to2_us": copy_us, "copy_1to2_GBps": copy_gbs, "ratio_to_copy": gbs / copy_gbs,
     }
 
 
