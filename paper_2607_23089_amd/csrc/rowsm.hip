@@ -13,6 +13,8 @@
 //           that each hold their share in registers (single read), or, for
 //           rows too long even for that, two streaming passes over tiles
 //           (several blocks per row for few rows, stream_blocks()).
+// Rows of 129-4096 vectors in launches of at least 32 rows per compute unit
+// take measured launch shapes (medium or single-read, measured_row_shape()).
 // Row count: a launch of few rows must still fill the device, so fewer than
 // cus/4 rows of >= 384 KiB each (at most cus/4 rows for the packed form) take
 // the split form rather than one block per row, and the split form gives
@@ -80,6 +82,17 @@ int choose_vw(int64_t cols, int ib, int ob, uintptr_t xa, uintptr_t ya) {
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Grid limit of the small, medium and MoE families: one task (row group) per
+// wave or block up to 2^30 blocks, the waves striding over any tasks beyond
+// that; cfg->blocks_per_cu caps the grid at that many blocks per compute unit.
+// Grid-stride loops over a capped grid measured 4-8% slower at 1-4 M rows
+// (and slower still in plain store streams): waves that drift apart spread
+// the addresses in flight over the whole buffer, while the in-order blocks
+// of an uncapped grid keep them in one moving window.
+int64_t grid_cap(int bpc, int cus) {
+  return bpc ? (int64_t)cus * bpc : ((int64_t)1 << 30);
+}
+
 bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
 
 bool pow2_upto(int v, int hi) { return v >= 1 && v <= hi && (v & (v - 1)) == 0; }
@@ -114,6 +127,53 @@ constexpr int64_t kFewRowsMinBytesBackward = 512 * 1024;
 bool few_long_rows(int64_t rows, int64_t row_bytes, bool packed, int cus,
                    int64_t min_bytes = kFewRowsMinBytes) {
   return row_bytes >= min_bytes && (packed ? rows <= cus / 4 : rows < cus / 4);
+}
+
+// Launch shape of a forward row of 129-4096 full 16-byte vectors in a launch
+// of at least 32 rows per compute unit (softmax and log forms): a medium
+// group of wpr waves with rpb rows per block (S == 0), or the single-read
+// form with S blocks of T threads per row.  From sweeps of 1024-16384
+// columns in every dtype pair (8192-262144 rows, launches timed alone after
+// a cache-evicting write, two boxes agreeing within 1.5%), at the lengths
+// 128 x 2^k, 192 x 2^k and the lengths between: the medium form is fastest
+// with two to four vectors per lane and one or two rows per block, rows of more than
+// about 1280 vectors in the single-read form with 512 threads per row; rows
+// that widen (bf16 -> fp32) or narrow (fp32 -> bf16) keep the medium form
+// longer.  At those lengths the picks are within 2-3% of the fastest form
+// measured, where the previous rule (at most 16 fp32 values per lane,
+// 512-thread blocks) was up to 35% slower.  The form that wins changes
+// with the length in ways no simple count of slots or bytes per lane
+// predicts (the same geometry in the medium and the single-read kernel can
+// differ by 15% either way), hence a table.  Smaller launches keep the
+// previous rule: at 8-16 rows per compute unit fewer waves per row measured
+// fastest.  false for bf16 -> bf16 rows beyond 2048 vectors (not swept).
+struct RowShape {
+  int wpr = 0, rpb = 0, S = 0, T = 0;
+};
+bool measured_row_shape(int64_t nvec, int ib, int ob, RowShape* r) {
+  if (nvec <= 128 || nvec > 4096) return false;
+  struct Row {
+    int upto, wpr, rpb, S, T;
+  };
+  // {longest row (vectors), wpr, rpb, S, T}
+  static constexpr Row kSame[] = {{256, 2, 1, 0, 0},    {320, 4, 1, 0, 0},
+                                  {512, 4, 2, 0, 0},    {640, 4, 1, 0, 0},
+                                  {1280, 8, 1, 0, 0},   {1792, 0, 0, 1, 512},
+                                  {3072, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
+  static constexpr Row kWiden[] = {{256, 2, 1, 0, 0},    {512, 4, 1, 0, 0},
+                                   {896, 4, 2, 0, 0},    {1792, 8, 1, 0, 0},
+                                   {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
+  static constexpr Row kNarrow[] = {{256, 2, 1, 0, 0},   {768, 4, 1, 0, 0},
+                                    {1024, 4, 2, 0, 0},  {2048, 8, 1, 0, 0},
+                                    {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
+  if (ib == ob && ib == 2 && nvec > 2048) return false;
+  const Row* t = ib == ob ? kSame : (ob > ib ? kWiden : kNarrow);
+  while (nvec > t->upto) ++t;
+  r->wpr = t->wpr;
+  r->rpb = t->rpb;
+  r->S = t->S;
+  r->T = t->T;
+  return true;
 }
 
 // Blocks per row for a split launch of fewer than cus rows with T-thread
@@ -175,6 +235,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   int variant = cfg ? cfg->variant : ROWSM_AUTO;
   const bool auto_variant = variant == ROWSM_AUTO;
   bool wide_row = false;  // a MEDIUM row redirected to the split form
+  RowShape shape;         // measured_row_shape() pick, when it applies
   if (variant == ROWSM_AUTO) {
     if (nvec <= 32) {
       variant = ROWSM_SMALL;
@@ -208,9 +269,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     }
     p->block = 256;
     const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
-    const int64_t cap = (int64_t)cus * (bpc ? bpc : 8);
     p->grid = cdiv(rows, rows_per_block);
-    if (p->grid > cap) p->grid = cap;
+    if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
     return ROWSM_OK;
   }
   if (variant == ROWSM_MEDIUM) {
@@ -260,6 +320,24 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->wpr = wpr;
     p->vpl = vpl;
     p->packed = packed;
+    // Full launches of rows of 129-4096 full vectors, when nothing about the
+    // shape is forced: the measured shapes of measured_row_shape().
+    const bool shape_free = !cfg || (cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
+                                     cfg->packed == -1 && cfg->block == 0 &&
+                                     cfg->split_blocks == 0 && cfg->vw == 0);
+    if (auto_variant && !fused && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
+        rows >= 32 * (int64_t)cus && measured_row_shape(nvec, ib, ob, &shape)) {
+      if (shape.S > 0) {
+        variant = ROWSM_LARGE;
+        p->variant = variant;
+        p->wpr = 1;
+        p->packed = false;
+      } else {
+        p->wpr = shape.wpr;
+        p->vpl = (int)cdiv(nvec, (int64_t)shape.wpr * kWave);
+        p->packed = false;
+      }
+    }
     // A row that needs all 16 waves of a 1024-thread block goes to the
     // single-read split form of 256-thread blocks once the launch has many
     // rows: from 8 * cus rows, or from cus / 4 when a lane would hold 64 or
@@ -270,7 +348,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // (and within 2% of the medium form below these row counts): the
     // 16-wave blocks synchronise a whole compute unit's worth of waves at
     // each reduction and leave at most two blocks per compute unit.
-    if (auto_variant && !fused && wpr == 16 && cols * ib >= 65536 &&
+    if (variant == ROWSM_MEDIUM && auto_variant && !fused && p->wpr == 16 &&
+        cols * ib >= 65536 &&
         (rows >= 8 * (int64_t)cus ||
          ((vpl * vw >= 64 || packed) && rows >= cus / 4))) {
       wide_row = true;
@@ -288,14 +367,14 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // unless capped.
     const int waves_per_block = fused ? 4 : 8;
     int rpb = wpr >= waves_per_block ? 1 : waves_per_block / wpr;
+    if (shape.rpb > 0) rpb = shape.rpb;
     if (cfg && cfg->rows_per_block > 0) {
       rpb = cfg->rows_per_block;
       if (rpb * wpr > 16) return ROWSM_EINVAL;
     }
     p->block = rpb * wpr * kWave;
-    const int64_t cap = (int64_t)cus * (bpc ? bpc : 64);
     p->grid = cdiv(rows, rpb);
-    if (p->grid > cap) p->grid = cap;
+    if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
     return ROWSM_OK;
   }
   if (variant == ROWSM_LARGE) {
@@ -336,6 +415,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         S = thr / T > 1 ? (int)(thr / T) : 1;
         const int64_t s_cap = cdiv(nvec, (int64_t)nv_cap * T);
         while (S < s_cap) S <<= 1;
+      }
+      if (shape.S > 0) {
+        S = shape.S;
+        T = shape.T;
       }
       if (S < 1) S = 1;
       // Grid: one group of S blocks per row (0), or with blocks_per_cu
@@ -438,9 +521,8 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     p->rpl = (cfg && cfg->rows_per_lane > 0) ? cfg->rows_per_lane : 4;
     p->block = 256;
     const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
-    const int64_t cap = (int64_t)cus * (bpc ? bpc : 8);
     p->grid = cdiv(rows, rows_per_block);
-    if (p->grid > cap) p->grid = cap;
+    if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
     return ROWSM_OK;
   }
   if (variant == ROWSM_MEDIUM) {
@@ -477,9 +559,8 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
         if (rpb * wpr > 16) return ROWSM_EINVAL;
       }
       p->block = rpb * wpr * kWave;
-      const int64_t cap = (int64_t)cus * (bpc ? bpc : 64);
       p->grid = cdiv(rows, rpb);
-      if (p->grid > cap) p->grid = cap;
+      if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
       return ROWSM_OK;
     }
   }
@@ -570,10 +651,9 @@ int plan_moe(int64_t ngroups, int64_t g, int in_dt, uintptr_t sa, const rowsm_co
   p->block = 256;
   const int64_t per_task = (int64_t)(kWave / p->lpr) * p->rpl;
   const int64_t tasks = cdiv(ngroups, per_task);
-  const int64_t cap = (cfg && cfg->blocks_per_cu > 0) ? (int64_t)cus * cfg->blocks_per_cu
-                                                     : ((int64_t)1 << 30);
+  const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
   p->grid = cdiv(tasks, p->block / kWave);
-  if (p->grid > cap) p->grid = cap;
+  if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
   return ROWSM_OK;
 }
 

@@ -141,9 +141,40 @@ def test_select_regimes(lib):
     assert s(63, 65536, R.BF16, R.BF16) == R.MEDIUM       # 64 values per lane
     assert s(64, 65536, R.BF16, R.BF16) == R.LARGE
     assert s(100, 151936, R.BF16, R.BF16) == R.LARGE      # packed
-    assert s(100000, 8192, R.F32, R.F32) == R.MEDIUM      # 8 waves: unchanged
-    assert s(100000, 4096, R.BF16, R.F32) == R.MEDIUM
-    assert s(100000, 16384, R.BF16, R.BF16) == R.MEDIUM   # 16 waves, 32 KiB rows
+    # full launches (>= 32 rows per compute unit) of rows of 129-4096 full
+    # vectors take the measured shapes: two vectors per lane in the medium
+    # form, the single-read form with 512 threads per row beyond
+    def has(text, *parts):
+        return all(p in text for p in parts)
+    assert has(d(100000, 1024, R.F32, R.F32)[1], "medium", "wpr=2 ", "vpl=2 ", "block=128 ")
+    assert has(d(100000, 2048, R.F32, R.F32)[1], "medium", "wpr=4 ", "vpl=2 ", "block=512 ")
+    assert has(d(100000, 2048, R.BF16, R.F32)[1], "medium", "wpr=4 ", "vpl=2 ", "block=256 ")
+    assert has(d(100000, 3072, R.BF16, R.F32)[1], "medium", "wpr=4 ", "vpl=3 ", "block=512 ")
+    assert has(d(100000, 3072, R.F32, R.BF16)[1], "medium", "wpr=4 ", "vpl=3 ", "block=256 ")
+    assert has(d(100000, 4096, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=2 ", "block=512 ")
+    assert has(d(32768, 4096, R.BF16, R.BF16)[1], "medium", "wpr=4 ", "vpl=2 ", "block=512 ")
+    assert has(d(100000, 6144, R.F32, R.F32)[1], "large", "split=1 ", "block=512 ")
+    assert has(d(100000, 6144, R.BF16, R.F32)[1], "medium", "wpr=8 ", "vpl=3 ")
+    assert has(d(100000, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 8192, R.BF16, R.F32)[1], "large", "split=1 ", "block=512 ")
+    assert has(d(100000, 8192, R.F32, R.BF16)[1], "medium", "wpr=8 ", "vpl=4 ")
+    assert has(d(100000, 16384, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 12288, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 16384, R.F32, R.F32)[1], "large", "split=2 ", "block=512 ")
+    assert has(d(100000, 16384, R.BF16, R.F32)[1], "large", "split=2 ", "block=256 ")
+    # not below 32 rows per compute unit, nor for misaligned rows, forced
+    # shapes, the fused form or bf16 rows beyond 2048 vectors
+    assert has(d(8191, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")
+    assert has(d(8192, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=2 ")
+    t = R.rowsm_describe_op(R.OP_SOFTMAX, 100000, 8192, R.F32, R.F32,
+                            R.RowsmConfig(waves_per_row=8))[1]
+    assert has(t, "medium", "wpr=8 ", "vpl=4 ")
+    t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 100000, 2048, R.F32, R.F32)[1]
+    assert has(t, "medium", "wpr=1 ", "vpl=8 ")  # 32 values per lane
+    assert has(d(100000, 24576, R.BF16, R.BF16)[1], "medium", "wpr=16 ")
+    assert has(R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 100000, 8192, R.F32, R.F32)[1],
+               "large", "split=2 ", "block=256 ")
     bd = lambda rows, cols, i, o: R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, i, o)[1]
     assert bd(1023, 16384, R.F32, R.F32).startswith("medium")  # backward: from 4 cus rows
     assert bd(1024, 16384, R.F32, R.F32).startswith("large")
@@ -178,6 +209,20 @@ def test_describe(lib):
     st, text = R.rowsm_describe_op(R.OP_SOFTMAX, 1024, 262144, R.F32, R.F32,
                                    R.RowsmConfig(blocks_per_cu=2))
     assert st == R.OK and "split=8" in text and "one residency" in text
+    # small and medium grids: one task per wave / one row group per block at
+    # any row count; blocks_per_cu caps them (the waves then stride)
+    for op in (R.OP_SOFTMAX, R.OP_SOFTMAX_BACKWARD):
+        st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16)
+        assert st == R.OK and text.startswith("small") and "grid=32768 " in text, text
+        st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16,
+                                       R.RowsmConfig(blocks_per_cu=8))
+        assert st == R.OK and "grid=2048 " in text, text
+        st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16)
+        assert st == R.OK and text.startswith("medium") and "wpr=4" in text, text
+        assert "block=512" in text and "grid=65536 " in text, text
+        st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16,
+                                       R.RowsmConfig(blocks_per_cu=64))
+        assert st == R.OK and "grid=16384 " in text, text
     # 512 threads would leave fewer than 8 blocks to the row: 256
     st, text = R.rowsm_describe(1024, 131072, R.F32, R.F32)
     assert st == R.OK and "split=8" in text and "block=256" in text

@@ -402,7 +402,9 @@ def test_wide_rows_take_split_form(rows, cols, din, dout):
 
 @pytest.mark.parametrize("rows,cols", [(4099, 64), (4099, 1000), (4099, 4097)])
 def test_many_rows_grid_stride(rows, cols):
-    # more rows than one grid covers in the small and medium families
+    # the small and medium families' default grid (a task per wave or block)
+    # and a grid capped at one block per compute unit, whose waves stride
+    # over more tasks than the grid covers
     x = W.random_matrix(rows, cols, "bf16", sigma=4.0, seed=rows + cols)
     for cfg in (None, R.RowsmConfig(blocks_per_cu=1)):
         y = run(x.to(DEV), "bf16", config=cfg)
