@@ -192,3 +192,24 @@ def test_log_bounded_writes_and_deterministic():
         assert torch.equal(y, y2)
         assert torch.all(buf[:guard] == -123.0) and torch.all(buf[guard + n:] == -123.0)
         assert torch.equal(x, x0)
+
+
+@pytest.mark.parametrize("cols,din,dout,want", [
+    (6144, "f32", "f32", ("large", "split=1 ", "block=512 ")),
+    (2560, "bf16", "bf16", ("medium", "wpr=4 ", "block=256 ")),
+    (10240, "bf16", "f32", ("large", "split=1 ", "block=512 ")),
+    (8192, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 "))])
+def test_log_measured_launch_shapes(cols, din, dout, want):
+    # full launches of medium-length rows take the same measured shapes as
+    # softmax; sampled rows element by element
+    rows = 8201
+    st, desc = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and all(w in desc for w in want), desc
+    print(f"log measured shape {rows}x{cols} {din}->{dout}: {desc}", flush=True)
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols + 3, device=DEV)
+    y = run_log(x, dout)
+    sample = list(range(0, rows, 101)) + [rows - 1]
+    assert_log_parity(x[sample].cpu(), y[sample].cpu(), dout, f"log {rows}x{cols} [{desc}]")
+    assert R.rowsm_split_wait_failures() == 0
+    del x, y

@@ -400,6 +400,47 @@ def test_wide_rows_take_split_form(rows, cols, din, dout):
     assert R.rowsm_split_wait_failures() == 0
 
 
+# Full launches of medium-length rows: one case per kind of measured launch
+# shape (medium groups with one or two rows per block, the single-read form
+# with one or two blocks per row), at 8201 rows (32 rows per compute unit of
+# 256, an odd count).
+MEASURED_SHAPES = [
+    (1024, "f32", "f32", ("medium", "wpr=2 ", "block=128 ")),
+    (2048, "f32", "f32", ("medium", "wpr=4 ", "block=512 ")),
+    (2560, "f32", "f32", ("medium", "wpr=4 ", "block=256 ")),
+    (4096, "f32", "f32", ("medium", "wpr=8 ", "block=512 ")),
+    (6144, "f32", "f32", ("large", "split=1 ", "block=512 ")),
+    (8192, "f32", "f32", ("large", "split=2 ", "block=256 ")),
+    (14336, "f32", "f32", ("large", "split=2 ", "block=512 ")),
+    (2560, "bf16", "bf16", ("medium", "wpr=4 ", "block=256 ")),
+    (16384, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
+    (3072, "bf16", "f32", ("medium", "wpr=4 ", "block=512 ")),
+    (6144, "bf16", "f32", ("medium", "wpr=8 ", "vpl=3 ")),
+    (10240, "bf16", "f32", ("large", "split=1 ", "block=512 ")),
+    (16384, "bf16", "f32", ("large", "split=2 ", "block=256 ")),
+    (3584, "f32", "bf16", ("medium", "wpr=4 ", "block=512 ")),
+    (8192, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 ")),
+    (12288, "f32", "bf16", ("large", "split=1 ", "block=512 ")),
+]
+
+
+@pytest.mark.parametrize("cols,din,dout,want", MEASURED_SHAPES)
+def test_measured_launch_shapes(cols, din, dout, want):
+    rows = 8201
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and all(w in desc for w in want), desc
+    print(f"measured shape {rows}x{cols} {din}->{dout}: {desc}", flush=True)
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols + rows, device=DEV)
+    y = run(x, dout)
+    sample = list(range(0, rows, 97)) + [rows - 2, rows - 1]
+    assert_parity(x[sample].cpu(), y[sample].cpu(), dout, f"{rows}x{cols} {din}->{dout} [{desc}]")
+    sums = y.double().sum(dim=1)
+    tol = 1e-5 if dout == "f32" else 2.0 ** -8 + 1e-5
+    assert float((sums - 1.0).abs().max()) <= tol
+    assert R.rowsm_split_wait_failures() == 0
+    del x, y
+
+
 @pytest.mark.parametrize("rows,cols", [(4099, 64), (4099, 1000), (4099, 4097)])
 def test_many_rows_grid_stride(rows, cols):
     # the small and medium families' default grid (a task per wave or block)
