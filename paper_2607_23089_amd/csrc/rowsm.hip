@@ -327,12 +327,15 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
                                      cfg->split_blocks == 0 && cfg->vw == 0);
     if (auto_variant && !fused && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
         rows >= 32 * (int64_t)cus && measured_row_shape(nvec, ib, ob, &shape)) {
+      // (a single-read pick holds one group of blocks per row only while
+      // the rows fit the exchange workspace; beyond, the medium rule stays)
+      if (shape.S > 0 && rows * shape.S > kSplitMaxBlocks) shape = RowShape{};
       if (shape.S > 0) {
         variant = ROWSM_LARGE;
         p->variant = variant;
         p->wpr = 1;
         p->packed = false;
-      } else {
+      } else if (shape.wpr > 0) {
         p->wpr = shape.wpr;
         p->vpl = (int)cdiv(nvec, (int64_t)shape.wpr * kWave);
         p->packed = false;

@@ -173,6 +173,10 @@ def test_select_regimes(lib):
     t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 100000, 2048, R.F32, R.F32)[1]
     assert has(t, "medium", "wpr=1 ", "vpl=8 ")  # 32 values per lane
     assert has(d(100000, 24576, R.BF16, R.BF16)[1], "medium", "wpr=16 ")
+    # a single-read pick only while one group of blocks per row fits the
+    # 2^20-block exchange workspace
+    assert has(d(524288, 8192, R.F32, R.F32)[1], "large", "split=2 ")
+    assert has(d(524289, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")
     assert has(R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 100000, 8192, R.F32, R.F32)[1],
                "large", "split=2 ", "block=256 ")
     bd = lambda rows, cols, i, o: R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, i, o)[1]
