@@ -158,7 +158,8 @@ typedef struct rowsm_config {
     int32_t rows_per_block; /* MEDIUM: rows per block (rows*waves_per_row <= 16)  */
     int32_t packed;         /* MEDIUM: 1 keep raw bf16 and recompute exp,
                                0 keep fp32 exp values, -1 launcher's choice       */
-    int32_t block;          /* LARGE: threads per block, multiple of 64, <= 1024  */
+    int32_t block;          /* LARGE: threads per block, multiple of 64, <= 1024;
+                               SMALL and the MoE score: 64, 128 or 256           */
     int32_t tile_vectors;   /* LARGE: vectors per thread per tile: 2, 4, 8        */
     int32_t blocks_per_cu;  /* grid cap = blocks_per_cu * compute units           */
     int32_t split_blocks;   /* LARGE: blocks sharing one row in the single-read

@@ -95,6 +95,17 @@ int64_t grid_cap(int bpc, int cus) {
 
 bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
 
+// Block size of the small-row and MoE kernels (whose waves work on their own
+// rows): 256 threads, or cfg->block when given, at most 256.
+int small_block(const rowsm_config* cfg, int* block) {
+  *block = 256;
+  if (cfg && cfg->block > 0) {
+    if (cfg->block > 256) return ROWSM_EINVAL;
+    *block = cfg->block;
+  }
+  return ROWSM_OK;
+}
+
 bool pow2_upto(int v, int hi) { return v >= 1 && v <= hi && (v & (v - 1)) == 0; }
 
 // Every override must lie in its documented domain, whichever family or form
@@ -267,7 +278,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       if (fused && r != 4) return ROWSM_EINVAL;  // fused kernels: 4 rows per lane
       p->rpl = r;
     }
-    p->block = 256;
+    if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
     const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
     p->grid = cdiv(rows, rows_per_block);
     if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
@@ -522,7 +533,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       p->lpr = cfg->lanes_per_row;
     }
     p->rpl = (cfg && cfg->rows_per_lane > 0) ? cfg->rows_per_lane : 4;
-    p->block = 256;
+    if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
     const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
     p->grid = cdiv(rows, rows_per_block);
     if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
@@ -651,7 +662,7 @@ int plan_moe(int64_t ngroups, int64_t g, int in_dt, uintptr_t sa, const rowsm_co
   p->nvec = (int)(g / vw);
   p->lpr = (int)(g / vw);  // lanes per group
   p->rpl = (cfg && cfg->rows_per_lane > 0) ? cfg->rows_per_lane : 4;
-  p->block = 256;
+  if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
   const int64_t per_task = (int64_t)(kWave / p->lpr) * p->rpl;
   const int64_t tasks = cdiv(ngroups, per_task);
   const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;

@@ -87,6 +87,7 @@ def test_bad_variant_and_config(lib):
            dict(variant=R.MEDIUM, waves_per_row=4, rows_per_block=8),
            dict(variant=R.LARGE, block=100), dict(variant=R.LARGE, tile_vectors=3),
            dict(variant=R.LARGE, block=2048), dict(variant=R.SMALL, rows_per_block=17),
+           dict(variant=R.SMALL, block=512),
            dict(variant=R.LARGE, split_blocks=-2), dict(variant=R.MEDIUM, packed=2),
            dict(variant=R.SMALL, blocks_per_cu=-1), dict(variant=7),
            dict(variant=R.AUTO, vw=3), dict(variant=R.AUTO, vw=2),

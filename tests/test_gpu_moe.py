@@ -72,6 +72,16 @@ def test_moe_vector_widths(din, vw):
     assert_moe_exact(x, o, 32, "f32", f"vw={vw} {din}")
 
 
+@pytest.mark.parametrize("block,rpl,bpc", [(64, 1, 0), (128, 2, 1), (64, 8, 1)])
+def test_moe_block_sizes(block, rpl, bpc):
+    # smaller blocks (and a capped grid whose waves stride) give the same
+    # bit-exact scores
+    x = tie_heavy(4099, 256, "f32", seed=block + rpl)
+    o = run_moe(x.to(DEV), 32, "f32",
+                config=R.RowsmConfig(block=block, rows_per_lane=rpl, blocks_per_cu=bpc))
+    assert_moe_exact(x, o, 32, "f32", f"block={block} rpl={rpl} bpc={bpc}")
+
+
 @pytest.mark.parametrize("din,dout", PAIRS)
 def test_moe_special_values(din, dout):
     x = W.random_matrix(8, 64, "f32", sigma=1.0, seed=3)

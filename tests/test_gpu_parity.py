@@ -169,6 +169,8 @@ def test_empty_and_degenerate():
     dict(variant=R.SMALL, lanes_per_row=16, rows_per_lane=1),
     dict(variant=R.SMALL, lanes_per_row=32, rows_per_lane=8, blocks_per_cu=1),
     dict(variant=R.SMALL, rows_per_lane=2, blocks_per_cu=1),
+    dict(variant=R.SMALL, block=64, rows_per_lane=1),
+    dict(variant=R.SMALL, block=128, rows_per_lane=8, blocks_per_cu=1),
     dict(variant=R.MEDIUM, waves_per_row=1, rows_per_block=8, blocks_per_cu=1),
     dict(variant=R.MEDIUM, waves_per_row=2, blocks_per_cu=1),
     dict(variant=R.MEDIUM, waves_per_row=16),
