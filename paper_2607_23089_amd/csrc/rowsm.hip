@@ -346,6 +346,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->variant = variant;
         p->wpr = 1;
         p->packed = false;
+        p->measured = true;
       } else if (shape.wpr > 0) {
         p->wpr = shape.wpr;
         p->vpl = (int)cdiv(nvec, (int64_t)shape.wpr * kWave);
@@ -730,8 +731,11 @@ bool stream_capturing(hipStream_t s) {
 template <typename Replan>
 int prepare_capture(const rowsm_config* cfg, Call* c, Replan replan) {
   Plan* p = &c->p;
+  // The single-read form exchanges through the workspace at any S (S = 1
+  // included); the two-pass form only with several blocks per row.
   const int S = p->split > 0 ? p->split : p->stream;
-  if (p->variant != ROWSM_LARGE || S <= 1 || !stream_capturing(c->st)) return ROWSM_OK;
+  const bool exchanges = p->split > 0 || p->stream > 1;
+  if (p->variant != ROWSM_LARGE || !exchanges || !stream_capturing(c->st)) return ROWSM_OK;
   const int64_t groups = kCaptureMaxBlocks / S;
   const int64_t blocks = (c->rows < groups ? c->rows : groups) * S;
   if (split_capture_reserve(blocks, &c->cap_slice) == ROWSM_OK) {
@@ -739,6 +743,20 @@ int prepare_capture(const rowsm_config* cfg, Call* c, Replan replan) {
     return ROWSM_OK;
   }
   if (cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
+  if (p->measured) {
+    // A row that the measured table sent to the single-read form fits the
+    // medium form, which keeps no state between launches either and reads
+    // x once: the medium family's own plan.
+    rowsm_config medium;
+    if (cfg) {
+      medium = *cfg;
+    } else {
+      std::memset(&medium, 0, sizeof(medium));
+      medium.packed = -1;
+    }
+    medium.variant = ROWSM_MEDIUM;
+    return replan(&medium);
+  }
   // The two-pass form with one block per row keeps no state between
   // launches (a grid cap of one block per compute unit, unless given).
   rowsm_config two_pass;

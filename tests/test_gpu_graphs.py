@@ -257,12 +257,44 @@ def test_forced_split_form_under_capture():
     assert R.rowsm_split_wait_failures() == 0
 
 
+@pytest.mark.parametrize("rows,cols,din,dout,cfg,want", [
+    # the launcher's own single-read pick with one block per row (a full
+    # launch of 1536-vector rows), more rows than one capture slice holds
+    (40000, 6144, "f32", "f32", None, "split=1 "),
+    # forced: one block per row, and two
+    (1000, 3000, "bf16", "f32", dict(variant=R.LARGE, split_blocks=1), "split=1 "),
+    (9000, 16384, "bf16", "bf16", None, "split=2 "),
+])
+def test_single_read_one_block_per_row_under_capture(rows, cols, din, dout, cfg, want):
+    # every single-read launch exchanges through the workspace, one block
+    # per row included: under capture it takes a slice like any other, and
+    # replays (with eager single-read launches in between) match eager
+    # launches bitwise
+    config = R.RowsmConfig(**cfg) if cfg else None
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]), config)
+    assert st == R.OK and want in desc, desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols, device=DEV)
+    y = torch.empty(rows, cols, dtype=DT[dout], device=DEV)
+    ref = R.softmax(x, out_dtype=DT[dout], config=config).clone()
+    g = capture(lambda: R.softmax(x, out=y, config=config))
+    for i in range(3):
+        y.zero_()
+        eager_split_launch()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref), f"replay {i} [{desc}]"
+    assert R.rowsm_split_wait_failures() == 0
+
+
 @pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")  # refused launches record nothing
 def test_zz_capture_region_exhausted_falls_back():
     # Runs last in this file: it fills the per-device capture region (64 MiB,
     # 1 MiB per captured 2^15-block launch).  A forced single-read launch is
-    # then refused under capture and the launcher's own plan takes the
-    # two-pass form, whose replays stay exact.
+    # then refused under capture, the launcher's own plan for long rows takes
+    # the two-pass form and its single-read pick for medium-length rows the
+    # medium form; their replays stay exact.
     eager_split_launch()
     rows, cols = 4096, 4096
     x = torch.zeros(rows, cols, device=DEV)
@@ -296,3 +328,25 @@ def test_zz_capture_region_exhausted_falls_back():
         assert res["ok"], f"two-pass fallback replay {i}: {res}"
 
     replay_and_check(g, lambda i: xl.copy_(xs[i].to(DEV)), check)
+    # a full launch of medium-length rows that the launcher sends to the
+    # single-read form takes the medium form instead (no state, one read)
+    rows_m, cols_m = 8201, 6144
+    st, desc = R.rowsm_describe(rows_m, cols_m, R.F32, R.F32)
+    assert st == R.OK and "split=1 " in desc, desc
+    xm_src = [W.random_matrix(rows_m, cols_m, "f32", sigma=4.0, seed=70 + i) for i in range(3)]
+    xm = torch.empty(rows_m, cols_m, device=DEV)
+    ym = torch.empty_like(xm)
+    xm.copy_(xm_src[0].to(DEV))
+    gm = capture(lambda: R.softmax(xm, out=ym))
+    sample = list(range(0, rows_m, 211)) + [rows_m - 1]
+
+    def check_m(i):
+        want = R.softmax(xm, variant=R.MEDIUM)
+        torch.cuda.synchronize()
+        assert torch.equal(ym, want), f"medium fallback replay {i}"
+        res = compare(out_np(ym[sample], "f32"),
+                      oracle.softmax_f64(widen(xm_src[i][sample]), threads=4), "f32")
+        assert res["ok"], f"medium fallback replay {i}: {res}"
+
+    replay_and_check(gm, lambda i: xm.copy_(xm_src[i].to(DEV)), check_m)
+    assert R.rowsm_split_wait_failures() == 0
