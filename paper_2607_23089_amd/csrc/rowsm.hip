@@ -145,19 +145,20 @@ bool few_long_rows(int64_t rows, int64_t row_bytes, bool packed, int cus,
 // group of wpr waves with rpb rows per block (S == 0), or the single-read
 // form with S blocks of T threads per row.  From sweeps of 1024-16384
 // columns in every dtype pair (8192-262144 rows, launches timed alone after
-// a cache-evicting write, two boxes agreeing within 1.5%), at the lengths
-// 128 x 2^k, 192 x 2^k and the lengths between: the medium form is fastest
-// with two to four vectors per lane and one or two rows per block, rows of more than
-// about 1280 vectors in the single-read form with 512 threads per row; rows
-// that widen (bf16 -> fp32) or narrow (fp32 -> bf16) keep the medium form
-// longer.  At those lengths the picks are within 2-3% of the fastest form
-// measured, where the previous rule (at most 16 fp32 values per lane,
-// 512-thread blocks) was up to 35% slower.  The form that wins changes
-// with the length in ways no simple count of slots or bytes per lane
-// predicts (the same geometry in the medium and the single-read kernel can
-// differ by 15% either way), hence a table.  Smaller launches keep the
-// previous rule: at 8-16 rows per compute unit fewer waves per row measured
-// fastest.  false for bf16 -> bf16 rows beyond 2048 vectors (not swept).
+// a cache-evicting write, two boxes agreeing within 1.5%): the medium form
+// is fastest with two to four vectors per lane and one or two rows per
+// block, rows of more than about 1280 vectors in the single-read form with
+// 512 threads per row; rows that widen (bf16 -> fp32) or narrow
+// (fp32 -> bf16) keep the medium form longer.  At the fitted lengths the
+// picks are within 3% of the fastest form measured (the previous rule, at
+// most 16 fp32 values per lane in 512-thread blocks, up to 24% slower), and
+// 1.5% above it on geometric mean at 44 lengths the table was not fitted to
+// (the previous rule 5.8%, at most 55%).  The form that wins changes with
+// the length in ways no count of slots or bytes per lane predicts (the
+// medium and the single-read kernel at the same geometry differ by up to
+// 20% either way), hence a table.  Smaller launches keep the previous rule:
+// at 8-16 rows per compute unit fewer waves per row measured fastest.
+// false for bf16 -> bf16 rows beyond 2048 vectors (not swept).
 struct RowShape {
   int wpr = 0, rpb = 0, S = 0, T = 0;
 };
