@@ -14,7 +14,8 @@
 //           rows too long even for that, two streaming passes over tiles
 //           (several blocks per row for few rows, stream_blocks()).
 // Rows of 129-4096 vectors in launches of at least 32 rows per compute unit
-// take measured launch shapes (medium or single-read, measured_row_shape()).
+// take measured launch shapes (medium or single-read, measured_row_shape()
+// and, for the fused form with fp32 output, measured_fused_shape()).
 // Row count: a launch of few rows must still fill the device, so fewer than
 // cus/4 rows of >= 384 KiB each (at most cus/4 rows for the packed form) take
 // the split form rather than one block per row, and the split form gives
@@ -188,6 +189,39 @@ bool measured_row_shape(int64_t nvec, int ib, int ob, RowShape* r) {
   return true;
 }
 
+// The same for the fused scale + causal mask form with fp32 output (fp32 or
+// bf16 input; the fused form writes every output entry but reads only the
+// kept ones, so its traffic leans to writes): the medium form with two to
+// five vectors per lane, wave groups growing with the row, and the
+// single-read form with 512 threads per row beyond 3072 vectors.  From
+// sweeps of 1024-16384-column causal heads (16384-262144 rows, every launch
+// timed alone after a cache-evicting write): 0.5% above the fastest form
+// measured on geometric mean (at most 3.4%), where the rule of at most 32
+// values per lane was 11% above it (at most 22%); 0.7% at lengths held out
+// of the fp32 fit (the rule 6%, at most 18%), and 2.2% (at most 9%) at a
+// third set of lengths, where the rule was about 4.5% above it (at most
+// 13%).  Fused rows with bf16 output
+// keep that rule, which was within 3.5% of the fastest form at every length.
+bool measured_fused_shape(int64_t nvec, int ib, int ob, RowShape* r) {
+  if (ob != 4 || nvec <= 128 || nvec > 4096) return false;
+  struct Row {
+    int upto, wpr, rpb, S, T;
+  };
+  static constexpr Row kF32[] = {{256, 2, 1, 0, 0},    {1024, 4, 1, 0, 0},
+                                 {2048, 8, 1, 0, 0},   {3072, 16, 1, 0, 0},
+                                 {4096, 0, 0, 2, 256}};
+  static constexpr Row kWiden[] = {{256, 2, 2, 0, 0},   {512, 2, 1, 0, 0},
+                                   {1280, 4, 1, 0, 0},  {2560, 8, 1, 0, 0},
+                                   {3072, 16, 1, 0, 0}, {4096, 0, 0, 2, 256}};
+  const Row* t = ib == 4 ? kF32 : kWiden;
+  while (nvec > t->upto) ++t;
+  r->wpr = t->wpr;
+  r->rpb = t->rpb;
+  r->S = t->S;
+  r->T = t->T;
+  return true;
+}
+
 // Blocks per row for a split launch of fewer than cus rows with T-thread
 // blocks holding at most nv_cap vectors per thread: about one block per
 // compute unit over the launch (the largest power of two with rows * S <=
@@ -333,12 +367,15 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->vpl = vpl;
     p->packed = packed;
     // Full launches of rows of 129-4096 full vectors, when nothing about the
-    // shape is forced: the measured shapes of measured_row_shape().
+    // shape is forced: the measured shapes of measured_row_shape() (fused
+    // form: measured_fused_shape()).
     const bool shape_free = !cfg || (cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
                                      cfg->packed == -1 && cfg->block == 0 &&
                                      cfg->split_blocks == 0 && cfg->vw == 0);
-    if (auto_variant && !fused && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
-        rows >= 32 * (int64_t)cus && measured_row_shape(nvec, ib, ob, &shape)) {
+    if (auto_variant && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
+        rows >= 32 * (int64_t)cus &&
+        (fused ? measured_fused_shape(nvec, ib, ob, &shape)
+               : measured_row_shape(nvec, ib, ob, &shape))) {
       // (a single-read pick holds one group of blocks per row only while
       // the rows fit the exchange workspace; beyond, the medium rule stays)
       if (shape.S > 0 && rows * shape.S > kSplitMaxBlocks) shape = RowShape{};

@@ -171,8 +171,17 @@ def test_select_regimes(lib):
     t = R.rowsm_describe_op(R.OP_SOFTMAX, 100000, 8192, R.F32, R.F32,
                             R.RowsmConfig(waves_per_row=8))[1]
     assert has(t, "medium", "wpr=8 ", "vpl=4 ")
-    t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 100000, 2048, R.F32, R.F32)[1]
-    assert has(t, "medium", "wpr=1 ", "vpl=8 ")  # 32 values per lane
+    t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 100000, 2048, R.F32, R.BF16)[1]
+    assert has(t, "medium", "wpr=1 ", "vpl=8 ")  # fused, bf16 out: 32 values per lane
+    # the fused form with fp32 output has a table of its own
+    fd = lambda cols, i: R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 100000, cols, i, R.F32)[1]
+    assert has(fd(1024, R.F32), "medium", "wpr=2 ", "vpl=2 ", "block=128 ")
+    assert has(fd(4096, R.F32), "medium", "wpr=4 ", "vpl=4 ", "block=256 ")
+    assert has(fd(12288, R.F32), "medium", "wpr=16 ", "vpl=3 ")
+    assert has(fd(16384, R.F32), "large", "split=2 ", "block=256 ")
+    assert has(fd(1024, R.BF16), "medium", "wpr=2 ", "block=256 ")
+    assert has(fd(2048, R.BF16), "medium", "wpr=2 ", "vpl=4 ", "block=128 ")
+    assert has(fd(5120, R.BF16), "medium", "wpr=4 ", "vpl=5 ")
     assert has(d(100000, 24576, R.BF16, R.BF16)[1], "medium", "wpr=16 ")
     # a single-read pick only while one group of blocks per row fits the
     # 2^20-block exchange workspace

@@ -116,3 +116,29 @@ def test_causal_workload_in_kernel_mask_matches_stored_mask():
     for r in (0, 1, 4095, 4096, 20000, 32767):
         assert_fused_parity(x[r:r + 1].cpu(), y_fused[r:r + 1].cpu(), "bf16", 1.0, w.period, 0,
                             f"fused causal row {r}", row0=r)
+
+
+@pytest.mark.parametrize("cols,din,want", [
+    (1024, "f32", ("medium", "wpr=2 ", "block=128 ")),
+    (4096, "f32", ("medium", "wpr=4 ", "vpl=4 ")),
+    (12288, "f32", ("medium", "wpr=16 ", "vpl=3 ")),
+    (16384, "f32", ("large", "split=2 ", "block=256 ")),
+    (2048, "bf16", ("medium", "wpr=2 ", "vpl=4 ", "block=128 ")),
+    (5120, "bf16", ("medium", "wpr=4 ", "vpl=5 ")),
+    (16384, "bf16", ("large", "split=2 ", "block=256 "))])
+def test_fused_measured_launch_shapes(cols, din, want):
+    # full launches of causal heads with fp32 output take the measured fused
+    # shapes; blocks of sampled rows element by element against the oracle
+    rows, scale = 8201, 0.125
+    st, desc = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, rows, cols, R.dtype_code(DT[din]), R.F32)
+    assert st == R.OK and all(w in desc for w in want), desc
+    print(f"fused measured shape {rows}x{cols} {din}->f32: {desc}", flush=True)
+    x = W.random_matrix(rows, cols, din, sigma=5.0, seed=cols + 11, device=DEV)
+    y = R.scaled_causal_softmax(x, scale, cols, 0, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for r0 in (0, cols - 3, rows // 2, rows - 4):
+        xs, ys = x[r0:r0 + 4].cpu(), y[r0:r0 + 4].cpu()
+        assert_fused_parity(xs, ys, "f32", scale, cols, 0, f"{rows}x{cols} rows {r0}+ [{desc}]",
+                            row0=r0)
+    assert R.rowsm_split_wait_failures() == 0
+    del x, y
