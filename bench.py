@@ -28,6 +28,11 @@ plain copy moving the same bytes in the same run, reported per launch as
 
 Prints ONE JSON line (rank 0).  ``--gpus`` above 1 is refused: this path runs
 on one GPU (rows shard across GPUs without communication).
+
+``--launcher-check`` runs no step: it times the launcher's choice for full
+launches of representative row lengths against the library's other launch
+shapes (each launch alone after a cache-evicting write) and prints that as
+the JSON line.
 """
 from __future__ import annotations
 
@@ -475,6 +480,74 @@ def fused_causal_leg(reps: int):
     }
 
 
+LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype): full launches
+    ("softmax", 4194304, 64, "bf16", "bf16"),
+    ("softmax", 32768, 4096, "f32", "f32"),
+    ("softmax", 65536, 2048, "bf16", "f32"),
+    ("softmax", 20480, 9216, "bf16", "bf16"),
+    ("softmax", 16384, 8192, "f32", "f32"),
+    ("softmax", 20480, 12288, "bf16", "bf16"),
+    ("softmax", 20480, 10240, "bf16", "f32"),
+    ("scaled_causal", 16384, 4096, "f32", "f32"),
+    ("scaled_causal", 32768, 16384, "f32", "f32"),
+]
+
+
+def launcher_check(reps: int = 8):
+    """The launcher's choice for full launches of the shapes above against the
+    other launch shapes of the library (medium wave groups with the default
+    or one row per block, the single-read form with 1-4 blocks of 256 or 512
+    threads, and for the small rows the grid capped at 8 or 64 blocks per
+    compute unit), each launch timed alone after a cache-evicting write.
+    Every timed shape makes reps + 2 launches, in the order listed."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    out = []
+    for op, rows, cols, din, dout in LAUNCHER_SHAPES:
+        x = W.random_matrix(rows, cols, din, sigma=3.0, seed=cols, device=dev)
+        y = torch.empty(rows, cols, dtype=W.TORCH_DTYPES[dout], device=dev)
+        if cols <= 256:
+            alts = [("auto", None)] + [(f"bpc{b}", R.RowsmConfig(blocks_per_cu=b)) for b in (8, 64)]
+        else:
+            alts = ([("auto", None)] +
+                    [(f"M{w}", R.RowsmConfig(variant=R.MEDIUM, waves_per_row=w))
+                     for w in (1, 2, 4, 8, 16)] +
+                    [(f"M{w}r1", R.RowsmConfig(variant=R.MEDIUM, waves_per_row=w,
+                                               rows_per_block=1)) for w in (2, 4, 8)] +
+                    [(f"S{S}T{T}", R.RowsmConfig(variant=R.LARGE, split_blocks=S, block=T))
+                     for S in (1, 2, 4) for T in (256, 512)])
+        code = R.OP_SCALED_CAUSAL if op == "scaled_causal" else R.OP_SOFTMAX
+        rec = {"op": op, "rows": rows, "cols": cols, "in": din, "out": dout,
+               "launch": R.rowsm_describe_op(code, rows, cols, R.dtype_code(x.dtype),
+                                             R.dtype_code(y.dtype))[1],
+               "timed": [], "us": {}}
+        for name, cfg in alts:
+            def call(cfg=cfg):
+                if op == "scaled_causal":
+                    R.scaled_causal_softmax(x, 0.125, cols, 0, out=y, config=cfg)
+                else:
+                    R.softmax(x, out=y, config=cfg)
+            try:
+                rec["us"][name] = timed_alone(call, reps, flush, stream)
+            except R.RowsmError:
+                continue  # a shape the family cannot take: refused, nothing launched
+            rec["timed"].append(name)
+        best = min(rec["us"], key=rec["us"].get)
+        rec["best"] = best
+        rec["auto_over_best"] = rec["us"]["auto"] / rec["us"][best]
+        out.append(rec)
+        del x, y
+    if R.rowsm_split_wait_failures() != 0:
+        raise R.RowsmError("split-row exchange waits gave up: results invalid")
+    return {"launcher_check": out, "reps_per_shape": reps + 2}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__,
                                  formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -490,6 +563,10 @@ def main() -> int:
                     help="host threads of the CPU baseline (0 = every core this process may use)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="minimum seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--launcher-check", action="store_true",
+                    help="instead of the step: time the launcher's choice for full launches "
+                         "of representative row lengths against the library's other launch "
+                         "shapes, and print that as the JSON line")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -506,6 +583,9 @@ def main() -> int:
     R.lib()  # fails loudly when the HIP library is missing
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.launcher_check:
+        print(json.dumps(launcher_check()), flush=True)
+        return 0
     regimes = list(W.REGIMES if not args.regimes else args.regimes.split(","))
 
     inputs, outputs, calls = {}, {}, []
