@@ -480,7 +480,7 @@ def fused_causal_leg(reps: int):
     }
 
 
-LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype): full launches
+LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype)
     ("softmax", 4194304, 64, "bf16", "bf16"),
     ("softmax", 32768, 4096, "f32", "f32"),
     ("softmax", 65536, 2048, "bf16", "f32"),
@@ -488,13 +488,15 @@ LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype): full launches
     ("softmax", 16384, 8192, "f32", "f32"),
     ("softmax", 20480, 12288, "bf16", "bf16"),
     ("softmax", 20480, 10240, "bf16", "f32"),
+    ("softmax", 2048, 12288, "bf16", "bf16"),
+    ("softmax", 1024, 8192, "f32", "f32"),
     ("scaled_causal", 16384, 4096, "f32", "f32"),
     ("scaled_causal", 32768, 16384, "f32", "f32"),
 ]
 
 
 def launcher_check(reps: int = 8):
-    """The launcher's choice for full launches of the shapes above against the
+    """The launcher's choice for launches of the shapes above against the
     other launch shapes of the library (medium wave groups with the default
     or one row per block, the single-read form with 1-4 blocks of 256 or 512
     threads, and for the small rows the grid capped at 8 or 64 blocks per
@@ -564,7 +566,7 @@ def main() -> int:
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="minimum seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--launcher-check", action="store_true",
-                    help="instead of the step: time the launcher's choice for full launches "
+                    help="instead of the step: time the launcher's choice for launches "
                          "of representative row lengths against the library's other launch "
                          "shapes, and print that as the JSON line")
     args = ap.parse_args()

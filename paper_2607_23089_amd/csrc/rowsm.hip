@@ -366,14 +366,44 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->wpr = wpr;
     p->vpl = vpl;
     p->packed = packed;
-    // Full launches of rows of 129-4096 full vectors, when nothing about the
-    // shape is forced: the measured shapes of measured_row_shape() (fused
-    // form: measured_fused_shape()).
+    // Launches of 4-16 rows per compute unit (softmax and log forms, rows of
+    // full vectors under 64 KiB of input, nothing about the shape forced):
+    // the fewest waves per row, at least what the registers need, that still
+    // give the launch about two 512-thread blocks per compute unit, so that
+    // each lane keeps more bytes in flight.  From sweeps of 1024-16384
+    // columns in every dtype pair: at 1024 and 2048 rows 1.6% above the
+    // fastest form measured on geometric mean (at most 9%), where the rule
+    // above was 8.9% (at most 54%); at 1536 and 3072 rows, not fitted, 4.8%
+    // (at most 24%) against 12% (at most 44%).  At 4096 and 6144 rows the two
+    // rules tie on geometric mean and the rule above stays.
     const bool shape_free = !cfg || (cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
                                      cfg->packed == -1 && cfg->block == 0 &&
                                      cfg->split_blocks == 0 && cfg->vw == 0);
-    if (auto_variant && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
-        rows >= 32 * (int64_t)cus &&
+    const bool full_vw = vw * (ib > ob ? ib : ob) == 16;
+    if (auto_variant && !fused && shape_free && full_vw && rows >= 4 * (int64_t)cus &&
+        rows < 16 * (int64_t)cus && cols * ib < 65536) {
+      int target = 1;
+      while ((int64_t)target * 2 * rows <= 16 * (int64_t)cus) target <<= 1;
+      for (int w = target; w <= 16; w <<= 1) {
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v * vw <= 64 && medium_unpacked_cap(vw, v)) {
+          p->wpr = w;
+          p->vpl = v;
+          p->packed = false;
+          break;
+        }
+        if (in_dt == ROWSM_BF16 && vw == 8 && v >= 9 && v <= 24) {
+          p->wpr = w;
+          p->vpl = v;
+          p->packed = true;
+          break;
+        }
+      }
+    }
+    // Full launches of rows of 129-4096 full vectors, when nothing about the
+    // shape is forced: the measured shapes of measured_row_shape() (fused
+    // form: measured_fused_shape()).
+    if (auto_variant && shape_free && full_vw && rows >= 32 * (int64_t)cus &&
         (fused ? measured_fused_shape(nvec, ib, ob, &shape)
                : measured_row_shape(nvec, ib, ob, &shape))) {
       // (a single-read pick holds one group of blocks per row only while

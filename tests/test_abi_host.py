@@ -163,6 +163,15 @@ def test_select_regimes(lib):
     assert has(d(100000, 12288, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
     assert has(d(100000, 16384, R.F32, R.F32)[1], "large", "split=2 ", "block=512 ")
     assert has(d(100000, 16384, R.BF16, R.F32)[1], "large", "split=2 ", "block=256 ")
+    # 4-16 rows per compute unit: the fewest waves per row that keep about two
+    # 512-thread blocks per compute unit (at least what the registers need)
+    assert has(d(1024, 8192, R.BF16, R.BF16)[1], "medium", "wpr=4 ", "vpl=4 ", "block=512 ")
+    assert has(d(2048, 12288, R.BF16, R.BF16)[1], "medium", "wpr=2 ", "packed=1 ", "block=512 ")
+    assert has(d(2048, 4096, R.F32, R.F32)[1], "medium", "wpr=2 ", "vpl=8 ", "block=512 ")
+    assert has(d(4095, 8192, R.F32, R.F32)[1], "medium", "wpr=2 ", "vpl=16 ")
+    assert has(d(4096, 4096, R.F32, R.F32)[1], "medium", "wpr=4 ", "vpl=4 ")   # the rule below
+    assert has(d(1023, 4096, R.F32, R.F32)[1], "medium", "wpr=4 ", "vpl=4 ")
+    assert has(d(2048, 16384, R.F32, R.F32)[1], "large")                      # 64 KiB rows
     # not below 32 rows per compute unit, nor for misaligned rows, forced
     # shapes, the fused form or bf16 rows beyond 2048 vectors
     assert has(d(8191, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")

@@ -443,6 +443,22 @@ def test_measured_launch_shapes(cols, din, dout, want):
     del x, y
 
 
+@pytest.mark.parametrize("rows,cols,din,dout,want", [
+    (1024, 8192, "bf16", "bf16", ("wpr=4 ", "vpl=4 ")),
+    (2048, 12288, "bf16", "bf16", ("wpr=2 ", "packed=1 ")),
+    (1531, 4096, "f32", "f32", ("wpr=2 ", "vpl=8 ")),
+    (3001, 14336, "bf16", "f32", ("wpr=4 ", "vpl=14 "))])
+def test_few_rows_per_cu_shapes(rows, cols, din, dout, want):
+    # launches of 4-16 rows per compute unit: few waves per row, many bytes
+    # per lane (the packed bf16 form among them); every row against the oracle
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("medium") and all(w in desc for w in want), desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + cols, device=DEV)
+    y = run(x, dout)
+    sample = list(range(0, rows, 7)) + [rows - 1]
+    assert_parity(x[sample].cpu(), y[sample].cpu(), dout, f"{rows}x{cols} {din}->{dout} [{desc}]")
+
+
 @pytest.mark.parametrize("rows,cols", [(4099, 64), (4099, 1000), (4099, 4097)])
 def test_many_rows_grid_stride(rows, cols):
     # the small and medium families' default grid (a task per wave or block)
