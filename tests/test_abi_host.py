@@ -203,6 +203,11 @@ def test_select_regimes(lib):
     assert bd(1024, 16384, R.F32, R.F32).startswith("large")
     assert "split=8 " in bd(1024, 16384, R.F32, R.F32) and "block=256" in bd(1024, 16384, R.F32, R.F32)
     assert bd(4096, 8192, R.F32, R.F32).startswith("medium")   # 32 KiB rows: unchanged
+    assert "wpr=16 " in bd(4096, 8192, R.F32, R.F32)
+    # backward launches of 4-16 rows per compute unit: few waves per row
+    assert "wpr=4 " in bd(1024, 8192, R.F32, R.F32) and "vpl=8 " in bd(1024, 8192, R.F32, R.F32)
+    assert "wpr=2 " in bd(2048, 6144, R.BF16, R.F32) and "vpl=12 " in bd(2048, 6144, R.BF16, R.F32)
+    assert "wpr=16 " in bd(1023, 8192, R.F32, R.F32)
     # few long rows (>= 384 KiB of traffic): the split form fills the device
     # (the select assumes 256 compute units)
     assert s(63, 65536, R.F32, R.F32) == R.LARGE

@@ -94,6 +94,23 @@ FORMS = {
 }
 
 
+@pytest.mark.parametrize("rows,cols,din,dout,want", [
+    (1024, 8192, "f32", "f32", ("wpr=4 ", "vpl=8 ")),
+    (2048, 6144, "bf16", "f32", ("wpr=2 ", "vpl=12 ")),
+    (1531, 16384, "bf16", "bf16", ("wpr=4 ", "vpl=8 "))])
+def test_bwd_few_rows_per_cu_shapes(rows, cols, din, dout, want):
+    # launches of 4-16 rows per compute unit: few waves per row, many bytes of
+    # each input per lane; sampled rows against the oracle
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("medium") and all(w in desc for w in want), desc
+    y, dy = inputs(rows, cols, din, alpha=0.2, seed=rows)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
+    sample = list(range(0, rows, 11)) + [rows - 1]
+    assert_bwd_parity(y[sample], dy[sample], dx[sample].cpu(), dout,
+                      f"bwd {rows}x{cols} {din}->{dout} [{desc}]")
+
+
 @pytest.mark.parametrize("rows,cols,din,dout", [
     (1024, 16384, "f32", "f32"), (1024, 32768, "bf16", "f32"), (1024, 32768, "bf16", "bf16"),
     (300, 65536, "f32", "f32")])
