@@ -223,6 +223,16 @@ def test_select_regimes(lib):
 def test_describe(lib):
     st, text = R.rowsm_describe(262144, 64, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("small") and "lpr=8" in text and "vw=8" in text
+    # rows that fill their lanes in launches of 40-160 MiB: one-wave blocks,
+    # one row group per lane; otherwise 256-thread blocks, 4 row groups
+    assert "block=64 " in text and "rpl=1 " in text and "grid=32768 " in text
+    for rows, cols, dt in [(131072, 64, R.BF16), (1048576, 64, R.BF16), (262144, 48, R.BF16)]:
+        t = R.rowsm_describe(rows, cols, dt, dt)[1]
+        assert "block=256 " in t and "rpl=4 " in t, t
+    t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 262144, 64, R.BF16, R.BF16)[1]
+    assert "block=256 " in t and "rpl=4 " in t, t                  # fused: 4 row groups
+    t = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 393216, 16, R.F32, R.F32)[1]
+    assert "block=64 " in t and "rpl=1 " in t, t
     st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("medium")
     st, text = R.rowsm_describe(128, 151936, R.BF16, R.BF16, R.MEDIUM)
