@@ -481,6 +481,7 @@ def fused_causal_leg(reps: int):
 
 
 LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype)
+    ("softmax", 262144, 64, "bf16", "bf16"),
     ("softmax", 4194304, 64, "bf16", "bf16"),
     ("softmax", 32768, 4096, "f32", "f32"),
     ("softmax", 65536, 2048, "bf16", "f32"),
@@ -499,8 +500,9 @@ def launcher_check(reps: int = 8):
     """The launcher's choice for launches of the shapes above against the
     other launch shapes of the library (medium wave groups with the default
     or one row per block, the single-read form with 1-4 blocks of 256 or 512
-    threads, and for the small rows the grid capped at 8 or 64 blocks per
-    compute unit), each launch timed alone after a cache-evicting write.
+    threads; for the small rows the grid capped at 8 or 64 blocks per compute
+    unit and blocks of 64 or 256 threads with 1 or 4 row groups per lane),
+    each launch timed alone after a cache-evicting write.
     Every timed shape makes reps + 2 launches, in the order listed."""
     import torch
 
@@ -515,7 +517,10 @@ def launcher_check(reps: int = 8):
         x = W.random_matrix(rows, cols, din, sigma=3.0, seed=cols, device=dev)
         y = torch.empty(rows, cols, dtype=W.TORCH_DTYPES[dout], device=dev)
         if cols <= 256:
-            alts = [("auto", None)] + [(f"bpc{b}", R.RowsmConfig(blocks_per_cu=b)) for b in (8, 64)]
+            alts = ([("auto", None)] +
+                    [(f"bpc{b}", R.RowsmConfig(blocks_per_cu=b)) for b in (8, 64)] +
+                    [(f"b{b}r{r}", R.RowsmConfig(block=b, rows_per_lane=r))
+                     for b, r in ((256, 4), (256, 1), (64, 1), (64, 4))])
         else:
             alts = ([("auto", None)] +
                     [(f"M{w}", R.RowsmConfig(variant=R.MEDIUM, waves_per_row=w))
