@@ -159,12 +159,16 @@ bool few_long_rows(int64_t rows, int64_t row_bytes, bool packed, int cus,
 // medium and the single-read kernel at the same geometry differ by up to
 // 20% either way), hence a table.  Smaller launches keep the previous rule:
 // at 8-16 rows per compute unit fewer waves per row measured fastest.
-// false for bf16 -> bf16 rows beyond 2048 vectors (not swept).
+// Widening rows continue to 8192 vectors, bf16 rows of 2049-4096 vectors
+// have picks of their own (sweeps of 18432-30720 columns, half of them not
+// fitted: within 1.7% of the fastest form, where the previous rule was up
+// to 12% slower).
 struct RowShape {
   int wpr = 0, rpb = 0, S = 0, T = 0;
 };
 bool measured_row_shape(int64_t nvec, int ib, int ob, RowShape* r) {
-  if (nvec <= 128 || nvec > 4096) return false;
+  const bool widen = ob > ib;
+  if (nvec <= 128 || nvec > (widen ? 8192 : 4096)) return false;
   struct Row {
     int upto, wpr, rpb, S, T;
   };
@@ -175,12 +179,19 @@ bool measured_row_shape(int64_t nvec, int ib, int ob, RowShape* r) {
                                   {3072, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
   static constexpr Row kWiden[] = {{256, 2, 1, 0, 0},    {512, 4, 1, 0, 0},
                                    {896, 4, 2, 0, 0},    {1792, 8, 1, 0, 0},
-                                   {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
+                                   {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256},
+                                   {8192, 0, 0, 2, 512}};
   static constexpr Row kNarrow[] = {{256, 2, 1, 0, 0},   {768, 4, 1, 0, 0},
                                     {1024, 4, 2, 0, 0},  {2048, 8, 1, 0, 0},
                                     {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
-  if (ib == ob && ib == 2 && nvec > 2048) return false;
-  const Row* t = ib == ob ? kSame : (ob > ib ? kWiden : kNarrow);
+  if (ib == ob && ib == 2 && nvec > 2048) {
+    // bf16 rows of 2049-4096 vectors: 512 threads per row, one block up to
+    // 2560 vectors, two beyond
+    r->S = nvec <= 2560 ? 1 : 2;
+    r->T = nvec <= 2560 ? 512 : 256;
+    return true;
+  }
+  const Row* t = ib == ob ? kSame : (widen ? kWiden : kNarrow);
   while (nvec > t->upto) ++t;
   r->wpr = t->wpr;
   r->rpb = t->rpb;

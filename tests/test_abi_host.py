@@ -173,7 +173,7 @@ def test_select_regimes(lib):
     assert has(d(1023, 4096, R.F32, R.F32)[1], "medium", "wpr=4 ", "vpl=4 ")
     assert has(d(2048, 16384, R.F32, R.F32)[1], "large")                      # 64 KiB rows
     # not below 32 rows per compute unit, nor for misaligned rows, forced
-    # shapes, the fused form or bf16 rows beyond 2048 vectors
+    # shapes or the fused form
     assert has(d(8191, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")
     assert has(d(8192, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
     assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=2 ")
@@ -191,7 +191,10 @@ def test_select_regimes(lib):
     assert has(fd(1024, R.BF16), "medium", "wpr=2 ", "block=256 ")
     assert has(fd(2048, R.BF16), "medium", "wpr=2 ", "vpl=4 ", "block=128 ")
     assert has(fd(5120, R.BF16), "medium", "wpr=4 ", "vpl=5 ")
-    assert has(d(100000, 24576, R.BF16, R.BF16)[1], "medium", "wpr=16 ")
+    assert has(d(100000, 24576, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 18432, R.BF16, R.BF16)[1], "large", "split=1 ", "block=512 ")
+    assert has(d(10000, 24576, R.BF16, R.F32)[1], "large", "split=2 ", "block=512 ")
+    assert has(d(10000, 36864, R.BF16, R.F32)[1], "large", "split=4 ")  # beyond 8192 vectors
     # a single-read pick only while one group of blocks per row fits the
     # 2^20-block exchange workspace
     assert has(d(524288, 8192, R.F32, R.F32)[1], "large", "split=2 ")

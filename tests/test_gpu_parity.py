@@ -416,6 +416,9 @@ MEASURED_SHAPES = [
     (14336, "f32", "f32", ("large", "split=2 ", "block=512 ")),
     (2560, "bf16", "bf16", ("medium", "wpr=4 ", "block=256 ")),
     (16384, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
+    (18432, "bf16", "bf16", ("large", "split=1 ", "block=512 ")),
+    (28672, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
+    (24576, "bf16", "f32", ("large", "split=2 ", "block=512 ")),
     (3072, "bf16", "f32", ("medium", "wpr=4 ", "block=512 ")),
     (6144, "bf16", "f32", ("medium", "wpr=8 ", "vpl=3 ")),
     (10240, "bf16", "f32", ("large", "split=1 ", "block=512 ")),
