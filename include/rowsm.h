@@ -88,11 +88,13 @@ typedef enum {
  * instantiations of one graph) must not run at the same time.  When no slice
  * is left, or the region does not exist yet (it is created with the shared
  * workspace by the first single-read launch outside capture on the device),
- * a captured LARGE plan uses the two-pass form with one block per row
- * instead (same results to the
- * stated tolerances, one extra read of each input), and a single-read form
- * forced through cfg->split_blocks > 0 returns ROWSM_EINVAL.  No entry point
- * records a memset or an allocation into a capture. */
+ * a captured LARGE plan is re-planned without workspace: a row that fits the
+ * registers of one medium block (which the launcher sent to the single-read
+ * form for speed) takes the medium form, any other row the two-pass form with
+ * one block per row (same results to the stated tolerances, one extra read
+ * of each input); a single-read form forced through cfg->split_blocks > 0
+ * returns ROWSM_EINVAL.  No entry point records a memset or an allocation
+ * into a capture. */
 typedef enum {
     ROWSM_AUTO = 0,
     ROWSM_SMALL = 1,
