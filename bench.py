@@ -493,6 +493,8 @@ LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype)
     ("softmax", 1024, 8192, "f32", "f32"),
     ("scaled_causal", 16384, 4096, "f32", "f32"),
     ("scaled_causal", 32768, 16384, "f32", "f32"),
+    ("backward", 1024, 8192, "f32", "f32"),
+    ("backward", 32768, 4096, "bf16", "bf16"),
 ]
 
 
@@ -514,7 +516,11 @@ def launcher_check(reps: int = 8):
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     out = []
     for op, rows, cols, din, dout in LAUNCHER_SHAPES:
-        x = W.random_matrix(rows, cols, din, sigma=3.0, seed=cols, device=dev)
+        if op == "backward":  # x holds probability rows, dy the upstream gradient
+            x = W.random_probabilities(rows, cols, din, 0.3, seed=cols, device=dev)
+            dy = W.random_matrix(rows, cols, din, sigma=1.0, seed=cols + 1, device=dev)
+        else:
+            x = W.random_matrix(rows, cols, din, sigma=3.0, seed=cols, device=dev)
         y = torch.empty(rows, cols, dtype=W.TORCH_DTYPES[dout], device=dev)
         if cols <= 256:
             alts = ([("auto", None)] +
@@ -529,7 +535,8 @@ def launcher_check(reps: int = 8):
                                                rows_per_block=1)) for w in (2, 4, 8)] +
                     [(f"S{S}T{T}", R.RowsmConfig(variant=R.LARGE, split_blocks=S, block=T))
                      for S in (1, 2, 4) for T in (256, 512)])
-        code = R.OP_SCALED_CAUSAL if op == "scaled_causal" else R.OP_SOFTMAX
+        code = {"scaled_causal": R.OP_SCALED_CAUSAL,
+                "backward": R.OP_SOFTMAX_BACKWARD}.get(op, R.OP_SOFTMAX)
         rec = {"op": op, "rows": rows, "cols": cols, "in": din, "out": dout,
                "launch": R.rowsm_describe_op(code, rows, cols, R.dtype_code(x.dtype),
                                              R.dtype_code(y.dtype))[1],
@@ -538,6 +545,8 @@ def launcher_check(reps: int = 8):
             def call(cfg=cfg):
                 if op == "scaled_causal":
                     R.scaled_causal_softmax(x, 0.125, cols, 0, out=y, config=cfg)
+                elif op == "backward":
+                    R.softmax_backward(x, dy, out=y, config=cfg)
                 else:
                     R.softmax(x, out=y, config=cfg)
             try:
