@@ -29,10 +29,13 @@
  *     uses a 32 MiB device workspace (and a 64 MiB region for captured
  *     launches, see HIP graphs below) that the first such call on a device
  *     allocates and clears (synchronously) and that lives until the process
- *     ends; make that first call outside stream capture.  Eager launches on
- *     one device are ordered one after another whatever their streams (each
- *     waits for the previous one through an event), so the workspace is never
- *     shared by two running launches.  The blocks of one row wait for each
+ *     ends; make that first call outside stream capture.  Eager single-read
+ *     launches on one device are ordered one after another whatever their
+ *     streams (each waits for the previous one through an event), so the
+ *     workspace is never shared by two running launches; the launcher takes
+ *     that form for long rows and for many full launches of medium-length
+ *     rows (rowsm_describe shows it as split > 0), which therefore do not
+ *     overlap across streams either.  The blocks of one row wait for each
  *     other; a launch's progress needs only that workgroups are dispatched
  *     in order, whatever else runs.  Work that itself waits on the device
  *     for blocks that are not yet resident (such a launch from another
