@@ -333,10 +333,13 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // slower below 32 MiB, level from 192 MiB, and 2-20% slower for rows
     // that leave lanes idle (48 or 96 bf16 columns, 100-column widening
     // rows), which keep the 256-thread blocks.
-    const int64_t launch_bytes = rows * cols * (ib + ob);
-    if (auto_variant && !fused && nvec == p->lpr &&
-        (!cfg || (cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->block == 0)) &&
-        launch_bytes >= ((int64_t)40 << 20) && launch_bytes <= ((int64_t)160 << 20)) {
+    // (row bytes are at most 32 vectors of 16 + 16 bytes here, so rows below
+    // the bound keep the product far from overflow)
+    const int64_t row_bytes = cols * (ib + ob);
+    const bool mid_launch = rows <= ((int64_t)160 << 20) / row_bytes &&
+                            rows * row_bytes >= ((int64_t)40 << 20);
+    if (auto_variant && !fused && nvec == p->lpr && mid_launch &&
+        (!cfg || (cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->block == 0))) {
       p->block = kWave;
       p->rpl = 1;
     }

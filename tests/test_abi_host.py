@@ -236,6 +236,9 @@ def test_describe(lib):
     assert "block=256 " in t and "rpl=4 " in t, t                  # fused: 4 row groups
     t = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 393216, 16, R.F32, R.F32)[1]
     assert "block=64 " in t and "rpl=1 " in t, t
+    # launch sizes whose byte count would not fit 64 bits take the default
+    t = R.rowsm_describe((1 << 61) + 1, 1, R.F32, R.F32)[1]
+    assert "block=256 " in t and "rpl=4 " in t, t
     st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("medium")
     st, text = R.rowsm_describe(128, 151936, R.BF16, R.BF16, R.MEDIUM)
