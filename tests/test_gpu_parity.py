@@ -473,6 +473,50 @@ def test_many_rows_grid_stride(rows, cols):
         assert_parity(x, y, "bf16", f"{rows}x{cols} cfg={cfg is not None}")
 
 
+def test_measured_single_read_picks_on_streams_and_threads():
+    # the launcher's own single-read picks for full launches of medium-length
+    # rows (one block of 512 threads, two of 256) from four host threads on
+    # four streams, interleaved with medium launches: bitwise equal to the
+    # same launches made one at a time
+    import threading
+    shapes = [(8192, 6144, "f32", "f32"), (8192, 16384, "bf16", "bf16"),
+              (8192, 6144, "bf16", "bf16"), (9000, 4096, "f32", "f32")]
+    xs, refs = [], []
+    for rows, cols, din, dout in shapes:
+        x = W.random_matrix(rows, cols, din, sigma=3.0, seed=rows + cols, device=DEV)
+        xs.append(x)
+        refs.append(run(x, dout))
+    descs = [R.rowsm_describe(r, c, R.dtype_code(DT[i]), R.dtype_code(DT[o]))[1]
+             for r, c, i, o in shapes]
+    assert "split=1 " in descs[0] and "split=2 " in descs[1], descs
+    errors = []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for _ in range(5):
+                    y = R.softmax(xs[i], out_dtype=DT[shapes[i][3]], stream=s)
+                    s.synchronize()
+                    if not torch.equal(y, refs[i]):
+                        errors.append(f"thread {i} [{descs[i]}]: result differs")
+                        return
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append(f"thread {i}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a launching thread did not finish"
+    assert not errors, errors
+    assert R.rowsm_split_wait_failures() == 0
+    for i, x in enumerate(xs):
+        sample = [0, x.shape[0] // 2, x.shape[0] - 1]
+        assert_parity(x[sample].cpu(), refs[i][sample].cpu(), shapes[i][3], f"shape {i}")
+
+
 def test_split_launches_from_host_threads():
     # four host threads, each with its own stream, launch single-read split
     # softmax and backward concurrently (the C calls run without the GIL):
