@@ -3,7 +3,8 @@
 ``python -m paper_2607_23089_amd.build`` or ``build_library()``.  hipcc
 cross-compiles for gfx950 without a GPU present.  The kernel families live in
 separate translation units (csrc/launch_*.hip), compiled in parallel and
-linked together with the launcher and C ABI (csrc/rowsm.hip).
+linked together with the launcher (csrc/plan.hip) and the C ABI
+(csrc/rowsm.hip).
 """
 from __future__ import annotations
 

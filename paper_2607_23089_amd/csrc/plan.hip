@@ -1,0 +1,794 @@
+// Launch planning of the row-softmax library: the row-length and row-count
+// launcher that picks a kernel family and its launch shape for each
+// operation (plan.hpp declares what the dispatch and the C ABI call).
+//
+// The launcher mirrors the structure the paper names for its running example
+// (small-, medium- and large-row kernels selected by a row launcher, preamble
+// listing style).  Its thresholds are this library's, stated in plan_for():
+//   SMALL   a row is at most 32 vectors (one vector per lane, >= 2 rows per wave)
+//   MEDIUM  the row fits the registers of at most 16 waves
+//           (<= 64 fp32 values per lane, or <= 24 raw 16-byte bf16 vectors
+//           per lane in the packed form)
+//   LARGE   anything longer: the row split over S <= 64 co-resident blocks
+//           that each hold their share in registers (single read), or, for
+//           rows too long even for that, two streaming passes over tiles
+//           (several blocks per row for few rows, stream_blocks()).
+// Rows of 129-4096 vectors in launches of at least 32 rows per compute unit
+// take measured launch shapes (medium or single-read, measured_row_shape()
+// and, for the fused form with fp32 output, measured_fused_shape()).
+// Row count: a launch of few rows must still fill the device, so fewer than
+// cus/4 rows of >= 384 KiB each (at most cus/4 rows for the packed form) take
+// the split form rather than one block per row, and the split form gives
+// each of fewer than cus rows up to cus/rows blocks (few_rows_split()).
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+
+#include "plan.hpp"
+
+namespace rowsm {
+namespace {
+
+std::atomic<int> g_cu_count[kMaxDevices];
+
+}  // namespace
+
+// Compute-unit count of the current device (cached per device).  Falls back
+// to 256, the MI355X count, when no device can be queried.
+int cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int n = g_cu_count[dev].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0)
+    n = 256;
+  g_cu_count[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+int dtype_bytes(int dt) { return dt == ROWSM_F32 ? 4 : 2; }
+bool dtype_ok(int dt) { return dt == ROWSM_F32 || dt == ROWSM_BF16; }
+
+namespace {
+
+int next_pow2(int v) {
+  int p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+
+// Vector widths (elements) with compiled kernels: 16-byte and 8-byte input
+// vectors, and single elements for rows that are not 8-byte aligned.
+bool vw_supported(int vw, int ib) { return vw == 1 || vw * ib == 16 || vw * ib == 8; }
+
+// Largest supported vector width that divides cols and keeps both the x and
+// the y accesses naturally aligned, with at most 16 bytes on either side: a
+// lane's output vector then never exceeds one 16-byte store, so each store
+// instruction of a wave writes one contiguous stretch of whole cache lines.
+int choose_vw(int64_t cols, int ib, int ob, uintptr_t xa, uintptr_t ya) {
+  for (int vw = 16 / (ib > ob ? ib : ob); vw > 1; vw >>= 1) {
+    if (!vw_supported(vw, ib)) continue;
+    const int xal = vw * ib;
+    const int yal = vw * ob < 16 ? vw * ob : 16;
+    if (cols % vw == 0 && xa % xal == 0 && ya % yal == 0) return vw;
+  }
+  return 1;
+}
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Grid limit of the small, medium and MoE families: one task (row group) per
+// wave or block up to 2^30 blocks, the waves striding over any tasks beyond
+// that; cfg->blocks_per_cu caps the grid at that many blocks per compute unit.
+// Grid-stride loops over a capped grid measured 4-8% slower at 1-4 M rows
+// (and slower still in plain store streams): waves that drift apart spread
+// the addresses in flight over the whole buffer, while the in-order blocks
+// of an uncapped grid keep them in one moving window.
+int64_t grid_cap(int bpc, int cus) {
+  return bpc ? (int64_t)cus * bpc : ((int64_t)1 << 30);
+}
+
+bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
+
+// Block size of the small-row and MoE kernels (whose waves work on their own
+// rows): 256 threads, or cfg->block when given, at most 256.
+int small_block(const rowsm_config* cfg, int* block) {
+  *block = 256;
+  if (cfg && cfg->block > 0) {
+    if (cfg->block > 256) return ROWSM_EINVAL;
+    *block = cfg->block;
+  }
+  return ROWSM_OK;
+}
+
+bool pow2_upto(int v, int hi) { return v >= 1 && v <= hi && (v & (v - 1)) == 0; }
+
+// Every override must lie in its documented domain, whichever family or form
+// ends up being used.
+bool config_in_domain(const rowsm_config* c) {
+  if (!c) return true;
+  return c->variant >= ROWSM_AUTO && c->variant <= ROWSM_LARGE && c->vw >= 0 &&
+         (c->lanes_per_row == 0 || pow2_upto(c->lanes_per_row, 32)) &&
+         (c->rows_per_lane == 0 || pow2_upto(c->rows_per_lane, 8)) &&
+         (c->waves_per_row == 0 || pow2_upto(c->waves_per_row, 16)) &&
+         c->rows_per_block >= 0 && c->rows_per_block <= 16 &&
+         c->packed >= -1 && c->packed <= 1 &&
+         c->block >= 0 && c->block <= 1024 && c->block % kWave == 0 &&
+         (c->tile_vectors == 0 || c->tile_vectors == 2 || c->tile_vectors == 4 ||
+          c->tile_vectors == 8) &&
+         c->blocks_per_cu >= 0 && c->split_blocks >= -1 && c->split_blocks <= 64 &&
+         c->prefetch >= -1 && c->prefetch <= 1;
+}
+
+// Row-count rules, from a sweep of 1-128 rows x 4096-262144 columns in every
+// dtype pair (cold caches): below ~384 KiB of traffic per row every form sits
+// at the launch floor; above it, a block per row on fewer than a quarter of
+// the compute units loses up to 17% to the split form (the packed bf16 form
+// up to 1.8x, still 1.4x at a quarter), and the split form is fastest with
+// about one block per compute unit over the launch.
+// The backward moves three streams per element and gains from splitting from
+// 512 KiB of traffic per row on.
+constexpr int64_t kFewRowsMinBytes = 384 * 1024;
+constexpr int64_t kFewRowsMinBytesBackward = 512 * 1024;
+bool few_long_rows(int64_t rows, int64_t row_bytes, bool packed, int cus,
+                   int64_t min_bytes = kFewRowsMinBytes) {
+  return row_bytes >= min_bytes && (packed ? rows <= cus / 4 : rows < cus / 4);
+}
+
+// Launch shape of a forward row of 129-4096 full 16-byte vectors in a launch
+// of at least 32 rows per compute unit (softmax and log forms): a medium
+// group of wpr waves with rpb rows per block (S == 0), or the single-read
+// form with S blocks of T threads per row.  From sweeps of 1024-16384
+// columns in every dtype pair (8192-262144 rows, launches timed alone after
+// a cache-evicting write, two boxes agreeing within 1.5%): the medium form
+// is fastest with two to four vectors per lane and one or two rows per
+// block, rows of more than about 1280 vectors in the single-read form with
+// 512 threads per row; rows that widen (bf16 -> fp32) or narrow
+// (fp32 -> bf16) keep the medium form longer.  At the fitted lengths the
+// picks are within 3% of the fastest form measured (the previous rule, at
+// most 16 fp32 values per lane in 512-thread blocks, up to 24% slower), and
+// 1.5% above it on geometric mean at 44 lengths the table was not fitted to
+// (the previous rule 5.8%, at most 55%).  The form that wins changes with
+// the length in ways no count of slots or bytes per lane predicts (the
+// medium and the single-read kernel at the same geometry differ by up to
+// 20% either way), hence a table.  Smaller launches keep the previous rule:
+// at 8-16 rows per compute unit fewer waves per row measured fastest.
+// Widening rows continue to 8192 vectors, bf16 rows of 2049-4096 vectors
+// have picks of their own (sweeps of 18432-30720 columns, half of them not
+// fitted: within 1.7% of the fastest form, where the previous rule was up
+// to 12% slower).
+struct RowShape {
+  int wpr = 0, rpb = 0, S = 0, T = 0;
+};
+bool measured_row_shape(int64_t nvec, int ib, int ob, RowShape* r) {
+  const bool widen = ob > ib;
+  if (nvec <= 128 || nvec > (widen ? 8192 : 4096)) return false;
+  struct Row {
+    int upto, wpr, rpb, S, T;
+  };
+  // {longest row (vectors), wpr, rpb, S, T}
+  static constexpr Row kSame[] = {{256, 2, 1, 0, 0},    {320, 4, 1, 0, 0},
+                                  {512, 4, 2, 0, 0},    {640, 4, 1, 0, 0},
+                                  {1280, 8, 1, 0, 0},   {1792, 0, 0, 1, 512},
+                                  {3072, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
+  static constexpr Row kWiden[] = {{256, 2, 1, 0, 0},    {512, 4, 1, 0, 0},
+                                   {896, 4, 2, 0, 0},    {1792, 8, 1, 0, 0},
+                                   {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256},
+                                   {8192, 0, 0, 2, 512}};
+  static constexpr Row kNarrow[] = {{256, 2, 1, 0, 0},   {768, 4, 1, 0, 0},
+                                    {1024, 4, 2, 0, 0},  {2048, 8, 1, 0, 0},
+                                    {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
+  if (ib == ob && ib == 2 && nvec > 2048) {
+    // bf16 rows of 2049-4096 vectors: 512 threads per row, one block up to
+    // 2560 vectors, two beyond
+    r->S = nvec <= 2560 ? 1 : 2;
+    r->T = nvec <= 2560 ? 512 : 256;
+    return true;
+  }
+  const Row* t = ib == ob ? kSame : (widen ? kWiden : kNarrow);
+  while (nvec > t->upto) ++t;
+  r->wpr = t->wpr;
+  r->rpb = t->rpb;
+  r->S = t->S;
+  r->T = t->T;
+  return true;
+}
+
+// The same for the fused scale + causal mask form with fp32 output (fp32 or
+// bf16 input; the fused form writes every output entry but reads only the
+// kept ones, so its traffic leans to writes): the medium form with two to
+// five vectors per lane, wave groups growing with the row, and the
+// single-read form with 512 threads per row beyond 3072 vectors.  From
+// sweeps of 1024-16384-column causal heads (16384-262144 rows, every launch
+// timed alone after a cache-evicting write): 0.5% above the fastest form
+// measured on geometric mean (at most 3.4%), where the rule of at most 32
+// values per lane was 11% above it (at most 22%); 0.7% at lengths held out
+// of the fp32 fit (the rule 6%, at most 18%), and 2.2% (at most 9%) at a
+// third set of lengths, where the rule was about 4.5% above it (at most
+// 13%).  Fused rows with bf16 output
+// keep that rule, which was within 3.5% of the fastest form at every length.
+bool measured_fused_shape(int64_t nvec, int ib, int ob, RowShape* r) {
+  if (ob != 4 || nvec <= 128 || nvec > 4096) return false;
+  struct Row {
+    int upto, wpr, rpb, S, T;
+  };
+  static constexpr Row kF32[] = {{256, 2, 1, 0, 0},    {1024, 4, 1, 0, 0},
+                                 {2048, 8, 1, 0, 0},   {3072, 16, 1, 0, 0},
+                                 {4096, 0, 0, 2, 256}};
+  static constexpr Row kWiden[] = {{256, 2, 2, 0, 0},   {512, 2, 1, 0, 0},
+                                   {1280, 4, 1, 0, 0},  {2560, 8, 1, 0, 0},
+                                   {3072, 16, 1, 0, 0}, {4096, 0, 0, 2, 256}};
+  const Row* t = ib == 4 ? kF32 : kWiden;
+  while (nvec > t->upto) ++t;
+  r->wpr = t->wpr;
+  r->rpb = t->rpb;
+  r->S = t->S;
+  r->T = t->T;
+  return true;
+}
+
+// Blocks per row for a split launch of fewer than cus rows with T-thread
+// blocks holding at most nv_cap vectors per thread: about one block per
+// compute unit over the launch (the largest power of two with rows * S <=
+// cus), at least 8, and at most what gives every thread two vectors (smaller
+// blocks measured slower); raised to the power of two that the register cap
+// needs.  0 when rows >= cus, or when the result exceeds 64 blocks per row or
+// 4 blocks per compute unit over the launch (a register-limited plan with
+// fewer, larger blocks then measured faster).
+int few_rows_split(int64_t rows, int64_t nvec, int T, int nv_cap, int cus) {
+  if (rows >= cus) return 0;
+  int sf = 1;
+  while (sf < 64 && rows * (sf * 2) <= cus) sf *= 2;
+  if (sf < 8) sf = 8;
+  while (sf > 1 && (int64_t)sf * T * 2 > nvec) sf >>= 1;
+  while ((int64_t)sf * T * nv_cap < nvec) sf *= 2;  // register cap
+  if (sf > 64 || rows * sf > 4 * (int64_t)cus) return 0;
+  return sf;
+}
+
+// Blocks per row of the two-pass LARGE form: 1 for launches of at least
+// 2 * cus rows, or with a grid capped per compute unit (bpc); otherwise the
+// power of two that gives the launch about two blocks per compute unit, at
+// most kStreamMaxSplit and the compute units, and at most what leaves every
+// thread U vectors of the row.  One block per row would leave a launch of
+// few such rows on a few compute units.
+int stream_blocks(int64_t rows, int64_t nvec, int T, int U, int bpc, int cus) {
+  if (bpc || rows >= 2 * (int64_t)cus) return 1;
+  int S = 1;
+  while (S * 2 <= kStreamMaxSplit && S * 2 <= cus && rows * S < 2 * (int64_t)cus) S *= 2;
+  while (S > 1 && (int64_t)S * T * U > nvec) S >>= 1;
+  return S;
+}
+
+}  // namespace
+
+// Forward plan: fills p for the family cfg asks for (AUTO resolves first)
+// and the config overrides; returns ROWSM_OK, or ROWSM_EINVAL when the family
+// cannot take this shape.  mode is the output form (kPlain, kFused or kLog);
+// the log form holds x where softmax holds exp(x - m), so it takes the plain
+// plans.
+int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
+             const rowsm_config* cfg, int cus, int mode, Plan* p) {
+  if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  const bool fused = mode == kFused;
+  const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
+  int vw = choose_vw(cols, ib, ob, xa, ya);
+  if (cfg && cfg->vw > 0) {
+    const int want = cfg->vw;
+    if (want > 16 / (ib > ob ? ib : ob) || (want & (want - 1)) || !vw_supported(want, ib) ||
+        cols % want ||
+        xa % (want * ib) || ya % (want * ob < 16 ? want * ob : 16))
+      return ROWSM_EINVAL;
+    vw = want;
+  }
+  const int nvec = (int)(cols / vw);
+  p->vw = vw;
+  p->nvec = nvec;
+
+  int variant = cfg ? cfg->variant : ROWSM_AUTO;
+  const bool auto_variant = variant == ROWSM_AUTO;
+  bool wide_row = false;  // a MEDIUM row redirected to the split form
+  RowShape shape;         // measured_row_shape() pick, when it applies
+  if (variant == ROWSM_AUTO) {
+    if (nvec <= 32) {
+      variant = ROWSM_SMALL;
+    } else if (nvec <= 16 * kWave * ((fused ? 32 : 64) / vw < 16 ? (fused ? 32 : 64) / vw : 16)) {
+      // whole row in the registers of one block, unless few long rows would
+      // then leave most of the device idle
+      variant = few_long_rows(rows, cols * (ib + ob), false, cus) ? ROWSM_LARGE : ROWSM_MEDIUM;
+    } else if (!fused && in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24) {
+      variant = few_long_rows(rows, cols * (ib + ob), true, cus) ? ROWSM_LARGE : ROWSM_MEDIUM;
+    } else {
+      variant = ROWSM_LARGE;
+    }
+  }
+  p->variant = variant;
+
+  const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
+  if (variant == ROWSM_SMALL) {
+    if (nvec > 32) return ROWSM_EINVAL;
+    p->lpr = next_pow2(nvec);
+    if (cfg && cfg->lanes_per_row > 0) {
+      const int l = cfg->lanes_per_row;
+      if ((l & (l - 1)) || l > 32 || l < p->lpr) return ROWSM_EINVAL;
+      p->lpr = l;
+    }
+    p->rpl = 4;
+    if (cfg && cfg->rows_per_lane > 0) {
+      const int r = cfg->rows_per_lane;
+      if (r != 1 && r != 2 && r != 4 && r != 8) return ROWSM_EINVAL;
+      if (fused && r != 4) return ROWSM_EINVAL;  // fused kernels: 4 rows per lane
+      p->rpl = r;
+    }
+    if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
+    // Rows that fill their lanes exactly, in launches of 40-160 MiB
+    // (softmax and log forms, nothing about the shape forced): one-wave
+    // blocks with one row group per lane.  Sweeps of 16-128-column rows
+    // (launches timed alone after a cache-evicting write) measured them
+    // 2-6% faster there at every such length, fitted and held out; 5-10%
+    // slower below 32 MiB, level from 192 MiB, and 2-20% slower for rows
+    // that leave lanes idle (48 or 96 bf16 columns, 100-column widening
+    // rows), which keep the 256-thread blocks.
+    // (row bytes are at most 32 vectors of 16 + 16 bytes here, so rows below
+    // the bound keep the product far from overflow)
+    const int64_t row_bytes = cols * (ib + ob);
+    const bool mid_launch = rows <= ((int64_t)160 << 20) / row_bytes &&
+                            rows * row_bytes >= ((int64_t)40 << 20);
+    if (auto_variant && !fused && nvec == p->lpr && mid_launch &&
+        (!cfg || (cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->block == 0))) {
+      p->block = kWave;
+      p->rpl = 1;
+    }
+    const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
+    p->grid = cdiv(rows, rows_per_block);
+    if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_MEDIUM) {
+    int wpr = 0, vpl = 0;
+    bool packed = false;
+    const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
+    const int want_packed = fused ? 0 : (cfg ? cfg->packed : -1);
+    if (fused && cfg && cfg->packed == 1) return ROWSM_EINVAL;
+    if (want_wpr && (want_wpr & (want_wpr - 1) || want_wpr > 16)) return ROWSM_EINVAL;
+    // Unpacked: the smallest group whose lanes hold <= 16 fp32 values each
+    // (<= 32, then <= 64 when the row is longer), unless a group size is
+    // forced.  Fewer values per lane and more resident rows measured faster
+    // than longer per-lane rows on the 32768 x 4096 workload.
+    if (want_packed != 1) {
+      // Fused rows keep column indices live as well: at most 32 values, and
+      // 32 (fewer waves per row) measured fastest on the causal workload.
+      for (int cap_vals : {16, 32, 64}) {
+        if (fused && cap_vals != 32) continue;
+        for (int w = 1; w <= 16; w <<= 1) {
+          if (want_wpr && w != want_wpr) continue;
+          const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+          if (v * vw <= cap_vals && medium_unpacked_cap(vw, v)) {
+            wpr = w;
+            vpl = v;
+            break;
+          }
+        }
+        if (wpr) break;
+      }
+    }
+    if (!wpr && want_packed != 0 && in_dt == ROWSM_BF16 && vw == 8) {
+      for (int w = 1; w <= 16; w <<= 1) {
+        if (want_wpr && w != want_wpr) continue;
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v <= 24 && (w == 16 || want_wpr)) {
+          wpr = w;
+          vpl = v;
+          packed = true;
+          break;
+        }
+      }
+    }
+    if (!wpr) return ROWSM_EINVAL;
+    // Slot counts are exact (only the last slot may be partial); packed
+    // kernels exist for 9..24 slots.
+    if (packed && (vpl < 9 || vpl > 24)) return ROWSM_EINVAL;
+    p->wpr = wpr;
+    p->vpl = vpl;
+    p->packed = packed;
+    // Launches of 4-16 rows per compute unit (softmax and log forms, rows of
+    // full vectors under 64 KiB of input, nothing about the shape forced):
+    // the fewest waves per row, at least what the registers need, that still
+    // give the launch about two 512-thread blocks per compute unit, so that
+    // each lane keeps more bytes in flight.  From sweeps of 1024-16384
+    // columns in every dtype pair: at 1024 and 2048 rows 1.6% above the
+    // fastest form measured on geometric mean (at most 9%), where the rule
+    // above was 8.9% (at most 54%); at 1536 and 3072 rows, not fitted, 4.8%
+    // (at most 24%) against 12% (at most 44%).  At 4096 and 6144 rows the two
+    // rules tie on geometric mean and the rule above stays.
+    const bool shape_free = !cfg || (cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
+                                     cfg->packed == -1 && cfg->block == 0 &&
+                                     cfg->split_blocks == 0 && cfg->vw == 0);
+    const bool full_vw = vw * (ib > ob ? ib : ob) == 16;
+    if (auto_variant && !fused && shape_free && full_vw && rows >= 4 * (int64_t)cus &&
+        rows < 16 * (int64_t)cus && cols * ib < 65536) {
+      int target = 1;
+      while ((int64_t)target * 2 * rows <= 16 * (int64_t)cus) target <<= 1;
+      for (int w = target; w <= 16; w <<= 1) {
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v * vw <= 64 && medium_unpacked_cap(vw, v)) {
+          p->wpr = w;
+          p->vpl = v;
+          p->packed = false;
+          break;
+        }
+        if (in_dt == ROWSM_BF16 && vw == 8 && v >= 9 && v <= 24) {
+          p->wpr = w;
+          p->vpl = v;
+          p->packed = true;
+          break;
+        }
+      }
+    }
+    // Full launches of rows of 129-4096 full vectors, when nothing about the
+    // shape is forced: the measured shapes of measured_row_shape() (fused
+    // form: measured_fused_shape()).
+    if (auto_variant && shape_free && full_vw && rows >= 32 * (int64_t)cus &&
+        (fused ? measured_fused_shape(nvec, ib, ob, &shape)
+               : measured_row_shape(nvec, ib, ob, &shape))) {
+      // (a single-read pick holds one group of blocks per row only while
+      // the rows fit the exchange workspace; beyond, the medium rule stays)
+      if (shape.S > 0 && rows * shape.S > kSplitMaxBlocks) shape = RowShape{};
+      if (shape.S > 0) {
+        variant = ROWSM_LARGE;
+        p->variant = variant;
+        p->wpr = 1;
+        p->packed = false;
+        p->measured = true;
+      } else if (shape.wpr > 0) {
+        p->wpr = shape.wpr;
+        p->vpl = (int)cdiv(nvec, (int64_t)shape.wpr * kWave);
+        p->packed = false;
+      }
+    }
+    // A row that needs all 16 waves of a 1024-thread block goes to the
+    // single-read split form of 256-thread blocks once the launch has many
+    // rows: from 8 * cus rows, or from cus / 4 when a lane would hold 64 or
+    // more values (or the packed form); rows of at least 64 KiB of input,
+    // the range measured.  A sweep of 256-8192 rows x
+    // 16384-151936 columns in every dtype pair (launches timed alone after
+    // a cache-evicting write) measured the split form 5-31% faster there
+    // (and within 2% of the medium form below these row counts): the
+    // 16-wave blocks synchronise a whole compute unit's worth of waves at
+    // each reduction and leave at most two blocks per compute unit.
+    if (variant == ROWSM_MEDIUM && auto_variant && !fused && p->wpr == 16 &&
+        cols * ib >= 65536 &&
+        (rows >= 8 * (int64_t)cus ||
+         ((vpl * vw >= 64 || packed) && rows >= cus / 4))) {
+      wide_row = true;
+      variant = ROWSM_LARGE;
+      p->variant = variant;
+      p->wpr = 1;
+      p->packed = false;
+    }
+  }
+  if (variant == ROWSM_MEDIUM) {
+    const int wpr = p->wpr;
+    p->nv = p->vpl;
+    // 512-thread blocks (256 for the fused form, fewer rows per block when a
+    // row needs more waves); one block per row group, no grid-stride loop
+    // unless capped.
+    const int waves_per_block = fused ? 4 : 8;
+    int rpb = wpr >= waves_per_block ? 1 : waves_per_block / wpr;
+    if (shape.rpb > 0) rpb = shape.rpb;
+    if (cfg && cfg->rows_per_block > 0) {
+      rpb = cfg->rows_per_block;
+      if (rpb * wpr > 16) return ROWSM_EINVAL;
+    }
+    p->block = rpb * wpr * kWave;
+    p->grid = cdiv(rows, rpb);
+    if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_LARGE) {
+    const int want_split = cfg ? cfg->split_blocks : 0;
+    if (cfg && cfg->block > 0) {
+      const int b = cfg->block;
+      if (b % kWave || b > 1024) return ROWSM_EINVAL;
+    }
+    if (want_split >= 0) {
+      // Single-read form: T threads per block, S blocks per row (S <= 64:
+      // one wave polls the S peers), at most 64 fp32 values per lane (40
+      // for widening rows, bf16 -> f32, which write twice what they read).
+      // 512-thread blocks, except 256 where 512 would leave fewer than 8
+      // blocks to a row that does not widen (a sweep of 1024-4096 rows x
+      // 98304-1048576 columns in every dtype pair, one group per row: 512
+      // gains up to 15% on the longest rows; 256 is 8% faster on
+      // 1024 x 131072 f32).
+      const bool widening = ob > ib;
+      const bool forced_block = cfg && cfg->block > 0;
+      const int vals = fused ? 32 : (widening ? 40 : 64);
+      int nv_cap = vals / vw < 16 ? vals / vw : 16;
+      if (nv_cap < 1) nv_cap = 1;
+      int T = 512;
+      if (forced_block) T = cfg->block;
+      else if (!widening && cdiv(nvec, (int64_t)nv_cap * 512) < 8) T = 256;
+      int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
+      if (wide_row && want_split == 0 && !forced_block) {
+        // Rows redirected from the 16-wave medium form: the power of two of
+        // threads per row that gives each lane 64-128 bytes of the input,
+        // in 256-thread blocks up to 2048 threads per row and 512-thread
+        // blocks beyond, and a power of two of blocks at least as large as
+        // the register cap needs (whole slots: 7 blocks of a 65536-wide
+        // bf16 -> f32 row measured 10-13% slower than 8).  Fastest or
+        // within 3% at 16384-151936 columns and 256-8192 rows.
+        int64_t thr = 1;
+        while (thr * 128 < cols * ib) thr <<= 1;
+        T = thr <= 2048 ? 256 : 512;
+        S = thr / T > 1 ? (int)(thr / T) : 1;
+        const int64_t s_cap = cdiv(nvec, (int64_t)nv_cap * T);
+        while (S < s_cap) S <<= 1;
+      }
+      if (shape.S > 0) {
+        S = shape.S;
+        T = shape.T;
+      }
+      if (S < 1) S = 1;
+      // Grid: one group of S blocks per row (0), or with blocks_per_cu
+      // given, one residency of at most that many blocks per compute unit
+      // whose groups loop over the rows (negative; split_slots()).
+      int64_t grid = bpc ? -(int64_t)bpc : 0;
+      if (want_split == 0) {
+        // Few rows: more, smaller blocks per row so that the launch fills
+        // the device (256-thread blocks unless a block size is given; also
+        // when the row then has as many threads as in the plan above, which
+        // measured up to 9% faster at 16-64 rows of 151936-262144 columns).
+        const int Tf = forced_block ? T : 256;
+        const int sf = few_rows_split(rows, nvec, Tf, nv_cap, cus);
+        if (sf > 0 && (int64_t)sf * Tf >= (int64_t)S * T) {
+          S = sf;
+          T = Tf;
+        }
+      }
+      const int nv = (int)cdiv(nvec, (int64_t)S * T);
+      if (S <= 64 && nv <= nv_cap && nv * vw <= 64) {
+        p->split = S;
+        p->nv = nv;
+        p->vpl = nv;
+        p->block = T;
+        p->grid = grid;
+        p->prefetch = cfg && cfg->prefetch == 1;
+        // registers: at most 48 values per lane, plain and log forms only
+        // (split_launch.hpp)
+        if (p->prefetch && (fused || nv * vw > 48)) return ROWSM_EINVAL;
+        return ROWSM_OK;
+      }
+      if (want_split > 0) return ROWSM_EINVAL;
+    }
+    p->split = 0;
+    p->u = 4;
+    if (cfg && cfg->tile_vectors > 0) {
+      const int u = cfg->tile_vectors;
+      if (u != 2 && u != 4 && u != 8) return ROWSM_EINVAL;
+      p->u = u;
+    }
+    p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
+    p->grid = rows < cap ? rows : cap;
+    p->stream = stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
+    return ROWSM_OK;
+  }
+  return ROWSM_EINVAL;
+}
+
+// Plan of the softmax backward: y and dy of in_dt (both aligned as ia), dx
+// of out_dt at dxa.  The register-resident forms hold y and dy raw; a lane's
+// share of each input is at most 128 bytes (and 16 slots).
+//   SMALL   a row is at most 32 vectors;
+//   MEDIUM  the smallest row group of <= 16 waves whose lanes hold at most 32
+//           bytes of each input (then 64, then 128), unless the rows are few
+//           and long (the forward's row-count rule, on the backward's bytes);
+//   LARGE   the row split over S <= 64 co-resident 512-thread blocks (more,
+//           256-thread blocks per row for few rows, as the forward), or two
+//           streaming passes for rows longer than that.
+int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t ia,
+                  uintptr_t dxa, const rowsm_config* cfg, int cus, Plan* p) {
+  if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  if (cfg && cfg->packed == 1) return ROWSM_EINVAL;  // no packed form: always raw
+  const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
+  int vw = choose_vw(cols, ib, ob, ia, dxa);
+  if (cfg && cfg->vw > 0) {
+    const int want = cfg->vw;
+    if (want > 16 / (ib > ob ? ib : ob) || (want & (want - 1)) || !vw_supported(want, ib) ||
+        cols % want || ia % (want * ib) || dxa % (want * ob < 16 ? want * ob : 16))
+      return ROWSM_EINVAL;
+    vw = want;
+  }
+  const int nvec = (int)(cols / vw);
+  const int vbytes = vw * ib;  // bytes of one input vector
+  int nv_cap = 128 / vbytes < 16 ? 128 / vbytes : 16;
+  p->vw = vw;
+  p->nvec = nvec;
+
+  int variant = cfg ? cfg->variant : ROWSM_AUTO;
+  const bool auto_variant = variant == ROWSM_AUTO;
+  if (variant == ROWSM_AUTO) {
+    if (nvec <= 32)
+      variant = ROWSM_SMALL;
+    else if (nvec <= 16 * kWave * nv_cap &&
+             !few_long_rows(rows, cols * (2 * ib + ob), false, cus, kFewRowsMinBytesBackward))
+      variant = ROWSM_MEDIUM;
+    else
+      variant = ROWSM_LARGE;
+  }
+  p->variant = variant;
+  const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
+
+  if (variant == ROWSM_SMALL) {
+    if (nvec > 32) return ROWSM_EINVAL;
+    p->lpr = next_pow2(nvec);
+    if (cfg && cfg->lanes_per_row > 0) {
+      if (cfg->lanes_per_row < p->lpr) return ROWSM_EINVAL;
+      p->lpr = cfg->lanes_per_row;
+    }
+    p->rpl = (cfg && cfg->rows_per_lane > 0) ? cfg->rows_per_lane : 4;
+    if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
+    const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
+    p->grid = cdiv(rows, rows_per_block);
+    if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+    return ROWSM_OK;
+  }
+  if (variant == ROWSM_MEDIUM) {
+    const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
+    int wpr = 0, nv = 0;
+    for (int cap_bytes : {32, 64, 128}) {
+      for (int w = 1; w <= 16; w <<= 1) {
+        if (want_wpr && w != want_wpr) continue;
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v * vbytes <= cap_bytes && v <= nv_cap) {
+          wpr = w;
+          nv = v;
+          break;
+        }
+      }
+      if (wpr) break;
+    }
+    if (!wpr) return ROWSM_EINVAL;
+    // Launches of 4-16 rows per compute unit (rows of full vectors under 64
+    // KiB of each input, nothing about the shape forced): as the forward,
+    // the fewest waves per row that the per-lane cap allows and that keep
+    // about two 512-thread blocks per compute unit.  Sweeps of 1024-16384
+    // columns in every dtype pair: at 1024 and 2048 rows 3.1% and 2.3% above
+    // the fastest form on geometric mean, where the rule above was 7.3% and
+    // 3.7%; at 1536 and 3072 rows, not fitted, 3.1% against 5.2%, and level.
+    const bool shape_free = !cfg || (cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
+                                     cfg->block == 0 && cfg->split_blocks == 0 && cfg->vw == 0);
+    if (auto_variant && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
+        rows >= 4 * (int64_t)cus && rows < 16 * (int64_t)cus && cols * ib < 65536) {
+      int target = 1;
+      while ((int64_t)target * 2 * rows <= 16 * (int64_t)cus) target <<= 1;
+      for (int w = target; w <= 16; w <<= 1) {
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v <= nv_cap) {
+          wpr = w;
+          nv = v;
+          break;
+        }
+      }
+    }
+    // A row that needs all 16 waves of a 1024-thread block goes to the
+    // split form from 4 * cus rows when it holds at least 64 KiB of each
+    // input (measured 4-20% faster there at 16384-65536 columns in every
+    // dtype pair, and within 1% of the medium form at 256-512 rows; the
+    // forward's reason).
+    if (auto_variant && wpr == 16 && cols * ib >= 65536 && rows >= 4 * (int64_t)cus) {
+      variant = ROWSM_LARGE;
+      p->variant = variant;
+    } else {
+      p->wpr = wpr;
+      p->vpl = nv;
+      p->nv = nv;
+      int rpb = wpr >= 8 ? 1 : 8 / wpr;  // 512-thread blocks
+      if (cfg && cfg->rows_per_block > 0) {
+        rpb = cfg->rows_per_block;
+        if (rpb * wpr > 16) return ROWSM_EINVAL;
+      }
+      p->block = rpb * wpr * kWave;
+      p->grid = cdiv(rows, rpb);
+      if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+      return ROWSM_OK;
+    }
+  }
+  if (variant == ROWSM_LARGE) {
+    const int want_split = cfg ? cfg->split_blocks : 0;
+    if (want_split >= 0) {
+      // 512-thread blocks (measured 0-4% faster than 256 on long rows of
+      // every dtype pair with one group per row); few rows as the forward
+      // plan, with 256-thread blocks unless a block size is given.
+      const bool forced_block = cfg && cfg->block > 0;
+      int T = forced_block ? cfg->block : 512;
+      int S = want_split > 0 ? want_split : (int)cdiv(nvec, (int64_t)nv_cap * T);
+      if (want_split == 0 && !forced_block && rows >= cus && cols * ib <= 4096 * 128) {
+        // Rows of at most 512 KiB per input in launches of at least cus
+        // rows: 2048 threads per row, 4096 beyond 128 KiB per input, about
+        // 32-64 bytes of each input per lane, in 256- and 512-thread blocks
+        // (within 3% of the fastest form at 16384-151936 columns and
+        // 256-4096 rows; the register-cap plan above was up to 8% slower);
+        // a power of two of blocks at least as large as the cap needs.
+        const int64_t thr = cols * ib > 2048 * 64 ? 4096 : 2048;
+        T = thr <= 2048 ? 256 : 512;
+        S = (int)(thr / T);
+        const int64_t s_cap = cdiv(nvec, (int64_t)nv_cap * T);
+        while (S < s_cap) S <<= 1;
+      }
+      if (S < 1) S = 1;
+      if (want_split == 0) {
+        // (ties go to the few-rows plan, as in the forward)
+        const int Tf = forced_block ? T : 256;
+        const int sf = few_rows_split(rows, nvec, Tf, nv_cap, cus);
+        if (sf > 0 && (int64_t)sf * Tf >= (int64_t)S * T) {
+          S = sf;
+          T = Tf;
+        }
+      }
+      const int nv = (int)cdiv(nvec, (int64_t)S * T);
+      if (S <= 64 && nv <= nv_cap) {
+        p->split = S;
+        p->nv = nv;
+        p->vpl = nv;
+        p->block = T;
+        p->grid = bpc ? -(int64_t)bpc : 0;  // as the forward plan
+        return ROWSM_OK;
+      }
+      if (want_split > 0) return ROWSM_EINVAL;
+    }
+    p->split = 0;
+    p->u = (cfg && cfg->tile_vectors > 0) ? cfg->tile_vectors : 4;
+    p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
+    const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
+    p->grid = rows < cap ? rows : cap;
+    p->stream = stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
+    return ROWSM_OK;
+  }
+  return ROWSM_EINVAL;
+}
+
+// Plan of the MoE group score over ngroups groups of g scores (g a power of
+// two, 2..64): the widest vector (16 or 8 bytes, else one element) that
+// divides g and fits the scores' alignment sa; g / vw lanes per group; 4
+// groups per lane (cfg->rows_per_lane overrides); 256-thread blocks, one task
+// of 64 / (g / vw) * rpl groups per wave (a grid of up to 2^30 blocks; the
+// waves stride over any tasks beyond that).  A grid capped at a few blocks
+// per compute unit with the waves striding over tasks measured 14% slower on
+// the 1048576 x 256 workload; cfg->blocks_per_cu sets such a cap.
+int plan_moe(int64_t ngroups, int64_t g, int in_dt, uintptr_t sa, const rowsm_config* cfg,
+             int cus, Plan* p) {
+  if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  if (cfg && cfg->variant != ROWSM_AUTO && cfg->variant != ROWSM_SMALL) return ROWSM_EINVAL;
+  const int ib = dtype_bytes(in_dt);
+  int vw = 1;
+  for (int w = 16 / ib; w > 1; w >>= 1)
+    if (vw_supported(w, ib) && g % w == 0 && sa % (uintptr_t)(w * ib) == 0) {
+      vw = w;
+      break;
+    }
+  if (cfg && cfg->vw > 0) {
+    const int w = cfg->vw;
+    if (!vw_supported(w, ib) || w * ib > 16 || g % w || sa % (uintptr_t)(w * ib))
+      return ROWSM_EINVAL;
+    vw = w;
+  }
+  p->variant = ROWSM_SMALL;
+  p->vw = vw;
+  p->nvec = (int)(g / vw);
+  p->lpr = (int)(g / vw);  // lanes per group
+  p->rpl = (cfg && cfg->rows_per_lane > 0) ? cfg->rows_per_lane : 4;
+  if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
+  const int64_t per_task = (int64_t)(kWave / p->lpr) * p->rpl;
+  const int64_t tasks = cdiv(ngroups, per_task);
+  const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
+  p->grid = cdiv(tasks, p->block / kWave);
+  if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+  return ROWSM_OK;
+}
+
+bool moe_group_ok(int64_t g) { return g >= 2 && g <= kWave && (g & (g - 1)) == 0; }
+
+}  // namespace rowsm
