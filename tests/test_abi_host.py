@@ -239,6 +239,23 @@ def test_describe(lib):
     # launch sizes whose byte count would not fit 64 bits take the default
     t = R.rowsm_describe((1 << 61) + 1, 1, R.F32, R.F32)[1]
     assert "block=256 " in t and "rpl=4 " in t, t
+    # the backward: one-wave blocks from 96 MiB of its three streams on (no
+    # upper bound), for rows that fill their lanes and nothing forced
+    bt = lambda rows, cols, dt, cfg=None: R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols,
+                                                              dt, dt, cfg)[1]
+    for rows, cols, dt in [(262144, 64, R.BF16), (4194304, 32, R.BF16), (131072, 128, R.F32),
+                           ((1 << 40), 64, R.F32)]:
+        t = bt(rows, cols, dt)
+        assert t.startswith("small") and "block=64 " in t and "rpl=1 " in t, t
+    assert "grid=32768 " in bt(262144, 64, R.BF16)
+    for rows, cols, dt, cfg in [(262143, 64, R.BF16, None),      # just under 96 MiB
+                                (524288, 48, R.BF16, None),       # lanes left idle
+                                (262144, 64, R.BF16, R.RowsmConfig(rows_per_lane=4)),
+                                (262144, 64, R.BF16, R.RowsmConfig(variant=R.SMALL))]:
+        t = bt(rows, cols, dt, cfg)
+        assert "block=256 " in t and "rpl=4 " in t, t
+    t = bt(262144, 64, R.BF16, R.RowsmConfig(block=128))
+    assert "block=128 " in t and "rpl=4 " in t, t
     st, text = R.rowsm_describe(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("medium")
     st, text = R.rowsm_describe(128, 151936, R.BF16, R.BF16, R.MEDIUM)
@@ -255,9 +272,10 @@ def test_describe(lib):
     assert st == R.OK and "split=8" in text and "one residency" in text
     # small and medium grids: one task per wave / one row group per block at
     # any row count; blocks_per_cu caps them (the waves then stride)
-    for op in (R.OP_SOFTMAX, R.OP_SOFTMAX_BACKWARD):
+    # (the backward's 4M rows take one-wave blocks of one row group per lane)
+    for op, grid in ((R.OP_SOFTMAX, 32768), (R.OP_SOFTMAX_BACKWARD, 524288)):
         st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16)
-        assert st == R.OK and text.startswith("small") and "grid=32768 " in text, text
+        assert st == R.OK and text.startswith("small") and f"grid={grid} " in text, text
         st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16,
                                        R.RowsmConfig(blocks_per_cu=8))
         assert st == R.OK and "grid=2048 " in text, text
@@ -326,7 +344,7 @@ def test_backward_plans(lib):
     d = lambda rows, cols, i, o, **cfg: R.rowsm_describe_op(
         R.OP_SOFTMAX_BACKWARD, rows, cols, i, o, R.RowsmConfig(**cfg) if cfg else None)
     st, t = d(262144, 64, R.BF16, R.BF16)
-    assert st == R.OK and t.startswith("small") and "lpr=8" in t and "rpl=4" in t
+    assert st == R.OK and t.startswith("small") and "lpr=8" in t and "rpl=1" in t  # 96 MiB
     st, t = d(32768, 4096, R.BF16, R.BF16)
     assert st == R.OK and t.startswith("medium") and "wpr=4" in t and "nv=2" in t
     # medium holds at most 128 bytes of each input per lane: 16 x 64 x 8 vectors

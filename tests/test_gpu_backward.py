@@ -112,6 +112,23 @@ def test_bwd_few_rows_per_cu_shapes(rows, cols, din, dout, want):
 
 
 @pytest.mark.parametrize("rows,cols,din,dout", [
+    (262144, 64, "bf16", "bf16"), (262147, 64, "bf16", "bf16"), (131072, 128, "f32", "f32"),
+    (1048576, 32, "bf16", "f32"), (786435, 16, "f32", "bf16")])
+def test_bwd_small_one_wave_blocks(rows, cols, din, dout):
+    # launches of at least 96 MiB of rows that fill their lanes: one-wave
+    # blocks, one row group per lane (ragged row counts included); sampled
+    # rows, the last ones among them, against the oracle
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("small") and "block=64 " in desc and "rpl=1 " in desc
+    y, dy = inputs(rows, cols, din, alpha=0.3, seed=rows + cols)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
+    sample = list(range(0, rows, 997)) + list(range(rows - 9, rows))
+    assert_bwd_parity(y[sample], dy[sample], dx[sample].cpu(), dout,
+                      f"bwd {rows}x{cols} {din}->{dout} [{desc}]")
+
+
+@pytest.mark.parametrize("rows,cols,din,dout", [
     (1024, 16384, "f32", "f32"), (1024, 32768, "bf16", "f32"), (1024, 32768, "bf16", "bf16"),
     (300, 65536, "f32", "f32")])
 def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
