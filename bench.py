@@ -495,6 +495,8 @@ LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype)
     ("scaled_causal", 32768, 16384, "f32", "f32"),
     ("backward", 1024, 8192, "f32", "f32"),
     ("backward", 32768, 4096, "bf16", "bf16"),
+    ("backward", 524288, 128, "bf16", "bf16"),
+    ("backward", 131072, 64, "bf16", "bf16"),
 ]
 
 
