@@ -6,8 +6,6 @@
 
 #include <cstdio>
 #include <cstring>
-#include <type_traits>
-#include <utility>
 
 #include "plan.hpp"
 
