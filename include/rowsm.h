@@ -24,24 +24,25 @@
  *     Arithmetic is fp32: bf16 inputs widen exactly, bf16 outputs are rounded
  *     to nearest even.
  *   - stream is a hipStream_t (NULL = the legacy default stream).  The call
- *     only enqueues work; results are visible once the caller synchronises the
- *     stream.  Nothing is allocated per call.  The single-read LARGE form
- *     uses a 32 MiB device workspace (and a 64 MiB region for captured
- *     launches, see HIP graphs below) that the first such call on a device
- *     allocates and clears (synchronously) and that lives until the process
- *     ends; make that first call outside stream capture.  Eager single-read
- *     launches on one device are ordered one after another whatever their
- *     streams (each waits for the previous one through an event), so the
- *     workspace is never shared by two running launches; the launcher takes
- *     that form for long rows and for many full launches of medium-length
- *     rows (rowsm_describe shows it as split > 0), which therefore do not
- *     overlap across streams either.  The blocks of one row wait for each
- *     other; a launch's progress needs only that workgroups are dispatched
- *     in order, whatever else runs.  Work that itself waits on the device
- *     for blocks that are not yet resident (such a launch from another
- *     process on the same GPU) can hold blocks out in the worst case: a wait
- *     then gives up after about a second, the row's result is wrong, and
- *     rowsm_split_wait_failures() counts it.
+ *     only enqueues work on that stream; results are visible once the caller
+ *     synchronises it.  No call waits for, or is ordered after, work on any
+ *     other stream.  Nothing is allocated per call.  The forms whose blocks
+ *     exchange partial results (LARGE with split > 0 in rowsm_describe, or
+ *     the two-pass form with several blocks per row) take a region of a
+ *     64 MiB exchange ring per device: the library's static device array,
+ *     zero when the library's device code is loaded, so the first such call
+ *     allocates, clears and waits for nothing either.  After 2^30 rows of
+ *     exchanging launches on a device the ring is replaced by a 64 MiB
+ *     allocation that the library clears on a private stream of its own and
+ *     waits for (outside stream capture only); replaced rings stay allocated
+ *     until the process ends.
+ *   - Exchanging forms never depend on timing for their results: a block
+ *     whose wait for another block's partial result gives up (after about
+ *     0.1 s, rowsm_set_split_wait_limit()) computes that partial itself from
+ *     the input and the row comes out bit for bit as it would have, so a
+ *     launch finishes with the right result whatever else runs on the
+ *     device.  rowsm_split_wait_failures() counts such give-ups.  An
+ *     in-place call (y == x) is never planned on an exchanging form.
  *   - Errors are reported through the return value only (a rowsm_status);
  *     the library never aborts, prints or throws.  Argument errors are found
  *     on the host before any HIP call.  A failed launch maps to ROWSM_EHIP.
@@ -71,9 +72,9 @@ typedef enum {
 
 /* Kernel families.  SMALL packs several rows into one 64-lane wavefront;
  * MEDIUM gives each row one workgroup (or one wavefront) and keeps the row in
- * registers; LARGE spreads a row over several co-resident workgroups that
- * keep their shares in registers and exchange (max, sum) pairs through a
- * small device workspace (single read), or, for rows too long for that,
+ * registers; LARGE spreads a row over several workgroups that keep their
+ * shares in registers and exchange (max, sum) pairs through the device
+ * workspace (single read), or, for rows too long for that,
  * streams the row through tiles twice (online max/sum pass, then normalize),
  * over one block per row for many rows and over up to 256 blocks per row,
  * which exchange their pairs the same way, for few.  Both launch one group
@@ -82,22 +83,13 @@ typedef enum {
  * the two-pass form one block per row.
  *
  * HIP graphs: every entry point may be called on a stream that is being
- * captured.  An eager single-read LARGE launch takes its exchange tags from
- * the host, which a replayed graph cannot do; a captured one instead records
- * a small epoch kernel before it that advances the tags on the device at
- * every replay, in a private slice of a per-device 64 MiB capture region (at
- * most 2^15 blocks per launch; larger launches loop over their rows).  Graph
- * executables that contain the same captured launch (e.g. two
- * instantiations of one graph) must not run at the same time.  When no slice
- * is left, or the region does not exist yet (it is created with the shared
- * workspace by the first single-read launch outside capture on the device),
- * a captured LARGE plan is re-planned without workspace: a row that fits the
- * registers of one medium block (which the launcher sent to the single-read
- * form for speed) takes the medium form, any other row the two-pass form with
- * one block per row (same results to the stated tolerances, one extra read
- * of each input); a single-read form forced through cfg->split_blocks > 0
- * returns ROWSM_EINVAL.  No entry point records a memset or an allocation
- * into a capture. */
+ * captured, from the first call on, and keeps its plan.  A captured
+ * exchanging launch records, before its kernel, a small kernel that clears
+ * the launch's region of the exchange ring, so that every replay starts from
+ * cleared exchange words (a replay reuses the region and the tags recorded
+ * at capture).  Graph executables that contain the same captured launch
+ * (e.g. two instantiations of one graph) must not run at the same time.  No
+ * entry point records a memset or an allocation into a capture. */
 typedef enum {
     ROWSM_AUTO = 0,
     ROWSM_SMALL = 1,
@@ -169,10 +161,12 @@ typedef struct rowsm_config {
     int32_t blocks_per_cu;  /* grid cap = blocks_per_cu * compute units           */
     int32_t split_blocks;   /* LARGE: blocks sharing one row in the single-read
                                form (1..64), 0 launcher's choice, -1 the
-                               two-pass streaming form                            */
+                               two-pass streaming form; > 0 in place is
+                               ROWSM_EINVAL (no exchanging form in place)         */
     int32_t prefetch;       /* LARGE single-read form: 1 load a block's next row
                                while the current one is exchanged and written
-                               (software pipelining), -1 never, 0 launcher's
+                               (software pipelining; at most 48 values per lane,
+                               44 for fp32 input), -1 never, 0 launcher's
                                choice                                             */
 } rowsm_config;
 
@@ -250,9 +244,9 @@ int rowsm_log_softmax(const void *x, void *y, int64_t rows, int64_t cols, int in
  * and with it the whole row of dx, NaN; an infinite product makes it +-inf
  * (or NaN), and dx follows from the formula (e.g. -inf where y > 0, NaN where
  * y == 0 or at the infinite entry).  y == 0 with a finite dot product gives
- * an exact zero.  The single-read
- * LARGE form shares the forward's device workspace and ordering (see
- * rowsm_split_wait_failures).
+ * an exact zero.  The exchanging LARGE forms share the forward's device
+ * workspace and behave as the forward's (see rowsm_split_wait_failures); dx
+ * equal to y or dy is never planned on them.
  */
 int rowsm_softmax_backward(const void *y, const void *dy, void *dx, int64_t rows, int64_t cols,
                            int in_dtype, int out_dtype, void *stream, const rowsm_config *cfg);
@@ -305,16 +299,25 @@ int rowsm_describe(int64_t rows, int64_t cols, int in_dtype, int out_dtype,
                    int variant, char *buf, int64_t len);
 
 /*
- * rowsm_split_wait_failures: diagnostics of the single-read LARGE form on
- * the current device.  Waits for the last eager such launch to finish
- * (synchronise the streams of graph replays first), then returns
- * how many exchange waits have given up since the workspace was created (0
- * when every row's blocks met; a non-zero count means some rows of some
- * launch are wrong), 0 when no such launch has run, or ROWSM_EHIP.  It
- * synchronises with the device: not to be called while a stream capture is
- * in progress.
+ * rowsm_split_wait_failures: diagnostics of the exchanging forms on the
+ * current device: how many exchange waits have given up since the library's
+ * device code was loaded (each one made a block recompute another block's
+ * partial result from the input: the results are unaffected, the launch was
+ * slower), 0 when no exchanging launch has run, or ROWSM_EHIP.  It first
+ * synchronises the device (hipDeviceSynchronize): not to be called while a
+ * stream capture is in progress.
  */
 int64_t rowsm_split_wait_failures(void);
+
+/*
+ * rowsm_set_split_wait_limit: sets how many times an exchange wait polls for
+ * another block's partial result before it gives up and recomputes it (for
+ * launches made after the call, on every device); polls < 0 restores the
+ * default (2^16, about 0.1 s), 0 makes every wait give up at once.  Results
+ * are the same for any limit; the setting exists so that tests can drive the
+ * recomputation.  Returns the previous limit.  Pure host function.
+ */
+int64_t rowsm_set_split_wait_limit(int64_t polls);
 
 /*
  * rowsm_stream_copy: y[i] = x[i] converted from in_dtype to out_dtype, for

@@ -15,7 +15,8 @@ Raw entry points (same names and arguments as the C ABI; pointers are ints,
                                 causal_period, causal_offset, stream, cfg)
     rowsm_select(rows, cols, in_dtype, out_dtype) -> variant or status
     rowsm_describe(rows, cols, in_dtype, out_dtype, variant) -> (status, text)
-    rowsm_split_wait_failures() -> count (diagnostics of the split LARGE form)
+    rowsm_split_wait_failures() -> count (diagnostics of the exchanging forms)
+    rowsm_set_split_wait_limit(polls) -> previous limit (test setting)
     rowsm_status_string(status) -> str
 
 Tensor helper: ``softmax(x, out_dtype=None, out=None, ...)`` for torch tensors
@@ -42,7 +43,8 @@ EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
            "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_log_softmax",
            "rowsm_softmax_backward", "rowsm_moe_group_top2", "rowsm_describe",
            "rowsm_describe_op",
-           "rowsm_split_wait_failures", "rowsm_stream_copy", "rowsm_status_string")
+           "rowsm_split_wait_failures", "rowsm_set_split_wait_limit", "rowsm_stream_copy",
+           "rowsm_status_string")
 
 
 class RowsmError(RuntimeError):
@@ -111,6 +113,8 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     h.rowsm_stream_copy.restype = i32
     h.rowsm_split_wait_failures.argtypes = []
     h.rowsm_split_wait_failures.restype = i64
+    h.rowsm_set_split_wait_limit.argtypes = [i64]
+    h.rowsm_set_split_wait_limit.restype = i64
     h.rowsm_status_string.argtypes = [i32]
     h.rowsm_status_string.restype = ctypes.c_char_p
     if path is None:
@@ -192,6 +196,10 @@ def rowsm_stream_copy(x, y, n, in_dtype, out_dtype, stream=0) -> int:
 
 def rowsm_split_wait_failures() -> int:
     return lib().rowsm_split_wait_failures()
+
+
+def rowsm_set_split_wait_limit(polls: int) -> int:
+    return lib().rowsm_set_split_wait_limit(polls)
 
 
 def rowsm_status_string(status) -> str:

@@ -177,21 +177,49 @@ __global__ __launch_bounds__(1024) void bwd_medium_kernel(
 // ---- long rows: split over co-resident blocks -----------------------------------
 //
 // Layout, grid and co-residency as split_row_kernel.  Each block publishes
-// its partial d_b as the word ws[b][k & 1] = (tag << 32) | bits(d_b) (relaxed
-// agent-scope 64-bit atomic store; tag = tag0 + k unique to the launch and
-// the block's row count k) and the first wave polls the S words of its row
-// group until their tags match, then sums them in block order.  The wm words
-// are not used.  LDS reuse across rows: a wave rewrites red only after this
-// row's second barrier, and bcast (wave 0) only after the next row's first
-// barrier; every wave reads red before the second barrier and bcast before
-// the next row's first, so no value is overwritten before it is read.
+// its partial d_b through the split form's tagged words (split_row.hpp; both
+// words carry d_b) and the first wave polls the S blocks of its row group,
+// then sums the partials in block order.  A block whose wait for a peer gives
+// up computes that peer's partial itself (bwd_share_dot(), the same steps as
+// its own), so the sum does not depend on the wait.  LDS reuse across rows:
+// red is rewritten only after a barrier that every wave reaches after reading
+// it; bcast, missing_lanes and peer (wave 0) only after the next row's
+// reduction barrier, which every wave passes only after reading them.
+
+// Partial dot product of the block whose global threads are gt = c * T + t
+// (slots gt + s * RT), reduced over the wave and then over waves in wave
+// order through red[] (one barrier): the steps of the kernel's own share,
+// for a peer's, one slot at a time.  Called by every thread of the block.
+template <typename In, int VW, int NV>
+__device__ __forceinline__ float bwd_share_dot(rsrc_t ry, rsrc_t rdy, int gt, int RT, int nvec,
+                                               float* red, int lane, int wave, int nwaves) {
+  const bool last_ok = (NV - 1) * RT + gt < nvec;
+  const uint32_t vin = (uint32_t)gt * (VW * In::bytes);
+  const uint32_t sin = (uint32_t)RT * (VW * In::bytes);
+  float d = 0.0f;
+#pragma unroll 1
+  for (int s = 0; s < NV; ++s) {
+    InVec<In, VW> a, b;
+    if (s < NV - 1 || last_ok) {
+      a.load(ry, vin, s * sin);
+      b.load(rdy, vin, s * sin);
+    } else {
+      a.set_zero();
+      b.set_zero();
+    }
+    d = dot_vec(a, b, d);
+  }
+  return block_sum(d, red, lane, wave, nwaves);
+}
+
 template <typename In, typename Out, int VW, int NV>
 __global__ __launch_bounds__(1024) void bwd_split_kernel(
-    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
-    typename Out::storage* __restrict__ dx, int64_t rows, int cols, int S, SplitWorkspace w,
-    uint32_t tag0) {
+    const typename In::storage* y, const typename In::storage* dy, typename Out::storage* dx,
+    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0) {
   __shared__ float red[16];
   __shared__ float bcast;
+  __shared__ uint64_t missing_lanes;
+  __shared__ float peer[kWave];  // the row's partials, when a wait gave up
 
   const int T = blockDim.x;
   const int lane = threadIdx.x & (kWave - 1);
@@ -209,7 +237,6 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
   const uint32_t sin = (uint32_t)RT * (VW * In::bytes);
   const uint32_t sout = (uint32_t)RT * (VW * Out::bytes);
 
-  tag0 = split_tag0(w, tag0);
   bool gave_up = false;  // per lane of the first wave
   uint32_t k = 0;
   for (int64_t row = q; row < rows; row += slots, ++k) {
@@ -228,6 +255,7 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
         b[s].set_zero();
       }
     }
+    // (bwd_share_dot() repeats exactly these steps for a peer's share)
     float d = 0.0f;
 #pragma unroll
     for (int s = 0; s < NV; ++s) d = dot_vec(a[s], b[s], d);
@@ -236,25 +264,55 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
       a[s].opaque();
       b[s].opaque();
     }
-    d = group_reduce<kWave, SumOp>(d);
-    if (lane == 0) red[wave] = d;
-    __syncthreads();
-    float db = red[0];
-    for (int i = 1; i < nwaves; ++i) db += red[i];
+    const float db = block_sum(d, red, lane, wave, nwaves);
 
+    // When a wait gave up, wave 0 parks its partials in LDS, the block
+    // recomputes the missing ones and then loads its own share again (none
+    // of its registers stays live through the recomputation).
+    auto finish = [&](float pr) {
+      pr = group_reduce<kWave, SumOp>(pr);  // fixed lane order: deterministic
+      if (lane == 0) bcast = pr;
+    };
     if (wave == 0) {
-      const uint32_t b0 = (uint32_t)q * S;
-      const uint64_t tag = (uint64_t)(tag0 + k) << 32;
-      const uint32_t slot = k & 1;
-      if (lane == 0)
-        __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(db),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t tag = tag0 + k;
+      uint64_t* gw = split_group_words(w, q, k & 1, S);
+      if (lane == 0 && S > 1) split_publish(gw, S, c, tag, db, db);
       float p = 0.0f;
-      if (lane < S) p = split_poll_word(w, b0 + lane, slot, tag, &gave_up);
-      p = group_reduce<kWave, SumOp>(p);  // fixed lane order: deterministic
-      if (lane == 0) bcast = p;
+      bool ok = true;
+      float unused = 0.0f;
+      if (lane == c) p = db;
+      else if (lane < S) ok = split_poll(w, gw, S, lane, tag, &gave_up, &unused, &p);
+      const uint64_t missing = lanes_missing(ok);
+      if (lane == 0) missing_lanes = missing;
+      if (missing == 0) finish(p);
+      else peer[lane] = p;
     }
     __syncthreads();
+    const uint64_t missing = missing_lanes;
+    if (missing != 0) {
+      for (uint64_t mm = missing; mm != 0; mm &= mm - 1) {
+        const int bb = __builtin_ctzll(mm);
+        // red is free again: every wave read it before the barrier above
+        // (or before the previous recomputation's).
+        __syncthreads();
+        const float r = bwd_share_dot<In, VW, NV>(ry, rdy, bb * T + threadIdx.x, RT, nvec, red,
+                                                  lane, wave, nwaves);
+        if (threadIdx.x == 0) peer[bb] = r;
+      }
+      __syncthreads();
+      if (wave == 0) finish(peer[lane]);
+      __syncthreads();
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        if (s < NV - 1 || last_ok) {
+          a[s].load(ry, vin, s * sin);
+          b[s].load(rdy, vin, s * sin);
+        } else {
+          a[s].set_zero();
+          b[s].set_zero();
+        }
+      }
+    }
     d = bcast;
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
@@ -272,18 +330,55 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
 // vector pairs g + j * S * T, U per tile).  Pass 1 accumulates d over tiles
 // (a tile's partial on its own, then added to the running sum with a Kahan
 // compensation term: up to 2^16 tile partials per thread on the longest
-// rows); with S > 1 the blocks exchange their partial d once (one tagged
-// word each, as bwd_split_kernel) and sum them in block order.  Pass 2 reads
-// the block's share again, last tile first, and writes dx.  An infinite
-// running sum drops the compensation, so d keeps IEEE semantics (+-inf, or
-// NaN from inf - inf or a NaN term).
+// rows); with S > 1 the blocks exchange their partial d once (as
+// bwd_split_kernel, up to 4 peers per lane of wave 0, a peer whose wait gives
+// up recomputed with bwd_large_pass1()) and sum them in block order.  Pass 2
+// reads the block's share again, last tile first, and writes dx.  An
+// infinite running sum drops the compensation, so d keeps IEEE semantics
+// (+-inf, or NaN from inf - inf or a NaN term).
+
+// Pass 1 of the block whose global threads are g = c * T + t, reduced over the
+// block (wave, then waves in wave order through red[]; one barrier).
+template <typename In, int VW, int U>
+__device__ __forceinline__ float bwd_large_pass1(rsrc_t ry, rsrc_t rdy, int g, int RT, int nvec, int ntiles,
+                                 float* red, int lane, int wave, int nwaves) {
+  const uint32_t vin = (uint32_t)g * (VW * In::bytes);
+  float d = 0.0f, cd = 0.0f;  // running sum and its compensation
+  for (int tt = 0; tt < ntiles; ++tt) {
+    InVec<In, VW> a[U], b[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = (tt * U + u) * RT;
+      const uint32_t so = (uint32_t)j * (VW * In::bytes);
+      if (j + g < nvec) {
+        a[u].load(ry, vin, so);
+        b[u].load(rdy, vin, so);
+      } else {
+        a[u].set_zero();
+        b[u].set_zero();
+      }
+    }
+    float ts = 0.0f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) ts = dot_vec(a[u], b[u], ts);
+    const float yk = ts - cd;
+    const float t = d + yk;
+    cd = __builtin_isfinite(t) ? (t - d) - yk : 0.0f;
+    d = t;
+  }
+  d -= cd;
+  return block_sum(d, red, lane, wave, nwaves);
+}
+
 template <typename In, typename Out, int VW, int U>
 __global__ __launch_bounds__(1024) void bwd_large_kernel(
-    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
-    typename Out::storage* __restrict__ dx, int64_t rows, int cols, int S, SplitWorkspace w,
-    uint32_t tag0) {
+    const typename In::storage* y, const typename In::storage* dy, typename Out::storage* dx,
+    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0) {
+  constexpr int kPeersPerLane = 4;
   __shared__ float red[16];
   __shared__ float bcast;
+  __shared__ uint64_t missing_lanes[kPeersPerLane];
+  __shared__ float peer[kPeersPerLane * kWave];  // the row's partials, when a wait gave up
 
   const int T = blockDim.x;
   const int tid = threadIdx.x;
@@ -300,7 +395,6 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
   const int ntiles = (per_thread + U - 1) / U;
   const uint32_t vin = (uint32_t)g * (VW * In::bytes);
   const uint32_t vout = (uint32_t)g * (VW * Out::bytes);
-  if (S > 1) tag0 = split_tag0(w, tag0);
   bool gave_up = false;  // per lane of the first wave
 
   uint32_t k = 0;
@@ -309,51 +403,68 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
     const rsrc_t rdy = make_rsrc(dy + row * cols, (uint64_t)cols * In::bytes);
     const rsrc_t rdx = make_rsrc(dx + row * cols, (uint64_t)cols * Out::bytes);
 
-    float d = 0.0f, cd = 0.0f;  // running sum and its compensation
-    for (int tt = 0; tt < ntiles; ++tt) {
-      InVec<In, VW> a[U], b[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int j = (tt * U + u) * RT;
-        const uint32_t so = (uint32_t)j * (VW * In::bytes);
-        if (j + g < nvec) {
-          a[u].load(ry, vin, so);
-          b[u].load(rdy, vin, so);
-        } else {
-          a[u].set_zero();
-          b[u].set_zero();
-        }
-      }
-      float ts = 0.0f;
-#pragma unroll
-      for (int u = 0; u < U; ++u) ts = dot_vec(a[u], b[u], ts);
-      const float yk = ts - cd;
-      const float t = d + yk;
-      cd = __builtin_isfinite(t) ? (t - d) - yk : 0.0f;
-      d = t;
-    }
-    d -= cd;
-    d = group_reduce<kWave, SumOp>(d);
-    if (lane == 0) red[wave] = d;
-    __syncthreads();
-    d = red[0];
-    for (int i = 1; i < nwaves; ++i) d += red[i];
+    float d = bwd_large_pass1<In, VW, U>(ry, rdy, g, RT, nvec, ntiles, red, lane, wave, nwaves);
 
     if (S > 1) {
-      if (wave == 0) {
-        const uint32_t b0 = (uint32_t)q * S;
-        const uint64_t tag = (uint64_t)(tag0 + k) << 32;
-        const uint32_t slot = k & 1;
-        if (lane == 0)
-          __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(d),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // When a wait gave up, wave 0 parks its partials in LDS (peer[l + 64 j])
+      // and the block recomputes the missing ones.
+      auto finish = [&](const float (&pr)[kPeersPerLane]) {
         float p = 0.0f;
-        for (int bb = lane; bb < S; bb += kWave) p += split_poll_word(w, b0 + bb, slot, tag,
-                                                                      &gave_up);
+#pragma unroll
+        for (int j = 0; j < kPeersPerLane; ++j)
+          if (lane + j * kWave < S) p += pr[j];
         p = group_reduce<kWave, SumOp>(p);  // fixed lane order: deterministic
         if (lane == 0) bcast = p;
+      };
+      if (wave == 0) {
+        const uint32_t tag = tag0 + k;
+        uint64_t* gw = split_group_words(w, q, k & 1, S);
+        if (lane == 0) split_publish(gw, S, c, tag, d, d);
+        float pr[kPeersPerLane];
+        uint64_t any = 0;
+#pragma unroll
+        for (int j = 0; j < kPeersPerLane; ++j) {
+          const int bb = lane + j * kWave;
+          bool ok = true;
+          float unused = 0.0f;
+          pr[j] = 0.0f;
+          if (bb == c) pr[j] = d;
+          else if (bb < S) ok = split_poll(w, gw, S, bb, tag, &gave_up, &unused, &pr[j]);
+          const uint64_t miss = lanes_missing(ok);
+          if (lane == 0) missing_lanes[j] = miss;
+          any |= miss;
+        }
+        if (any == 0) {
+          finish(pr);
+        } else {
+#pragma unroll
+          for (int j = 0; j < kPeersPerLane; ++j) peer[lane + j * kWave] = pr[j];
+        }
       }
       __syncthreads();
+      uint64_t any = 0;
+#pragma unroll
+      for (int j = 0; j < kPeersPerLane; ++j) any |= missing_lanes[j];
+      if (any != 0) {
+#pragma unroll 1
+        for (int j = 0; j < kPeersPerLane; ++j) {
+          for (uint64_t mm = missing_lanes[j]; mm != 0; mm &= mm - 1) {
+            const int l = __builtin_ctzll(mm);
+            __syncthreads();  // red is free again (read before the last barrier)
+            const float r = bwd_large_pass1<In, VW, U>(ry, rdy, (l + j * kWave) * T + tid, RT,
+                                                       nvec, ntiles, red, lane, wave, nwaves);
+            if (tid == 0) peer[l + j * kWave] = r;
+          }
+        }
+        __syncthreads();
+        if (wave == 0) {
+          float pr[kPeersPerLane];
+#pragma unroll
+          for (int j = 0; j < kPeersPerLane; ++j) pr[j] = peer[lane + j * kWave];
+          finish(pr);
+        }
+        __syncthreads();
+      }
       d = bcast;
     }
 
@@ -380,7 +491,8 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
           store_out<Out, VW>(rdx, vout + (uint32_t)j * (VW * Out::bytes), o);
       }
     }
-    // Every wave has read red and bcast before the next row rewrites them.
+    // Every wave has read red, bcast, missing_lanes and peer before the next
+    // row rewrites them.
     __syncthreads();
   }
 }

@@ -14,8 +14,10 @@
 // error that grows with their count.  The per-thread pairs are merged across
 // the wave with DPP/permlane steps and across waves through LDS.  With S > 1
 // the blocks of a row then exchange their pairs once, through the split
-// form's tagged words and workspace (split_row.hpp: protocol, tags, forward
-// progress), and merge them in block order.  Pass 2 reads the block's share
+// form's tagged words and workspace (split_row.hpp: protocol, tags, the
+// bounded wait), and merge them in block order; a block whose wait for a peer
+// gives up runs that peer's pass 1 itself (large_pass1(), the same code), so
+// the merged pair does not depend on the wait.  Pass 2 reads the block's share
 // again, last tile first so that the most recently fetched tiles are re-read
 // while they are most likely still cached, and writes exp(x - M) / sum.
 //
@@ -41,14 +43,93 @@
 
 namespace rowsm {
 
+// Pass 1 of the block whose global threads are g = c * T + t: the block's
+// (max, sum) pair over its share of the row, merged across the wave and then
+// across waves in wave order through red_m / red_s (one barrier).  Called by
+// every thread of the block, for its own share and for a peer's.
+template <typename In, int VW, int U, int MODE>
+__device__ __forceinline__ MaxSum large_pass1(rsrc_t rx, int g, int RT, int nvec, int ntiles, int lim,
+                              float scale, float* red_m, float* red_s, int lane, int wave,
+                              int nwaves) {
+  constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
+  const float ninf = -__builtin_inff();
+  const uint32_t vin = (uint32_t)g * (VW * In::bytes);
+  // Running (max, sum); cs is the compensation of s (the sum is s - cs).
+  float m = ninf, s = 0.0f, cs = 0.0f;
+  for (int tt = 0; tt < ntiles; ++tt) {
+    float f[U][VW];
+    {
+      InVec<In, VW> v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = (tt * U + u) * RT;      // first vector of this slot
+        const int idx = j + g;
+        if (idx < nvec && (!FUSED || idx * VW <= lim))
+          v[u].load(rx, vin, (uint32_t)j * (VW * In::bytes));
+        else
+          v[u].set_neg_inf();
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        v[u].to_float(f[u]);
+        if constexpr (FUSED) fused_apply(f[u], ((tt * U + u) * RT + g) * VW, lim, scale);
+      }
+    }
+    float tm = ninf;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < VW; ++i) tm = fmax_nn(tm, f[u][i]);
+    const float M = fmax_nn(m, tm);
+    const float nml = (M == ninf) ? 0.0f : -M * kLog2e;
+    // The tile is summed on its own and then added to the running sum, so a
+    // thread's serial chain of additions is one tile plus one per tile.
+    float ts = 0.0f;
+    if constexpr (LOG) {
+      const float ref = exp_ref(M);
+#pragma unroll
+      for (int u = 0; u < U; ++u) exp_sum_keep(f[u], ref, &ts);
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < VW; ++i)
+          ts += exp2_fast(__builtin_fmaf(f[u][i], kLog2e, nml));
+    }
+    if (M != m) {
+      s = rescale(s, m, M);
+      cs = rescale(cs, m, M);
+    }
+    const float yk = ts - cs;
+    const float t = s + yk;
+    cs = (t - s) - yk;
+    s = t;
+    m = M;
+  }
+
+  MaxSum ms = group_merge<kWave>({m, s - cs});
+  if (lane == 0) {
+    red_m[wave] = ms.m;
+    red_s[wave] = ms.s;
+  }
+  __syncthreads();
+  ms = {red_m[0], red_s[0]};
+  for (int i = 1; i < nwaves; ++i) ms = merge(ms, {red_m[i], red_s[i]});
+  return ms;
+}
+
 template <typename In, typename Out, int VW, int U, int MODE>
 __global__ __launch_bounds__(1024) void large_row_kernel(
-    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
-    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0, Fused fz) {
+    const typename In::storage* x, typename Out::storage* y, int64_t rows, int cols, int S,
+    SplitWorkspace w, uint32_t tag0, Fused fz) {
   constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
+  // Wave 0 holds up to kPeersPerLane peers per lane in the exchange.
+  constexpr int kPeersPerLane = 4;
   __shared__ float red_m[16];
   __shared__ float red_s[16];
   __shared__ float bcast[2];
+  __shared__ uint64_t missing_lanes[kPeersPerLane];
+  __shared__ MaxSum peer[kPeersPerLane * kWave];  // the row's pairs, when a wait gave up
 
   const int T = blockDim.x;
   const int tid = threadIdx.x;
@@ -63,10 +144,8 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
   const int nvec = cols / VW;
   const int per_thread = (nvec + RT - 1) / RT;  // vector slots of a thread
   const int ntiles = (per_thread + U - 1) / U;
-  const float ninf = -__builtin_inff();
   const uint32_t vin = (uint32_t)g * (VW * In::bytes);
   const uint32_t vout = (uint32_t)g * (VW * Out::bytes);
-  if (S > 1) tag0 = split_tag0(w, tag0);
   bool gave_up = false;  // per lane of the first wave
 
   uint32_t k = 0;
@@ -75,92 +154,77 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
     const rsrc_t ry = make_rsrc(y + row * cols, (uint64_t)cols * Out::bytes);
     const int lim = FUSED ? fused_limit(fz, row, cols) : cols - 1;
 
-    // Pass 1: running (max, sum); cs is the compensation of s (the sum is
-    // s - cs).
-    float m = ninf, s = 0.0f, cs = 0.0f;
-    for (int tt = 0; tt < ntiles; ++tt) {
-      float f[U][VW];
-      {
-        InVec<In, VW> v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int j = (tt * U + u) * RT;      // first vector of this slot
-          const int idx = j + g;
-          if (idx < nvec && (!FUSED || idx * VW <= lim))
-            v[u].load(rx, vin, (uint32_t)j * (VW * In::bytes));
-          else
-            v[u].set_neg_inf();
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          v[u].to_float(f[u]);
-          if constexpr (FUSED) fused_apply(f[u], ((tt * U + u) * RT + g) * VW, lim, fz.scale);
-        }
-      }
-      float tm = ninf;
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int i = 0; i < VW; ++i) tm = fmax_nn(tm, f[u][i]);
-      const float M = fmax_nn(m, tm);
-      const float nml = (M == ninf) ? 0.0f : -M * kLog2e;
-      // The tile is summed on its own and then added to the running sum, so
-      // a thread's serial chain of additions is one tile plus one per tile.
-      float ts = 0.0f;
-      if constexpr (LOG) {
-        const float ref = exp_ref(M);
-#pragma unroll
-        for (int u = 0; u < U; ++u) exp_sum_keep(f[u], ref, &ts);
-      } else {
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-          for (int i = 0; i < VW; ++i)
-            ts += exp2_fast(__builtin_fmaf(f[u][i], kLog2e, nml));
-      }
-      if (M != m) {
-        s = rescale(s, m, M);
-        cs = rescale(cs, m, M);
-      }
-      const float yk = ts - cs;
-      const float t = s + yk;
-      cs = (t - s) - yk;
-      s = t;
-      m = M;
-    }
-
-    MaxSum ms = group_merge<kWave>({m, s - cs});
-    if (lane == 0) {
-      red_m[wave] = ms.m;
-      red_s[wave] = ms.s;
-    }
-    __syncthreads();
-    ms = {red_m[0], red_s[0]};
-    for (int i = 1; i < nwaves; ++i) ms = merge(ms, {red_m[i], red_s[i]});
+    MaxSum ms = large_pass1<In, VW, U, MODE>(rx, g, RT, nvec, ntiles, lim, fz.scale, red_m, red_s,
+                                             lane, wave, nwaves);
 
     if (S > 1) {
-      // Exchange with the other blocks of the row (first wave only): publish
-      // this block's pair, merge all S pairs in block order.
-      if (wave == 0) {
-        const uint32_t b0 = (uint32_t)q * S;
-        const uint64_t tag = (uint64_t)(tag0 + k) << 32;
-        const uint32_t slot = k & 1;
-        if (lane == 0) {
-          __hip_atomic_store(&w.wm[2 * (b0 + c) + slot], tag | __float_as_uint(ms.m),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(ms.s),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        MaxSum p = {ninf, 0.0f};
-        for (int b = lane; b < S; b += kWave) p = merge(p, split_poll_pair(w, b0 + b, slot, tag,
-                                                                           &gave_up));
+      // Exchange with the other blocks of the row: wave 0's lane l holds the
+      // pairs of blocks l + 64 j, j < kPeersPerLane; they are merged in block
+      // order (per lane over j, then across lanes).  When a wait gave up,
+      // wave 0 parks its pairs in LDS (peer[l + 64 j]) and the block
+      // recomputes the missing ones.
+      auto finish = [&](const MaxSum (&pr)[kPeersPerLane]) {
+        MaxSum p = {-__builtin_inff(), 0.0f};
+#pragma unroll
+        for (int j = 0; j < kPeersPerLane; ++j)
+          if (lane + j * kWave < S) p = merge(p, pr[j]);
         p = group_merge<kWave>(p);  // fixed lane order: deterministic
         if (lane == 0) {
           bcast[0] = p.m;
           bcast[1] = p.s;
         }
+      };
+      if (wave == 0) {
+        const uint32_t tag = tag0 + k;
+        uint64_t* gw = split_group_words(w, q, k & 1, S);
+        if (lane == 0) split_publish(gw, S, c, tag, ms.m, ms.s);
+        MaxSum pr[kPeersPerLane];
+        uint64_t any = 0;
+#pragma unroll
+        for (int j = 0; j < kPeersPerLane; ++j) {
+          const int b = lane + j * kWave;
+          bool ok = true;
+          pr[j] = {-__builtin_inff(), 0.0f};
+          if (b == c) pr[j] = ms;
+          else if (b < S) ok = split_poll(w, gw, S, b, tag, &gave_up, &pr[j].m, &pr[j].s);
+          const uint64_t miss = lanes_missing(ok);
+          if (lane == 0) missing_lanes[j] = miss;
+          any |= miss;
+        }
+        if (any == 0) {
+          finish(pr);
+        } else {
+#pragma unroll
+          for (int j = 0; j < kPeersPerLane; ++j) peer[lane + j * kWave] = pr[j];
+        }
       }
       __syncthreads();
+      uint64_t any = 0;
+#pragma unroll
+      for (int j = 0; j < kPeersPerLane; ++j) any |= missing_lanes[j];
+      if (any != 0) {
+#pragma unroll 1
+        for (int j = 0; j < kPeersPerLane; ++j) {
+          for (uint64_t mm = missing_lanes[j]; mm != 0; mm &= mm - 1) {
+            const int l = __builtin_ctzll(mm);
+            // red_m / red_s are free again: every wave read them before the
+            // barrier above (or before the previous recomputation's).
+            __syncthreads();
+            const MaxSum r = large_pass1<In, VW, U, MODE>(rx, (l + j * kWave) * T + tid, RT, nvec,
+                                                          ntiles, lim, fz.scale, red_m, red_s,
+                                                          lane, wave, nwaves);
+            if (tid == 0) peer[l + j * kWave] = r;
+          }
+        }
+        __syncthreads();
+        if (wave == 0) {
+          MaxSum pr[kPeersPerLane];
+#pragma unroll
+          for (int j = 0; j < kPeersPerLane; ++j) pr[j] = peer[lane + j * kWave];
+          finish(pr);
+        }
+        __syncthreads();
+      }
       ms = {bcast[0], bcast[1]};
     }
 
@@ -193,8 +257,8 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
         if (idx < nvec) store_out<Out, VW>(ry, vout + (uint32_t)j * (VW * Out::bytes), o);
       }
     }
-    // Every wave has read red_m / red_s and bcast before the next row
-    // rewrites them.
+    // Every wave has read red_m / red_s, bcast, missing_lanes and peer before
+    // the next row rewrites them.
     __syncthreads();
   }
 }

@@ -13,10 +13,9 @@
 namespace rowsm {
 
 constexpr int kMaxDevices = 64;
-constexpr int kSplitMaxBlocks = 1 << 20;  // split-form workspace capacity in blocks
-// Blocks of one single-read launch recorded under stream capture (the size
-// of its private workspace slice; split_capture_reserve()).
-constexpr int kCaptureMaxBlocks = 1 << 15;
+// Blocks one launch of an exchanging form may use in an exchange workspace
+// (32 bytes each); larger grids loop their row groups over the rows.
+constexpr int kSplitMaxBlocks = 1 << 20;
 // Blocks per row of the two-pass LARGE form at most (and at most the compute
 // units: all of a row's blocks must be resident at once, and a 1024-thread
 // block of it may take a whole compute unit's registers).  Wave 0 of a
@@ -58,11 +57,6 @@ struct Call {
   int mode = kPlain;
   Fused fz{1.0f, 0, 0};
   const void* dy = nullptr;  // softmax backward: x holds y, dy the gradient, y receives dx
-  // LARGE forms that exchange between blocks (single-read, or two-pass with
-  // more than one block per row) on a capturing stream: the launch's private
-  // workspace slice and its capacity in blocks (null when not captured).
-  char* cap_slice = nullptr;
-  int64_t cap_blocks = 0;
 };
 
 // Calls L<In, Out, VW, MODE>::run(c) for the call's dtype pair and vector
@@ -108,11 +102,8 @@ int launch_bwd_large(const Call& c, int in_dt, int out_dt);
 int launch_moe_f32(const Call& c, int out_dt);
 int launch_moe_bf16(const Call& c, int out_dt);
 
-// Split-form diagnostics (launch_split_common.hip).
+// Exchange workspace diagnostics and test settings (launch_split_common.hip).
 int64_t split_wait_failures_current_device();
-// Reserves a private workspace slice for a single-read launch of at most
-// `blocks` blocks recorded under stream capture (launch_split_common.hip).
-// ROWSM_EINVAL when there is no room or no capture region on this device.
-int split_capture_reserve(int64_t blocks, char** slice);
+int64_t split_set_wait_limit(int64_t polls);
 
 }  // namespace rowsm

@@ -1,197 +1,220 @@
-// Per-device state of the single-read split-row form.
+// Exchange workspaces of the forms whose blocks share a row (the single-read
+// split forms, and the two-pass forms with several blocks per row).
 //
-// The workspace (two 64-bit words per block and row parity, an error count;
-// 32 MiB) is allocated and cleared on the first split launch on a device and
-// kept until the process ends.  Split launches on one device are ordered
-// through `last` (each waits for the previous one, whatever its stream), so
-// two launches never use the workspace at the same time.  `last` only orders
-// device work against device work, so it is recorded without a system-scope
-// fence (and without timing).  Tags are handed
-// out from `next_tag`: a launch whose blocks process at most n rows each uses
-// tags tag0 .. tag0 + n - 1, so a tag is never reused while the workspace may
-// still hold it; when the 32-bit tag space runs out the workspace is cleared
-// again and tags restart at 1.
+// A launch takes a region of 32 bytes per block (two parities of a max and a
+// sum word, split_row.hpp) and a run of 32-bit tags from a ring of words per
+// device.  The first ring is the static device array `exchange_words` (64 MiB
+// per device, zero from the moment the library's device code is loaded, so
+// no call allocates, clears or waits for anything to use it); its address is
+// looked up once per device (hipGetSymbolAddress, with that device current)
+// and host code never passes the array's own name to a kernel.  A ring's tags
+// count up from 1, and once they pass 2^30 the ring is retired (kept, unused)
+// and replaced by a 64 MiB allocation cleared on a private stream of the
+// library that the host waits for (that stream holds nothing else, so no
+// caller's work is waited for): a ring never sees two launches with the same
+// tag, so a word it holds that carries a launch's tag was written by that
+// launch.  Regions are handed out in turn by an atomic cursor, so launches in
+// flight together on any streams take disjoint regions unless the ring wraps
+// while one of them is still waiting to run.  No launch waits for or is
+// ordered after another.  Launches in flight together have different tags,
+// so words of another launch that shares the region after a wrap cost at most
+// waits that give up and a recomputation, never a wrong result.
 //
-// Launches recorded under stream capture cannot take tags from the host (a
-// graph replays the recorded arguments), so each gets a private slice of a
-// per-device capture region (64 MiB, allocated and cleared with the shared
-// workspace): a 256-byte header {epoch, tag base} followed by the exchange
-// words of at most kCaptureMaxBlocks blocks.  The graph replays the slice's
-// epoch kernel before the split kernel; it advances the epoch by the
-// launch's n tags and publishes the tag base, epoch + 1, which the kernel
-// reads.  Only that one recorded launch ever uses the slice, with the same
-// grid and row count at every replay, so every word a replay reads was
-// written by that replay or by the one before it, whose tags are the n
-// values just below the current ones (modulo 2^32): stale words never match
-// and the slice never needs clearing.  Replays of one recorded launch are
-// ordered by their stream; graph executables that share a recorded launch
-// must not run at the same time.  A slice is never reclaimed: when the
-// region is full (or was never created because no single-read launch has run
-// outside capture on the device) a captured launch takes the two-pass form.
+// Stream capture: a graph replays the region and the tags recorded at
+// capture, so a captured launch is preceded by a recorded kernel that clears
+// its region; every replay then starts from cleared words.  Graph
+// executables that contain the same captured launch must not run at the same
+// time (they would share tags as well as words).  A ring is never renewed
+// under capture.
+#include <atomic>
 #include <mutex>
 
 #include "split_launch.hpp"
 
 namespace rowsm {
+
+constexpr int64_t kRingBlocks = (int64_t)1 << 21;  // 64 MiB per ring
+constexpr int64_t kRingHeaderWords = 32;           // 256 bytes: the give-up counter
+static_assert(kSplitMaxBlocks <= kRingBlocks / 2, "a launch takes at most half the ring");
+static __device__ __align__(256) uint64_t exchange_words[kRingHeaderWords + 4 * kRingBlocks];
+
 namespace {
 
-struct SplitState {
-  std::mutex mu;
-  void* base = nullptr;
-  hipEvent_t last = nullptr;
-  bool have_last = false;
-  uint32_t next_tag = 1;
-  char* cap = nullptr;   // capture region
-  size_t cap_used = 0;   // bytes handed out as slices
+// A ring is replaced once its tags pass this count (a launch takes at most
+// kMaxLaunchTags), so a ring's tags stay below 2^31: unique and never 0 in
+// 32 bits.
+constexpr uint64_t kRingRenewTag = (uint64_t)1 << 30;
+constexpr uint64_t kMaxLaunchTags = (uint64_t)1 << 30;
+// Polls before a wait gives up: about 0.1 s at the latency of an agent-scope
+// load under streaming traffic.
+constexpr uint32_t kDefaultWaitLimit = 1u << 16;
+
+struct Ring {
+  uint64_t* words = nullptr;  // device memory, 4 words per block
+  int64_t blocks = 0;
+  std::atomic<int64_t> cursor{0};
+  std::atomic<uint64_t> next_tag{1};
+
+  // First block of a region of n <= blocks blocks.
+  int64_t take(int64_t n) {
+    int64_t old = cursor.load(std::memory_order_relaxed);
+    for (;;) {
+      const int64_t at = old + n <= blocks ? old : 0;
+      if (cursor.compare_exchange_weak(old, at + n, std::memory_order_relaxed)) return at;
+    }
+  }
+  // First of n consecutive tags (1 <= n <= kMaxLaunchTags), all below 2^31;
+  // false when they would not be (the ring is renewed long before, so this
+  // needs several launches of about 2^30 rows per block group at once).
+  bool tags(uint64_t n, uint32_t* t0) {
+    const uint64_t t = next_tag.fetch_add(n, std::memory_order_relaxed);
+    if (t + n > ((uint64_t)1 << 31)) return false;
+    *t0 = (uint32_t)t;
+    return true;
+  }
 };
-SplitState g_split[kMaxDevices];
 
-constexpr size_t kSplitWorkspaceBytes = (size_t)kSplitMaxBlocks * 32 + 256;
-constexpr size_t kSplitErrorOffset = (size_t)kSplitMaxBlocks * 32;
-constexpr size_t kCaptureRegionBytes = (size_t)64 << 20;
-constexpr size_t kSliceHeaderBytes = 256;
+struct DeviceState {
+  std::mutex mu;                     // set-up and renewal of this device's rings
+  std::atomic<Ring*> ring{nullptr};  // current ring (retired ones are kept)
+  uint32_t* failures = nullptr;      // give-up counter (exchange_words header)
+};
 
-size_t slice_bytes(int64_t blocks) {
-  return (kSliceHeaderBytes + (size_t)blocks * 32 + 255) / 256 * 256;
+DeviceState g_dev[kMaxDevices];
+std::atomic<uint32_t> g_wait_limit{kDefaultWaitLimit};
+
+__global__ void exchange_clear_kernel(uint64_t* w, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    w[i] = 0;
 }
 
-// Advances a captured launch's epoch by its tag count and publishes the tag
-// base of this replay (hdr[0] epoch, hdr[1] tag base).
-__global__ void split_epoch_kernel(uint32_t* hdr, uint32_t ntags) {
-  if (threadIdx.x == 0) {
-    const uint32_t e = __hip_atomic_load(&hdr[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&hdr[1], e + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&hdr[0], e + ntags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+int clear_words(uint64_t* w, int64_t n, hipStream_t st) {
+  const int64_t blocks = (n + 255) / 256;
+  (void)hipGetLastError();
+  exchange_clear_kernel<<<dim3((unsigned)(blocks < 1024 ? blocks : 1024)), dim3(256), 0, st>>>(w, n);
+  return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
 }
 
-int split_clear(void* p) {
-  if (hipMemset(p, 0, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
-  return hipDeviceSynchronize() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+// A failed query counts as capture.
+bool stream_capturing(hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess) return true;
+  return cs != hipStreamCaptureStatusNone;
 }
 
-int split_workspace(SplitState& st, SplitWorkspace* ws) {
-  if (!st.base) {
-    void* p = nullptr;
-    if (hipMalloc(&p, kSplitWorkspaceBytes) != hipSuccess) return ROWSM_EHIP;
-    if (split_clear(p) != ROWSM_OK ||
-        hipEventCreateWithFlags(&st.last, hipEventDisableTiming | hipEventDisableSystemFence) !=
-            hipSuccess) {
-      (void)hipFree(p);
-      return ROWSM_EHIP;
-    }
-    st.base = p;
-    st.next_tag = 1;
-    // The capture region is optional: without it captured launches take the
-    // two-pass form.
-    void* r = nullptr;
-    if (hipMalloc(&r, kCaptureRegionBytes) == hipSuccess) {
-      if (hipMemset(r, 0, kCaptureRegionBytes) == hipSuccess &&
-          hipDeviceSynchronize() == hipSuccess) {
-        st.cap = static_cast<char*>(r);
-        st.cap_used = 0;
-      } else {
-        (void)hipFree(r);
-      }
-    }
-    (void)hipGetLastError();
-  }
-  char* b = static_cast<char*>(st.base);
-  ws->wm = reinterpret_cast<uint64_t*>(b);
-  ws->ws = reinterpret_cast<uint64_t*>(b + (size_t)kSplitMaxBlocks * 16);
-  ws->error = reinterpret_cast<uint32_t*>(b + kSplitErrorOffset);
+int current_device(DeviceState** d) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
+  *d = &g_dev[dev];
   return ROWSM_OK;
 }
 
-// Reserve n consecutive tags (n >= 1); clears the workspace when the tag
-// space would wrap.
-int split_tags(SplitState& st, uint64_t n, uint32_t* tag0) {
-  if (n >= 0x80000000ull) return ROWSM_EINVAL;
-  if ((uint64_t)st.next_tag + n > 0xffffffffull) {
-    if (st.have_last && hipEventSynchronize(st.last) != hipSuccess) return ROWSM_EHIP;
-    if (split_clear(st.base) != ROWSM_OK) return ROWSM_EHIP;
-    st.next_tag = 1;
+// A fresh ring in place of one whose tags passed kRingRenewTag: an
+// allocation cleared on a private stream that the host waits for.  nullptr
+// when that fails.
+Ring* fresh_ring() {
+  hipStream_t s = nullptr;
+  void* p = nullptr;
+  Ring* fresh = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) == hipSuccess) {
+    if (hipMalloc(&p, (size_t)kRingBlocks * 32) == hipSuccess) {
+      const bool cleared = clear_words(static_cast<uint64_t*>(p), 4 * kRingBlocks, s) == ROWSM_OK;
+      if (hipStreamSynchronize(s) == hipSuccess && cleared) {
+        fresh = new Ring();
+        fresh->words = static_cast<uint64_t*>(p);
+        fresh->blocks = kRingBlocks;
+      } else {
+        (void)hipFree(p);
+      }
+    }
+    (void)hipStreamDestroy(s);
   }
-  *tag0 = st.next_tag;
-  st.next_tag += (uint32_t)n;
+  (void)hipGetLastError();
+  return fresh;
+}
+
+// The current ring of the device: exchange_words (its address looked up on
+// first use), or its replacement once the tags pass kRingRenewTag (not under
+// capture; when a replacement cannot be made the ring stays, and its launches
+// fail once the tags run out).
+int device_ring(DeviceState* d, bool capturing, Ring** out) {
+  Ring* r = d->ring.load(std::memory_order_acquire);
+  if (r && (capturing || r->next_tag.load(std::memory_order_relaxed) <= kRingRenewTag)) {
+    *out = r;
+    return ROWSM_OK;
+  }
+  std::lock_guard<std::mutex> lock(d->mu);
+  r = d->ring.load(std::memory_order_relaxed);
+  if (!r) {
+    uint64_t* p = nullptr;
+    if (hipGetSymbolAddress(reinterpret_cast<void**>(&p), HIP_SYMBOL(exchange_words)) !=
+            hipSuccess ||
+        p == nullptr) {
+      (void)hipGetLastError();
+      return ROWSM_EHIP;
+    }
+    r = new Ring();
+    r->words = p + kRingHeaderWords;
+    r->blocks = kRingBlocks;
+    d->failures = reinterpret_cast<uint32_t*>(p);
+    d->ring.store(r, std::memory_order_release);
+  } else if (!capturing && r->next_tag.load(std::memory_order_relaxed) > kRingRenewTag) {
+    if (Ring* fresh = fresh_ring()) {
+      r = fresh;
+      d->ring.store(r, std::memory_order_release);
+    }
+  }
+  *out = r;
   return ROWSM_OK;
 }
 
 }  // namespace
 
-int split_begin(const Call& c, uint64_t ntags, SplitTicket* t) {
-  if (c.cap_slice) {
-    if (ntags >= 0x80000000ull) return ROWSM_EINVAL;
-    uint32_t* hdr = reinterpret_cast<uint32_t*>(c.cap_slice);
-    uint64_t* words = reinterpret_cast<uint64_t*>(c.cap_slice + kSliceHeaderBytes);
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
-    t->captured = true;
-    t->ws.wm = words;
-    t->ws.ws = words + 2 * c.cap_blocks;
-    t->ws.error = reinterpret_cast<uint32_t*>(static_cast<char*>(g_split[dev].base) +
-                                              kSplitErrorOffset);
-    t->ws.dtag = hdr + 1;
-    t->tag0 = 0;
-    (void)hipGetLastError();
-    split_epoch_kernel<<<1, 64, 0, c.st>>>(hdr, (uint32_t)ntags);
-    return hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
-  }
-  hipStream_t stream = c.st;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
-  SplitState& st = g_split[dev];
-  st.mu.lock();
-  int r = split_workspace(st, &t->ws);
-  if (r == ROWSM_OK) r = split_tags(st, ntags, &t->tag0);
-  if (r == ROWSM_OK && st.have_last && hipStreamWaitEvent(stream, st.last, 0) != hipSuccess)
-    r = ROWSM_EHIP;
-  if (r != ROWSM_OK) {
-    st.mu.unlock();
-    return r;
-  }
-  t->dev = dev;
+int exchange_ring(const Call& c, ExchangeRing* r) {
+  DeviceState* d = nullptr;
+  int st = current_device(&d);
+  r->capturing = stream_capturing(c.st);
+  Ring* ring = nullptr;
+  if (st == ROWSM_OK) st = device_ring(d, r->capturing, &ring);
+  if (st != ROWSM_OK) return st;
+  r->ring = ring;
+  r->failures = d->failures;
+  r->max_blocks = kSplitMaxBlocks;
   return ROWSM_OK;
 }
 
-int split_end(SplitTicket* t, hipStream_t stream, bool launched) {
-  if (t->captured) return ROWSM_OK;
-  SplitState& st = g_split[t->dev];
-  int r = ROWSM_OK;
-  if (launched) {
-    if (hipEventRecord(st.last, stream) == hipSuccess) st.have_last = true;
-    else r = ROWSM_EHIP;
-  }
-  st.mu.unlock();
-  t->dev = -1;
-  return r;
-}
-
-int split_capture_reserve(int64_t blocks, char** slice) {
-  int dev = 0;
-  if (blocks < 1 || blocks > kCaptureMaxBlocks) return ROWSM_EINVAL;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EINVAL;
-  SplitState& st = g_split[dev];
-  std::lock_guard<std::mutex> lock(st.mu);
-  const size_t need = slice_bytes(blocks);
-  if (!st.cap || st.cap_used + need > kCaptureRegionBytes) return ROWSM_EINVAL;
-  *slice = st.cap + st.cap_used;
-  st.cap_used += need;
+int exchange_begin(const Call& c, const ExchangeRing& r, int64_t blocks, uint64_t ntags,
+                   Exchange* e) {
+  if (blocks < 1 || blocks > r.max_blocks || ntags < 1 || ntags > kMaxLaunchTags)
+    return ROWSM_EINVAL;
+  Ring* ring = static_cast<Ring*>(r.ring);
+  uint32_t t0 = 0;
+  if (!ring->tags(ntags, &t0)) return ROWSM_EINVAL;
+  uint64_t* words = ring->words + 4 * ring->take(blocks);
+  if (r.capturing && clear_words(words, 4 * blocks, c.st) != ROWSM_OK) return ROWSM_EHIP;
+  e->ws.words = words;
+  e->ws.error = r.failures;
+  e->ws.limit = g_wait_limit.load(std::memory_order_relaxed);
+  e->tag0 = t0;
   return ROWSM_OK;
 }
 
 int64_t split_wait_failures_current_device() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ROWSM_EHIP;
-  SplitState& st = g_split[dev];
-  std::lock_guard<std::mutex> lock(st.mu);
-  if (!st.base) return 0;  // no split launch on this device yet
-  if (st.have_last && hipEventSynchronize(st.last) != hipSuccess) return ROWSM_EHIP;
+  DeviceState* d = nullptr;
+  if (current_device(&d) != ROWSM_OK) return ROWSM_EHIP;
+  if (!d->ring.load(std::memory_order_acquire)) return 0;  // no exchange yet
   uint32_t n = 0;
-  if (hipMemcpy(&n, static_cast<const char*>(st.base) + kSplitErrorOffset, sizeof(n),
-                hipMemcpyDeviceToHost) != hipSuccess)
+  if (hipDeviceSynchronize() != hipSuccess ||
+      hipMemcpy(&n, d->failures, sizeof(n), hipMemcpyDeviceToHost) != hipSuccess)
     return ROWSM_EHIP;
   return (int64_t)n;
+}
+
+int64_t split_set_wait_limit(int64_t polls) {
+  uint32_t v = kDefaultWaitLimit;
+  if (polls >= 0) v = polls > 0xffffffffll ? 0xffffffffu : (uint32_t)polls;
+  return (int64_t)g_wait_limit.exchange(v, std::memory_order_relaxed);
 }
 
 }  // namespace rowsm

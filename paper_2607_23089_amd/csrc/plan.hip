@@ -270,8 +270,12 @@ int stream_blocks(int64_t rows, int64_t nvec, int T, int U, int bpc, int cus) {
 // the log form holds x where softmax holds exp(x - m), so it takes the plain
 // plans.
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
-             const rowsm_config* cfg, int cus, int mode, Plan* p) {
+             const rowsm_config* cfg, int cus, int mode, bool inplace, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  // In place (y == x) no form whose blocks exchange partial results is
+  // planned: a block that recomputes a peer's partial reads the peer's share
+  // of x, which the peer may already have overwritten.
+  if (inplace && cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
   const bool fused = mode == kFused;
   const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
   int vw = choose_vw(cols, ib, ob, xa, ya);
@@ -297,9 +301,11 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     } else if (nvec <= 16 * kWave * ((fused ? 32 : 64) / vw < 16 ? (fused ? 32 : 64) / vw : 16)) {
       // whole row in the registers of one block, unless few long rows would
       // then leave most of the device idle
-      variant = few_long_rows(rows, cols * (ib + ob), false, cus) ? ROWSM_LARGE : ROWSM_MEDIUM;
+      variant = !inplace && few_long_rows(rows, cols * (ib + ob), false, cus) ? ROWSM_LARGE
+                                                                             : ROWSM_MEDIUM;
     } else if (!fused && in_dt == ROWSM_BF16 && vw == 8 && nvec <= 16 * kWave * 24) {
-      variant = few_long_rows(rows, cols * (ib + ob), true, cus) ? ROWSM_LARGE : ROWSM_MEDIUM;
+      variant = !inplace && few_long_rows(rows, cols * (ib + ob), true, cus) ? ROWSM_LARGE
+                                                                            : ROWSM_MEDIUM;
     } else {
       variant = ROWSM_LARGE;
     }
@@ -434,8 +440,9 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         (fused ? measured_fused_shape(nvec, ib, ob, &shape)
                : measured_row_shape(nvec, ib, ob, &shape))) {
       // (a single-read pick holds one group of blocks per row only while
-      // the rows fit the exchange workspace; beyond, the medium rule stays)
-      if (shape.S > 0 && rows * shape.S > kSplitMaxBlocks) shape = RowShape{};
+      // the rows fit the exchange workspace; beyond, and in place, the
+      // medium rule stays)
+      if (shape.S > 0 && (inplace || rows * shape.S > kSplitMaxBlocks)) shape = RowShape{};
       if (shape.S > 0) {
         variant = ROWSM_LARGE;
         p->variant = variant;
@@ -458,7 +465,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // (and within 2% of the medium form below these row counts): the
     // 16-wave blocks synchronise a whole compute unit's worth of waves at
     // each reduction and leave at most two blocks per compute unit.
-    if (variant == ROWSM_MEDIUM && auto_variant && !fused && p->wpr == 16 &&
+    if (variant == ROWSM_MEDIUM && auto_variant && !fused && !inplace && p->wpr == 16 &&
         cols * ib >= 65536 &&
         (rows >= 8 * (int64_t)cus ||
          ((vpl * vw >= 64 || packed) && rows >= cus / 4))) {
@@ -493,7 +500,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       const int b = cfg->block;
       if (b % kWave || b > 1024) return ROWSM_EINVAL;
     }
-    if (want_split >= 0) {
+    if (want_split >= 0 && !inplace) {
       // Single-read form: T threads per block, S blocks per row (S <= 64:
       // one wave polls the S peers), at most 64 fp32 values per lane (40
       // for widening rows, bf16 -> f32, which write twice what they read).
@@ -555,9 +562,9 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->block = T;
         p->grid = grid;
         p->prefetch = cfg && cfg->prefetch == 1;
-        // registers: at most 48 values per lane, plain and log forms only
-        // (split_launch.hpp)
-        if (p->prefetch && (fused || nv * vw > 48)) return ROWSM_EINVAL;
+        // registers: at most 48 values per lane (44 for fp32 input), plain
+        // and log forms only (split_launch.hpp)
+        if (p->prefetch && (fused || nv * vw > (ib == 4 ? 44 : 48))) return ROWSM_EINVAL;
         return ROWSM_OK;
       }
       if (want_split > 0) return ROWSM_EINVAL;
@@ -572,7 +579,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
     const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
     p->grid = rows < cap ? rows : cap;
-    p->stream = stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
+    p->stream = inplace ? 1 : stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
     return ROWSM_OK;
   }
   return ROWSM_EINVAL;
@@ -589,8 +596,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
 //           256-thread blocks per row for few rows, as the forward), or two
 //           streaming passes for rows longer than that.
 int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t ia,
-                  uintptr_t dxa, const rowsm_config* cfg, int cus, Plan* p) {
+                  uintptr_t dxa, const rowsm_config* cfg, int cus, bool inplace, Plan* p) {
   if (!config_in_domain(cfg)) return ROWSM_EINVAL;
+  // In place (dx == y or dx == dy): no exchanging form, as plan_for().
+  if (inplace && cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
   if (cfg && cfg->packed == 1) return ROWSM_EINVAL;  // no packed form: always raw
   const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
   int vw = choose_vw(cols, ib, ob, ia, dxa);
@@ -613,7 +622,8 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     if (nvec <= 32)
       variant = ROWSM_SMALL;
     else if (nvec <= 16 * kWave * nv_cap &&
-             !few_long_rows(rows, cols * (2 * ib + ob), false, cus, kFewRowsMinBytesBackward))
+             (inplace ||
+              !few_long_rows(rows, cols * (2 * ib + ob), false, cus, kFewRowsMinBytesBackward)))
       variant = ROWSM_MEDIUM;
     else
       variant = ROWSM_LARGE;
@@ -691,7 +701,8 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     // input (measured 4-20% faster there at 16384-65536 columns in every
     // dtype pair, and within 1% of the medium form at 256-512 rows; the
     // forward's reason).
-    if (auto_variant && wpr == 16 && cols * ib >= 65536 && rows >= 4 * (int64_t)cus) {
+    if (auto_variant && !inplace && wpr == 16 && cols * ib >= 65536 &&
+        rows >= 4 * (int64_t)cus) {
       variant = ROWSM_LARGE;
       p->variant = variant;
     } else {
@@ -711,7 +722,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
   }
   if (variant == ROWSM_LARGE) {
     const int want_split = cfg ? cfg->split_blocks : 0;
-    if (want_split >= 0) {
+    if (want_split >= 0 && !inplace) {
       // 512-thread blocks (measured 0-4% faster than 256 on long rows of
       // every dtype pair with one group per row); few rows as the forward
       // plan, with 256-thread blocks unless a block size is given.
@@ -757,7 +768,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     p->block = (cfg && cfg->block > 0) ? cfg->block : 1024;
     const int64_t cap = (int64_t)cus * (bpc ? bpc : 1);
     p->grid = rows < cap ? rows : cap;
-    p->stream = stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
+    p->stream = inplace ? 1 : stream_blocks(rows, nvec, p->block, p->u, bpc, cus);
     return ROWSM_OK;
   }
   return ROWSM_EINVAL;

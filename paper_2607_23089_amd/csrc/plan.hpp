@@ -19,14 +19,15 @@ int dtype_bytes(int dt);  // 4 for ROWSM_F32, 2 for ROWSM_BF16
 bool dtype_ok(int dt);    // ROWSM_F32 or ROWSM_BF16
 
 // Forward plan for mode kPlain, kFused or kLog over rows x cols, x at address
-// xa and y at ya (alignment only), on a device of cus compute units.
+// xa and y at ya (alignment only), on a device of cus compute units; inplace
+// (y == x) excludes the forms whose blocks exchange partial results.
 int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, uintptr_t ya,
-             const rowsm_config* cfg, int cus, int mode, Plan* p);
+             const rowsm_config* cfg, int cus, int mode, bool inplace, Plan* p);
 
 // Backward plan: ia is the alignment of the inputs y and dy together, dxa of
-// the output dx.
+// the output dx; inplace (dx == y or dx == dy) as plan_for().
 int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t ia,
-                  uintptr_t dxa, const rowsm_config* cfg, int cus, Plan* p);
+                  uintptr_t dxa, const rowsm_config* cfg, int cus, bool inplace, Plan* p);
 
 // Grouped top-2 plan over ngroups groups of g scores at address sa.
 int plan_moe(int64_t ngroups, int64_t g, int in_dt, uintptr_t sa, const rowsm_config* cfg,

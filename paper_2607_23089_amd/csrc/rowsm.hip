@@ -1,6 +1,6 @@
 // Host side of the row-softmax library: argument validation, the template
-// dispatch over the kernel families, stream-capture handling and the C ABI
-// declared in include/rowsm.h.  The launcher that picks a family and its
+// dispatch over the kernel families and the C ABI declared in
+// include/rowsm.h.  The launcher that picks a family and its
 // launch shape for each call is in plan.hip.
 #include <hip/hip_runtime.h>
 
@@ -52,69 +52,6 @@ int launch(const Call& c, int in_dt, int out_dt) {
   }
 }
 
-// ---- stream capture -------------------------------------------------------------
-//
-// The single-read split form takes exchange tags from the host for every
-// eager launch; a captured graph would replay one launch's tags, and a replay
-// could then accept words left by the previous replay as its own.  While the
-// launch stream is being captured, a single-read launch therefore gets a
-// private workspace slice whose tags a small epoch kernel, recorded before
-// it, advances on the device at every replay (launch_split_common.hip).
-// Without a slice (the capture region is full, or was never created because
-// no single-read launch has run outside capture on this device) long rows
-// take the two-pass form, which keeps no state between launches, and a
-// single-read form forced by the caller is refused.  A failed query counts
-// as capture.
-bool stream_capturing(hipStream_t s) {
-  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(s, &cs) != hipSuccess) return true;
-  return cs != hipStreamCaptureStatusNone;
-}
-
-template <typename Replan>
-int prepare_capture(const rowsm_config* cfg, Call* c, Replan replan) {
-  Plan* p = &c->p;
-  // The single-read form exchanges through the workspace at any S (S = 1
-  // included); the two-pass form only with several blocks per row.
-  const int S = p->split > 0 ? p->split : p->stream;
-  const bool exchanges = p->split > 0 || p->stream > 1;
-  if (p->variant != ROWSM_LARGE || !exchanges || !stream_capturing(c->st)) return ROWSM_OK;
-  const int64_t groups = kCaptureMaxBlocks / S;
-  const int64_t blocks = (c->rows < groups ? c->rows : groups) * S;
-  if (split_capture_reserve(blocks, &c->cap_slice) == ROWSM_OK) {
-    c->cap_blocks = blocks;
-    return ROWSM_OK;
-  }
-  if (cfg && cfg->split_blocks > 0) return ROWSM_EINVAL;
-  if (p->measured) {
-    // A row that the measured table sent to the single-read form fits the
-    // medium form, which keeps no state between launches either and reads
-    // x once: the medium family's own plan.
-    rowsm_config medium;
-    if (cfg) {
-      medium = *cfg;
-    } else {
-      std::memset(&medium, 0, sizeof(medium));
-      medium.packed = -1;
-    }
-    medium.variant = ROWSM_MEDIUM;
-    return replan(&medium);
-  }
-  // The two-pass form with one block per row keeps no state between
-  // launches (a grid cap of one block per compute unit, unless given).
-  rowsm_config two_pass;
-  if (cfg) {
-    two_pass = *cfg;
-  } else {
-    std::memset(&two_pass, 0, sizeof(two_pass));
-    two_pass.packed = -1;
-  }
-  two_pass.variant = ROWSM_LARGE;
-  two_pass.split_blocks = -1;
-  if (two_pass.blocks_per_cu <= 0) two_pass.blocks_per_cu = 1;
-  return replan(&two_pass);
-}
-
 // ---- validation -------------------------------------------------------------
 
 // Host-only argument checks shared by every entry point.  *noop is set when
@@ -158,7 +95,8 @@ int backward_impl(const void* yp, const void* dyp, void* dxp, int64_t rows, int6
   Call c;
   c.cus = cu_count();
   const uintptr_t ia = (uintptr_t)yp | (uintptr_t)dyp;
-  st = plan_backward(rows, cols, in_dt, out_dt, ia, (uintptr_t)dxp, cfg, c.cus, &c.p);
+  const bool inplace = dxp == yp || dxp == dyp;
+  st = plan_backward(rows, cols, in_dt, out_dt, ia, (uintptr_t)dxp, cfg, c.cus, inplace, &c.p);
   if (st != ROWSM_OK) return st;
   c.x = yp;
   c.dy = dyp;
@@ -167,10 +105,6 @@ int backward_impl(const void* yp, const void* dyp, void* dxp, int64_t rows, int6
   c.cols = (int)cols;
   c.st = static_cast<hipStream_t>(stream);
   c.mode = kBackward;
-  st = prepare_capture(cfg, &c, [&](const rowsm_config* tp) {
-    return plan_backward(rows, cols, in_dt, out_dt, ia, (uintptr_t)dxp, tp, c.cus, &c.p);
-  });
-  if (st != ROWSM_OK) return st;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   return launch(c, in_dt, out_dt);
 }
@@ -227,7 +161,8 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   if (st != ROWSM_OK || noop) return st;
   Call c;
   c.cus = cu_count();
-  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus, mode, &c.p);
+  st = plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, cfg, c.cus, mode, x == y,
+                &c.p);
   if (st != ROWSM_OK) return st;
   c.x = x;
   c.y = y;
@@ -236,10 +171,6 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   c.st = static_cast<hipStream_t>(stream);
   c.mode = mode;
   c.fz = fz;
-  st = prepare_capture(cfg, &c, [&](const rowsm_config* tp) {
-    return plan_for(rows, cols, in_dt, out_dt, (uintptr_t)x, (uintptr_t)y, tp, c.cus, mode, &c.p);
-  });
-  if (st != ROWSM_OK) return st;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   return launch(c, in_dt, out_dt);
 }
@@ -321,7 +252,8 @@ extern "C" int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dt
   if (st != ROWSM_OK) return st;
   if (noop) return ROWSM_SMALL;  // nothing is launched; report the smallest family
   Plan p;
-  const int r = plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, kPlain, &p);
+  const int r =
+      plan_for(rows, cols, in_dtype, out_dtype, 256, 256, nullptr, 256, kPlain, false, &p);
   return r == ROWSM_OK ? p.variant : r;
 }
 
@@ -342,9 +274,9 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
     if (mode == kMoe)
       st = plan_moe(rows, cols, in_dt, 256, cfg, 256, &p);
     else if (mode == kBackward)
-      st = plan_backward(rows, cols, in_dt, out_dt, 256, 256, cfg, 256, &p);
+      st = plan_backward(rows, cols, in_dt, out_dt, 256, 256, cfg, 256, false, &p);
     else
-      st = plan_for(rows, cols, in_dt, out_dt, 256, 256, cfg, 256, mode, &p);
+      st = plan_for(rows, cols, in_dt, out_dt, 256, 256, cfg, 256, mode, false, &p);
   }
   if (buf && len > 0) {
     if (st != ROWSM_OK) {
@@ -352,8 +284,8 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
     } else if (noop) {
       std::snprintf(buf, (size_t)len, "empty: no launch");
     } else {
-      // The split form's grid: one group of S blocks per row up to the
-      // workspace capacity (split_slots()), or a residency sized at launch.
+      // The split form's grid: one group of S blocks per row up to the room
+      // of the workspace (split_slots()), or a residency sized at launch.
       int64_t grid = p.grid;
       const char* how = "grid assumes 256 CUs";
       const int S = p.split > 0 ? p.split : (p.variant == ROWSM_LARGE ? p.stream : 1);
@@ -400,6 +332,10 @@ extern "C" int rowsm_describe_op(int op, int64_t rows, int64_t cols, int in_dtyp
 
 extern "C" int64_t rowsm_split_wait_failures(void) {
   return split_wait_failures_current_device();
+}
+
+extern "C" int64_t rowsm_set_split_wait_limit(int64_t polls) {
+  return split_set_wait_limit(polls);
 }
 
 extern "C" const char* rowsm_status_string(int status) {

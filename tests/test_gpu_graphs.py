@@ -2,11 +2,11 @@
 replayed several times, with new inputs written eagerly and the device
 synchronised between replays; every replay is checked against the fp64
 oracle with the operation's tolerance.  Long rows keep the single-read split
-form under capture (a private workspace slice whose tags an epoch kernel
-recorded before each launch advances at every replay): captured replays are
-bitwise equal to eager launches of the same plan, also with eager split
-launches and other graphs' replays in between.  When the capture region is
-full, long rows take the two-pass form and a forced split form is refused.
+form under capture (a region of the device's workspace ring, cleared by a
+kernel recorded before each launch): captured replays are bitwise equal to
+eager launches of the same plan, also with eager split launches (which reuse
+the ring) and other graphs' replays in between, and any number of captured
+exchanging launches can be recorded.
 """
 import numpy as np
 import pytest
@@ -134,7 +134,7 @@ def test_moe_graph_replays():
 
 
 def eager_split_launch():
-    # the first single-read launch outside capture creates the workspaces
+    # a single-read launch outside capture (the first one creates the ring)
     x = torch.zeros(2, 262144, device=DEV)
     R.softmax(x, variant=R.LARGE)
     torch.cuda.synchronize()
@@ -208,7 +208,6 @@ def test_captured_split_form_matches_eager(op, rows, cols, din, dout):
         res = compare_backward(out_np(y, dout), oracle.softmax_backward_f64(xw, dyw, threads=4),
                                xw, dyw, dout)
     assert res["ok"], f"{op} {rows}x{cols}: {res}"
-    assert R.rowsm_split_wait_failures() == 0
 
 
 def test_two_graphs_with_split_launches_alternate():
@@ -231,7 +230,6 @@ def test_two_graphs_with_split_launches_alternate():
             run(out=ref)
             torch.cuda.synchronize()
             assert torch.equal(y, ref), f"alternating graphs, round {i}"
-    assert R.rowsm_split_wait_failures() == 0
 
 
 def test_forced_split_form_under_capture():
@@ -254,12 +252,11 @@ def test_forced_split_form_under_capture():
         torch.cuda.synchronize()
         assert torch.allclose(y, torch.full_like(y, 1.0 / 262144))
         assert torch.allclose(y2, torch.full_like(y2, 1.0 / 262144))
-    assert R.rowsm_split_wait_failures() == 0
 
 
 @pytest.mark.parametrize("rows,cols,din,dout,cfg,want", [
     # the launcher's own single-read pick with one block per row (a full
-    # launch of 1536-vector rows), more rows than one capture slice holds
+    # launch of 1536-vector rows)
     (40000, 6144, "f32", "f32", None, "split=1 "),
     # forced: one block per row, and two
     (1000, 3000, "bf16", "f32", dict(variant=R.LARGE, split_blocks=1), "split=1 "),
@@ -267,8 +264,8 @@ def test_forced_split_form_under_capture():
 ])
 def test_single_read_one_block_per_row_under_capture(rows, cols, din, dout, cfg, want):
     # every single-read launch exchanges through the workspace, one block
-    # per row included: under capture it takes a slice like any other, and
-    # replays (with eager single-read launches in between) match eager
+    # per row included: under capture it takes a ring region like any other,
+    # and replays (with eager single-read launches in between) match eager
     # launches bitwise
     config = R.RowsmConfig(**cfg) if cfg else None
     st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.dtype_code(DT[din]),
@@ -285,68 +282,40 @@ def test_single_read_one_block_per_row_under_capture(rows, cols, din, dout, cfg,
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(y, ref), f"replay {i} [{desc}]"
-    assert R.rowsm_split_wait_failures() == 0
 
 
-@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")  # refused launches record nothing
-def test_zz_capture_region_exhausted_falls_back():
-    # Runs last in this file: it fills the per-device capture region (64 MiB,
-    # 1 MiB per captured 2^15-block launch).  A forced single-read launch is
-    # then refused under capture, the launcher's own plan for long rows takes
-    # the two-pass form and its single-read pick for medium-length rows the
-    # medium form; their replays stay exact.
+def test_many_captured_exchanging_launches():
+    # Captured exchanging launches take ring regions like eager ones and
+    # nothing is reserved for a graph's lifetime: 80 graphs of one
+    # 32768-block single-read launch each (80 MiB of exchange words, more
+    # than the 64 MiB ring) all capture, and each replays exactly, with eager
+    # launches reusing the ring in between.
     eager_split_launch()
     rows, cols = 4096, 4096
-    x = torch.zeros(rows, cols, device=DEV)
-    y = torch.empty_like(x)
+    x = W.random_matrix(rows, cols, "f32", sigma=4.0, seed=11, device=DEV)
     cfg = R.RowsmConfig(variant=R.LARGE, split_blocks=8, block=64)
     st, desc = R.rowsm_describe_op(R.OP_SOFTMAX, rows, cols, R.F32, R.F32, cfg)
     assert st == R.OK and "grid=32768" in desc
-    refused_at = None
+    ref = R.softmax(x, config=cfg).clone()
+    graphs, outs = [], []
     for k in range(80):
+        y = torch.empty_like(x)
         status = []
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             status.append(R.rowsm_forward_config(x.data_ptr(), y.data_ptr(), rows, cols, R.F32,
                                                  R.F32, torch.cuda.current_stream().cuda_stream,
                                                  cfg))
-        if status[0] == R.EINVAL:
-            refused_at = k
-            break
-        assert status[0] == R.OK
-        del g
-    assert refused_at is not None and refused_at <= 64, refused_at
-    # the launcher's own plan for long rows still captures (two-pass form)
-    xs = [W.random_matrix(8, 262144, "f32", sigma=4.0, seed=60 + i) for i in range(3)]
-    xl = torch.empty(8, 262144, device=DEV)
-    yl = torch.empty_like(xl)
-    xl.copy_(xs[0].to(DEV))
-    g = capture(lambda: R.softmax(xl, out=yl))
-
-    def check(i):
-        res = compare(out_np(yl, "f32"), oracle.softmax_f64(widen(xs[i]), threads=4), "f32")
-        assert res["ok"], f"two-pass fallback replay {i}: {res}"
-
-    replay_and_check(g, lambda i: xl.copy_(xs[i].to(DEV)), check)
-    # a full launch of medium-length rows that the launcher sends to the
-    # single-read form takes the medium form instead (no state, one read)
-    rows_m, cols_m = 8201, 6144
-    st, desc = R.rowsm_describe(rows_m, cols_m, R.F32, R.F32)
-    assert st == R.OK and "split=1 " in desc, desc
-    xm_src = [W.random_matrix(rows_m, cols_m, "f32", sigma=4.0, seed=70 + i) for i in range(3)]
-    xm = torch.empty(rows_m, cols_m, device=DEV)
-    ym = torch.empty_like(xm)
-    xm.copy_(xm_src[0].to(DEV))
-    gm = capture(lambda: R.softmax(xm, out=ym))
-    sample = list(range(0, rows_m, 211)) + [rows_m - 1]
-
-    def check_m(i):
-        want = R.softmax(xm, variant=R.MEDIUM)
+        assert status[0] == R.OK, f"capture {k}"
+        graphs.append(g)
+        outs.append(y)
+    for k in (0, 1, 40, 79, 0):
+        outs[k].zero_()
+        eager_split_launch()
         torch.cuda.synchronize()
-        assert torch.equal(ym, want), f"medium fallback replay {i}"
-        res = compare(out_np(ym[sample], "f32"),
-                      oracle.softmax_f64(widen(xm_src[i][sample]), threads=4), "f32")
-        assert res["ok"], f"medium fallback replay {i}: {res}"
-
-    replay_and_check(gm, lambda i: xm.copy_(xm_src[i].to(DEV)), check_m)
-    assert R.rowsm_split_wait_failures() == 0
+        graphs[k].replay()
+        torch.cuda.synchronize()
+        assert torch.equal(outs[k], ref), f"graph {k}"
+    res = compare(out_np(outs[79][::97].contiguous().cpu(), "f32"),
+                  oracle.softmax_f64(widen(x[::97].contiguous().cpu()), threads=4), "f32")
+    assert res["ok"], res

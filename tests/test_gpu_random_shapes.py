@@ -106,4 +106,3 @@ def test_random_shape(case):
         else:
             res = compare(got, oracle.softmax_f64(widen(x[r0:r1].cpu()), threads=4), dout)
         assert res["ok"], f"{what}: {res}"
-    assert R.rowsm_split_wait_failures() == 0

@@ -67,6 +67,5 @@ def test_workload_full_size(name):
             assert torch.all(yb[~at_max] == 0)
     if w.structure == "spike":
         assert torch.all(y.max(dim=1).values >= 1.0 - 1e-6)
-    assert R.rowsm_split_wait_failures() == 0
     del x, y
     torch.cuda.empty_cache()
