@@ -130,6 +130,27 @@ int rowsm_forward(const void *x, void *y, int64_t rows, int64_t cols,
 int rowsm_select(int64_t rows, int64_t cols, int in_dtype, int out_dtype);
 
 /*
+ * rowsm_forward_noalloc: rowsm_forward for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same operation, launcher and kernels, but it
+ * never calls hipMalloc, hipFree or any other allocating routine, on any
+ * call.  The exchange words of the forms whose blocks share a row live in
+ * the library's static device array `scratch` (4 MiB per device, 32 bytes
+ * per block, 2^17 blocks), set up on the first call on each device; a launch
+ * whose row groups would need more blocks than that loops them over the
+ * rows instead, so no shape exceeds it (a launch that still would returns
+ * ROWSM_EINVAL without launching).  Each launch of those forms first clears
+ * its region of the array with a small kernel on `stream`.  Every call on a
+ * device shares the array, which keeps the last call's words: calls that
+ * overlap in time on one device may take the same words and slow each other
+ * down (a block recomputes what it finds cleared or overwritten), never
+ * change each other's results.  Arguments, results and errors as
+ * rowsm_forward.
+ */
+int rowsm_forward_noalloc(const void *x, void *y, int64_t rows, int64_t cols,
+                          int in_dtype, int out_dtype, void *stream);
+
+/*
  * rowsm_forward_variant: rowsm_forward with the kernel family forced
  * (ROWSM_AUTO behaves like rowsm_forward).  Used by tests and benchmarks to
  * check every family on every shape it supports.  A family that cannot run

@@ -9,6 +9,7 @@ Raw entry points (same names and arguments as the C ABI; pointers are ints,
 ``stream`` a hipStream_t handle as an int, 0 = default stream):
 
     rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream) -> status
+    rowsm_forward_noalloc(x, y, rows, cols, in_dtype, out_dtype, stream) -> status
     rowsm_forward_variant(x, y, rows, cols, in_dtype, out_dtype, stream, variant)
     rowsm_forward_config(x, y, rows, cols, in_dtype, out_dtype, stream, cfg)
     rowsm_forward_scaled_causal(x, y, rows, cols, in_dtype, out_dtype, scale,
@@ -39,7 +40,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "librowsm.so")
 
 # Symbols declared in include/rowsm.h.
-EXPORTS = ("rowsm_forward", "rowsm_select", "rowsm_forward_variant",
+EXPORTS = ("rowsm_forward", "rowsm_forward_noalloc", "rowsm_select", "rowsm_forward_variant",
            "rowsm_forward_config", "rowsm_forward_scaled_causal", "rowsm_log_softmax",
            "rowsm_softmax_backward", "rowsm_moe_group_top2", "rowsm_describe",
            "rowsm_describe_op",
@@ -87,6 +88,8 @@ def lib(path: str | None = None) -> ctypes.CDLL:
     fwd = [vp, vp, i64, i64, i32, i32, vp]
     h.rowsm_forward.argtypes = fwd
     h.rowsm_forward.restype = i32
+    h.rowsm_forward_noalloc.argtypes = fwd
+    h.rowsm_forward_noalloc.restype = i32
     h.rowsm_forward_variant.argtypes = fwd + [i32]
     h.rowsm_forward_variant.restype = i32
     h.rowsm_forward_config.argtypes = fwd + [ctypes.POINTER(RowsmConfig)]
@@ -124,6 +127,10 @@ def lib(path: str | None = None) -> ctypes.CDLL:
 
 def rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream=0) -> int:
     return lib().rowsm_forward(x, y, rows, cols, in_dtype, out_dtype, stream)
+
+
+def rowsm_forward_noalloc(x, y, rows, cols, in_dtype, out_dtype, stream=0) -> int:
+    return lib().rowsm_forward_noalloc(x, y, rows, cols, in_dtype, out_dtype, stream)
 
 
 def rowsm_forward_variant(x, y, rows, cols, in_dtype, out_dtype, stream, variant) -> int:

@@ -57,6 +57,9 @@ struct Call {
   int mode = kPlain;
   Fused fz{1.0f, 0, 0};
   const void* dy = nullptr;  // softmax backward: x holds y, dy the gradient, y receives dx
+  // Exchanging launches take their workspace from the static `scratch` array
+  // (rowsm_forward_noalloc), whatever the device's exchange ring.
+  bool noalloc = false;
 };
 
 // Calls L<In, Out, VW, MODE>::run(c) for the call's dtype pair and vector

@@ -38,6 +38,17 @@ constexpr int64_t kRingHeaderWords = 32;           // 256 bytes: the give-up cou
 static_assert(kSplitMaxBlocks <= kRingBlocks / 2, "a launch takes at most half the ring");
 static __device__ __align__(256) uint64_t exchange_words[kRingHeaderWords + 4 * kRingBlocks];
 
+// The workspace of rowsm_forward_noalloc(), for callers that cannot allocate:
+// the static device array `scratch` (4 MiB per device and a 256-byte header
+// whose first word counts its give-ups), never replaced, so its tags wrap
+// around and every launch on it first clears its own region with a kernel on
+// its stream.  Every call on a device shares it; calls in flight together
+// take different regions unless it wraps, and different tags, so overlapping
+// calls can slow each other down (a block whose peer's words were cleared or
+// overwritten recomputes them) but not change each other's results.
+constexpr int64_t kScratchBlocks = (int64_t)1 << 17;
+static __device__ __align__(256) uint64_t scratch[kRingHeaderWords + 4 * kScratchBlocks];
+
 namespace {
 
 // A ring is replaced once its tags pass this count (a launch takes at most
@@ -52,6 +63,7 @@ constexpr uint32_t kDefaultWaitLimit = 1u << 16;
 struct Ring {
   uint64_t* words = nullptr;  // device memory, 4 words per block
   int64_t blocks = 0;
+  bool clears = false;        // every launch clears its region first (tags wrap)
   std::atomic<int64_t> cursor{0};
   std::atomic<uint64_t> next_tag{1};
 
@@ -63,14 +75,24 @@ struct Ring {
       if (cursor.compare_exchange_weak(old, at + n, std::memory_order_relaxed)) return at;
     }
   }
-  // First of n consecutive tags (1 <= n <= kMaxLaunchTags), all below 2^31;
-  // false when they would not be (the ring is renewed long before, so this
-  // needs several launches of about 2^30 rows per block group at once).
+  // First of n consecutive tags (1 <= n <= kMaxLaunchTags).  A ring that
+  // does not clear keeps them below 2^31 and returns false when they would
+  // not be (it is renewed long before, so this needs several launches of
+  // about 2^30 rows per block group at once); on a clearing ring they wrap
+  // around, skipping runs that would hold 0.
   bool tags(uint64_t n, uint32_t* t0) {
-    const uint64_t t = next_tag.fetch_add(n, std::memory_order_relaxed);
-    if (t + n > ((uint64_t)1 << 31)) return false;
-    *t0 = (uint32_t)t;
-    return true;
+    for (;;) {
+      const uint64_t t = next_tag.fetch_add(n, std::memory_order_relaxed);
+      if (!clears) {
+        if (t + n > ((uint64_t)1 << 31)) return false;
+        *t0 = (uint32_t)t;
+        return true;
+      }
+      if ((uint32_t)t != 0 && (t >> 32) == ((t + n - 1) >> 32)) {
+        *t0 = (uint32_t)t;
+        return true;
+      }
+    }
   }
 };
 
@@ -78,6 +100,8 @@ struct DeviceState {
   std::mutex mu;                     // set-up and renewal of this device's rings
   std::atomic<Ring*> ring{nullptr};  // current ring (retired ones are kept)
   uint32_t* failures = nullptr;      // give-up counter (exchange_words header)
+  std::atomic<Ring*> scratch_ring{nullptr};  // the scratch array, once looked up
+  uint32_t* scratch_failures = nullptr;      // its give-up counter
 };
 
 DeviceState g_dev[kMaxDevices];
@@ -169,6 +193,32 @@ int device_ring(DeviceState* d, bool capturing, Ring** out) {
   return ROWSM_OK;
 }
 
+// The scratch ring of the device: `scratch`, its address looked up on the
+// first allocation-free call on the device, with that device current.
+int device_scratch(DeviceState* d, Ring** out) {
+  Ring* r = d->scratch_ring.load(std::memory_order_acquire);
+  if (!r) {
+    std::lock_guard<std::mutex> lock(d->mu);
+    r = d->scratch_ring.load(std::memory_order_relaxed);
+    if (!r) {
+      uint64_t* p = nullptr;
+      if (hipGetSymbolAddress(reinterpret_cast<void**>(&p), HIP_SYMBOL(scratch)) != hipSuccess ||
+          p == nullptr) {
+        (void)hipGetLastError();
+        return ROWSM_EHIP;
+      }
+      r = new Ring();
+      r->words = p + kRingHeaderWords;
+      r->blocks = kScratchBlocks;
+      r->clears = true;
+      d->scratch_failures = reinterpret_cast<uint32_t*>(p);
+      d->scratch_ring.store(r, std::memory_order_release);
+    }
+  }
+  *out = r;
+  return ROWSM_OK;
+}
+
 }  // namespace
 
 int exchange_ring(const Call& c, ExchangeRing* r) {
@@ -176,11 +226,12 @@ int exchange_ring(const Call& c, ExchangeRing* r) {
   int st = current_device(&d);
   r->capturing = stream_capturing(c.st);
   Ring* ring = nullptr;
-  if (st == ROWSM_OK) st = device_ring(d, r->capturing, &ring);
+  if (st == ROWSM_OK)
+    st = c.noalloc ? device_scratch(d, &ring) : device_ring(d, r->capturing, &ring);
   if (st != ROWSM_OK) return st;
   r->ring = ring;
-  r->failures = d->failures;
-  r->max_blocks = kSplitMaxBlocks;
+  r->failures = c.noalloc ? d->scratch_failures : d->failures;
+  r->max_blocks = c.noalloc ? kScratchBlocks : kSplitMaxBlocks;
   return ROWSM_OK;
 }
 
@@ -192,7 +243,8 @@ int exchange_begin(const Call& c, const ExchangeRing& r, int64_t blocks, uint64_
   uint32_t t0 = 0;
   if (!ring->tags(ntags, &t0)) return ROWSM_EINVAL;
   uint64_t* words = ring->words + 4 * ring->take(blocks);
-  if (r.capturing && clear_words(words, 4 * blocks, c.st) != ROWSM_OK) return ROWSM_EHIP;
+  if ((r.capturing || ring->clears) && clear_words(words, 4 * blocks, c.st) != ROWSM_OK)
+    return ROWSM_EHIP;
   e->ws.words = words;
   e->ws.error = r.failures;
   e->ws.limit = g_wait_limit.load(std::memory_order_relaxed);
@@ -203,12 +255,18 @@ int exchange_begin(const Call& c, const ExchangeRing& r, int64_t blocks, uint64_
 int64_t split_wait_failures_current_device() {
   DeviceState* d = nullptr;
   if (current_device(&d) != ROWSM_OK) return ROWSM_EHIP;
-  if (!d->ring.load(std::memory_order_acquire)) return 0;  // no exchange yet
-  uint32_t n = 0;
-  if (hipDeviceSynchronize() != hipSuccess ||
-      hipMemcpy(&n, d->failures, sizeof(n), hipMemcpyDeviceToHost) != hipSuccess)
-    return ROWSM_EHIP;
-  return (int64_t)n;
+  const bool ring = d->ring.load(std::memory_order_acquire) != nullptr;
+  const bool scr = d->scratch_ring.load(std::memory_order_acquire) != nullptr;
+  if (!ring && !scr) return 0;  // no exchange yet
+  if (hipDeviceSynchronize() != hipSuccess) return ROWSM_EHIP;
+  int64_t total = 0;
+  for (uint32_t* counter : {ring ? d->failures : nullptr, scr ? d->scratch_failures : nullptr}) {
+    uint32_t n = 0;
+    if (counter && hipMemcpy(&n, counter, sizeof(n), hipMemcpyDeviceToHost) != hipSuccess)
+      return ROWSM_EHIP;
+    total += n;
+  }
+  return total;
 }
 
 int64_t split_set_wait_limit(int64_t polls) {

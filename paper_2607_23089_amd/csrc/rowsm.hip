@@ -155,7 +155,8 @@ int moe_impl(const void* sp, void* op, int64_t tokens, int64_t experts, int64_t 
 }
 
 int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, int out_dt,
-                 void* stream, const rowsm_config* cfg, int mode, Fused fz = {1.0f, 0, 0}) {
+                 void* stream, const rowsm_config* cfg, int mode, Fused fz = {1.0f, 0, 0},
+                 bool noalloc = false) {
   bool noop = false;
   int st = validate(x, y, rows, cols, in_dt, out_dt, true, &noop);
   if (st != ROWSM_OK || noop) return st;
@@ -171,6 +172,7 @@ int forward_impl(const void* x, void* y, int64_t rows, int64_t cols, int in_dt, 
   c.st = static_cast<hipStream_t>(stream);
   c.mode = mode;
   c.fz = fz;
+  c.noalloc = noalloc;
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   return launch(c, in_dt, out_dt);
 }
@@ -192,6 +194,12 @@ using namespace rowsm;
 extern "C" int rowsm_forward(const void* x, void* y, int64_t rows, int64_t cols, int in_dtype,
                              int out_dtype, void* stream) {
   return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr, kPlain);
+}
+
+extern "C" int rowsm_forward_noalloc(const void* x, void* y, int64_t rows, int64_t cols,
+                                     int in_dtype, int out_dtype, void* stream) {
+  return forward_impl(x, y, rows, cols, in_dtype, out_dtype, stream, nullptr, kPlain,
+                      Fused{1.0f, 0, 0}, true);
 }
 
 extern "C" int rowsm_forward_variant(const void* x, void* y, int64_t rows, int64_t cols,
