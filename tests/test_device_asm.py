@@ -11,7 +11,8 @@ scanned for properties the kernels rely on:
   * no kernel spills to scratch (and the benchmark workloads' kernels are
     checked by name);
   * the reductions use DPP and the gfx950 permlane swaps, the exponentials
-    v_exp_f32, and bf16 outputs v_cvt_pk_bf16_f32.
+    v_exp_f32, and bf16 outputs v_cvt_pk_bf16_f32;
+  * row loads are non-temporal and row stores non-temporal at device scope.
 """
 import os
 import re
@@ -123,3 +124,15 @@ def test_expected_instructions(asm):
         assert ins in asm, ins
     # no packed-fp32 arithmetic anywhere
     assert not re.search(r"v_pk_(add|mul|fma)_f32", asm)
+
+
+def test_stream_cache_policy(asm):
+    # row data streams through: loads non-temporal, stores non-temporal at
+    # device scope; no row store or load without those bits
+    stores = re.findall(r"buffer_store_dword\S* .*", asm)
+    loads = re.findall(r"buffer_load_(?:dword|ushort)\S* .*", asm)
+    assert stores and loads
+    assert all(re.search(r" nt sc1$", st) for st in stores), \
+        [st for st in stores if not re.search(r" nt sc1$", st)][:3]
+    assert all(re.search(r" nt$", ld) for ld in loads), \
+        [ld for ld in loads if not re.search(r" nt$", ld)][:3]
