@@ -53,8 +53,8 @@ __device__ __forceinline__ void grad_vec(const InVec<In, VW>& a, const InVec<In,
 
 template <typename In, typename Out, int VW, int LPR, int RPL>
 __global__ __launch_bounds__(256) void bwd_small_kernel(
-    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
-    typename Out::storage* __restrict__ dx, int64_t rows, int cols) {
+    const typename In::storage* y, const typename In::storage* dy,
+    typename Out::storage* dx, int64_t rows, int cols) {
   constexpr int RPW = kWave / LPR;     // rows per wave per load instruction
   constexpr int RPT = RPW * RPL;       // rows per wave per task
   const int lane = threadIdx.x & (kWave - 1);
@@ -118,8 +118,8 @@ __global__ __launch_bounds__(256) void bwd_small_kernel(
 // row never overwrites a partial sum a slower wave of its group still reads.
 template <typename In, typename Out, int VW, int NV>
 __global__ __launch_bounds__(1024) void bwd_medium_kernel(
-    const typename In::storage* __restrict__ y, const typename In::storage* __restrict__ dy,
-    typename Out::storage* __restrict__ dx, int64_t rows, int cols, int wpr) {
+    const typename In::storage* y, const typename In::storage* dy,
+    typename Out::storage* dx, int64_t rows, int cols, int wpr) {
   __shared__ float red[2][16];
 
   const int lane = threadIdx.x & (kWave - 1);

@@ -52,7 +52,7 @@ __device__ __forceinline__ float block_row_reduce(float v, int wpr, int wave, in
 
 template <typename In, typename Out, int VW, int NV, bool PACKED, int MODE>
 __global__ __launch_bounds__(1024) void medium_row_kernel(
-    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
+    const typename In::storage* x, typename Out::storage* y,
     int64_t rows, int cols, int wpr, Fused fz) {
   constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   static_assert(!(PACKED && FUSED), "the fused variants keep the row in fp32");

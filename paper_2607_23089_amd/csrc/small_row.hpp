@@ -25,7 +25,7 @@ namespace rowsm {
 
 template <typename In, typename Out, int VW, int LPR, int RPL, int MODE>
 __global__ __launch_bounds__(256) void small_row_kernel(
-    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y,
+    const typename In::storage* x, typename Out::storage* y,
     int64_t rows, int cols, Fused fz) {
   constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   constexpr int RPW = kWave / LPR;     // rows per wave per load instruction

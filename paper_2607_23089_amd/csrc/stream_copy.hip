@@ -21,7 +21,7 @@ constexpr int kCopyBlock = 256;
 // vector is copied element by element.
 template <typename In, typename Out, int VW>
 __global__ __launch_bounds__(kCopyBlock) void stream_copy_kernel(
-    const typename In::storage* __restrict__ x, typename Out::storage* __restrict__ y, int64_t n,
+    const typename In::storage* x, typename Out::storage* y, int64_t n,
     int64_t nblocks) {
   constexpr int64_t CH = (int64_t)kCopyBlock * VW;
   const int i0 = threadIdx.x * VW;
