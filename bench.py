@@ -26,8 +26,18 @@ Before the timed steps the same protocol times the library's streaming copy
 plain copy moving the same bytes in the same run, reported per launch as
 ``ratio_to_copy`` (kernel rate / copy rate).
 
+Parity gate: before anything is timed, one untimed step runs and its outputs
+are checked against the fp64 oracle on sampled rows of every regime (first and
+last rows and evenly spaced ones); a failure prints a line with no value and
+exits non-zero.  After timing, the CPU baseline checks every 16th row of the
+timed steps' outputs on the way, with the same consequence on failure.
+
 Prints ONE JSON line (rank 0).  ``--gpus`` above 1 is refused: this path runs
 on one GPU (rows shard across GPUs without communication).
+
+``--summarize-trace``, ``--summarize-counters`` and ``--summarize-launcher``
+need no GPU: they write the summaries under profiles/ from the CSV output of
+rocprofv3 runs of this script (bench_profiles.py).
 
 ``--launcher-check`` runs no step: it times the launcher's choice for full
 launches of representative row lengths against the library's other launch
@@ -53,6 +63,9 @@ PEAK_HBM_GBS = 8000.0  # MI355X published HBM3E bandwidth
 TARGET_FRAC = {"small_262144x64": 0.60, "causal_32768x4096": 0.80,
                "large_1024x262144": 0.80, "vocab_4096x151936": 0.80}
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+# hipDeviceAttribute_t values of the HIP runtime headers (hip_runtime_api.h).
+HIP_ATTR_MEMORY_BUS_WIDTH = 59
+HIP_ATTR_MEMORY_CLOCK_RATE = 60
 # Device code each kernel family is compiled from; a profile entry records the
 # hash of its family's sources and the launch's shape.
 KERNEL_SOURCES = {
@@ -198,6 +211,58 @@ def cpu_baseline(inputs, outputs, regimes, min_seconds: float, threads: int = 0)
         "cpu_model": cpu_model(),
         "parity_on_sample": parity,
     }
+
+
+def gate_rows(rows: int, n: int = 24):
+    """Rows the parity gate checks: the first and last four and n evenly spaced
+    ones in between (row 0 and every 4096th row are the causal workload's
+    one-hot rows)."""
+    picks = set(range(min(4, rows))) | set(range(max(0, rows - 4), rows))
+    picks |= {(i * (rows - 1)) // max(1, n - 1) for i in range(n)}
+    return sorted(picks)
+
+
+def parity_gate(inputs, outputs, regimes, threads: int = 0):
+    """Parity of the launches the bench times, checked before any timing: the
+    outputs of one untimed step against the fp64 oracle on sampled rows of
+    every regime (compare(): NaN and zero patterns exact, 2e-6 absolute for
+    fp32 output, one bf16 ulp of the oracle value for bf16 output)."""
+    import torch
+
+    import oracle
+    from oracle.compare import compare, widen_output
+    from paper_2607_23089_amd import workloads as W
+
+    threads = threads or len(os.sched_getaffinity(0))
+    oracle.load()
+    out = {}
+    for name in regimes:
+        w = W.WORKLOADS[name]
+        rows = gate_rows(w.rows)
+        ti = torch.tensor(rows, dtype=torch.int64, device=inputs[name].device)
+        xs = W.to_bits_numpy(inputs[name].index_select(0, ti))
+        v = oracle.widen_bf16_bits(xs) if w.in_dtype == "bf16" else oracle.widen_f32(xs)
+        ref = oracle.softmax_f64(v, threads=threads)
+        got = widen_output(W.to_bits_numpy(outputs[name].index_select(0, ti)), w.out_dtype)
+        res = compare(got, ref, w.out_dtype)
+        out[name] = {"rows_checked": len(rows), "parity_ok": bool(res["ok"]),
+                     "max_abs": res["max_abs"], "max_tol_ratio": res["max_tol_ratio"]}
+    return out
+
+
+def device_memory_info(device_index: int = 0):
+    """The device-reported HBM figures (hipDeviceGetAttribute): memory clock
+    in kHz and bus width in bits."""
+    import ctypes
+    h = ctypes.CDLL("libamdhip64.so")
+    h.hipDeviceGetAttribute.argtypes = [ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.c_int]
+    vals = {}
+    for key, attr in (("memory_clock_khz", HIP_ATTR_MEMORY_CLOCK_RATE),
+                      ("bus_width_bits", HIP_ATTR_MEMORY_BUS_WIDTH)):
+        v = ctypes.c_int(0)
+        st = h.hipDeviceGetAttribute(ctypes.byref(v), attr, device_index)
+        vals[key] = v.value if st == 0 else None
+    return vals
 
 
 class HipEvent:
@@ -469,10 +534,11 @@ def fused_causal_leg(reps: int):
         x.data_ptr(), wide.data_ptr(), kept, R.BF16, R.F32, sh)))
     copy_gbs = kept * 6 / (copy_us * 1e-6) / 1e9
     del wide
-    st, desc = R.rowsm_describe(w.rows, w.cols, R.BF16, R.BF16)
+    _, desc = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, w.rows, w.cols, R.BF16, R.BF16)
     return {
         "workload": "causal_32768x4096 scores without stored mask, scale 0.125, "
                     "mask (r, c) = -inf for c > r mod 4096 computed in the kernel",
+        "launch": desc, "copy_elements": kept,
         "algorithmic_bytes": alg, "kept_fraction": kept / (w.rows * w.cols),
         "avg_us": fused_us, "GBps": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS,
         "stored_mask_same_protocol_us": plain_us, "speedup_vs_stored_mask": plain_us / fused_us,
@@ -566,6 +632,36 @@ def launcher_check(reps: int = 8):
     return {"launcher_check": out, "reps_per_shape": reps + 2}
 
 
+# The calibration copy of the traffic counters: torch's device copy of 1 GiB
+# (the runtime's copyBuffer kernel), run under rocprofv3 --pmc FETCH_SIZE and
+# --pmc WRITE_SIZE.
+CALIBRATION_BYTES = 1 << 30
+CALIBRATION_COPY = ("import torch; a=torch.ones(1<<28, device='cuda'); b=torch.empty_like(a); "
+                    "torch.cuda.synchronize(); [b.copy_(a) for _ in range(3)]; "
+                    "torch.cuda.synchronize()")
+
+
+def summarize(args) -> int:
+    """Write profiles/ summaries from rocprofv3 CSV output (no GPU)."""
+    import bench_profiles as P
+    if args.summarize_trace:
+        log, d, out = args.summarize_trace
+        text = P.summarize_trace(log, d, args.command, PEAK_HBM_GBS)
+    elif args.summarize_launcher:
+        log, d, out = args.summarize_launcher
+        text = P.summarize_launcher(log, d, args.command, PEAK_HBM_GBS)
+    else:
+        log, fd, wd, cfd, cwd, out, out_json = args.summarize_counters
+        text, table = P.summarize_counters(log, fd, wd, cfd, cwd, CALIBRATION_BYTES,
+                                           args.command, kernel_source_hash, kernel_family)
+        with open(out_json, "w") as f:
+            json.dump(table, f, indent=1)
+            f.write("\n")
+    with open(out, "w") as f:
+        f.write(text)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__,
                                  formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -585,7 +681,25 @@ def main() -> int:
                     help="instead of the step: time the launcher's choice for launches "
                          "of representative row lengths against the library's other launch "
                          "shapes, and print that as the JSON line")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("BENCH_LOG", "TRACE_DIR", "OUT_MD"),
+                    help="no GPU: write the kernel-trace summary of a rocprofv3 --kernel-trace "
+                         "run of bench.py (its printed JSON line in BENCH_LOG)")
+    ap.add_argument("--summarize-launcher", nargs=3,
+                    metavar=("BENCH_LOG", "TRACE_DIR", "OUT_MD"),
+                    help="no GPU: the same for a rocprofv3 run of bench.py --launcher-check")
+    ap.add_argument("--summarize-counters", nargs=7,
+                    metavar=("BENCH_LOG", "FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR",
+                             "CAL_WRITE_DIR", "OUT_MD", "OUT_JSON"),
+                    help="no GPU: the HBM traffic summary and table from rocprofv3 --pmc "
+                         "FETCH_SIZE and WRITE_SIZE runs of bench.py and of the calibration "
+                         "copy (CALIBRATION_COPY)")
+    ap.add_argument("--command", default="",
+                    help="with --summarize-*: the command(s) that produced the rocprofv3 "
+                         "output, written into the summary")
     args = ap.parse_args()
+
+    if args.summarize_trace or args.summarize_launcher or args.summarize_counters:
+        return summarize(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this row-softmax path runs on one GPU; rows shard across "
@@ -639,6 +753,22 @@ def main() -> int:
                 raise R.RowsmError(f"copy {name}: status {st} {R.rowsm_status_string(st)}")
             if events is not None:
                 events[i][1].record(stream)
+
+    # Parity gate: one untimed step, its outputs checked against the oracle on
+    # sampled rows of every regime before anything is timed.  A failure ends
+    # the run with no value.
+    step()
+    torch.cuda.synchronize()
+    gate = parity_gate(inputs, outputs, regimes, args.cpu_threads)
+    gate_ok = all(g["parity_ok"] for g in gate.values())
+    if R.rowsm_split_wait_failures() != 0:
+        gate_ok = False
+    if not gate_ok:
+        print("bench.py: parity gate failed, nothing timed: " + json.dumps(gate),
+              file=sys.stderr)
+        print(json.dumps({"metric": METRIC, "value": None, "unit": "GB/s", "n_gpus": 1,
+                          "parity_gate": gate}), flush=True)
+        return 1
 
     for _ in range(args.warmup):
         step()
@@ -706,6 +836,14 @@ def main() -> int:
     failures = R.rowsm_split_wait_failures()
     if failures != 0:
         raise R.RowsmError(f"{failures} split-row exchange waits gave up: results invalid")
+    mem = device_memory_info(torch.cuda.current_device())
+    hbm_info = dict(mem, spec_peak_GBps=PEAK_HBM_GBS)
+    if mem.get("memory_clock_khz") and mem.get("bus_width_bits"):
+        # bytes per second the reported clock and width give at one transfer
+        # per pin per clock; the per-pin data rate the spec peak implies
+        one = mem["memory_clock_khz"] * 1e3 * mem["bus_width_bits"] / 8 / 1e9
+        hbm_info["GBps_at_one_transfer_per_clock"] = one
+        hbm_info["transfers_per_clock_at_spec_peak"] = PEAK_HBM_GBS / one
     dom = max(per, key=lambda n: per[n]["avg_us"])
     d = per[dom]
     value = step_bytes / (wall / args.steps) / 1e9
@@ -756,6 +894,11 @@ def main() -> int:
             "ms_per_step": copy_wall / args.steps * 1e3,
         },
         "regimes_detail": per,
+        "parity_gate": {"parity_ok": gate_ok,
+                        "max_tol_ratio": max(g["max_tol_ratio"] for g in gate.values()),
+                        "when": "before timing, on the outputs of one untimed step",
+                        "regimes": gate},
+        "device_hbm": hbm_info,
     }
     # The same step captured into a HIP graph and replayed (the single-read
     # form keeps its one-read plan under capture).
@@ -796,8 +939,16 @@ def main() -> int:
                                "softmax_backward": backward_leg(reps=10),
                                "moe_group_top2": moe_leg(reps=10)}
     if args.cpu_budget > 0:
-        result["cpu_baseline"] = cpu_baseline(inputs, outputs, regimes, args.cpu_budget,
-                                              args.cpu_threads)
+        cb = cpu_baseline(inputs, outputs, regimes, args.cpu_budget, args.cpu_threads)
+        cb["parity_ok"] = all(p["parity_ok"] for p in cb["parity_on_sample"].values())
+        cb["max_tol_ratio"] = max(p["max_tol_ratio"] for p in cb["parity_on_sample"].values())
+        result["cpu_baseline"] = cb
+        if not cb["parity_ok"]:
+            print("bench.py: the timed steps' outputs fail parity on the CPU baseline's "
+                  "rows: " + json.dumps(cb["parity_on_sample"]), file=sys.stderr)
+            result["value"] = None
+            print(json.dumps(result), flush=True)
+            return 1
     print(json.dumps(result), flush=True)
     return 0
 
