@@ -329,7 +329,7 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
 // blocks per row with the same layout (global thread g = c * T + t reads the
 // vector pairs g + j * S * T, U per tile).  Pass 1 accumulates d over tiles
 // (a tile's partial on its own, then added to the running sum with a Kahan
-// compensation term: up to 2^16 tile partials per thread on the longest
+// compensation term: up to 1024 tile partials per thread on the longest
 // rows); with S > 1 the blocks exchange their partial d once (as
 // bwd_split_kernel, up to 4 peers per lane of wave 0, a peer whose wait gives
 // up recomputed with bwd_large_pass1()) and sum them in block order.  Pass 2

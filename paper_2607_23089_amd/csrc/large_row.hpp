@@ -5,14 +5,18 @@
 // A row is read by S >= 1 blocks of T threads that act as one group of
 // S * T threads: global thread g = c * T + t of block c reads the vectors
 // g + j * S * T of the row, U of them per tile (each load instruction of a
-// wave reads 64 consecutive vectors).  Pass 1 keeps a running (max, sum) per
-// thread: for each tile it takes the tile maximum M' = max(m, tile max),
-// rescales the running sum by exp(m - M') and adds exp(x - M') for the tile's
-// entries.  The running sum carries a compensation term (Kahan summation): a
-// thread adds one tile sum per tile, up to 2^16 of them on the longest rows,
-// and near-equal addends would otherwise round the same way at every step, an
-// error that grows with their count.  The per-thread pairs are merged across
-// the wave with DPP/permlane steps and across waves through LDS.  With S > 1
+// wave reads 64 consecutive vectors).  Pass 1 keeps a running (reference,
+// sum) per thread: for each tile it takes the tile maximum; when that exceeds
+// the reference m by more than kRefSlack the reference moves to it (M') and
+// the running sum is rescaled by exp(m - M'); then it adds exp(x - m) for the
+// tile's entries.  The running sum carries a compensation term (Kahan
+// summation): a thread adds one tile sum per tile (1024 of them on the
+// longest rows the launcher plans, 2^23 with the narrowest forced shape), and
+// near-equal addends would otherwise round the same way at every step, an
+// error that grows with their count.  Together the two keep the rounding
+// error of the sum independent of the row length.  The per-thread pairs are
+// merged across the wave with DPP/permlane steps and across waves through
+// LDS (maximum first, then one rescale per partial sum).  With S > 1
 // the blocks of a row then exchange their pairs once, through the split
 // form's tagged words and workspace (split_row.hpp: protocol, tags, the
 // bounded wait), and merge them in block order; a block whose wait for a peer
@@ -43,6 +47,10 @@
 
 namespace rowsm {
 
+// How far (natural-log units) a tile maximum may exceed the exponent
+// reference of pass 1 before the reference moves to it.
+constexpr float kRefSlack = 8.0f;
+
 // Pass 1 of the block whose global threads are g = c * T + t: the block's
 // (max, sum) pair over its share of the row, merged across the wave and then
 // across waves in wave order through red_m / red_s (one barrier).  Called by
@@ -54,8 +62,9 @@ __device__ __forceinline__ MaxSum large_pass1(rsrc_t rx, int g, int RT, int nvec
   constexpr bool FUSED = MODE == kFused, LOG = MODE == kLog;
   const float ninf = -__builtin_inff();
   const uint32_t vin = (uint32_t)g * (VW * In::bytes);
-  // Running (max, sum); cs is the compensation of s (the sum is s - cs).
-  float m = ninf, s = 0.0f, cs = 0.0f;
+  // Running exponent reference m and sum s relative to it; cs is the
+  // compensation of s (the sum is s - cs); mx is the running maximum.
+  float m = ninf, s = 0.0f, cs = 0.0f, mx = ninf;
   for (int tt = 0; tt < ntiles; ++tt) {
     float f[U][VW];
     {
@@ -80,7 +89,15 @@ __device__ __forceinline__ MaxSum large_pass1(rsrc_t rx, int g, int RT, int nvec
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int i = 0; i < VW; ++i) tm = fmax_nn(tm, f[u][i]);
-    const float M = fmax_nn(m, tm);
+    // The exponent reference m follows the running maximum lazily: it moves
+    // only to a tile maximum that exceeds it by more than kRefSlack.  Every
+    // term exp(x - m) then stays below e^kRefSlack, and every move scales the
+    // sum gathered so far by less than e^-kRefSlack, so the rounding of the
+    // rescale factors does not build up with the number of tiles (a reference
+    // that followed each rise of the maximum would rescale once per tile on
+    // an ascending row).
+    const float M = (tm > m + kRefSlack) ? tm : m;
+    mx = fmax_nn(mx, tm);
     const float nml = (M == ninf) ? 0.0f : -M * kLog2e;
     // The tile is summed on its own and then added to the running sum, so a
     // thread's serial chain of additions is one tile plus one per tile.
@@ -107,15 +124,21 @@ __device__ __forceinline__ MaxSum large_pass1(rsrc_t rx, int g, int RT, int nvec
     m = M;
   }
 
-  MaxSum ms = group_merge<kWave>({m, s - cs});
+  // The thread's pair relative to its maximum (one more rescale), so that
+  // every later step sees sums of terms <= 1, as the other forms do.
+  MaxSum ms = group_merge<kWave>({mx, rescale(s - cs, m, mx)});
   if (lane == 0) {
     red_m[wave] = ms.m;
     red_s[wave] = ms.s;
   }
   __syncthreads();
-  ms = {red_m[0], red_s[0]};
-  for (int i = 1; i < nwaves; ++i) ms = merge(ms, {red_m[i], red_s[i]});
-  return ms;
+  // Across waves: the maximum first, then each wave's sum rescaled once to it
+  // and added in wave order.
+  float M = red_m[0];
+  for (int i = 1; i < nwaves; ++i) M = fmax_nn(M, red_m[i]);
+  float s_all = rescale(red_s[0], red_m[0], M);
+  for (int i = 1; i < nwaves; ++i) s_all += rescale(red_s[i], red_m[i], M);
+  return {M, s_all};
 }
 
 template <typename In, typename Out, int VW, int U, int MODE>
@@ -164,10 +187,15 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
       // wave 0 parks its pairs in LDS (peer[l + 64 j]) and the block
       // recomputes the missing ones.
       auto finish = [&](const MaxSum (&pr)[kPeersPerLane]) {
+        // The lane's peers: their maximum, then each sum rescaled once to it
+        // and added in block order; then across the lanes.
         MaxSum p = {-__builtin_inff(), 0.0f};
 #pragma unroll
         for (int j = 0; j < kPeersPerLane; ++j)
-          if (lane + j * kWave < S) p = merge(p, pr[j]);
+          if (lane + j * kWave < S) p.m = fmax_nn(p.m, pr[j].m);
+#pragma unroll
+        for (int j = 0; j < kPeersPerLane; ++j)
+          if (lane + j * kWave < S) p.s += rescale(pr[j].s, pr[j].m, p.m);
         p = group_merge<kWave>(p);  // fixed lane order: deterministic
         if (lane == 0) {
           bcast[0] = p.m;

@@ -3,7 +3,7 @@ the same definition, for every family and form and every dtype pair; special
 values, in place, misaligned rows; and the full-size long-row workloads
 (sampled rows element by element, every row through properties that hold at
 any size).  Tolerance (oracle/compare.py, compare_log): fp32 output within
-1e-5 + 2^-22 |v|, bf16 output one bf16 ulp more; NaN and -inf positions
+2e-5 + 2^-22 |v|, bf16 output one bf16 ulp more; NaN and -inf positions
 identical.
 """
 import numpy as np
@@ -157,7 +157,7 @@ def test_log_workload_full_size(name):
             k = at_max.sum(dim=1, keepdim=True).double()
             want = (-torch.log(k)).expand(-1, w.cols)
             got = y[r0:r0 + 512].double()
-            assert float((got - want)[at_max].abs().max()) <= 1e-5 + 2.0 ** -22 * 8
+            assert float((got - want)[at_max].abs().max()) <= 2e-5 + 2.0 ** -22 * 8
     del x, y
     torch.cuda.empty_cache()
 
