@@ -37,7 +37,8 @@ OP_SOFTMAX, OP_SCALED_CAUSAL, OP_LOG_SOFTMAX, OP_SOFTMAX_BACKWARD = 0, 1, 2, 3
 OP_MOE_GROUP_TOP2 = 4
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "librowsm.so")
+# ROWSM_LIB names another build of the library (the host-logic check build).
+LIB_PATH = os.environ.get("ROWSM_LIB") or os.path.join(_PKG, "librowsm.so")
 
 # Symbols declared in include/rowsm.h.
 EXPORTS = ("rowsm_forward", "rowsm_forward_noalloc", "rowsm_select", "rowsm_forward_variant",

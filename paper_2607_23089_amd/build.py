@@ -59,5 +59,38 @@ def build_library(verbose: bool = False, jobs: int | None = None) -> str:
     return LIB
 
 
+# Translation units of the host-logic check build: the planner, the argument
+# checks and C ABI, the exchange ring and the streaming copy.
+HOST_CHECK_SOURCES = ["plan.hip", "rowsm.hip", "launch_split_common.hip", "stream_copy.hip"]
+# Host-side sanitizers only; device code is built as usual.
+HOST_SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer",
+                 "-g"]
+
+
+def build_host_check(out: str, stubs: str, jobs: int | None = None) -> str:
+    """Build the host-logic check library at ``out``: HOST_CHECK_SOURCES plus
+    ``stubs`` (launchers that launch nothing) with the host compiler's address
+    and undefined-behaviour sanitizers.  Load it with the sanitizer runtime
+    preloaded (sanitizer_runtime())."""
+    srcs = [os.path.join(CSRC, f) for f in HOST_CHECK_SOURCES] + [stubs]
+    flags = [f for f in HIP_FLAGS if f != "-O3"] + ["-O1"] + HOST_SANITIZE
+    with tempfile.TemporaryDirectory(prefix="rowsm_check_") as tmp:
+        objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]
+        cmds = [["hipcc"] + flags + ["-c", s, "-o", o] for s, o in zip(srcs, objs)]
+        with ThreadPoolExecutor(max_workers=jobs or min(4, os.cpu_count() or 1)) as pool:
+            list(pool.map(_run, cmds))
+        _run(["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-shared-libasan", "-o", out]
+             + HOST_SANITIZE + objs)
+    return out
+
+
+def sanitizer_runtime() -> str:
+    """Path of the compiler's shared address-sanitizer runtime."""
+    res = subprocess.run(["hipcc", "-print-file-name=libclang_rt.asan-x86_64.so"],
+                         capture_output=True, text=True, check=True)
+    return res.stdout.strip()
+
+
 if __name__ == "__main__":
     print(build_library(verbose=True))
