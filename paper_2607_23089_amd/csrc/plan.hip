@@ -329,23 +329,25 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       p->rpl = r;
     }
     if (small_block(cfg, &p->block) != ROWSM_OK) return ROWSM_EINVAL;
-    // Rows that fill their lanes exactly, in launches of 40-160 MiB
-    // (softmax and log forms, nothing about the shape forced): one-wave
-    // blocks with one row group per lane.  Sweeps of 16-128-column rows
-    // (launches timed alone after a cache-evicting write) measured them
-    // 2-6% faster there at every such length, fitted and held out; 5-10%
-    // slower below 32 MiB, level from 192 MiB, and 2-20% slower for rows
-    // that leave lanes idle (48 or 96 bf16 columns, 100-column widening
-    // rows), which keep the 256-thread blocks.
-    // (row bytes are at most 32 vectors of 16 + 16 bytes here, so rows below
-    // the bound keep the product far from overflow)
+    // Rows that fill their lanes exactly, in launches of at least 40 MiB
+    // (softmax and log forms, nothing about the shape forced): for a dtype
+    // pair of one width, one-wave blocks with one row group per lane; for a
+    // widening or narrowing pair, 128-thread blocks with two row groups per
+    // lane.  Sweeps of 16-128-column rows at 24 MiB-2 GiB, each launch alone
+    // after a cache-evicting write, on two devices: one-wave blocks were the
+    // fastest or within 1% of it at every same-width size from 40 MiB, 3-5%
+    // faster than 256-thread blocks of 4 row groups from 256 MiB on; on
+    // bf16 <-> fp32 rows they were 5-19% slower than two row groups per lane,
+    // which were 2-17% faster than the 256-thread blocks from 40 MiB on.
+    // Below 40 MiB, and for rows that leave lanes idle (48 or 96 bf16
+    // columns), the 256-thread blocks stay.  (No product of rows and row
+    // bytes is formed: rows may be close to 2^62.)
     const int64_t row_bytes = cols * (ib + ob);
-    const bool mid_launch = rows <= ((int64_t)160 << 20) / row_bytes &&
-                            rows * row_bytes >= ((int64_t)40 << 20);
-    if (auto_variant && !fused && nvec == p->lpr && mid_launch &&
+    const bool big_launch = rows >= cdiv((int64_t)40 << 20, row_bytes);
+    if (auto_variant && !fused && nvec == p->lpr && big_launch &&
         (!cfg || (cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->block == 0))) {
-      p->block = kWave;
-      p->rpl = 1;
+      p->block = ib == ob ? kWave : 2 * kWave;
+      p->rpl = ib == ob ? 1 : 2;
     }
     const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
     p->grid = cdiv(rows, rows_per_block);

@@ -226,19 +226,39 @@ def test_select_regimes(lib):
 def test_describe(lib):
     st, text = R.rowsm_describe(262144, 64, R.BF16, R.BF16)
     assert st == R.OK and text.startswith("small") and "lpr=8" in text and "vw=8" in text
-    # rows that fill their lanes in launches of 40-160 MiB: one-wave blocks,
-    # one row group per lane; otherwise 256-thread blocks, 4 row groups
+    # rows that fill their lanes in launches of at least 40 MiB: one-wave
+    # blocks with one row group per lane for a dtype pair of one width,
+    # 128-thread blocks with two for a widening or narrowing pair; otherwise
+    # 256-thread blocks, 4 row groups
     assert "block=64 " in text and "rpl=1 " in text and "grid=32768 " in text
-    for rows, cols, dt in [(131072, 64, R.BF16), (1048576, 64, R.BF16), (262144, 48, R.BF16)]:
+    for rows, cols, dt in [(1048576, 64, R.BF16), (163840, 64, R.BF16), (8388608, 16, R.F32)]:
         t = R.rowsm_describe(rows, cols, dt, dt)[1]
+        assert "block=64 " in t and "rpl=1 " in t, t
+    for rows, cols, di, do in [(262144, 64, R.BF16, R.F32), (109227, 64, R.F32, R.BF16),
+                               (2796202, 16, R.BF16, R.F32)]:
+        t = R.rowsm_describe(rows, cols, di, do)[1]
+        assert "block=128 " in t and "rpl=2 " in t, t
+    for rows, cols, di, do in [(131072, 64, R.BF16, R.BF16),     # 32 MiB
+                               (163839, 64, R.BF16, R.BF16),     # one row under 40 MiB
+                               (65536, 64, R.BF16, R.F32),       # 24 MiB
+                               (262144, 48, R.BF16, R.BF16)]:    # lanes left idle
+        t = R.rowsm_describe(rows, cols, di, do)[1]
         assert "block=256 " in t and "rpl=4 " in t, t
     t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 262144, 64, R.BF16, R.BF16)[1]
     assert "block=256 " in t and "rpl=4 " in t, t                  # fused: 4 row groups
     t = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 393216, 16, R.F32, R.F32)[1]
     assert "block=64 " in t and "rpl=1 " in t, t
-    # launch sizes whose byte count would not fit 64 bits take the default
-    t = R.rowsm_describe((1 << 61) + 1, 1, R.F32, R.F32)[1]
+    t = R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 262144, 64, R.BF16, R.F32)[1]
+    assert "block=128 " in t and "rpl=2 " in t, t
+    # with the family or a lane grouping forced, the default grouping stays
+    t = R.rowsm_describe(1048576, 64, R.BF16, R.BF16, R.SMALL)[1]
     assert "block=256 " in t and "rpl=4 " in t, t
+    t = R.rowsm_describe_op(R.OP_SOFTMAX, 1048576, 64, R.BF16, R.BF16,
+                            R.RowsmConfig(rows_per_lane=4))[1]
+    assert "block=256 " in t and "rpl=4 " in t, t
+    # the largest row counts: no product of rows and row bytes is formed
+    t = R.rowsm_describe((1 << 61) + 1, 1, R.F32, R.F32)[1]
+    assert "block=64 " in t and "rpl=1 " in t, t
     # the backward: one-wave blocks from 96 MiB of its three streams on (no
     # upper bound), for rows that fill their lanes and nothing forced
     bt = lambda rows, cols, dt, cfg=None: R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols,
@@ -272,8 +292,9 @@ def test_describe(lib):
     assert st == R.OK and "split=8" in text and "one residency" in text
     # small and medium grids: one task per wave / one row group per block at
     # any row count; blocks_per_cu caps them (the waves then stride)
-    # (the backward's 4M rows take one-wave blocks of one row group per lane)
-    for op, grid in ((R.OP_SOFTMAX, 32768), (R.OP_SOFTMAX_BACKWARD, 524288)):
+    # (4M rows of 64 bf16 columns take one-wave blocks of one row group per
+    # lane, forward and backward)
+    for op, grid in ((R.OP_SOFTMAX, 524288), (R.OP_SOFTMAX_BACKWARD, 524288)):
         st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16)
         assert st == R.OK and text.startswith("small") and f"grid={grid} " in text, text
         st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16,

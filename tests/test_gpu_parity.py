@@ -540,3 +540,31 @@ def test_split_launches_from_host_threads():
     assert not errors, errors
     for i, x in enumerate(xs):
         assert_parity(x.cpu(), refs[i], "f32", f"threaded shape {i}")
+
+
+@pytest.mark.parametrize("rows,cols,din,dout,want", [
+    (262144, 64, "bf16", "bf16", ("block=64 ", "rpl=1 ")),      # 64 MiB, one width
+    (1048576, 64, "bf16", "bf16", ("block=64 ", "rpl=1 ")),     # 256 MiB
+    (2097152, 16, "f32", "f32", ("block=64 ", "rpl=1 ")),       # 256 MiB
+    (262144, 64, "bf16", "f32", ("block=128 ", "rpl=2 ")),      # 96 MiB, widening
+    (109227, 64, "f32", "bf16", ("block=128 ", "rpl=2 ")),      # 40 MiB, narrowing
+    (1398101, 32, "bf16", "f32", ("block=128 ", "rpl=2 ")),     # 256 MiB
+    (65536, 64, "bf16", "f32", ("block=256 ", "rpl=4 ")),       # 24 MiB: default
+])
+def test_small_row_launch_picks(rows, cols, din, dout, want):
+    # the launcher's small-row block and row-group picks by launch size and
+    # dtype pair: sampled rows element by element, every row sums to one
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("small") and all(w in desc for w in want), desc
+    print(f"small pick {rows}x{cols} {din}->{dout}: {desc}", flush=True)
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + cols, device=DEV)
+    y = run(x, dout)
+    sample = sorted({0, 1, 2, 3, 5, 7, rows // 3, rows // 2, rows - 3, rows - 2, rows - 1}
+                    | set(range(0, rows, max(1, rows // 61))))
+    idx = torch.tensor(sample, device=DEV)
+    assert_parity(x.index_select(0, idx).cpu(), y.index_select(0, idx).cpu(), dout,
+                  f"{rows}x{cols} {din}->{dout} [{desc}]")
+    sums = y.double().sum(dim=1)
+    tol = 1e-5 if dout == "f32" else 2.0 ** -8 * 2 + 1e-5
+    assert float((sums - 1.0).abs().max()) <= tol
+    del x, y
