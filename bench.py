@@ -566,6 +566,82 @@ LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype)
 ]
 
 
+SWEEP_ROWS = (16384, 32768, 65536, 131072, 262144, 524288, 1048576, 2097152, 4194304)
+
+
+def size_sweep(reps: int = 10):
+    """The small-row workload's kernel at 4 MiB to 1 GiB (64 bf16 columns, the
+    launcher's choice at each row count), next to the library's streaming copy
+    of the same bytes; every launch alone after a 1 GiB cache-evicting write,
+    2 untimed and reps timed launches each, kernel before copy, sizes in
+    order.  A kernel trace of this run gives duration against bytes: the
+    fixed cost of a launch and the rate it approaches."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    out = []
+    for rows in SWEEP_ROWS:
+        x = W.random_matrix(rows, 64, "bf16", sigma=4.0, seed=1, device=dev)
+        y = torch.empty_like(x)
+        kern = timed_alone(lambda: R.check(R.rowsm_forward(
+            x.data_ptr(), y.data_ptr(), rows, 64, R.BF16, R.BF16, sh)), reps, flush, stream)
+        copy = timed_alone(lambda: R.check(R.rowsm_stream_copy(
+            x.data_ptr(), y.data_ptr(), rows * 64, R.BF16, R.BF16, sh)), reps, flush, stream)
+        out.append({"rows": rows, "cols": 64, "bytes": rows * 64 * 4,
+                    "launch": R.rowsm_describe(rows, 64, R.BF16, R.BF16)[1],
+                    "avg_us": kern, "copy_us": copy})
+        del x, y
+    return {"size_sweep": out, "launches_per_size": reps + 2}
+
+
+def stream_overlap(pairs: int = 4):
+    """Two exchanging launches of long rows on two streams that are never
+    ordered against each other, issued in pairs (A on one stream, B on the
+    other).  Each launch is capped at one block per compute unit (its groups
+    loop over the rows), so it occupies part of every compute unit for a
+    millisecond or more and the two streams' launches can run at the same
+    time.  Every output is compared with the same launch made alone
+    beforehand (bitwise).  A kernel trace of this run shows how much the two
+    streams' dispatches overlap in time."""
+    import torch
+
+    import paper_2607_23089_amd as R
+    from paper_2607_23089_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    cfg = R.RowsmConfig(blocks_per_cu=1)
+    xa = W.random_matrix(256, 262144, "f32", sigma=2.0, seed=1, device=dev)
+    xb = W.random_matrix(512, 151936, "bf16", sigma=3.0, seed=2, device=dev)
+    ya_ref = R.softmax(xa, config=cfg)
+    yb_ref = R.softmax(xb, out_dtype=torch.float32, config=cfg)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    ya = [torch.empty_like(ya_ref) for _ in range(pairs)]
+    yb = [torch.empty_like(yb_ref) for _ in range(pairs)]
+    # one launch on each stream first, so that neither stream's first use
+    # falls inside the pairs
+    R.softmax(xa, out=ya[0], config=cfg, stream=s1)
+    R.softmax(xb, out=yb[0], config=cfg, stream=s2)
+    torch.cuda.synchronize()
+    for i in range(pairs):
+        R.softmax(xa, out=ya[i], config=cfg, stream=s1)
+        R.softmax(xb, out=yb[i], config=cfg, stream=s2)
+    torch.cuda.synchronize()
+    same = all(torch.equal(a, ya_ref) for a in ya) and all(torch.equal(b, yb_ref) for b in yb)
+    if not same or R.rowsm_split_wait_failures() != 0:
+        raise R.RowsmError("two-stream launches differ from the same launches made alone")
+    return {"stream_overlap": {
+        "launch_a": R.rowsm_describe_op(R.OP_SOFTMAX, 256, 262144, R.F32, R.F32, cfg)[1],
+        "launch_b": R.rowsm_describe_op(R.OP_SOFTMAX, 512, 151936, R.BF16, R.F32, cfg)[1],
+        "rows_a": 256, "rows_b": 512, "pairs": pairs, "warm_up_launches": 2,
+        "outputs_equal_to_launches_alone": same}}
+
+
 def launcher_check(reps: int = 8):
     """The launcher's choice for launches of the shapes above against the
     other launch shapes of the library (medium wave groups with the default
@@ -650,6 +726,15 @@ def summarize(args) -> int:
     elif args.summarize_launcher:
         log, d, out = args.summarize_launcher
         text = P.summarize_launcher(log, d, args.command, PEAK_HBM_GBS)
+    elif args.summarize_sweep:
+        log, d, out = args.summarize_sweep
+        text = P.summarize_sweep(log, d, args.command, PEAK_HBM_GBS)
+    elif args.summarize_overlap:
+        log, d, out = args.summarize_overlap
+        text = P.summarize_overlap(log, d, args.command)
+    elif args.summarize_pmc:
+        log, d, out = args.summarize_pmc
+        text = P.summarize_pmc(log, d, args.command)
     else:
         log, fd, wd, cfd, cwd, out, out_json = args.summarize_counters
         text, table = P.summarize_counters(log, fd, wd, cfd, cwd, CALIBRATION_BYTES,
@@ -681,6 +766,24 @@ def main() -> int:
                     help="instead of the step: time the launcher's choice for launches "
                          "of representative row lengths against the library's other launch "
                          "shapes, and print that as the JSON line")
+    ap.add_argument("--size-sweep", action="store_true",
+                    help="instead of the step: the small-row kernel and the plain copy at "
+                         "4 MiB to 1 GiB, each launch alone (for a kernel trace)")
+    ap.add_argument("--stream-overlap", action="store_true",
+                    help="instead of the step: exchanging launches of few long rows on two "
+                         "unordered streams, in pairs (for a kernel trace)")
+    ap.add_argument("--summarize-overlap", nargs=3, metavar=("BENCH_LOG", "TRACE_DIR", "OUT_MD"),
+                    help="no GPU: the overlap in time of the two streams' dispatches, from a "
+                         "rocprofv3 --kernel-trace run of bench.py --stream-overlap")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="only run the calibration copy of the traffic counters "
+                         "(CALIBRATION_COPY) and exit")
+    ap.add_argument("--summarize-sweep", nargs=3, metavar=("BENCH_LOG", "TRACE_DIR", "OUT_MD"),
+                    help="no GPU: the size-sweep summary from a rocprofv3 --kernel-trace run "
+                         "of bench.py --size-sweep")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("BENCH_LOG", "PMC_DIR", "OUT_MD"),
+                    help="no GPU: per-launch averages of every counter of a rocprofv3 --pmc "
+                         "run of bench.py")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("BENCH_LOG", "TRACE_DIR", "OUT_MD"),
                     help="no GPU: write the kernel-trace summary of a rocprofv3 --kernel-trace "
                          "run of bench.py (its printed JSON line in BENCH_LOG)")
@@ -698,8 +801,12 @@ def main() -> int:
                          "output, written into the summary")
     args = ap.parse_args()
 
-    if args.summarize_trace or args.summarize_launcher or args.summarize_counters:
+    if (args.summarize_trace or args.summarize_launcher or args.summarize_counters
+            or args.summarize_sweep or args.summarize_pmc or args.summarize_overlap):
         return summarize(args)
+    if args.calibration_copy:
+        exec(CALIBRATION_COPY, {})
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this row-softmax path runs on one GPU; rows shard across "
@@ -717,6 +824,12 @@ def main() -> int:
     torch.cuda.set_device(dev)
     if args.launcher_check:
         print(json.dumps(launcher_check()), flush=True)
+        return 0
+    if args.size_sweep:
+        print(json.dumps(size_sweep()), flush=True)
+        return 0
+    if args.stream_overlap:
+        print(json.dumps(stream_overlap()), flush=True)
         return 0
     regimes = list(W.REGIMES if not args.regimes else args.regimes.split(","))
 

@@ -431,3 +431,143 @@ def summarize_launcher(bench_log: str, trace_dir: str, command: str, peak_gbs: f
                      f"{choice} | {us['auto']:.1f} | {best} | {us[best]:.1f} | "
                      f"{us['auto'] / us[best]:.3f} | {gbs:.0f} | {100 * gbs / peak_gbs:.1f} |")
     return "\n".join(lines) + "\n"
+
+
+def summarize_sweep(bench_log: str, trace_dir: str, command: str, peak_gbs: float) -> str:
+    """Size sweep: per size, the kernel's and the copy's rocprofv3 durations
+    (timed launches, in launch order), and a least-squares line
+    duration = t0 + bytes / rate over the sizes of at least 64 MiB."""
+    res = read_bench_json(bench_log)
+    per = res["launches_per_size"]
+    untimed = 2
+    ds = [d for d in dispatches(read_csv_rows(trace_dir, "kernel_trace.csv"))
+          if d["base"] in ("small_row_kernel", "medium_row_kernel", "stream_copy_kernel")]
+    need = 2 * per * len(res["size_sweep"])
+    if len(ds) != need:
+        raise ValueError(f"{len(ds)} dispatches in the trace, {need} expected")
+    rows, pts = [], []
+    i = 0
+    for s in res["size_sweep"]:
+        k, c = ds[i:i + per], ds[i + per:i + 2 * per]
+        i += 2 * per
+        spec = launch_spec("softmax", s["launch"], "bf16", "bf16")
+        if not all(matches(spec, d) for d in k) or any(d["base"] != "stream_copy_kernel"
+                                                        for d in c):
+            raise ValueError(f"dispatches of {s['rows']} rows do not match {s['launch']}")
+        kt = sorted(d["us"] for d in k[untimed:])
+        ct = sorted(d["us"] for d in c[untimed:])
+        km, cm = kt[len(kt) // 2], ct[len(ct) // 2]
+        rows.append((s, km, cm, _short(k[0]["name"]), k[0]["block"], k[0]["grid"]))
+        if s["bytes"] >= 64 << 20:
+            pts.append((s["bytes"], km))
+    n = len(pts)
+    mb = sum(b for b, _ in pts) / n
+    mt = sum(t for _, t in pts) / n
+    slope = sum((b - mb) * (t - mt) for b, t in pts) / sum((b - mb) ** 2 for b, _ in pts)
+    t0 = mt - slope * mb
+    rate = 1.0 / slope / 1e3  # GB/s (bytes per us / 1e3)
+    lines = [
+        "# Size sweep: small-row kernel and plain copy from 4 MiB to 1 GiB (kernel trace)", "",
+        "Command (repository root, MI355X):", "",
+        "    " + command.replace("\n", "\n    "), "",
+        "Written by `python3 bench.py --summarize-sweep`.  The small-row workload's shape "
+        "(64 bf16 columns, bf16 output) at 16384 to 4194304 rows, the launcher's choice at "
+        "each, and the library's streaming copy of the same bytes; each launch alone after a "
+        f"1 GiB cache-evicting write, {untimed} untimed and {per - untimed} timed launches "
+        "each; medians of the timed launches' rocprofv3 durations.  Bytes: x read plus y "
+        "written.", "",
+        "| rows | MiB | kernel | block | grid threads | kernel us | GB/s | % of peak | copy us "
+        "| copy GB/s |",
+        "|---|---|---|---|---|---|---|---|---|---|",
+    ]
+    for s, km, cm, name, blk, grid in rows:
+        g = s["bytes"] / (km * 1e3)
+        lines.append(f"| {s['rows']} | {s['bytes'] >> 20} | `{name}` | {blk} | {grid} | "
+                     f"{km:.2f} | {g:.0f} | {100 * g / peak_gbs:.1f} | {cm:.2f} | "
+                     f"{s['bytes'] / (cm * 1e3):.0f} |")
+    lines += ["", f"Least-squares line over the {n} sizes of at least 64 MiB: duration = "
+              f"{t0:.2f} us + bytes / {rate:.0f} GB/s ({100 * rate / peak_gbs:.1f}% of peak)."]
+    return "\n".join(lines) + "\n"
+
+
+def summarize_pmc(bench_log: str, pmc_dir: str, command: str) -> str:
+    """Per-launch averages of every counter in a rocprofv3 --pmc run of bench.py."""
+    res = read_bench_json(bench_log)
+    rows = read_csv_rows(pmc_dir, "counter_collection.csv")
+    names = sorted({r["Counter_Name"] for r in rows})
+    vals = {n: counter_values(rows, n) for n in names}
+    lines = [
+        "# Counters per launch: " + ", ".join(names), "",
+        "Command (repository root, MI355X):", "",
+        "    " + command.replace("\n", "\n    "), "",
+        "Written by `python3 bench.py --summarize-pmc`: the average of each counter over the "
+        "dispatches of each launch of the bench JSON line, matched by kernel name, template "
+        "arguments, workgroup size and grid size.", "",
+        "| row | workload | kernel | dispatches | " + " | ".join(names) + " |",
+        "|---|---|---|---|" + "---|" * len(names),
+    ]
+    for row, wl, spec, _alg, _ev, _key in bench_targets(res):
+        per = [[v for d, v in vals[n] if matches(spec, d)] for n in names]
+        if not per[0]:
+            continue
+        name = next(d["name"] for d, _v in vals[names[0]] if matches(spec, d))
+        cells = " | ".join(f"{sum(v) / len(v):.4g}" if v else "-" for v in per)
+        lines.append(f"| {row} | {wl} | `{_short(name)}` | {len(per[0])} | {cells} |")
+    return "\n".join(lines) + "\n"
+
+
+def summarize_overlap(bench_log: str, trace_dir: str, command: str) -> str:
+    """Overlap in time of the two streams' dispatches of bench.py
+    --stream-overlap: the dispatches of launch A and of launch B after the
+    reference and warm-up launches, paired in issue order.  (Their grid is
+    sized from occupancy at launch, so they are matched by kernel, template
+    arguments and workgroup size.)"""
+    res = read_bench_json(bench_log)["stream_overlap"]
+    ds = [d for d in dispatches(read_csv_rows(trace_dir, "kernel_trace.csv"))
+          if d["base"] in ("split_row_kernel", "large_row_kernel")]
+    sa = dict(launch_spec("softmax", res["launch_a"], "f32", "f32"), grid=None)
+    sb = dict(launch_spec("softmax", res["launch_b"], "bf16", "f32"), grid=None)
+
+    def like(spec, d):
+        return matches(dict(spec, grid=d["grid"]), d)
+
+    skip = 1 + res.get("warm_up_launches", 0) // 2
+    a = [d for d in ds if like(sa, d)][skip:]
+    b = [d for d in ds if like(sb, d)][skip:]
+    n = res["pairs"]
+    if len(a) != n or len(b) != n:
+        raise ValueError(f"{len(a)} and {len(b)} dispatches, {n} pairs expected")
+    lines = [
+        "# Two unordered streams: overlap in time of exchanging launches (kernel trace)", "",
+        "Command (repository root, MI355X):", "",
+        "    " + command.replace("\n", "\n    "), "",
+        "Written by `python3 bench.py --summarize-overlap`.  bench.py --stream-overlap issues "
+        f"{n} pairs of launches, A on one stream and B on another, never ordered against "
+        "each other (after one launch on each stream, so that neither stream's first use "
+        "falls inside the pairs).  Both take the single-read form, whose blocks exchange "
+        "their partial results through the library's exchange ring, capped at one block "
+        "per compute unit so that each leaves room for the other.  Every output equals the "
+        "same launch made alone, bitwise (`outputs_equal_to_launches_alone`: "
+        f"{res['outputs_equal_to_launches_alone']}).", "",
+        f"- A: {res.get('rows_a', '?')} x 262144 f32 -> f32, `{res['launch_a']}`",
+        f"- B: {res.get('rows_b', '?')} x 151936 bf16 -> f32, `{res['launch_b']}`", "",
+        "| launch | stream | start (us) | end (us) | us | time shared with the other stream's "
+        "kernels (us) |",
+        "|---|---|---|---|---|---|",
+    ]
+    iv = lambda d: (int(d["row"]["Start_Timestamp"]), int(d["row"]["End_Timestamp"]))
+    ia, ib = [iv(d) for d in a], [iv(d) for d in b]
+    t0 = min(ia[0][0], ib[0][0])
+    shared = lambda x, others: sum(max(0, min(x[1], o[1]) - max(x[0], o[0])) for o in others)
+    rows = sorted([("A", i, x, shared(x, ib)) for i, x in enumerate(ia)] +
+                  [("B", i, x, shared(x, ia)) for i, x in enumerate(ib)], key=lambda r: r[2][0])
+    for lab, i, (x0, x1), sh in rows:
+        lines.append(f"| {lab}{i} | {lab} | {(x0 - t0) / 1e3:.1f} | {(x1 - t0) / 1e3:.1f} | "
+                     f"{(x1 - x0) / 1e3:.1f} | {sh / 1e3:.1f} |")
+    both = sum(shared(x, ib) for x in ia)
+    span = max(ia[-1][1], ib[-1][1]) - t0
+    lines += ["", f"Both streams had a kernel running for {both / 1e3:.1f} us of the "
+              f"{span / 1e3:.1f} us from the first pair's first start to the last end "
+              f"({100 * both / span:.0f}%); {sum(1 for _l, _i, _x, sh in rows if sh > 0)} of "
+              f"{len(rows)} launches ran partly alongside the other stream's."]
+    return "\n".join(lines) + "\n"

@@ -183,3 +183,69 @@ def test_parity_gate_rows_and_planted_error():
     y[bench.gate_rows(64)[5], 17] += 1e-5       # a planted error on a gated row
     bad = bench.parity_gate({w.name: x}, {w.name: y}, [w.name], threads=2)
     assert not bad[w.name]["parity_ok"]
+
+
+def test_size_sweep_summary_fits_fixed_cost_and_rate(tmp_path):
+    # two sizes of at least 64 MiB whose durations lie on 1 us + bytes / 6400 GB/s
+    sizes = [(1048576, 256, 2097152), (2097152, 256, 4194304)]
+    res = {"launches_per_size": 3, "size_sweep": []}
+    rows = []
+    for r, blk, grid_threads in sizes:
+        nbytes = r * 64 * 4
+        desc = SMALL_DESC.replace("block=64 grid=32768", f"block={blk} grid={grid_threads // blk}")
+        res["size_sweep"].append({"rows": r, "cols": 64, "bytes": nbytes, "launch": desc,
+                                  "avg_us": 0.0, "copy_us": 0.0})
+        t = 1.0 + nbytes / 6400e3
+        rows += [(SMALL, blk, grid_threads, 99.0)] + [(SMALL, blk, grid_threads, t)] * 2
+        rows += [(COPY.replace("F32, rowsm::F32, 4", "BF16, rowsm::BF16, 8"), 256,
+                  nbytes // 4 // 16 * 4, t + 0.5)] * 3
+    log = tmp_path / "sweep.log"
+    log.write_text(json.dumps(res) + "\n")
+    write_trace(tmp_path / "t", rows)
+    text = P.summarize_sweep(str(log), str(tmp_path / "t"), "cmd", 8000.0)
+    fit = [ln for ln in text.splitlines() if ln.startswith("Least-squares")][0]
+    assert "= 1.00 us + bytes / 6400 GB/s" in fit, fit
+    write_trace(tmp_path / "t2", rows[:-1])
+    with pytest.raises(ValueError):
+        P.summarize_sweep(str(log), str(tmp_path / "t2"), "cmd", 8000.0)
+
+
+def test_pmc_summary(tmp_path):
+    log = tmp_path / "bench.log"
+    log.write_text(json.dumps(bench_line()) + "\n")
+    d = tmp_path / "pmc"
+    write_pmc(d, "VALUBusy", [(SMALL, 64, 2097152, 20.0), (SMALL, 64, 2097152, 30.0)])
+    text = P.summarize_pmc(str(log), str(d), "cmd")
+    line = [ln for ln in text.splitlines() if ln.startswith("| regimes | small")][0]
+    assert "| 2 | 25 |" in line
+
+
+def test_overlap_summary(tmp_path):
+    da = ("large vw=4 nvec=65536 lpr=1 rpl=4 wpr=1 vpl=16 nv=16 packed=0 u=4 split=16 "
+          "stream=0 prefetch=0 block=256 grid=256 (one group of blocks per row)")
+    db = ("large vw=4 nvec=37984 lpr=1 rpl=4 wpr=1 vpl=10 nv=10 packed=0 u=4 split=16 "
+          "stream=0 prefetch=0 block=256 grid=512 (one group of blocks per row)")
+    res = {"stream_overlap": {"launch_a": da, "launch_b": db, "pairs": 2,
+                              "warm_up_launches": 2, "outputs_equal_to_launches_alone": True}}
+    log = tmp_path / "ov.log"
+    log.write_text(json.dumps(res) + "\n")
+    A = "void rowsm::split_row_kernel<rowsm::F32, rowsm::F32, 4, 16, 0, false>(...)"
+    B = "void rowsm::split_row_kernel<rowsm::BF16, rowsm::F32, 4, 10, 0, false>(...)"
+    d = tmp_path / "t" / "h" / "1"
+    os.makedirs(d)
+    rows = [(A, 256, 65536, 0, 10), (B, 256, 131072, 20, 30),        # references, alone
+            (A, 256, 65536, 40, 50), (B, 256, 131072, 60, 70),      # warm-up, one per stream
+            (A, 256, 65536, 100, 110), (B, 256, 99999, 105, 115),   # half overlap
+            (A, 256, 65536, 200, 210), (B, 256, 131072, 220, 230)]  # none
+    with open(d / "1_t_kernel_trace.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=TRACE_COLS)
+        w.writeheader()
+        for i, (name, blk, grid, t0, t1) in enumerate(rows):
+            w.writerow({"Dispatch_Id": i + 1, "Kernel_Name": name, "Start_Timestamp": t0 * 1000,
+                        "End_Timestamp": t1 * 1000, "Workgroup_Size_X": blk,
+                        "Workgroup_Size_Y": 1, "Workgroup_Size_Z": 1, "Grid_Size_X": grid,
+                        "Grid_Size_Y": 1, "Grid_Size_Z": 1})
+    text = P.summarize_overlap(str(log), str(tmp_path / "t"), "cmd")
+    # A at 100-110 shares 5 us with B at 105-115; A at 200-210 shares nothing
+    assert "Both streams had a kernel running for 5.0 us of the 130.0 us" in text, text
+    assert "2 of 4 launches ran partly alongside" in text, text
