@@ -682,6 +682,7 @@ def launcher_check(reps: int = 8):
         code = {"scaled_causal": R.OP_SCALED_CAUSAL,
                 "backward": R.OP_SOFTMAX_BACKWARD}.get(op, R.OP_SOFTMAX)
         rec = {"op": op, "rows": rows, "cols": cols, "in": din, "out": dout,
+               "causal_period": cols if op == "scaled_causal" else 0,
                "launch": R.rowsm_describe_op(code, rows, cols, R.dtype_code(x.dtype),
                                              R.dtype_code(y.dtype))[1],
                "timed": [], "us": {}}

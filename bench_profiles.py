@@ -405,6 +405,7 @@ def summarize_launcher(bench_log: str, trace_dir: str, command: str, peak_gbs: f
         "|---|---|---|---|---|---|---|---|---|---|",
     ]
     i = 0
+    ratios = []
     for r in res["launcher_check"]:
         us = {}
         for name in r["timed"]:
@@ -422,7 +423,17 @@ def summarize_launcher(bench_log: str, trace_dir: str, command: str, peak_gbs: f
         best = min(us, key=us.get)
         ib, ob = DTYPE_BYTES[r["in"]], DTYPE_BYTES[r["out"]]
         n = r["rows"] * r["cols"]
-        alg = n * (2 * ib + ob) if r["op"] == "backward" else n * (ib + ob)
+        if r["op"] == "backward":
+            alg = n * (2 * ib + ob)
+        elif r["op"] == "scaled_causal":
+            # the kept entries of x (column c of row r kept for c <= r mod q,
+            # q = causal_period; the launcher check passes q = cols) and all of y
+            q = r.get("causal_period") or r["cols"]
+            full, rem = divmod(r["rows"], q)
+            kept = full * (q * (q + 1) // 2) + rem * (rem + 1) // 2
+            alg = kept * ib + n * ob
+        else:
+            alg = n * (ib + ob)
         gbs = alg / (us["auto"] * 1e3)
         f = parse_launch(r["launch"])
         choice = (f"{f['family']} wpr={f.get('wpr')} nv={f.get('nv')} split={f.get('split')} "
@@ -430,6 +441,14 @@ def summarize_launcher(bench_log: str, trace_dir: str, command: str, peak_gbs: f
         lines.append(f"| {r['op']} | {r['rows']} x {r['cols']} | {r['in']} -> {r['out']} | "
                      f"{choice} | {us['auto']:.1f} | {best} | {us[best]:.1f} | "
                      f"{us['auto'] / us[best]:.3f} | {gbs:.0f} | {100 * gbs / peak_gbs:.1f} |")
+        ratios.append(us["auto"] / us[best])
+    gm = 1.0
+    for q in ratios:
+        gm *= q ** (1.0 / len(ratios))
+    lines += ["", f"The launcher's choice over the fastest shape: geometric mean {gm:.3f} over "
+              f"{len(ratios)} launches, at most {max(ratios):.3f}.  Algorithmic bytes: x read "
+              "once and y written once (the kept entries of x for the fused rows; y and dy "
+              "for the backward)."]
     return "\n".join(lines) + "\n"
 
 
