@@ -452,6 +452,34 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->packed = false;
         p->measured = true;
       } else if (shape.wpr > 0) {
+        // Lane fill: when the table's wave group leaves too much of its last
+        // slot empty (less than 60% of the group's slots hold a vector, 70%
+        // for bf16 <-> fp32 rows), the largest smaller group that fills them
+        // is taken, in 256-thread blocks.  Rows just past a group boundary
+        // (e.g. 260-350 vectors on 4 waves, 136-170 on 2) measured 10-42%
+        // slower than the smaller group for bf16 <-> fp32 and up to 15% for
+        // one width.  Over 193 full launches of 136-1024-vector rows in every
+        // dtype pair (three sweeps, each launch alone after a cache-evicting
+        // write) the table's picks were 6.1% above the fastest form on
+        // geometric mean and are 2.0% with this rule, no launch more than 2%
+        // slower than before; at the 88 lengths of the third sweep, which
+        // were not used to set the thresholds, 7.7% and 2.7%.
+        const int fill_pct = ib == ob ? 60 : 70;
+        auto filled = [&](int w) {
+          const int64_t slots = cdiv(nvec, (int64_t)w * kWave) * w * kWave;
+          return nvec * 100 >= (int64_t)fill_pct * slots;
+        };
+        if (!filled(shape.wpr)) {
+          for (int w = shape.wpr / 2; w >= 1; w /= 2) {
+            const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+            if (v * vw > 64 || !medium_unpacked_cap(vw, v)) break;
+            if (filled(w)) {
+              shape.wpr = w;
+              shape.rpb = 4 / w > 1 ? 4 / w : 1;
+              break;
+            }
+          }
+        }
         p->wpr = shape.wpr;
         p->vpl = (int)cdiv(nvec, (int64_t)shape.wpr * kWave);
         p->packed = false;

@@ -418,6 +418,12 @@ MEASURED_SHAPES = [
     (3584, "f32", "bf16", ("medium", "wpr=4 ", "block=512 ")),
     (8192, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 ")),
     (12288, "f32", "bf16", ("large", "split=1 ", "block=512 ")),
+    # lane fill: a smaller wave group when the table's leaves its last slot
+    # mostly empty (256-thread blocks)
+    (544, "bf16", "f32", ("medium", "wpr=1 ", "nv=3 ", "block=256 ")),    # 136 vectors
+    (1152, "f32", "bf16", ("medium", "wpr=2 ", "nv=3 ", "block=256 ")),   # 288 vectors
+    (2176, "bf16", "bf16", ("medium", "wpr=2 ", "nv=3 ", "block=256 ")),  # 272 vectors
+    (1120, "f32", "f32", ("medium", "wpr=2 ", "nv=3 ", "block=256 ")),    # 280 vectors
 ]
 
 
