@@ -155,10 +155,16 @@ bool few_long_rows(int64_t rows, int64_t row_bytes, bool packed, int cus,
 // medium and the single-read kernel at the same geometry differ by up to
 // 20% either way), hence a table.  Smaller launches keep the previous rule:
 // at 8-16 rows per compute unit fewer waves per row measured fastest.
-// Widening rows continue to 8192 vectors, bf16 rows of 2049-4096 vectors
-// have picks of their own (sweeps of 18432-30720 columns, half of them not
-// fitted: within 1.7% of the fastest form, where the previous rule was up
-// to 12% slower).
+// Widening rows continue to 8192 vectors.  The single-read picks beyond 1280
+// vectors were re-measured after the row stores became non-temporal at
+// device scope, at 8192, 16384 and 32768 rows of 1536-8192 vectors on three
+// boxes (206 launches): the best shape there depends on the row count as
+// well (e.g. 2048-vector fp32 rows: one 512-thread block level with two
+// 256-thread blocks at 8192 rows, 12% slower at 32768), so each entry is the
+// shape with the lowest mean slowdown over the three counts.  The previous
+// picks were 1.5% above the fastest shape on geometric mean there (at most
+// 13%), these 0.5% (at most 5%); at 60 launches of other lengths and row
+// counts (12288 and 24576 rows) 1.6% and 0.6%.
 struct RowShape {
   int wpr = 0, rpb = 0, S = 0, T = 0;
 };
@@ -169,25 +175,22 @@ bool measured_row_shape(int64_t nvec, int ib, int ob, RowShape* r) {
     int upto, wpr, rpb, S, T;
   };
   // {longest row (vectors), wpr, rpb, S, T}
-  static constexpr Row kSame[] = {{256, 2, 1, 0, 0},    {320, 4, 1, 0, 0},
-                                  {512, 4, 2, 0, 0},    {640, 4, 1, 0, 0},
-                                  {1280, 8, 1, 0, 0},   {1792, 0, 0, 1, 512},
-                                  {3072, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
+  static constexpr Row kSameF32[] = {{256, 2, 1, 0, 0},    {320, 4, 1, 0, 0},
+                                     {512, 4, 2, 0, 0},    {640, 4, 1, 0, 0},
+                                     {1280, 8, 1, 0, 0},   {1920, 0, 0, 1, 512},
+                                     {3584, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
+  static constexpr Row kSameBf16[] = {{256, 2, 1, 0, 0},    {320, 4, 1, 0, 0},
+                                      {512, 4, 2, 0, 0},    {640, 4, 1, 0, 0},
+                                      {1280, 8, 1, 0, 0},   {1920, 0, 0, 1, 512},
+                                      {3840, 0, 0, 2, 256}, {4096, 0, 0, 4, 256}};
   static constexpr Row kWiden[] = {{256, 2, 1, 0, 0},    {512, 4, 1, 0, 0},
                                    {896, 4, 2, 0, 0},    {1792, 8, 1, 0, 0},
-                                   {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256},
+                                   {2432, 0, 0, 1, 512}, {4608, 0, 0, 2, 256},
                                    {8192, 0, 0, 2, 512}};
   static constexpr Row kNarrow[] = {{256, 2, 1, 0, 0},   {768, 4, 1, 0, 0},
-                                    {1024, 4, 2, 0, 0},  {2048, 8, 1, 0, 0},
-                                    {3072, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
-  if (ib == ob && ib == 2 && nvec > 2048) {
-    // bf16 rows of 2049-4096 vectors: 512 threads per row, one block up to
-    // 2560 vectors, two beyond
-    r->S = nvec <= 2560 ? 1 : 2;
-    r->T = nvec <= 2560 ? 512 : 256;
-    return true;
-  }
-  const Row* t = ib == ob ? kSame : (widen ? kWiden : kNarrow);
+                                    {1024, 4, 2, 0, 0},  {1664, 8, 1, 0, 0},
+                                    {2816, 0, 0, 1, 512}, {4096, 0, 0, 2, 256}};
+  const Row* t = ib == ob ? (ib == 2 ? kSameBf16 : kSameF32) : (widen ? kWiden : kNarrow);
   while (nvec > t->upto) ++t;
   r->wpr = t->wpr;
   r->rpb = t->rpb;

@@ -158,11 +158,20 @@ def test_select_regimes(lib):
     assert has(d(100000, 6144, R.BF16, R.F32)[1], "medium", "wpr=8 ", "vpl=3 ")
     assert has(d(100000, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
     assert has(d(100000, 8192, R.BF16, R.F32)[1], "large", "split=1 ", "block=512 ")
-    assert has(d(100000, 8192, R.F32, R.BF16)[1], "medium", "wpr=8 ", "vpl=4 ")
+    assert has(d(100000, 8192, R.F32, R.BF16)[1], "large", "split=1 ", "block=512 ")
     assert has(d(100000, 16384, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 15360, R.BF16, R.BF16)[1], "large", "split=1 ", "block=512 ")
+    assert has(d(100000, 20480, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
     assert has(d(100000, 12288, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 14336, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
     assert has(d(100000, 16384, R.F32, R.F32)[1], "large", "split=2 ", "block=512 ")
     assert has(d(100000, 16384, R.BF16, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 11264, R.BF16, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 9728, R.BF16, R.F32)[1], "large", "split=1 ", "block=512 ")
+    assert has(d(100000, 9732, R.BF16, R.F32)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 18436, R.BF16, R.F32)[1], "large", "split=2 ", "block=512 ")
+    assert has(d(100000, 16384, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
+    assert has(d(100000, 32768, R.BF16, R.BF16)[1], "large", "split=4 ", "block=256 ")
     # 4-16 rows per compute unit: the fewest waves per row that keep about two
     # 512-thread blocks per compute unit (at least what the registers need)
     assert has(d(1024, 8192, R.BF16, R.BF16)[1], "medium", "wpr=4 ", "vpl=4 ", "block=512 ")
@@ -192,13 +201,13 @@ def test_select_regimes(lib):
     assert has(fd(2048, R.BF16), "medium", "wpr=2 ", "vpl=4 ", "block=128 ")
     assert has(fd(5120, R.BF16), "medium", "wpr=4 ", "vpl=5 ")
     assert has(d(100000, 24576, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
-    assert has(d(100000, 18432, R.BF16, R.BF16)[1], "large", "split=1 ", "block=512 ")
+    assert has(d(100000, 18432, R.BF16, R.BF16)[1], "large", "split=2 ", "block=256 ")
     assert has(d(10000, 24576, R.BF16, R.F32)[1], "large", "split=2 ", "block=512 ")
     assert has(d(10000, 36864, R.BF16, R.F32)[1], "large", "split=4 ")  # beyond 8192 vectors
     # a single-read pick only while one group of blocks per row fits the
     # 2^20-block exchange workspace
-    assert has(d(524288, 8192, R.F32, R.F32)[1], "large", "split=2 ")
-    assert has(d(524289, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")
+    assert has(d(524288, 12288, R.F32, R.F32)[1], "large", "split=2 ")
+    assert has(d(524289, 12288, R.F32, R.F32)[1], "medium", "wpr=16 ", "vpl=3 ")
     assert has(R.rowsm_describe_op(R.OP_LOG_SOFTMAX, 100000, 8192, R.F32, R.F32)[1],
                "large", "split=2 ", "block=256 ")
     bd = lambda rows, cols, i, o: R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, i, o)[1]

@@ -260,7 +260,7 @@ def test_forced_split_form_under_capture():
     (40000, 6144, "f32", "f32", None, "split=1 "),
     # forced: one block per row, and two
     (1000, 3000, "bf16", "f32", dict(variant=R.LARGE, split_blocks=1), "split=1 "),
-    (9000, 16384, "bf16", "bf16", None, "split=2 "),
+    (9000, 20480, "bf16", "bf16", None, "split=2 "),
 ])
 def test_single_read_one_block_per_row_under_capture(rows, cols, din, dout, cfg, want):
     # every single-read launch exchanges through the workspace, one block

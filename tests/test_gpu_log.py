@@ -196,8 +196,9 @@ def test_log_bounded_writes_and_deterministic():
 @pytest.mark.parametrize("cols,din,dout,want", [
     (6144, "f32", "f32", ("large", "split=1 ", "block=512 ")),
     (2560, "bf16", "bf16", ("medium", "wpr=4 ", "block=256 ")),
-    (10240, "bf16", "f32", ("large", "split=1 ", "block=512 ")),
-    (8192, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 "))])
+    (10240, "bf16", "f32", ("large", "split=2 ", "block=256 ")),
+    (6656, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 ")),
+    (8192, "f32", "bf16", ("large", "split=1 ", "block=512 "))])
 def test_log_measured_launch_shapes(cols, din, dout, want):
     # full launches of medium-length rows take the same measured shapes as
     # softmax; sampled rows element by element

@@ -404,20 +404,27 @@ MEASURED_SHAPES = [
     (2560, "f32", "f32", ("medium", "wpr=4 ", "block=256 ")),
     (4096, "f32", "f32", ("medium", "wpr=8 ", "block=512 ")),
     (6144, "f32", "f32", ("large", "split=1 ", "block=512 ")),
+    (7680, "f32", "f32", ("large", "split=1 ", "block=512 ")),
     (8192, "f32", "f32", ("large", "split=2 ", "block=256 ")),
-    (14336, "f32", "f32", ("large", "split=2 ", "block=512 ")),
+    (14336, "f32", "f32", ("large", "split=2 ", "block=256 ")),
+    (16384, "f32", "f32", ("large", "split=2 ", "block=512 ")),
     (2560, "bf16", "bf16", ("medium", "wpr=4 ", "block=256 ")),
-    (16384, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
-    (18432, "bf16", "bf16", ("large", "split=1 ", "block=512 ")),
+    (15360, "bf16", "bf16", ("large", "split=1 ", "block=512 ")),
+    (32768, "bf16", "bf16", ("large", "split=4 ", "block=256 ")),
+    (20480, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
+    (18432, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
     (28672, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
     (24576, "bf16", "f32", ("large", "split=2 ", "block=512 ")),
     (3072, "bf16", "f32", ("medium", "wpr=4 ", "block=512 ")),
     (6144, "bf16", "f32", ("medium", "wpr=8 ", "vpl=3 ")),
-    (10240, "bf16", "f32", ("large", "split=1 ", "block=512 ")),
+    (9728, "bf16", "f32", ("large", "split=1 ", "block=512 ")),
+    (10240, "bf16", "f32", ("large", "split=2 ", "block=256 ")),
     (16384, "bf16", "f32", ("large", "split=2 ", "block=256 ")),
+    (11264, "bf16", "f32", ("large", "split=2 ", "block=256 ")),
     (3584, "f32", "bf16", ("medium", "wpr=4 ", "block=512 ")),
-    (8192, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 ")),
-    (12288, "f32", "bf16", ("large", "split=1 ", "block=512 ")),
+    (6656, "f32", "bf16", ("medium", "wpr=8 ", "vpl=4 ")),
+    (11264, "f32", "bf16", ("large", "split=1 ", "block=512 ")),
+    (12288, "f32", "bf16", ("large", "split=2 ", "block=256 ")),
     # lane fill: a smaller wave group when the table's leaves its last slot
     # mostly empty (256-thread blocks)
     (544, "bf16", "f32", ("medium", "wpr=1 ", "nv=3 ", "block=256 ")),    # 136 vectors
@@ -476,7 +483,7 @@ def test_measured_single_read_picks_on_streams_and_threads():
     # four streams, interleaved with medium launches: bitwise equal to the
     # same launches made one at a time
     import threading
-    shapes = [(8192, 6144, "f32", "f32"), (8192, 16384, "bf16", "bf16"),
+    shapes = [(8192, 6144, "f32", "f32"), (8192, 20480, "bf16", "bf16"),
               (8192, 6144, "bf16", "bf16"), (9000, 4096, "f32", "f32")]
     xs, refs = [], []
     for rows, cols, din, dout in shapes:
