@@ -24,8 +24,11 @@ SOURCES = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 HEADERS = sorted(glob.glob(os.path.join(CSRC, "*.hpp")))
 
 # Packed-fp32 instructions are disabled for every HIP translation unit: the
-# host pass warns that it does not know the feature, which is harmless.
-HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+# host pass warns that it does not know the feature, which is harmless.  The
+# device code objects are stored compressed (--offload-compress; the HIP
+# runtime unpacks them when the library loads), which takes the library from
+# about 23 MiB to about 8 MiB.
+HIP_FLAGS = ["--offload-arch=gfx950", "--offload-compress", "-O3", "-std=c++17", "-fPIC",
              "-Wall", "-Wextra", "-Wno-unused-parameter",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-I", INCLUDE, "-I", CSRC]
