@@ -301,8 +301,11 @@ class HipEvent:
         return ms.value
 
     def __del__(self):
-        if HipEvent._hip is not None and self.ev:
-            HipEvent._hip.hipEventDestroy(self.ev)
+        # through type(self): at interpreter exit the module's globals may
+        # already be cleared when a module-level event is collected
+        hip = type(self)._hip
+        if hip is not None and self.ev:
+            hip.hipEventDestroy(self.ev)
 
 
 # Read-only and write-only rates of streaming probes with 8 vectors per
