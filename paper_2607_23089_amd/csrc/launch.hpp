@@ -37,7 +37,6 @@ struct Plan {
   int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
   int stream = 1;   // two-pass form: blocks per row (1: one block per row)
   bool prefetch = false;  // single-read form: load the next row during the exchange
-  bool measured = false;  // single-read form picked by the measured row-shape table
   // launch
   int block = 256;
   int64_t grid = 1;  // split form: 0 = one group per row, < 0 = minus the blocks-per-CU cap

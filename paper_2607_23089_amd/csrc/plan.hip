@@ -232,6 +232,53 @@ bool measured_fused_shape(int64_t nvec, int ib, int ob, RowShape* r) {
   return true;
 }
 
+// The same for the softmax backward (y and dy read, dx written): rows of
+// 129-4096 full 16-byte vectors in launches of at least 32 rows per compute
+// unit.  The medium form for short rows, the single-read form with one
+// block of 256 or 512 threads per row from about 300 vectors (fp32 input,
+// or bf16 of one width) and two to four blocks per row from about 1400-2700;
+// widening rows (bf16 -> fp32) stay in the medium form throughout.  From
+// sweeps of 144-4096 vectors in every dtype pair (56 lengths, two row counts
+// each between 8192 and 131072 rows, every launch timed alone after a
+// cache-evicting write), each entry the shape with the lowest mean slowdown
+// over its lengths, an entry of one length only where it gains several
+// percent: 0.4-0.7% above the fastest shape measured on geometric mean per
+// dtype pair, where the register-cap rule below was 2.3-4.2% (at most 16%).
+// Fitted with each length left out in turn and judged on it: 0.7-1.3% (at
+// most 11-13%).  At 21 further lengths used in no fit (149 launches of
+// 9216 and 18432 rows): 1.3% above the fastest shape (at most 8.6%), the
+// register-cap rule 2.9% (at most 10.1%).
+bool measured_backward_shape(int64_t nvec, int ib, int ob, RowShape* r) {
+  if (nvec <= 128 || nvec > 4096) return false;
+  struct Row {
+    int upto, wpr, rpb, S, T;
+  };
+  // {longest row (vectors), wpr, rpb, S, T}
+  static constexpr Row kSameF32[] = {{280, 4, 1, 0, 0},    {432, 0, 0, 1, 256},
+                                     {608, 8, 1, 0, 0},    {1312, 0, 0, 1, 512},
+                                     {2624, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
+  static constexpr Row kSameBf16[] = {{168, 2, 1, 0, 0},    {304, 4, 1, 0, 0},
+                                      {408, 0, 0, 1, 256},  {736, 8, 1, 0, 0},
+                                      {1376, 0, 0, 1, 512}, {1632, 16, 1, 0, 0},
+                                      {2112, 0, 0, 2, 256}, {3392, 0, 0, 2, 512},
+                                      {4096, 0, 0, 4, 256}};
+  static constexpr Row kWiden[] = {{264, 2, 1, 0, 0},  {432, 4, 1, 0, 0},
+                                   {608, 4, 2, 0, 0},  {1216, 8, 1, 0, 0},
+                                   {2240, 4, 1, 0, 0}, {4096, 16, 1, 0, 0}};
+  static constexpr Row kNarrow[] = {{168, 2, 2, 0, 0},    {304, 4, 1, 0, 0},
+                                    {432, 0, 0, 1, 256},  {608, 8, 1, 0, 0},
+                                    {1120, 0, 0, 1, 512}, {1376, 8, 2, 0, 0},
+                                    {2752, 0, 0, 2, 256}, {4096, 0, 0, 2, 512}};
+  const bool widen = ob > ib;
+  const Row* t = ib == ob ? (ib == 2 ? kSameBf16 : kSameF32) : (widen ? kWiden : kNarrow);
+  while (nvec > t->upto) ++t;
+  r->wpr = t->wpr;
+  r->rpb = t->rpb;
+  r->S = t->S;
+  r->T = t->T;
+  return true;
+}
+
 // Blocks per row for a split launch of fewer than cus rows with T-thread
 // blocks holding at most nv_cap vectors per thread: about one block per
 // compute unit over the launch (the largest power of two with rows * S <=
@@ -453,7 +500,6 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->variant = variant;
         p->wpr = 1;
         p->packed = false;
-        p->measured = true;
       } else if (shape.wpr > 0) {
         // Lane fill: when the table's wave group leaves too much of its last
         // slot empty (less than 60% of the group's slots hold a vector, 70%
@@ -651,6 +697,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
 
   int variant = cfg ? cfg->variant : ROWSM_AUTO;
   const bool auto_variant = variant == ROWSM_AUTO;
+  RowShape shape;  // measured_backward_shape() pick, when it applies
   if (variant == ROWSM_AUTO) {
     if (nvec <= 32)
       variant = ROWSM_SMALL;
@@ -729,20 +776,35 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
         }
       }
     }
+    // Full launches of rows of 129-4096 full vectors, when nothing about the
+    // shape is forced: the measured shapes of measured_backward_shape() (a
+    // single-read pick only out of place and while the rows fit the
+    // exchange workspace with one group of blocks per row).
+    int table_rpb = 0;
+    if (auto_variant && shape_free && vw * (ib > ob ? ib : ob) == 16 &&
+        rows >= 32 * (int64_t)cus && measured_backward_shape(nvec, ib, ob, &shape)) {
+      if (shape.S > 0 && (inplace || rows * shape.S > kSplitMaxBlocks)) {
+        shape = RowShape{};
+      } else if (shape.wpr > 0) {
+        wpr = shape.wpr;
+        nv = (int)cdiv(nvec, (int64_t)wpr * kWave);
+        table_rpb = shape.rpb;
+      }
+    }
     // A row that needs all 16 waves of a 1024-thread block goes to the
     // split form from 4 * cus rows when it holds at least 64 KiB of each
     // input (measured 4-20% faster there at 16384-65536 columns in every
     // dtype pair, and within 1% of the medium form at 256-512 rows; the
     // forward's reason).
-    if (auto_variant && !inplace && wpr == 16 && cols * ib >= 65536 &&
-        rows >= 4 * (int64_t)cus) {
+    if (shape.S > 0 || (auto_variant && !inplace && wpr == 16 && cols * ib >= 65536 &&
+                        rows >= 4 * (int64_t)cus)) {
       variant = ROWSM_LARGE;
       p->variant = variant;
     } else {
       p->wpr = wpr;
       p->vpl = nv;
       p->nv = nv;
-      int rpb = wpr >= 8 ? 1 : 8 / wpr;  // 512-thread blocks
+      int rpb = table_rpb ? table_rpb : (wpr >= 8 ? 1 : 8 / wpr);  // 512-thread blocks
       if (cfg && cfg->rows_per_block > 0) {
         rpb = cfg->rows_per_block;
         if (rpb * wpr > 16) return ROWSM_EINVAL;
@@ -774,6 +836,10 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
         S = (int)(thr / T);
         const int64_t s_cap = cdiv(nvec, (int64_t)nv_cap * T);
         while (S < s_cap) S <<= 1;
+      }
+      if (shape.S > 0) {
+        S = shape.S;
+        T = shape.T;
       }
       if (S < 1) S = 1;
       if (want_split == 0) {

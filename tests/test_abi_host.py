@@ -303,15 +303,18 @@ def test_describe(lib):
     # any row count; blocks_per_cu caps them (the waves then stride)
     # (4M rows of 64 bf16 columns take one-wave blocks of one row group per
     # lane, forward and backward)
-    for op, grid in ((R.OP_SOFTMAX, 524288), (R.OP_SOFTMAX_BACKWARD, 524288)):
+    # (131072 rows of 4096 bf16 columns: the forward's 4 waves per row with 2
+    # rows per block, the backward's measured 8 waves per row)
+    for op, grid, wpr, mgrid in ((R.OP_SOFTMAX, 524288, 4, 65536),
+                                 (R.OP_SOFTMAX_BACKWARD, 524288, 8, 131072)):
         st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16)
         assert st == R.OK and text.startswith("small") and f"grid={grid} " in text, text
         st, text = R.rowsm_describe_op(op, 4194304, 64, R.BF16, R.BF16,
                                        R.RowsmConfig(blocks_per_cu=8))
         assert st == R.OK and "grid=2048 " in text, text
         st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16)
-        assert st == R.OK and text.startswith("medium") and "wpr=4" in text, text
-        assert "block=512" in text and "grid=65536 " in text, text
+        assert st == R.OK and text.startswith("medium") and f"wpr={wpr} " in text, text
+        assert "block=512" in text and f"grid={mgrid} " in text, text
         st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16,
                                        R.RowsmConfig(blocks_per_cu=64))
         assert st == R.OK and "grid=16384 " in text, text
@@ -375,8 +378,25 @@ def test_backward_plans(lib):
         R.OP_SOFTMAX_BACKWARD, rows, cols, i, o, R.RowsmConfig(**cfg) if cfg else None)
     st, t = d(262144, 64, R.BF16, R.BF16)
     assert st == R.OK and t.startswith("small") and "lpr=8" in t and "rpl=1" in t  # 96 MiB
-    st, t = d(32768, 4096, R.BF16, R.BF16)
-    assert st == R.OK and t.startswith("medium") and "wpr=4" in t and "nv=2" in t
+    # full launches (>= 32 rows per compute unit) of 129-4096 full vectors:
+    # the measured backward shapes
+    st, t = d(32768, 4096, R.BF16, R.BF16)                         # 512 vectors
+    assert st == R.OK and t.startswith("medium") and "wpr=8 " in t and "nv=1 " in t, t
+    st, t = d(8192, 4096, R.F32, R.F32)                            # 1024 vectors
+    assert st == R.OK and t.startswith("large") and "split=1 " in t and "block=512" in t, t
+    st, t = d(8192, 16384, R.F32, R.F32)                           # 4096 vectors
+    assert st == R.OK and "split=2 " in t and "block=512" in t and "nv=4 " in t, t
+    st, t = d(8192, 16384, R.F32, R.BF16)
+    assert st == R.OK and "split=2 " in t and "block=512" in t and "nv=4 " in t, t
+    st, t = d(8192, 16384, R.BF16, R.F32)                          # widening: medium
+    assert st == R.OK and t.startswith("medium") and "wpr=16 " in t and "nv=4 " in t, t
+    st, t = d(8192, 1024, R.BF16, R.BF16)                          # 128 vectors: not in it
+    assert st == R.OK and "wpr=1 " in t and "nv=2 " in t, t
+    # fewer rows, or a shape field given: the register-cap rule
+    st, t = d(8191, 16384, R.F32, R.F32)
+    assert st == R.OK and t.startswith("large") and "split=8 " in t, t
+    st, t = d(32768, 4096, R.BF16, R.BF16, rows_per_block=2)
+    assert st == R.OK and "wpr=4 " in t and "nv=2 " in t and "block=512" in t, t
     # medium holds at most 128 bytes of each input per lane: 16 x 64 x 8 vectors
     assert d(100, 65536, R.BF16, R.BF16)[1].startswith("medium")
     assert d(100, 65544, R.BF16, R.BF16)[1].startswith("large")

@@ -111,6 +111,75 @@ def test_bwd_few_rows_per_cu_shapes(rows, cols, din, dout, want):
                       f"bwd {rows}x{cols} {din}->{dout} [{desc}]")
 
 
+BWD_MEASURED_SHAPES = [  # (cols, din, dout, expected plan fields): one length per table entry
+    (1200, "bf16", "bf16", ("medium", "wpr=2 ", "block=128 ")),
+    (2000, "bf16", "bf16", ("medium", "wpr=4 ", "block=256 ")),
+    (2800, "bf16", "bf16", ("large", "split=1 ", "block=256 ")),
+    (4800, "bf16", "bf16", ("medium", "wpr=8 ", "block=512 ")),
+    (8000, "bf16", "bf16", ("large", "split=1 ", "block=512 ")),
+    (12000, "bf16", "bf16", ("medium", "wpr=16 ", "block=1024 ")),
+    (16000, "bf16", "bf16", ("large", "split=2 ", "block=256 ")),
+    (24000, "bf16", "bf16", ("large", "split=2 ", "block=512 ")),
+    (32000, "bf16", "bf16", ("large", "split=4 ", "block=256 ")),
+    (800, "f32", "f32", ("medium", "wpr=4 ", "block=256 ")),
+    (1680, "f32", "f32", ("large", "split=1 ", "block=256 ")),
+    (2400, "f32", "f32", ("medium", "wpr=8 ", "block=512 ")),
+    (4000, "f32", "f32", ("large", "split=1 ", "block=512 ")),
+    (8000, "f32", "f32", ("large", "split=2 ", "block=256 ")),
+    (16384, "f32", "f32", ("large", "split=2 ", "block=512 ")),
+    (600, "bf16", "f32", ("medium", "wpr=2 ", "block=128 ")),
+    (1200, "bf16", "f32", ("medium", "wpr=4 ", "block=256 ")),
+    (2400, "bf16", "f32", ("medium", "wpr=4 ", "block=512 ")),
+    (4000, "bf16", "f32", ("medium", "wpr=8 ", "block=512 ")),
+    (8000, "bf16", "f32", ("medium", "wpr=4 ", "nv=8 ", "block=256 ")),
+    (12000, "bf16", "f32", ("medium", "wpr=16 ", "block=1024 ")),
+    (600, "f32", "bf16", ("medium", "wpr=2 ", "block=256 ")),
+    (1024, "f32", "bf16", ("medium", "wpr=4 ", "block=256 ")),
+    (1680, "f32", "bf16", ("large", "split=1 ", "block=256 ")),
+    (2400, "f32", "bf16", ("medium", "wpr=8 ", "block=512 ")),
+    (4000, "f32", "bf16", ("large", "split=1 ", "block=512 ")),
+    (5200, "f32", "bf16", ("medium", "wpr=8 ", "block=1024 ")),
+    (8000, "f32", "bf16", ("large", "split=2 ", "block=256 ")),
+    (12000, "f32", "bf16", ("large", "split=2 ", "block=512 ")),
+]
+
+
+@pytest.mark.parametrize("cols,din,dout,want", BWD_MEASURED_SHAPES)
+def test_bwd_measured_launch_shapes(cols, din, dout, want):
+    # full launches (8201 rows: >= 32 per compute unit, ragged) take the
+    # measured backward shapes; sampled rows, the last ones among them,
+    # against the oracle
+    rows = 8201
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith(want[0]) and all(w in desc for w in want), desc
+    print(f"bwd measured shape {rows}x{cols} {din}->{dout}: {desc}", flush=True)
+    y = W.random_probabilities(rows, cols, din, 0.3, seed=cols + 2, device=DEV)
+    dy = W.random_matrix(rows, cols, din, sigma=1.0, seed=cols + 3, device=DEV)
+    dx = run_bwd(y, dy, dout)
+    sample = list(range(0, rows, 131)) + [rows - 2, rows - 1]
+    assert_bwd_parity(y[sample].cpu(), dy[sample].cpu(), dx[sample].cpu(), dout,
+                      f"bwd {rows}x{cols} {din}->{dout} [{desc}]")
+    del y, dy, dx
+
+
+@pytest.mark.parametrize("cols,dt", [(4000, "f32"), (16000, "bf16")])
+def test_bwd_in_place_full_launch(cols, dt):
+    # in place, a full launch whose measured shape is the single-read form
+    # keeps the medium form (no exchanging form in place): over dy and over y
+    rows = 8201
+    y = W.random_probabilities(rows, cols, dt, 0.3, seed=cols, device=DEV)
+    dy = W.random_matrix(rows, cols, dt, sigma=1.0, seed=cols + 1, device=DEV)
+    sample = list(range(0, rows, 257)) + [rows - 1]
+    ys, dys = y[sample].cpu(), dy[sample].cpu()
+    for over in ("dy", "y"):
+        yd, dyd = y.clone(), dy.clone()
+        out = dyd if over == "dy" else yd
+        run_bwd(yd, dyd, dt, out=out)
+        assert_bwd_parity(ys, dys, out[sample].cpu(), dt, f"bwd in place over {over} {rows}x{cols}")
+        del yd, dyd
+
+
 @pytest.mark.parametrize("rows,cols,din,dout", [
     (262144, 64, "bf16", "bf16"), (262147, 64, "bf16", "bf16"), (131072, 128, "f32", "f32"),
     (1048576, 32, "bf16", "f32"), (786435, 16, "f32", "bf16")])
