@@ -723,7 +723,27 @@ CALIBRATION_COPY = ("import torch; a=torch.ones(1<<28, device='cuda'); b=torch.e
 
 def summarize(args) -> int:
     """Write profiles/ summaries from rocprofv3 CSV output (no GPU)."""
+    import shlex
+
     import bench_profiles as P
+    if not args.command.strip():
+        print("a summary names the commands that made its rocprofv3 output: pass --command",
+              file=sys.stderr)
+        return 2
+    # the header: the given commands, then this summariser's own invocation
+    argv, skip = [], False
+    for a in sys.argv[1:]:
+        if skip:
+            skip = False
+        elif a == "--command":
+            skip = True
+        elif not a.startswith("--command="):
+            argv.append(a)
+    given = [ln for ln in args.command.strip().splitlines()
+             if not ln.lstrip().startswith("python3 bench.py --summarize")]
+    args.command = "\n".join(given + [
+        "python3 bench.py " + " ".join(shlex.quote(a) for a in argv) +
+        ' --command "<the lines above>"'])
     if args.summarize_trace:
         log, d, out = args.summarize_trace
         text = P.summarize_trace(log, d, args.command, PEAK_HBM_GBS)
