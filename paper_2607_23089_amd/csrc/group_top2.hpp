@@ -109,8 +109,7 @@ __global__ __launch_bounds__(256) void group_top2_kernel(
     InVec<In, VW> v[RPL];
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
-      if (k * GPW + grp < n) v[k].load(rs, vin, k * kStepIn);
-      else v[k].set_neg_inf();
+      v[k].load_or_neg_inf(k * GPW + grp < n, rs, vin, k * kStepIn);
     }
     Top2 p[RPL];
 #pragma unroll

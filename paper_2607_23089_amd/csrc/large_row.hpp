@@ -73,10 +73,8 @@ __device__ __forceinline__ MaxSum large_pass1(rsrc_t rx, int g, int RT, int nvec
       for (int u = 0; u < U; ++u) {
         const int j = (tt * U + u) * RT;      // first vector of this slot
         const int idx = j + g;
-        if (idx < nvec && (!FUSED || idx * VW <= lim))
-          v[u].load(rx, vin, (uint32_t)j * (VW * In::bytes));
-        else
-          v[u].set_neg_inf();
+        v[u].load_or_neg_inf(idx < nvec && (!FUSED || idx * VW <= lim), rx, vin,
+                             (uint32_t)j * (VW * In::bytes));
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -267,10 +265,8 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
       for (int u = 0; u < U; ++u) {
         const int j = (tt * U + u) * RT;
         const int idx = j + g;
-        if (idx < nvec && (!FUSED || idx * VW <= lim))
-          v[u].load(rx, vin, (uint32_t)j * (VW * In::bytes));
-        else
-          v[u].set_neg_inf();
+        v[u].load_or_neg_inf(idx < nvec && (!FUSED || idx * VW <= lim), rx, vin,
+                             (uint32_t)j * (VW * In::bytes));
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {

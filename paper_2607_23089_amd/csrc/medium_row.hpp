@@ -87,8 +87,7 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
       InVec<In, VW> v[NV];
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
-        if (row_ok && (s < NV - 1 || last_ok)) v[s].load(rx, vin, s * sin);
-        else v[s].set_neg_inf();
+        v[s].load_or_neg_inf(row_ok && (s < NV - 1 || last_ok), rx, vin, s * sin);
       }
       float mx = -__builtin_inff();
 #pragma unroll
@@ -126,10 +125,9 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
         InVec<In, VW> v[NV];
 #pragma unroll
         for (int s = 0; s < NV; ++s) {
-          if (row_ok && (s < NV - 1 || last_ok) && (!FUSED || (s * T + t) * VW <= lim))
-            v[s].load(rx, vin, s * sin);
-          else
-            v[s].set_neg_inf();
+          v[s].load_or_neg_inf(
+              row_ok && (s < NV - 1 || last_ok) && (!FUSED || (s * T + t) * VW <= lim), rx, vin,
+              s * sin);
         }
 #pragma unroll
         for (int s = 0; s < NV; ++s) {

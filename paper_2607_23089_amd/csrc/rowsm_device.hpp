@@ -89,6 +89,9 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
                                            kBufDword3);
 }
 
+// A buffer offset past the end of every descriptor of up to 2 GiB.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
 template <int BYTES>
 __device__ __forceinline__ typename raw_of<BYTES>::type buf_load(rsrc_t r, uint32_t voff,
                                                                   uint32_t soff) {
@@ -120,6 +123,23 @@ struct InVec {
 
   __device__ __forceinline__ void load(rsrc_t rs, uint32_t voff, uint32_t soff) {
     r = buf_load<BYTES>(rs, voff, soff);
+  }
+  // The vector where ok holds, else -inf.  A 2-byte vector (one bf16) is
+  // loaded whatever ok says, from an offset past the descriptor's end where
+  // ok fails (out of range: the load reads nothing and returns 0), and the
+  // result selected afterwards: inside a branch the compiler widens each such
+  // value in the branch and waits for every load before issuing the next,
+  // one memory round trip per slot.  Where ok fails the caller's offsets may
+  // also fall inside the descriptor (readable memory); nothing else is read.
+  __device__ __forceinline__ void load_or_neg_inf(bool ok, rsrc_t rs, uint32_t voff,
+                                                  uint32_t soff) {
+    if constexpr (BYTES == 2) {
+      const R t = buf_load<2>(rs, ok ? voff : kOutOfRange, soff);
+      r = ok ? t : (R)0xff80u;
+    } else {
+      if (ok) load(rs, voff, soff);
+      else set_neg_inf();
+    }
   }
   __device__ __forceinline__ void set_neg_inf() {
     if constexpr (BYTES == 2) {

@@ -59,8 +59,7 @@ __global__ __launch_bounds__(256) void small_row_kernel(
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
       const bool ok = col_ok && (k * RPW + grp < nrows) && (!FUSED || sub * VW <= lim[k]);
-      if (ok) v[k].load(rx, vin, k * group_elts * In::bytes);
-      else v[k].set_neg_inf();
+      v[k].load_or_neg_inf(ok, rx, vin, k * group_elts * In::bytes);
     }
 
     float f[RPL][VW];

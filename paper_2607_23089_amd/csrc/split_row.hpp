@@ -128,10 +128,8 @@ __device__ __forceinline__ void split_load_share(InVec<In, VW> (&v)[NV], rsrc_t 
                                                  int lim) {
 #pragma unroll
   for (int s = 0; s < NV; ++s) {
-    if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim))
-      v[s].load(rx, vin, s * sin);
-    else
-      v[s].set_neg_inf();
+    v[s].load_or_neg_inf((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim), rx,
+                         vin, s * sin);
   }
 }
 
@@ -141,10 +139,8 @@ template <typename In, int VW, int NV, bool FUSED>
 __device__ __forceinline__ void split_slot_values(float (&f)[VW], rsrc_t rx, int s, int RT, int g,
                                                   bool last_ok, int lim, float scale) {
   InVec<In, VW> v;
-  if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim))
-    v.load(rx, (uint32_t)g * (VW * In::bytes), (uint32_t)(s * RT) * (VW * In::bytes));
-  else
-    v.set_neg_inf();
+  v.load_or_neg_inf((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim), rx,
+                    (uint32_t)g * (VW * In::bytes), (uint32_t)(s * RT) * (VW * In::bytes));
   v.to_float(f);
   if constexpr (FUSED) fused_apply(f, (s * RT + g) * VW, lim, scale);
 }

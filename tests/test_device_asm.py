@@ -136,3 +136,48 @@ def test_stream_cache_policy(asm):
         [st for st in stores if not re.search(r" nt sc1$", st)][:3]
     assert all(re.search(r" nt$", ld) for ld in loads), \
         [ld for ld in loads if not re.search(r" nt$", ld)][:3]
+
+
+def kernel_bodies(asm):
+    return {m.group(1): m.group(2) for m in
+            re.finditer(r"^(_ZN5rowsm\S*):[^\n]*\n(.*?)\.Lfunc_end", asm, re.S | re.M)}
+
+
+def serialised_loads(body):
+    """Row loads followed by a wait for every load in flight before the next
+    row load is issued, and the number of row loads."""
+    lines = [ln.strip() for ln in body.splitlines()]
+    loads = serial = 0
+    for i, ln in enumerate(lines):
+        if ln.startswith("buffer_load"):
+            loads += 1
+            for nxt in lines[i + 1:i + 12]:
+                if nxt.startswith("buffer_load"):
+                    break
+                if nxt.startswith("s_waitcnt") and "vmcnt(0)" in nxt:
+                    serial += 1
+                    break
+    return serial, loads
+
+
+def test_one_element_bf16_loads_stay_in_flight_together(asm):
+    # rows of bf16 that take one-element (2-byte) vectors: the per-slot
+    # loads of the medium, small, single-read and MoE kernels are all issued
+    # before the first wait, not one memory round trip per slot (a load in a
+    # branch had its widening sunk into the branch, with a wait for each)
+    # (kernels with at least 4 slots: NV of the medium and single-read
+    # forms, row groups per lane of the small and MoE forms)
+    bodies = kernel_bodies(asm)
+    checked = 0
+    for n, body in bodies.items():
+        m = re.match(r"_ZN5rowsm(17medium_row|16split_row|16small_row|17group_top2)_kernelINS_4BF16E"
+                     r"(?:NS_3F32E|S1_)Li1ELi(\d+)E(?:Li(\d+)E)?", n)
+        if not m:
+            continue
+        slots = int(m.group(2) if m.group(1) in ("17medium_row", "16split_row") else m.group(3))
+        if slots < 4:
+            continue
+        serial, loads = serialised_loads(body)
+        checked += 1
+        assert serial <= loads // 2, (n, serial, loads)
+    assert checked > 100, checked
