@@ -85,7 +85,8 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Grid-stride loops over a capped grid measured 4-8% slower at 1-4 M rows
 // (and slower still in plain store streams): waves that drift apart spread
 // the addresses in flight over the whole buffer, while the in-order blocks
-// of an uncapped grid keep them in one moving window.
+// of an uncapped grid keep them in one moving window.  (Medium rows of one
+// wave and at most 8 input bytes per lane are the exception, in plan_for().)
 int64_t grid_cap(int bpc, int cus) {
   return bpc ? (int64_t)cus * bpc : ((int64_t)1 << 30);
 }
@@ -571,6 +572,24 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->block = rpb * wpr * kWave;
     p->grid = cdiv(rows, rpb);
     if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+    // One wave per row holding at most 8 input bytes per lane (one slot, or
+    // two slots of one or two elements), softmax and log forms, nothing
+    // about the shape or grid given: one residency of 4 blocks per compute
+    // unit (2048 threads) whose waves loop over the rows, instead of a block
+    // per 8 such short rows.  Sweeps of 33-128-vector rows (one-element,
+    // two-element and full vectors, every dtype pair, 32-800 MiB, each
+    // launch alone after a cache-evicting write): 3.0% above the fastest
+    // grid measured on geometric mean where a block per row group was 29%
+    // (at most 70%), and 2.7% against 21% (at most 19% against 46%) on 162
+    // launches of other lengths and sizes.  Two full 16-byte slots per lane
+    // measured faster with a block per row group, which they keep.
+    const int in_bytes_per_slot = vw * ib;
+    if (auto_variant && !fused && wpr == 1 && bpc == 0 &&
+        (p->vpl == 1 || (p->vpl == 2 && in_bytes_per_slot <= 4)) &&
+        (!cfg || (cfg->rows_per_block == 0 && cfg->block == 0 && cfg->waves_per_row == 0 &&
+                  cfg->vw == 0)) &&
+        p->grid > 4 * (int64_t)cus)
+      p->grid = 4 * (int64_t)cus;
     return ROWSM_OK;
   }
   if (variant == ROWSM_LARGE) {

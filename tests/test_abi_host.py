@@ -318,6 +318,22 @@ def test_describe(lib):
         st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16,
                                        R.RowsmConfig(blocks_per_cu=64))
         assert st == R.OK and "grid=16384 " in text, text
+    # one wave per row with at most 8 input bytes per lane: one residency of
+    # 4 blocks per compute unit; two full 16-byte slots keep a block per row
+    # group, and a grid cap given stays
+    for rows, cols, i, o in ((1000000, 37, R.F32, R.F32), (500000, 75, R.BF16, R.BF16),
+                             (500000, 256, R.F32, R.F32), (500000, 512, R.BF16, R.BF16)):
+        st, text = R.rowsm_describe(rows, cols, i, o)
+        assert st == R.OK and "wpr=1 " in text and "grid=1024 " in text, text
+    st, text = R.rowsm_describe(500000, 260, R.BF16, R.BF16)
+    assert st == R.OK and "nv=2 " in text and "grid=62500 " in text, text
+    st, text = R.rowsm_describe(500000, 151, R.F32, R.F32)              # three slots
+    assert st == R.OK and "nv=3 " in text and "grid=62500 " in text, text
+    st, text = R.rowsm_describe_op(R.OP_SOFTMAX, 1000000, 37, R.F32, R.F32,
+                                   R.RowsmConfig(blocks_per_cu=16))
+    assert st == R.OK and "grid=4096 " in text, text
+    st, text = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 1000000, 37, R.F32, R.F32)
+    assert st == R.OK and "grid=250000 " in text, text                    # fused: unchanged
     # 512 threads would leave fewer than 8 blocks to the row: 256
     st, text = R.rowsm_describe(1024, 131072, R.F32, R.F32)
     assert st == R.OK and "split=8" in text and "block=256" in text
