@@ -582,14 +582,25 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // grid measured on geometric mean where a block per row group was 29%
     // (at most 70%), and 2.7% against 21% (at most 19% against 46%) on 162
     // launches of other lengths and sizes.  Two full 16-byte slots per lane
-    // measured faster with a block per row group, which they keep.
+    // measured faster with a block per row group, which they keep.  Rows of
+    // one full 16-byte slot per lane in a dtype pair of one width that fill
+    // at least 65% of the wave's lanes (42-64 vectors) take one-wave blocks
+    // of one row instead, uncapped, as the small rows of one width do: 0-22%
+    // faster than the residency from 160 MiB on (e.g. 499321 x 168 fp32 and
+    // bf16 rows of 448 columns), up to 7% slower at 40 MiB; at lower fill
+    // the residency stays ahead.
     const int in_bytes_per_slot = vw * ib;
     if (auto_variant && !fused && wpr == 1 && bpc == 0 &&
-        (p->vpl == 1 || (p->vpl == 2 && in_bytes_per_slot <= 4)) &&
         (!cfg || (cfg->rows_per_block == 0 && cfg->block == 0 && cfg->waves_per_row == 0 &&
-                  cfg->vw == 0)) &&
-        p->grid > 4 * (int64_t)cus)
-      p->grid = 4 * (int64_t)cus;
+                  cfg->vw == 0))) {
+      if (p->vpl == 1 && ib == ob && in_bytes_per_slot == 16 && nvec * 100 >= 65 * kWave) {
+        p->block = kWave;
+        p->grid = rows < grid_cap(0, cus) ? rows : grid_cap(0, cus);
+      } else if ((p->vpl == 1 || (p->vpl == 2 && in_bytes_per_slot <= 4)) &&
+                 p->grid > 4 * (int64_t)cus) {
+        p->grid = 4 * (int64_t)cus;
+      }
+    }
     return ROWSM_OK;
   }
   if (variant == ROWSM_LARGE) {

@@ -319,12 +319,17 @@ def test_describe(lib):
                                        R.RowsmConfig(blocks_per_cu=64))
         assert st == R.OK and "grid=16384 " in text, text
     # one wave per row with at most 8 input bytes per lane: one residency of
-    # 4 blocks per compute unit; two full 16-byte slots keep a block per row
-    # group, and a grid cap given stays
+    # 4 blocks per compute unit; same-width rows of one full slot filling 65%
+    # of the wave or more: one-wave blocks of one row; two full 16-byte
+    # slots keep a block per row group, and a grid cap given stays
     for rows, cols, i, o in ((1000000, 37, R.F32, R.F32), (500000, 75, R.BF16, R.BF16),
-                             (500000, 256, R.F32, R.F32), (500000, 512, R.BF16, R.BF16)):
+                             (500000, 164, R.F32, R.F32), (500000, 256, R.F32, R.BF16)):
         st, text = R.rowsm_describe(rows, cols, i, o)
         assert st == R.OK and "wpr=1 " in text and "grid=1024 " in text, text
+    for rows, cols, i, o in ((500000, 168, R.F32, R.F32), (500000, 256, R.F32, R.F32),
+                             (500000, 512, R.BF16, R.BF16)):
+        st, text = R.rowsm_describe(rows, cols, i, o)
+        assert st == R.OK and "block=64 " in text and "grid=500000 " in text, text
     st, text = R.rowsm_describe(500000, 260, R.BF16, R.BF16)
     assert st == R.OK and "nv=2 " in text and "grid=62500 " in text, text
     st, text = R.rowsm_describe(500000, 151, R.F32, R.F32)              # three slots

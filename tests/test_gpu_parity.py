@@ -466,17 +466,24 @@ def test_few_rows_per_cu_shapes(rows, cols, din, dout, want):
     assert_parity(x[sample].cpu(), y[sample].cpu(), dout, f"{rows}x{cols} {din}->{dout} [{desc}]")
 
 
-@pytest.mark.parametrize("rows,cols,din,dout", [
-    (1000003, 37, "f32", "f32"), (700001, 37, "bf16", "bf16"), (500001, 75, "bf16", "f32"),
-    (600011, 101, "f32", "bf16"), (400009, 256, "f32", "f32"), (250001, 512, "bf16", "bf16")])
-def test_one_residency_short_rows(rows, cols, din, dout):
+@pytest.mark.parametrize("rows,cols,din,dout,want", [
+    (1000003, 37, "f32", "f32", ("block=512 ", "grid=1024 ")),
+    (700001, 37, "bf16", "bf16", ("block=512 ", "grid=1024 ")),
+    (500001, 75, "bf16", "f32", ("block=512 ", "grid=1024 ")),
+    (600011, 101, "f32", "bf16", ("block=512 ", "grid=1024 ")),
+    (500003, 144, "f32", "f32", ("block=512 ", "grid=1024 ")),
+    (400009, 256, "f32", "f32", ("block=64 ", "grid=400009 ")),
+    (250001, 512, "bf16", "bf16", ("block=64 ", "grid=250001 ")),
+    (300007, 168, "f32", "f32", ("block=64 ", "grid=300007 "))])
+def test_one_wave_short_rows(rows, cols, din, dout, want):
     # one wave per row with at most 8 input bytes per lane: the launcher's
     # one residency of 4 blocks per compute unit, whose waves loop over many
-    # rows each (ragged row counts); sampled rows, the last ones among them,
-    # against the oracle, every row's sum
+    # rows each; same-width rows of one full 16-byte slot filling most of the
+    # wave: one-wave blocks of one row (ragged row counts); sampled rows, the
+    # last ones among them, against the oracle, every row's sum
     st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
     assert st == R.OK and desc.startswith("medium") and "wpr=1 " in desc, desc
-    assert "block=512 " in desc and "grid=1024 " in desc, desc
+    assert all(w in desc for w in want), desc
     x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + cols, device=DEV)
     y = run(x, dout)
     sample = list(range(0, rows, 4999)) + list(range(rows - 7, rows))
