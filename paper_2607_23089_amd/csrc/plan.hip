@@ -535,21 +535,27 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->packed = false;
       }
     }
-    // A row that needs all 16 waves of a 1024-thread block goes to the
-    // single-read split form of 256-thread blocks once the launch has many
-    // rows: from 8 * cus rows, or from cus / 4 when a lane would hold 64 or
-    // more values (or the packed form); rows of at least 64 KiB of input,
-    // the range measured.  A sweep of 256-8192 rows x
-    // 16384-151936 columns in every dtype pair (launches timed alone after
-    // a cache-evicting write) measured the split form 5-31% faster there
-    // (and within 2% of the medium form below these row counts): the
+    // A row of at least 64 KiB of input that needs all 16 waves of a
+    // 1024-thread block goes to the single-read split form: from 8 * cus
+    // rows, or from cus / 4 rows when a lane would hold 64 or more values (or
+    // the packed form), with 256-thread blocks and the threads per row of
+    // the wide-row plan below (a sweep of 256-8192 rows x 16384-151936
+    // columns in every dtype pair: 5-31% faster than the medium form); and,
+    // with the register-cap plan, rows of 80 KiB or more at any other row
+    // count and shorter ones in launches of fewer than cus / 2 rows.  The
     // 16-wave blocks synchronise a whole compute unit's worth of waves at
-    // each reduction and leave at most two blocks per compute unit.
+    // each reduction and leave at most two blocks per compute unit.  Sweeps
+    // of 16-4096 rows of 64-240 KiB in every dtype pair (each launch alone
+    // after a cache-evicting write): 2.3% above the fastest shape measured on
+    // geometric mean, where the first two conditions alone were 11% (at most
+    // 2.07x, few rows); 2.0% at 95 launches of 72-192 KiB rows not used to
+    // set the bounds.  Rows of 64-80 KiB in launches of cus / 2 to 8 * cus
+    // rows stay in the medium form, up to 18% faster there.
+    const bool wide_plan =
+        rows >= 8 * (int64_t)cus || ((vpl * vw >= 64 || packed) && rows >= cus / 4);
     if (variant == ROWSM_MEDIUM && auto_variant && !fused && !inplace && p->wpr == 16 &&
-        cols * ib >= 65536 &&
-        (rows >= 8 * (int64_t)cus ||
-         ((vpl * vw >= 64 || packed) && rows >= cus / 4))) {
-      wide_row = true;
+        cols * ib >= 65536 && (wide_plan || rows < cus / 2 || cols * ib >= 81920)) {
+      wide_row = wide_plan;
       variant = ROWSM_LARGE;
       p->variant = variant;
       p->wpr = 1;

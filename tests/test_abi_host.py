@@ -134,14 +134,21 @@ def test_select_regimes(lib):
     assert d(100, 196616, R.BF16, R.BF16, R.MEDIUM)[0] == R.EINVAL
     assert s(100, 196616, R.BF16, R.BF16) == R.LARGE
     assert s(4096, 151936, R.BF16, R.F32) == R.LARGE
-    # rows that need all 16 waves of a block: the split form from 8 cus rows,
-    # from cus / 4 rows at 64 values per lane or packed (256 compute units)
-    assert s(2047, 32768, R.F32, R.F32) == R.MEDIUM       # 32 values per lane
+    # rows of at least 64 KiB that need all 16 waves of a block: the split
+    # form for rows of 80 KiB or more, shorter ones below cus / 2 or from
+    # 8 cus rows (256 compute units)
+    assert s(2047, 16384, R.F32, R.F32) == R.MEDIUM       # 64 KiB
+    assert s(128, 16384, R.F32, R.F32) == R.MEDIUM
+    assert s(127, 16384, R.F32, R.F32) == R.LARGE
+    assert s(2048, 16384, R.F32, R.F32) == R.LARGE
+    assert s(300, 32768, R.BF16, R.BF16) == R.MEDIUM      # 64 KiB
+    assert s(300, 40960, R.BF16, R.BF16) == R.LARGE       # 80 KiB
+    assert s(2047, 32768, R.F32, R.F32) == R.LARGE        # 128 KiB
     assert s(2048, 32768, R.F32, R.F32) == R.LARGE
     assert "split=4 " in d(2048, 32768, R.F32, R.F32)[1]     # ~128 bytes per lane
-    assert s(63, 65536, R.BF16, R.BF16) == R.MEDIUM       # 64 values per lane
-    assert s(64, 65536, R.BF16, R.BF16) == R.LARGE
     assert s(100, 151936, R.BF16, R.BF16) == R.LARGE      # packed
+    for rows, cols, dt in ((2047, 16384, R.F32), (300, 40960, R.BF16)):  # 16 waves
+        assert "wpr=16 " in d(rows, cols, dt, dt, R.MEDIUM)[1]
     # full launches (>= 32 rows per compute unit) of rows of 129-4096 full
     # vectors take the measured shapes: two vectors per lane in the medium
     # form, the single-read form with 512 threads per row beyond
@@ -225,7 +232,8 @@ def test_select_regimes(lib):
     assert s(63, 65536, R.F32, R.F32) == R.LARGE
     assert s(64, 65536, R.F32, R.F32) == R.LARGE          # and 64 values per lane
     assert s(64, 151936, R.BF16, R.BF16) == R.LARGE
-    assert s(8, 32768, R.F32, R.F32) == R.MEDIUM          # 256 KiB rows
+    assert s(8, 32768, R.F32, R.F32) == R.LARGE           # 128 KiB rows, few: split
+    assert s(8, 8192, R.F32, R.F32) == R.MEDIUM           # 32 KiB rows
     assert s(1024, 262144, R.F32, R.F32) == R.LARGE
     assert s(0, 5, R.F32, R.F32) > 0
     assert s(5, 5, 3, R.F32) == R.EDTYPE
