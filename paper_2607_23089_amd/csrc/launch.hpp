@@ -37,6 +37,9 @@ struct Plan {
   int split = 0;    // blocks per row of the single-read form; 0 = two-pass form
   int stream = 1;   // two-pass form: blocks per row (1: one block per row)
   bool prefetch = false;  // single-read form: load the next row during the exchange
+  // MEDIUM: a row width that is not a multiple of vw, read in whole vectors
+  // aligned to the tensor with element-wise row edges (ragged_row.hpp)
+  bool ragged = false;
   // launch
   int block = 256;
   int64_t grid = 1;  // split form: 0 = one group per row, < 0 = minus the blocks-per-CU cap
@@ -93,6 +96,7 @@ template <int MODE> int launch_small(const Call& c, int in_dt, int out_dt);
 template <int MODE> int launch_medium(const Call& c, int in_dt, int out_dt);
 template <int MODE> int launch_large(const Call& c, int in_dt, int out_dt);
 template <int MODE> int launch_split(const Call& c, int in_dt, int out_dt);
+template <int MODE> int launch_ragged(const Call& c, int in_dt, int out_dt);
 
 // Softmax-backward launchers (launch_bwd_<family>.hip).
 int launch_bwd_small(const Call& c, int in_dt, int out_dt);

@@ -330,7 +330,50 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   const bool fused = mode == kFused;
   const int ib = dtype_bytes(in_dt), ob = dtype_bytes(out_dt);
   int vw = choose_vw(cols, ib, ob, xa, ya);
-  if (cfg && cfg->vw > 0) {
+  // Ragged rows (ragged_row.hpp): a width that is not a multiple of the full
+  // 16-byte vector width, with both tensors aligned to it, softmax and log
+  // forms.  Taken when cfg->vw asks for the full width (with the medium
+  // variant or none), and by the launcher for rows that span at least a
+  // wave of vectors and fit one block's registers, unless few long rows
+  // would leave the device idle; otherwise such rows use narrower vectors.
+  const int vw_full = 16 / (ib > ob ? ib : ob);
+  const bool ragged_ok = !fused && cols % vw_full != 0 && vw_supported(vw_full, ib) &&
+                         xa % (uintptr_t)(vw_full * ib) == 0 &&
+                         ya % (uintptr_t)(vw_full * ob < 16 ? vw_full * ob : 16) == 0;
+  const int64_t ragged_span = cdiv(cols + vw_full - 1, vw_full);  // longest row span
+  // values per lane of the ragged kernels (ragged_cap(); more spill)
+  const int ragged_vals = ib == 2 && ob == 4 ? 36 : 40;
+  const int64_t ragged_max_span = 16 * (int64_t)kWave * (ragged_vals / vw_full);
+  bool ragged = false;
+  if (ragged_ok && cfg && cfg->vw == vw_full) {
+    if (cfg->variant != ROWSM_AUTO && cfg->variant != ROWSM_MEDIUM) return ROWSM_EINVAL;
+    if (ragged_span > ragged_max_span) return ROWSM_EINVAL;
+    ragged = true;
+  } else if (ragged_ok && (!cfg || (cfg->variant == ROWSM_AUTO && cfg->vw == 0 &&
+                                    cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
+                                    cfg->block == 0 && cfg->split_blocks == 0 &&
+                                    cfg->packed != 1))) {
+    // (rows whose narrow-vector plan spreads them over several blocks each,
+    // too long for one block or few and long, keep it below cus rows: the
+    // ragged form has one block per row)
+    const int64_t narrow_nvec = cols / vw;
+    const bool narrow_medium =
+        narrow_nvec <= 16 * kWave * (64 / vw < 16 ? 64 / vw : 16) &&
+        (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus));
+    // Spans of 256-8192 vectors (4-128 KiB of 16-byte vectors): sweeps of
+    // 301-50257-column rows in every dtype pair (96 and 512 MiB launches,
+    // each alone after a cache-evicting write) measured the ragged form
+    // 0.6-0.9x the narrow-vector time there; shorter rows spend too much on
+    // their edges (up to 1.45x slower), and rows of 12565 vectors, which take
+    // 16 waves of 13 slots, ran 3-30% slower than the narrow single-read form.
+    ragged = ragged_span >= 4 * kWave && ragged_span <= 16 * kWave * 8 &&
+             ragged_span <= ragged_max_span &&
+             (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus)) &&
+             (narrow_medium || rows >= cus);
+  }
+  if (ragged) {
+    vw = vw_full;
+  } else if (cfg && cfg->vw > 0) {
     const int want = cfg->vw;
     if (want > 16 / (ib > ob ? ib : ob) || (want & (want - 1)) || !vw_supported(want, ib) ||
         cols % want ||
@@ -338,12 +381,14 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
       return ROWSM_EINVAL;
     vw = want;
   }
-  const int nvec = (int)(cols / vw);
+  const int nvec = ragged ? (int)ragged_span : (int)(cols / vw);
   p->vw = vw;
   p->nvec = nvec;
+  p->ragged = ragged;
 
   int variant = cfg ? cfg->variant : ROWSM_AUTO;
-  const bool auto_variant = variant == ROWSM_AUTO;
+  if (ragged) variant = ROWSM_MEDIUM;
+  const bool auto_variant = (cfg ? cfg->variant : ROWSM_AUTO) == ROWSM_AUTO;
   bool wide_row = false;  // a MEDIUM row redirected to the split form
   RowShape shape;         // measured_row_shape() pick, when it applies
   if (variant == ROWSM_AUTO) {
@@ -410,7 +455,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     bool packed = false;
     const int want_wpr = (cfg && cfg->waves_per_row > 0) ? cfg->waves_per_row : 0;
     const int want_packed = fused ? 0 : (cfg ? cfg->packed : -1);
-    if (fused && cfg && cfg->packed == 1) return ROWSM_EINVAL;
+    if ((fused || ragged) && cfg && cfg->packed == 1) return ROWSM_EINVAL;
     if (want_wpr && (want_wpr & (want_wpr - 1) || want_wpr > 16)) return ROWSM_EINVAL;
     // Unpacked: the smallest group whose lanes hold <= 16 fp32 values each
     // (<= 32, then <= 64 when the row is longer), unless a group size is
@@ -433,7 +478,26 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         if (wpr) break;
       }
     }
-    if (!wpr && want_packed != 0 && in_dt == ROWSM_BF16 && vw == 8) {
+    // Ragged rows: the fewest waves whose lanes hold at most 40 values each
+    // (36 for bf16 -> fp32, the most their kernels hold without spilling),
+    // or the wave count given if its lanes stay within that.  Over the sweep
+    // above: 3.1% above the fastest wave count and rows per block measured
+    // on geometric mean, where the 16-value rule took 15% and the
+    // narrow-vector plan 20%.
+    if (ragged) {
+      wpr = 0;
+      for (int w = 1; w <= 16; w <<= 1) {
+        if (want_wpr && w != want_wpr) continue;
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v * vw <= ragged_vals) {
+          wpr = w;
+          vpl = v;
+          break;
+        }
+      }
+      if (!wpr) return ROWSM_EINVAL;
+    }
+    if (!wpr && !ragged && want_packed != 0 && in_dt == ROWSM_BF16 && vw == 8) {
       for (int w = 1; w <= 16; w <<= 1) {
         if (want_wpr && w != want_wpr) continue;
         const int v = (int)cdiv(nvec, (int64_t)w * kWave);
@@ -465,7 +529,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     const bool shape_free = !cfg || (cfg->waves_per_row == 0 && cfg->rows_per_block == 0 &&
                                      cfg->packed == -1 && cfg->block == 0 &&
                                      cfg->split_blocks == 0 && cfg->vw == 0);
-    const bool full_vw = vw * (ib > ob ? ib : ob) == 16;
+    // (rows of whole full-width vectors; the ragged form keeps the base rule)
+    const bool full_vw = vw * (ib > ob ? ib : ob) == 16 && !ragged;
     if (auto_variant && !fused && shape_free && full_vw && rows >= 4 * (int64_t)cus &&
         rows < 16 * (int64_t)cus && cols * ib < 65536) {
       int target = 1;
@@ -553,8 +618,9 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // rows stay in the medium form, up to 18% faster there.
     const bool wide_plan =
         rows >= 8 * (int64_t)cus || ((vpl * vw >= 64 || packed) && rows >= cus / 4);
-    if (variant == ROWSM_MEDIUM && auto_variant && !fused && !inplace && p->wpr == 16 &&
-        cols * ib >= 65536 && (wide_plan || rows < cus / 2 || cols * ib >= 81920)) {
+    if (variant == ROWSM_MEDIUM && auto_variant && !fused && !inplace && !ragged &&
+        p->wpr == 16 && cols * ib >= 65536 &&
+        (wide_plan || rows < cus / 2 || cols * ib >= 81920)) {
       wide_row = wide_plan;
       variant = ROWSM_LARGE;
       p->variant = variant;
@@ -596,7 +662,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // bf16 rows of 448 columns), up to 7% slower at 40 MiB; at lower fill
     // the residency stays ahead.
     const int in_bytes_per_slot = vw * ib;
-    if (auto_variant && !fused && wpr == 1 && bpc == 0 &&
+    if (auto_variant && !fused && !ragged && wpr == 1 && bpc == 0 &&
         (!cfg || (cfg->rows_per_block == 0 && cfg->block == 0 && cfg->waves_per_row == 0 &&
                   cfg->vw == 0))) {
       if (p->vpl == 1 && ib == ob && in_bytes_per_slot == 16 && nvec * 100 >= 65 * kWave) {

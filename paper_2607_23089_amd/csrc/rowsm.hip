@@ -23,7 +23,11 @@ template <int MODE>
 int launch_mode(const Call& c, int in_dt, int out_dt) {
   switch (c.p.variant) {
     case ROWSM_SMALL: return launch_small<MODE>(c, in_dt, out_dt);
-    case ROWSM_MEDIUM: return launch_medium<MODE>(c, in_dt, out_dt);
+    case ROWSM_MEDIUM:
+      if constexpr (MODE == kPlain || MODE == kLog) {
+        if (c.p.ragged) return launch_ragged<MODE>(c, in_dt, out_dt);
+      }
+      return c.p.ragged ? ROWSM_EINVAL : launch_medium<MODE>(c, in_dt, out_dt);
     case ROWSM_LARGE:
       return c.p.split > 0 ? launch_split<MODE>(c, in_dt, out_dt)
                            : launch_large<MODE>(c, in_dt, out_dt);
@@ -305,10 +309,10 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
       }
       std::snprintf(buf, (size_t)len,
                     "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
-                    "split=%d stream=%d prefetch=%d block=%d grid=%lld (%s)",
+                    "split=%d stream=%d prefetch=%d ragged=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
                     (int)p.packed, p.u, p.split, p.variant == ROWSM_LARGE && !p.split ? p.stream : 0,
-                    (int)p.prefetch, p.block, (long long)grid, how);
+                    (int)p.prefetch, (int)p.ragged, p.block, (long long)grid, how);
     }
   }
   return st;

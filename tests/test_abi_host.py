@@ -192,7 +192,7 @@ def test_select_regimes(lib):
     # shapes or the fused form
     assert has(d(8191, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")
     assert has(d(8192, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
-    assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=2 ")
+    assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=4 ", "ragged=1 ")  # ragged
     t = R.rowsm_describe_op(R.OP_SOFTMAX, 100000, 8192, R.F32, R.F32,
                             R.RowsmConfig(waves_per_row=8))[1]
     assert has(t, "medium", "wpr=8 ", "vpl=4 ")
