@@ -894,12 +894,18 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       }
     }
     // A row that needs all 16 waves of a 1024-thread block goes to the
-    // split form from 4 * cus rows when it holds at least 64 KiB of each
-    // input (measured 4-20% faster there at 16384-65536 columns in every
+    // split form when it holds at least 64 KiB of each input, from 4 * cus
+    // rows (measured 4-20% faster there at 16384-65536 columns in every
     // dtype pair, and within 1% of the medium form at 256-512 rows; the
-    // forward's reason).
+    // forward's reason) and in launches of fewer than cus / 2 rows, where
+    // the split form's blocks spread a row over more compute units (16-48
+    // rows of 64-96 KiB: 10-43% faster; at cus / 2 rows the medium form is
+    // up to 20% ahead).  Sweeps of 16-1536 rows of 64-160 KiB in every dtype
+    // pair, each launch alone after a cache-evicting write: 3.7% above the
+    // fastest shape measured on geometric mean, where the first bound alone
+    // was 10.5%.
     if (shape.S > 0 || (auto_variant && !inplace && wpr == 16 && cols * ib >= 65536 &&
-                        rows >= 4 * (int64_t)cus)) {
+                        (rows >= 4 * (int64_t)cus || rows < cus / 2))) {
       variant = ROWSM_LARGE;
       p->variant = variant;
     } else {
@@ -914,6 +920,19 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       p->block = rpb * wpr * kWave;
       p->grid = cdiv(rows, rpb);
       if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+      // One wave per row holding at most 8 bytes of each input per lane,
+      // the row filling at most 3/4 of the wave's slots, nothing about the
+      // shape or grid given: one residency of 4 blocks per compute unit
+      // whose waves loop over the rows (the forward's short-row rule, with a
+      // bound on the fill: at 93% fill the block per row group stays up to
+      // 30% faster).  Sweeps of 41-182-vector rows (one- and two-element and
+      // full vectors, every dtype pair, 48-300 MiB of the three streams,
+      // each launch alone after a cache-evicting write): 2.2% above the
+      // fastest grid measured on geometric mean, where a block per row group
+      // was 13% (at most 61%), and never more than 3% slower than it.
+      if (auto_variant && shape_free && bpc == 0 && wpr == 1 && nv * vbytes <= 8 &&
+          nvec * 4 <= 3 * kWave * nv && p->grid > 4 * (int64_t)cus)
+        p->grid = 4 * (int64_t)cus;
       return ROWSM_OK;
     }
   }

@@ -427,14 +427,36 @@ def test_backward_plans(lib):
     st, t = d(32768, 4096, R.BF16, R.BF16, rows_per_block=2)
     assert st == R.OK and "wpr=4 " in t and "nv=2 " in t and "block=512" in t, t
     # medium holds at most 128 bytes of each input per lane: 16 x 64 x 8 vectors
-    assert d(100, 65536, R.BF16, R.BF16)[1].startswith("medium")
-    assert d(100, 65544, R.BF16, R.BF16)[1].startswith("large")
-    assert d(100, 32768, R.F32, R.F32)[1].startswith("medium")
+    assert d(200, 65536, R.BF16, R.BF16)[1].startswith("medium")
+    assert d(200, 65544, R.BF16, R.BF16)[1].startswith("large")
+    assert d(200, 32768, R.F32, R.F32)[1].startswith("medium")
+    # 16-wave rows of at least 64 KiB of each input in launches of fewer than
+    # cus / 2 rows: the split form; from cus / 2 rows the medium form
+    st, t = d(127, 16384, R.F32, R.F32)
+    assert st == R.OK and t.startswith("large") and "split=8 " in t and "block=256" in t, t
+    st, t = d(128, 16384, R.F32, R.F32)
+    assert st == R.OK and t.startswith("medium") and "wpr=16 " in t, t
+    assert d(127, 16380, R.F32, R.F32)[1].startswith("medium")     # under 64 KiB
+    st, t = d(100, 65536, R.BF16, R.BF16, variant=R.MEDIUM)        # asked for
+    assert st == R.OK and t.startswith("medium") and "wpr=16 " in t, t
+    # one-wave rows of at most 8 bytes of each input per lane filling at most
+    # 3/4 of the wave's slots: one residency of 4 blocks per compute unit
+    cap = lambda rows, cols, dt, **cfg: int(d(rows, cols, dt, dt, **cfg)[1].split("grid=")[1].split()[0])
+    assert cap(204600, 41, R.BF16) == 1024                        # 41 one-element vectors
+    assert cap(291271, 90, R.F32) == 1024                         # 45 two-element vectors
+    assert cap(582542, 90, R.BF16) == 1024                        # 2 x 1 element, 70%
+    assert cap(220289, 119, R.F32) == 27537                       # 93% of the slots
+    assert cap(163840, 320, R.BF16) == 20480                      # 16-byte vectors
+    assert cap(288070, 182, R.BF16) == 36009                      # three slots
+    assert cap(4000, 41, R.BF16) == 500                           # under the cap
+    assert cap(204600, 41, R.BF16, blocks_per_cu=8) == 2048       # grid given
+    assert cap(204600, 41, R.BF16, rows_per_block=4) == 51150     # shape given
     # few long rows (>= 512 KiB of y, dy and dx per row): the split form,
     # about one block per compute unit
     st, t = d(8, 65536, R.F32, R.F32)
     assert st == R.OK and t.startswith("large") and "split=32" in t
-    assert d(4, 65536, R.BF16, R.BF16)[1].startswith("medium")    # 384 KiB rows
+    st, t = d(4, 65536, R.BF16, R.BF16)                            # 384 KiB rows: the
+    assert st == R.OK and t.startswith("large") and "split=16 " in t  # 16-wave redirect
     st, t = d(32, 151936, R.BF16, R.BF16)                          # register cap: 16
     assert st == R.OK and "split=16" in t and "nv=5" in t
     st, t = d(1024, 262144, R.F32, R.F32)

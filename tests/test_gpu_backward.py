@@ -199,16 +199,38 @@ def test_bwd_small_one_wave_blocks(rows, cols, din, dout):
 
 @pytest.mark.parametrize("rows,cols,din,dout", [
     (1024, 16384, "f32", "f32"), (1024, 32768, "bf16", "f32"), (1024, 32768, "bf16", "bf16"),
-    (300, 65536, "f32", "f32")])
+    (300, 65536, "f32", "f32"), (16, 16384, "f32", "f32"), (48, 49152, "bf16", "f32"),
+    (127, 32768, "bf16", "bf16"), (100, 16384, "f32", "bf16")])
 def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
-    # rows that would need all 16 waves of one block, many rows: the split
-    # form with 2048-4096 threads per row (the launcher's own choice)
+    # rows that would need all 16 waves of one block, many rows or fewer
+    # than cus / 2: the split form (the launcher's own choice)
     st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
                                    R.dtype_code(DT[dout]))
     assert st == R.OK and desc.startswith("large") and "split=0" not in desc, desc
     y, dy = inputs(rows, cols, din, alpha=0.1, seed=rows + cols)
     dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
     assert_bwd_parity(y, dy, dx, dout, f"bwd wide rows {rows}x{cols} {din}->{dout} [{desc}]")
+
+
+@pytest.mark.parametrize("rows,cols,din,dout", [
+    (204600, 41, "bf16", "bf16"), (153450, 41, "bf16", "f32"), (122760, 41, "f32", "bf16"),
+    (291271, 90, "f32", "f32"), (582542, 90, "bf16", "bf16"), (81707, 77, "bf16", "f32")])
+def test_bwd_short_rows_one_residency(rows, cols, din, dout):
+    # one-wave rows of at most 8 bytes of each input per lane filling at most
+    # 3/4 of the wave: a grid of 4 blocks per compute unit whose waves loop
+    # over the rows; the output prefilled with NaN so that every row is seen
+    # written, sampled rows (the last ones among them) against the oracle
+    st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
+                                   R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("medium") and "wpr=1 " in desc, desc
+    assert "block=512 grid=1024 " in desc, desc
+    y, dy = inputs(rows, cols, din, alpha=0.3, seed=rows)
+    out = torch.full((rows, cols), float("nan"), dtype=DT[dout], device=DEV)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), dout, out=out)
+    assert bool(torch.isfinite(dx).all())
+    sample = list(range(0, rows, 991)) + list(range(rows - 9, rows))
+    assert_bwd_parity(y[sample], dy[sample], dx[sample].cpu(), dout,
+                      f"bwd short {rows}x{cols} {din}->{dout} [{desc}]")
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
