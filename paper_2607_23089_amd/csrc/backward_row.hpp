@@ -58,6 +58,7 @@ __global__ __launch_bounds__(256) void bwd_small_kernel(
   constexpr int RPW = kWave / LPR;     // rows per wave per load instruction
   constexpr int RPT = RPW * RPL;       // rows per wave per task
   const int lane = threadIdx.x & (kWave - 1);
+  const bool wl = stores_whole_lines(dx, (int64_t)cols * Out::bytes);  // sc1 stores
   const int sub = lane % LPR;
   const int grp = lane / LPR;
   const int nvec = cols / VW;
@@ -105,7 +106,7 @@ __global__ __launch_bounds__(256) void bwd_small_kernel(
       float o[VW];
       grad_vec(a[k], b[k], d[k], o);
       if (col_ok && k * RPW + grp < nrows)
-        store_out<Out, VW>(rdx, vout + k * group_elts * Out::bytes, o);
+        store_out<Out, VW>(rdx, vout + k * group_elts * Out::bytes, o, wl);
     }
   }
 }
@@ -123,6 +124,7 @@ __global__ __launch_bounds__(1024) void bwd_medium_kernel(
   __shared__ float red[2][16];
 
   const int lane = threadIdx.x & (kWave - 1);
+  const bool wl = stores_whole_lines(dx, (int64_t)cols * Out::bytes);  // sc1 stores
   const int wave = wave_id();
   const int rpb = (blockDim.x / kWave) / wpr;
   const int g = wave / wpr;
@@ -169,7 +171,7 @@ __global__ __launch_bounds__(1024) void bwd_medium_kernel(
     for (int s = 0; s < NV; ++s) {
       float o[VW];
       grad_vec(a[s], b[s], d, o);
-      if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(rdx, vout + s * sout, o);
+      if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(rdx, vout + s * sout, o, wl);
     }
   }
 }
@@ -223,6 +225,7 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
 
   const int T = blockDim.x;
   const int lane = threadIdx.x & (kWave - 1);
+  const bool wl = stores_whole_lines(dx, (int64_t)cols * Out::bytes);  // sc1 stores
   const int wave = wave_id();
   const int nwaves = T / kWave;
   const int c = blockIdx.x % S;
@@ -318,7 +321,7 @@ __global__ __launch_bounds__(1024) void bwd_split_kernel(
     for (int s = 0; s < NV; ++s) {
       float o[VW];
       grad_vec(a[s], b[s], d, o);
-      if (s < NV - 1 || last_ok) store_out<Out, VW>(rdx, vout + s * sout, o);
+      if (s < NV - 1 || last_ok) store_out<Out, VW>(rdx, vout + s * sout, o, wl);
     }
   }
 }
@@ -383,6 +386,7 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
   const int T = blockDim.x;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
+  const bool wl = stores_whole_lines(dx, (int64_t)cols * Out::bytes);  // sc1 stores
   const int wave = wave_id();
   const int nwaves = T / kWave;
   const int c = blockIdx.x % S;
@@ -488,7 +492,7 @@ __global__ __launch_bounds__(1024) void bwd_large_kernel(
         float o[VW];
         grad_vec(a[u], b[u], d, o);
         if (j + g < nvec)
-          store_out<Out, VW>(rdx, vout + (uint32_t)j * (VW * Out::bytes), o);
+          store_out<Out, VW>(rdx, vout + (uint32_t)j * (VW * Out::bytes), o, wl);
       }
     }
     // Every wave has read red, bcast, missing_lanes and peer before the next

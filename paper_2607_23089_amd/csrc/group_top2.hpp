@@ -90,6 +90,8 @@ __global__ __launch_bounds__(256) void group_top2_kernel(
   constexpr int GPW = kWave / LPG;      // groups per wave per load instruction
   constexpr int GPT = GPW * RPL;        // groups per wave per task
   const int lane = threadIdx.x & (kWave - 1);
+  // (a task's GPT outputs play the part of a row for the store policy)
+  const bool wl = stores_whole_lines(o, (int64_t)GPT * Out::bytes);  // sc1 stores
   const int sub = lane % LPG;
   const int grp = lane / LPG;
   const uint32_t vin = (uint32_t)(grp * G + sub * VW) * In::bytes;
@@ -144,7 +146,7 @@ __global__ __launch_bounds__(256) void group_top2_kernel(
       }
       if (q < n) {
         const float o1[1] = {val};
-        store_out<Out, 1>(ro, (uint32_t)q * Out::bytes, o1);
+        store_out<Out, 1>(ro, (uint32_t)q * Out::bytes, o1, wl);
       }
     }
   }

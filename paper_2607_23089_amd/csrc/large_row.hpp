@@ -155,6 +155,7 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
   const int T = blockDim.x;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
+  const bool wl = stores_whole_lines(y, (int64_t)cols * Out::bytes);  // sc1 stores
   const int wave = wave_id();
   const int nwaves = T / kWave;
   const int c = blockIdx.x % S;                 // block of the row group
@@ -278,7 +279,7 @@ __global__ __launch_bounds__(1024) void large_row_kernel(
 #pragma unroll
         for (int i = 0; i < VW; ++i)
           o[i] = LOG ? (o[i] - ms.m) - lns : exp2_fast(__builtin_fmaf(o[i], kLog2e, nml)) * inv;
-        if (idx < nvec) store_out<Out, VW>(ry, vout + (uint32_t)j * (VW * Out::bytes), o);
+        if (idx < nvec) store_out<Out, VW>(ry, vout + (uint32_t)j * (VW * Out::bytes), o, wl);
       }
     }
     // Every wave has read red_m / red_s, bcast, missing_lanes and peer before

@@ -11,11 +11,11 @@
 
 namespace rowsm {
 
-// Values per lane of the ragged kernels: at most 40 (36 for bf16 -> fp32);
-// within the 1024-thread launch bound more than that spill.
+// Values per lane of the ragged kernels: at most 40 (about 100 VGPRs at the
+// cap, within the 1024-thread launch bound's 128).
 template <typename In, typename Out>
 constexpr int ragged_cap() {
-  return In::bytes == 2 && Out::bytes == 4 ? 36 : 40;
+  return 40;
 }
 
 template <typename In, typename Out, int VW, int NV, int MODE>

@@ -60,6 +60,7 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
   __shared__ float red_s[16];
 
   const int lane = threadIdx.x & (kWave - 1);
+  const bool wl = stores_whole_lines(y, (int64_t)cols * Out::bytes);  // sc1 stores
   const int wave = wave_id();
   const int rpb = (blockDim.x / kWave) / wpr;
   const int g = wave / wpr;
@@ -117,7 +118,7 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
         for (int i = 0; i < VW; ++i)
           o[i] = LOG ? (v[s].get(i) - mx) - lns
                      : exp2_fast(__builtin_fmaf(v[s].get(i), kLog2e, nml)) * inv;
-        if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(ry, vout + s * sout, o);
+        if (row_ok && (s < NV - 1 || last_ok)) store_out<Out, VW>(ry, vout + s * sout, o, wl);
       }
     } else {
       float f[NV][VW];
@@ -144,7 +145,7 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
 #pragma unroll
         for (int s = 0; s < NV; ++s)
           if (row_ok && (s < NV - 1 || last_ok) && (s * T + t) * VW > lim)
-            store_out<Out, VW>(ry, vout + s * sout, z);
+            store_out<Out, VW>(ry, vout + s * sout, z, wl);
       }
       float mx = -__builtin_inff();
 #pragma unroll
@@ -171,7 +172,7 @@ __global__ __launch_bounds__(1024) void medium_row_kernel(
         for (int i = 0; i < VW; ++i) f[s][i] = LOG ? (f[s][i] - mx) - lns : f[s][i] * inv;
         if (row_ok && (s < NV - 1 || last_ok) &&
             (!FUSED || (s * T + t) * VW <= lim || redo_masked))
-          store_out<Out, VW>(ry, vout + s * sout, f[s]);
+          store_out<Out, VW>(ry, vout + s * sout, f[s], wl);
       }
     }
   }

@@ -341,8 +341,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
                          xa % (uintptr_t)(vw_full * ib) == 0 &&
                          ya % (uintptr_t)(vw_full * ob < 16 ? vw_full * ob : 16) == 0;
   const int64_t ragged_span = cdiv(cols + vw_full - 1, vw_full);  // longest row span
-  // values per lane of the ragged kernels (ragged_cap(); more spill)
-  const int ragged_vals = ib == 2 && ob == 4 ? 36 : 40;
+  // values per lane of the ragged kernels (ragged_cap())
+  const int ragged_vals = 40;
   const int64_t ragged_max_span = 16 * (int64_t)kWave * (ragged_vals / vw_full);
   bool ragged = false;
   if (ragged_ok && cfg && cfg->vw == vw_full) {
@@ -478,8 +478,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         if (wpr) break;
       }
     }
-    // Ragged rows: the fewest waves whose lanes hold at most 40 values each
-    // (36 for bf16 -> fp32, the most their kernels hold without spilling),
+    // Ragged rows: the fewest waves whose lanes hold at most 40 values each,
     // or the wave count given if its lanes stay within that.  Over the sweep
     // above: 3.1% above the fastest wave count and rows per block measured
     // on geometric mean, where the 16-value rule took 15% and the
@@ -600,6 +599,28 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
         p->packed = false;
       }
     }
+    // Rows under 64 KiB of input that the 16-value rule puts on all 16 waves
+    // of a 1024-thread block, in launches that neither the measured shapes
+    // (from 32 * cus rows) nor the rule for 4-16 rows per compute unit
+    // cover: the fewest waves whose lanes hold at most 48 values (the
+    // 16-wave blocks synchronise a compute unit's worth of waves at each
+    // reduction).  A sweep of 1-32 rows per compute unit of 1024-40000
+    // columns in every dtype pair (each launch alone after a cache-evicting
+    // write): 3.1% above the fastest shape measured on geometric mean where
+    // the 16-wave rows took 4.8% (at most 33%: 6144 x 8240 bf16 -> fp32),
+    // no launch more than 3% slower.
+    if (variant == ROWSM_MEDIUM && auto_variant && !fused && shape_free && full_vw &&
+        p->wpr == 16 && !p->packed && rows < 32 * (int64_t)cus &&
+        !(rows >= 4 * (int64_t)cus && rows < 16 * (int64_t)cus) && cols * ib < 65536) {
+      for (int w = 1; w < 16; w <<= 1) {
+        const int v = (int)cdiv(nvec, (int64_t)w * kWave);
+        if (v * vw <= 48 && medium_unpacked_cap(vw, v)) {
+          p->wpr = w;
+          p->vpl = v;
+          break;
+        }
+      }
+    }
     // A row of at least 64 KiB of input that needs all 16 waves of a
     // 1024-thread block goes to the single-read split form: from 8 * cus
     // rows, or from cus / 4 rows when a lane would hold 64 or more values (or
@@ -637,6 +658,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     const int waves_per_block = fused ? 4 : 8;
     int rpb = wpr >= waves_per_block ? 1 : waves_per_block / wpr;
     if (shape.rpb > 0) rpb = shape.rpb;
+    // Ragged rows: one row per block.  Over the sweep of 1-32 rows per
+    // compute unit: 4.4% above the fastest shape measured on geometric mean
+    // where the blocks of 512 threads took 9.1%, none slower.
+    if (ragged) rpb = 1;
     if (cfg && cfg->rows_per_block > 0) {
       rpb = cfg->rows_per_block;
       if (rpb * wpr > 16) return ROWSM_EINVAL;

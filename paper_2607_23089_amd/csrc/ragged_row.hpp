@@ -5,10 +5,15 @@
 //
 // Row r starts h = (r * cols) mod VW elements past a vector boundary, so it
 // spans ceil((cols + h) / VW) vectors of that grid.  The descriptors of the
-// row are based at that boundary and end at the row's last element; vectors
-// wholly inside the row move as one load and one store, and the first and
-// last vectors, which share elements with the neighbouring rows, move one
-// element at a time (only the row's own elements are read or written).
+// row are based at that boundary.  Every vector the row touches is read as
+// one load, its first and last too: their other elements belong to the
+// neighbouring rows (inside the tensor) and are set to -inf once loaded, so
+// that every load of a row is in flight at once.  Only a last vector that
+// would reach past the end of the tensor (the final row's) is read element
+// by element.  Stores write vectors wholly inside the row as one store and
+// the row's own elements of the first and last vectors one at a time; rows
+// of such widths never start every row on a 128-byte line, so the stores
+// are non-temporal without the device-scope bit (kCpolStorePart).
 //
 // Layout and reductions are the medium kernel's (unpacked form): a row group
 // of WPR waves, lane t owns vectors t, t + T, ... of the row's span, NV slots
@@ -37,6 +42,7 @@ __global__ __launch_bounds__(1024) void ragged_row_kernel(const typename In::sto
   const int T = wpr * kWave;
   const int t = (wave - g * wpr) * kWave + lane;
   const float ninf = -__builtin_inff();
+  const int64_t total = rows * (int64_t)cols;        // elements of the tensor
 
   for (int64_t base = (int64_t)blockIdx.x * rpb; base < rows;
        base += (int64_t)gridDim.x * rpb) {
@@ -45,7 +51,16 @@ __global__ __launch_bounds__(1024) void ragged_row_kernel(const typename In::sto
     const int64_t e0 = (row_ok ? row : 0) * cols;   // first element of the row
     const int h = (int)(e0 & (VW - 1));              // its place in its vector
     const int span = cols + h;                       // elements from the boundary on
-    const rsrc_t rx = make_rsrc(x + (e0 - h), (uint64_t)span * In::bytes);
+    // The row's last vector: its index, owner (lane t1, slot s1) and the
+    // number of the row's elements in it (1..VW).
+    const int lv = (span - 1) / VW;
+    const int s1 = lv / T, t1 = lv - s1 * T;
+    const int rem = span - lv * VW;
+    // Elements the load descriptor covers: the row's vectors, cut at the end
+    // of the tensor (never shorter than span).
+    const int64_t room = total - (e0 - h);
+    const int lim = (int)((int64_t)(lv + 1) * VW < room ? (int64_t)(lv + 1) * VW : room);
+    const rsrc_t rx = make_rsrc(x + (e0 - h), (uint64_t)lim * In::bytes);
     const rsrc_t ry = make_rsrc(y + (e0 - h), (uint64_t)span * Out::bytes);
 
     float f[NV][VW];
@@ -54,22 +69,33 @@ __global__ __launch_bounds__(1024) void ragged_row_kernel(const typename In::sto
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
         const int first = (s * T + t) * VW;          // the vector's first element
-        const bool whole = row_ok && first >= h && first + VW <= span;
-        v[s].load_or_neg_inf(whole, rx, (uint32_t)first * In::bytes, 0);
+        const bool vec = row_ok && first < span && first + VW <= lim;
+        v[s].load_or_neg_inf(vec, rx, (uint32_t)first * In::bytes, 0);
       }
 #pragma unroll
       for (int s = 0; s < NV; ++s) v[s].to_float(f[s]);
-      // The row's first and last vectors, element by element.
+    }
+    // The neighbouring rows' elements of the first and last vectors to -inf;
+    // a last vector reaching past the end of the tensor was not loaded and
+    // is read element by element.
+    if (row_ok && t == 0) {
 #pragma unroll
-      for (int s = 0; s < NV; ++s) {
-        const int first = (s * T + t) * VW;
-        const bool edge = row_ok && first < span && !(first >= h && first + VW <= span);
-        if (edge) {
+      for (int k = 0; k < VW; ++k)
+        if (k < h) f[0][k] = ninf;
+    }
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      if (row_ok && s == s1 && t == t1) {
+        if ((lv + 1) * VW <= lim) {
+#pragma unroll
+          for (int k = 0; k < VW; ++k)
+            if (k >= rem) f[s][k] = ninf;
+        } else {
+          const int lo = lv == 0 ? h : 0;
 #pragma unroll
           for (int k = 0; k < VW; ++k) {
-            const int e = first + k;
             InVec<In, 1> u;
-            u.load_or_neg_inf(e >= h && e < span, rx, (uint32_t)e * In::bytes, 0);
+            u.load_or_neg_inf(k >= lo && k < rem, rx, (uint32_t)(lv * VW + k) * In::bytes, 0);
             f[s][k] = u.get(0);
           }
         }
@@ -97,16 +123,25 @@ __global__ __launch_bounds__(1024) void ragged_row_kernel(const typename In::sto
 #pragma unroll
       for (int i = 0; i < VW; ++i) f[s][i] = LOG ? (f[s][i] - mx) - lns : f[s][i] * inv;
       const int first = (s * T + t) * VW;
-      if (row_ok && first >= h && first + VW <= span) {
-        store_out<Out, VW>(ry, (uint32_t)first * Out::bytes, f[s]);
-      } else if (row_ok && first < span) {
+      if (row_ok && first >= h && first + VW <= span)
+        store_out<Out, VW>(ry, (uint32_t)first * Out::bytes, f[s], false);
+    }
+    // The row's own elements of a partial first vector (lane 0, slot 0;
+    // when the row has more than one vector) and of a partial last vector.
+    if (row_ok && t == 0 && h > 0 && lv > 0) {
 #pragma unroll
-        for (int k = 0; k < VW; ++k) {
-          const int e = first + k;
-          if (e >= h && e < span) {
-            const float o[1] = {f[s][k]};
-            store_out<Out, 1>(ry, (uint32_t)e * Out::bytes, o);
-          }
+      for (int k = 0; k < VW; ++k)
+        if (k >= h) store_out<Out, 1>(ry, (uint32_t)k * Out::bytes, {f[0][k]}, false);
+    }
+    if (row_ok && (rem < VW || (lv == 0 && h > 0))) {
+      const int lo = lv == 0 ? h : 0;
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        if (s == s1 && t == t1) {
+#pragma unroll
+          for (int k = 0; k < VW; ++k)
+            if (k >= lo && k < rem)
+              store_out<Out, 1>(ry, (uint32_t)(lv * VW + k) * Out::bytes, {f[s][k]}, false);
         }
       }
     }

@@ -74,12 +74,25 @@ __device__ __forceinline__ float exp2_fast(float t) {
 
 constexpr int32_t kBufDword3 = 0x00020000;  // gfx9-family raw buffer word 3
 // Cache policy bits (gfx950: bit 0 sc0, bit 1 nt, bit 4 sc1).  Loads are
-// non-temporal; stores non-temporal at device scope (sc1 nt), which wrote a
-// streaming copy 0.5-1.5% faster than nt alone, and every row regime's step
-// about 0.7% (same box, interleaved runs); plain loads halved the medium
-// kernel's rate.
+// non-temporal (plain loads halved the medium kernel's rate).  Stores are
+// non-temporal at device scope (sc1 nt) when every store of the launch covers
+// whole 128-byte lines: that wrote a streaming copy 0.5-1.5% faster than nt
+// alone and line-aligned rows 1-4% faster (262144 x 64 and 32768 x 4096
+// bf16).  Stores that cover part of a line are non-temporal alone: with sc1
+// they took up to 1.8x the launch time (12288 x 4004 fp32 rows 79.5 against
+// 65.0 us, one-element bf16 vectors 76 against 41 us, the single-lane edge
+// stores of ragged rows 57 against 38 us).
 constexpr int kCpolLoad = 2;
-constexpr int kCpolStore = 18;
+constexpr int kCpolStore = 18;      // sc1 nt
+constexpr int kCpolStorePart = 2;   // nt
+
+// Whether every store of a launch covers whole 128-byte lines: the output
+// starts on a line and each row is a whole number of lines, or a power-of-two
+// fraction of one (rows then pack lines whole).
+__device__ __forceinline__ bool stores_whole_lines(const void* y, int64_t row_bytes) {
+  return ((uintptr_t)y & 127) == 0 &&
+         ((row_bytes & 127) == 0 || (row_bytes > 0 && row_bytes < 128 && 128 % row_bytes == 0));
+}
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
@@ -101,13 +114,21 @@ __device__ __forceinline__ typename raw_of<BYTES>::type buf_load(rsrc_t r, uint3
   else return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, kCpolLoad);
 }
 
+template <int BYTES, int CPOL>
+__device__ __forceinline__ void buf_store_cpol(typename raw_of<BYTES>::type v, rsrc_t r,
+                                               uint32_t voff, uint32_t soff) {
+  if constexpr (BYTES == 16) __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, CPOL);
+  else if constexpr (BYTES == 8) __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, CPOL);
+  else if constexpr (BYTES == 4) __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, CPOL);
+  else __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, CPOL);
+}
+
+// sc1: the launch's stores cover whole lines (stores_whole_lines()).
 template <int BYTES>
 __device__ __forceinline__ void buf_store(typename raw_of<BYTES>::type v, rsrc_t r,
-                                          uint32_t voff, uint32_t soff) {
-  if constexpr (BYTES == 16) __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kCpolStore);
-  else if constexpr (BYTES == 8) __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, kCpolStore);
-  else if constexpr (BYTES == 4) __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, kCpolStore);
-  else __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, kCpolStore);
+                                          uint32_t voff, uint32_t soff, bool sc1) {
+  if (sc1) buf_store_cpol<BYTES, kCpolStore>(v, r, voff, soff);
+  else buf_store_cpol<BYTES, kCpolStorePart>(v, r, voff, soff);
 }
 
 __device__ __forceinline__ int wave_id() {
@@ -205,25 +226,26 @@ struct InVec {
 // write overtake the store's read of its data (seen as raw input values in
 // the output).  With a constant soffset the compiler inserts the wait states.
 template <typename Out, int VW>
-__device__ __forceinline__ void store_out(rsrc_t rs, uint32_t voff, const float (&f)[VW]) {
+__device__ __forceinline__ void store_out(rsrc_t rs, uint32_t voff, const float (&f)[VW],
+                                          bool sc1) {
   constexpr uint32_t soff = 0;
   if constexpr (Out::bytes == 4) {
     if constexpr (VW == 1) {
-      buf_store<4>(__float_as_uint(f[0]), rs, voff, soff);
+      buf_store<4>(__float_as_uint(f[0]), rs, voff, soff, sc1);
     } else if constexpr (VW == 2) {
       u32x2 v = {__float_as_uint(f[0]), __float_as_uint(f[1])};
-      buf_store<8>(v, rs, voff, soff);
+      buf_store<8>(v, rs, voff, soff, sc1);
     } else {
 #pragma unroll
       for (int c = 0; c < VW; c += 4) {
         u32x4 v = {__float_as_uint(f[c]), __float_as_uint(f[c + 1]),
                    __float_as_uint(f[c + 2]), __float_as_uint(f[c + 3])};
-        buf_store<16>(v, rs, voff + 4u * c, soff);
+        buf_store<16>(v, rs, voff + 4u * c, soff, sc1);
       }
     }
   } else {
     if constexpr (VW == 1) {
-      buf_store<2>(__builtin_bit_cast(uint16_t, (__bf16)f[0]), rs, voff, soff);
+      buf_store<2>(__builtin_bit_cast(uint16_t, (__bf16)f[0]), rs, voff, soff, sc1);
     } else {
       uint32_t w[VW / 2];
 #pragma unroll
@@ -232,13 +254,13 @@ __device__ __forceinline__ void store_out(rsrc_t rs, uint32_t voff, const float 
         w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pr, bf16x2));
       }
       if constexpr (VW == 2) {
-        buf_store<4>(w[0], rs, voff, soff);
+        buf_store<4>(w[0], rs, voff, soff, sc1);
       } else if constexpr (VW == 4) {
         u32x2 v = {w[0], w[1]};
-        buf_store<8>(v, rs, voff, soff);
+        buf_store<8>(v, rs, voff, soff, sc1);
       } else {
         u32x4 v = {w[0], w[1], w[2], w[3]};
-        buf_store<16>(v, rs, voff, soff);
+        buf_store<16>(v, rs, voff, soff, sc1);
       }
     }
   }

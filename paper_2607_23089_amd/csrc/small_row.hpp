@@ -31,6 +31,7 @@ __global__ __launch_bounds__(256) void small_row_kernel(
   constexpr int RPW = kWave / LPR;     // rows per wave per load instruction
   constexpr int RPT = RPW * RPL;       // rows per wave per task
   const int lane = threadIdx.x & (kWave - 1);
+  const bool wl = stores_whole_lines(y, (int64_t)cols * Out::bytes);  // sc1 stores
   const int sub = lane % LPR;          // vector index inside the row
   const int grp = lane / LPR;          // row inside the load group
   const int nvec = cols / VW;
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(256) void small_row_kernel(
         for (int i = 0; i < VW; ++i) f[k][i] *= inv;
       }
       const bool ok = col_ok && (k * RPW + grp < nrows);
-      if (ok) store_out<Out, VW>(ry, vout + k * group_elts * Out::bytes, f[k]);
+      if (ok) store_out<Out, VW>(ry, vout + k * group_elts * Out::bytes, f[k], wl);
     }
   }
 }

@@ -222,6 +222,7 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
 
   const int T = blockDim.x;
   const int lane = threadIdx.x & (kWave - 1);
+  const bool wl = stores_whole_lines(y, (int64_t)cols * Out::bytes);  // sc1 stores
   const int wave = wave_id();
   const int nwaves = T / kWave;
   const int c = blockIdx.x % S;                 // chunk of the row
@@ -281,7 +282,7 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
 #pragma unroll
       for (int s = 0; s < NV; ++s)
         if ((s < NV - 1 || last_ok) && (s * RT + g) * VW > lim)
-          store_out<Out, VW>(ry, vout + s * sout, z);
+          store_out<Out, VW>(ry, vout + s * sout, z, wl);
     }
 
     // Block maximum, then the block sum relative to it (split_share_pair()
@@ -352,7 +353,7 @@ __global__ __launch_bounds__(1024) void split_row_kernel(
 #pragma unroll
       for (int i = 0; i < VW; ++i) f[s][i] = LOG ? (f[s][i] - M) - scale : f[s][i] * scale;
       if ((s < NV - 1 || last_ok) && (!FUSED || (s * RT + g) * VW <= lim || redo_masked))
-        store_out<Out, VW>(ry, vout + s * sout, f[s]);
+        store_out<Out, VW>(ry, vout + s * sout, f[s], wl);
     }
     // LDS reuse across rows: red_m and red_s are rewritten only after a
     // barrier that every wave reaches after reading them (the next reduction's

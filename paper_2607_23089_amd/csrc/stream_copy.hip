@@ -25,6 +25,8 @@ __global__ __launch_bounds__(kCopyBlock) void stream_copy_kernel(
     int64_t nblocks) {
   constexpr int64_t CH = (int64_t)kCopyBlock * VW;
   const int i0 = threadIdx.x * VW;
+  // (each block's chunk plays the part of a row for the store policy)
+  const bool wl = stores_whole_lines(y, CH * Out::bytes);  // sc1 stores
   for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
     const int64_t base = b * CH;
     const int cnt = (int)(n - base < CH ? n - base : CH);
@@ -35,14 +37,14 @@ __global__ __launch_bounds__(kCopyBlock) void stream_copy_kernel(
       v.load(rx, (uint32_t)i0 * In::bytes, 0);
       float f[VW];
       v.to_float(f);
-      store_out<Out, VW>(ry, (uint32_t)i0 * Out::bytes, f);
+      store_out<Out, VW>(ry, (uint32_t)i0 * Out::bytes, f, wl);
     } else {
       for (int e = i0; e < cnt; ++e) {
         InVec<In, 1> v;
         v.load(rx, (uint32_t)e * In::bytes, 0);
         float f[1];
         v.to_float(f);
-        store_out<Out, 1>(ry, (uint32_t)e * Out::bytes, f);
+        store_out<Out, 1>(ry, (uint32_t)e * Out::bytes, f, wl);
       }
     }
   }

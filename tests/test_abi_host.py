@@ -192,7 +192,18 @@ def test_select_regimes(lib):
     # shapes or the fused form
     assert has(d(8191, 8192, R.F32, R.F32)[1], "medium", "wpr=8 ", "vpl=4 ")
     assert has(d(8192, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
-    assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=4 ", "ragged=1 ")  # ragged
+    assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=4 ", "ragged=1 ",  # ragged:
+               "wpr=4 ", "block=256 ")                                            # a row a block
+    # rows under 64 KiB that the 16-value rule puts on 16 waves, outside the
+    # row counts of the measured shapes and of the 4-16 rows per compute unit
+    # rule: the fewest waves holding at most 48 values
+    assert has(d(4096, 11984, R.BF16, R.BF16)[1], "medium", "wpr=4 ", "vpl=6 ", "packed=0 ")
+    assert has(d(6144, 8240, R.BF16, R.F32)[1], "medium", "wpr=4 ", "vpl=9 ")
+    assert has(d(768, 9920, R.F32, R.F32)[1], "medium", "wpr=4 ", "vpl=10 ")
+    assert has(d(2048, 11984, R.BF16, R.BF16)[1], "medium", "wpr=2 ", "packed=1 ")  # 4-16 rule
+    t = R.rowsm_describe_op(R.OP_SOFTMAX, 4096, 11984, R.BF16, R.BF16,
+                            R.RowsmConfig(waves_per_row=16))[1]
+    assert has(t, "medium", "wpr=16 ", "vpl=2 ")                                     # asked for
     t = R.rowsm_describe_op(R.OP_SOFTMAX, 100000, 8192, R.F32, R.F32,
                             R.RowsmConfig(waves_per_row=8))[1]
     assert has(t, "medium", "wpr=8 ", "vpl=4 ")
