@@ -93,6 +93,45 @@ int64_t grid_cap(int bpc, int cus) {
 
 bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
 
+// Host form of the kernels' stores_whole_lines(): every store of a launch
+// covers whole 128-byte lines (the output starts on a line, and a row is a
+// whole number of lines or a power-of-two fraction of one).  Such launches
+// store with the device-scope bit; the others without it.
+bool whole_lines(uintptr_t y, int64_t row_bytes) {
+  return (y & 127) == 0 &&
+         ((row_bytes & 127) == 0 || (row_bytes > 0 && row_bytes < 128 && 128 % row_bytes == 0));
+}
+
+// Launches of short rows whose stores cover parts of lines (rows of widths
+// that are not multiples of 128 bytes): a grid of about one block per
+// `per_block` bytes of traffic, at least 4 blocks per compute unit and at
+// most the uncapped grid, each block looping over its rows.  Sweeps of
+// one-wave medium rows (33-121 vectors of one element, half and full width)
+// and small rows of 13-27 one-element columns in every dtype pair at 32-864
+// MiB, each launch alone after a cache-evicting write, grids of 4-128 blocks
+// per compute unit: the best grid grows with the launch (4 blocks per
+// compute unit at 32-48 MiB, 64 at 768-864 MiB) and a fixed traffic per
+// block tracks it: 32 KiB for the forward medium rows of one to four slots
+// (1.4-1.8% above the fastest grid measured on geometric mean over three
+// sweeps, where the grids tuned with device-scope stores took 3.4-7.7%),
+// 16 KiB for the forward small rows, at most 128 blocks per compute unit
+// (0.9-2.7% against 5.8-17%), 24 KiB of the three streams for the backward
+// medium rows (1.7-2.2% against 2.3-11%).  The grid is rounded to whole residencies (the blocks
+// of `block` threads that fit the compute units at once, 2048 threads per
+// compute unit): a grid of 2049 blocks of 512 threads left one block to run
+// alone after two full residencies and measured 9% slower than 2048.
+// (rows / (per_block / row_bytes): no product of rows and row bytes is
+// formed.)
+int64_t part_line_grid(int64_t rows, int64_t row_bytes, int64_t per_block, int64_t dflt,
+                       int block, int cus, int max_per_cu = 0) {
+  const int64_t rpb = per_block / row_bytes > 1 ? per_block / row_bytes : 1;
+  const int64_t unit = (int64_t)cus * (2048 / block > 1 ? 2048 / block : 1);
+  int64_t g = (cdiv(rows, rpb) + unit / 2) / unit * unit;
+  if (g < unit) g = unit;
+  if (max_per_cu > 0 && g > (int64_t)max_per_cu * cus) g = (int64_t)max_per_cu * cus;
+  return g < dflt ? g : dflt;
+}
+
 // Block size of the small-row and MoE kernels (whose waves work on their own
 // rows): 256 threads, or cfg->block when given, at most 256.
 int small_block(const rowsm_config* cfg, int* block) {
@@ -448,6 +487,12 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     const int64_t rows_per_block = (int64_t)(p->block / kWave) * (kWave / p->lpr) * p->rpl;
     p->grid = cdiv(rows, rows_per_block);
     if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
+    // Narrow-vector rows whose stores cover parts of lines: about 16 KiB of
+    // traffic per block (part_line_grid()).
+    if (auto_variant && !fused && bpc == 0 && vw * (ib > ob ? ib : ob) < 16 &&
+        !whole_lines(ya, cols * ob) &&
+        (!cfg || (cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->block == 0)))
+      p->grid = part_line_grid(rows, row_bytes, 16 << 10, p->grid, p->block, cus, 128);
     return ROWSM_OK;
   }
   if (variant == ROWSM_MEDIUM) {
@@ -686,11 +731,18 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // faster than the residency from 160 MiB on (e.g. 499321 x 168 fp32 and
     // bf16 rows of 448 columns), up to 7% slower at 40 MiB; at lower fill
     // the residency stays ahead.
+    // These rules were measured on launches whose stores cover whole lines;
+    // rows whose stores cover parts of lines take about 32 KiB of traffic
+    // per block instead (part_line_grid(); rows of one to four slots).
     const int in_bytes_per_slot = vw * ib;
     if (auto_variant && !fused && !ragged && wpr == 1 && bpc == 0 &&
         (!cfg || (cfg->rows_per_block == 0 && cfg->block == 0 && cfg->waves_per_row == 0 &&
                   cfg->vw == 0))) {
-      if (p->vpl == 1 && ib == ob && in_bytes_per_slot == 16 && nvec * 100 >= 65 * kWave) {
+      if (!whole_lines(ya, cols * ob)) {
+        if (p->vpl <= 4)
+          p->grid = part_line_grid(rows, cols * (ib + ob), 32 << 10, p->grid, p->block, cus);
+      } else if (p->vpl == 1 && ib == ob && in_bytes_per_slot == 16 &&
+                 nvec * 100 >= 65 * kWave) {
         p->block = kWave;
         p->grid = rows < grid_cap(0, cus) ? rows : grid_cap(0, cus);
       } else if ((p->vpl == 1 || (p->vpl == 2 && in_bytes_per_slot <= 4)) &&
@@ -945,19 +997,14 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       p->block = rpb * wpr * kWave;
       p->grid = cdiv(rows, rpb);
       if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
-      // One wave per row holding at most 8 bytes of each input per lane,
-      // the row filling at most 3/4 of the wave's slots, nothing about the
-      // shape or grid given: one residency of 4 blocks per compute unit
-      // whose waves loop over the rows (the forward's short-row rule, with a
-      // bound on the fill: at 93% fill the block per row group stays up to
-      // 30% faster).  Sweeps of 41-182-vector rows (one- and two-element and
-      // full vectors, every dtype pair, 48-300 MiB of the three streams,
-      // each launch alone after a cache-evicting write): 2.2% above the
-      // fastest grid measured on geometric mean, where a block per row group
-      // was 13% (at most 61%), and never more than 3% slower than it.
-      if (auto_variant && shape_free && bpc == 0 && wpr == 1 && nv * vbytes <= 8 &&
-          nvec * 4 <= 3 * kWave * nv && p->grid > 4 * (int64_t)cus)
-        p->grid = 4 * (int64_t)cus;
+      // Rows of one wave and one to four slots whose dx stores cover parts of
+      // lines, nothing about the shape or grid given: about 24 KiB of the
+      // three streams per block (part_line_grid()).  Rows of whole lines
+      // keep a block per row group (no such row of one wave has narrow
+      // vectors unless its inputs are misaligned).
+      if (auto_variant && shape_free && bpc == 0 && wpr == 1 && nv <= 4 &&
+          !whole_lines(dxa, cols * ob))
+        p->grid = part_line_grid(rows, cols * (2 * ib + ob), 24 << 10, p->grid, p->block, cus);
       return ROWSM_OK;
     }
   }

@@ -337,22 +337,39 @@ def test_describe(lib):
         st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16,
                                        R.RowsmConfig(blocks_per_cu=64))
         assert st == R.OK and "grid=16384 " in text, text
-    # one wave per row with at most 8 input bytes per lane: one residency of
-    # 4 blocks per compute unit; same-width rows of one full slot filling 65%
-    # of the wave or more: one-wave blocks of one row; two full 16-byte
-    # slots keep a block per row group, and a grid cap given stays
-    for rows, cols, i, o in ((1000000, 37, R.F32, R.F32), (500000, 75, R.BF16, R.BF16),
-                             (500000, 164, R.F32, R.F32), (500000, 256, R.F32, R.BF16)):
-        st, text = R.rowsm_describe(rows, cols, i, o)
-        assert st == R.OK and "wpr=1 " in text and "grid=1024 " in text, text
-    for rows, cols, i, o in ((500000, 168, R.F32, R.F32), (500000, 256, R.F32, R.F32),
-                             (500000, 512, R.BF16, R.BF16)):
+    # rows of whole 128-byte lines (device-scope stores): one wave per row
+    # with at most 8 input bytes per lane, one residency of 4 blocks per
+    # compute unit; same-width rows of one full slot filling 65% of the wave
+    # or more, one-wave blocks of one row
+    st, text = R.rowsm_describe(500000, 256, R.F32, R.BF16)
+    assert st == R.OK and "wpr=1 " in text and "grid=1024 " in text, text
+    for rows, cols, i, o in ((500000, 256, R.F32, R.F32), (500000, 512, R.BF16, R.BF16)):
         st, text = R.rowsm_describe(rows, cols, i, o)
         assert st == R.OK and "block=64 " in text and "grid=500000 " in text, text
-    st, text = R.rowsm_describe(500000, 260, R.BF16, R.BF16)
-    assert st == R.OK and "nv=2 " in text and "grid=62500 " in text, text
+    # rows whose stores cover parts of lines, one to four slots: about 32 KiB
+    # of traffic per block, rows / (32768 // row bytes) blocks rounded to
+    # whole residencies of 4 blocks per compute unit
+    for rows, cols, i, o, grid in ((1000000, 37, R.F32, R.F32, 9216),     # 296-byte rows
+                                   (500000, 75, R.BF16, R.BF16, 4096),
+                                   (500000, 164, R.F32, R.F32, 20480),
+                                   (500000, 168, R.F32, R.F32, 20480),
+                                   (500000, 260, R.BF16, R.BF16, 16384),   # two slots
+                                   (2000, 37, R.F32, R.F32, 250)):         # uncapped grid
+        st, text = R.rowsm_describe(rows, cols, i, o)
+        assert st == R.OK and "wpr=1 " in text and f"grid={grid} " in text, text
+    st, text = R.rowsm_describe(20000, 37, R.F32, R.F32)                 # at least 4 per CU
+    assert st == R.OK and "grid=1024 " in text, text
     st, text = R.rowsm_describe(500000, 151, R.F32, R.F32)              # three slots
-    assert st == R.OK and "nv=3 " in text and "grid=62500 " in text, text
+    assert st == R.OK and "nv=3 " in text and "grid=18432 " in text, text
+    st, text = R.rowsm_describe(500000, 301, R.F32, R.F32)              # five: default grid
+    assert st == R.OK and "nv=5 " in text and "grid=62500 " in text, text
+    # small rows of narrow vectors whose stores cover parts of lines: about
+    # 16 KiB per block, whole residencies of 8 blocks per compute unit; full
+    # vectors keep their rules
+    st, text = R.rowsm_describe(1048576, 21, R.BF16, R.BF16)            # 84-byte rows
+    assert st == R.OK and text.startswith("small") and "grid=6144 " in text, text
+    st, text = R.rowsm_describe(1048576, 24, R.F32, R.F32)              # full vectors
+    assert st == R.OK and text.startswith("small") and "grid=8192 " in text, text
     st, text = R.rowsm_describe_op(R.OP_SOFTMAX, 1000000, 37, R.F32, R.F32,
                                    R.RowsmConfig(blocks_per_cu=16))
     assert st == R.OK and "grid=4096 " in text, text
@@ -450,16 +467,20 @@ def test_backward_plans(lib):
     assert d(127, 16380, R.F32, R.F32)[1].startswith("medium")     # under 64 KiB
     st, t = d(100, 65536, R.BF16, R.BF16, variant=R.MEDIUM)        # asked for
     assert st == R.OK and t.startswith("medium") and "wpr=16 " in t, t
-    # one-wave rows of at most 8 bytes of each input per lane filling at most
-    # 3/4 of the wave's slots: one residency of 4 blocks per compute unit
+    # rows of one wave and one to four slots whose dx stores cover parts of
+    # lines: about 24 KiB of the three streams per block, rows / (24576 //
+    # (cols * (2 ib + ob))) blocks in whole residencies; whole-line rows,
+    # five or more slots, small launches, a grid or a shape given keep their
+    # plans
     cap = lambda rows, cols, dt, **cfg: int(d(rows, cols, dt, dt, **cfg)[1].split("grid=")[1].split()[0])
-    assert cap(204600, 41, R.BF16) == 1024                        # 41 one-element vectors
-    assert cap(291271, 90, R.F32) == 1024                         # 45 two-element vectors
-    assert cap(582542, 90, R.BF16) == 1024                        # 2 x 1 element, 70%
-    assert cap(220289, 119, R.F32) == 27537                       # 93% of the slots
-    assert cap(163840, 320, R.BF16) == 20480                      # 16-byte vectors
-    assert cap(288070, 182, R.BF16) == 36009                      # three slots
-    assert cap(4000, 41, R.BF16) == 500                           # under the cap
+    assert cap(204600, 41, R.BF16) == 2048                        # 246-byte rows of 3 streams
+    assert cap(291271, 90, R.F32) == 13312                        # 45 two-element vectors
+    assert cap(582542, 90, R.BF16) == 13312                       # two slots
+    assert cap(220289, 119, R.F32) == 13312
+    assert cap(163840, 320, R.BF16) == 20480                      # 640-byte rows: whole lines
+    assert cap(288070, 182, R.BF16) == 13312                      # three slots
+    assert cap(288070, 330, R.BF16) == 36009                      # six: default grid
+    assert cap(4000, 41, R.BF16) == 500                           # under the grid
     assert cap(204600, 41, R.BF16, blocks_per_cu=8) == 2048       # grid given
     assert cap(204600, 41, R.BF16, rows_per_block=4) == 51150     # shape given
     # few long rows (>= 512 KiB of y, dy and dx per row): the split form,

@@ -214,16 +214,19 @@ def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
 
 @pytest.mark.parametrize("rows,cols,din,dout", [
     (204600, 41, "bf16", "bf16"), (153450, 41, "bf16", "f32"), (122760, 41, "f32", "bf16"),
-    (291271, 90, "f32", "f32"), (582542, 90, "bf16", "bf16"), (81707, 77, "bf16", "f32")])
-def test_bwd_short_rows_one_residency(rows, cols, din, dout):
-    # one-wave rows of at most 8 bytes of each input per lane filling at most
-    # 3/4 of the wave: a grid of 4 blocks per compute unit whose waves loop
+    (291271, 90, "f32", "f32"), (582542, 90, "bf16", "bf16"), (81707, 77, "bf16", "f32"),
+    (288070, 182, "bf16", "bf16")])
+def test_bwd_short_rows_looping_grid(rows, cols, din, dout):
+    # rows of one wave and one to four slots whose stores cover parts of lines:
+    # a grid of about 24 KiB of the three streams per block, whose waves loop
     # over the rows; the output prefilled with NaN so that every row is seen
     # written, sampled rows (the last ones among them) against the oracle
     st, desc = R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, R.dtype_code(DT[din]),
                                    R.dtype_code(DT[dout]))
     assert st == R.OK and desc.startswith("medium") and "wpr=1 " in desc, desc
-    assert "block=512 grid=1024 " in desc, desc
+    per_row = cols * (2 * DT[din].itemsize + DT[dout].itemsize)
+    grid = max(1024, (-(-rows // max(1, 24576 // per_row)) + 512) // 1024 * 1024)
+    assert f"block=512 grid={grid} " in desc, desc
     y, dy = inputs(rows, cols, din, alpha=0.3, seed=rows)
     out = torch.full((rows, cols), float("nan"), dtype=DT[dout], device=DEV)
     dx = run_bwd(y.to(DEV), dy.to(DEV), dout, out=out)

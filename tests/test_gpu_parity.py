@@ -467,20 +467,24 @@ def test_few_rows_per_cu_shapes(rows, cols, din, dout, want):
 
 
 @pytest.mark.parametrize("rows,cols,din,dout,want", [
-    (1000003, 37, "f32", "f32", ("block=512 ", "grid=1024 ")),
-    (700001, 37, "bf16", "bf16", ("block=512 ", "grid=1024 ")),
-    (500001, 75, "bf16", "f32", ("block=512 ", "grid=1024 ")),
-    (600011, 101, "f32", "bf16", ("block=512 ", "grid=1024 ")),
-    (500003, 144, "f32", "f32", ("block=512 ", "grid=1024 ")),
+    (1000003, 37, "f32", "f32", ("block=512 ", "grid=9216 ")),
+    (700001, 37, "bf16", "bf16", ("block=512 ", "grid=3072 ")),
+    (500001, 75, "bf16", "f32", ("block=512 ", "grid=7168 ")),
+    (600011, 101, "f32", "bf16", ("block=512 ", "grid=11264 ")),
+    (500003, 144, "f32", "f32", ("block=512 ", "grid=17408 ")),
+    (300007, 168, "f32", "f32", ("block=512 ", "grid=12288 ")),
+    (500001, 256, "f32", "bf16", ("block=512 ", "grid=1024 ")),
     (400009, 256, "f32", "f32", ("block=64 ", "grid=400009 ")),
     (250001, 512, "bf16", "bf16", ("block=64 ", "grid=250001 ")),
-    (300007, 168, "f32", "f32", ("block=64 ", "grid=300007 "))])
+    (400009, 142, "bf16", "f32", ("block=512 ", "grid=10240 "))])      # three slots
 def test_one_wave_short_rows(rows, cols, din, dout, want):
-    # one wave per row with at most 8 input bytes per lane: the launcher's
-    # one residency of 4 blocks per compute unit, whose waves loop over many
-    # rows each; same-width rows of one full 16-byte slot filling most of the
-    # wave: one-wave blocks of one row (ragged row counts); sampled rows, the
-    # last ones among them, against the oracle, every row's sum
+    # one wave per row: rows whose stores cover parts of 128-byte lines take
+    # a grid of about 32 KiB of traffic per block, whose waves loop over many
+    # rows each; rows of whole lines with at most 8 input bytes per lane one
+    # residency of 4 blocks per compute unit, and same-width rows of one full
+    # 16-byte slot filling most of the wave one-wave blocks of one row
+    # (ragged row counts); sampled rows, the last ones among them, against
+    # the oracle, every row's sum
     st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
     assert st == R.OK and desc.startswith("medium") and "wpr=1 " in desc, desc
     assert all(w in desc for w in want), desc
@@ -491,6 +495,26 @@ def test_one_wave_short_rows(rows, cols, din, dout, want):
     sums = y.double().sum(dim=1)
     tol = 1e-5 if dout == "f32" else 2.0 ** -8 * 2 + 1e-5
     assert float((sums - 1.0).abs().max()) <= tol
+    del x, y
+
+
+@pytest.mark.parametrize("rows,cols,din,dout,grid", [
+    (1048583, 21, "bf16", "bf16", 6144), (2000003, 13, "f32", "f32", 12288),
+    (1500007, 27, "bf16", "f32", 14336), (800011, 29, "f32", "bf16", 8192)])
+def test_small_rows_of_part_lines(rows, cols, din, dout, grid):
+    # small rows of one-element vectors whose stores cover parts of 128-byte
+    # lines: a grid of about 16 KiB of traffic per block in whole residencies
+    # of 8 blocks per compute unit, whose waves loop over many row groups;
+    # the output prefilled with NaN so that every row is seen written,
+    # sampled rows (the last ones among them) against the oracle
+    st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
+    assert st == R.OK and desc.startswith("small") and f"block=256 grid={grid} " in desc, desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + cols, device=DEV)
+    y = torch.full((rows, cols), float("nan"), dtype=DT[dout], device=DEV)
+    run(x, dout, out=y)
+    assert bool(torch.isfinite(y).all())
+    sample = list(range(0, rows, 4999)) + list(range(rows - 7, rows))
+    assert_parity(x[sample].cpu(), y[sample].cpu(), dout, f"{rows}x{cols} {din}->{dout} [{desc}]")
     del x, y
 
 
