@@ -86,7 +86,8 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // (and slower still in plain store streams): waves that drift apart spread
 // the addresses in flight over the whole buffer, while the in-order blocks
 // of an uncapped grid keep them in one moving window.  (Medium rows of one
-// wave and at most 8 input bytes per lane are the exception, in plan_for().)
+// wave and up to four slots per lane, and small rows of narrow vectors whose
+// stores cover parts of lines, are the exception: looping_grid().)
 int64_t grid_cap(int bpc, int cus) {
   return bpc ? (int64_t)cus * bpc : ((int64_t)1 << 30);
 }
@@ -102,27 +103,30 @@ bool whole_lines(uintptr_t y, int64_t row_bytes) {
          ((row_bytes & 127) == 0 || (row_bytes > 0 && row_bytes < 128 && 128 % row_bytes == 0));
 }
 
-// Launches of short rows whose stores cover parts of lines (rows of widths
-// that are not multiples of 128 bytes): a grid of about one block per
-// `per_block` bytes of traffic, at least 4 blocks per compute unit and at
-// most the uncapped grid, each block looping over its rows.  Sweeps of
-// one-wave medium rows (33-121 vectors of one element, half and full width)
-// and small rows of 13-27 one-element columns in every dtype pair at 32-864
-// MiB, each launch alone after a cache-evicting write, grids of 4-128 blocks
-// per compute unit: the best grid grows with the launch (4 blocks per
-// compute unit at 32-48 MiB, 64 at 768-864 MiB) and a fixed traffic per
-// block tracks it: 32 KiB for the forward medium rows of one to four slots
-// (1.4-1.8% above the fastest grid measured on geometric mean over three
-// sweeps, where the grids tuned with device-scope stores took 3.4-7.7%),
-// 16 KiB for the forward small rows, at most 128 blocks per compute unit
-// (0.9-2.7% against 5.8-17%), 24 KiB of the three streams for the backward
-// medium rows (1.7-2.2% against 2.3-11%).  The grid is rounded to whole residencies (the blocks
-// of `block` threads that fit the compute units at once, 2048 threads per
-// compute unit): a grid of 2049 blocks of 512 threads left one block to run
-// alone after two full residencies and measured 9% slower than 2048.
-// (rows / (per_block / row_bytes): no product of rows and row bytes is
-// formed.)
-int64_t part_line_grid(int64_t rows, int64_t row_bytes, int64_t per_block, int64_t dflt,
+// Launches of short rows whose waves each take few bytes: a grid of about
+// one block per `per_block` bytes of traffic, rounded to whole residencies
+// (the blocks of `block` threads that fit the compute units at once, 2048
+// threads per compute unit), at least one residency and at most the
+// uncapped grid (and `max_per_cu` blocks per compute unit when given), each
+// block looping over its rows.  Sweeps of one-wave medium rows (33-242
+// vectors of one element, half and full width, rows of whole 128-byte lines
+// and of parts of lines) and small rows of 11-29 one-element columns, every
+// dtype pair, 32 MiB-2 GiB, grids of 4-128 blocks per compute unit, each
+// launch alone after a cache-evicting write: the best grid grows with the
+// launch (4 blocks per compute unit at 32-64 MiB, 64-128 at 1-2 GiB) and a
+// fixed traffic per block tracks it.  Forward one-wave medium rows of one
+// to four slots: 32 KiB, 1.4-1.8% above the fastest grid measured on
+// geometric mean over four sweeps where the earlier rules (one residency
+// of 4 blocks per compute unit for up to 8 input bytes per lane, one-wave
+// blocks for same-width rows of one full slot, a block per 8 rows
+// otherwise) took 3.4-7.7%.  Forward small rows of narrow vectors whose
+// stores cover parts of lines: 16 KiB, at most 128 blocks per compute unit
+// (0.9-2.7% against 5.8-17%).  Backward one-wave medium rows of one to four
+// slots: 24 KiB of the three streams (1.7-2.3% against 2.3-11%).  A grid of
+// 2049 blocks of 512 threads left one block to run alone after two full
+// residencies and measured 9% slower than 2048.  (rows / (per_block /
+// row_bytes): no product of rows and row bytes is formed.)
+int64_t looping_grid(int64_t rows, int64_t row_bytes, int64_t per_block, int64_t dflt,
                        int block, int cus, int max_per_cu = 0) {
   const int64_t rpb = per_block / row_bytes > 1 ? per_block / row_bytes : 1;
   const int64_t unit = (int64_t)cus * (2048 / block > 1 ? 2048 / block : 1);
@@ -488,11 +492,11 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->grid = cdiv(rows, rows_per_block);
     if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
     // Narrow-vector rows whose stores cover parts of lines: about 16 KiB of
-    // traffic per block (part_line_grid()).
+    // traffic per block (looping_grid()).
     if (auto_variant && !fused && bpc == 0 && vw * (ib > ob ? ib : ob) < 16 &&
         !whole_lines(ya, cols * ob) &&
         (!cfg || (cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->block == 0)))
-      p->grid = part_line_grid(rows, row_bytes, 16 << 10, p->grid, p->block, cus, 128);
+      p->grid = looping_grid(rows, row_bytes, 16 << 10, p->grid, p->block, cus, 128);
     return ROWSM_OK;
   }
   if (variant == ROWSM_MEDIUM) {
@@ -714,42 +718,14 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->block = rpb * wpr * kWave;
     p->grid = cdiv(rows, rpb);
     if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
-    // One wave per row holding at most 8 input bytes per lane (one slot, or
-    // two slots of one or two elements), softmax and log forms, nothing
-    // about the shape or grid given: one residency of 4 blocks per compute
-    // unit (2048 threads) whose waves loop over the rows, instead of a block
-    // per 8 such short rows.  Sweeps of 33-128-vector rows (one-element,
-    // two-element and full vectors, every dtype pair, 32-800 MiB, each
-    // launch alone after a cache-evicting write): 3.0% above the fastest
-    // grid measured on geometric mean where a block per row group was 29%
-    // (at most 70%), and 2.7% against 21% (at most 19% against 46%) on 162
-    // launches of other lengths and sizes.  Two full 16-byte slots per lane
-    // measured faster with a block per row group, which they keep.  Rows of
-    // one full 16-byte slot per lane in a dtype pair of one width that fill
-    // at least 65% of the wave's lanes (42-64 vectors) take one-wave blocks
-    // of one row instead, uncapped, as the small rows of one width do: 0-22%
-    // faster than the residency from 160 MiB on (e.g. 499321 x 168 fp32 and
-    // bf16 rows of 448 columns), up to 7% slower at 40 MiB; at lower fill
-    // the residency stays ahead.
-    // These rules were measured on launches whose stores cover whole lines;
-    // rows whose stores cover parts of lines take about 32 KiB of traffic
-    // per block instead (part_line_grid(); rows of one to four slots).
-    const int in_bytes_per_slot = vw * ib;
-    if (auto_variant && !fused && !ragged && wpr == 1 && bpc == 0 &&
+    // One wave per row and one to four slots per lane, softmax and log
+    // forms, nothing about the shape or grid given: about 32 KiB of traffic
+    // per block, each block looping over its rows (looping_grid()), instead
+    // of a block per 8 such short rows.
+    if (auto_variant && !fused && !ragged && wpr == 1 && bpc == 0 && p->vpl <= 4 &&
         (!cfg || (cfg->rows_per_block == 0 && cfg->block == 0 && cfg->waves_per_row == 0 &&
-                  cfg->vw == 0))) {
-      if (!whole_lines(ya, cols * ob)) {
-        if (p->vpl <= 4)
-          p->grid = part_line_grid(rows, cols * (ib + ob), 32 << 10, p->grid, p->block, cus);
-      } else if (p->vpl == 1 && ib == ob && in_bytes_per_slot == 16 &&
-                 nvec * 100 >= 65 * kWave) {
-        p->block = kWave;
-        p->grid = rows < grid_cap(0, cus) ? rows : grid_cap(0, cus);
-      } else if ((p->vpl == 1 || (p->vpl == 2 && in_bytes_per_slot <= 4)) &&
-                 p->grid > 4 * (int64_t)cus) {
-        p->grid = 4 * (int64_t)cus;
-      }
-    }
+                  cfg->vw == 0)))
+      p->grid = looping_grid(rows, cols * (ib + ob), 32 << 10, p->grid, p->block, cus);
     return ROWSM_OK;
   }
   if (variant == ROWSM_LARGE) {
@@ -997,14 +973,11 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
       p->block = rpb * wpr * kWave;
       p->grid = cdiv(rows, rpb);
       if (p->grid > grid_cap(bpc, cus)) p->grid = grid_cap(bpc, cus);
-      // Rows of one wave and one to four slots whose dx stores cover parts of
-      // lines, nothing about the shape or grid given: about 24 KiB of the
-      // three streams per block (part_line_grid()).  Rows of whole lines
-      // keep a block per row group (no such row of one wave has narrow
-      // vectors unless its inputs are misaligned).
-      if (auto_variant && shape_free && bpc == 0 && wpr == 1 && nv <= 4 &&
-          !whole_lines(dxa, cols * ob))
-        p->grid = part_line_grid(rows, cols * (2 * ib + ob), 24 << 10, p->grid, p->block, cus);
+      // Rows of one wave and one to four slots, nothing about the shape or
+      // grid given: about 24 KiB of the three streams per block, each block
+      // looping over its rows (looping_grid()).
+      if (auto_variant && shape_free && bpc == 0 && wpr == 1 && nv <= 4)
+        p->grid = looping_grid(rows, cols * (2 * ib + ob), 24 << 10, p->grid, p->block, cus);
       return ROWSM_OK;
     }
   }

@@ -337,26 +337,20 @@ def test_describe(lib):
         st, text = R.rowsm_describe_op(op, 131072, 4096, R.BF16, R.BF16,
                                        R.RowsmConfig(blocks_per_cu=64))
         assert st == R.OK and "grid=16384 " in text, text
-    # rows of whole 128-byte lines (device-scope stores): one wave per row
-    # with at most 8 input bytes per lane, one residency of 4 blocks per
-    # compute unit; same-width rows of one full slot filling 65% of the wave
-    # or more, one-wave blocks of one row
-    st, text = R.rowsm_describe(500000, 256, R.F32, R.BF16)
-    assert st == R.OK and "wpr=1 " in text and "grid=1024 " in text, text
-    for rows, cols, i, o in ((500000, 256, R.F32, R.F32), (500000, 512, R.BF16, R.BF16)):
-        st, text = R.rowsm_describe(rows, cols, i, o)
-        assert st == R.OK and "block=64 " in text and "grid=500000 " in text, text
-    # rows whose stores cover parts of lines, one to four slots: about 32 KiB
-    # of traffic per block, rows / (32768 // row bytes) blocks rounded to
-    # whole residencies of 4 blocks per compute unit
+    # one wave per row and one to four slots: about 32 KiB of traffic per
+    # block, rows / (32768 // row bytes) blocks rounded to whole residencies
+    # of 4 blocks per compute unit, rows of whole lines or not
     for rows, cols, i, o, grid in ((1000000, 37, R.F32, R.F32, 9216),     # 296-byte rows
                                    (500000, 75, R.BF16, R.BF16, 4096),
                                    (500000, 164, R.F32, R.F32, 20480),
                                    (500000, 168, R.F32, R.F32, 20480),
+                                   (500000, 256, R.F32, R.BF16, 23552),    # whole lines
+                                   (500000, 256, R.F32, R.F32, 31744),
+                                   (500000, 512, R.BF16, R.BF16, 31744),
                                    (500000, 260, R.BF16, R.BF16, 16384),   # two slots
                                    (2000, 37, R.F32, R.F32, 250)):         # uncapped grid
         st, text = R.rowsm_describe(rows, cols, i, o)
-        assert st == R.OK and "wpr=1 " in text and f"grid={grid} " in text, text
+        assert st == R.OK and "wpr=1 " in text and f"block=512 grid={grid} " in text, text
     st, text = R.rowsm_describe(20000, 37, R.F32, R.F32)                 # at least 4 per CU
     assert st == R.OK and "grid=1024 " in text, text
     st, text = R.rowsm_describe(500000, 151, R.F32, R.F32)              # three slots
@@ -467,17 +461,16 @@ def test_backward_plans(lib):
     assert d(127, 16380, R.F32, R.F32)[1].startswith("medium")     # under 64 KiB
     st, t = d(100, 65536, R.BF16, R.BF16, variant=R.MEDIUM)        # asked for
     assert st == R.OK and t.startswith("medium") and "wpr=16 " in t, t
-    # rows of one wave and one to four slots whose dx stores cover parts of
-    # lines: about 24 KiB of the three streams per block, rows / (24576 //
-    # (cols * (2 ib + ob))) blocks in whole residencies; whole-line rows,
-    # five or more slots, small launches, a grid or a shape given keep their
-    # plans
+    # rows of one wave and one to four slots: about 24 KiB of the three
+    # streams per block, rows / (24576 // (cols * (2 ib + ob))) blocks in
+    # whole residencies; five or more slots, small launches, a grid or a
+    # shape given keep their plans
     cap = lambda rows, cols, dt, **cfg: int(d(rows, cols, dt, dt, **cfg)[1].split("grid=")[1].split()[0])
     assert cap(204600, 41, R.BF16) == 2048                        # 246-byte rows of 3 streams
     assert cap(291271, 90, R.F32) == 13312                        # 45 two-element vectors
     assert cap(582542, 90, R.BF16) == 13312                       # two slots
     assert cap(220289, 119, R.F32) == 13312
-    assert cap(163840, 320, R.BF16) == 20480                      # 640-byte rows: whole lines
+    assert cap(163840, 320, R.BF16) == 13312                      # 640-byte rows: whole lines
     assert cap(288070, 182, R.BF16) == 13312                      # three slots
     assert cap(288070, 330, R.BF16) == 36009                      # six: default grid
     assert cap(4000, 41, R.BF16) == 500                           # under the grid

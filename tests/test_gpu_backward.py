@@ -215,9 +215,10 @@ def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
 @pytest.mark.parametrize("rows,cols,din,dout", [
     (204600, 41, "bf16", "bf16"), (153450, 41, "bf16", "f32"), (122760, 41, "f32", "bf16"),
     (291271, 90, "f32", "f32"), (582542, 90, "bf16", "bf16"), (81707, 77, "bf16", "f32"),
-    (288070, 182, "bf16", "bf16")])
+    (288070, 182, "bf16", "bf16"), (163840, 320, "bf16", "bf16")])
 def test_bwd_short_rows_looping_grid(rows, cols, din, dout):
-    # rows of one wave and one to four slots whose stores cover parts of lines:
+    # rows of one wave and one to four slots (parts of 128-byte lines, and
+    # whole lines: 640-byte bf16 rows):
     # a grid of about 24 KiB of the three streams per block, whose waves loop
     # over the rows; the output prefilled with NaN so that every row is seen
     # written, sampled rows (the last ones among them) against the oracle

@@ -473,18 +473,16 @@ def test_few_rows_per_cu_shapes(rows, cols, din, dout, want):
     (600011, 101, "f32", "bf16", ("block=512 ", "grid=11264 ")),
     (500003, 144, "f32", "f32", ("block=512 ", "grid=17408 ")),
     (300007, 168, "f32", "f32", ("block=512 ", "grid=12288 ")),
-    (500001, 256, "f32", "bf16", ("block=512 ", "grid=1024 ")),
-    (400009, 256, "f32", "f32", ("block=64 ", "grid=400009 ")),
-    (250001, 512, "bf16", "bf16", ("block=64 ", "grid=250001 ")),
+    (500001, 256, "f32", "bf16", ("block=512 ", "grid=23552 ")),
+    (400009, 256, "f32", "f32", ("block=512 ", "grid=24576 ")),
+    (250001, 512, "bf16", "bf16", ("block=512 ", "grid=15360 ")),
     (400009, 142, "bf16", "f32", ("block=512 ", "grid=10240 "))])      # three slots
 def test_one_wave_short_rows(rows, cols, din, dout, want):
-    # one wave per row: rows whose stores cover parts of 128-byte lines take
-    # a grid of about 32 KiB of traffic per block, whose waves loop over many
-    # rows each; rows of whole lines with at most 8 input bytes per lane one
-    # residency of 4 blocks per compute unit, and same-width rows of one full
-    # 16-byte slot filling most of the wave one-wave blocks of one row
-    # (ragged row counts); sampled rows, the last ones among them, against
-    # the oracle, every row's sum
+    # one wave per row and one to four slots: a grid of about 32 KiB of
+    # traffic per block in whole residencies, whose waves loop over many
+    # rows each (ragged row counts, rows of whole 128-byte lines and of parts
+    # of lines); sampled rows, the last ones among them, against the oracle,
+    # every row's sum
     st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
     assert st == R.OK and desc.startswith("medium") and "wpr=1 " in desc, desc
     assert all(w in desc for w in want), desc
