@@ -397,22 +397,25 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
                                     cfg->block == 0 && cfg->split_blocks == 0 &&
                                     cfg->packed != 1))) {
     // (rows whose narrow-vector plan spreads them over several blocks each,
-    // too long for one block or few and long, keep it below cus rows: the
-    // ragged form has one block per row)
+    // too long for one block or few and long, keep it below cus / 4 rows:
+    // the ragged form has one block per row.  A sweep of 8-400 rows of
+    // 16385-38401 columns in every dtype pair: from 96 rows the ragged form
+    // was 0.64-1.06x the split form's time, 0.84x on geometric mean; at 8
+    // and 32 rows 1.02-1.40x.)
     const int64_t narrow_nvec = cols / vw;
     const bool narrow_medium =
         narrow_nvec <= 16 * kWave * (64 / vw < 16 ? 64 / vw : 16) &&
         (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus));
-    // Spans of 256-8192 vectors (4-128 KiB of 16-byte vectors): sweeps of
+    // Spans of 256 vectors up to what 16 waves hold: sweeps of
     // 301-50257-column rows in every dtype pair (96 and 512 MiB launches,
     // each alone after a cache-evicting write) measured the ragged form
     // 0.6-0.9x the narrow-vector time there; shorter rows spend too much on
-    // their edges (up to 1.45x slower), and rows of 12565 vectors, which take
-    // 16 waves of 13 slots, ran 3-30% slower than the narrow single-read form.
-    ragged = ragged_span >= 4 * kWave && ragged_span <= 16 * kWave * 8 &&
-             ragged_span <= ragged_max_span &&
+    // their edges (up to 1.45x slower).  (Spans of 8193-10240 fp32-width
+    // vectors, 9-10 slots of 16 waves: 0.80-0.94x the split form from 200
+    // rows.)
+    ragged = ragged_span >= 4 * kWave && ragged_span <= ragged_max_span &&
              (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus)) &&
-             (narrow_medium || rows >= cus);
+             (narrow_medium || rows >= cus / 4);
   }
   if (ragged) {
     vw = vw_full;
@@ -591,7 +594,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
           p->packed = false;
           break;
         }
-        if (in_dt == ROWSM_BF16 && vw == 8 && v >= 9 && v <= 24) {
+        // (the packed form up to 8 rows per compute unit: from 9 to 16 it
+        // was 5-20% slower than the unpacked rows of more waves, at 8 level
+        // or faster; sweeps of 9544-28344 bf16 columns)
+        if (in_dt == ROWSM_BF16 && vw == 8 && v >= 9 && v <= 24 && rows <= 8 * (int64_t)cus) {
           p->wpr = w;
           p->vpl = v;
           p->packed = true;

@@ -194,6 +194,16 @@ def test_select_regimes(lib):
     assert has(d(8192, 8192, R.F32, R.F32)[1], "large", "split=2 ", "block=256 ")
     assert has(d(100000, 8190, R.F32, R.F32)[1], "medium", "vw=4 ", "ragged=1 ",  # ragged:
                "wpr=4 ", "block=256 ")                                            # a row a block
+    # ragged rows longer than one block's narrow vectors: from cus / 4 rows,
+    # up to 16 waves of 10 fp32-width slots
+    assert has(d(96, 30001, R.F32, R.F32)[1], "medium", "ragged=1 ", "wpr=16 ", "nv=8 ")
+    assert has(d(32, 30001, R.F32, R.F32)[1], "large", "vw=1 ")
+    assert has(d(200, 38401, R.F32, R.F32)[1], "medium", "ragged=1 ", "wpr=16 ", "nv=10 ")
+    assert has(d(64, 16385, R.BF16, R.BF16)[1], "medium", "ragged=1 ")
+    assert has(d(63, 16385, R.BF16, R.BF16)[1], "large", "vw=1 ")
+    # the 4-16 rows per compute unit rule keeps the packed form up to 8 rows
+    # per compute unit
+    assert has(d(3656, 18520, R.BF16, R.BF16)[1], "medium", "wpr=8 ", "vpl=5 ", "packed=0 ")
     # rows under 64 KiB that the 16-value rule puts on 16 waves, outside the
     # row counts of the measured shapes and of the 4-16 rows per compute unit
     # rule: the fewest waves holding at most 48 values

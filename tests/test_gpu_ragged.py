@@ -149,3 +149,20 @@ def test_ragged_vocabulary_width(din, dout, cols):
     sums = y.double().sum(dim=1)
     tol = 1e-5 if dout == "f32" else 2.0 ** -8 * 4 + 1e-5
     assert float((sums - 1.0).abs().max()) <= tol
+
+
+@pytest.mark.parametrize("din,dout,rows,cols", [("f32", "f32", 96, 30001),
+                                                ("f32", "f32", 200, 38401),
+                                                ("bf16", "f32", 200, 38401),
+                                                ("bf16", "bf16", 64, 16385),
+                                                ("f32", "bf16", 131, 24577)])
+def test_ragged_few_long_rows(din, dout, rows, cols):
+    # rows too long for one block's narrow vectors, from cus / 4 rows: the
+    # ragged form on 8-16 waves (up to 10 slots of 4-element vectors), every
+    # row against the oracle
+    desc = describe(rows, cols, din, dout)
+    assert desc.startswith("medium") and "ragged=1 " in desc, desc
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=rows + cols)
+    y = R.softmax(x.to(DEV), out_dtype=DT[dout])
+    torch.cuda.synchronize()
+    assert_parity(x, y, dout, f"ragged few rows {rows}x{cols} {din}->{dout} [{desc}]")
