@@ -566,6 +566,10 @@ LAUNCHER_SHAPES = [  # (op, rows, cols, in dtype, out dtype)
     ("backward", 32768, 4096, "bf16", "bf16"),
     ("backward", 524288, 128, "bf16", "bf16"),
     ("backward", 131072, 64, "bf16", "bf16"),
+    ("softmax", 1000003, 37, "f32", "f32"),      # one-wave rows, looping grid
+    ("softmax", 1048576, 21, "bf16", "bf16"),    # small rows of one-element vectors
+    ("softmax", 12288, 4001, "bf16", "bf16"),    # ragged width
+    ("backward", 204600, 41, "bf16", "bf16"),    # one-wave rows, looping grid
 ]
 
 
@@ -649,8 +653,9 @@ def launcher_check(reps: int = 8):
     """The launcher's choice for launches of the shapes above against the
     other launch shapes of the library (medium wave groups with the default
     or one row per block, the single-read form with 1-4 blocks of 256 or 512
-    threads; for the small rows the grid capped at 8 or 64 blocks per compute
-    unit and blocks of 64 or 256 threads with 1 or 4 row groups per lane),
+    threads; for rows of at most 256 columns the grid capped at 4-128 blocks
+    per compute unit, blocks of 64 or 256 threads with 1 or 4 row groups per
+    lane, and one-wave medium groups with the default or one row per block),
     each launch timed alone after a cache-evicting write.
     Every timed shape makes reps + 2 launches, in the order listed."""
     import torch
@@ -663,6 +668,7 @@ def launcher_check(reps: int = 8):
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     out = []
     for op, rows, cols, din, dout in LAUNCHER_SHAPES:
+        print(f"launcher check: {op} {rows}x{cols} {din}->{dout}", file=sys.stderr, flush=True)
         if op == "backward":  # x holds probability rows, dy the upstream gradient
             x = W.random_probabilities(rows, cols, din, 0.3, seed=cols, device=dev)
             dy = W.random_matrix(rows, cols, din, sigma=1.0, seed=cols + 1, device=dev)
@@ -671,9 +677,12 @@ def launcher_check(reps: int = 8):
         y = torch.empty(rows, cols, dtype=W.TORCH_DTYPES[dout], device=dev)
         if cols <= 256:
             alts = ([("auto", None)] +
-                    [(f"bpc{b}", R.RowsmConfig(blocks_per_cu=b)) for b in (8, 64)] +
+                    [(f"bpc{b}", R.RowsmConfig(blocks_per_cu=b)) for b in (4, 8, 16, 64, 128)] +
                     [(f"b{b}r{r}", R.RowsmConfig(block=b, rows_per_lane=r))
-                     for b, r in ((256, 4), (256, 1), (64, 1), (64, 4))])
+                     for b, r in ((256, 4), (256, 1), (64, 1), (64, 4))] +
+                    [("M1", R.RowsmConfig(variant=R.MEDIUM, waves_per_row=1)),
+                     ("M1r1", R.RowsmConfig(variant=R.MEDIUM, waves_per_row=1,
+                                            rows_per_block=1))])
         else:
             alts = ([("auto", None)] +
                     [(f"M{w}", R.RowsmConfig(variant=R.MEDIUM, waves_per_row=w))

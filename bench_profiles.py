@@ -397,8 +397,9 @@ def summarize_launcher(bench_log: str, trace_dir: str, command: str, peak_gbs: f
         "(`auto`) and every other launch shape of the library that takes the shape: medium "
         "groups of w waves with the default rows per block (`Mw`) or one row per block "
         "(`Mwr1`), the single-read form with S blocks of T threads per row (`SsTt`), and "
-        "for small rows the grid capped at 8 or 64 blocks per compute unit (`bpcN`) and "
-        "blocks of b threads with r row groups per lane (`bBrR`); each launch alone after a "
+        "for rows of at most 256 columns the grid capped at N = 4-128 blocks per compute "
+        "unit (`bpcN`) and blocks of b threads with r row groups per lane (`bBrR`); each "
+        "launch alone after a "
         f"1 GiB cache-evicting write, {untimed} untimed and {per_shape - untimed} timed "
         "launches per shape.  Times are the rocprofv3 durations of the timed launches, "
         "matched to their shape in launch order.", "",
