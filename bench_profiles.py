@@ -20,12 +20,13 @@ import re
 
 # Kernels of the library (names without the namespace).
 ROW_KERNELS = ("small_row_kernel", "medium_row_kernel", "split_row_kernel",
-               "large_row_kernel", "ragged_row_kernel", "bwd_small_kernel", "bwd_medium_kernel",
+               "large_row_kernel", "ragged_row_kernel", "flat_row_kernel", "bwd_small_kernel",
+               "bwd_medium_kernel",
                "bwd_split_kernel", "bwd_large_kernel", "group_top2_kernel",
                "stream_copy_kernel")
 # Index of the output-form template argument (plain 0, fused 1, log 2).
 MODE_ARG = {"small_row_kernel": 5, "medium_row_kernel": 5, "split_row_kernel": 4,
-            "large_row_kernel": 4, "ragged_row_kernel": 4}
+            "large_row_kernel": 4, "ragged_row_kernel": 4, "flat_row_kernel": 5}
 MODES = {"softmax": 0, "scaled_causal": 1, "log_softmax": 2}
 TYPE_NAMES = {"f32": "rowsm::F32", "bf16": "rowsm::BF16"}
 DTYPE_BYTES = {"f32": 4, "bf16": 2}
@@ -107,12 +108,17 @@ def launch_spec(op: str, desc: str, din: str, dout: str) -> dict:
             ("split_row_kernel" if f.get("split", 0) > 0 else "large_row_kernel")
         if base == "medium_row_kernel" and f.get("ragged", 0):
             base = "ragged_row_kernel"
+        if base == "small_row_kernel" and f.get("flat", 0):
+            base = "flat_row_kernel"
     args = {0: TYPE_NAMES[din], 1: TYPE_NAMES[dout], 2: str(f["vw"])}
     if base in MODE_ARG:
         args[MODE_ARG[base]] = str(MODES[op])
     if base in ("medium_row_kernel", "split_row_kernel", "ragged_row_kernel") or \
             base in ("bwd_medium_kernel", "bwd_split_kernel"):
         args[3] = str(f["nv"])
+    if base == "flat_row_kernel":  # lanes per row and elements per lane of the row phase
+        args[3] = str(f["lpr"])
+        args[4] = str(f["nv"])
     return {"base": base, "args": args, "block": f["block"], "grid": f["block"] * f["grid"]}
 
 

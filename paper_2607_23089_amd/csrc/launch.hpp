@@ -40,6 +40,10 @@ struct Plan {
   // MEDIUM: a row width that is not a multiple of vw, read in whole vectors
   // aligned to the tensor with element-wise row edges (ragged_row.hpp)
   bool ragged = false;
+  // SMALL: short rows of such widths as one flat stream of whole vectors,
+  // regrouped into rows through LDS (flat_row.hpp); lpr lanes per row and nv
+  // elements per lane in the row phase
+  bool flat = false;
   // launch
   int block = 256;
   int64_t grid = 1;  // split form: 0 = one group per row, < 0 = minus the blocks-per-CU cap
@@ -97,6 +101,7 @@ template <int MODE> int launch_medium(const Call& c, int in_dt, int out_dt);
 template <int MODE> int launch_large(const Call& c, int in_dt, int out_dt);
 template <int MODE> int launch_split(const Call& c, int in_dt, int out_dt);
 template <int MODE> int launch_ragged(const Call& c, int in_dt, int out_dt);
+template <int MODE> int launch_flat(const Call& c, int in_dt, int out_dt);
 
 // Softmax-backward launchers (launch_bwd_<family>.hip).
 int launch_bwd_small(const Call& c, int in_dt, int out_dt);

@@ -1,0 +1,49 @@
+// Launcher of the flat short-row kernel (flat_row.hpp): the full 16-byte
+// vector width of the dtype pair, dispatch on the lanes per row and elements
+// per lane of the row phase.  Instantiated once per output form
+// (launch_flat_<form>.hip).
+#pragma once
+
+#include "flat_row.hpp"
+#include "launch.hpp"
+
+namespace rowsm {
+
+template <typename In, typename Out, int VW, int LPR, int E, int MODE>
+bool try_flat(const Call& c, int* status) {
+  if (c.p.lpr != LPR || c.p.nv != E) return false;
+  const int G = (kFlatSlots * kWave * VW - (VW - 1)) / c.cols;
+  if (G < 1) return false;
+  flat_row_kernel<In, Out, VW, LPR, E, MODE><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
+      static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
+      c.rows, c.cols, G);
+  *status = hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
+  return true;
+}
+
+// (lanes per row, elements per lane): LPR = max(8, pow2 >= cols / 8) up to 64,
+// E the power of two >= cols / LPR (flat_shape() in plan.hip).
+template <typename In, typename Out, int MODE>
+int flat_pair(const Call& c) {
+  constexpr int VW = 16 / (In::bytes > Out::bytes ? In::bytes : Out::bytes);
+  int status = ROWSM_EINVAL;
+  if (c.p.vw != VW || c.p.block != kWave) return status;
+  (void)(try_flat<In, Out, VW, 8, 2, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 8, 4, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 8, 8, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 16, 8, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 32, 8, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 64, 8, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 64, 16, MODE>(c, &status));
+  return status;
+}
+
+template <int MODE>
+int launch_flat(const Call& c, int in_dt, int out_dt) {
+  if (in_dt == ROWSM_F32 && out_dt == ROWSM_F32) return flat_pair<F32, F32, MODE>(c);
+  if (in_dt == ROWSM_F32) return flat_pair<F32, BF16, MODE>(c);
+  if (out_dt == ROWSM_F32) return flat_pair<BF16, F32, MODE>(c);
+  return flat_pair<BF16, BF16, MODE>(c);
+}
+
+}  // namespace rowsm

@@ -388,7 +388,18 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   const int ragged_vals = 40;
   const int64_t ragged_max_span = 16 * (int64_t)kWave * (ragged_vals / vw_full);
   bool ragged = false;
-  if (ragged_ok && cfg && cfg->vw == vw_full) {
+  // Flat short rows (flat_row.hpp): such widths up to what a tile of 4
+  // vectors per lane holds in one row, read as one flat stream of whole
+  // vectors; taken when cfg asks for the small variant at the full vector
+  // width, and by the launcher (below).
+  // (at most 1024 columns: 64 lanes of 16 elements in the row phase)
+  const int64_t flat_tile_cols = (int64_t)kFlatSlots * kWave * vw_full - (vw_full - 1);
+  const int64_t flat_max_cols = flat_tile_cols < 1024 ? flat_tile_cols : 1024;
+  bool flat = false;
+  if (ragged_ok && cfg && cfg->vw == vw_full && cfg->variant == ROWSM_SMALL) {
+    if (cols > flat_max_cols) return ROWSM_EINVAL;
+    flat = true;
+  } else if (ragged_ok && cfg && cfg->vw == vw_full) {
     if (cfg->variant != ROWSM_AUTO && cfg->variant != ROWSM_MEDIUM) return ROWSM_EINVAL;
     if (ragged_span > ragged_max_span) return ROWSM_EINVAL;
     ragged = true;
@@ -416,6 +427,43 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     ragged = ragged_span >= 4 * kWave && ragged_span <= ragged_max_span &&
              (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus)) &&
              (narrow_medium || rows >= cus / 4);
+  }
+  // The launcher takes the flat form for rows of 9-256 columns whose narrow
+  // vectors would be of at most 4 bytes (one fp32 or one or two bf16
+  // elements).  A sweep of 3-1001-column rows in every dtype pair at 64 and
+  // 512 MiB (each launch alone after a cache-evicting write): 1.04-1.37x
+  // the time of a plain copy of the same bytes at 13-1001 columns, where
+  // the narrow-vector plans took up to 3.9x; against the narrow plans'
+  // fastest grid 0.26-0.98x at 13-129 columns (0.35x at 37), level at 257
+  // and beyond; slower at 3-7 columns (the small-row kernel packs such rows
+  // into its lanes, 1.04-2.0x) and for rows of half-width vectors (60 and
+  // 100 bf16 columns, 1.01-1.19x).
+  if (!ragged && !flat && ragged_ok && cols > 8 && cols <= 256 &&
+      vw * (ib > ob ? ib : ob) <= 4 &&
+      (!cfg || (cfg->variant == ROWSM_AUTO && cfg->vw == 0 && cfg->waves_per_row == 0 &&
+                cfg->rows_per_block == 0 && cfg->block == 0 && cfg->split_blocks == 0 &&
+                cfg->lanes_per_row == 0 && cfg->rows_per_lane == 0 && cfg->packed != 1)))
+    flat = true;
+  if (flat) {
+    // lanes per row and elements per lane of the row phase (launch_flat.hpp)
+    int lpr = (int)next_pow2((int)cdiv(cols, 8));
+    if (lpr < 8) lpr = 8;
+    if (lpr > kWave) lpr = kWave;
+    int e = (int)next_pow2((int)cdiv(cols, lpr));
+    if (e < 2) e = 2;
+    const int64_t G = ((int64_t)kFlatSlots * kWave * vw_full - (vw_full - 1)) / cols;
+    const int64_t tiles = cdiv(rows, G);
+    p->variant = ROWSM_SMALL;
+    p->flat = true;
+    p->vw = vw_full;
+    p->nvec = (int)ragged_span;
+    p->lpr = lpr;
+    p->nv = e;
+    p->vpl = e;
+    p->block = kWave;
+    const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
+    p->grid = tiles < grid_cap(bpc, cus) ? tiles : grid_cap(bpc, cus);
+    return ROWSM_OK;
   }
   if (ragged) {
     vw = vw_full;

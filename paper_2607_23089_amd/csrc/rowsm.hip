@@ -22,7 +22,11 @@ static_assert(ROWSM_OP_MOE_GROUP_TOP2 == kMoe, "rowsm_op values are the launch m
 template <int MODE>
 int launch_mode(const Call& c, int in_dt, int out_dt) {
   switch (c.p.variant) {
-    case ROWSM_SMALL: return launch_small<MODE>(c, in_dt, out_dt);
+    case ROWSM_SMALL:
+      if constexpr (MODE == kPlain || MODE == kLog) {
+        if (c.p.flat) return launch_flat<MODE>(c, in_dt, out_dt);
+      }
+      return c.p.flat ? ROWSM_EINVAL : launch_small<MODE>(c, in_dt, out_dt);
     case ROWSM_MEDIUM:
       if constexpr (MODE == kPlain || MODE == kLog) {
         if (c.p.ragged) return launch_ragged<MODE>(c, in_dt, out_dt);
@@ -309,10 +313,10 @@ int describe_impl(int mode, int64_t rows, int64_t cols, int in_dt, int out_dt,
       }
       std::snprintf(buf, (size_t)len,
                     "%s vw=%d nvec=%d lpr=%d rpl=%d wpr=%d vpl=%d nv=%d packed=%d u=%d "
-                    "split=%d stream=%d prefetch=%d ragged=%d block=%d grid=%lld (%s)",
+                    "split=%d stream=%d prefetch=%d ragged=%d flat=%d block=%d grid=%lld (%s)",
                     variant_name(p.variant), p.vw, p.nvec, p.lpr, p.rpl, p.wpr, p.vpl, p.nv,
                     (int)p.packed, p.u, p.split, p.variant == ROWSM_LARGE && !p.split ? p.stream : 0,
-                    (int)p.prefetch, (int)p.ragged, p.block, (long long)grid, how);
+                    (int)p.prefetch, (int)p.ragged, (int)p.flat, p.block, (long long)grid, how);
     }
   }
   return st;

@@ -31,6 +31,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.44269504088896340736f;
 constexpr int kWave = 64;
+constexpr int kFlatSlots = 4;  // flat short rows: vectors per lane per tile (flat_row.hpp)
 
 // ---- element types --------------------------------------------------------
 

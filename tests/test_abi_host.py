@@ -112,6 +112,7 @@ def test_scaled_causal_argument_errors(lib):
 
 def test_select_regimes(lib):
     s = R.rowsm_select
+    d = lambda rows, cols, i, o, v=R.AUTO: R.rowsm_describe(rows, cols, i, o, v)
     # row of <= 32 vectors -> SMALL
     assert s(262144, 64, R.BF16, R.BF16) == R.SMALL
     assert s(10, 256, R.BF16, R.BF16) == R.SMALL      # 32 bf16 vectors of 8
@@ -120,7 +121,16 @@ def test_select_regimes(lib):
     assert s(10, 128, R.F32, R.F32) == R.SMALL
     assert s(10, 132, R.F32, R.F32) == R.MEDIUM
     assert s(10, 32, R.F32, R.F32) == R.SMALL
-    assert s(10, 33, R.F32, R.F32) == R.MEDIUM        # 33 single elements
+    # odd widths of 9-256 columns (narrow vectors of at most 4 bytes): the
+    # flat form of the small family; 3-8 columns keep the packed small rows,
+    # half-width vectors (60 bf16 columns) their plan
+    for cols, i, o in ((33, R.F32, R.F32), (9, R.BF16, R.BF16), (77, R.BF16, R.F32),
+                       (255, R.F32, R.BF16), (42, R.BF16, R.BF16)):
+        t = d(10, cols, i, o)[1]
+        assert t.startswith("small") and "flat=1 " in t and "block=64 " in t, t
+    for cols, i, o in ((7, R.BF16, R.BF16), (257, R.F32, R.F32), (60, R.BF16, R.BF16),
+                       (100, R.BF16, R.BF16)):
+        assert "flat=0 " in d(10, cols, i, o)[1], (cols, d(10, cols, i, o)[1])
     # medium holds up to 16 waves x 64 lanes x 64 fp32 values (forced)
     d = lambda rows, cols, i, o, v=R.AUTO: R.rowsm_describe(rows, cols, i, o, v)
     assert s(64, 1000, R.F32, R.F32) == R.MEDIUM
@@ -350,27 +360,27 @@ def test_describe(lib):
     # one wave per row and one to four slots: about 32 KiB of traffic per
     # block, rows / (32768 // row bytes) blocks rounded to whole residencies
     # of 4 blocks per compute unit, rows of whole lines or not
-    for rows, cols, i, o, grid in ((1000000, 37, R.F32, R.F32, 9216),     # 296-byte rows
-                                   (500000, 75, R.BF16, R.BF16, 4096),
+    for rows, cols, i, o, grid in ((1000000, 74, R.F32, R.F32, 18432),    # 296-byte rows
+                                   (500000, 156, R.BF16, R.BF16, 9216),
                                    (500000, 164, R.F32, R.F32, 20480),
                                    (500000, 168, R.F32, R.F32, 20480),
                                    (500000, 256, R.F32, R.BF16, 23552),    # whole lines
                                    (500000, 256, R.F32, R.F32, 31744),
                                    (500000, 512, R.BF16, R.BF16, 31744),
                                    (500000, 260, R.BF16, R.BF16, 16384),   # two slots
-                                   (2000, 37, R.F32, R.F32, 250)):         # uncapped grid
+                                   (2000, 74, R.F32, R.F32, 250)):         # uncapped grid
         st, text = R.rowsm_describe(rows, cols, i, o)
         assert st == R.OK and "wpr=1 " in text and f"block=512 grid={grid} " in text, text
-    st, text = R.rowsm_describe(20000, 37, R.F32, R.F32)                 # at least 4 per CU
+    st, text = R.rowsm_describe(20000, 74, R.F32, R.F32)                 # at least 4 per CU
     assert st == R.OK and "grid=1024 " in text, text
-    st, text = R.rowsm_describe(500000, 151, R.F32, R.F32)              # three slots
-    assert st == R.OK and "nv=3 " in text and "grid=18432 " in text, text
+    st, text = R.rowsm_describe(500000, 302, R.F32, R.F32)              # three slots
+    assert st == R.OK and "nv=3 " in text and "grid=38912 " in text, text
     st, text = R.rowsm_describe(500000, 301, R.F32, R.F32)              # five: default grid
     assert st == R.OK and "nv=5 " in text and "grid=62500 " in text, text
     # small rows of narrow vectors whose stores cover parts of lines: about
     # 16 KiB per block, whole residencies of 8 blocks per compute unit; full
     # vectors keep their rules
-    st, text = R.rowsm_describe(1048576, 21, R.BF16, R.BF16)            # 84-byte rows
+    st, text = R.rowsm_describe(1048576, 20, R.BF16, R.BF16)            # 80-byte rows
     assert st == R.OK and text.startswith("small") and "grid=6144 " in text, text
     st, text = R.rowsm_describe(1048576, 24, R.F32, R.F32)              # full vectors
     assert st == R.OK and text.startswith("small") and "grid=8192 " in text, text

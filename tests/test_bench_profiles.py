@@ -87,6 +87,16 @@ def test_launch_specs():
     two_pass = SPLIT_DESC.replace("split=8", "split=0")
     assert P.launch_spec("softmax", two_pass, "f32", "f32")["base"] == "large_row_kernel"
     assert P.launch_spec("moe", SMALL_DESC, "bf16", "f32")["base"] == "group_top2_kernel"
+    ragged = ("medium vw=8 nvec=501 lpr=1 rpl=4 wpr=2 vpl=4 nv=4 packed=0 u=4 split=0 "
+              "stream=0 prefetch=0 ragged=1 flat=0 block=128 grid=12288 (grid assumes 256 CUs)")
+    r = P.launch_spec("log_softmax", ragged, "bf16", "bf16")
+    assert r["base"] == "ragged_row_kernel" and r["args"][3] == "4" and r["args"][4] == "2"
+    flat = ("small vw=8 nvec=11 lpr=16 rpl=4 wpr=1 vpl=8 nv=8 packed=0 u=4 split=0 stream=0 "
+            "prefetch=0 ragged=0 flat=1 block=64 grid=80660 (grid assumes 256 CUs)")
+    fl = P.launch_spec("softmax", flat, "bf16", "bf16")
+    assert fl["base"] == "flat_row_kernel" and fl["block"] == 64 and fl["grid"] == 64 * 80660
+    assert fl["args"][2] == "8" and fl["args"][3] == "16" and fl["args"][4] == "8"
+    assert fl["args"][5] == "0"
     c = P.copy_spec(1024 * 262144, "f32", "f32")
     assert c["grid"] == 1024 * 262144 // 4 and c["args"][2] == "4"
     assert P.copy_spec(1000, "bf16", "f32")["grid"] == 256  # one partial block

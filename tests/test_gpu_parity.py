@@ -467,16 +467,16 @@ def test_few_rows_per_cu_shapes(rows, cols, din, dout, want):
 
 
 @pytest.mark.parametrize("rows,cols,din,dout,want", [
-    (1000003, 37, "f32", "f32", ("block=512 ", "grid=9216 ")),
-    (700001, 37, "bf16", "bf16", ("block=512 ", "grid=3072 ")),
-    (500001, 75, "bf16", "f32", ("block=512 ", "grid=7168 ")),
-    (600011, 101, "f32", "bf16", ("block=512 ", "grid=11264 ")),
+    (1000003, 74, "f32", "f32", ("block=512 ", "grid=18432 ")),
+    (700001, 156, "bf16", "bf16", ("block=512 ", "grid=13312 ")),
+    (500001, 148, "bf16", "f32", ("block=512 ", "grid=14336 ")),
+    (600011, 102, "f32", "bf16", ("block=512 ", "grid=11264 ")),
     (500003, 144, "f32", "f32", ("block=512 ", "grid=17408 ")),
     (300007, 168, "f32", "f32", ("block=512 ", "grid=12288 ")),
     (500001, 256, "f32", "bf16", ("block=512 ", "grid=23552 ")),
     (400009, 256, "f32", "f32", ("block=512 ", "grid=24576 ")),
     (250001, 512, "bf16", "bf16", ("block=512 ", "grid=15360 ")),
-    (400009, 142, "bf16", "f32", ("block=512 ", "grid=10240 "))])      # three slots
+    (400009, 302, "f32", "f32", ("block=512 ", "grid=30720 "))])      # three slots
 def test_one_wave_short_rows(rows, cols, din, dout, want):
     # one wave per row and one to four slots: a grid of about 32 KiB of
     # traffic per block in whole residencies, whose waves loop over many
@@ -497,12 +497,13 @@ def test_one_wave_short_rows(rows, cols, din, dout, want):
 
 
 @pytest.mark.parametrize("rows,cols,din,dout,grid", [
-    (1048583, 21, "bf16", "bf16", 6144), (2000003, 13, "f32", "f32", 12288),
-    (1500007, 27, "bf16", "f32", 14336), (800011, 29, "f32", "bf16", 8192)])
+    (1048583, 20, "bf16", "bf16", 6144), (2000003, 14, "f32", "f32", 14336),
+    (1500007, 26, "f32", "f32", 18432), (800011, 30, "f32", "bf16", 8192)])
 def test_small_rows_of_part_lines(rows, cols, din, dout, grid):
-    # small rows of one-element vectors whose stores cover parts of 128-byte
-    # lines: a grid of about 16 KiB of traffic per block in whole residencies
-    # of 8 blocks per compute unit, whose waves loop over many row groups;
+    # small rows of narrow (8-byte) vectors whose stores cover parts of
+    # 128-byte lines: a grid of about 16 KiB of traffic per block in whole
+    # residencies of 8 blocks per compute unit, whose waves loop over many
+    # row groups;
     # the output prefilled with NaN so that every row is seen written,
     # sampled rows (the last ones among them) against the oracle
     st, desc = R.rowsm_describe(rows, cols, R.dtype_code(DT[din]), R.dtype_code(DT[dout]))
