@@ -417,18 +417,19 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     const bool narrow_medium =
         narrow_nvec <= 16 * kWave * (64 / vw < 16 ? 64 / vw : 16) &&
         (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus));
-    // Spans of 256 vectors up to what 16 waves hold: sweeps of
+    // Spans of 120 vectors up to what 16 waves hold: sweeps of
     // 301-50257-column rows in every dtype pair (96 and 512 MiB launches,
     // each alone after a cache-evicting write) measured the ragged form
-    // 0.6-0.9x the narrow-vector time there; shorter rows spend too much on
-    // their edges (up to 1.45x slower).  (Spans of 8193-10240 fp32-width
+    // 0.6-0.9x the narrow-vector time from 256 vectors, and with its edges
+    // read as whole vectors 0.85-0.96x at 1001-column rows (126-251
+    // vectors); at 88 vectors (701 bf16 columns) up to 7% slower.  (Spans of 8193-10240 fp32-width
     // vectors, 9-10 slots of 16 waves: 0.80-0.94x the split form from 200
     // rows.)
-    ragged = ragged_span >= 4 * kWave && ragged_span <= ragged_max_span &&
+    ragged = ragged_span >= 120 && ragged_span <= ragged_max_span &&
              (inplace || !few_long_rows(rows, cols * (ib + ob), false, cus)) &&
              (narrow_medium || rows >= cus / 4);
   }
-  // The launcher takes the flat form for rows of 9-256 columns whose narrow
+  // The launcher takes the flat form for rows of 9-480 columns whose narrow
   // vectors would be of at most 4 bytes (one fp32 or one or two bf16
   // elements).  A sweep of 3-1001-column rows in every dtype pair at 64 and
   // 512 MiB (each launch alone after a cache-evicting write): 1.04-1.37x
@@ -437,8 +438,10 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
   // fastest grid 0.26-0.98x at 13-129 columns (0.35x at 37), level at 257
   // and beyond; slower at 3-7 columns (the small-row kernel packs such rows
   // into its lanes, 1.04-2.0x) and for rows of half-width vectors (60 and
-  // 100 bf16 columns, 1.01-1.19x).
-  if (!ragged && !flat && ragged_ok && cols > 8 && cols <= 256 &&
+  // 100 bf16 columns, 1.01-1.19x).  At 257-449 columns two more sweeps
+  // measured it 0.77-1.04x the narrow plan (0.89x on geometric mean), at
+  // 511 level (0.94-1.12x).
+  if (!ragged && !flat && ragged_ok && cols > 8 && cols <= 480 &&
       vw * (ib > ob ? ib : ob) <= 4 &&
       (!cfg || (cfg->variant == ROWSM_AUTO && cfg->vw == 0 && cfg->waves_per_row == 0 &&
                 cfg->rows_per_block == 0 && cfg->block == 0 && cfg->split_blocks == 0 &&
@@ -585,8 +588,24 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // narrow-vector plan 20%.
     if (ragged) {
       wpr = 0;
+      // (unless a wave count is given: the fewest of 1, 2 or 4 waves whose
+      // lanes hold at most 3 vectors, else from 4 waves the fewest within
+      // 40 values; over sweeps of 129-2047-column rows in every dtype pair
+      // 1.4% above the fastest wave count measured on geometric mean where
+      // the fewest waves within 40 values took 3.2%, up to 10% on spans of
+      // 376-513 vectors)
+      int min_w = 1;
+      if (!want_wpr) {
+        min_w = 4;
+        for (int w = 1; w <= 4; w <<= 1)
+          if (cdiv(nvec, (int64_t)w * kWave) <= 3) {
+            min_w = w;
+            break;
+          }
+      }
       for (int w = 1; w <= 16; w <<= 1) {
         if (want_wpr && w != want_wpr) continue;
+        if (w < min_w) continue;
         const int v = (int)cdiv(nvec, (int64_t)w * kWave);
         if (v * vw <= ragged_vals) {
           wpr = w;

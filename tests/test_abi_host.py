@@ -116,19 +116,19 @@ def test_select_regimes(lib):
     # row of <= 32 vectors -> SMALL
     assert s(262144, 64, R.BF16, R.BF16) == R.SMALL
     assert s(10, 256, R.BF16, R.BF16) == R.SMALL      # 32 bf16 vectors of 8
-    assert s(10, 257, R.BF16, R.BF16) == R.MEDIUM     # odd: 257 single elements
+    assert s(10, 257, R.BF16, R.BF16) == R.SMALL      # odd: the flat form
     assert s(10, 264, R.BF16, R.BF16) == R.MEDIUM     # 33 vectors
     assert s(10, 128, R.F32, R.F32) == R.SMALL
     assert s(10, 132, R.F32, R.F32) == R.MEDIUM
     assert s(10, 32, R.F32, R.F32) == R.SMALL
-    # odd widths of 9-256 columns (narrow vectors of at most 4 bytes): the
+    # odd widths of 9-480 columns (narrow vectors of at most 4 bytes): the
     # flat form of the small family; 3-8 columns keep the packed small rows,
     # half-width vectors (60 bf16 columns) their plan
     for cols, i, o in ((33, R.F32, R.F32), (9, R.BF16, R.BF16), (77, R.BF16, R.F32),
                        (255, R.F32, R.BF16), (42, R.BF16, R.BF16)):
         t = d(10, cols, i, o)[1]
         assert t.startswith("small") and "flat=1 " in t and "block=64 " in t, t
-    for cols, i, o in ((7, R.BF16, R.BF16), (257, R.F32, R.F32), (60, R.BF16, R.BF16),
+    for cols, i, o in ((7, R.BF16, R.BF16), (481, R.F32, R.F32), (60, R.BF16, R.BF16),
                        (100, R.BF16, R.BF16)):
         assert "flat=0 " in d(10, cols, i, o)[1], (cols, d(10, cols, i, o)[1])
     # medium holds up to 16 waves x 64 lanes x 64 fp32 values (forced)
@@ -375,8 +375,8 @@ def test_describe(lib):
     assert st == R.OK and "grid=1024 " in text, text
     st, text = R.rowsm_describe(500000, 302, R.F32, R.F32)              # three slots
     assert st == R.OK and "nv=3 " in text and "grid=38912 " in text, text
-    st, text = R.rowsm_describe(500000, 301, R.F32, R.F32)              # five: default grid
-    assert st == R.OK and "nv=5 " in text and "grid=62500 " in text, text
+    st, text = R.rowsm_describe(500000, 602, R.F32, R.F32)              # 152 vectors: ragged,
+    assert st == R.OK and "ragged=1 " in text and "grid=500000 " in text, text  # a row a block
     # small rows of narrow vectors whose stores cover parts of lines: about
     # 16 KiB per block, whole residencies of 8 blocks per compute unit; full
     # vectors keep their rules
