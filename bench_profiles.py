@@ -21,7 +21,7 @@ import re
 # Kernels of the library (names without the namespace).
 ROW_KERNELS = ("small_row_kernel", "medium_row_kernel", "split_row_kernel",
                "large_row_kernel", "ragged_row_kernel", "flat_row_kernel", "bwd_small_kernel",
-               "bwd_medium_kernel",
+               "bwd_flat_kernel", "bwd_medium_kernel",
                "bwd_split_kernel", "bwd_large_kernel", "group_top2_kernel",
                "stream_copy_kernel")
 # Index of the output-form template argument (plain 0, fused 1, log 2).
@@ -103,6 +103,8 @@ def launch_spec(op: str, desc: str, din: str, dout: str) -> dict:
     elif op == "backward":
         base = {"small": "bwd_small_kernel", "medium": "bwd_medium_kernel"}.get(fam) or \
             ("bwd_split_kernel" if f.get("split", 0) > 0 else "bwd_large_kernel")
+        if base == "bwd_small_kernel" and f.get("flat", 0):
+            base = "bwd_flat_kernel"
     else:
         base = {"small": "small_row_kernel", "medium": "medium_row_kernel"}.get(fam) or \
             ("split_row_kernel" if f.get("split", 0) > 0 else "large_row_kernel")
@@ -116,7 +118,7 @@ def launch_spec(op: str, desc: str, din: str, dout: str) -> dict:
     if base in ("medium_row_kernel", "split_row_kernel", "ragged_row_kernel") or \
             base in ("bwd_medium_kernel", "bwd_split_kernel"):
         args[3] = str(f["nv"])
-    if base == "flat_row_kernel":  # lanes per row and elements per lane of the row phase
+    if base in ("flat_row_kernel", "bwd_flat_kernel"):  # lanes per row and elements per lane of the row phase
         args[3] = str(f["lpr"])
         args[4] = str(f["nv"])
     return {"base": base, "args": args, "block": f["block"], "grid": f["block"] * f["grid"]}

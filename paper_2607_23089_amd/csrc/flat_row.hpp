@@ -156,4 +156,120 @@ __global__ __launch_bounds__(64) void flat_row_kernel(const typename In::storage
   }
 }
 
+// Softmax backward of such rows, dx = y (dy - sum(y dy)): the same tiles,
+// y and dy each through its own LDS buffer, one dot product per row (fp32
+// fused multiply-adds, then DPP over the LPR lanes), dx written back over y.
+template <typename In, typename Out, int VW, int LPR, int E>
+__global__ __launch_bounds__(64) void bwd_flat_kernel(const typename In::storage* y,
+                                                      const typename In::storage* dy,
+                                                      typename Out::storage* dx, int64_t rows,
+                                                      int cols, int G) {
+  static_assert(LPR >= 1 && LPR <= kWave && (LPR & (LPR - 1)) == 0, "power-of-two row groups");
+  constexpr int S = kFlatSlots;
+  constexpr int RPP = kWave / LPR;
+  __shared__ float by[S * kWave * VW];
+  __shared__ float bd[S * kWave * VW];
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int sub = lane % LPR, grp = lane / LPR;
+  const int64_t total = rows * (int64_t)cols;
+  const int64_t ntiles = (rows + G - 1) / G;
+
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t r0 = tile * G;
+    const int nr = rows - r0 < G ? (int)(rows - r0) : G;
+    const int64_t e0 = r0 * cols;
+    const int h = (int)(e0 & (VW - 1));
+    const int span = nr * cols + h;
+    const int lv = (span - 1) / VW;
+    const int64_t room = total - (e0 - h);
+    const int lim = (int)((int64_t)(lv + 1) * VW < room ? (int64_t)(lv + 1) * VW : room);
+    const rsrc_t ry = make_rsrc(y + (e0 - h), (uint64_t)lim * In::bytes);
+    const rsrc_t rdy = make_rsrc(dy + (e0 - h), (uint64_t)lim * In::bytes);
+    const rsrc_t rdx = make_rsrc(dx + (e0 - h), (uint64_t)span * Out::bytes);
+
+    {
+      InVec<In, VW> a[S], b[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const int first = (s * kWave + lane) * VW;
+        const bool ok = first < span && first + VW <= lim;
+        a[s].load_or_neg_inf(ok, ry, (uint32_t)first * In::bytes, 0);
+        b[s].load_or_neg_inf(ok, rdy, (uint32_t)first * In::bytes, 0);
+      }
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        float fa[VW], fb[VW];
+        a[s].to_float(fa);
+        b[s].to_float(fb);
+#pragma unroll
+        for (int k = 0; k < VW; ++k) {
+          by[(s * kWave + lane) * VW + k] = fa[k];
+          bd[(s * kWave + lane) * VW + k] = fb[k];
+        }
+      }
+    }
+    if (lim < (lv + 1) * VW) {  // the final tile's last vector, element by element
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        if (s * kWave + lane == lv) {
+#pragma unroll
+          for (int k = 0; k < VW; ++k) {
+            const int e = lv * VW + k;
+            const bool ok = e >= h && e < span;
+            InVec<In, 1> u, v;
+            u.load_or_neg_inf(ok, ry, (uint32_t)e * In::bytes, 0);
+            v.load_or_neg_inf(ok, rdy, (uint32_t)e * In::bytes, 0);
+            by[e] = u.get(0);
+            bd[e] = v.get(0);
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    for (int p = 0; p * RPP < nr; ++p) {
+      const int g = p * RPP + grp;
+      const bool rok = g < nr;
+      const int base = h + g * cols;
+      float a[E], b[E];
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        const int c = i * LPR + sub;
+        const bool ok = rok && c < cols;
+        a[i] = ok ? by[base + c] : 0.0f;
+        b[i] = ok ? bd[base + c] : 0.0f;
+      }
+      float d = 0.0f;
+#pragma unroll
+      for (int i = 0; i < E; ++i) d = __builtin_fmaf(a[i], b[i], d);
+      d = group_reduce<LPR, SumOp>(d);
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        const int c = i * LPR + sub;
+        if (rok && c < cols) by[base + c] = a[i] * (b[i] - d);
+      }
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const int first = (s * kWave + lane) * VW;
+      if (first >= h && first + VW <= span) {
+        float o[VW];
+#pragma unroll
+        for (int k = 0; k < VW; ++k) o[k] = by[first + k];
+        store_out<Out, VW>(rdx, (uint32_t)first * Out::bytes, o, false);
+      } else if (first < span && first + VW > h) {
+#pragma unroll
+        for (int k = 0; k < VW; ++k) {
+          const int e = first + k;
+          if (e >= h && e < span) store_out<Out, 1>(rdx, (uint32_t)e * Out::bytes, {by[e]}, false);
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace rowsm

@@ -1,7 +1,8 @@
 // Launcher of the flat short-row kernel (flat_row.hpp): the full 16-byte
 // vector width of the dtype pair, dispatch on the lanes per row and elements
-// per lane of the row phase.  Instantiated once per output form
-// (launch_flat_<form>.hip).
+// per lane of the row phase.  Instantiated once per output form and for the
+// backward (launch_flat_<form>.hip; for the backward c.x is y, c.dy is dy and
+// c.y is dx).
 #pragma once
 
 #include "flat_row.hpp"
@@ -14,9 +15,16 @@ bool try_flat(const Call& c, int* status) {
   if (c.p.lpr != LPR || c.p.nv != E) return false;
   const int G = (kFlatSlots * kWave * VW - (VW - 1)) / c.cols;
   if (G < 1) return false;
-  flat_row_kernel<In, Out, VW, LPR, E, MODE><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
-      static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
-      c.rows, c.cols, G);
+  if constexpr (MODE == kBackward) {
+    bwd_flat_kernel<In, Out, VW, LPR, E><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
+        static_cast<const typename In::storage*>(c.x),
+        static_cast<const typename In::storage*>(c.dy), static_cast<typename Out::storage*>(c.y),
+        c.rows, c.cols, G);
+  } else {
+    flat_row_kernel<In, Out, VW, LPR, E, MODE><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
+        static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
+        c.rows, c.cols, G);
+  }
   *status = hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
   return true;
 }

@@ -41,7 +41,9 @@ int launch_mode(const Call& c, int in_dt, int out_dt) {
 
 int launch_backward(const Call& c, int in_dt, int out_dt) {
   switch (c.p.variant) {
-    case ROWSM_SMALL: return launch_bwd_small(c, in_dt, out_dt);
+    case ROWSM_SMALL:
+      return c.p.flat ? launch_flat<kBackward>(c, in_dt, out_dt)
+                      : launch_bwd_small(c, in_dt, out_dt);
     case ROWSM_MEDIUM: return launch_bwd_medium(c, in_dt, out_dt);
     case ROWSM_LARGE:
       return c.p.split > 0 ? launch_bwd_split(c, in_dt, out_dt)

@@ -29,6 +29,7 @@ template int launch_ragged<kLog>(const Call&, int, int);
 template <int MODE> int launch_flat(const Call&, int, int) { return ROWSM_EHIP; }
 template int launch_flat<kPlain>(const Call&, int, int);
 template int launch_flat<kLog>(const Call&, int, int);
+template int launch_flat<kBackward>(const Call&, int, int);
 
 int launch_bwd_small(const Call&, int, int) { return ROWSM_EHIP; }
 int launch_bwd_medium(const Call&, int, int) { return ROWSM_EHIP; }

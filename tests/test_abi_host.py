@@ -486,16 +486,16 @@ def test_backward_plans(lib):
     # whole residencies; five or more slots, small launches, a grid or a
     # shape given keep their plans
     cap = lambda rows, cols, dt, **cfg: int(d(rows, cols, dt, dt, **cfg)[1].split("grid=")[1].split()[0])
-    assert cap(204600, 41, R.BF16) == 2048                        # 246-byte rows of 3 streams
+    assert cap(204600, 131, R.BF16) == 6144                       # 786-byte rows of 3 streams
     assert cap(291271, 90, R.F32) == 13312                        # 45 two-element vectors
-    assert cap(582542, 90, R.BF16) == 13312                       # two slots
-    assert cap(220289, 119, R.F32) == 13312
+    assert cap(204600, 300, R.BF16) == 15360                      # two slots
+    assert cap(220289, 118, R.F32) == 13312
     assert cap(163840, 320, R.BF16) == 13312                      # 640-byte rows: whole lines
     assert cap(288070, 182, R.BF16) == 13312                      # three slots
     assert cap(288070, 330, R.BF16) == 36009                      # six: default grid
-    assert cap(4000, 41, R.BF16) == 500                           # under the grid
-    assert cap(204600, 41, R.BF16, blocks_per_cu=8) == 2048       # grid given
-    assert cap(204600, 41, R.BF16, rows_per_block=4) == 51150     # shape given
+    assert cap(4000, 131, R.BF16) == 500                          # under the grid
+    assert cap(204600, 131, R.BF16, blocks_per_cu=8) == 2048       # grid given
+    assert cap(204600, 131, R.BF16, rows_per_block=4) == 51150     # shape given
     # few long rows (>= 512 KiB of y, dy and dx per row): the split form,
     # about one block per compute unit
     st, t = d(8, 65536, R.F32, R.F32)
@@ -593,3 +593,31 @@ def test_prefetch_config(lib):
     st, t = R.rowsm_describe_op(R.OP_SCALED_CAUSAL, 64, 262144, R.F32, R.F32,
                                 R.RowsmConfig(prefetch=1, split_blocks=32))
     assert st == R.EINVAL                                                # fused: no prefetching
+
+
+def test_backward_flat_plans():
+    # odd widths of short rows: the flat form (flat_row.hpp) for 9-480
+    # columns whose narrow vectors would be of at most 4 bytes, bf16 to bf16
+    # only at 33-128 columns; asked for (small variant at the full vector
+    # width) up to what one tile row holds; refused where the pointers are
+    # not aligned to the full vector width
+    def d(rows, cols, i, o, cfg=None):
+        return R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, i, o, cfg)
+    flat = lambda *a: "flat=1 " in d(*a)[1]
+    assert flat(204600, 41, R.BF16, R.BF16) and flat(1000, 127, R.BF16, R.BF16)
+    assert not flat(204600, 21, R.BF16, R.BF16) and not flat(1000, 131, R.BF16, R.BF16)
+    assert flat(1000, 21, R.F32, R.F32) and flat(1000, 479, R.F32, R.BF16)
+    assert flat(1000, 9, R.BF16, R.F32) and not flat(1000, 7, R.BF16, R.F32)
+    assert not flat(1000, 481, R.F32, R.F32) and not flat(1000, 90, R.F32, R.F32)
+    assert not flat(1000, 44, R.BF16, R.BF16)                     # a multiple of 4
+    st, t = d(1000, 41, R.BF16, R.BF16)
+    assert t.startswith("small") and "vw=8 " in t and "lpr=8 " in t and "nv=8 " in t, t
+    assert "block=64 " in t and "grid=" + str(-(-1000 // (2041 // 41))) + " " in t, t
+    cf = lambda vw: R.RowsmConfig(variant=R.SMALL, vw=vw)
+    st, t = d(100, 1017, R.F32, R.F32, cf(4))
+    assert st == R.OK and "flat=1 " in t and "lpr=64 " in t and "nv=16 " in t, t
+    assert d(100, 1023, R.F32, R.F32, cf(4))[0] == R.EINVAL      # past one tile row
+    assert d(100, 1023, R.BF16, R.BF16, cf(8))[0] == R.OK
+    assert d(100, 1025, R.BF16, R.BF16, cf(8))[0] == R.EINVAL    # past 1024
+    assert "flat=1 " in d(10, 5, R.F32, R.F32, cf(4))[1]
+    assert d(10, 64, R.F32, R.F32, R.RowsmConfig(variant=R.SMALL, vw=8))[0] == R.EINVAL

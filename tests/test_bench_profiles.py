@@ -95,6 +95,9 @@ def test_launch_specs():
             "prefetch=0 ragged=0 flat=1 block=64 grid=80660 (grid assumes 256 CUs)")
     fl = P.launch_spec("softmax", flat, "bf16", "bf16")
     assert fl["base"] == "flat_row_kernel" and fl["block"] == 64 and fl["grid"] == 64 * 80660
+    bf = P.launch_spec("backward", flat, "bf16", "bf16")
+    assert bf["base"] == "bwd_flat_kernel" and bf["grid"] == 64 * 80660
+    assert bf["args"] == {0: "rowsm::BF16", 1: "rowsm::BF16", 2: "8", 3: "16", 4: "8"}
     assert fl["args"][2] == "8" and fl["args"][3] == "16" and fl["args"][4] == "8"
     assert fl["args"][5] == "0"
     c = P.copy_spec(1024 * 262144, "f32", "f32")

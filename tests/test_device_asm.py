@@ -131,7 +131,8 @@ def test_stream_cache_policy(asm):
     # row data streams through: loads non-temporal; stores non-temporal, at
     # device scope only where the launch's stores cover whole 128-byte lines
     # (each store site has both forms behind a uniform branch), never at
-    # device scope in the ragged kernels, whose rows never start on lines
+    # device scope in the ragged and flat kernels, whose rows never start on
+    # lines
     stores = re.findall(r"buffer_store_(?:dword|short)\S* .*", asm)
     loads = re.findall(r"buffer_load_(?:dword|ushort)\S* .*", asm)
     assert stores and loads
@@ -146,7 +147,7 @@ def test_stream_cache_policy(asm):
         if not st:
             continue
         dev = sum(bool(re.search(r" nt sc1$", x)) for x in st)
-        if "ragged_row_kernel" in n:
+        if re.search(r"ragged_row_kernel|flat_row_kernel|bwd_flat_kernel", n):
             assert dev == 0, n
         elif re.search(r"(small|medium|split|large)_row_kernel|bwd_\w+_kernel", n):
             assert 0 < dev < len(st), (n, dev, len(st))

@@ -213,8 +213,8 @@ def test_bwd_wide_rows_take_split_form(rows, cols, din, dout):
 
 
 @pytest.mark.parametrize("rows,cols,din,dout", [
-    (204600, 41, "bf16", "bf16"), (153450, 41, "bf16", "f32"), (122760, 41, "f32", "bf16"),
-    (291271, 90, "f32", "f32"), (582542, 90, "bf16", "bf16"), (81707, 77, "bf16", "f32"),
+    (204600, 131, "bf16", "bf16"), (153450, 132, "bf16", "f32"), (122760, 90, "f32", "bf16"),
+    (291271, 90, "f32", "f32"), (349525, 150, "bf16", "bf16"), (81707, 94, "f32", "f32"),
     (288070, 182, "bf16", "bf16"), (163840, 320, "bf16", "bf16")])
 def test_bwd_short_rows_looping_grid(rows, cols, din, dout):
     # rows of one wave and one to four slots (parts of 128-byte lines, and
