@@ -156,16 +156,18 @@ __global__ __launch_bounds__(64) void flat_row_kernel(const typename In::storage
   }
 }
 
-// Softmax backward of such rows, dx = y (dy - sum(y dy)): the same tiles,
-// y and dy each through its own LDS buffer, one dot product per row (fp32
-// fused multiply-adds, then DPP over the LPR lanes), dx written back over y.
-template <typename In, typename Out, int VW, int LPR, int E>
+// Softmax backward of such rows, dx = y (dy - sum(y dy)): the same tiles of
+// S vectors per lane (S = 2 keeps the bf16 instantiation at 8 KiB of LDS per
+// wave), y and dy each through its own LDS buffer, one dot product per row
+// (fp32 fused multiply-adds, then DPP over the LPR lanes), dx written back
+// over y.
+template <typename In, typename Out, int VW, int LPR, int E, int S>
 __global__ __launch_bounds__(64) void bwd_flat_kernel(const typename In::storage* y,
                                                       const typename In::storage* dy,
                                                       typename Out::storage* dx, int64_t rows,
                                                       int cols, int G) {
   static_assert(LPR >= 1 && LPR <= kWave && (LPR & (LPR - 1)) == 0, "power-of-two row groups");
-  constexpr int S = kFlatSlots;
+  static_assert(S == 2 || S == kFlatSlots, "two or four vectors per lane");
   constexpr int RPP = kWave / LPR;
   __shared__ float by[S * kWave * VW];
   __shared__ float bd[S * kWave * VW];

@@ -13,13 +13,24 @@ namespace rowsm {
 template <typename In, typename Out, int VW, int LPR, int E, int MODE>
 bool try_flat(const Call& c, int* status) {
   if (c.p.lpr != LPR || c.p.nv != E) return false;
-  const int G = (kFlatSlots * kWave * VW - (VW - 1)) / c.cols;
+  // vectors per lane of a tile: 4, or 2 for the bf16 backward (c.p.rpl)
+  constexpr bool kTwo = MODE == kBackward && In::bytes == 2 && Out::bytes == 2;
+  const int slots = kTwo && c.p.rpl == 2 ? 2 : kFlatSlots;
+  if (MODE == kBackward && c.p.rpl != slots) return false;
+  const int G = (slots * kWave * VW - (VW - 1)) / c.cols;
   if (G < 1) return false;
   if constexpr (MODE == kBackward) {
-    bwd_flat_kernel<In, Out, VW, LPR, E><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
-        static_cast<const typename In::storage*>(c.x),
-        static_cast<const typename In::storage*>(c.dy), static_cast<typename Out::storage*>(c.y),
-        c.rows, c.cols, G);
+    const auto yp = static_cast<const typename In::storage*>(c.x);
+    const auto dyp = static_cast<const typename In::storage*>(c.dy);
+    const auto dxp = static_cast<typename Out::storage*>(c.y);
+    if (slots == 2) {
+      if constexpr (kTwo)
+        bwd_flat_kernel<In, Out, VW, LPR, E, 2><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
+            yp, dyp, dxp, c.rows, c.cols, G);
+    } else {
+      bwd_flat_kernel<In, Out, VW, LPR, E, kFlatSlots>
+          <<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(yp, dyp, dxp, c.rows, c.cols, G);
+    }
   } else {
     flat_row_kernel<In, Out, VW, LPR, E, MODE><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
         static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),

@@ -914,23 +914,29 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
   // multiple of the full 16-byte vector width, y, dy and dx aligned to it;
   // taken when cfg asks for the small variant at the full vector width, and
   // by the launcher for 9-480 columns whose narrow vectors would be of at
-  // most 4 bytes, bf16 to bf16 only at 33-128 columns.  A sweep of 5-1001
+  // most 4 bytes, bf16 to bf16 only up to 128 columns.  A sweep of 5-1001
   // columns in every dtype pair at 64 and 384 MiB (each launch alone after
   // a cache-evicting write): 0.85x the narrow-vector plans' time on
-  // geometric mean at 9-480 columns, 0.40-0.62x at 37-41; bf16 to bf16 at
-  // 13-21 and 129-479 columns 0.88-1.28x (1.11x on geometric mean), its
-  // kernel holding 129 VGPRs and 16 KiB of LDS per wave.
+  // geometric mean at 9-480 columns with tiles of 4 vectors per lane,
+  // 0.40-0.62x at 37-41.  bf16 to bf16 takes tiles of 2 vectors per lane
+  // (81 VGPRs and 8 KiB of LDS per wave where 4 took 129 and 16 KiB):
+  // 0.35-0.96x at 13-129 columns (41: 198 -> 69 us at 384 MiB), 1.03x on
+  // geometric mean at 255-479, where a tile holds 2-3 rows.
   const int vw_full = 16 / (ib > ob ? ib : ob);
   const bool flat_ok = cols % vw_full != 0 && vw_supported(vw_full, ib) &&
                        ia % (uintptr_t)(vw_full * ib) == 0 &&
                        dxa % (uintptr_t)(vw_full * ob < 16 ? vw_full * ob : 16) == 0;
-  const int64_t flat_tile_cols = (int64_t)kFlatSlots * kWave * vw_full - (vw_full - 1);
+  // (tiles of 4 vectors per lane, 2 for bf16 to bf16 rows that fit them)
+  const int64_t two_tile_cols = 2 * (int64_t)kWave * vw_full - (vw_full - 1);
+  const int flat_slots = ib == 2 && ob == 2 && cols <= two_tile_cols ? 2 : kFlatSlots;
+  const int64_t flat_tile_cols = (int64_t)flat_slots * kWave * vw_full - (vw_full - 1);
   bool flat = false;
   if (flat_ok && cfg && cfg->vw == vw_full && cfg->variant == ROWSM_SMALL) {
-    if (cols > (flat_tile_cols < 1024 ? flat_tile_cols : 1024)) return ROWSM_EINVAL;
+    const int64_t most = (int64_t)kFlatSlots * kWave * vw_full - (vw_full - 1);
+    if (cols > (most < 1024 ? most : 1024)) return ROWSM_EINVAL;
     flat = true;
   } else if (flat_ok && cols > 8 && cols <= 480 && vw * (ib > ob ? ib : ob) <= 4 &&
-             (ib == 4 || ob == 4 || (cols > 32 && cols <= 128)) &&
+             (ib == 4 || ob == 4 || cols <= 128) &&
              (!cfg || (cfg->variant == ROWSM_AUTO && cfg->vw == 0 && cfg->waves_per_row == 0 &&
                        cfg->rows_per_block == 0 && cfg->block == 0 &&
                        cfg->split_blocks == 0 && cfg->lanes_per_row == 0 &&
@@ -952,6 +958,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     p->lpr = lpr;
     p->nv = e;
     p->vpl = e;
+    p->rpl = flat_slots;
     p->block = kWave;
     p->grid = tiles < grid_cap(bpc, cus) ? tiles : grid_cap(bpc, cus);
     return ROWSM_OK;

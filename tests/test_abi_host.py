@@ -598,26 +598,33 @@ def test_prefetch_config(lib):
 def test_backward_flat_plans():
     # odd widths of short rows: the flat form (flat_row.hpp) for 9-480
     # columns whose narrow vectors would be of at most 4 bytes, bf16 to bf16
-    # only at 33-128 columns; asked for (small variant at the full vector
-    # width) up to what one tile row holds; refused where the pointers are
-    # not aligned to the full vector width
+    # only up to 128 columns (tiles of 2 vectors per lane where a row fits
+    # them); asked for (small variant at the full vector width) up to what
+    # one tile row holds; refused where the pointers are not aligned to the
+    # full vector width
     def d(rows, cols, i, o, cfg=None):
         return R.rowsm_describe_op(R.OP_SOFTMAX_BACKWARD, rows, cols, i, o, cfg)
     flat = lambda *a: "flat=1 " in d(*a)[1]
     assert flat(204600, 41, R.BF16, R.BF16) and flat(1000, 127, R.BF16, R.BF16)
-    assert not flat(204600, 21, R.BF16, R.BF16) and not flat(1000, 131, R.BF16, R.BF16)
+    assert flat(204600, 21, R.BF16, R.BF16) and not flat(1000, 131, R.BF16, R.BF16)
+    assert not flat(1000, 7, R.BF16, R.BF16) and flat(1000, 9, R.BF16, R.BF16)
     assert flat(1000, 21, R.F32, R.F32) and flat(1000, 479, R.F32, R.BF16)
     assert flat(1000, 9, R.BF16, R.F32) and not flat(1000, 7, R.BF16, R.F32)
     assert not flat(1000, 481, R.F32, R.F32) and not flat(1000, 90, R.F32, R.F32)
     assert not flat(1000, 44, R.BF16, R.BF16)                     # a multiple of 4
     st, t = d(1000, 41, R.BF16, R.BF16)
     assert t.startswith("small") and "vw=8 " in t and "lpr=8 " in t and "nv=8 " in t, t
-    assert "block=64 " in t and "grid=" + str(-(-1000 // (2041 // 41))) + " " in t, t
+    assert "rpl=2 " in t and "block=64 " in t, t
+    assert "grid=" + str(-(-1000 // (1017 // 41))) + " " in t, t
+    st, t = d(1000, 41, R.BF16, R.F32)                            # 4 vectors per lane
+    assert "rpl=4 " in t and "grid=" + str(-(-1000 // (1021 // 41))) + " " in t, t
     cf = lambda vw: R.RowsmConfig(variant=R.SMALL, vw=vw)
     st, t = d(100, 1017, R.F32, R.F32, cf(4))
     assert st == R.OK and "flat=1 " in t and "lpr=64 " in t and "nv=16 " in t, t
     assert d(100, 1023, R.F32, R.F32, cf(4))[0] == R.EINVAL      # past one tile row
-    assert d(100, 1023, R.BF16, R.BF16, cf(8))[0] == R.OK
+    st, t = d(100, 1023, R.BF16, R.BF16, cf(8))                 # past 2 vectors per lane
+    assert st == R.OK and "rpl=4 " in t, t
+    assert "rpl=2 " in d(100, 1017, R.BF16, R.BF16, cf(8))[1]
     assert d(100, 1025, R.BF16, R.BF16, cf(8))[0] == R.EINVAL    # past 1024
     assert "flat=1 " in d(10, 5, R.F32, R.F32, cf(4))[1]
     assert d(10, 64, R.F32, R.F32, R.RowsmConfig(variant=R.SMALL, vw=8))[0] == R.EINVAL

@@ -116,13 +116,17 @@ def test_bwd_flat_bounded_writes(cols):
 
 
 @pytest.mark.parametrize("din,dout", PAIRS)
-@pytest.mark.parametrize("rows,cols", [(204600, 41), (20000, 77), (5000, 255), (3000, 479)])
+@pytest.mark.parametrize("rows,cols", [(204600, 41), (300001, 21), (20000, 77), (5000, 255),
+                                       (3000, 479)])
 def test_bwd_flat_launcher_choice(rows, cols, din, dout):
     desc = describe(rows, cols, din, dout)
     vw = full_vw(din, dout)
-    # (bf16 to bf16: the flat form at 33-128 columns only)
+    # (bf16 to bf16: the flat form up to 128 columns, tiles of 2 vectors per
+    # lane)
     bf = din == dout == "bf16"
-    assert ("flat=1 " in desc) == (cols % vw != 0 and (not bf or 32 < cols <= 128)), desc
+    assert ("flat=1 " in desc) == (cols % vw != 0 and (not bf or cols <= 128)), desc
+    if bf and "flat=1 " in desc:
+        assert "rpl=2 " in desc, desc
     y, dy = inputs(rows, cols, din, seed=rows + cols)
     dx = run_bwd(y.to(DEV), dy.to(DEV), dout)
     assert_bwd_parity(y, dy, dx, dout, f"bwd launcher {rows}x{cols} {din}->{dout} [{desc}]")
