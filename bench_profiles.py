@@ -121,6 +121,8 @@ def launch_spec(op: str, desc: str, din: str, dout: str) -> dict:
     if base in ("flat_row_kernel", "bwd_flat_kernel"):  # lanes per row and elements per lane of the row phase
         args[3] = str(f["lpr"])
         args[4] = str(f["nv"])
+        # vectors per lane of a tile
+        args[6 if base == "flat_row_kernel" else 5] = str(f["rpl"])
     return {"base": base, "args": args, "block": f["block"], "grid": f["block"] * f["grid"]}
 
 

@@ -169,9 +169,17 @@ typedef struct rowsm_config {
     int32_t variant;        /* rowsm_variant; ROWSM_AUTO = launcher's choice      */
     int32_t vw;             /* elements per vector access: power of two that
                                divides cols, <= 16 bytes of input, with x and y
-                               aligned to it                                      */
+                               aligned to it; or, for a width it does not
+                               divide, the full 16-byte width with x and y
+                               aligned to 16 bytes: variant SMALL the flat
+                               form (rows read as one stream of whole vectors,
+                               at most 1024 columns and 4 vectors per lane of
+                               a tile; also the backward), AUTO or MEDIUM the
+                               ragged form (softmax and log-softmax only)      */
     int32_t lanes_per_row;  /* SMALL: lanes holding one row, power of two <= 32   */
-    int32_t rows_per_lane;  /* SMALL: rows each lane handles per pass: 1,2,4,8    */
+    int32_t rows_per_lane;  /* SMALL: rows each lane handles per pass: 1,2,4,8;
+                               the flat form: 16-byte vectors per lane of a
+                               tile, 4, or 2 for bf16 to bf16 rows that fit   */
     int32_t waves_per_row;  /* MEDIUM: wavefronts holding one row: 1,2,4,8,16     */
     int32_t rows_per_block; /* MEDIUM: rows per block (rows*waves_per_row <= 16)  */
     int32_t packed;         /* MEDIUM: 1 keep raw bf16 and recompute exp,

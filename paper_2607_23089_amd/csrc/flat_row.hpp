@@ -9,7 +9,7 @@
 //
 // A block is one wave.  A tile is G consecutive rows, G the most whose
 // elements, from the vector boundary at or before the first, fit S = 4
-// vectors per lane.  Per tile:
+// vectors per lane (or S = 2: half the registers and LDS).  Per tile:
 //   1. each lane loads its S vectors (lane-major, so every instruction reads
 //      64 consecutive vectors) and writes them to LDS as fp32; the first and
 //      last vectors also hold elements of the neighbouring tiles (inside the
@@ -33,14 +33,14 @@
 
 namespace rowsm {
 
-template <typename In, typename Out, int VW, int LPR, int E, int MODE>
+template <typename In, typename Out, int VW, int LPR, int E, int MODE, int S>
 __global__ __launch_bounds__(64) void flat_row_kernel(const typename In::storage* x,
                                                       typename Out::storage* y, int64_t rows,
                                                       int cols, int G) {
   static_assert(MODE == kPlain || MODE == kLog, "softmax and log forms only");
   static_assert(LPR >= 1 && LPR <= kWave && (LPR & (LPR - 1)) == 0, "power-of-two row groups");
+  static_assert(S == 2 || S == kFlatSlots, "two or four vectors per lane");
   constexpr bool LOG = MODE == kLog;
-  constexpr int S = kFlatSlots;
   constexpr int RPP = kWave / LPR;  // rows per pass
   __shared__ float buf[S * kWave * VW];
 

@@ -13,10 +13,10 @@ namespace rowsm {
 template <typename In, typename Out, int VW, int LPR, int E, int MODE>
 bool try_flat(const Call& c, int* status) {
   if (c.p.lpr != LPR || c.p.nv != E) return false;
-  // vectors per lane of a tile: 4, or 2 for the bf16 backward (c.p.rpl)
-  constexpr bool kTwo = MODE == kBackward && In::bytes == 2 && Out::bytes == 2;
+  // vectors per lane of a tile (c.p.rpl): 4, or 2 for bf16 to bf16
+  constexpr bool kTwo = In::bytes == 2 && Out::bytes == 2;
   const int slots = kTwo && c.p.rpl == 2 ? 2 : kFlatSlots;
-  if (MODE == kBackward && c.p.rpl != slots) return false;
+  if (c.p.rpl != slots) return false;
   const int G = (slots * kWave * VW - (VW - 1)) / c.cols;
   if (G < 1) return false;
   if constexpr (MODE == kBackward) {
@@ -32,16 +32,23 @@ bool try_flat(const Call& c, int* status) {
           <<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(yp, dyp, dxp, c.rows, c.cols, G);
     }
   } else {
-    flat_row_kernel<In, Out, VW, LPR, E, MODE><<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(
-        static_cast<const typename In::storage*>(c.x), static_cast<typename Out::storage*>(c.y),
-        c.rows, c.cols, G);
+    const auto xp = static_cast<const typename In::storage*>(c.x);
+    const auto yp = static_cast<typename Out::storage*>(c.y);
+    if (slots == 2) {
+      if constexpr (kTwo)
+        flat_row_kernel<In, Out, VW, LPR, E, MODE, 2>
+            <<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(xp, yp, c.rows, c.cols, G);
+    } else {
+      flat_row_kernel<In, Out, VW, LPR, E, MODE, kFlatSlots>
+          <<<dim3((unsigned)c.p.grid), dim3(kWave), 0, c.st>>>(xp, yp, c.rows, c.cols, G);
+    }
   }
   *status = hipGetLastError() == hipSuccess ? ROWSM_OK : ROWSM_EHIP;
   return true;
 }
 
 // (lanes per row, elements per lane): LPR = max(8, pow2 >= cols / 8) up to 64,
-// E the power of two >= cols / LPR (flat_shape() in plan.hip).
+// E the power of two >= cols / LPR (the flat plans of plan.hip).
 template <typename In, typename Out, int MODE>
 int flat_pair(const Call& c) {
   constexpr int VW = 16 / (In::bytes > Out::bytes ? In::bytes : Out::bytes);

@@ -92,6 +92,18 @@ int64_t grid_cap(int bpc, int cus) {
   return bpc ? (int64_t)cus * bpc : ((int64_t)1 << 30);
 }
 
+// Vectors per lane of a flat tile (flat_row.hpp): cfg->rows_per_lane when
+// given (4, or 2 for bf16 to bf16 rows that fit such a tile), else 2 for
+// such rows when two_default, else 4; 0 for a value the form cannot take.
+int flat_slots(const rowsm_config* cfg, int ib, int ob, int64_t cols, int vw_full,
+               bool two_default) {
+  const bool fits2 = ib == 2 && ob == 2 && cols <= 2 * (int64_t)kWave * vw_full - (vw_full - 1);
+  const int want = cfg ? cfg->rows_per_lane : 0;
+  if (want == 0) return two_default && fits2 ? 2 : kFlatSlots;
+  if (want == kFlatSlots || (want == 2 && fits2)) return want;
+  return 0;
+}
+
 bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
 
 // Host form of the kernels' stores_whole_lines(): every store of a launch
@@ -454,7 +466,15 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     if (lpr > kWave) lpr = kWave;
     int e = (int)next_pow2((int)cdiv(cols, lpr));
     if (e < 2) e = 2;
-    const int64_t G = ((int64_t)kFlatSlots * kWave * vw_full - (vw_full - 1)) / cols;
+    // bf16 to bf16 rows of up to 64 columns: tiles of 2 vectors per lane
+    // (58-61 VGPRs and 4 KiB of LDS per wave where 4 take 96 and 8 KiB).
+    // Forced tiles of both sizes at 64 and 384 MiB, each launch alone after
+    // a cache-evicting write: 0.77-0.97x the time of 4 at 9-41 columns
+    // (0.88x on geometric mean, softmax and log form alike), 0.92-1.11x at
+    // 77-127 and up to 1.3x at 255-479, where a tile holds fewer rows.
+    const int slots = flat_slots(cfg, ib, ob, cols, vw_full, cols <= 64);
+    if (!slots) return ROWSM_EINVAL;
+    const int64_t G = ((int64_t)slots * kWave * vw_full - (vw_full - 1)) / cols;
     const int64_t tiles = cdiv(rows, G);
     p->variant = ROWSM_SMALL;
     p->flat = true;
@@ -463,6 +483,7 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     p->lpr = lpr;
     p->nv = e;
     p->vpl = e;
+    p->rpl = slots;
     p->block = kWave;
     const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
     p->grid = tiles < grid_cap(bpc, cus) ? tiles : grid_cap(bpc, cus);
@@ -926,10 +947,6 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
   const bool flat_ok = cols % vw_full != 0 && vw_supported(vw_full, ib) &&
                        ia % (uintptr_t)(vw_full * ib) == 0 &&
                        dxa % (uintptr_t)(vw_full * ob < 16 ? vw_full * ob : 16) == 0;
-  // (tiles of 4 vectors per lane, 2 for bf16 to bf16 rows that fit them)
-  const int64_t two_tile_cols = 2 * (int64_t)kWave * vw_full - (vw_full - 1);
-  const int flat_slots = ib == 2 && ob == 2 && cols <= two_tile_cols ? 2 : kFlatSlots;
-  const int64_t flat_tile_cols = (int64_t)flat_slots * kWave * vw_full - (vw_full - 1);
   bool flat = false;
   if (flat_ok && cfg && cfg->vw == vw_full && cfg->variant == ROWSM_SMALL) {
     const int64_t most = (int64_t)kFlatSlots * kWave * vw_full - (vw_full - 1);
@@ -949,7 +966,10 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     if (lpr > kWave) lpr = kWave;
     int e = (int)next_pow2((int)cdiv(cols, lpr));
     if (e < 2) e = 2;
-    const int64_t tiles = cdiv(rows, flat_tile_cols / cols);
+    // tiles of 4 vectors per lane, 2 for bf16 to bf16 rows that fit them
+    const int slots = flat_slots(cfg, ib, ob, cols, vw_full, true);
+    if (!slots) return ROWSM_EINVAL;
+    const int64_t tiles = cdiv(rows, ((int64_t)slots * kWave * vw_full - (vw_full - 1)) / cols);
     const int bpc = (cfg && cfg->blocks_per_cu > 0) ? cfg->blocks_per_cu : 0;
     p->variant = ROWSM_SMALL;
     p->flat = true;
@@ -958,7 +978,7 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     p->lpr = lpr;
     p->nv = e;
     p->vpl = e;
-    p->rpl = flat_slots;
+    p->rpl = slots;
     p->block = kWave;
     p->grid = tiles < grid_cap(bpc, cus) ? tiles : grid_cap(bpc, cus);
     return ROWSM_OK;

@@ -627,4 +627,24 @@ def test_backward_flat_plans():
     assert "rpl=2 " in d(100, 1017, R.BF16, R.BF16, cf(8))[1]
     assert d(100, 1025, R.BF16, R.BF16, cf(8))[0] == R.EINVAL    # past 1024
     assert "flat=1 " in d(10, 5, R.F32, R.F32, cf(4))[1]
+    # vectors per lane of a tile through rows_per_lane: 4, or 2 for bf16 to
+    # bf16 rows that fit such a tile (forward and backward)
+    sl = lambda op, cols, i, o, vw, r: R.rowsm_describe_op(
+        op, 1000, cols, i, o, R.RowsmConfig(variant=R.SMALL, vw=vw, rows_per_lane=r))
+    for op in (R.OP_SOFTMAX, R.OP_LOG_SOFTMAX, R.OP_SOFTMAX_BACKWARD):
+        assert "rpl=2 " in sl(op, 21, R.BF16, R.BF16, 8, 2)[1]
+        assert "rpl=4 " in sl(op, 21, R.BF16, R.BF16, 8, 4)[1]
+        assert "rpl=2 " in sl(op, 1017, R.BF16, R.BF16, 8, 2)[1]
+        assert sl(op, 1023, R.BF16, R.BF16, 8, 2)[0] == R.EINVAL  # past 2 vectors
+        assert sl(op, 21, R.F32, R.BF16, 4, 2)[0] == R.EINVAL     # bf16 pairs only
+        assert sl(op, 21, R.BF16, R.BF16, 8, 1)[0] == R.EINVAL
+        assert sl(op, 21, R.BF16, R.BF16, 8, 8)[0] == R.EINVAL
+    # the launcher: for bf16 to bf16, 2 up to 64 columns in the forward and
+    # up to 128 in the backward; 4 otherwise
+    au = lambda op, cols, i=R.BF16, o=R.BF16: R.rowsm_describe_op(op, 1000, cols, i, o, None)[1]
+    for op in (R.OP_SOFTMAX, R.OP_LOG_SOFTMAX):
+        assert "rpl=2 " in au(op, 21) and "rpl=2 " in au(op, 63) and "rpl=4 " in au(op, 77)
+        assert "rpl=4 " in au(op, 21, R.F32, R.F32) and "rpl=4 " in au(op, 21, R.BF16, R.F32)
+    assert "rpl=2 " in au(R.OP_SOFTMAX_BACKWARD, 127)
+    assert "rpl=4 " in au(R.OP_SOFTMAX_BACKWARD, 21, R.F32, R.BF16)
     assert d(10, 64, R.F32, R.F32, R.RowsmConfig(variant=R.SMALL, vw=8))[0] == R.EINVAL

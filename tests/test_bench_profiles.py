@@ -97,7 +97,8 @@ def test_launch_specs():
     assert fl["base"] == "flat_row_kernel" and fl["block"] == 64 and fl["grid"] == 64 * 80660
     bf = P.launch_spec("backward", flat, "bf16", "bf16")
     assert bf["base"] == "bwd_flat_kernel" and bf["grid"] == 64 * 80660
-    assert bf["args"] == {0: "rowsm::BF16", 1: "rowsm::BF16", 2: "8", 3: "16", 4: "8"}
+    assert bf["args"] == {0: "rowsm::BF16", 1: "rowsm::BF16", 2: "8", 3: "16", 4: "8", 5: "4"}
+    assert fl["args"][6] == "4"
     assert fl["args"][2] == "8" and fl["args"][3] == "16" and fl["args"][4] == "8"
     assert fl["args"][5] == "0"
     c = P.copy_spec(1024 * 262144, "f32", "f32")

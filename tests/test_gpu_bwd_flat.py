@@ -142,3 +142,19 @@ def test_bwd_flat_misaligned_inputs_take_narrow_vectors():
     assert_bwd_parity(y.cpu(), dy.cpu(), dx, "f32", "bwd misaligned odd width")
     with pytest.raises(R.RowsmError):
         run_bwd(y, dy, "f32", config=flat_cfg("f32", "f32"))
+
+
+@pytest.mark.parametrize("slots", [2, 4])
+@pytest.mark.parametrize("cols", [9, 41, 255, 1017])
+def test_bwd_flat_bf16_tile_slots(cols, slots):
+    # bf16 to bf16 tiles of 2 or 4 vectors per lane (rows_per_lane)
+    g = (slots * 64 * 8 - 7) // cols
+    rows = 3 * g + max(1, g // 2)
+    if (rows * cols) % 8 == 0:
+        rows += 1
+    cfg = R.RowsmConfig(variant=R.SMALL, vw=8, rows_per_lane=slots)
+    desc = describe(rows, cols, "bf16", "bf16", cfg)
+    assert "flat=1 " in desc and f"rpl={slots} " in desc, desc
+    y, dy = inputs(rows, cols, "bf16", seed=cols + slots)
+    dx = run_bwd(y.to(DEV), dy.to(DEV), "bf16", config=cfg)
+    assert_bwd_parity(y, dy, dx, "bf16", f"bwd flat {rows}x{cols} slots {slots} [{desc}]")

@@ -175,3 +175,28 @@ def test_flat_launcher_choice(din, dout, cols):
     sums = y.double().sum(dim=1)
     tol = 1e-5 if dout == "f32" else 2.0 ** -8 * 2 + 1e-5
     assert float((sums - 1.0).abs().max()) <= tol
+
+
+@pytest.mark.parametrize("slots", [2, 4])
+@pytest.mark.parametrize("cols", [9, 21, 77, 255, 1017])
+@pytest.mark.parametrize("op", [R.OP_SOFTMAX, R.OP_LOG_SOFTMAX])
+def test_flat_bf16_tile_slots(op, cols, slots):
+    # bf16 to bf16 tiles of 2 or 4 vectors per lane (rows_per_lane)
+    g = (slots * 64 * 8 - 7) // cols
+    rows = 3 * g + max(1, g // 2)
+    if (rows * cols) % 8 == 0:
+        rows += 1
+    cfg = R.RowsmConfig(variant=R.SMALL, vw=8, rows_per_lane=slots)
+    desc = describe(rows, cols, "bf16", "bf16", cfg, op=op)
+    assert "flat=1 " in desc and f"rpl={slots} " in desc, desc
+    x = W.random_matrix(rows, cols, "bf16", sigma=4.0, seed=cols + slots)
+    if op == R.OP_SOFTMAX:
+        y = R.softmax(x.to(DEV), config=cfg)
+        torch.cuda.synchronize()
+        assert_parity(x, y, "bf16", f"flat {rows}x{cols} slots {slots} [{desc}]")
+    else:
+        y = R.log_softmax(x.to(DEV), config=cfg)
+        torch.cuda.synchronize()
+        want = oracle.log_softmax_f64(oracle.widen_bf16_bits(W.to_bits_numpy(x)).reshape(rows, cols))
+        res = compare_log(widen_output(W.to_bits_numpy(y), "bf16").reshape(rows, cols), want, "bf16")
+        assert res["ok"], (desc, res)
