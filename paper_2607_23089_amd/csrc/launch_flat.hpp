@@ -48,7 +48,8 @@ bool try_flat(const Call& c, int* status) {
 }
 
 // (lanes per row, elements per lane): LPR = max(8, pow2 >= cols / 8) up to 64,
-// E the power of two >= cols / LPR (the flat plans of plan.hip).
+// 4 for rows of at most 16 columns, E the power of two >= cols / LPR
+// (flat_row_shape() in plan.hip).
 template <typename In, typename Out, int MODE>
 int flat_pair(const Call& c) {
   constexpr int VW = 16 / (In::bytes > Out::bytes ? In::bytes : Out::bytes);
@@ -60,7 +61,8 @@ int flat_pair(const Call& c) {
          try_flat<In, Out, VW, 16, 8, MODE>(c, &status) ||
          try_flat<In, Out, VW, 32, 8, MODE>(c, &status) ||
          try_flat<In, Out, VW, 64, 8, MODE>(c, &status) ||
-         try_flat<In, Out, VW, 64, 16, MODE>(c, &status));
+         try_flat<In, Out, VW, 64, 16, MODE>(c, &status) ||
+         try_flat<In, Out, VW, 4, 4, MODE>(c, &status));
   return status;
 }
 

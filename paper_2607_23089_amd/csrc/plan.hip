@@ -104,6 +104,32 @@ int flat_slots(const rowsm_config* cfg, int ib, int ob, int64_t cols, int vw_ful
   return 0;
 }
 
+// Lanes per row and elements per lane of a flat plan's row phase: the
+// launcher's LPR = the power of two >= cols / 8, within 8..64, and 4 for
+// rows of 9-16 columns, or cfg->lanes_per_row when given; E the power of
+// two >= cols / LPR, at least 2.  False for a pair launch_flat.hpp does not
+// compile.  (Forced row shapes of 1-8 lanes at 9-29 columns, every dtype
+// pair, softmax and backward, 64 and 384 MiB: 4 lanes took 0.97x the time
+// of 8 on geometric mean at 9-15 columns, 0.86-0.95x at 9 bf16 columns,
+// and 0.99x at 21-29; 1 and 2 lanes were fastest only here and there.)
+bool flat_row_shape(const rowsm_config* cfg, int64_t cols, int* lpr_out, int* e_out) {
+  int lpr = (int)next_pow2((int)cdiv(cols, 8));
+  if (lpr < 8) lpr = cols > 8 && cols <= 16 ? 4 : 8;
+  if (lpr > kWave) lpr = kWave;
+  if (cfg && cfg->lanes_per_row > 0) lpr = cfg->lanes_per_row;
+  int e = (int)next_pow2((int)cdiv(cols, lpr));
+  if (e < 2) e = 2;
+  *lpr_out = lpr;
+  *e_out = e;
+  switch (lpr) {
+    case 4: return e == 4;
+    case 8: return e == 2 || e == 4 || e == 8;
+    case 16: case 32: return e == 8;
+    case 64: return e == 8 || e == 16;
+    default: return false;
+  }
+}
+
 bool medium_unpacked_cap(int vw, int vpl) { return vpl * vw <= 64 && vpl <= 16; }
 
 // Host form of the kernels' stores_whole_lines(): every store of a launch
@@ -461,11 +487,8 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     flat = true;
   if (flat) {
     // lanes per row and elements per lane of the row phase (launch_flat.hpp)
-    int lpr = (int)next_pow2((int)cdiv(cols, 8));
-    if (lpr < 8) lpr = 8;
-    if (lpr > kWave) lpr = kWave;
-    int e = (int)next_pow2((int)cdiv(cols, lpr));
-    if (e < 2) e = 2;
+    int lpr = 0, e = 0;
+    if (!flat_row_shape(cfg, cols, &lpr, &e)) return ROWSM_EINVAL;
     // bf16 to bf16 rows of up to 64 columns: tiles of 2 vectors per lane
     // (58-61 VGPRs and 4 KiB of LDS per wave where 4 take 96 and 8 KiB).
     // Forced tiles of both sizes at 64 and 384 MiB, each launch alone after
@@ -961,11 +984,8 @@ int plan_backward(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t i
     flat = true;
   }
   if (flat) {
-    int lpr = (int)next_pow2((int)cdiv(cols, 8));
-    if (lpr < 8) lpr = 8;
-    if (lpr > kWave) lpr = kWave;
-    int e = (int)next_pow2((int)cdiv(cols, lpr));
-    if (e < 2) e = 2;
+    int lpr = 0, e = 0;
+    if (!flat_row_shape(cfg, cols, &lpr, &e)) return ROWSM_EINVAL;
     // tiles of 4 vectors per lane, 2 for bf16 to bf16 rows that fit them
     const int slots = flat_slots(cfg, ib, ob, cols, vw_full, true);
     if (!slots) return ROWSM_EINVAL;

@@ -639,6 +639,18 @@ def test_backward_flat_plans():
         assert sl(op, 21, R.F32, R.BF16, 4, 2)[0] == R.EINVAL     # bf16 pairs only
         assert sl(op, 21, R.BF16, R.BF16, 8, 1)[0] == R.EINVAL
         assert sl(op, 21, R.BF16, R.BF16, 8, 8)[0] == R.EINVAL
+    # row phase: 4 lanes of 4 elements at 9-16 columns, else from 8 lanes;
+    # lanes_per_row picks any compiled shape
+    for op in (R.OP_SOFTMAX, R.OP_SOFTMAX_BACKWARD):
+        for cols, lanes, e in ((9, 4, 4), (15, 4, 4), (17, 8, 4), (41, 8, 8), (255, 32, 8)):
+            t = R.rowsm_describe_op(op, 1000, cols, R.F32, R.F32, None)[1]
+            assert f"lpr={lanes} " in t and f"nv={e} " in t, (cols, t)
+        lp = lambda cols, lanes: R.rowsm_describe_op(
+            op, 1000, cols, R.F32, R.F32, R.RowsmConfig(variant=R.SMALL, vw=4, lanes_per_row=lanes))
+        assert "lpr=8 " in lp(13, 8)[1] and "nv=2 " in lp(13, 8)[1]
+        assert lp(21, 4)[0] == R.EINVAL                           # 4 x 8: not compiled
+        assert lp(13, 2)[0] == R.EINVAL and lp(13, 1)[0] == R.EINVAL
+        assert "lpr=8 " in lp(5, 0)[1]
     # the launcher: for bf16 to bf16, 2 up to 64 columns in the forward and
     # up to 128 in the backward; 4 otherwise
     au = lambda op, cols, i=R.BF16, o=R.BF16: R.rowsm_describe_op(op, 1000, cols, i, o, None)[1]

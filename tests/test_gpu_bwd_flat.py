@@ -158,3 +158,20 @@ def test_bwd_flat_bf16_tile_slots(cols, slots):
     y, dy = inputs(rows, cols, "bf16", seed=cols + slots)
     dx = run_bwd(y.to(DEV), dy.to(DEV), "bf16", config=cfg)
     assert_bwd_parity(y, dy, dx, "bf16", f"bwd flat {rows}x{cols} slots {slots} [{desc}]")
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("cols", [9, 13])
+def test_bwd_flat_row_phase_lanes(cols, din, dout):
+    # 9-16 columns: 4 lanes of 4 elements by default; 8 lanes of 2 asked for
+    vw = full_vw(din, dout)
+    if cols % vw == 0:
+        pytest.skip("a multiple of the vector width")
+    rows = 4000 + 1
+    y, dy = inputs(rows, cols, din, seed=cols + 2)
+    for lanes, e in ((0, 4), (8, 2)):
+        cfg = R.RowsmConfig(variant=R.SMALL, vw=vw, lanes_per_row=lanes)
+        desc = describe(rows, cols, din, dout, cfg)
+        assert f"lpr={lanes or 4} " in desc and f"nv={e} " in desc, desc
+        dx = run_bwd(y.to(DEV), dy.to(DEV), dout, config=cfg)
+        assert_bwd_parity(y, dy, dx, dout, f"bwd flat {rows}x{cols} [{desc}]")

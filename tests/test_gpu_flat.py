@@ -200,3 +200,21 @@ def test_flat_bf16_tile_slots(op, cols, slots):
         want = oracle.log_softmax_f64(oracle.widen_bf16_bits(W.to_bits_numpy(x)).reshape(rows, cols))
         res = compare_log(widen_output(W.to_bits_numpy(y), "bf16").reshape(rows, cols), want, "bf16")
         assert res["ok"], (desc, res)
+
+
+@pytest.mark.parametrize("din,dout", PAIRS)
+@pytest.mark.parametrize("cols", [9, 13, 15])
+def test_flat_row_phase_lanes(cols, din, dout):
+    # 9-16 columns: 4 lanes of 4 elements by default; 8 lanes of 2 asked for
+    vw = full_vw(din, dout)
+    if cols % vw == 0:
+        pytest.skip("a multiple of the vector width")
+    rows = 5000 + 3
+    x = W.random_matrix(rows, cols, din, sigma=4.0, seed=cols + 1)
+    for lanes, e in ((0, 4), (8, 2)):
+        cfg = R.RowsmConfig(variant=R.SMALL, vw=vw, lanes_per_row=lanes)
+        desc = describe(rows, cols, din, dout, cfg)
+        assert f"lpr={lanes or 4} " in desc and f"nv={e} " in desc, desc
+        y = R.softmax(x.to(DEV), out_dtype=DT[dout], config=cfg)
+        torch.cuda.synchronize()
+        assert_parity(x, y, dout, f"flat {rows}x{cols} {din}->{dout} [{desc}]")
