@@ -176,7 +176,10 @@ typedef struct rowsm_config {
                                at most 1024 columns and 4 vectors per lane of
                                a tile; also the backward), AUTO or MEDIUM the
                                ragged form (softmax and log-softmax only)      */
-    int32_t lanes_per_row;  /* SMALL: lanes holding one row, power of two <= 32   */
+    int32_t lanes_per_row;  /* SMALL: lanes holding one row, power of two <= 32;
+                               the flat form: lanes per row of its row phase
+                               (4 with 4 elements, 8 with 2-8, 16-32 with 8,
+                               64 with 8 or 16 elements per lane)              */
     int32_t rows_per_lane;  /* SMALL: rows each lane handles per pass: 1,2,4,8;
                                the flat form: 16-byte vectors per lane of a
                                tile, 4, or 2 for bf16 to bf16 rows that fit   */
