@@ -489,13 +489,15 @@ int plan_for(int64_t rows, int64_t cols, int in_dt, int out_dt, uintptr_t xa, ui
     // lanes per row and elements per lane of the row phase (launch_flat.hpp)
     int lpr = 0, e = 0;
     if (!flat_row_shape(cfg, cols, &lpr, &e)) return ROWSM_EINVAL;
-    // bf16 to bf16 rows of up to 64 columns: tiles of 2 vectors per lane
+    // bf16 to bf16 rows of up to 45 columns: tiles of 2 vectors per lane
     // (58-61 VGPRs and 4 KiB of LDS per wave where 4 take 96 and 8 KiB).
     // Forced tiles of both sizes at 64 and 384 MiB, each launch alone after
     // a cache-evicting write: 0.77-0.97x the time of 4 at 9-41 columns
     // (0.88x on geometric mean, softmax and log form alike), 0.92-1.11x at
-    // 77-127 and up to 1.3x at 255-479, where a tile holds fewer rows.
-    const int slots = flat_slots(cfg, ib, ob, cols, vw_full, cols <= 64);
+    // 77-127 and up to 1.3x at 255-479, where a tile holds fewer rows; at
+    // 45-63 columns, not fitted, 0.98x at 45 and 0.87-1.12x beyond (1.07-
+    // 1.12x at 47-59 columns and 384 MiB).
+    const int slots = flat_slots(cfg, ib, ob, cols, vw_full, cols <= 45);
     if (!slots) return ROWSM_EINVAL;
     const int64_t G = ((int64_t)slots * kWave * vw_full - (vw_full - 1)) / cols;
     const int64_t tiles = cdiv(rows, G);

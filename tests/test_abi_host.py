@@ -651,11 +651,12 @@ def test_backward_flat_plans():
         assert lp(21, 4)[0] == R.EINVAL                           # 4 x 8: not compiled
         assert lp(13, 2)[0] == R.EINVAL and lp(13, 1)[0] == R.EINVAL
         assert "lpr=8 " in lp(5, 0)[1]
-    # the launcher: for bf16 to bf16, 2 up to 64 columns in the forward and
+    # the launcher: for bf16 to bf16, 2 up to 45 columns in the forward and
     # up to 128 in the backward; 4 otherwise
     au = lambda op, cols, i=R.BF16, o=R.BF16: R.rowsm_describe_op(op, 1000, cols, i, o, None)[1]
     for op in (R.OP_SOFTMAX, R.OP_LOG_SOFTMAX):
-        assert "rpl=2 " in au(op, 21) and "rpl=2 " in au(op, 63) and "rpl=4 " in au(op, 77)
+        assert "rpl=2 " in au(op, 21) and "rpl=2 " in au(op, 45) and "rpl=4 " in au(op, 47)
+        assert "rpl=4 " in au(op, 77)
         assert "rpl=4 " in au(op, 21, R.F32, R.F32) and "rpl=4 " in au(op, 21, R.BF16, R.F32)
     assert "rpl=2 " in au(R.OP_SOFTMAX_BACKWARD, 127)
     assert "rpl=4 " in au(R.OP_SOFTMAX_BACKWARD, 21, R.F32, R.BF16)
